@@ -1,0 +1,288 @@
+"""CPU oracle for the MiTA forward pass (Mixture-of-Top-k Attention, arXiv 2602.01219).
+
+TEST INFRASTRUCTURE ONLY. Nothing on the product path may import, call or run
+this module: only the tests, the smoke check and the benchmark's CPU-baseline
+leg use it. It shares no code with the HIP library (no kernels, headers,
+tables or helpers) and it never imports the package.
+
+Plain, slow and written to be checked by eye against the paper. Arithmetic is
+numpy float64 on the exact input values (bf16/fp32 inputs widened exactly).
+Everything is per (batch, head) slice; nothing is shared across slices.
+
+Notation follows Sec. 3.2 with tokens as rows: q, k, v are [N, d] (the paper's
+Q, K, V in R^{d x N} have tokens as columns), landmarks q_lm, v_lm are [M, d]
+(the paper's m is M here), the expert width is k (here `topk`).
+
+Steps, in the order of Algorithm 1 (Appendix B):
+  1. landmark queries by adaptive average pooling over the token grid
+     (Sec. 3.2, landmark queries; Tab. A1: 2-D pooling is the default)
+  2. scores S = K^T q_lm / sqrt(d)                 (Eq. top-k; Algorithm 1)
+  3. I_i = Top_k(S[i, :])                           (Eq. top-k)
+  4. K^(i) = K[:, I_i], V^(i) = V[:, I_i]           (Eq. gather)
+  5. v_lm_i = Atten(q_lm_i, K, V)                   (Eq. landmark-value)
+  6. e(q) = argmax_i q . q_lm_i (routing logits Q^T Q_lm, Sec. 3.2)
+  7. MiTA(q) = V* softmax(K*^T q / sqrt(d)),  K* = [Q_lm, K^(e(q))],
+     V* = [V_lm, V^(e(q))]                          (Eq. mita, s = 1)
+A second formulation (Algorithm 1's grouped form: shared-expert attention,
+varlen attention over queries grouped by expert, log-sum-exp combine) is
+provided for cross-checking step 7.
+
+Readings where the paper is silent or ambiguous (listed in the design doc):
+  * pooling windows: start = floor(i*G/g), end = ceil((i+1)*G/g) per axis
+    (the adaptive-average-pool rule Algorithm 1 names); 1-D pooling when
+    grid_h == 1.
+  * top-k order: larger score first, equal scores by lower token index;
+    -0 == +0; the index set is returned ascending.
+  * selection uses the scaled scores S (Algorithm 1), which Eq. landmark-value's
+    softmax also uses.
+  * routing: e(q) is the lowest landmark index attaining the maximum of
+    (q . q_lm_i) / sqrt(d); counts are the bincount of e (minlength M),
+    offsets = [0, cumsum(counts)], grouping is stable.
+  * s = 1 only.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+
+# ----------------------------------------------------------------------------
+# Step 1: landmark queries (Sec. 3.2, average pooling over uniformly spaced
+# windows; Algorithm 1's AdaptiveAvgPool; Tab. A1 default is 2-D pooling).
+# ----------------------------------------------------------------------------
+def pool_windows(G: int, g: int) -> list[tuple[int, int]]:
+    """Adaptive pooling windows splitting G positions into g windows:
+    window i covers [floor(i*G/g), ceil((i+1)*G/g))."""
+    return [((i * G) // g, -((-(i + 1) * G) // g)) for i in range(g)]
+
+
+def landmarks(q: np.ndarray, grid_h: int, grid_w: int, lm_h: int, lm_w: int) -> np.ndarray:
+    """q: [N, d] with token t at grid position (t // grid_w, t % grid_w).
+    Returns q_lm [M, d], M = lm_h * lm_w, landmark i at (i // lm_w, i % lm_w)
+    is the arithmetic mean of q over its 2-D window."""
+    N, d = q.shape
+    assert N == grid_h * grid_w
+    grid = q.reshape(grid_h, grid_w, d)
+    rows = pool_windows(grid_h, lm_h)
+    cols = pool_windows(grid_w, lm_w)
+    out = np.empty((lm_h * lm_w, d), dtype=np.float64)
+    for a, (r0, r1) in enumerate(rows):
+        for b, (c0, c1) in enumerate(cols):
+            out[a * lm_w + b] = grid[r0:r1, c0:c1, :].reshape(-1, d).mean(axis=0)
+    return out
+
+
+# ----------------------------------------------------------------------------
+# Step 2: landmark-key scores (Eq. top-k; Algorithm 1 scales by 1/sqrt(d)).
+# ----------------------------------------------------------------------------
+def scores(q_lm: np.ndarray, k: np.ndarray, scale: float) -> np.ndarray:
+    """S[i, n] = (q_lm_i . k_n) * scale, shape [M, N]."""
+    return (q_lm @ k.T) * scale
+
+
+# ----------------------------------------------------------------------------
+# Step 3: top-k selection per landmark (Eq. top-k).
+# ----------------------------------------------------------------------------
+def topk_indices(S: np.ndarray, topk: int) -> np.ndarray:
+    """For each row of S [M, N], the topk token indices that come first in the
+    order (larger score first, then lower index), returned ascending.
+    Returns int64 [M, topk]."""
+    M, N = S.shape
+    assert 1 <= topk <= N
+    idx = np.empty((M, topk), dtype=np.int64)
+    n = np.arange(N)
+    for i in range(M):
+        order = np.lexsort((n, -S[i]))      # primary: -S ascending; secondary: n ascending
+        idx[i] = np.sort(order[:topk])
+    return idx
+
+
+# ----------------------------------------------------------------------------
+# Step 4: gather (Eq. gather).
+# ----------------------------------------------------------------------------
+def gather(k: np.ndarray, v: np.ndarray, idx: np.ndarray):
+    """Expert tiles K^(i) = K[I_i], V^(i) = V[I_i]: [M, topk, d] each."""
+    return k[idx], v[idx]
+
+
+# ----------------------------------------------------------------------------
+# Step 5: landmark values (Eq. landmark-value): v_lm_i = Atten(q_lm_i, K, V),
+# the softmax running over the N keys of landmark i.
+# ----------------------------------------------------------------------------
+def softmax_rows(z: np.ndarray) -> np.ndarray:
+    w = np.exp(z - z.max(axis=-1, keepdims=True))
+    return w / w.sum(axis=-1, keepdims=True)
+
+
+def landmark_values(S: np.ndarray, v: np.ndarray) -> np.ndarray:
+    return softmax_rows(S) @ v
+
+
+# ----------------------------------------------------------------------------
+# Step 6: routing (Sec. 3.2: logits Q^T Q_lm; rank-1 expert e_1(q); Algorithm 1
+# ArgMax / ArgSort / BinCount / CumSum).
+# ----------------------------------------------------------------------------
+@dataclass
+class Routing:
+    expert: np.ndarray     # [N] int64, e(q) in [0, M)
+    counts: np.ndarray     # [M] int64
+    offsets: np.ndarray    # [M+1] int64, offsets[0] = 0, offsets[M] = N
+    perm: np.ndarray       # [N] int64, tokens grouped by expert, ascending within a group
+
+
+def route(q: np.ndarray, q_lm: np.ndarray, scale: float) -> Routing:
+    logits = (q @ q_lm.T) * scale               # [N, M]
+    expert = np.argmax(logits, axis=1)          # first maximum = lowest landmark index
+    return routing_from_expert(expert, q_lm.shape[0])
+
+
+def routing_from_expert(expert: np.ndarray, M: int) -> Routing:
+    expert = np.asarray(expert, dtype=np.int64)
+    counts = np.bincount(expert, minlength=M)
+    offsets = np.concatenate([[0], np.cumsum(counts)])
+    perm = np.argsort(expert, kind="stable")
+    return Routing(expert, counts, offsets, perm)
+
+
+# ----------------------------------------------------------------------------
+# Step 7: the MiTA output (Eq. mita with s = 1), per query.
+# ----------------------------------------------------------------------------
+def output_per_query(q, q_lm, v_lm, kx, vx, expert, scale, use_shared=1, use_routed=1):
+    """o_n = V* softmax(K*^T q_n * scale) with K* = [q_lm ; kx[e(n)]] and
+    V* = [v_lm ; vx[e(n)]] (either part dropped by its flag)."""
+    N, d = q.shape
+    o = np.empty((N, d), dtype=np.float64)
+    for n in range(N):
+        keys, vals = [], []
+        if use_shared:
+            keys.append(q_lm)
+            vals.append(v_lm)
+        if use_routed:
+            keys.append(kx[expert[n]])
+            vals.append(vx[expert[n]])
+        Ks = np.concatenate(keys, axis=0)
+        Vs = np.concatenate(vals, axis=0)
+        p = softmax_rows((Ks @ q[n]) * scale)
+        o[n] = p @ Vs
+    return o
+
+
+def output_grouped(q, q_lm, v_lm, kx, vx, routing: Routing, scale, use_shared=1, use_routed=1):
+    """Algorithm 1's form: shared-expert attention and per-expert (varlen)
+    attention over queries grouped by expert, each with its log-sum-exp,
+    combined by online-softmax weights (Sec. 3.2, computing expert-wise and
+    combining). Returns o [N, d]."""
+    N, d = q.shape
+    parts = []
+    if use_shared:
+        z = (q @ q_lm.T) * scale                      # [N, M]
+        mx = z.max(axis=1, keepdims=True)
+        w = np.exp(z - mx)
+        s = w.sum(axis=1, keepdims=True)
+        parts.append(((w @ v_lm) / s, (mx + np.log(s))[:, 0]))
+    if use_routed:
+        o_e = np.empty((N, d))
+        lse_e = np.empty(N)
+        qs = q[routing.perm]
+        for i in range(q_lm.shape[0]):
+            a, b = routing.offsets[i], routing.offsets[i + 1]
+            if a == b:
+                continue
+            z = (qs[a:b] @ kx[i].T) * scale
+            mx = z.max(axis=1, keepdims=True)
+            w = np.exp(z - mx)
+            s = w.sum(axis=1, keepdims=True)
+            rows = routing.perm[a:b]                   # scatter back to token order
+            o_e[rows] = (w @ vx[i]) / s
+            lse_e[rows] = (mx + np.log(s))[:, 0]
+        parts.append((o_e, lse_e))
+    if len(parts) == 1:
+        return parts[0][0]
+    (o1, l1), (o2, l2) = parts
+    mx = np.maximum(l1, l2)
+    w1 = np.exp(l1 - mx)[:, None]
+    w2 = np.exp(l2 - mx)[:, None]
+    return (w1 * o1 + w2 * o2) / (w1 + w2)
+
+
+def effective_weights(q, k, q_lm, S, idx, expert, scale, use_shared=1, use_routed=1):
+    """W [N, N] with o = W v: the shared part spreads landmark j's weight over
+    the keys through softmax(S[j, :]) (Eq. landmark-value), the routed part puts
+    its weights on the selected keys. Tiny inputs only."""
+    N = q.shape[0]
+    A = softmax_rows(S)
+    W = np.zeros((N, N))
+    M = q_lm.shape[0]
+    for n in range(N):
+        z = []
+        if use_shared:
+            z.append((q_lm @ q[n]) * scale)
+        if use_routed:
+            z.append((k[idx[expert[n]]] @ q[n]) * scale)
+        p = softmax_rows(np.concatenate(z))
+        j = 0
+        if use_shared:
+            W[n] += p[:M] @ A
+            j = M
+        if use_routed:
+            np.add.at(W[n], idx[expert[n]], p[j:])
+    return W
+
+
+# ----------------------------------------------------------------------------
+# The whole forward over [B, H, N, d] inputs.
+# ----------------------------------------------------------------------------
+@dataclass
+class SliceResult:
+    q_lm: np.ndarray
+    S: np.ndarray
+    idx: np.ndarray
+    v_lm: np.ndarray
+    routing: Routing
+    o: np.ndarray
+
+
+def forward_slice(q, k, v, grid_h, grid_w, lm_h, lm_w, topk, scale=None,
+                  use_shared=1, use_routed=1, force_idx=None, force_expert=None,
+                  rows=None) -> SliceResult:
+    """One (b, h) slice of the forward. force_idx / force_expert replace the
+    oracle's own selection / routing (to compare outputs given another
+    implementation's discrete choices). rows: compute o only for these tokens
+    (o is then [len(rows), d])."""
+    N, d = q.shape
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    q_lm = landmarks(q, grid_h, grid_w, lm_h, lm_w)
+    S = scores(q_lm, k, scale)
+    idx = topk_indices(S, topk) if force_idx is None else np.asarray(force_idx, dtype=np.int64)
+    v_lm = landmark_values(S, v)
+    if force_expert is None:
+        routing = route(q, q_lm, scale)
+    else:
+        routing = routing_from_expert(force_expert, q_lm.shape[0])
+    kx, vx = gather(k, v, idx)
+    if rows is None:
+        o = output_per_query(q, q_lm, v_lm, kx, vx, routing.expert, scale, use_shared, use_routed)
+    else:
+        rows = np.asarray(rows)
+        o = output_per_query(q[rows], q_lm, v_lm, kx, vx, routing.expert[rows], scale,
+                             use_shared, use_routed)
+    return SliceResult(q_lm, S, idx, v_lm, routing, o)
+
+
+def forward(q, k, v, grid_h, grid_w, lm_h, lm_w, topk, scale=None, use_shared=1,
+            use_routed=1):
+    """q, k, v: [B, H, N, d] float64. Returns o [B, H, N, d] and the per-slice
+    results (a list in (b, h) order)."""
+    B, H, N, d = q.shape
+    o = np.empty((B, H, N, d))
+    res = []
+    for b in range(B):
+        for h in range(H):
+            r = forward_slice(q[b, h], k[b, h], v[b, h], grid_h, grid_w, lm_h, lm_w,
+                              topk, scale, use_shared, use_routed)
+            o[b, h] = r.o
+            res.append(r)
+    return o, res
