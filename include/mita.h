@@ -1,0 +1,201 @@
+/*
+ * mita.h - C ABI of the MI355X (gfx950) MiTA forward library.
+ *
+ * Mixture-of-Top-k Attention (arXiv 2602.01219, Sec. 3.2 and Algorithm 1 in
+ * Appendix B), forward pass, one routed expert per query (s = 1):
+ *
+ *   q_lm  = AdaptiveAvgPool(Q)                 landmark queries  (Sec. 3.2; Tab. A1)
+ *   S     = K^T q_lm / sqrt(d)                 landmark-key scores (Eq. top-k; Alg. 1)
+ *   I_i   = Top_k(S[i, :])                     expert key sets     (Eq. top-k)
+ *   K^(i), V^(i) = K[:, I_i], V[:, I_i]        expert tiles        (Eq. gather)
+ *   v_lm_i = Atten(q_lm_i, K, V)               landmark values     (Eq. landmark-value)
+ *   e(q)  = argmax_i q . q_lm_i                routing             (Sec. 3.2, routing logits)
+ *   o     = V* softmax(K*^T q / sqrt(d)),  K* = [q_lm, K^(e(q))],
+ *           V* = [v_lm, V^(e(q))]              output              (Eq. mita; Eq. shared-expert)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Device pointers. Every tensor argument is a device pointer (HIP device
+ *    memory) owned by the caller; the library never allocates device memory
+ *    and keeps no state between calls (apart from a thread-local error
+ *    string). Pointers must be 16-byte aligned.
+ *  - Layout. Tensors are contiguous row-major. q, k, v, o are [B, H, N, d]
+ *    (the paper's d x N per head, tokens as rows). Token t sits at position
+ *    (t / grid_w, t % grid_w) of the patch grid. Landmark i sits at
+ *    (i / lm_w, i % lm_w) of the landmark grid.
+ *  - Element type. cfg->dtype selects the storage type of q, k, v, o, q_lm,
+ *    v_lm, k_x, v_x: MITA_F32 (float) or MITA_BF16 (bfloat16 bits). All
+ *    accumulation, scores, logits and softmax are fp32 in both cases.
+ *  - Streams. `stream` is a hipStream_t (NULL = the legacy default stream).
+ *    Calls only enqueue work on it and return; they never synchronise the
+ *    host (except mita_timer_read).
+ *  - Errors. Arguments are validated on the host before anything is
+ *    enqueued; on error nothing is launched and a status != MITA_OK is
+ *    returned, with details from mita_last_error(). No exception crosses the
+ *    ABI. NaN inputs are a caller error: results are then unspecified (but
+ *    every kernel still stays in bounds and terminates).
+ *  - Workspace. Entry points that take (ws, ws_bytes) need at least
+ *    mita_workspace_size(cfg, which) bytes of device memory there, 256-byte
+ *    aligned; its contents on entry do not matter. Calls sharing one
+ *    workspace on different streams race.
+ */
+#ifndef MITA_H
+#define MITA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define MITA_OK 0
+#define MITA_ERR_INVALID_ARG 1   /* bad sizes/grids, k or M out of [1, N], null or misaligned pointer, o aliasing an input, both branches off */
+#define MITA_ERR_UNSUPPORTED 2   /* d not in {64, 128}; s != 1; unknown dtype; N beyond the supported maximum */
+#define MITA_ERR_WORKSPACE 3     /* ws_bytes smaller than mita_workspace_size() */
+#define MITA_ERR_HIP 4           /* a HIP runtime or launch failure; see mita_last_error() */
+
+/* Storage types. */
+#define MITA_F32 0
+#define MITA_BF16 1
+
+/* Flags (cfg->flags). */
+#define MITA_FLAG_STAGED_GATHER 0x1u  /* mita_forward: materialise the expert tiles (Eq. gather) and
+                                         attend over them, instead of reading the selected K/V rows
+                                         in place inside the attention kernel. Same results. */
+
+/* Largest sequence length the top-k kernel accepts (one workgroup keeps a whole score row on chip). */
+#define MITA_MAX_N 65536
+
+typedef void *mita_stream_t; /* a hipStream_t */
+
+/*
+ * Problem description (Algorithm 1 "Require": Q, K, V in R^{d x N}, the number of
+ * landmark queries m, the expert width k, s = 1 routed expert per query).
+ */
+typedef struct {
+  int32_t B, H, N, d;      /* batch, heads, tokens, head dim; d in {64, 128} */
+  int32_t grid_h, grid_w;  /* token grid, grid_h * grid_w == N; grid_h == 1 gives 1-D pooling */
+  int32_t M, lm_h, lm_w;   /* landmarks (the paper's m), lm_h * lm_w == M, lm_h <= grid_h, lm_w <= grid_w */
+  int32_t k;               /* expert width, 1 <= k <= N */
+  int32_t s;               /* routed experts per query; must be 1 (Sec. 3.2 implementation) */
+  int32_t use_shared;      /* shared expert (Eq. shared-expert): landmarks as keys, landmark values as values */
+  int32_t use_routed;      /* routed top-k expert (Eq. mita-expert); at least one of the two must be set */
+  int32_t dtype;           /* MITA_F32 or MITA_BF16 */
+  float scale;             /* softmax/score scale; 0 means 1/sqrt(d) */
+  uint32_t flags;          /* MITA_FLAG_* */
+} mita_cfg_t;
+
+/* Workspace kinds for mita_workspace_size. */
+#define MITA_WS_FORWARD 0
+#define MITA_WS_SCORES 1
+#define MITA_WS_TOPK 2
+#define MITA_WS_ROUTE 3
+#define MITA_WS_ATTEND 4
+
+/* Host-only validation of cfg (no device needed). Returns a status code. */
+int mita_check(const mita_cfg_t *cfg);
+
+/* Bytes of workspace entry point `which` needs for cfg (0 if cfg is invalid). */
+size_t mita_workspace_size(const mita_cfg_t *cfg, int which);
+
+/* Static description of a status code; never NULL. */
+const char *mita_status_string(int status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char *mita_last_error(void);
+
+/*
+ * The whole forward (Algorithm 1 with s = 1; output Eq. mita).
+ *   q, k, v : [B, H, N, d] inputs;  o : [B, H, N, d] output (must not overlap q, k, v).
+ *   ws      : >= mita_workspace_size(cfg, MITA_WS_FORWARD) bytes.
+ */
+int mita_forward(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, void *o,
+                 void *ws, size_t ws_bytes, mita_stream_t stream);
+
+/*
+ * Landmark queries (Sec. 3.2: average pooling over uniformly spaced windows;
+ * Algorithm 1 AdaptiveAvgPool; Tab. A1 makes 2-D pooling the default).
+ * Window of landmark (a, b): rows [floor(a*gh/lh), ceil((a+1)*gh/lh)), columns
+ * [floor(b*gw/lw), ceil((b+1)*gw/lw)).
+ *   q    : [B, H, N, d];  q_lm : [B, H, M, d] output (fp32 mean, rounded once to dtype).
+ */
+int mita_landmarks(const mita_cfg_t *cfg, const void *q, void *q_lm, mita_stream_t stream);
+
+/*
+ * Landmark-key scores and landmark values, computed together (Sec. 3.2 notes
+ * Eq. top-k and Eq. landmark-value share K^T q_lm).
+ *   q_lm   : [B, H, M, d] landmark queries;  k, v : [B, H, N, d].
+ *   scores : [B, H, M, N] fp32 output, S[i, n] = fl(q_lm_i . k_n) * scale, or NULL.
+ *   v_lm   : [B, H, M, d] output, v_lm_i = sum_n softmax_n(S[i, :]) v_n (Eq. landmark-value), or NULL.
+ *   ws     : >= mita_workspace_size(cfg, MITA_WS_SCORES) bytes.
+ */
+int mita_scores(const mita_cfg_t *cfg, const void *q_lm, const void *k, const void *v,
+                float *scores, void *v_lm, void *ws, size_t ws_bytes, mita_stream_t stream);
+
+/*
+ * Top-k selection per landmark (Eq. top-k), exact: I_i holds the k token
+ * indices that come first when tokens are ordered by larger S[i, n], equal
+ * scores by lower n (-0 equals +0). Written in ascending index order.
+ *   scores : [B, H, M, N] fp32;  idx : [B, H, M, k] int32 output.  Requires N <= MITA_MAX_N.
+ *   ws     : may be NULL (mita_workspace_size(cfg, MITA_WS_TOPK) is 0).
+ */
+int mita_topk(const mita_cfg_t *cfg, const float *scores, int32_t *idx, void *ws, size_t ws_bytes,
+              mita_stream_t stream);
+
+/*
+ * Expert tiles (Eq. gather): k_x[b,h,i,j,:] = k[b,h,idx[b,h,i,j],:], likewise v_x.
+ *   idx : [B, H, M, k] int32, every entry in [0, N);  k_x, v_x : [B, H, M, k, d] outputs.
+ */
+int mita_gather(const mita_cfg_t *cfg, const void *k, const void *v, const int32_t *idx,
+                void *k_x, void *v_x, mita_stream_t stream);
+
+/*
+ * Routing (Sec. 3.2: logits Q^T q_lm, rank-1 expert e(q); Algorithm 1 ArgMax,
+ * ArgSort, BinCount, CumSum). expert[n] is the lowest i attaining the maximum
+ * of fl(q_n . q_lm_i) * scale. Queries are grouped by expert, stably.
+ *   q : [B, H, N, d];  q_lm : [B, H, M, d].
+ *   expert  : [B, H, N] int32 output;
+ *   perm    : [B, H, N] int32 output, tokens of expert 0, then expert 1, ..., ascending inside a group;
+ *   offsets : [B, H, M+1] int32 output, offsets[0] = 0, offsets[M] = N, group i = perm[offsets[i] : offsets[i+1]].
+ *   ws      : >= mita_workspace_size(cfg, MITA_WS_ROUTE) bytes.
+ */
+int mita_route(const mita_cfg_t *cfg, const void *q, const void *q_lm, int32_t *expert,
+               int32_t *perm, int32_t *offsets, void *ws, size_t ws_bytes, mita_stream_t stream);
+
+/*
+ * Attention of every query over the shared expert and its routed expert, as
+ * one softmax over the concatenated keys (Eq. mita, s = 1; Algorithm 1's
+ * shared-expert attention, varlen expert attention and online-softmax combine).
+ *   q : [B, H, N, d];  q_lm, v_lm : [B, H, M, d] (read if use_shared);
+ *   k_x, v_x : [B, H, M, k, d] expert tiles (read if use_routed);
+ *   perm, offsets : routing as produced by mita_route (read if use_routed);
+ *   o : [B, H, N, d] output in token order.
+ *   ws : >= mita_workspace_size(cfg, MITA_WS_ATTEND) bytes.
+ */
+int mita_attend(const mita_cfg_t *cfg, const void *q, const void *q_lm, const void *v_lm,
+                const void *k_x, const void *v_x, const int32_t *perm, const int32_t *offsets,
+                void *o, void *ws, size_t ws_bytes, mita_stream_t stream);
+
+/*
+ * Per-stage timing of mita_forward with HIP events (profiling aid).
+ * A timer holds event slots for up to max_calls forward calls; each
+ * mita_forward_timed call records MITA_NUM_STAGES + 1 events on the stream
+ * around the stages (landmarks, scores, top-k, gather, routing, attention; a
+ * stage that does not run records an empty interval).
+ */
+#define MITA_NUM_STAGES 6
+typedef struct mita_timer mita_timer_t;
+int mita_timer_create(mita_timer_t **timer, int max_calls);
+int mita_timer_destroy(mita_timer_t *timer);
+int mita_timer_reset(mita_timer_t *timer);
+/* Waits for the recorded events; fills ms[call * MITA_NUM_STAGES + stage]; *n_calls = calls recorded. */
+int mita_timer_read(mita_timer_t *timer, float *ms, int ms_len, int *n_calls);
+int mita_forward_timed(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, void *o,
+                       void *ws, size_t ws_bytes, mita_stream_t stream, mita_timer_t *timer);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MITA_H */

@@ -1,0 +1,293 @@
+// mita_api.hip - the C ABI (include/mita.h): validation, workspace carving and
+// the launch sequence of the forward pass (Algorithm 1 order).
+#include <hip/hip_runtime.h>
+
+#include <string>
+#include <vector>
+
+#include "check.hpp"
+#include "kernels.hpp"
+
+using namespace mita;
+
+namespace {
+
+thread_local std::string g_err;
+
+int set_err(int status, const std::string &msg) {
+  g_err = msg;
+  return status;
+}
+
+int hip_status(hipError_t e, const char *what) {
+  if (e == hipSuccess) return MITA_OK;
+  return set_err(MITA_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+int validate(const mita_cfg_t *c) {
+  std::string msg;
+  const int st = check_cfg(c, &msg);
+  if (st != MITA_OK) return set_err(st, msg);
+  return MITA_OK;
+}
+
+int need_ptr(const void *p, const char *name) {
+  if (!p) return set_err(MITA_ERR_INVALID_ARG, std::string(name) + " is NULL");
+  if (!aligned16(p)) return set_err(MITA_ERR_INVALID_ARG, std::string(name) + " is not 16-byte aligned");
+  return MITA_OK;
+}
+
+int need_ws(const mita_cfg_t *c, int which, const void *ws, size_t ws_bytes) {
+  const size_t need = workspace_size(c, which);
+  if (need == 0) return MITA_OK;
+  if (!ws || ws_bytes < need)
+    return set_err(MITA_ERR_WORKSPACE, "workspace needs " + std::to_string(need) + " bytes, got " +
+                                           std::to_string(ws ? ws_bytes : 0));
+  if (((uintptr_t)ws & (WS_ALIGN - 1)) != 0) return set_err(MITA_ERR_INVALID_ARG, "workspace is not 256-byte aligned");
+  return MITA_OK;
+}
+
+#define TRY(x)                   \
+  do {                           \
+    const int _s = (x);          \
+    if (_s != MITA_OK) return _s; \
+  } while (0)
+
+size_t tensor_bytes(const mita_cfg_t *c) { return (size_t)BH(*c) * c->N * c->d * elem_bytes(*c); }
+
+}  // namespace
+
+struct mita_timer {
+  int max_calls = 0;
+  int used = 0;
+  std::vector<hipEvent_t> ev;  // max_calls * (MITA_NUM_STAGES + 1)
+};
+
+namespace {
+
+int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *v, void *o, void *ws,
+                 size_t ws_bytes, hipStream_t st, mita_timer *timer) {
+  TRY(validate(c));
+  TRY(need_ptr(q, "q"));
+  TRY(need_ptr(k, "k"));
+  TRY(need_ptr(v, "v"));
+  TRY(need_ptr(o, "o"));
+  const size_t tb = tensor_bytes(c);
+  if (overlaps(o, tb, q, tb) || overlaps(o, tb, k, tb) || overlaps(o, tb, v, tb))
+    return set_err(MITA_ERR_INVALID_ARG, "o overlaps an input");
+  TRY(need_ws(c, MITA_WS_FORWARD, ws, ws_bytes));
+  hipEvent_t *ev = nullptr;
+  if (timer) {
+    if (timer->used >= timer->max_calls) return set_err(MITA_ERR_INVALID_ARG, "timer is full");
+    ev = &timer->ev[(size_t)timer->used * (MITA_NUM_STAGES + 1)];
+    timer->used++;
+  }
+  auto mark = [&](int i) -> int {
+    if (!ev) return MITA_OK;
+    return hip_status(hipEventRecord(ev[i], st), "hipEventRecord");
+  };
+
+  const FwdLayout L = forward_layout(*c);
+  char *w = (char *)ws;
+  void *q_lm = w + L.q_lm;
+  void *v_lm = c->use_shared ? (void *)(w + L.v_lm) : nullptr;
+  float *S = c->use_routed ? (float *)(w + L.scores) : nullptr;
+  int32_t *idx = (int32_t *)(w + L.idx);
+  const bool staged = c->use_routed && (c->flags & MITA_FLAG_STAGED_GATHER);
+  void *kx = w + L.kx, *vx = w + L.vx;
+  int32_t *expert = (int32_t *)(w + L.expert), *perm = (int32_t *)(w + L.perm);
+  int32_t *offsets = (int32_t *)(w + L.offsets), *tile_cnt = (int32_t *)(w + L.tile_cnt);
+  int32_t *tile_base = (int32_t *)(w + L.tile_base), *tile_start = (int32_t *)(w + L.tile_start);
+
+  TRY(mark(0));
+  TRY(hip_status(launch_pool(*c, q, q_lm, st), "landmarks"));
+  TRY(mark(1));
+  TRY(hip_status(launch_scores(*c, q_lm, k, v, S, v_lm, w + L.partial, st), "scores"));
+  TRY(mark(2));
+  if (c->use_routed) TRY(hip_status(launch_topk(*c, S, idx, st), "topk"));
+  TRY(mark(3));
+  if (staged) TRY(hip_status(launch_gather(*c, k, v, idx, kx, vx, st), "gather"));
+  TRY(mark(4));
+  if (c->use_routed) {
+    TRY(hip_status(launch_route(*c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, st), "route"));
+    TRY(hip_status(launch_worklist(*c, offsets, tile_start, st), "worklist"));
+  }
+  TRY(mark(5));
+  TRY(hip_status(launch_attend(*c, q, q_lm, v_lm, staged ? kx : k, staged ? vx : v, staged ? nullptr : idx, perm,
+                               offsets, tile_start, o, st),
+                 "attend"));
+  TRY(mark(6));
+  return MITA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mita_check(const mita_cfg_t *cfg) { return validate(cfg); }
+
+size_t mita_workspace_size(const mita_cfg_t *cfg, int which) { return workspace_size(cfg, which); }
+
+const char *mita_status_string(int status) {
+  switch (status) {
+    case MITA_OK: return "ok";
+    case MITA_ERR_INVALID_ARG: return "invalid argument";
+    case MITA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case MITA_ERR_WORKSPACE: return "workspace too small";
+    case MITA_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char *mita_last_error(void) { return g_err.c_str(); }
+
+int mita_forward(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, void *o, void *ws,
+                 size_t ws_bytes, mita_stream_t stream) {
+  g_err.clear();
+  return forward_impl(cfg, q, k, v, o, ws, ws_bytes, (hipStream_t)stream, nullptr);
+}
+
+int mita_forward_timed(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, void *o, void *ws,
+                       size_t ws_bytes, mita_stream_t stream, mita_timer_t *timer) {
+  g_err.clear();
+  if (!timer) return set_err(MITA_ERR_INVALID_ARG, "timer is NULL");
+  return forward_impl(cfg, q, k, v, o, ws, ws_bytes, (hipStream_t)stream, timer);
+}
+
+int mita_landmarks(const mita_cfg_t *cfg, const void *q, void *q_lm, mita_stream_t stream) {
+  g_err.clear();
+  TRY(validate(cfg));
+  TRY(need_ptr(q, "q"));
+  TRY(need_ptr(q_lm, "q_lm"));
+  return hip_status(launch_pool(*cfg, q, q_lm, (hipStream_t)stream), "landmarks");
+}
+
+int mita_scores(const mita_cfg_t *cfg, const void *q_lm, const void *k, const void *v, float *scores, void *v_lm,
+                void *ws, size_t ws_bytes, mita_stream_t stream) {
+  g_err.clear();
+  TRY(validate(cfg));
+  TRY(need_ptr(q_lm, "q_lm"));
+  TRY(need_ptr(k, "k"));
+  if (scores) TRY(need_ptr(scores, "scores"));
+  if (v_lm) {
+    TRY(need_ptr(v_lm, "v_lm"));
+    TRY(need_ptr(v, "v"));
+    TRY(need_ws(cfg, MITA_WS_SCORES, ws, ws_bytes));
+  }
+  return hip_status(launch_scores(*cfg, q_lm, k, v, scores, v_lm, ws, (hipStream_t)stream), "scores");
+}
+
+int mita_topk(const mita_cfg_t *cfg, const float *scores, int32_t *idx, void *ws, size_t ws_bytes,
+              mita_stream_t stream) {
+  g_err.clear();
+  (void)ws;
+  (void)ws_bytes;
+  TRY(validate(cfg));
+  TRY(need_ptr(scores, "scores"));
+  TRY(need_ptr(idx, "idx"));
+  return hip_status(launch_topk(*cfg, scores, idx, (hipStream_t)stream), "topk");
+}
+
+int mita_gather(const mita_cfg_t *cfg, const void *k, const void *v, const int32_t *idx, void *k_x, void *v_x,
+                mita_stream_t stream) {
+  g_err.clear();
+  TRY(validate(cfg));
+  TRY(need_ptr(k, "k"));
+  TRY(need_ptr(v, "v"));
+  TRY(need_ptr(idx, "idx"));
+  TRY(need_ptr(k_x, "k_x"));
+  TRY(need_ptr(v_x, "v_x"));
+  return hip_status(launch_gather(*cfg, k, v, idx, k_x, v_x, (hipStream_t)stream), "gather");
+}
+
+int mita_route(const mita_cfg_t *cfg, const void *q, const void *q_lm, int32_t *expert, int32_t *perm,
+               int32_t *offsets, void *ws, size_t ws_bytes, mita_stream_t stream) {
+  g_err.clear();
+  TRY(validate(cfg));
+  TRY(need_ptr(q, "q"));
+  TRY(need_ptr(q_lm, "q_lm"));
+  TRY(need_ptr(expert, "expert"));
+  TRY(need_ptr(perm, "perm"));
+  TRY(need_ptr(offsets, "offsets"));
+  TRY(need_ws(cfg, MITA_WS_ROUTE, ws, ws_bytes));
+  int32_t *tile_cnt = (int32_t *)ws;
+  int32_t *tile_base = (int32_t *)((char *)ws + route_ws_bytes(*cfg) / 2);
+  return hip_status(launch_route(*cfg, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, (hipStream_t)stream),
+                    "route");
+}
+
+int mita_attend(const mita_cfg_t *cfg, const void *q, const void *q_lm, const void *v_lm, const void *k_x,
+                const void *v_x, const int32_t *perm, const int32_t *offsets, void *o, void *ws, size_t ws_bytes,
+                mita_stream_t stream) {
+  g_err.clear();
+  TRY(validate(cfg));
+  TRY(need_ptr(q, "q"));
+  TRY(need_ptr(o, "o"));
+  if (cfg->use_shared) {
+    TRY(need_ptr(q_lm, "q_lm"));
+    TRY(need_ptr(v_lm, "v_lm"));
+  }
+  if (cfg->use_routed) {
+    TRY(need_ptr(k_x, "k_x"));
+    TRY(need_ptr(v_x, "v_x"));
+    TRY(need_ptr(perm, "perm"));
+    TRY(need_ptr(offsets, "offsets"));
+  }
+  const size_t tb = tensor_bytes(cfg);
+  if (overlaps(o, tb, q, tb)) return set_err(MITA_ERR_INVALID_ARG, "o overlaps q");
+  TRY(need_ws(cfg, MITA_WS_ATTEND, ws, ws_bytes));
+  hipStream_t st = (hipStream_t)stream;
+  int32_t *tile_start = (int32_t *)ws;
+  if (cfg->use_routed) TRY(hip_status(launch_worklist(*cfg, offsets, tile_start, st), "worklist"));
+  return hip_status(
+      launch_attend(*cfg, q, q_lm, v_lm, k_x, v_x, nullptr, perm, offsets, tile_start, o, st), "attend");
+}
+
+int mita_timer_create(mita_timer_t **timer, int max_calls) {
+  g_err.clear();
+  if (!timer || max_calls < 1) return set_err(MITA_ERR_INVALID_ARG, "bad timer arguments");
+  mita_timer *t = new mita_timer();
+  t->max_calls = max_calls;
+  t->ev.resize((size_t)max_calls * (MITA_NUM_STAGES + 1));
+  for (size_t i = 0; i < t->ev.size(); ++i) {
+    hipError_t e = hipEventCreate(&t->ev[i]);
+    if (e != hipSuccess) {
+      for (size_t j = 0; j < i; ++j) (void)hipEventDestroy(t->ev[j]);
+      delete t;
+      return hip_status(e, "hipEventCreate");
+    }
+  }
+  *timer = t;
+  return MITA_OK;
+}
+
+int mita_timer_destroy(mita_timer_t *timer) {
+  if (!timer) return MITA_OK;
+  for (hipEvent_t e : timer->ev) (void)hipEventDestroy(e);
+  delete timer;
+  return MITA_OK;
+}
+
+int mita_timer_reset(mita_timer_t *timer) {
+  if (!timer) return set_err(MITA_ERR_INVALID_ARG, "timer is NULL");
+  timer->used = 0;
+  return MITA_OK;
+}
+
+int mita_timer_read(mita_timer_t *timer, float *ms, int ms_len, int *n_calls) {
+  g_err.clear();
+  if (!timer || !ms || !n_calls) return set_err(MITA_ERR_INVALID_ARG, "NULL argument");
+  if (ms_len < timer->used * MITA_NUM_STAGES) return set_err(MITA_ERR_INVALID_ARG, "ms buffer too small");
+  *n_calls = timer->used;
+  if (timer->used == 0) return MITA_OK;
+  TRY(hip_status(hipEventSynchronize(timer->ev[(size_t)timer->used * (MITA_NUM_STAGES + 1) - 1]),
+                 "hipEventSynchronize"));
+  for (int c = 0; c < timer->used; ++c) {
+    hipEvent_t *ev = &timer->ev[(size_t)c * (MITA_NUM_STAGES + 1)];
+    for (int s = 0; s < MITA_NUM_STAGES; ++s)
+      TRY(hip_status(hipEventElapsedTime(&ms[c * MITA_NUM_STAGES + s], ev[s], ev[s + 1]), "hipEventElapsedTime"));
+  }
+  return MITA_OK;
+}
+
+}  // extern "C"

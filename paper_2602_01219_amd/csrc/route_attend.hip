@@ -1,0 +1,356 @@
+// route_attend.hip - routing of queries to landmarks and the MiTA attention.
+#include "cdna4.hpp"
+#include "flash.hpp"
+#include "kernels.hpp"
+#include "check.hpp"
+
+namespace mita {
+
+// ---------------------------------------------------------------------------
+// Routing logits and argmax (Sec. 3.2: logits Q^T Q_lm, rank-1 expert;
+// Algorithm 1 ArgMax). Workgroup = 4 waves x 16 queries = one 64-query tile.
+// Each wave forms L^T = Q_lm Q^T on MFMA one 16-landmark block at a time and
+// keeps a lane-local running (max, argmax) with strict '>' in increasing
+// landmark order, then merges the four lane groups preferring the lower
+// landmark on equal values. Also counts the tile's queries per expert.
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+__global__ __launch_bounds__(BLOCK) void route_logits_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
+                                                             int32_t *__restrict__ expert,
+                                                             int32_t *__restrict__ tile_cnt, int N, int M,
+                                                             float scale) {
+  extern __shared__ uint32_t cnt[];  // [M]
+  const int tile = blockIdx.x, ntiles = gridDim.x;
+  const int64_t bh = blockIdx.y;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
+  for (int i = threadIdx.x; i < M; i += BLOCK) cnt[i] = 0u;
+  const int n = tile * ROUTE_TQ + w * 16 + p;
+  Frag<T> qf[D / 32];
+#pragma unroll
+  for (int ks = 0; ks < D / 32; ++ks) {
+    if (n < N)
+      qf[ks].load(q + (bh * N + n) * D + ks * 32 + g * 8);
+    else
+      qf[ks].zero();
+  }
+  const T *lmb = q_lm + bh * (int64_t)M * D;
+  float best = -INFINITY;
+  int arg = 0;
+  for (int m0 = 0; m0 < M; m0 += 16) {
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int mrow = m0 + p;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      Frag<T> a;
+      if (mrow < M)
+        a.load(lmb + (int64_t)mrow * D + ks * 32 + g * 8);
+      else
+        a.zero();
+      acc = mma(a, qf[ks], acc);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int lmi = m0 + 4 * g + r;
+      const float val = acc[r] * scale;
+      if (lmi < M && val > best) {
+        best = val;
+        arg = lmi;
+      }
+    }
+  }
+  // merge the four lane groups of each query column (lower landmark wins ties)
+#pragma unroll
+  for (int o = 16; o <= 32; o <<= 1) {
+    const float ob = __shfl_xor(best, o);
+    const int oa = __shfl_xor(arg, o);
+    if (ob > best || (ob == best && oa < arg)) {
+      best = ob;
+      arg = oa;
+    }
+  }
+  __syncthreads();
+  if (g == 0 && n < N) {
+    expert[bh * N + n] = arg;
+    atomicAdd(&cnt[arg], 1u);
+  }
+  __syncthreads();
+  int32_t *tc = tile_cnt + (bh * ntiles + tile) * (int64_t)M;
+  for (int i = threadIdx.x; i < M; i += BLOCK) tc[i] = (int32_t)cnt[i];
+}
+
+// Block-wide exclusive scan of one value per thread (NT threads); returns the
+// exclusive prefix, *total gets the sum.
+template <int NT> __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t *wsum, uint32_t *total) {
+  constexpr int NW = NT / 64;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const uint32_t incl = wave_inclusive_scan(x);
+  if (lane == 63) wsum[w] = incl;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const uint32_t s = wsum[i];
+    before += i < w ? s : 0u;
+    all += s;
+  }
+  __syncthreads();
+  *total = all;
+  return before + incl - x;
+}
+
+// Per (b, h): expert sizes, offsets = [0, cumsum(counts)] (Algorithm 1 BinCount
+// and CumSum, counting the argmax output), and for every routing tile the
+// position its first query of each expert goes to. 1024 threads, one expert each.
+__global__ __launch_bounds__(1024) void route_scan_kernel(const int32_t *__restrict__ tile_cnt,
+                                                          int32_t *__restrict__ tile_base,
+                                                          int32_t *__restrict__ offsets, int ntiles, int M) {
+  __shared__ uint32_t wsum[16];
+  const int64_t bh = blockIdx.x;
+  const int e = threadIdx.x;
+  const int32_t *tc = tile_cnt + bh * ntiles * (int64_t)M;
+  uint32_t tot = 0;
+  if (e < M)
+    for (int t = 0; t < ntiles; ++t) tot += (uint32_t)tc[(int64_t)t * M + e];
+  uint32_t all;
+  const uint32_t off = block_exclusive_scan<1024>(tot, wsum, &all);
+  if (e < M) {
+    offsets[bh * (M + 1) + e] = (int32_t)off;
+    if (e == M - 1) offsets[bh * (M + 1) + M] = (int32_t)all;
+    int32_t *tb = tile_base + bh * ntiles * (int64_t)M;
+    uint32_t run = off;
+    for (int t = 0; t < ntiles; ++t) {
+      tb[(int64_t)t * M + e] = (int32_t)run;
+      run += (uint32_t)tc[(int64_t)t * M + e];
+    }
+  }
+}
+
+// Stable grouping (Algorithm 1 ArgSort of the argmax): within a 64-query tile
+// (one wave), a query's rank among earlier queries of the same expert comes
+// from matching expert ids bit by bit with ballots.
+__global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t *__restrict__ expert,
+                                                            const int32_t *__restrict__ tile_base,
+                                                            int32_t *__restrict__ perm, int N, int M, int ntiles,
+                                                            int ebits) {
+  const int64_t bh = blockIdx.y;
+  const int tile = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (tile >= ntiles) return;
+  const int n = tile * ROUTE_TQ + (threadIdx.x & 63);
+  const bool valid = n < N;
+  const int e = valid ? expert[bh * N + n] : 0;
+  uint64_t same = __ballot(valid);
+  for (int b = 0; b < ebits; ++b) {
+    const bool bit = (e >> b) & 1;
+    const uint64_t ones = __ballot(bit);
+    same &= bit ? ones : ~ones;
+  }
+  if (valid) {
+    const int pos = tile_base[(bh * ntiles + tile) * (int64_t)M + e] + (int)lanes_below(same);
+    perm[bh * N + pos] = n;
+  }
+}
+
+// Attention work list: tile_start[e] = sum over e' < e of ceil(size(e') / 64),
+// tile_start[M] = total tiles. 1024 threads, one expert each.
+__global__ __launch_bounds__(1024) void worklist_kernel(const int32_t *__restrict__ offsets,
+                                                        int32_t *__restrict__ tile_start, int M) {
+  __shared__ uint32_t wsum[16];
+  const int64_t bh = blockIdx.x;
+  const int e = threadIdx.x;
+  uint32_t nt = 0;
+  if (e < M) {
+    const int sz = offsets[bh * (M + 1) + e + 1] - offsets[bh * (M + 1) + e];
+    nt = (uint32_t)((sz + ATT_TQ - 1) / ATT_TQ);
+  }
+  uint32_t all;
+  const uint32_t before = block_exclusive_scan<1024>(nt, wsum, &all);
+  if (e < M) tile_start[bh * (M + 1) + e] = (int32_t)before;
+  if (e == 0) tile_start[bh * (M + 1) + M] = (int32_t)all;
+}
+
+// ---------------------------------------------------------------------------
+// MiTA attention (Eq. mita with s = 1): each query attends, in one online
+// softmax, over the shared expert (keys q_lm, values v_lm; Eq. shared-expert)
+// and then over the k keys of its routed expert (Eq. mita-expert). Workgroup
+// = 64 queries of one expert (4 waves x 16), taken from the routing work list
+// (Algorithm 1's varlen grouping); outputs are scattered back to token order.
+// With ROUTED, routed keys come from the expert tiles, or straight from the
+// K/V rows listed in idx (FUSED: the gather of Eq. gather done in place).
+// ---------------------------------------------------------------------------
+template <typename T, int D, bool SHARED, bool ROUTED, bool FUSED>
+__global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
+                                                       const T *__restrict__ v_lm, const T *__restrict__ rk,
+                                                       const T *__restrict__ rv, const int32_t *__restrict__ idx,
+                                                       const int32_t *__restrict__ perm,
+                                                       const int32_t *__restrict__ offsets,
+                                                       const int32_t *__restrict__ tile_start, T *__restrict__ o,
+                                                       int N, int M, int k, float scale) {
+  using TD = TileDims<T, D>;
+  __shared__ __align__(16) T Ks[TD::K_ELEMS];
+  __shared__ __align__(16) T Vt[TD::V_ELEMS];
+  const int64_t bh = blockIdx.y;
+  const int t = blockIdx.x;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
+
+  int e = 0, q_begin, q_end;
+  if (ROUTED) {
+    const int32_t *ts = tile_start + bh * (M + 1);
+    if (t >= ts[M]) return;  // uniform for the workgroup
+    int lo = 0, hi = M - 1;  // largest e with ts[e] <= t
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (ts[mid] <= t)
+        lo = mid;
+      else
+        hi = mid - 1;
+    }
+    e = lo;
+    const int32_t *of = offsets + bh * (M + 1);
+    q_begin = of[e] + (t - ts[e]) * ATT_TQ;
+    q_end = min(of[e + 1], q_begin + ATT_TQ);
+  } else {
+    q_begin = t * ATT_TQ;
+    q_end = min(N, q_begin + ATT_TQ);
+  }
+  const int qi = q_begin + w * 16 + p;
+  const bool qvalid = qi < q_end;
+  const int token = qvalid ? (ROUTED ? perm[bh * N + qi] : qi) : 0;
+
+  Frag<T> qf[D / 32];
+#pragma unroll
+  for (int ks = 0; ks < D / 32; ++ks) {
+    if (qvalid)
+      qf[ks].load(q + (bh * N + token) * D + ks * 32 + g * 8);
+    else
+      qf[ks].zero();
+  }
+  Online<D> st;
+  st.init();
+  const float sl2 = scale * LOG2E;
+
+  if (SHARED) {
+    const T *kb_ = q_lm + bh * (int64_t)M * D;
+    const T *vb_ = v_lm + bh * (int64_t)M * D;
+    for (int k0 = 0; k0 < M; k0 += TK) {
+      const int nvalid = min(TK, M - k0);
+      __syncthreads();
+      load_kv_tile<T, D>(Ks, Vt, kb_ + (int64_t)k0 * D, vb_ + (int64_t)k0 * D, nullptr, nvalid);
+      __syncthreads();
+      f32x4 acc[4];
+      tile_scores<T, D>(acc, Ks, qf);
+      tile_softmax_pv<T, D>(st, acc, Vt, nvalid, sl2);
+    }
+  }
+  if (ROUTED) {
+    const T *kb_;
+    const T *vb_;
+    const int32_t *ib = nullptr;
+    if (FUSED) {
+      kb_ = rk + bh * (int64_t)N * D;
+      vb_ = rv + bh * (int64_t)N * D;
+      ib = idx + (bh * M + e) * (int64_t)k;
+    } else {
+      kb_ = rk + (bh * M + e) * (int64_t)k * D;
+      vb_ = rv + (bh * M + e) * (int64_t)k * D;
+    }
+    for (int k0 = 0; k0 < k; k0 += TK) {
+      const int nvalid = min(TK, k - k0);
+      __syncthreads();
+      if (FUSED)
+        load_kv_tile<T, D>(Ks, Vt, kb_, vb_, ib + k0, nvalid);
+      else
+        load_kv_tile<T, D>(Ks, Vt, kb_ + (int64_t)k0 * D, vb_ + (int64_t)k0 * D, nullptr, nvalid);
+      __syncthreads();
+      f32x4 acc[4];
+      tile_scores<T, D>(acc, Ks, qf);
+      tile_softmax_pv<T, D>(st, acc, Vt, nvalid, sl2);
+    }
+  }
+  const float l = column_sum(st.l);
+  if (!qvalid) return;
+  const float inv = 1.0f / l;
+  T *orow = o + (bh * N + token) * D;
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db) {
+    T vals[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) vals[r] = from_f32<T>(st.o[db][r] * inv);
+    T *dst = orow + db * 16 + 4 * g;
+    if (sizeof(T) == 2)
+      *reinterpret_cast<uint2 *>(dst) = *reinterpret_cast<const uint2 *>(vals);
+    else
+      *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(vals);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+static hipError_t route_t(const mita_cfg_t &c, const void *q, const void *q_lm, int32_t *expert, int32_t *perm,
+                          int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, hipStream_t st) {
+  const int nt = route_tiles(c);
+  const unsigned bh = (unsigned)BH(c);
+  hipLaunchKernelGGL((route_logits_kernel<T, D>), dim3(nt, bh), dim3(BLOCK), c.M * sizeof(uint32_t), st,
+                     (const T *)q, (const T *)q_lm, expert, tile_cnt, c.N, c.M, eff_scale(c));
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(route_scan_kernel, dim3(bh), dim3(1024), 0, st, tile_cnt, tile_base, offsets, nt, c.M);
+  if ((err = hipGetLastError()) != hipSuccess) return err;
+  int ebits = 0;
+  while ((1 << ebits) < c.M) ++ebits;
+  hipLaunchKernelGGL(route_scatter_kernel, dim3((nt + 3) / 4, bh), dim3(256), 0, st, expert, tile_base, perm, c.N,
+                     c.M, nt, ebits);
+  return hipGetLastError();
+}
+
+hipError_t launch_route(const mita_cfg_t &c, const void *q, const void *q_lm, int32_t *expert, int32_t *perm,
+                        int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, hipStream_t st) {
+  if (c.dtype == MITA_F32)
+    return c.d == 64 ? route_t<float, 64>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, st)
+                     : route_t<float, 128>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, st);
+  return c.d == 64 ? route_t<bf16_t, 64>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, st)
+                   : route_t<bf16_t, 128>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, st);
+}
+
+hipError_t launch_worklist(const mita_cfg_t &c, const int32_t *offsets, int32_t *tile_start, hipStream_t st) {
+  hipLaunchKernelGGL(worklist_kernel, dim3((unsigned)BH(c)), dim3(1024), 0, st, offsets, tile_start, c.M);
+  return hipGetLastError();
+}
+
+template <typename T, int D, bool SH, bool RT, bool FU>
+static hipError_t attend_t3(const mita_cfg_t &c, const void *q, const void *q_lm, const void *v_lm, const void *rk,
+                            const void *rv, const int32_t *idx, const int32_t *perm, const int32_t *offsets,
+                            const int32_t *tile_start, void *o, hipStream_t st) {
+  // routed: at most ceil(N/64) + M tiles (each expert adds at most one partial tile)
+  const int tiles = RT ? (c.N + ATT_TQ - 1) / ATT_TQ + c.M : (c.N + ATT_TQ - 1) / ATT_TQ;
+  hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU>), dim3(tiles, (unsigned)BH(c)), dim3(BLOCK), 0, st,
+                     (const T *)q, (const T *)q_lm, (const T *)v_lm, (const T *)rk, (const T *)rv, idx, perm, offsets,
+                     tile_start, (T *)o, c.N, c.M, c.k, eff_scale(c));
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+static hipError_t attend_t(const mita_cfg_t &c, const void *q, const void *q_lm, const void *v_lm, const void *rk,
+                           const void *rv, const int32_t *idx, const int32_t *perm, const int32_t *offsets,
+                           const int32_t *tile_start, void *o, hipStream_t st) {
+  if (!c.use_routed) return attend_t3<T, D, true, false, false>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
+  if (idx) {
+    if (c.use_shared) return attend_t3<T, D, true, true, true>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
+    return attend_t3<T, D, false, true, true>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
+  }
+  if (c.use_shared) return attend_t3<T, D, true, true, false>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
+  return attend_t3<T, D, false, true, false>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
+}
+
+hipError_t launch_attend(const mita_cfg_t &c, const void *q, const void *q_lm, const void *v_lm, const void *rk,
+                         const void *rv, const int32_t *idx, const int32_t *perm, const int32_t *offsets,
+                         const int32_t *tile_start, void *o, hipStream_t st) {
+  if (c.dtype == MITA_F32)
+    return c.d == 64 ? attend_t<float, 64>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st)
+                     : attend_t<float, 128>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
+  return c.d == 64 ? attend_t<bf16_t, 64>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st)
+                   : attend_t<bf16_t, 128>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
+}
+
+}  // namespace mita

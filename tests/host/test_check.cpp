@@ -1,0 +1,69 @@
+// Host-only test of the argument validation and workspace layout (no GPU).
+#include <cassert>
+#include <cstdio>
+#include <string>
+
+#include "../../paper_2602_01219_amd/csrc/check.hpp"
+
+static mita_cfg_t base() {
+  mita_cfg_t c{};
+  c.B = 2; c.H = 12; c.N = 16384; c.d = 64; c.grid_h = 128; c.grid_w = 128;
+  c.M = 128; c.lm_h = 8; c.lm_w = 16; c.k = 512; c.s = 1; c.use_shared = 1; c.use_routed = 1;
+  c.dtype = MITA_BF16; c.scale = 0.f; c.flags = 0;
+  return c;
+}
+
+#define EXPECT(expr, code)                                                     \
+  do {                                                                         \
+    mita_cfg_t c = base();                                                     \
+    expr;                                                                      \
+    std::string e;                                                             \
+    int got = mita::check_cfg(&c, &e);                                         \
+    if (got != (code)) {                                                       \
+      std::printf("FAIL %s: got %d want %d (%s)\n", #expr, got, code, e.c_str()); \
+      return 1;                                                                \
+    }                                                                          \
+  } while (0)
+
+int main() {
+  EXPECT((void)0, MITA_OK);
+  EXPECT(c.d = 96, MITA_ERR_UNSUPPORTED);
+  EXPECT(c.s = 2, MITA_ERR_UNSUPPORTED);
+  EXPECT(c.dtype = 7, MITA_ERR_UNSUPPORTED);
+  EXPECT(c.N = 70000, MITA_ERR_INVALID_ARG);                       // grid no longer matches
+  EXPECT((c.N = 131072, c.grid_h = 256, c.grid_w = 512), MITA_ERR_UNSUPPORTED);
+  EXPECT(c.k = 0, MITA_ERR_INVALID_ARG);
+  EXPECT(c.k = 16385, MITA_ERR_INVALID_ARG);
+  EXPECT(c.k = 16384, MITA_OK);
+  EXPECT((c.M = 0, c.lm_h = 0), MITA_ERR_INVALID_ARG);
+  EXPECT((c.lm_h = 4, c.lm_w = 16), MITA_ERR_INVALID_ARG);         // lm grid != M
+  EXPECT((c.grid_h = 4, c.grid_w = 4096, c.lm_h = 8), MITA_ERR_INVALID_ARG);  // lm grid > token grid
+  EXPECT((c.use_shared = 0, c.use_routed = 0), MITA_ERR_INVALID_ARG);
+  EXPECT(c.use_shared = 2, MITA_ERR_INVALID_ARG);
+  EXPECT(c.scale = -1.f, MITA_ERR_INVALID_ARG);
+  EXPECT(c.flags = 0x80, MITA_ERR_INVALID_ARG);
+  EXPECT(c.flags = MITA_FLAG_STAGED_GATHER, MITA_OK);
+  EXPECT(c.B = 0, MITA_ERR_INVALID_ARG);
+  assert(mita::check_cfg(nullptr, nullptr) == MITA_ERR_INVALID_ARG);
+
+  // workspace layout: aligned, non-overlapping, monotone
+  mita_cfg_t c = base();
+  mita::FwdLayout L = mita::forward_layout(c);
+  const size_t offs[] = {L.q_lm, L.v_lm, L.scores, L.partial, L.idx, L.kx, L.vx, L.expert,
+                         L.perm, L.offsets, L.tile_cnt, L.tile_base, L.tile_start, L.total};
+  for (size_t i = 0; i + 1 < sizeof offs / sizeof offs[0]; ++i) {
+    assert(offs[i] % 256 == 0);
+    assert(offs[i] <= offs[i + 1]);
+  }
+  assert(L.scores - L.v_lm >= (size_t)2 * 12 * 128 * 64 * 2);
+  assert(L.idx - L.partial == mita::scores_ws_bytes(c));
+  assert(L.kx == L.vx && L.vx == L.expert);  // tiles absent without the staged-gather flag
+  c.flags = MITA_FLAG_STAGED_GATHER;
+  mita::FwdLayout L2 = mita::forward_layout(c);
+  assert(L2.vx - L2.kx == (size_t)24 * 128 * 512 * 64 * 2);
+  assert(mita::workspace_size(&c, MITA_WS_TOPK) == 0);
+  c.d = 96;
+  assert(mita::workspace_size(&c, MITA_WS_FORWARD) == 0);
+  std::printf("host checks ok\n");
+  return 0;
+}

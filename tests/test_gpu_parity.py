@@ -1,0 +1,405 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Protocol (stage level, identical inputs): each GPU stage is fed exactly the
+tensors the oracle's stage consumes (the GPU's own upstream outputs, widened
+exactly), so discrete results (top-k sets, gather, grouping) must be
+bit-identical and continuous ones within the stated tolerance.
+
+Protocol (end to end): the GPU forward runs on the seeded inputs; its top-k
+sets and routing are validated against the oracle's own float64 scores and
+logits within a rounding budget (a GPU choice may differ from the oracle's
+only where the two candidates are closer than the budget); the oracle is then
+re-run with the GPU's discrete choices and the outputs compared:
+max|o_gpu - o_ref| / max|o_ref| per (b, h) slice <= 1e-5 (fp32) / 2e-2 (bf16).
+"""
+from __future__ import annotations
+
+import dataclasses
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import mita_oracle as O
+from paper_2602_01219_amd import mita, synth
+from tests.gpu_helpers import (U, check_routing, check_selection, from_dev, landmark_error, log, maxrel, to_dev,
+                               tol_for, window_stats)
+
+pytestmark = pytest.mark.gpu
+
+ALL = synth.WORKLOAD_ORDER
+
+
+@functools.lru_cache(maxsize=None)
+def _inputs(name: str):
+    log(f"[gen] {name}")
+    return synth.generate(synth.WORKLOADS[name])
+
+
+@functools.lru_cache(maxsize=None)
+def _dev_inputs(name: str):
+    inp = _inputs(name)
+    return tuple(to_dev(x, inp.wl.dtype) for x in (inp.q, inp.k, inp.v))
+
+
+def _slice64(inp, b, h):
+    if inp.wl.dtype == "f32":
+        return tuple(x[b, h].astype(np.float64) for x in (inp.q, inp.k, inp.v))
+    return tuple(synth.bf16_bits_to_f32(x[b, h]).astype(np.float64) for x in (inp.q, inp.k, inp.v))
+
+
+def _slices(wl, n=2):
+    """The (b, h) slices compared against the oracle: first and last (and a middle one)."""
+    out = [(0, 0), (wl.B - 1, wl.H - 1)]
+    if n > 2:
+        out.append((wl.B // 2, wl.H // 2))
+    return sorted(set(out))[:n]
+
+
+def _rows(N, limit, seed=0):
+    if N <= limit:
+        return np.arange(N)
+    r = np.random.default_rng(seed)
+    rows = np.unique(np.concatenate([[0, N - 1], r.choice(N, limit - 2, replace=False)]))
+    return rows
+
+
+def _stages(cfg: mita.Config, q, k, v):
+    """Run the stage entry points in the forward's order (staged gather)."""
+    q_lm = mita.landmarks(cfg, q)
+    S, v_lm = mita.scores(cfg, q_lm, k, v, want_scores=bool(cfg.use_routed), want_v_lm=bool(cfg.use_shared))
+    out = dict(q_lm=q_lm, S=S, v_lm=v_lm)
+    if cfg.use_routed:
+        idx = mita.topk(cfg, S)
+        kx, vx = mita.gather(cfg, k, v, idx)
+        expert, perm, offsets = mita.route(cfg, q, q_lm)
+        out.update(idx=idx, kx=kx, vx=vx, expert=expert, perm=perm, offsets=offsets)
+    else:
+        kx = vx = perm = offsets = None
+    out["o"] = mita.attend(cfg, q, q_lm, v_lm, kx, vx, perm, offsets)
+    return out
+
+
+def _bounds(q, k, q_lm_ref, cfg, dtype):
+    """Rounding budgets of the GPU scores (landmark x key) and routing logits
+    (query x landmark) against the oracle's float64 values."""
+    qa, W = window_stats(q, cfg.grid_h, cfg.grid_w, cfg.lm_h, cfg.lm_w)
+    err = landmark_error(qa, q_lm_ref, W, dtype)
+    sc, d = cfg.eff_scale, cfg.d
+    ka, qabs, lma = np.abs(k), np.abs(q), np.abs(q_lm_ref) + err
+    tau_s = sc * (err @ ka.T) + sc * 2.0 * (d + 2) * U * (lma @ ka.T)
+    tau_r = sc * (qabs @ err.T) + sc * 2.0 * (d + 2) * U * (qabs @ lma.T)
+    return tau_s, tau_r
+
+
+def _end_to_end(cfg: mita.Config, inp: synth.Inputs, q, k, v, slices, row_limit, exact_sets=False):
+    o_fwd = mita.forward(cfg, q, k, v)
+    st = _stages(cfg, q, k, v)
+    torch.cuda.synchronize()
+    assert torch.equal(o_fwd.view(torch.int16) if o_fwd.dtype == torch.bfloat16 else o_fwd,
+                       st["o"].view(torch.int16) if o_fwd.dtype == torch.bfloat16 else st["o"]), \
+        "forward differs from the stage pipeline"
+    tol = tol_for(cfg.dtype)
+    o_g = o_fwd
+    worst = 0.0
+    for (b, h) in slices:
+        qs, ks, vs = _slice64(inp, b, h)
+        rows = _rows(cfg.N, row_limit, seed=b * 131 + h)
+        q_lm_ref = O.landmarks(qs, cfg.grid_h, cfg.grid_w, cfg.lm_h, cfg.lm_w)
+        force_idx = force_exp = None
+        if cfg.use_routed:
+            S_ref = O.scores(q_lm_ref, ks, cfg.eff_scale)
+            tau_s, tau_r = _bounds(qs, ks, q_lm_ref, cfg, cfg.dtype)
+            force_idx = st["idx"][b, h].cpu().numpy().astype(np.int64)
+            same = check_selection(S_ref, tau_s, force_idx, cfg.k)
+            force_exp = st["expert"][b, h].cpu().numpy().astype(np.int64)
+            L_ref = (qs @ q_lm_ref.T) * cfg.eff_scale
+            agree = check_routing(L_ref, tau_r, force_exp)
+            log(f"  slice ({b},{h}): top-k sets equal to the oracle's {same}/{cfg.M}, routing agrees {agree}/{cfg.N}")
+            if exact_sets:
+                # with every score gap above the budget the sets must be the oracle's own
+                for i in range(cfg.M):
+                    srt = np.sort(S_ref[i])[::-1]
+                    if cfg.k < cfg.N and srt[cfg.k - 1] - srt[cfg.k] > 2 * tau_s[i].max():
+                        ref = O.topk_indices(S_ref[i:i + 1], cfg.k)[0]
+                        assert (ref == force_idx[i]).all()
+        r = O.forward_slice(qs, ks, vs, cfg.grid_h, cfg.grid_w, cfg.lm_h, cfg.lm_w, cfg.k, None, cfg.use_shared,
+                            cfg.use_routed, force_idx, force_exp, rows=rows)
+        got = from_dev(o_g[b, h])[rows]
+        err = maxrel(got, r.o)
+        worst = max(worst, err)
+        log(f"  slice ({b},{h}) rows {len(rows)}: max-rel error {err:.3e} (tol {tol})")
+        assert err <= tol
+    return worst
+
+
+# ------------------------------------------------------------------ stage parity
+@pytest.mark.parametrize("name", ALL)
+def test_landmarks_parity(name):
+    inp = _inputs(name)
+    wl = inp.wl
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = _dev_inputs(name)
+    q_lm = from_dev(mita.landmarks(cfg, q))
+    for (b, h) in _slices(wl, 3):
+        qs = _slice64(inp, b, h)[0]
+        ref = O.landmarks(qs, wl.grid_h, wl.grid_w, wl.lm_h, wl.lm_w)
+        got = q_lm[b, h]
+        qa, W = window_stats(qs, wl.grid_h, wl.grid_w, wl.lm_h, wl.lm_w)
+        summation = 2 * (W[:, None] + 2) * U * qa + 1e-30     # fp32 summation of the window
+        if wl.dtype == "f32":
+            assert (np.abs(got - ref) <= summation).all()
+        else:
+            # one bf16 rounding of the fp32 mean: within one bf16 ulp of the exact mean
+            ulp = 2.0 ** (np.floor(np.log2(np.maximum(np.abs(ref), 1e-30))) - 7)
+            assert (np.abs(got - ref) <= ulp + summation).all()
+
+
+@pytest.mark.parametrize("name", ALL)
+def test_scores_and_landmark_values_parity(name):
+    inp = _inputs(name)
+    wl = inp.wl
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = _dev_inputs(name)
+    q_lm = mita.landmarks(cfg, q)
+    S, v_lm = mita.scores(cfg, q_lm, k, v)
+    S_g, v_lm_g, q_lm_g = from_dev(S), from_dev(v_lm), from_dev(q_lm)
+    for (b, h) in _slices(wl):
+        qs, ks, vs = _slice64(inp, b, h)
+        S_ref = O.scores(q_lm_g[b, h], ks, cfg.eff_scale)     # identical landmark input
+        tau = cfg.eff_scale * 2.0 * (cfg.d + 2) * U * (np.abs(q_lm_g[b, h]) @ np.abs(ks).T) + 1e-30
+        assert (np.abs(S_g[b, h] - S_ref) <= tau).all()
+        ref = O.landmark_values(S_ref, vs)
+        err = maxrel(v_lm_g[b, h], ref)
+        log(f"  v_lm slice ({b},{h}) max-rel {err:.3e}")
+        assert err <= tol_for(wl.dtype)
+
+
+@pytest.mark.parametrize("name", ALL)
+def test_topk_bit_exact_from_identical_scores(name):
+    inp = _inputs(name)
+    wl = inp.wl
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = _dev_inputs(name)
+    S, _ = mita.scores(cfg, mita.landmarks(cfg, q), k, v, want_v_lm=False)
+    idx = mita.topk(cfg, S).cpu().numpy()
+    S_g = S.cpu().numpy()
+    for (b, h) in _slices(wl):
+        ref = O.topk_indices(S_g[b, h].astype(np.float64), cfg.k)
+        assert np.array_equal(idx[b, h], ref)
+
+
+def _torture_scores(kind, M, N, seed):
+    r = np.random.default_rng(seed)
+    if kind == "quantised":
+        S = np.round(r.standard_normal((M, N)) * 2) / 3
+    elif kind == "signed_zero":
+        S = r.choice(np.array([0.0, -0.0, 1.0, -1.0]), size=(M, N), p=[0.45, 0.45, 0.05, 0.05])
+    elif kind == "inf":
+        S = r.choice(np.array([np.inf, -np.inf, 0.5, -0.5, 3.0]), size=(M, N))
+    elif kind == "constant":
+        S = np.full((M, N), 0.25)
+    elif kind == "subnormal":
+        S = r.choice(np.array([1e-45, -1e-45, 1e-40, 0.0, -3e-39]), size=(M, N))
+    elif kind == "clustered":
+        S = (r.integers(0, 4, size=(M, N)) + 1e-3 * r.standard_normal((M, N))) * 1e3
+    else:
+        S = r.standard_normal((M, N)) * np.exp(r.uniform(-20, 20, size=(M, 1)))
+    return S.astype(np.float32)
+
+
+@pytest.mark.parametrize("N", [1, 5, 63, 64, 65, 196, 256, 257, 1000, 4096, 4097, 8191, 16384, 30000, 65536])
+@pytest.mark.parametrize("kind", ["quantised", "signed_zero", "inf", "constant", "subnormal", "clustered", "random"])
+def test_topk_tie_torture(N, kind):
+    M = min(3, N)
+    S = _torture_scores(kind, M, N, seed=N * 7 + len(kind))
+    Sd = torch.from_numpy(S).cuda().reshape(1, 1, M, N)
+    for k in sorted({1, max(1, N // 3), N}):
+        cfg = mita.Config(B=1, H=1, N=N, d=64, grid_h=1, grid_w=N, M=M, lm_h=1, lm_w=M, k=k)
+        got = mita.topk(cfg, Sd).cpu().numpy()[0, 0]
+        ref = O.topk_indices(S.astype(np.float64), k)
+        assert np.array_equal(got, ref), (kind, N, k)
+
+
+def test_gather_bit_exact():
+    inp = synth.generate(synth.WORKLOADS["vitb_hr_bf16"].with_(B=1, H=2, grid_h=32, grid_w=32))
+    cfg = mita.Config.from_workload(inp.wl)
+    q, k, v = (to_dev(x, "bf16") for x in (inp.q, inp.k, inp.v))
+    r = np.random.default_rng(5)
+    idx = np.sort(r.integers(0, cfg.N, size=(1, 2, cfg.M, cfg.k)), axis=-1).astype(np.int32)
+    idx[0, 0, 0] = cfg.N - 1
+    kx, vx = mita.gather(cfg, k, v, torch.from_numpy(idx).cuda())
+    for h in range(2):
+        np.testing.assert_array_equal(kx[0, h].view(torch.int16).cpu().numpy().view(np.uint16),
+                                      inp.k[0, h][idx[0, h]])
+        np.testing.assert_array_equal(vx[0, h].view(torch.int16).cpu().numpy().view(np.uint16),
+                                      inp.v[0, h][idx[0, h]])
+
+
+@pytest.mark.parametrize("name", ALL)
+def test_routing_parity(name):
+    inp = _inputs(name)
+    wl = inp.wl
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = _dev_inputs(name)
+    q_lm = mita.landmarks(cfg, q)
+    expert, perm, offsets = mita.route(cfg, q, q_lm)
+    q_lm_g = from_dev(q_lm)
+    e_all, p_all, o_all = expert.cpu().numpy(), perm.cpu().numpy(), offsets.cpu().numpy()
+    for (b, h) in _slices(wl):
+        qs = _slice64(inp, b, h)[0]
+        L = (qs @ q_lm_g[b, h].T) * cfg.eff_scale            # identical landmark input
+        tau = cfg.eff_scale * 2.0 * (cfg.d + 2) * U * (np.abs(qs) @ np.abs(q_lm_g[b, h]).T) + 1e-30
+        agree = check_routing(L, tau, e_all[b, h])
+        log(f"  routing slice ({b},{h}) agrees with the fp64 argmax on {agree}/{cfg.N}")
+        rt = O.routing_from_expert(e_all[b, h], cfg.M)
+        assert np.array_equal(p_all[b, h], rt.perm)
+        assert np.array_equal(o_all[b, h], rt.offsets)
+
+
+@pytest.mark.parametrize("name", ALL)
+def test_attend_parity_identical_inputs(name):
+    inp = _inputs(name)
+    wl = inp.wl
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = _dev_inputs(name)
+    st = _stages(cfg, q, k, v)
+    o_g = st["o"]
+    for (b, h) in _slices(wl):
+        qs, ks, vs = _slice64(inp, b, h)
+        rows = _rows(cfg.N, 384, seed=b + h)
+        q_lm, v_lm = from_dev(st["q_lm"][b, h]), (from_dev(st["v_lm"][b, h]) if cfg.use_shared else None)
+        idx = st["idx"][b, h].cpu().numpy()
+        ex = st["expert"][b, h].cpu().numpy()
+        kx, vx = O.gather(ks, vs, idx)
+        ref = O.output_per_query(qs[rows], q_lm, v_lm, kx, vx, ex[rows], cfg.eff_scale, cfg.use_shared,
+                                 cfg.use_routed)
+        err = maxrel(from_dev(o_g[b, h])[rows], ref)
+        log(f"  attend slice ({b},{h}) max-rel {err:.3e}")
+        assert err <= tol_for(wl.dtype)
+
+
+# ------------------------------------------------------------------ end to end
+@pytest.mark.parametrize("name", ALL)
+def test_forward_end_to_end(name):
+    inp = _inputs(name)
+    wl = inp.wl
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = _dev_inputs(name)
+    log(f"[forward] {name} B={wl.B} H={wl.H} N={wl.N} d={wl.d} M={wl.M} k={wl.k} {wl.dtype}")
+    _end_to_end(cfg, inp, q, k, v, _slices(wl), row_limit=256 if wl.N > 4096 else 512,
+                exact_sets=(wl.dtype == "f32"))
+
+
+def test_dense_equivalence_is_full_attention():
+    """Route-only with k = N: every expert holds every key, so each query's
+    output is full softmax attention (compared with torch SDPA in float64),
+    whatever the number of landmarks."""
+    inp = _inputs("dense_equiv_bf16")
+    wl = inp.wl
+    q, k, v = _dev_inputs("dense_equiv_bf16")
+    outs = []
+    for M, (lh, lw) in ((wl.M, (wl.lm_h, wl.lm_w)), (16, (4, 4))):
+        cfg = mita.Config.from_workload(wl, M=M, lm_h=lh, lm_w=lw)
+        outs.append(mita.forward(cfg, q, k, v))
+    torch.cuda.synchronize()
+    for (b, h) in _slices(wl):
+        qs, ks, vs = _slice64(inp, b, h)
+        rows = _rows(wl.N, 256, seed=h)
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            torch.from_numpy(qs[rows])[None], torch.from_numpy(ks)[None], torch.from_numpy(vs)[None])[0].numpy()
+        for o in outs:
+            err = maxrel(from_dev(o[b, h])[rows], ref)
+            log(f"  dense slice ({b},{h}) max-rel vs SDPA {err:.3e}")
+            assert err <= 2e-2
+
+
+EDGE = [
+    # (grid_h, grid_w, lm_h, lm_w, k, d, dtype, use_shared, use_routed)
+    (1, 1, 1, 1, 1, 64, "f32", 1, 1),
+    (1, 7, 1, 3, 2, 64, "bf16", 1, 1),        # 1-D pooling, ragged windows
+    (7, 9, 2, 2, 63, 64, "f32", 1, 1),        # k = N
+    (5, 13, 1, 5, 17, 128, "bf16", 1, 1),
+    (15, 20, 3, 4, 1, 64, "bf16", 1, 1),      # k = 1
+    (14, 14, 7, 7, 49, 64, "bf16", 1, 1),     # m = k = 49 on a 14x14 grid
+    (14, 14, 5, 5, 25, 128, "f32", 1, 1),     # m = k = 25, non-divisible windows
+    (16, 16, 4, 4, 40, 64, "bf16", 0, 1),     # route-only
+    (16, 16, 4, 4, 40, 64, "bf16", 1, 0),     # compress-only
+    (16, 16, 4, 4, 40, 128, "f32", 0, 1),
+    (32, 33, 8, 11, 100, 64, "bf16", 1, 1),   # M = 88 (two partial landmark blocks), ragged N = 1056
+    (9, 8, 9, 8, 5, 64, "bf16", 1, 1),        # M = N
+]
+
+
+@pytest.mark.parametrize("case", EDGE, ids=[f"{c[0]}x{c[1]}_m{c[2]*c[3]}_k{c[4]}_d{c[5]}_{c[6]}_s{c[7]}r{c[8]}"
+                                            for c in EDGE])
+def test_forward_edge_cases(case):
+    gh, gw, lh, lw, kk, d, dtype, sh, rt = case
+    wl = synth.Workload(name="edge", B=2, H=2, grid_h=gh, grid_w=gw, d=d, lm_h=lh, lm_w=lw, k=kk, dtype=dtype,
+                        clusters=4, std=0.5, cluster_map="iid", seed=77 + gh * gw, use_shared=sh, use_routed=rt)
+    inp = synth.generate(wl)
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = (to_dev(x, dtype) for x in (inp.q, inp.k, inp.v))
+    log(f"[edge] {case}")
+    _end_to_end(cfg, inp, q, k, v, [(0, 0), (1, 1)], row_limit=10 ** 9, exact_sets=(dtype == "f32"))
+
+
+def test_staged_gather_equals_in_place_gather():
+    name = "vitb_hr_bf16"
+    cfg = mita.Config.from_workload(_inputs(name).wl)
+    q, k, v = _dev_inputs(name)
+    a = mita.forward(cfg, q, k, v)
+    b = mita.forward(dataclasses.replace(cfg, staged_gather=True), q, k, v)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_forward_is_deterministic():
+    name = "dense_pred_bf16"
+    cfg = mita.Config.from_workload(_inputs(name).wl)
+    q, k, v = _dev_inputs(name)
+    a = mita.forward(cfg, q, k, v)
+    b = mita.forward(cfg, q, k, v)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_timer_records_every_stage():
+    name = "vits_bf16"
+    cfg = mita.Config.from_workload(_inputs(name).wl)
+    q, k, v = _dev_inputs(name)
+    t = mita.Timer(3)
+    o1 = mita.forward(cfg, q, k, v, timer=t)
+    mita.forward(cfg, q, k, v, timer=t)
+    ms = t.read()
+    assert len(ms) == 2 and all(len(x) == mita.NUM_STAGES for x in ms)
+    assert all(x >= 0 for row in ms for x in row) and sum(ms[0]) > 0
+    o2 = mita.forward(cfg, q, k, v)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    t.close()
+
+
+def test_invalid_arguments_launch_nothing():
+    wl = synth.WORKLOADS["vits_bf16"].with_(B=1, H=1)
+    inp = synth.generate(wl)
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = (to_dev(x, "bf16") for x in (inp.q, inp.k, inp.v))
+    o = torch.full_like(q, 7.0)
+    lib = mita.load_library()
+    import ctypes
+    ws = torch.empty(mita.workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    st = mita._stream()
+
+    def call(c, o_=o, ws_=ws, nws=None, q_=q):
+        return lib.mita_forward(ctypes.byref(c.struct()), mita._p(q_), mita._p(k), mita._p(v), mita._p(o_),
+                                mita._p(ws_), ws_.numel() if nws is None else nws, st)
+
+    assert call(dataclasses.replace(cfg, d=96)) == mita.MITA_ERR_UNSUPPORTED
+    assert call(dataclasses.replace(cfg, s=2)) == mita.MITA_ERR_UNSUPPORTED
+    assert call(dataclasses.replace(cfg, k=cfg.N + 1)) == mita.MITA_ERR_INVALID_ARG
+    assert call(dataclasses.replace(cfg, use_shared=0, use_routed=0)) == mita.MITA_ERR_INVALID_ARG
+    assert call(cfg, nws=ws.numel() - 1) == mita.MITA_ERR_WORKSPACE
+    assert call(cfg, o_=q) == mita.MITA_ERR_INVALID_ARG          # output aliases an input
+    assert call(cfg, q_=None) == mita.MITA_ERR_INVALID_ARG
+    torch.cuda.synchronize()
+    assert (o.float() == 7.0).all()
+    assert call(cfg) == mita.MITA_OK
