@@ -8,7 +8,7 @@
 #include <cstdio>
 #include <string>
 
-#include "../../include/mita.h"
+#include "mita.h"
 
 namespace mita {
 
