@@ -60,7 +60,8 @@ inline int check_cfg(const mita_cfg_t *c, std::string *err) {
 
 // Workspace layout of mita_forward (offsets in bytes; 0-sized pieces allowed).
 struct FwdLayout {
-  size_t q_lm, v_lm, scores, partial, idx, kx, vx, expert, perm, offsets, tile_cnt, tile_base, tile_start, total;
+  size_t q_lm, v_lm, scores, partial, idx, kx, vx, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start,
+      total;
 };
 
 inline size_t scores_ws_bytes(const mita_cfg_t &c) {
@@ -68,9 +69,14 @@ inline size_t scores_ws_bytes(const mita_cfg_t &c) {
   const size_t rows = (size_t)BH(c) * score_chunks(c) * c.M;
   return align_up(rows * 2 * sizeof(float)) + align_up(rows * c.d * sizeof(float));
 }
+// Routing scratch: per-tile expert counts, per-tile scatter bases, per-expert
+// totals and the attention work list, in that order.
+inline size_t route_tiles_bytes(const mita_cfg_t &c) {
+  return align_up((size_t)BH(c) * route_tiles(c) * c.M * sizeof(int32_t));
+}
 inline size_t route_ws_bytes(const mita_cfg_t &c) {
-  // per-tile expert counts and per-tile scatter bases
-  return 2 * align_up((size_t)BH(c) * route_tiles(c) * c.M * sizeof(int32_t));
+  return 2 * route_tiles_bytes(c) + align_up((size_t)BH(c) * c.M * sizeof(int32_t)) +
+         align_up((size_t)BH(c) * (c.M + 1) * sizeof(int32_t));
 }
 inline size_t attend_ws_bytes(const mita_cfg_t &c) { return align_up((size_t)BH(c) * (c.M + 1) * sizeof(int32_t)); }
 
@@ -97,6 +103,7 @@ inline FwdLayout forward_layout(const mita_cfg_t &c) {
   L.offsets = take(c.use_routed ? bh * (c.M + 1) * 4 : 0);
   L.tile_cnt = take(c.use_routed ? bh * route_tiles(c) * c.M * 4 : 0);
   L.tile_base = take(c.use_routed ? bh * route_tiles(c) * c.M * 4 : 0);
+  L.counts = take(c.use_routed ? bh * c.M * 4 : 0);
   L.tile_start = take(c.use_routed ? bh * (c.M + 1) * 4 : 0);
   L.total = off;
   return L;

@@ -9,7 +9,11 @@
 namespace mita {
 
 // Landmark pooling (Sec. 3.2; Algorithm 1 AdaptiveAvgPool): q [BH,N,d] -> q_lm [BH,M,d].
-hipError_t launch_pool(const mita_cfg_t &c, const void *q, void *q_lm, hipStream_t st);
+// If zero_counts is not NULL its BH*M entries are set to 0 (routing totals).
+hipError_t launch_pool(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *zero_counts, hipStream_t st);
+
+// Set n int32 entries to 0.
+hipError_t launch_zero(int32_t *p, int64_t n, hipStream_t st);
 
 // Scores S = fl(q_lm . k) * scale (optional) and landmark values (optional):
 // split over key chunks, partials in `partial`, merged into v_lm.
@@ -23,9 +27,11 @@ hipError_t launch_topk(const mita_cfg_t &c, const float *scores, int32_t *idx, h
 hipError_t launch_gather(const mita_cfg_t &c, const void *k, const void *v, const int32_t *idx, void *kx, void *vx,
                          hipStream_t st);
 
-// Routing: expert [BH,N], per-tile counts and bases, offsets [BH,M+1], perm [BH,N].
+// Routing: expert [BH,N], per-tile counts and bases, offsets [BH,M+1], perm [BH,N],
+// attention work list tile_start [BH,M+1]. counts [BH,M] must be zero on entry.
 hipError_t launch_route(const mita_cfg_t &c, const void *q, const void *q_lm, int32_t *expert, int32_t *perm,
-                        int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, hipStream_t st);
+                        int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, int32_t *counts,
+                        int32_t *tile_start, hipStream_t st);
 
 // Attention work list from offsets: tile_start [BH, M+1].
 hipError_t launch_worklist(const mita_cfg_t &c, const int32_t *offsets, int32_t *tile_start, hipStream_t st);

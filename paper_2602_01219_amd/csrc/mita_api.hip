@@ -98,9 +98,10 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
   int32_t *expert = (int32_t *)(w + L.expert), *perm = (int32_t *)(w + L.perm);
   int32_t *offsets = (int32_t *)(w + L.offsets), *tile_cnt = (int32_t *)(w + L.tile_cnt);
   int32_t *tile_base = (int32_t *)(w + L.tile_base), *tile_start = (int32_t *)(w + L.tile_start);
+  int32_t *counts = (int32_t *)(w + L.counts);
 
   TRY(mark(0));
-  TRY(hip_status(launch_pool(*c, q, q_lm, st), "landmarks"));
+  TRY(hip_status(launch_pool(*c, q, q_lm, c->use_routed ? counts : nullptr, st), "landmarks"));
   TRY(mark(1));
   TRY(hip_status(launch_scores(*c, q_lm, k, v, S, v_lm, w + L.partial, st), "scores"));
   TRY(mark(2));
@@ -108,10 +109,9 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
   TRY(mark(3));
   if (staged) TRY(hip_status(launch_gather(*c, k, v, idx, kx, vx, st), "gather"));
   TRY(mark(4));
-  if (c->use_routed) {
-    TRY(hip_status(launch_route(*c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, st), "route"));
-    TRY(hip_status(launch_worklist(*c, offsets, tile_start, st), "worklist"));
-  }
+  if (c->use_routed)
+    TRY(hip_status(launch_route(*c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st),
+                   "route"));
   TRY(mark(5));
   TRY(hip_status(launch_attend(*c, q, q_lm, v_lm, staged ? kx : k, staged ? vx : v, staged ? nullptr : idx, perm,
                                offsets, tile_start, o, st),
@@ -159,7 +159,7 @@ int mita_landmarks(const mita_cfg_t *cfg, const void *q, void *q_lm, mita_stream
   TRY(validate(cfg));
   TRY(need_ptr(q, "q"));
   TRY(need_ptr(q_lm, "q_lm"));
-  return hip_status(launch_pool(*cfg, q, q_lm, (hipStream_t)stream), "landmarks");
+  return hip_status(launch_pool(*cfg, q, q_lm, nullptr, (hipStream_t)stream), "landmarks");
 }
 
 int mita_scores(const mita_cfg_t *cfg, const void *q_lm, const void *k, const void *v, float *scores, void *v_lm,
@@ -210,9 +210,14 @@ int mita_route(const mita_cfg_t *cfg, const void *q, const void *q_lm, int32_t *
   TRY(need_ptr(perm, "perm"));
   TRY(need_ptr(offsets, "offsets"));
   TRY(need_ws(cfg, MITA_WS_ROUTE, ws, ws_bytes));
+  const size_t tb = route_tiles_bytes(*cfg);
   int32_t *tile_cnt = (int32_t *)ws;
-  int32_t *tile_base = (int32_t *)((char *)ws + route_ws_bytes(*cfg) / 2);
-  return hip_status(launch_route(*cfg, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, (hipStream_t)stream),
+  int32_t *tile_base = (int32_t *)((char *)ws + tb);
+  int32_t *counts = (int32_t *)((char *)ws + 2 * tb);
+  int32_t *tile_start = (int32_t *)((char *)ws + 2 * tb + align_up((size_t)BH(*cfg) * cfg->M * sizeof(int32_t)));
+  hipStream_t st = (hipStream_t)stream;
+  TRY(hip_status(launch_zero(counts, BH(*cfg) * cfg->M, st), "route"));
+  return hip_status(launch_route(*cfg, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st),
                     "route");
 }
 

@@ -15,8 +15,9 @@ namespace mita {
 // over the token slots through LDS.
 // ---------------------------------------------------------------------------
 template <typename T, int D>
-__global__ __launch_bounds__(256) void pool_kernel(const T *__restrict__ q, T *__restrict__ q_lm, int N, int gh, int gw,
-                                                   int lh, int lw) {
+__global__ __launch_bounds__(256) void pool_kernel(const T *__restrict__ q, T *__restrict__ q_lm,
+                                                   int32_t *__restrict__ zero_counts, int N, int gh, int gw, int lh,
+                                                   int lw) {
   constexpr int VE = 16 / (int)sizeof(T);
   constexpr int CPT = D / VE;   // chunks per token row
   constexpr int P = 256 / CPT;  // token slots
@@ -28,6 +29,7 @@ __global__ __launch_bounds__(256) void pool_kernel(const T *__restrict__ q, T *_
   const int r0 = (int)(((int64_t)a * gh) / lh), r1 = (int)(((int64_t)(a + 1) * gh + lh - 1) / lh);
   const int c0 = (int)(((int64_t)b * gw) / lw), c1 = (int)(((int64_t)(b + 1) * gw + lw - 1) / lw);
   const int cols = c1 - c0, count = (r1 - r0) * cols;
+  if (zero_counts && threadIdx.x == 0) zero_counts[bh * M + i] = 0;
   const int ch = threadIdx.x % CPT, slot = threadIdx.x / CPT;
   float acc[VE];
 #pragma unroll
@@ -127,23 +129,28 @@ __global__ __launch_bounds__(BLOCK) void scores_kernel(const T *__restrict__ q_l
 }
 
 // Log-sum-exp merge of the per-chunk landmark-value partials (online softmax
-// across chunks). One workgroup of D threads per (b*h, landmark).
+// across chunks, in one pass: the loads do not depend on the running state,
+// so they stay in flight). 256 threads = 256 / D landmarks x D dimensions.
 template <typename T, int D>
-__global__ __launch_bounds__(D) void merge_kernel(const float2 *__restrict__ part_ml, const float *__restrict__ part_o,
-                                                  T *__restrict__ v_lm, int M, int nchunks) {
-  const int lm = blockIdx.x;
+__global__ __launch_bounds__(256) void merge_kernel(const float2 *__restrict__ part_ml, const float *__restrict__ part_o,
+                                                    T *__restrict__ v_lm, int M, int nchunks) {
+  constexpr int LPB = 256 / D;
+  const int lm = blockIdx.x * LPB + threadIdx.x / D, dim = threadIdx.x % D;
   const int64_t bh = blockIdx.y;
-  float mx = -INFINITY;
-  for (int c = 0; c < nchunks; ++c) mx = fmaxf(mx, part_ml[(bh * nchunks + c) * M + lm].x);
-  float L = 0.f, acc = 0.f;
+  if (lm >= M) return;
+  float mx = -INFINITY, L = 0.f, acc = 0.f;
+#pragma unroll 8
   for (int c = 0; c < nchunks; ++c) {
     const int64_t row = (bh * nchunks + c) * M + lm;
     const float2 ml = part_ml[row];
-    const float w = __builtin_amdgcn_exp2f(ml.x - mx);
-    L += ml.y * w;
-    acc += part_o[row * D + threadIdx.x] * w;
+    const float o = part_o[row * D + dim];
+    const float m_new = fmaxf(mx, ml.x);
+    const float a = __builtin_amdgcn_exp2f(mx - m_new), b = __builtin_amdgcn_exp2f(ml.x - m_new);
+    L = L * a + ml.y * b;
+    acc = acc * a + o * b;
+    mx = m_new;
   }
-  v_lm[(bh * M + lm) * D + threadIdx.x] = from_f32<T>(acc / L);
+  v_lm[(bh * M + lm) * D + dim] = from_f32<T>(acc / L);
 }
 
 // ---------------------------------------------------------------------------
@@ -171,16 +178,29 @@ __global__ __launch_bounds__(256) void gather_kernel(const T *__restrict__ k, co
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
-template <typename T, int D> static hipError_t pool_t(const mita_cfg_t &c, const void *q, void *q_lm, hipStream_t st) {
+template <typename T, int D>
+static hipError_t pool_t(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *zc, hipStream_t st) {
   dim3 grid(c.M, (unsigned)BH(c));
-  hipLaunchKernelGGL((pool_kernel<T, D>), grid, dim3(256), 0, st, (const T *)q, (T *)q_lm, c.N, c.grid_h, c.grid_w,
-                     c.lm_h, c.lm_w);
+  hipLaunchKernelGGL((pool_kernel<T, D>), grid, dim3(256), 0, st, (const T *)q, (T *)q_lm, zc, c.N, c.grid_h,
+                     c.grid_w, c.lm_h, c.lm_w);
   return hipGetLastError();
 }
 
-hipError_t launch_pool(const mita_cfg_t &c, const void *q, void *q_lm, hipStream_t st) {
-  if (c.dtype == MITA_F32) return c.d == 64 ? pool_t<float, 64>(c, q, q_lm, st) : pool_t<float, 128>(c, q, q_lm, st);
-  return c.d == 64 ? pool_t<bf16_t, 64>(c, q, q_lm, st) : pool_t<bf16_t, 128>(c, q, q_lm, st);
+hipError_t launch_pool(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *zc, hipStream_t st) {
+  if (c.dtype == MITA_F32)
+    return c.d == 64 ? pool_t<float, 64>(c, q, q_lm, zc, st) : pool_t<float, 128>(c, q, q_lm, zc, st);
+  return c.d == 64 ? pool_t<bf16_t, 64>(c, q, q_lm, zc, st) : pool_t<bf16_t, 128>(c, q, q_lm, zc, st);
+}
+
+__global__ __launch_bounds__(256) void zero_kernel(int32_t *__restrict__ p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+hipError_t launch_zero(int32_t *p, int64_t n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p, n);
+  return hipGetLastError();
 }
 
 template <typename T, int D>
@@ -204,7 +224,9 @@ static hipError_t scores_t(const mita_cfg_t &c, const void *q_lm, const void *k,
     return hipSuccess;
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !v_lm) return e;
-  hipLaunchKernelGGL((merge_kernel<T, D>), dim3(c.M, (unsigned)BH(c)), dim3(D), 0, st, ml, po, (T *)v_lm, c.M, nch);
+  constexpr int LPB = 256 / D;
+  hipLaunchKernelGGL((merge_kernel<T, D>), dim3((c.M + LPB - 1) / LPB, (unsigned)BH(c)), dim3(256), 0, st, ml, po,
+                     (T *)v_lm, c.M, nch);
   return hipGetLastError();
 }
 

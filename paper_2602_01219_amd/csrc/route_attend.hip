@@ -12,12 +12,14 @@ namespace mita {
 // Each wave forms L^T = Q_lm Q^T on MFMA one 16-landmark block at a time and
 // keeps a lane-local running (max, argmax) with strict '>' in increasing
 // landmark order, then merges the four lane groups preferring the lower
-// landmark on equal values. Also counts the tile's queries per expert.
+// landmark on equal values. Also counts the tile's queries per expert and
+// adds them to the per-expert totals (zeroed beforehand).
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 __global__ __launch_bounds__(BLOCK) void route_logits_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
                                                              int32_t *__restrict__ expert,
-                                                             int32_t *__restrict__ tile_cnt, int N, int M,
+                                                             int32_t *__restrict__ tile_cnt,
+                                                             int32_t *__restrict__ counts, int N, int M,
                                                              float scale) {
   extern __shared__ uint32_t cnt[];  // [M]
   const int tile = blockIdx.x, ntiles = gridDim.x;
@@ -75,7 +77,10 @@ __global__ __launch_bounds__(BLOCK) void route_logits_kernel(const T *__restrict
   }
   __syncthreads();
   int32_t *tc = tile_cnt + (bh * ntiles + tile) * (int64_t)M;
-  for (int i = threadIdx.x; i < M; i += BLOCK) tc[i] = (int32_t)cnt[i];
+  for (int i = threadIdx.x; i < M; i += BLOCK) {
+    tc[i] = (int32_t)cnt[i];
+    if (cnt[i]) atomicAdd(&counts[bh * M + i], (int32_t)cnt[i]);  // integer sums: order-independent
+  }
 }
 
 // Block-wide exclusive scan of one value per thread (NT threads); returns the
@@ -98,30 +103,68 @@ template <int NT> __device__ __forceinline__ uint32_t block_exclusive_scan(uint3
   return before + incl - x;
 }
 
-// Per (b, h): expert sizes, offsets = [0, cumsum(counts)] (Algorithm 1 BinCount
-// and CumSum, counting the argmax output), and for every routing tile the
-// position its first query of each expert goes to. 1024 threads, one expert each.
-__global__ __launch_bounds__(1024) void route_scan_kernel(const int32_t *__restrict__ tile_cnt,
-                                                          int32_t *__restrict__ tile_base,
-                                                          int32_t *__restrict__ offsets, int ntiles, int M) {
-  __shared__ uint32_t wsum[16];
-  const int64_t bh = blockIdx.x;
-  const int e = threadIdx.x;
-  const int32_t *tc = tile_cnt + bh * ntiles * (int64_t)M;
-  uint32_t tot = 0;
-  if (e < M)
-    for (int t = 0; t < ntiles; ++t) tot += (uint32_t)tc[(int64_t)t * M + e];
-  uint32_t all;
-  const uint32_t off = block_exclusive_scan<1024>(tot, wsum, &all);
-  if (e < M) {
+// Block-wide sum of one value per thread (256 threads).
+__device__ __forceinline__ uint32_t block_sum256(uint32_t x, uint32_t *wsum) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  x = wave_sum_u32(x);
+  if (lane == 0) wsum[w] = x;
+  __syncthreads();
+  const uint32_t t = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+  __syncthreads();
+  return t;
+}
+
+// One workgroup per (expert e, b*h): offsets[e] = sum of the sizes of experts
+// before e (Algorithm 1 BinCount of the argmax and CumSum), the attention work
+// list tile_start[e] = sum of ceil(size / 64) before e, and, by an exclusive
+// scan over the routing tiles, where each tile's first query of expert e goes.
+__global__ __launch_bounds__(256) void route_scan_kernel(const int32_t *__restrict__ tile_cnt,
+                                                         const int32_t *__restrict__ counts,
+                                                         int32_t *__restrict__ tile_base,
+                                                         int32_t *__restrict__ offsets,
+                                                         int32_t *__restrict__ tile_start, int ntiles, int M,
+                                                         int N) {
+  __shared__ uint32_t wsum[2][4];
+  const int e = blockIdx.x;
+  const int64_t bh = blockIdx.y;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int32_t *cn = counts + bh * M;
+  uint32_t a = 0, t = 0;
+  for (int i = tid; i < e; i += 256) {
+    const uint32_t c = (uint32_t)cn[i];
+    a += c;
+    t += (c + ATT_TQ - 1) / ATT_TQ;
+  }
+  const uint32_t off = block_sum256(a, wsum[0]);
+  const uint32_t ts = block_sum256(t, wsum[1]);
+  if (tid == 0) {
+    const uint32_t mine = (uint32_t)cn[e];
     offsets[bh * (M + 1) + e] = (int32_t)off;
-    if (e == M - 1) offsets[bh * (M + 1) + M] = (int32_t)all;
-    int32_t *tb = tile_base + bh * ntiles * (int64_t)M;
-    uint32_t run = off;
-    for (int t = 0; t < ntiles; ++t) {
-      tb[(int64_t)t * M + e] = (int32_t)run;
-      run += (uint32_t)tc[(int64_t)t * M + e];
+    tile_start[bh * (M + 1) + e] = (int32_t)ts;
+    if (e == M - 1) {
+      offsets[bh * (M + 1) + M] = (int32_t)(off + mine);
+      tile_start[bh * (M + 1) + M] = (int32_t)(ts + (mine + ATT_TQ - 1) / ATT_TQ);
     }
+  }
+  const int32_t *tc = tile_cnt + bh * ntiles * (int64_t)M + e;
+  int32_t *tb = tile_base + bh * ntiles * (int64_t)M + e;
+  uint32_t run = off;
+  int par = 0;
+  for (int t0 = 0; t0 < ntiles; t0 += 256) {
+    const int tt = t0 + tid;
+    const uint32_t c = tt < ntiles ? (uint32_t)tc[(int64_t)tt * M] : 0u;
+    const uint32_t incl = wave_inclusive_scan(c);
+    if (lane == 63) wsum[par][w] = incl;
+    __syncthreads();
+    uint32_t before = run + incl - c, tot = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      before += i < w ? wsum[par][i] : 0u;
+      tot += wsum[par][i];
+    }
+    if (tt < ntiles) tb[(int64_t)tt * M] = (int32_t)before;
+    run += tot;
+    par ^= 1;
   }
 }
 
@@ -288,14 +331,16 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 static hipError_t route_t(const mita_cfg_t &c, const void *q, const void *q_lm, int32_t *expert, int32_t *perm,
-                          int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, hipStream_t st) {
+                          int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, int32_t *counts,
+                          int32_t *tile_start, hipStream_t st) {
   const int nt = route_tiles(c);
   const unsigned bh = (unsigned)BH(c);
   hipLaunchKernelGGL((route_logits_kernel<T, D>), dim3(nt, bh), dim3(BLOCK), c.M * sizeof(uint32_t), st,
-                     (const T *)q, (const T *)q_lm, expert, tile_cnt, c.N, c.M, eff_scale(c));
+                     (const T *)q, (const T *)q_lm, expert, tile_cnt, counts, c.N, c.M, eff_scale(c));
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(route_scan_kernel, dim3(bh), dim3(1024), 0, st, tile_cnt, tile_base, offsets, nt, c.M);
+  hipLaunchKernelGGL(route_scan_kernel, dim3(c.M, bh), dim3(256), 0, st, tile_cnt, counts, tile_base, offsets,
+                     tile_start, nt, c.M, c.N);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   int ebits = 0;
   while ((1 << ebits) < c.M) ++ebits;
@@ -305,12 +350,13 @@ static hipError_t route_t(const mita_cfg_t &c, const void *q, const void *q_lm, 
 }
 
 hipError_t launch_route(const mita_cfg_t &c, const void *q, const void *q_lm, int32_t *expert, int32_t *perm,
-                        int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, hipStream_t st) {
+                        int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, int32_t *counts,
+                        int32_t *tile_start, hipStream_t st) {
   if (c.dtype == MITA_F32)
-    return c.d == 64 ? route_t<float, 64>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, st)
-                     : route_t<float, 128>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, st);
-  return c.d == 64 ? route_t<bf16_t, 64>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, st)
-                   : route_t<bf16_t, 128>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, st);
+    return c.d == 64 ? route_t<float, 64>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st)
+                     : route_t<float, 128>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st);
+  return c.d == 64 ? route_t<bf16_t, 64>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st)
+                   : route_t<bf16_t, 128>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st);
 }
 
 hipError_t launch_worklist(const mita_cfg_t &c, const int32_t *offsets, int32_t *tile_start, hipStream_t st) {

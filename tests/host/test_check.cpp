@@ -50,7 +50,7 @@ int main() {
   mita_cfg_t c = base();
   mita::FwdLayout L = mita::forward_layout(c);
   const size_t offs[] = {L.q_lm, L.v_lm, L.scores, L.partial, L.idx, L.kx, L.vx, L.expert,
-                         L.perm, L.offsets, L.tile_cnt, L.tile_base, L.tile_start, L.total};
+                         L.perm, L.offsets, L.tile_cnt, L.tile_base, L.counts, L.tile_start, L.total};
   for (size_t i = 0; i + 1 < sizeof offs / sizeof offs[0]; ++i) {
     assert(offs[i] % 256 == 0);
     assert(offs[i] <= offs[i + 1]);
