@@ -22,6 +22,12 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_floa
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
+typedef __attribute__((ext_vector_type(2))) float f32x2;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+// Two values rounded to bf16 in one instruction: lo = a, hi = b.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, bf16x2));
+}
 
 // ---------------------------------------------------------------------------
 // Operand fragments.  A 16x16 MFMA tile with a 32-long reduction step: lane l
@@ -46,11 +52,11 @@ template <> struct Frag<bf16_t> {
     uint2 b = *reinterpret_cast<const uint2 *>(p1);
     v = make_uint4(a.x, a.y, b.x, b.y);
   }
-  // from 8 fp32 values (rounded to bf16)
+  // from 8 fp32 values (rounded to bf16, two per v_cvt_pk_bf16_f32)
   __device__ __forceinline__ void from_f32(const float *x) {
     uint32_t w[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) w[i] = uint32_t(f32_to_bf16(x[2 * i])) | (uint32_t(f32_to_bf16(x[2 * i + 1])) << 16);
+    for (int i = 0; i < 4; ++i) w[i] = pack_bf16x2(x[2 * i], x[2 * i + 1]);
     v = make_uint4(w[0], w[1], w[2], w[3]);
   }
 };

@@ -21,7 +21,9 @@ constexpr float LOG2E = 1.4426950408889634f;
 template <typename T, int D> struct TileDims {
   static constexpr int VE = 16 / (int)sizeof(T);  // elements per 16-byte chunk
   static constexpr int KSTR = D + VE;             // padded K row (elements)
-  static constexpr int VSTR = TK + VE;            // padded V^T row (elements)
+  // padded V^T row: 136 bytes (bf16) / 272 bytes (fp32) keep the 8 / 16-byte
+  // fragment reads aligned and spread the transposing writes over the banks
+  static constexpr int VSTR = TK + 4;
   static constexpr int K_ELEMS = TK * KSTR;
   static constexpr int V_ELEMS = D * VSTR;
 };
@@ -85,39 +87,46 @@ template <int D> struct Online {
 };
 
 // Online-softmax update with the tile's scores (acc, unscaled dot products) and
-// O^T += V^T P^T. Keys kb*16 + 4g + r >= nvalid are masked out. sl2 = scale * log2(e).
-// The tile must hold at least one valid key.
-template <typename T, int D>
+// O^T += V^T P^T. sl2 = scale * log2(e); the running max is kept in scaled
+// log2 units, the tile max is taken on the raw dots (a positive scale keeps
+// the order) and p = exp2(dot * sl2 - m) is one FMA. With MASKED, keys
+// kb*16 + 4g + r >= nvalid are excluded (only the last tile of a key range is
+// partial). The tile must hold at least one valid key.
+template <typename T, int D, bool MASKED = true>
 __device__ __forceinline__ void tile_softmax_pv(Online<D> &st, const f32x4 (&acc)[4], const T *__restrict__ Vt, int nvalid,
                                                 float sl2) {
   using TD = TileDims<T, D>;
   const int lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
-  float t[4][4];
   float mx = -INFINITY;
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int key = kb * 16 + 4 * g + r;
-      t[kb][r] = key < nvalid ? acc[kb][r] * sl2 : -INFINITY;
-      mx = fmaxf(mx, t[kb][r]);
+      const bool ok = !MASKED || kb * 16 + 4 * g + r < nvalid;
+      mx = fmaxf(mx, ok ? acc[kb][r] : -INFINITY);
     }
   mx = fmaxf(mx, __shfl_xor(mx, 16));
   mx = fmaxf(mx, __shfl_xor(mx, 32));
-  const float m_new = fmaxf(st.m, mx);
+  const float m_new = fmaxf(st.m, mx * sl2);
   const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
   st.m = m_new;
+  float t[4][4];
   float ls = 0.f;
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      t[kb][r] = __builtin_amdgcn_exp2f(t[kb][r] - m_new);
-      ls += t[kb][r];
+      float e = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[kb][r], sl2, -m_new));
+      if (MASKED && kb * 16 + 4 * g + r >= nvalid) e = 0.f;
+      t[kb][r] = e;
+      ls += e;
     }
   st.l = st.l * alpha + ls;
+  // rescale only when some column's max moved (alpha == 1 exactly otherwise)
+  if (__ballot(alpha != 1.0f)) {
 #pragma unroll
-  for (int i = 0; i < D / 16; ++i) st.o[i] *= alpha;
+    for (int i = 0; i < D / 16; ++i) st.o[i] *= alpha;
+  }
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     // reduction slice of group g: keys 32j + 4g + (0..3) and 32j + 16 + 4g + (0..3)
@@ -132,6 +141,90 @@ __device__ __forceinline__ void tile_softmax_pv(Online<D> &st, const f32x4 (&acc
       a.load2x4(row, row + 16);
       st.o[db] = mma(a, b, st.o[db]);
     }
+  }
+}
+
+// Register-staged copy of one 64-row K/V tile (software pipelining: the
+// global loads of the next tile are issued before the current tile is
+// processed, the LDS stores after). Thread t owns rows CH*(t / CPR) + j,
+// j < CH, at 16-byte chunk t % CPR, so the transposing V store can write the
+// CH consecutive keys of one dimension as one packed word.
+template <typename T, int D> struct TileRegs {
+  static constexpr int VE = 16 / (int)sizeof(T);
+  static constexpr int CPR = D / VE;           // 16-byte chunks per row
+  static constexpr int CH = TK * CPR / BLOCK;  // rows per thread
+  uint4 k[CH], v[CH];
+  __device__ __forceinline__ int row0() const { return CH * ((int)threadIdx.x / CPR); }
+  __device__ __forceinline__ int chunk() const { return (int)threadIdx.x % CPR; }
+  // row r of the tile is source row (rowidx ? rowidx[r] : r); rows >= nrows load zeros
+  __device__ __forceinline__ void load(const T *__restrict__ kb, const T *__restrict__ vb, const int32_t *rowidx,
+                                       int nrows) {
+    const int r0 = row0(), ch = chunk();
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+      const int r = r0 + j;
+      k[j] = make_uint4(0, 0, 0, 0);
+      v[j] = make_uint4(0, 0, 0, 0);
+      if (r < nrows) {
+        const int64_t src = rowidx ? (int64_t)rowidx[r] : (int64_t)r;
+        k[j] = *reinterpret_cast<const uint4 *>(kb + src * D + ch * VE);
+        v[j] = *reinterpret_cast<const uint4 *>(vb + src * D + ch * VE);
+      }
+    }
+  }
+  __device__ __forceinline__ void store(T *__restrict__ Ks, T *__restrict__ Vt) const {
+    using TD = TileDims<T, D>;
+    const int r0 = row0(), ch = chunk();
+#pragma unroll
+    for (int j = 0; j < CH; ++j) *reinterpret_cast<uint4 *>(Ks + (r0 + j) * TD::KSTR + ch * VE) = k[j];
+    store_vt(Vt + (ch * VE) * TD::VSTR + r0);
+  }
+  // V^T: dimension ch*VE + e, keys r0 .. r0+CH-1
+  __device__ __forceinline__ void store_vt(T *__restrict__ dst) const;
+};
+
+template <> __device__ __forceinline__ void TileRegs<bf16_t, 64>::store_vt(bf16_t *__restrict__ dst) const {
+  // CH = 2: keys r0, r0+1 of dims 2m, 2m+1 from the two rows' words m
+  using TD = TileDims<bf16_t, 64>;
+  const uint32_t r0w[4] = {v[0].x, v[0].y, v[0].z, v[0].w}, r1w[4] = {v[1].x, v[1].y, v[1].z, v[1].w};
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    *reinterpret_cast<uint32_t *>(dst + (2 * m) * TD::VSTR) = __builtin_amdgcn_perm(r1w[m], r0w[m], 0x05040100u);
+    *reinterpret_cast<uint32_t *>(dst + (2 * m + 1) * TD::VSTR) = __builtin_amdgcn_perm(r1w[m], r0w[m], 0x07060302u);
+  }
+}
+template <> __device__ __forceinline__ void TileRegs<bf16_t, 128>::store_vt(bf16_t *__restrict__ dst) const {
+  // CH = 4: keys r0 .. r0+3 of dims 2m, 2m+1 as one 8-byte word each
+  using TD = TileDims<bf16_t, 128>;
+  const uint32_t w0[4] = {v[0].x, v[0].y, v[0].z, v[0].w}, w1[4] = {v[1].x, v[1].y, v[1].z, v[1].w};
+  const uint32_t w2[4] = {v[2].x, v[2].y, v[2].z, v[2].w}, w3[4] = {v[3].x, v[3].y, v[3].z, v[3].w};
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    *reinterpret_cast<uint2 *>(dst + (2 * m) * TD::VSTR) =
+        make_uint2(__builtin_amdgcn_perm(w1[m], w0[m], 0x05040100u), __builtin_amdgcn_perm(w3[m], w2[m], 0x05040100u));
+    *reinterpret_cast<uint2 *>(dst + (2 * m + 1) * TD::VSTR) =
+        make_uint2(__builtin_amdgcn_perm(w1[m], w0[m], 0x07060302u), __builtin_amdgcn_perm(w3[m], w2[m], 0x07060302u));
+  }
+}
+template <> __device__ __forceinline__ void TileRegs<float, 64>::store_vt(float *__restrict__ dst) const {
+  // CH = 4: keys r0 .. r0+3 of each of the 4 dims as one 16-byte word
+  using TD = TileDims<float, 64>;
+  const float *r[4] = {reinterpret_cast<const float *>(&v[0]), reinterpret_cast<const float *>(&v[1]),
+                       reinterpret_cast<const float *>(&v[2]), reinterpret_cast<const float *>(&v[3])};
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    *reinterpret_cast<float4 *>(dst + e * TD::VSTR) = make_float4(r[0][e], r[1][e], r[2][e], r[3][e]);
+}
+template <> __device__ __forceinline__ void TileRegs<float, 128>::store_vt(float *__restrict__ dst) const {
+  // CH = 8: keys r0 .. r0+7 of each of the 4 dims as two 16-byte words
+  using TD = TileDims<float, 128>;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    float x[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = reinterpret_cast<const float *>(&v[j])[e];
+    *reinterpret_cast<float4 *>(dst + e * TD::VSTR) = make_float4(x[0], x[1], x[2], x[3]);
+    *reinterpret_cast<float4 *>(dst + e * TD::VSTR + 4) = make_float4(x[4], x[5], x[6], x[7]);
   }
 }
 

@@ -218,8 +218,13 @@ __global__ __launch_bounds__(1024) void worklist_kernel(const int32_t *__restric
 // = 64 queries of one expert (4 waves x 16), taken from the routing work list
 // (Algorithm 1's varlen grouping); outputs are scattered back to token order.
 // With ROUTED, routed keys come from the expert tiles, or straight from the
-// K/V rows listed in idx (FUSED: the gather of Eq. gather done in place).
+// K/V rows listed in idx (FUSED: the gather of Eq. gather done in place; the
+// expert's index list is staged in LDS first when it fits).
+// Key tiles are double-buffered in LDS: the next tile's global loads are in
+// flight while the current one is multiplied, one barrier per tile.
 // ---------------------------------------------------------------------------
+constexpr int IDX_LDS = 1024;  // expert index lists up to this length are staged in LDS
+
 template <typename T, int D, bool SHARED, bool ROUTED, bool FUSED>
 __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
                                                        const T *__restrict__ v_lm, const T *__restrict__ rk,
@@ -229,10 +234,11 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
                                                        const int32_t *__restrict__ tile_start, T *__restrict__ o,
                                                        int N, int M, int k, float scale) {
   using TD = TileDims<T, D>;
-  __shared__ __align__(16) T Ks[TD::K_ELEMS];
-  __shared__ __align__(16) T Vt[TD::V_ELEMS];
-  const int64_t bh = blockIdx.y;
+  __shared__ __align__(16) T Ks[2][TD::K_ELEMS];
+  __shared__ __align__(16) T Vt[2][TD::V_ELEMS];
+  __shared__ int32_t sidx[FUSED ? IDX_LDS : 1];
   const int t = blockIdx.x;
+  const int64_t bh = blockIdx.y;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
 
   int e = 0, q_begin, q_end;
@@ -255,10 +261,47 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
     q_begin = t * ATT_TQ;
     q_end = min(N, q_begin + ATT_TQ);
   }
+
+  // key tiles: shared ones first, then routed ones
+  const int nA = SHARED ? (M + TK - 1) / TK : 0;
+  const int nB = ROUTED ? (k + TK - 1) / TK : 0;
+  const int ntile = nA + nB;
+  const int32_t *gidx = FUSED ? idx + (bh * M + e) * (int64_t)k : nullptr;
+  const bool idx_in_lds = FUSED && k <= IDX_LDS;
+  if (idx_in_lds) {
+    for (int i = threadIdx.x; i < k; i += BLOCK) sidx[i] = gidx[i];
+    __syncthreads();
+  }
+  // source of key tile i: K/V row bases, optional row list, valid rows
+  const T *kb_i, *vb_i;
+  const int32_t *ri_i;
+  int nr_i;
+  auto tile_src = [&](int i) {
+    if (SHARED && i < nA) {
+      const int64_t off = (bh * M + (int64_t)i * TK) * D;
+      kb_i = q_lm + off;
+      vb_i = v_lm + off;
+      ri_i = nullptr;
+      nr_i = min(TK, M - i * TK);
+    } else {
+      const int u = i - nA;
+      nr_i = min(TK, k - u * TK);
+      if (FUSED) {
+        kb_i = rk + bh * (int64_t)N * D;
+        vb_i = rv + bh * (int64_t)N * D;
+        ri_i = idx_in_lds ? sidx + u * TK : gidx + u * TK;
+      } else {
+        const int64_t off = ((bh * M + e) * (int64_t)k + (int64_t)u * TK) * D;
+        kb_i = rk + off;
+        vb_i = rv + off;
+        ri_i = nullptr;
+      }
+    }
+  };
+
   const int qi = q_begin + w * 16 + p;
   const bool qvalid = qi < q_end;
   const int token = qvalid ? (ROUTED ? perm[bh * N + qi] : qi) : 0;
-
   Frag<T> qf[D / 32];
 #pragma unroll
   for (int ks = 0; ks < D / 32; ++ks) {
@@ -271,43 +314,28 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
   st.init();
   const float sl2 = scale * LOG2E;
 
-  if (SHARED) {
-    const T *kb_ = q_lm + bh * (int64_t)M * D;
-    const T *vb_ = v_lm + bh * (int64_t)M * D;
-    for (int k0 = 0; k0 < M; k0 += TK) {
-      const int nvalid = min(TK, M - k0);
-      __syncthreads();
-      load_kv_tile<T, D>(Ks, Vt, kb_ + (int64_t)k0 * D, vb_ + (int64_t)k0 * D, nullptr, nvalid);
-      __syncthreads();
-      f32x4 acc[4];
-      tile_scores<T, D>(acc, Ks, qf);
-      tile_softmax_pv<T, D>(st, acc, Vt, nvalid, sl2);
+  TileRegs<T, D> R;
+  tile_src(0);
+  R.load(kb_i, vb_i, ri_i, nr_i);
+  R.store(Ks[0], Vt[0]);
+  __syncthreads();
+  int nvalid = nr_i;
+  for (int i = 0; i < ntile; ++i) {
+    const int buf = i & 1;
+    const int nv = nvalid;
+    if (i + 1 < ntile) {
+      tile_src(i + 1);
+      R.load(kb_i, vb_i, ri_i, nr_i);
+      nvalid = nr_i;
     }
-  }
-  if (ROUTED) {
-    const T *kb_;
-    const T *vb_;
-    const int32_t *ib = nullptr;
-    if (FUSED) {
-      kb_ = rk + bh * (int64_t)N * D;
-      vb_ = rv + bh * (int64_t)N * D;
-      ib = idx + (bh * M + e) * (int64_t)k;
-    } else {
-      kb_ = rk + (bh * M + e) * (int64_t)k * D;
-      vb_ = rv + (bh * M + e) * (int64_t)k * D;
-    }
-    for (int k0 = 0; k0 < k; k0 += TK) {
-      const int nvalid = min(TK, k - k0);
-      __syncthreads();
-      if (FUSED)
-        load_kv_tile<T, D>(Ks, Vt, kb_, vb_, ib + k0, nvalid);
-      else
-        load_kv_tile<T, D>(Ks, Vt, kb_ + (int64_t)k0 * D, vb_ + (int64_t)k0 * D, nullptr, nvalid);
-      __syncthreads();
-      f32x4 acc[4];
-      tile_scores<T, D>(acc, Ks, qf);
-      tile_softmax_pv<T, D>(st, acc, Vt, nvalid, sl2);
-    }
+    f32x4 acc[4];
+    tile_scores<T, D>(acc, Ks[buf], qf);
+    if (nv == TK)
+      tile_softmax_pv<T, D, false>(st, acc, Vt[buf], TK, sl2);
+    else
+      tile_softmax_pv<T, D, true>(st, acc, Vt[buf], nv, sl2);
+    if (i + 1 < ntile) R.store(Ks[buf ^ 1], Vt[buf ^ 1]);
+    __syncthreads();
   }
   const float l = column_sum(st.l);
   if (!qvalid) return;
