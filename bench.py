@@ -44,18 +44,20 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def stage_work(wl, staged: bool):
+def stage_work(wl, staged: bool, fused: bool):
     """Algorithmic work per stage launch: (bound, bytes, flops).
 
     bytes: what the stage must read and write at least (inputs once, outputs
-    once); flops: its multiply-adds x 2 on the MFMA path."""
+    once); flops: its multiply-adds x 2 on the MFMA path. With the fused
+    selection the score matrix is neither written nor read back."""
     e = 4 if wl.dtype == "f32" else 2
     BH, N, d, M, k = wl.BH, wl.N, wl.d, wl.M, wl.k
     sh, rt = wl.use_shared, wl.use_routed
     lm = ("hbm", BH * N * d * e + BH * M * d * e, 0)
-    sc_bytes = BH * N * d * e * (1 + sh) + (4 * BH * M * N if rt else 0) + BH * M * d * e * (1 + sh)
+    s_bytes = 4 * BH * M * N if (rt and not fused) else 0
+    sc_bytes = BH * N * d * e * (1 + sh) + s_bytes + BH * M * d * e * (1 + sh)
     sc = ("hbm", sc_bytes, 2 * M * N * d * BH * (1 + sh))
-    tk = ("hbm", 4 * BH * M * N + 4 * BH * M * k, 0) if rt else ("hbm", 0, 0)
+    tk = ("hbm", s_bytes + 4 * BH * M * k, 0) if rt else ("hbm", 0, 0)
     ga = ("hbm", BH * M * k * (4 + 4 * d * e), 0) if (rt and staged) else ("hbm", 0, 0)
     ro = ("mfma", BH * N * d * e + BH * M * d * e + 4 * 3 * BH * N, 2 * N * M * d * BH) if rt else ("hbm", 0, 0)
     keys = M * sh + k * rt
@@ -106,6 +108,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=None)
     ap.add_argument("--staged-gather", action="store_true", help="materialise expert tiles (flag path)")
+    ap.add_argument("--full-scores", action="store_true",
+                    help="store the score matrix and select from it (flag path) instead of the fused selection")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -135,7 +139,8 @@ def main():
         return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda()
 
     q, k, v = dev(inp.q), dev(inp.k), dev(inp.v)
-    cfg = mita.Config.from_workload(wl, staged_gather=a.staged_gather)
+    cfg = mita.Config.from_workload(wl, staged_gather=a.staged_gather, full_scores=a.full_scores)
+    fused = (not a.full_scores) and bool(wl.use_routed) and (wl.N <= 2048 or 4 * wl.k <= 4096)
     o = torch.empty_like(q)
     ws = torch.empty(mita.workspace_size(cfg), dtype=torch.uint8, device="cuda")
     eprint(f"[bench] workspace {ws.numel() / 2**20:.1f} MiB")
@@ -161,7 +166,7 @@ def main():
     ms_per_step = wall * 1e3 / a.steps
     value = wl.tokens * a.steps / wall
     stage_ms = {s: sum(c[i] for c in per_call) / len(per_call) for i, s in enumerate(mita.STAGES)}
-    work = stage_work(wl, a.staged_gather)
+    work = stage_work(wl, a.staged_gather, fused)
     eprint(f"[bench] {ms_per_step:.3f} ms/step, {value / 1e6:.2f} M tokens/s")
     for s in mita.STAGES:
         bound, by, fl = work[s]
@@ -203,7 +208,8 @@ def main():
         "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": name, "B": wl.B, "H": wl.H, "N": wl.N, "d": wl.d, "M": wl.M, "k": wl.k,
                    "grid": [wl.grid_h, wl.grid_w], "use_shared": wl.use_shared, "use_routed": wl.use_routed,
-                   "gather": "staged" if a.staged_gather else "in-place", "parallelism": "none (1 GPU)"},
+                   "gather": "staged" if a.staged_gather else "in-place",
+                   "select": "fused" if fused else "full-scores", "parallelism": "none (1 GPU)"},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "stages_us": {s: round(stage_ms[s] * 1e3, 2) for s in mita.STAGES},

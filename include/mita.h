@@ -33,7 +33,8 @@
  *    enqueued; on error nothing is launched and a status != MITA_OK is
  *    returned, with details from mita_last_error(). No exception crosses the
  *    ABI. NaN inputs are a caller error: results are then unspecified (but
- *    every kernel still stays in bounds and terminates).
+ *    every kernel still stays in bounds and terminates); the top-k order
+ *    ranks a NaN score as -inf.
  *  - Workspace. Entry points that take (ws, ws_bytes) need at least
  *    mita_workspace_size(cfg, which) bytes of device memory there, 256-byte
  *    aligned; its contents on entry do not matter. Calls sharing one
@@ -64,8 +65,11 @@ extern "C" {
 #define MITA_FLAG_STAGED_GATHER 0x1u  /* mita_forward: materialise the expert tiles (Eq. gather) and
                                          attend over them, instead of reading the selected K/V rows
                                          in place inside the attention kernel. Same results. */
+#define MITA_FLAG_FULL_SCORES 0x2u    /* mita_forward: store the whole score matrix S and select the
+                                         top-k sets from it (the mita_scores + mita_topk path), instead
+                                         of selecting inside the score pass. Same results. */
 
-/* Largest sequence length the top-k kernel accepts (one workgroup keeps a whole score row on chip). */
+/* Largest sequence length the library accepts. */
 #define MITA_MAX_N 65536
 
 typedef void *mita_stream_t; /* a hipStream_t */
@@ -110,9 +114,25 @@ const char *mita_last_error(void);
  * The whole forward (Algorithm 1 with s = 1; output Eq. mita).
  *   q, k, v : [B, H, N, d] inputs;  o : [B, H, N, d] output (must not overlap q, k, v).
  *   ws      : >= mita_workspace_size(cfg, MITA_WS_FORWARD) bytes.
+ * The top-k sets are those mita_topk computes from mita_scores' S (bit for
+ * bit), but S is normally not stored: a pivot estimated from a sample of
+ * each score row bounds the row's top-k from below, the score pass lists
+ * only the scores above it, and the exact selection runs on that list. A row
+ * whose list turns out too short or too long is recomputed in full and
+ * selected exactly (see mita_forward_fallbacks). Without MITA_FLAG_FULL_SCORES
+ * this applies when N <= 2048 or k <= 1024.
  */
 int mita_forward(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, void *o,
                  void *ws, size_t ws_bytes, mita_stream_t stream);
+
+/*
+ * Diagnostic: the number of landmark rows whose top-k selection in the last
+ * mita_forward on workspace ws fell back to recomputing the full score row
+ * (0 when that forward stored the whole score matrix). Waits for `stream`.
+ *   count : host pointer, output.
+ */
+int mita_forward_fallbacks(const mita_cfg_t *cfg, const void *ws, size_t ws_bytes, int64_t *count,
+                           mita_stream_t stream);
 
 /*
  * Landmark queries (Sec. 3.2: average pooling over uniformly spaced windows;

@@ -181,5 +181,29 @@ __device__ __forceinline__ float key_to_float(uint32_t k) {
   uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
   return __uint_as_float(u);
 }
+// Key of a score for the top-k order: NaN ranks as -inf, -0 as +0. Every
+// key of a canonical score is >= ordered_key(-inf) = 0x007fffff, so 0 never
+// occurs and can mark an empty slot.
+__device__ __forceinline__ uint32_t score_key(float x) { return ordered_key(x != x ? -INFINITY : x); }
+
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t y = ((uint64_t)(uint32_t)__shfl_xor((int)(x >> 32), o) << 32) | (uint32_t)__shfl_xor((int)x, o);
+    x = y < x ? y : x;
+  }
+  return x;
+}
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t y = ((uint64_t)(uint32_t)__shfl_xor((int)(x >> 32), o) << 32) | (uint32_t)__shfl_xor((int)x, o);
+    x = y > x ? y : x;
+  }
+  return x;
+}
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t x, int src) {
+  return ((uint64_t)(uint32_t)__shfl((int)(x >> 32), src) << 32) | (uint32_t)__shfl((int)x, src);
+}
 
 }  // namespace mita

@@ -16,6 +16,10 @@ constexpr size_t WS_ALIGN = 256;
 constexpr int ATT_TQ = 64;     // queries per attention workgroup
 constexpr int ROUTE_TQ = 64;   // queries per routing tile (one wave)
 constexpr int SCORE_NC = 512;  // keys per score/landmark-value workgroup chunk
+// Top-k selection fused with the score pass of the forward.
+constexpr int SEL_NS = 2048;   // sampled keys per landmark row (pivot estimate)
+constexpr int SEL_CAP = 4096;  // most candidates the exact selection of one row takes
+constexpr int SAMPLE_NC = 64;  // sampled keys per sample-kernel workgroup
 
 inline size_t align_up(size_t x) { return (x + WS_ALIGN - 1) / WS_ALIGN * WS_ALIGN; }
 inline size_t elem_bytes(const mita_cfg_t &c) { return c.dtype == MITA_F32 ? 4 : 2; }
@@ -23,6 +27,39 @@ inline int64_t BH(const mita_cfg_t &c) { return (int64_t)c.B * c.H; }
 inline int score_chunks(const mita_cfg_t &c) { return (c.N + SCORE_NC - 1) / SCORE_NC; }
 inline int route_tiles(const mita_cfg_t &c) { return (c.N + ROUTE_TQ - 1) / ROUTE_TQ; }
 inline float eff_scale(const mita_cfg_t &c) { return c.scale != 0.f ? c.scale : 1.0f / std::sqrt((float)c.d); }
+
+inline int sel_ns(const mita_cfg_t &c) { return c.N < SEL_NS ? c.N : SEL_NS; }
+// Does the forward select the top-k sets inside the score pass? Rows whose
+// sample covers the whole row always fit their list; otherwise the expected
+// list length, at most k + 5 sqrt(32 k) + 64 for N / ns <= 32, must stay well
+// inside SEL_CAP, which k <= SEL_CAP / 4 ensures.
+inline bool fused_select(const mita_cfg_t &c) {
+  return c.use_routed && !(c.flags & MITA_FLAG_FULL_SCORES) && (c.N <= SEL_NS || 4 * (int64_t)c.k <= SEL_CAP);
+}
+// Rank r of the pivot among the ns sampled scores of a row: the pivot is the
+// r-th largest sample score. With the sample equal to the row, r = k exactly;
+// otherwise r is the expected rank of the k-th token, k ns / N, plus five
+// binomial standard deviations (and one), so that at least k tokens of the
+// row score >= pivot except with negligible probability.
+inline int sel_rank(const mita_cfg_t &c) {
+  const int ns = sel_ns(c);
+  if (ns == c.N) return c.k;
+  const double f = (double)c.k * ns / c.N;
+  const double sd = std::sqrt(f * (1.0 - (double)c.k / c.N));
+  const int r = (int)std::ceil(f + 5.0 * sd) + 1;
+  return r < ns ? r : ns;
+}
+// Candidates one row may list before it falls back: a power of two in
+// [1024, SEL_CAP] above the count expected at the pivot rank plus six
+// standard deviations (the whole row when it is shorter).
+inline int sel_cap(const mita_cfg_t &c) {
+  const int ns = sel_ns(c);
+  const double r = sel_rank(c);
+  const double bound = ns == c.N ? c.N : (r + 6.0 * std::sqrt(r)) * ((double)c.N / ns);
+  int cap = 1024;
+  while (cap < SEL_CAP && cap < bound) cap *= 2;
+  return c.N < cap ? c.N : cap;
+}
 
 // Validate a configuration. On failure, writes a message into err.
 inline int check_cfg(const mita_cfg_t *c, std::string *err) {
@@ -52,7 +89,8 @@ inline int check_cfg(const mita_cfg_t *c, std::string *err) {
     return fail(MITA_ERR_UNSUPPORTED, buf);
   }
   if (!(c->scale >= 0.f) || std::isinf(c->scale)) return fail(MITA_ERR_INVALID_ARG, "scale must be finite and >= 0");
-  if (c->flags & ~(uint32_t)MITA_FLAG_STAGED_GATHER) return fail(MITA_ERR_INVALID_ARG, "unknown flag bits");
+  if (c->flags & ~(uint32_t)(MITA_FLAG_STAGED_GATHER | MITA_FLAG_FULL_SCORES))
+    return fail(MITA_ERR_INVALID_ARG, "unknown flag bits");
   // Every index/offset the kernels form fits in 64-bit; int32 outputs need N and M*k in range.
   if ((int64_t)c->M * c->k > INT32_MAX) return fail(MITA_ERR_UNSUPPORTED, "M * k too large");
   return MITA_OK;
@@ -61,7 +99,7 @@ inline int check_cfg(const mita_cfg_t *c, std::string *err) {
 // Workspace layout of mita_forward (offsets in bytes; 0-sized pieces allowed).
 struct FwdLayout {
   size_t q_lm, v_lm, scores, partial, idx, kx, vx, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start,
-      total;
+      samp, plo, ccnt, cand, fail, total;
 };
 
 inline size_t scores_ws_bytes(const mita_cfg_t &c) {
@@ -105,6 +143,15 @@ inline FwdLayout forward_layout(const mita_cfg_t &c) {
   L.tile_base = take(c.use_routed ? bh * route_tiles(c) * c.M * 4 : 0);
   L.counts = take(c.use_routed ? bh * c.M * 4 : 0);
   L.tile_start = take(c.use_routed ? bh * (c.M + 1) * 4 : 0);
+  // fused selection: sampled score keys, pivots, candidate counts and lists,
+  // then the fallback counter followed by the fallback row list
+  const bool fs = fused_select(c);
+  L.samp = take(fs ? bh * c.M * (size_t)sel_ns(c) * 4 : 0);
+  L.plo = take(fs ? bh * c.M * 4 : 0);
+  // per (row, key chunk): candidate count and a list region of SCORE_NC entries
+  L.ccnt = take(fs ? bh * c.M * (size_t)score_chunks(c) * 4 : 0);
+  L.cand = take(fs ? bh * c.M * (size_t)score_chunks(c) * SCORE_NC * 8 : 0);
+  L.fail = take(fs ? (bh * c.M + 1) * 4 : 0);
   L.total = off;
   return L;
 }

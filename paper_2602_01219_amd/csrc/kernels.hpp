@@ -15,13 +15,43 @@ hipError_t launch_pool(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *
 // Set n int32 entries to 0.
 hipError_t launch_zero(int32_t *p, int64_t n, hipStream_t st);
 
+// Buffers of the top-k selection fused with the score pass (rows = BH*M).
+struct SelectBufs {
+  uint32_t *samp;       // [rows, ns] ordered keys of the sampled scores
+  uint32_t *plo;        // [rows] pivot keys
+  uint32_t *ccnt;       // [rows] candidates found (may exceed cap)
+  uint2 *cand;          // [rows, cap] (key, token index) candidate lists
+  uint32_t *fail_cnt;   // rows that fall back to the full score row
+  int32_t *fail_list;   // [rows] their row numbers
+  int ns, cap, rank;
+};
+
 // Scores S = fl(q_lm . k) * scale (optional) and landmark values (optional):
-// split over key chunks, partials in `partial`, merged into v_lm.
+// split over key chunks, partials in `partial`, merged into v_lm. With sel,
+// the candidates of the fused selection are listed instead of storing S
+// (launch_select_pivots must have run).
 hipError_t launch_scores(const mita_cfg_t &c, const void *q_lm, const void *k, const void *v, float *scores,
-                         void *v_lm, void *partial, hipStream_t st);
+                         void *v_lm, void *partial, const SelectBufs *sel, hipStream_t st);
+
+// Fused selection, before the score pass: sampled scores, per-row pivots;
+// zeroes the candidate and fallback counters.
+hipError_t launch_select_pivots(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sel,
+                                hipStream_t st);
+
+// Fused selection, after the score pass: exact top-k from the candidate
+// lists into idx; rows whose list is unusable get their score row recomputed
+// into S (same arithmetic as the score pass) and the exact top-k of it.
+hipError_t launch_select_finish(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sel,
+                                float *S, int32_t *idx, hipStream_t st);
+
+// Score rows of the listed landmark rows only (fallback of the fused selection).
+hipError_t launch_scores_rows(const mita_cfg_t &c, const void *q_lm, const void *k, float *S,
+                              const uint32_t *nrows, const int32_t *rows, hipStream_t st);
 
 // Exact per-row top-k of fp32 scores [rows, N] -> ascending int32 indices [rows, k].
-hipError_t launch_topk(const mita_cfg_t &c, const float *scores, int32_t *idx, hipStream_t st);
+// With nrows/rows != NULL only the *nrows rows listed in rows are processed.
+hipError_t launch_topk(const mita_cfg_t &c, const float *scores, int32_t *idx, hipStream_t st,
+                       const uint32_t *nrows = nullptr, const int32_t *rows = nullptr);
 
 // Expert tiles k_x/v_x [BH,M,k,d] from idx [BH,M,k].
 hipError_t launch_gather(const mita_cfg_t &c, const void *k, const void *v, const int32_t *idx, void *kx, void *vx,

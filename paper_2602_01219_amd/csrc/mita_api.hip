@@ -99,13 +99,31 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
   int32_t *offsets = (int32_t *)(w + L.offsets), *tile_cnt = (int32_t *)(w + L.tile_cnt);
   int32_t *tile_base = (int32_t *)(w + L.tile_base), *tile_start = (int32_t *)(w + L.tile_start);
   int32_t *counts = (int32_t *)(w + L.counts);
+  const bool fused = fused_select(*c);
+  SelectBufs sel{};
+  if (fused) {
+    sel.samp = (uint32_t *)(w + L.samp);
+    sel.plo = (uint32_t *)(w + L.plo);
+    sel.ccnt = (uint32_t *)(w + L.ccnt);
+    sel.cand = (uint2 *)(w + L.cand);
+    sel.fail_cnt = (uint32_t *)(w + L.fail);
+    sel.fail_list = (int32_t *)(w + L.fail) + 1;
+    sel.ns = sel_ns(*c);
+    sel.cap = sel_cap(*c);
+    sel.rank = sel_rank(*c);
+  }
 
   TRY(mark(0));
   TRY(hip_status(launch_pool(*c, q, q_lm, c->use_routed ? counts : nullptr, st), "landmarks"));
   TRY(mark(1));
-  TRY(hip_status(launch_scores(*c, q_lm, k, v, S, v_lm, w + L.partial, st), "scores"));
+  if (fused) TRY(hip_status(launch_select_pivots(*c, q_lm, k, sel, st), "select pivots"));
+  TRY(hip_status(launch_scores(*c, q_lm, k, v, fused ? nullptr : S, v_lm, w + L.partial, fused ? &sel : nullptr, st),
+                 "scores"));
   TRY(mark(2));
-  if (c->use_routed) TRY(hip_status(launch_topk(*c, S, idx, st), "topk"));
+  if (fused)
+    TRY(hip_status(launch_select_finish(*c, q_lm, k, sel, S, idx, st), "topk"));
+  else if (c->use_routed)
+    TRY(hip_status(launch_topk(*c, S, idx, st), "topk"));
   TRY(mark(3));
   if (staged) TRY(hip_status(launch_gather(*c, k, v, idx, kx, vx, st), "gather"));
   TRY(mark(4));
@@ -154,6 +172,23 @@ int mita_forward_timed(const mita_cfg_t *cfg, const void *q, const void *k, cons
   return forward_impl(cfg, q, k, v, o, ws, ws_bytes, (hipStream_t)stream, timer);
 }
 
+int mita_forward_fallbacks(const mita_cfg_t *cfg, const void *ws, size_t ws_bytes, int64_t *count,
+                           mita_stream_t stream) {
+  g_err.clear();
+  TRY(validate(cfg));
+  if (!count) return set_err(MITA_ERR_INVALID_ARG, "count is NULL");
+  TRY(need_ws(cfg, MITA_WS_FORWARD, ws, ws_bytes));
+  hipStream_t st = (hipStream_t)stream;
+  *count = 0;
+  TRY(hip_status(hipStreamSynchronize(st), "hipStreamSynchronize"));
+  if (!fused_select(*cfg)) return MITA_OK;
+  uint32_t n = 0;
+  TRY(hip_status(hipMemcpy(&n, (const char *)ws + forward_layout(*cfg).fail, sizeof n, hipMemcpyDeviceToHost),
+                 "hipMemcpy"));
+  *count = n;
+  return MITA_OK;
+}
+
 int mita_landmarks(const mita_cfg_t *cfg, const void *q, void *q_lm, mita_stream_t stream) {
   g_err.clear();
   TRY(validate(cfg));
@@ -174,7 +209,7 @@ int mita_scores(const mita_cfg_t *cfg, const void *q_lm, const void *k, const vo
     TRY(need_ptr(v, "v"));
     TRY(need_ws(cfg, MITA_WS_SCORES, ws, ws_bytes));
   }
-  return hip_status(launch_scores(*cfg, q_lm, k, v, scores, v_lm, ws, (hipStream_t)stream), "scores");
+  return hip_status(launch_scores(*cfg, q_lm, k, v, scores, v_lm, ws, nullptr, (hipStream_t)stream), "scores");
 }
 
 int mita_topk(const mita_cfg_t *cfg, const float *scores, int32_t *idx, void *ws, size_t ws_bytes,

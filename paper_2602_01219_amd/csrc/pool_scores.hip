@@ -56,37 +56,54 @@ __global__ __launch_bounds__(256) void pool_kernel(const T *__restrict__ q, T *_
 // ---------------------------------------------------------------------------
 // Scores and landmark values. Workgroup = 4 waves x 16 landmarks over one
 // chunk of SCORE_NC keys, key tiles of 64 staged in LDS (K row-major, V
-// transposed). Each wave forms S^T for its landmarks on MFMA, optionally
-// writes S = fl(dot) * scale (fp32, landmark-major), and runs an online
-// softmax with P V on MFMA for the landmark values (Eq. landmark-value: the
-// softmax runs over the keys of each landmark). Per-chunk partials (running
-// max in log2 units, running sum, unnormalised accumulator) go to `partial`.
+// transposed). Each wave forms S^T for its landmarks on MFMA and, per mode:
+//  - WRITE_S: writes S = fl(dot) * scale (fp32, landmark-major);
+//  - SELECT: lists the keys whose score is >= the row's pivot, in ascending
+//    token order, in the (row, chunk) region of the candidate lists (ordered
+//    score key, token index) and writes the region's count. In a tile a
+//    landmark's 64 keys sit in 4 lanes (lane group g holds keys
+//    16 kb + 4 g + r): per 16-key block kb, a scan over the 4 lanes of
+//    per-block counts packed in bytes gives each candidate its position, and
+//    a running count carries over the tiles of the chunk (no atomics);
+//  - DO_V: runs an online softmax with P V on MFMA for the landmark values
+//    (Eq. landmark-value: the softmax runs over the keys of each landmark);
+//    per-chunk partials (running max in log2 units, running sum,
+//    unnormalised accumulator) go to `partial`.
+// only_lm >= 0 restricts the S write to that landmark (the arithmetic of
+// every score is the same whichever rows are written).
 // ---------------------------------------------------------------------------
-template <typename T, int D, bool WRITE_S, bool DO_V>
-__global__ __launch_bounds__(BLOCK) void scores_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
-                                                       const T *__restrict__ v, float *__restrict__ S,
-                                                       float2 *__restrict__ part_ml, float *__restrict__ part_o,
-                                                       int N, int M, float scale) {
-  using TD = TileDims<T, D>;
-  __shared__ __align__(16) T Ks[TD::K_ELEMS];
-  __shared__ __align__(16) T Vt[DO_V ? TD::V_ELEMS : 1];
-  const int chunk = blockIdx.x, nchunks = gridDim.x;
-  const int64_t bh = blockIdx.z;
+struct SelectArgs {
+  const uint32_t *plo;  // [rows] pivot keys
+  uint32_t *ccnt;       // [rows, chunks] candidates listed
+  uint2 *cand;          // [rows, chunks, SCORE_NC] (key, token index)
+};
+
+template <typename T, int D, bool WRITE_S, bool DO_V, bool SELECT>
+__device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ Vt, const T *__restrict__ q_lm,
+                                            const T *__restrict__ k, const T *__restrict__ v, float *__restrict__ S,
+                                            float2 *__restrict__ part_ml, float *__restrict__ part_o,
+                                            const SelectArgs &sel, int N, int M, float scale, int chunk, int nchunks,
+                                            int lmblock, int64_t bh, int only_lm) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
-  const int lm0 = (blockIdx.y * 4 + w) * 16;
-  const bool active = lm0 < M;
+  const int lm0 = (lmblock * 4 + w) * 16;
+  const bool active = lm0 < M && (only_lm < 0 || (only_lm >= lm0 && only_lm < lm0 + 16));
   const int lm = lm0 + p;
+  const int64_t row = bh * M + lm;
   const T *kb_ = k + bh * (int64_t)N * D;
-  const T *vb_ = v + bh * (int64_t)N * D;
+  const T *vb_ = DO_V ? v + bh * (int64_t)N * D : nullptr;
 
   Frag<T> qf[D / 32];
 #pragma unroll
   for (int ks = 0; ks < D / 32; ++ks) {
     if (lm < M)
-      qf[ks].load(q_lm + (bh * M + lm) * D + ks * 32 + g * 8);
+      qf[ks].load(q_lm + row * D + ks * 32 + g * 8);
     else
       qf[ks].zero();
   }
+  // keys >= plo are candidates; 0xffffffff (above every score key) lists nothing
+  const uint32_t plo = SELECT && lm < M ? sel.plo[row] : 0xffffffffu;
+  const bool write_row = WRITE_S && lm < M && (only_lm < 0 || lm == only_lm);
+  uint32_t listed = 0;  // SELECT: candidates of this landmark listed so far in the chunk
   Online<D> st;
   st.init();
   const float sl2 = scale * LOG2E;
@@ -94,13 +111,13 @@ __global__ __launch_bounds__(BLOCK) void scores_kernel(const T *__restrict__ q_l
   for (int k0 = key_begin; k0 < key_end; k0 += TK) {
     const int nvalid = min(TK, key_end - k0);
     __syncthreads();
-    load_kv_tile<T, D, DO_V>(Ks, Vt, kb_ + (int64_t)k0 * D, vb_ + (int64_t)k0 * D, nullptr, nvalid);
+    load_kv_tile<T, D, DO_V>(Ks, Vt, kb_ + (int64_t)k0 * D, DO_V ? vb_ + (int64_t)k0 * D : nullptr, nullptr, nvalid);
     __syncthreads();
     if (!active) continue;
     f32x4 acc[4];
     tile_scores<T, D>(acc, Ks, qf);
-    if (WRITE_S && lm < M) {
-      float *srow = S + (bh * M + lm) * (int64_t)N + k0;
+    if (write_row) {
+      float *srow = S + row * (int64_t)N + k0;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
         const int key = kb * 16 + 4 * g;
@@ -114,17 +131,81 @@ __global__ __launch_bounds__(BLOCK) void scores_kernel(const T *__restrict__ q_l
         }
       }
     }
+    if (SELECT) {
+      uint32_t msk = 0, packed = 0;  // candidate bits (4 kb + r); per-kb counts in bytes
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        uint32_t m = 0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (kb * 16 + 4 * g + r < nvalid && score_key(acc[kb][r] * scale) >= plo) m |= 1u << r;
+        msk |= m << (4 * kb);
+        packed |= (uint32_t)__popc(m) << (8 * kb);
+      }
+      // inclusive scan over the lane groups of landmark p (bytes stay below 17)
+      uint32_t incl = packed;
+      uint32_t y = (uint32_t)__shfl_up((int)incl, 16);
+      if (g >= 1) incl += y;
+      y = (uint32_t)__shfl_up((int)incl, 32);
+      if (g >= 2) incl += y;
+      const uint32_t tot = (uint32_t)__shfl((int)incl, 48 + p);  // per-kb totals of the landmark
+      // byte kb of pos: candidates of the landmark before this lane's block kb
+      uint32_t pos = (incl - packed) + (tot << 8) + (tot << 16) + (tot << 24);
+      uint2 *list = sel.cand + (row * nchunks + chunk) * (int64_t)SCORE_NC + listed;
+      while (msk) {
+        const int e = __builtin_ctz(msk);
+        msk &= msk - 1u;
+        const int kb = e >> 2, r = e & 3;
+        list[(pos >> (8 * kb)) & 255u] = make_uint2(score_key(acc[kb][r] * scale), (uint32_t)(k0 + kb * 16 + 4 * g + r));
+        pos += 1u << (8 * kb);
+      }
+      listed += (tot * 0x01010101u) >> 24;
+    }
     if (DO_V) tile_softmax_pv<T, D>(st, acc, Vt, nvalid, sl2);
   }
+  if (SELECT && active && lm < M && g == 0) sel.ccnt[row * nchunks + chunk] = listed;
   if (!DO_V || !active) return;
   const float l = column_sum(st.l);
   if (lm < M) {
-    const int64_t row = (bh * nchunks + chunk) * M + lm;
-    if (g == 0) part_ml[row] = make_float2(st.m, l);
+    const int64_t prow = (bh * nchunks + chunk) * M + lm;
+    if (g == 0) part_ml[prow] = make_float2(st.m, l);
 #pragma unroll
     for (int db = 0; db < D / 16; ++db)
-      *reinterpret_cast<float4 *>(part_o + row * D + db * 16 + 4 * g) =
+      *reinterpret_cast<float4 *>(part_o + prow * D + db * 16 + 4 * g) =
           make_float4(st.o[db][0], st.o[db][1], st.o[db][2], st.o[db][3]);
+  }
+}
+
+template <typename T, int D, bool WRITE_S, bool DO_V, bool SELECT>
+__global__ __launch_bounds__(BLOCK) void scores_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
+                                                       const T *__restrict__ v, float *__restrict__ S,
+                                                       float2 *__restrict__ part_ml, float *__restrict__ part_o,
+                                                       SelectArgs sel, int N, int M, float scale) {
+  using TD = TileDims<T, D>;
+  __shared__ __align__(16) T Ks[TD::K_ELEMS];
+  __shared__ __align__(16) T Vt[DO_V ? TD::V_ELEMS : 1];
+  score_chunk<T, D, WRITE_S, DO_V, SELECT>(Ks, Vt, q_lm, k, v, S, part_ml, part_o, sel, N, M, scale, blockIdx.x,
+                                           gridDim.x, blockIdx.y, blockIdx.z, -1);
+}
+
+// Score rows of listed landmark rows (fallback of the fused selection): work
+// item = (listed row, key chunk); each item recomputes the row's 64-landmark
+// block exactly as the score pass does and writes that row only.
+template <typename T, int D>
+__global__ __launch_bounds__(BLOCK) void scores_rows_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
+                                                            float *__restrict__ S, const uint32_t *__restrict__ nrows,
+                                                            const int32_t *__restrict__ rows, int N, int M,
+                                                            float scale, int nchunks) {
+  using TD = TileDims<T, D>;
+  __shared__ __align__(16) T Ks[TD::K_ELEMS];
+  const int64_t items = (int64_t)*nrows * nchunks;
+  const SelectArgs none{nullptr, nullptr, nullptr};
+  for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
+    const int row = rows[it / nchunks];
+    const int chunk = (int)(it % nchunks);
+    const int lm = row % M;
+    score_chunk<T, D, true, false, false>(Ks, nullptr, q_lm, k, nullptr, S, nullptr, nullptr, none, N, M, scale,
+                                          chunk, nchunks, lm / 64, row / M, lm);
   }
 }
 
@@ -205,23 +286,31 @@ hipError_t launch_zero(int32_t *p, int64_t n, hipStream_t st) {
 
 template <typename T, int D>
 static hipError_t scores_t(const mita_cfg_t &c, const void *q_lm, const void *k, const void *v, float *S, void *v_lm,
-                           void *partial, hipStream_t st) {
+                           void *partial, const SelectBufs *sb, hipStream_t st) {
   const int nch = score_chunks(c);
   dim3 grid(nch, (c.M + 63) / 64, (unsigned)BH(c));
   float2 *ml = (float2 *)partial;
-  float *po = (float *)((char *)partial + align_up((size_t)BH(c) * nch * c.M * sizeof(float2)));
+  float *po = v_lm ? (float *)((char *)partial + align_up((size_t)BH(c) * nch * c.M * sizeof(float2))) : nullptr;
   const float sc = eff_scale(c);
-  if (S && v_lm)
-    hipLaunchKernelGGL((scores_kernel<T, D, true, true>), grid, dim3(BLOCK), 0, st, (const T *)q_lm, (const T *)k,
-                       (const T *)v, S, ml, po, c.N, c.M, sc);
-  else if (S)
-    hipLaunchKernelGGL((scores_kernel<T, D, true, false>), grid, dim3(BLOCK), 0, st, (const T *)q_lm, (const T *)k,
-                       (const T *)v, S, ml, po, c.N, c.M, sc);
-  else if (v_lm)
-    hipLaunchKernelGGL((scores_kernel<T, D, false, true>), grid, dim3(BLOCK), 0, st, (const T *)q_lm, (const T *)k,
-                       (const T *)v, S, ml, po, c.N, c.M, sc);
-  else
+  const SelectArgs sel = sb ? SelectArgs{sb->plo, sb->ccnt, sb->cand} : SelectArgs{nullptr, nullptr, nullptr};
+  const T *ql = (const T *)q_lm, *kk = (const T *)k, *vv = (const T *)v;
+#define MITA_SCORES(W, V, SEL) \
+  hipLaunchKernelGGL((scores_kernel<T, D, W, V, SEL>), grid, dim3(BLOCK), 0, st, ql, kk, vv, S, ml, po, sel, c.N, c.M, sc)
+  if (sb) {
+    if (v_lm)
+      MITA_SCORES(false, true, true);
+    else
+      MITA_SCORES(false, false, true);
+  } else if (S && v_lm) {
+    MITA_SCORES(true, true, false);
+  } else if (S) {
+    MITA_SCORES(true, false, false);
+  } else if (v_lm) {
+    MITA_SCORES(false, true, false);
+  } else {
     return hipSuccess;
+  }
+#undef MITA_SCORES
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !v_lm) return e;
   constexpr int LPB = 256 / D;
@@ -231,12 +320,34 @@ static hipError_t scores_t(const mita_cfg_t &c, const void *q_lm, const void *k,
 }
 
 hipError_t launch_scores(const mita_cfg_t &c, const void *q_lm, const void *k, const void *v, float *S, void *v_lm,
-                         void *partial, hipStream_t st) {
+                         void *partial, const SelectBufs *sel, hipStream_t st) {
   if (c.dtype == MITA_F32)
-    return c.d == 64 ? scores_t<float, 64>(c, q_lm, k, v, S, v_lm, partial, st)
-                     : scores_t<float, 128>(c, q_lm, k, v, S, v_lm, partial, st);
-  return c.d == 64 ? scores_t<bf16_t, 64>(c, q_lm, k, v, S, v_lm, partial, st)
-                   : scores_t<bf16_t, 128>(c, q_lm, k, v, S, v_lm, partial, st);
+    return c.d == 64 ? scores_t<float, 64>(c, q_lm, k, v, S, v_lm, partial, sel, st)
+                     : scores_t<float, 128>(c, q_lm, k, v, S, v_lm, partial, sel, st);
+  return c.d == 64 ? scores_t<bf16_t, 64>(c, q_lm, k, v, S, v_lm, partial, sel, st)
+                   : scores_t<bf16_t, 128>(c, q_lm, k, v, S, v_lm, partial, sel, st);
+}
+
+template <typename T, int D>
+static hipError_t scores_rows_t(const mita_cfg_t &c, const void *q_lm, const void *k, float *S, const uint32_t *nrows,
+                                const int32_t *rows, hipStream_t st) {
+  // a fixed grid walks the (row, chunk) items; with no listed rows every
+  // workgroup exits at once
+  const int nch = score_chunks(c);
+  const int64_t most = BH(c) * c.M * (int64_t)nch;
+  const unsigned grid = (unsigned)(most < 1024 ? most : 1024);
+  hipLaunchKernelGGL((scores_rows_kernel<T, D>), dim3(grid), dim3(BLOCK), 0, st, (const T *)q_lm, (const T *)k, S,
+                     nrows, rows, c.N, c.M, eff_scale(c), nch);
+  return hipGetLastError();
+}
+
+hipError_t launch_scores_rows(const mita_cfg_t &c, const void *q_lm, const void *k, float *S, const uint32_t *nrows,
+                              const int32_t *rows, hipStream_t st) {
+  if (c.dtype == MITA_F32)
+    return c.d == 64 ? scores_rows_t<float, 64>(c, q_lm, k, S, nrows, rows, st)
+                     : scores_rows_t<float, 128>(c, q_lm, k, S, nrows, rows, st);
+  return c.d == 64 ? scores_rows_t<bf16_t, 64>(c, q_lm, k, S, nrows, rows, st)
+                   : scores_rows_t<bf16_t, 128>(c, q_lm, k, S, nrows, rows, st);
 }
 
 template <typename T, int D>

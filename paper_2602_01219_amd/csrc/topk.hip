@@ -263,14 +263,9 @@ __device__ __forceinline__ void ordered_stream(TopkSmem<CAP> &sh, const Src &s, 
 }  // namespace
 
 template <int CAP, bool VEC, int ROWCAP>
-__global__ __launch_bounds__(NT) void topk_kernel(const float *__restrict__ S, int32_t *__restrict__ idx, int N,
-                                                  int k) {
+__device__ __forceinline__ void topk_row(TopkSmem<CAP> &sh, float *lrow, const float *__restrict__ grow,
+                                         int32_t *__restrict__ out, int N, int k) {
   constexpr bool IN_LDS = ROWCAP > 0;
-  __shared__ TopkSmem<CAP> sh;
-  __shared__ __align__(16) float lrow[IN_LDS ? ROWCAP : 1];
-  const int64_t row = blockIdx.x;
-  const float *grow = S + row * (int64_t)N;
-  int32_t *out = idx + row * (int64_t)k;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   if (IN_LDS) {
     // one coalesced pass copies the row into LDS
@@ -600,22 +595,46 @@ __global__ __launch_bounds__(NT) void topk_kernel(const float *__restrict__ S, i
                            });
 }
 
+// One workgroup per row; with a row list, a fixed grid walks the *nrows
+// listed rows (every workgroup exits at once when there are none).
+template <int CAP, bool VEC, int ROWCAP>
+__global__ __launch_bounds__(NT) void topk_kernel(const float *__restrict__ S, int32_t *__restrict__ idx, int N, int k,
+                                                  const uint32_t *__restrict__ nrows,
+                                                  const int32_t *__restrict__ rows) {
+  __shared__ TopkSmem<CAP> sh;
+  __shared__ __align__(16) float lrow[ROWCAP > 0 ? ROWCAP : 1];
+  if (!rows) {
+    const int64_t row = blockIdx.x;
+    topk_row<CAP, VEC, ROWCAP>(sh, lrow, S + row * (int64_t)N, idx + row * (int64_t)k, N, k);
+    return;
+  }
+  const uint32_t n = *nrows;
+  for (uint32_t f = blockIdx.x; f < n; f += gridDim.x) {
+    const int64_t row = rows[f];
+    __syncthreads();  // the previous row's last reads of LDS are done
+    topk_row<CAP, VEC, ROWCAP>(sh, lrow, S + row * (int64_t)N, idx + row * (int64_t)k, N, k);
+  }
+}
+
 template <int CAP, int ROWCAP>
-static hipError_t topk_t(const mita_cfg_t &c, const float *S, int32_t *idx, hipStream_t st) {
-  const int64_t rows = BH(c) * c.M;
+static hipError_t topk_t(const mita_cfg_t &c, const float *S, int32_t *idx, hipStream_t st, const uint32_t *nrows,
+                         const int32_t *rows) {
+  const int64_t all = BH(c) * c.M;
+  const unsigned grid = (unsigned)(rows ? (all < 512 ? all : 512) : all);
   if (c.N % 4 == 0)
-    hipLaunchKernelGGL((topk_kernel<CAP, true, ROWCAP>), dim3((unsigned)rows), dim3(NT), 0, st, S, idx, c.N, c.k);
+    hipLaunchKernelGGL((topk_kernel<CAP, true, ROWCAP>), dim3(grid), dim3(NT), 0, st, S, idx, c.N, c.k, nrows, rows);
   else
-    hipLaunchKernelGGL((topk_kernel<CAP, false, ROWCAP>), dim3((unsigned)rows), dim3(NT), 0, st, S, idx, c.N, c.k);
+    hipLaunchKernelGGL((topk_kernel<CAP, false, ROWCAP>), dim3(grid), dim3(NT), 0, st, S, idx, c.N, c.k, nrows, rows);
   return hipGetLastError();
 }
 
 // Rows up to 16384 scores (64 KiB) are copied into LDS once; longer rows are
 // streamed from memory in every pass.
-hipError_t launch_topk(const mita_cfg_t &c, const float *S, int32_t *idx, hipStream_t st) {
-  if (c.N <= 4096) return topk_t<512, 4096>(c, S, idx, st);
-  if (c.N <= 16384) return topk_t<512, 16384>(c, S, idx, st);
-  return topk_t<2048, 0>(c, S, idx, st);
+hipError_t launch_topk(const mita_cfg_t &c, const float *S, int32_t *idx, hipStream_t st, const uint32_t *nrows,
+                       const int32_t *rows) {
+  if (c.N <= 4096) return topk_t<512, 4096>(c, S, idx, st, nrows, rows);
+  if (c.N <= 16384) return topk_t<512, 16384>(c, S, idx, st, nrows, rows);
+  return topk_t<2048, 0>(c, S, idx, st, nrows, rows);
 }
 
 }  // namespace mita

@@ -24,6 +24,7 @@ LIB_PATH = os.path.join(_PKG, "libmita.so")
 MITA_OK, MITA_ERR_INVALID_ARG, MITA_ERR_UNSUPPORTED, MITA_ERR_WORKSPACE, MITA_ERR_HIP = range(5)
 MITA_F32, MITA_BF16 = 0, 1
 MITA_FLAG_STAGED_GATHER = 0x1
+MITA_FLAG_FULL_SCORES = 0x2
 WS_FORWARD, WS_SCORES, WS_TOPK, WS_ROUTE, WS_ATTEND = range(5)
 NUM_STAGES = 6
 STAGES = ("landmarks", "scores", "topk", "gather", "route", "attend")
@@ -32,7 +33,7 @@ MAX_N = 65536
 EXPORTED = ("mita_check", "mita_workspace_size", "mita_status_string", "mita_last_error", "mita_forward",
             "mita_landmarks", "mita_scores", "mita_topk", "mita_gather", "mita_route", "mita_attend",
             "mita_timer_create", "mita_timer_destroy", "mita_timer_reset", "mita_timer_read",
-            "mita_forward_timed")
+            "mita_forward_timed", "mita_forward_fallbacks")
 
 
 class CfgStruct(ctypes.Structure):
@@ -67,6 +68,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "mita_last_error": (ctypes.c_char_p, []),
         "mita_forward": (I, [cfgp, P, P, P, P, P, Z, P]),
         "mita_forward_timed": (I, [cfgp, P, P, P, P, P, Z, P, P]),
+        "mita_forward_fallbacks": (I, [cfgp, P, Z, ctypes.POINTER(ctypes.c_int64), P]),
         "mita_landmarks": (I, [cfgp, P, P, P]),
         "mita_scores": (I, [cfgp, P, P, P, P, P, P, Z, P]),
         "mita_topk": (I, [cfgp, P, P, P, Z, P]),
@@ -111,6 +113,7 @@ class Config:
     s: int = 1
     scale: float = 0.0           # 0 -> 1/sqrt(d)
     staged_gather: bool = False
+    full_scores: bool = False    # store S and select from it instead of the fused selection
 
     @staticmethod
     def from_workload(wl, **kw) -> "Config":
@@ -123,7 +126,8 @@ class Config:
         return CfgStruct(self.B, self.H, self.N, self.d, self.grid_h, self.grid_w, self.M, self.lm_h, self.lm_w,
                          self.k, self.s, self.use_shared, self.use_routed,
                          MITA_F32 if self.dtype == "f32" else MITA_BF16, float(self.scale),
-                         MITA_FLAG_STAGED_GATHER if self.staged_gather else 0)
+                         (MITA_FLAG_STAGED_GATHER if self.staged_gather else 0)
+                         | (MITA_FLAG_FULL_SCORES if self.full_scores else 0))
 
     @property
     def torch_dtype(self):
@@ -179,6 +183,15 @@ def forward(cfg: Config, q, k, v, o=None, ws=None, stream=None, timer: "Timer" =
                                     timer.handle)
     _check(st)
     return o
+
+
+def forward_fallbacks(cfg: Config, ws, stream=None) -> int:
+    """Landmark rows whose fused top-k selection fell back to the full score
+    row in the last forward on workspace ws (synchronises the stream)."""
+    n = ctypes.c_int64()
+    _check(load_library().mita_forward_fallbacks(ctypes.byref(cfg.struct()), _p(ws), ws.numel(), ctypes.byref(n),
+                                                 _stream(stream)))
+    return n.value
 
 
 def landmarks(cfg: Config, q, q_lm=None, stream=None):

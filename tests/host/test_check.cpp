@@ -43,14 +43,16 @@ int main() {
   EXPECT(c.scale = -1.f, MITA_ERR_INVALID_ARG);
   EXPECT(c.flags = 0x80, MITA_ERR_INVALID_ARG);
   EXPECT(c.flags = MITA_FLAG_STAGED_GATHER, MITA_OK);
+  EXPECT(c.flags = MITA_FLAG_STAGED_GATHER | MITA_FLAG_FULL_SCORES, MITA_OK);
   EXPECT(c.B = 0, MITA_ERR_INVALID_ARG);
   assert(mita::check_cfg(nullptr, nullptr) == MITA_ERR_INVALID_ARG);
 
   // workspace layout: aligned, non-overlapping, monotone
   mita_cfg_t c = base();
   mita::FwdLayout L = mita::forward_layout(c);
-  const size_t offs[] = {L.q_lm, L.v_lm, L.scores, L.partial, L.idx, L.kx, L.vx, L.expert,
-                         L.perm, L.offsets, L.tile_cnt, L.tile_base, L.counts, L.tile_start, L.total};
+  const size_t offs[] = {L.q_lm,      L.v_lm,   L.scores, L.partial, L.idx,     L.kx,   L.vx,
+                         L.expert,    L.perm,   L.offsets, L.tile_cnt, L.tile_base, L.counts, L.tile_start,
+                         L.samp,      L.plo,    L.ccnt,   L.cand,    L.fail,    L.total};
   for (size_t i = 0; i + 1 < sizeof offs / sizeof offs[0]; ++i) {
     assert(offs[i] % 256 == 0);
     assert(offs[i] <= offs[i + 1]);
@@ -62,6 +64,24 @@ int main() {
   mita::FwdLayout L2 = mita::forward_layout(c);
   assert(L2.vx - L2.kx == (size_t)24 * 128 * 512 * 64 * 2);
   assert(mita::workspace_size(&c, MITA_WS_TOPK) == 0);
+  // fused selection: sample of 2048 keys, pivot rank 64 + 5 * sqrt(64 * 31 / 32) + 1
+  // -> 105 at N = 16384, k = 512; expected count bound (105 + 6 sqrt(105)) * 8 -> cap 2048
+  assert(mita::fused_select(c) && mita::sel_ns(c) == 2048 && mita::sel_cap(c) == 2048);
+  assert(mita::sel_rank(c) == 105);
+  assert(L2.plo - L2.samp == (size_t)24 * 128 * 2048 * 4);
+  assert(L2.cand - L2.ccnt == (size_t)24 * 128 * 32 * 4);
+  assert(L2.fail - L2.cand == (size_t)24 * 128 * 32 * 512 * 8);
+  assert(L2.total - L2.fail >= (size_t)(24 * 128 + 1) * 4);
+  c.flags = MITA_FLAG_FULL_SCORES;
+  assert(!mita::fused_select(c) && mita::forward_layout(c).samp == mita::forward_layout(c).total);
+  c.flags = 0;
+  c.k = 1025;
+  assert(!mita::fused_select(c));
+  c.grid_h = 32; c.grid_w = 64; c.N = 2048; c.k = 2048;  // the sample is the whole row: rank = k
+  assert(mita::fused_select(c) && mita::sel_rank(c) == 2048 && mita::sel_cap(c) == 2048);
+  c.grid_h = 256; c.grid_w = 256; c.N = 65536; c.k = 1024;  // rank 62, bound (62 + 47) * 32 -> cap 4096
+  assert(mita::fused_select(c) && mita::sel_rank(c) == 62 && mita::sel_cap(c) == 4096);
+  c = base();
   c.d = 96;
   assert(mita::workspace_size(&c, MITA_WS_FORWARD) == 0);
   std::printf("host checks ok\n");

@@ -345,6 +345,94 @@ def test_forward_edge_cases(case):
     _end_to_end(cfg, inp, q, k, v, [(0, 0), (1, 1)], row_limit=10 ** 9, exact_sets=(dtype == "f32"))
 
 
+# ------------------------------------------------------------------ fused top-k selection
+def _same(a, b):
+    return torch.equal(a.view(torch.int16), b.view(torch.int16)) if a.dtype == torch.bfloat16 else torch.equal(a, b)
+
+
+@pytest.mark.parametrize("name", ALL)
+def test_fused_selection_equals_full_score_path(name):
+    """The forward's selection inside the score pass gives the sets of the
+    exact top-k over the stored score matrix: identical outputs."""
+    cfg = mita.Config.from_workload(_inputs(name).wl)
+    q, k, v = _dev_inputs(name)
+    ws = torch.empty(mita.workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    a = mita.forward(cfg, q, k, v, ws=ws)
+    fb = mita.forward_fallbacks(cfg, ws)
+    full = dataclasses.replace(cfg, full_scores=True)
+    b = mita.forward(full, q, k, v)
+    log(f"  {name}: rows recomputed in full {fb} of {cfg.B * cfg.H * cfg.M}")
+    assert _same(a, b)
+    assert mita.forward_fallbacks(full, torch.empty(mita.workspace_size(full), dtype=torch.uint8,
+                                                    device="cuda")) == 0
+
+
+def _fallback_case(K, cfg, q, v, expect_fb):
+    ws = torch.empty(mita.workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    a = mita.forward(cfg, q, K, v, ws=ws)
+    fb = mita.forward_fallbacks(cfg, ws)
+    b = mita.forward(dataclasses.replace(cfg, full_scores=True), q, K, v)
+    torch.cuda.synchronize()
+    log(f"  fallback rows {fb} (expected {expect_fb})")
+    assert fb == expect_fb
+    assert _same(a, b)
+
+
+def _small_dense(H=2):
+    wl = synth.WORKLOADS["dense_pred_bf16"].with_(B=1, H=H)
+    inp = synth.generate(wl)
+    cfg = mita.Config.from_workload(wl)
+    return inp, cfg, tuple(to_dev(x, "bf16") for x in (inp.q, inp.k, inp.v))
+
+
+def test_fused_selection_rows_beyond_the_list_fall_back():
+    """Head 0 with all-zero keys: every score ties at 0, all N = 16384 tokens
+    reach the pivot, more than a list holds: those rows are recomputed in
+    full and selected exactly (the first k indices); head 1 stays fused."""
+    inp, cfg, (q, k, v) = _small_dense()
+    K = k.clone()
+    K[0, 0] = 0
+    _fallback_case(K, cfg, q, v, expect_fb=cfg.M)
+
+
+def test_fused_selection_unrepresentative_sample_falls_back():
+    """Keys at exactly the sampled positions (the middle of each of 2048 equal
+    parts of the row) scaled up 8x: the pivot from the sample then lies above
+    all but about r of the row's scores, fewer than k, so every row falls back."""
+    inp, cfg, (q, k, v) = _small_dense(H=1)
+    ns = min(cfg.N, 2048)
+    pos = ((2 * np.arange(ns) + 1) * cfg.N) // (2 * ns)
+    K = k.clone()
+    K[0, 0, torch.from_numpy(pos).cuda()] *= 8
+    _fallback_case(K, cfg, q, v, expect_fb=cfg.M)
+
+
+def test_fused_selection_exact_ties_within_the_list():
+    """N = 2048 (the sample is the whole row, a list holds it all) with
+    all-zero keys: every score ties, every token is listed and the selection
+    is the first k."""
+    wl = synth.WORKLOADS["dense_pred_bf16"].with_(B=1, H=1, grid_h=32, grid_w=64)
+    inp = synth.generate(wl)
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = (to_dev(x, "bf16") for x in (inp.q, inp.k, inp.v))
+    _fallback_case(torch.zeros_like(k), cfg, q, v, expect_fb=0)
+
+
+def test_fused_selection_quantised_keys():
+    """Keys in {-1, 0, 1}: scores take few distinct values, so the k-th score
+    is shared by many tokens and the cut falls inside a run of ties."""
+    inp, cfg, (q, k, v) = _small_dense()
+    r = np.random.default_rng(11)
+    kq = r.integers(-1, 2, size=k.shape).astype(np.float32)
+    K = torch.from_numpy(kq).to(torch.bfloat16).cuda()
+    ws = torch.empty(mita.workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    a = mita.forward(cfg, q, K, v, ws=ws)
+    fb = mita.forward_fallbacks(cfg, ws)
+    b = mita.forward(dataclasses.replace(cfg, full_scores=True), q, K, v)
+    log(f"  quantised keys: fallback rows {fb}")
+    assert _same(a, b)
+
+
 def test_staged_gather_equals_in_place_gather():
     name = "vitb_hr_bf16"
     cfg = mita.Config.from_workload(_inputs(name).wl)
