@@ -148,12 +148,13 @@ __device__ __forceinline__ void tile_softmax_pv(Online<D> &st, const f32x4 (&acc
 // global loads of the next tile are issued before the current tile is
 // processed, the LDS stores after). Thread t owns rows CH*(t / CPR) + j,
 // j < CH, at 16-byte chunk t % CPR, so the transposing V store can write the
-// CH consecutive keys of one dimension as one packed word.
-template <typename T, int D> struct TileRegs {
+// CH consecutive keys of one dimension as one packed word. WITH_V = false
+// stages keys only.
+template <typename T, int D, bool WITH_V = true> struct TileRegs {
   static constexpr int VE = 16 / (int)sizeof(T);
   static constexpr int CPR = D / VE;           // 16-byte chunks per row
   static constexpr int CH = TK * CPR / BLOCK;  // rows per thread
-  uint4 k[CH], v[CH];
+  uint4 k[CH], v[WITH_V ? CH : 1];
   __device__ __forceinline__ int row0() const { return CH * ((int)threadIdx.x / CPR); }
   __device__ __forceinline__ int chunk() const { return (int)threadIdx.x % CPR; }
   // row r of the tile is source row (rowidx ? rowidx[r] : r); rows >= nrows load zeros
@@ -164,11 +165,11 @@ template <typename T, int D> struct TileRegs {
     for (int j = 0; j < CH; ++j) {
       const int r = r0 + j;
       k[j] = make_uint4(0, 0, 0, 0);
-      v[j] = make_uint4(0, 0, 0, 0);
+      if (WITH_V) v[j] = make_uint4(0, 0, 0, 0);
       if (r < nrows) {
         const int64_t src = rowidx ? (int64_t)rowidx[r] : (int64_t)r;
         k[j] = *reinterpret_cast<const uint4 *>(kb + src * D + ch * VE);
-        v[j] = *reinterpret_cast<const uint4 *>(vb + src * D + ch * VE);
+        if (WITH_V) v[j] = *reinterpret_cast<const uint4 *>(vb + src * D + ch * VE);
       }
     }
   }
@@ -177,13 +178,13 @@ template <typename T, int D> struct TileRegs {
     const int r0 = row0(), ch = chunk();
 #pragma unroll
     for (int j = 0; j < CH; ++j) *reinterpret_cast<uint4 *>(Ks + (r0 + j) * TD::KSTR + ch * VE) = k[j];
-    store_vt(Vt + (ch * VE) * TD::VSTR + r0);
+    if constexpr (WITH_V) store_vt(Vt + (ch * VE) * TD::VSTR + r0);
   }
   // V^T: dimension ch*VE + e, keys r0 .. r0+CH-1
   __device__ __forceinline__ void store_vt(T *__restrict__ dst) const;
 };
 
-template <> __device__ __forceinline__ void TileRegs<bf16_t, 64>::store_vt(bf16_t *__restrict__ dst) const {
+template <> __device__ __forceinline__ void TileRegs<bf16_t, 64, true>::store_vt(bf16_t *__restrict__ dst) const {
   // CH = 2: keys r0, r0+1 of dims 2m, 2m+1 from the two rows' words m
   using TD = TileDims<bf16_t, 64>;
   const uint32_t r0w[4] = {v[0].x, v[0].y, v[0].z, v[0].w}, r1w[4] = {v[1].x, v[1].y, v[1].z, v[1].w};
@@ -193,7 +194,7 @@ template <> __device__ __forceinline__ void TileRegs<bf16_t, 64>::store_vt(bf16_
     *reinterpret_cast<uint32_t *>(dst + (2 * m + 1) * TD::VSTR) = __builtin_amdgcn_perm(r1w[m], r0w[m], 0x07060302u);
   }
 }
-template <> __device__ __forceinline__ void TileRegs<bf16_t, 128>::store_vt(bf16_t *__restrict__ dst) const {
+template <> __device__ __forceinline__ void TileRegs<bf16_t, 128, true>::store_vt(bf16_t *__restrict__ dst) const {
   // CH = 4: keys r0 .. r0+3 of dims 2m, 2m+1 as one 8-byte word each
   using TD = TileDims<bf16_t, 128>;
   const uint32_t w0[4] = {v[0].x, v[0].y, v[0].z, v[0].w}, w1[4] = {v[1].x, v[1].y, v[1].z, v[1].w};
@@ -206,7 +207,7 @@ template <> __device__ __forceinline__ void TileRegs<bf16_t, 128>::store_vt(bf16
         make_uint2(__builtin_amdgcn_perm(w1[m], w0[m], 0x07060302u), __builtin_amdgcn_perm(w3[m], w2[m], 0x07060302u));
   }
 }
-template <> __device__ __forceinline__ void TileRegs<float, 64>::store_vt(float *__restrict__ dst) const {
+template <> __device__ __forceinline__ void TileRegs<float, 64, true>::store_vt(float *__restrict__ dst) const {
   // CH = 4: keys r0 .. r0+3 of each of the 4 dims as one 16-byte word
   using TD = TileDims<float, 64>;
   const float *r[4] = {reinterpret_cast<const float *>(&v[0]), reinterpret_cast<const float *>(&v[1]),
@@ -215,7 +216,7 @@ template <> __device__ __forceinline__ void TileRegs<float, 64>::store_vt(float 
   for (int e = 0; e < 4; ++e)
     *reinterpret_cast<float4 *>(dst + e * TD::VSTR) = make_float4(r[0][e], r[1][e], r[2][e], r[3][e]);
 }
-template <> __device__ __forceinline__ void TileRegs<float, 128>::store_vt(float *__restrict__ dst) const {
+template <> __device__ __forceinline__ void TileRegs<float, 128, true>::store_vt(float *__restrict__ dst) const {
   // CH = 8: keys r0 .. r0+7 of each of the 4 dims as two 16-byte words
   using TD = TileDims<float, 128>;
 #pragma unroll

@@ -19,8 +19,8 @@ hipError_t launch_zero(int32_t *p, int64_t n, hipStream_t st);
 struct SelectBufs {
   uint32_t *samp;       // [rows, ns] ordered keys of the sampled scores
   uint32_t *plo;        // [rows] pivot keys
-  uint32_t *ccnt;       // [rows] candidates found (may exceed cap)
-  uint2 *cand;          // [rows, cap] (key, token index) candidate lists
+  uint32_t *ccnt;       // [rows, chunks] candidates listed per key chunk
+  uint2 *cand;          // [rows, chunks, SCORE_NC] (score bits, token index) lists
   uint32_t *fail_cnt;   // rows that fall back to the full score row
   int32_t *fail_list;   // [rows] their row numbers
   int ns, cap, rank;

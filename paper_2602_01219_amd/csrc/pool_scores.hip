@@ -59,8 +59,8 @@ __global__ __launch_bounds__(256) void pool_kernel(const T *__restrict__ q, T *_
 // transposed). Each wave forms S^T for its landmarks on MFMA and, per mode:
 //  - WRITE_S: writes S = fl(dot) * scale (fp32, landmark-major);
 //  - SELECT: lists the keys whose score is >= the row's pivot, in ascending
-//    token order, in the (row, chunk) region of the candidate lists (ordered
-//    score key, token index) and writes the region's count. In a tile a
+//    token order, in the (row, chunk) region of the candidate lists (score
+//    bits, token index) and writes the region's count. In a tile a
 //    landmark's 64 keys sit in 4 lanes (lane group g holds keys
 //    16 kb + 4 g + r): per 16-key block kb, a scan over the 4 lanes of
 //    per-block counts packed in bytes gives each candidate its position, and
@@ -75,7 +75,7 @@ __global__ __launch_bounds__(256) void pool_kernel(const T *__restrict__ q, T *_
 struct SelectArgs {
   const uint32_t *plo;  // [rows] pivot keys
   uint32_t *ccnt;       // [rows, chunks] candidates listed
-  uint2 *cand;          // [rows, chunks, SCORE_NC] (key, token index)
+  uint2 *cand;          // [rows, chunks, SCORE_NC] (score bits, token index)
 };
 
 template <typename T, int D, bool WRITE_S, bool DO_V, bool SELECT>
@@ -84,6 +84,8 @@ __device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ 
                                             float2 *__restrict__ part_ml, float *__restrict__ part_o,
                                             const SelectArgs &sel, int N, int M, float scale, int chunk, int nchunks,
                                             int lmblock, int64_t bh, int only_lm) {
+  // Ks / Vt: two tile buffers each, K_ELEMS / V_ELEMS apart (Vt unused without DO_V)
+  using TD = TileDims<T, D>;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
   const int lm0 = (lmblock * 4 + w) * 16;
   const bool active = lm0 < M && (only_lm < 0 || (only_lm >= lm0 && only_lm < lm0 + 16));
@@ -100,68 +102,99 @@ __device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ 
     else
       qf[ks].zero();
   }
-  // keys >= plo are candidates; 0xffffffff (above every score key) lists nothing
-  const uint32_t plo = SELECT && lm < M ? sel.plo[row] : 0xffffffffu;
+  // SELECT: a score x is listed iff score_key(x) >= plo, i.e. x >= key_to_float(plo)
+  // for x not NaN (the key order is the float order with -0 == +0), and for
+  // NaN (ranked as -inf) iff the pivot is -inf. plo = 0xffffffff (no row)
+  // gives a NaN bound that lists nothing.
+  float piv = 0.f;
+  bool nan_in = false;
+  if (SELECT) {
+    const uint32_t plo = lm < M ? sel.plo[row] : 0xffffffffu;
+    piv = key_to_float(plo);
+    nan_in = plo == ordered_key(-INFINITY);
+  }
   const bool write_row = WRITE_S && lm < M && (only_lm < 0 || lm == only_lm);
   uint32_t listed = 0;  // SELECT: candidates of this landmark listed so far in the chunk
   Online<D> st;
   st.init();
   const float sl2 = scale * LOG2E;
   const int key_begin = chunk * SCORE_NC, key_end = min(N, key_begin + SCORE_NC);
-  for (int k0 = key_begin; k0 < key_end; k0 += TK) {
+  const int ntile = (key_end - key_begin + TK - 1) / TK;
+
+  // key tiles double-buffered in LDS: the next tile's loads are in flight
+  // while the current one is used, one barrier per tile
+  TileRegs<T, D, DO_V> R;
+  R.load(kb_ + (int64_t)key_begin * D, DO_V ? vb_ + (int64_t)key_begin * D : nullptr, nullptr,
+         min(TK, key_end - key_begin));
+  R.store(Ks, Vt);
+  __syncthreads();
+  for (int t = 0; t < ntile; ++t) {
+    const int buf = t & 1;
+    T *Kc = Ks + buf * TD::K_ELEMS, *Vc = DO_V ? Vt + buf * TD::V_ELEMS : Vt;
+    const int k0 = key_begin + t * TK;
     const int nvalid = min(TK, key_end - k0);
-    __syncthreads();
-    load_kv_tile<T, D, DO_V>(Ks, Vt, kb_ + (int64_t)k0 * D, DO_V ? vb_ + (int64_t)k0 * D : nullptr, nullptr, nvalid);
-    __syncthreads();
-    if (!active) continue;
-    f32x4 acc[4];
-    tile_scores<T, D>(acc, Ks, qf);
-    if (write_row) {
-      float *srow = S + row * (int64_t)N + k0;
+    if (t + 1 < ntile)
+      R.load(kb_ + (int64_t)(k0 + TK) * D, DO_V ? vb_ + (int64_t)(k0 + TK) * D : nullptr, nullptr,
+             min(TK, key_end - k0 - TK));
+    if (active) {
+      f32x4 acc[4];
+      tile_scores<T, D>(acc, Kc, qf);
+      if (write_row) {
+        float *srow = S + row * (int64_t)N + k0;
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        const int key = kb * 16 + 4 * g;
-        if (key + 3 < nvalid) {
-          *reinterpret_cast<float4 *>(srow + key) =
-              make_float4(acc[kb][0] * scale, acc[kb][1] * scale, acc[kb][2] * scale, acc[kb][3] * scale);
-        } else {
+        for (int kb = 0; kb < 4; ++kb) {
+          const int key = kb * 16 + 4 * g;
+          if (key + 3 < nvalid) {
+            *reinterpret_cast<float4 *>(srow + key) =
+                make_float4(acc[kb][0] * scale, acc[kb][1] * scale, acc[kb][2] * scale, acc[kb][3] * scale);
+          } else {
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (key + r < nvalid) srow[key + r] = acc[kb][r] * scale;
+            for (int r = 0; r < 4; ++r)
+              if (key + r < nvalid) srow[key + r] = acc[kb][r] * scale;
+          }
         }
       }
-    }
-    if (SELECT) {
-      uint32_t msk = 0, packed = 0;  // candidate bits (4 kb + r); per-kb counts in bytes
+      if (SELECT) {
+        float x[4][4];
+        uint32_t m[4], packed = 0;  // per-kb candidate bits (r); per-kb counts in bytes
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        uint32_t m = 0;
+        for (int kb = 0; kb < 4; ++kb) {
+          m[kb] = 0;
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (kb * 16 + 4 * g + r < nvalid && score_key(acc[kb][r] * scale) >= plo) m |= 1u << r;
-        msk |= m << (4 * kb);
-        packed |= (uint32_t)__popc(m) << (8 * kb);
+          for (int r = 0; r < 4; ++r) {
+            x[kb][r] = acc[kb][r] * scale;
+            const bool c = x[kb][r] >= piv || (nan_in && x[kb][r] != x[kb][r]);
+            if (c && kb * 16 + 4 * g + r < nvalid) m[kb] |= 1u << r;
+          }
+          packed |= (uint32_t)__popc(m[kb]) << (8 * kb);
+        }
+        // inclusive scan over the lane groups of landmark p (bytes stay below 17)
+        uint32_t incl = packed;
+        uint32_t y = (uint32_t)__shfl_up((int)incl, 16);
+        if (g >= 1) incl += y;
+        y = (uint32_t)__shfl_up((int)incl, 32);
+        if (g >= 2) incl += y;
+        const uint32_t tot = (uint32_t)__shfl((int)incl, 48 + p);  // per-kb totals of the landmark
+        // byte kb of pos: candidates of the landmark before this lane's block kb
+        const uint32_t pos = (incl - packed) + (tot << 8) + (tot << 16) + (tot << 24);
+        uint2 *list = sel.cand + (row * nchunks + chunk) * (int64_t)SCORE_NC + listed;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) {
+          if (!__ballot(m[kb] != 0u)) continue;  // no candidate of this block in the wave
+          uint32_t at = (pos >> (8 * kb)) & 255u;
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (m[kb] & (1u << r)) {
+              list[at] = make_uint2(__float_as_uint(x[kb][r]), (uint32_t)(k0 + kb * 16 + 4 * g + r));
+              ++at;
+            }
+        }
+        listed += (tot * 0x01010101u) >> 24;
       }
-      // inclusive scan over the lane groups of landmark p (bytes stay below 17)
-      uint32_t incl = packed;
-      uint32_t y = (uint32_t)__shfl_up((int)incl, 16);
-      if (g >= 1) incl += y;
-      y = (uint32_t)__shfl_up((int)incl, 32);
-      if (g >= 2) incl += y;
-      const uint32_t tot = (uint32_t)__shfl((int)incl, 48 + p);  // per-kb totals of the landmark
-      // byte kb of pos: candidates of the landmark before this lane's block kb
-      uint32_t pos = (incl - packed) + (tot << 8) + (tot << 16) + (tot << 24);
-      uint2 *list = sel.cand + (row * nchunks + chunk) * (int64_t)SCORE_NC + listed;
-      while (msk) {
-        const int e = __builtin_ctz(msk);
-        msk &= msk - 1u;
-        const int kb = e >> 2, r = e & 3;
-        list[(pos >> (8 * kb)) & 255u] = make_uint2(score_key(acc[kb][r] * scale), (uint32_t)(k0 + kb * 16 + 4 * g + r));
-        pos += 1u << (8 * kb);
-      }
-      listed += (tot * 0x01010101u) >> 24;
+      if (DO_V) tile_softmax_pv<T, D>(st, acc, Vc, nvalid, sl2);
     }
-    if (DO_V) tile_softmax_pv<T, D>(st, acc, Vt, nvalid, sl2);
+    if (t + 1 < ntile) R.store(Ks + (buf ^ 1) * TD::K_ELEMS, DO_V ? Vt + (buf ^ 1) * TD::V_ELEMS : Vt);
+    __syncthreads();
   }
   if (SELECT && active && lm < M && g == 0) sel.ccnt[row * nchunks + chunk] = listed;
   if (!DO_V || !active) return;
@@ -182,10 +215,10 @@ __global__ __launch_bounds__(BLOCK) void scores_kernel(const T *__restrict__ q_l
                                                        float2 *__restrict__ part_ml, float *__restrict__ part_o,
                                                        SelectArgs sel, int N, int M, float scale) {
   using TD = TileDims<T, D>;
-  __shared__ __align__(16) T Ks[TD::K_ELEMS];
-  __shared__ __align__(16) T Vt[DO_V ? TD::V_ELEMS : 1];
-  score_chunk<T, D, WRITE_S, DO_V, SELECT>(Ks, Vt, q_lm, k, v, S, part_ml, part_o, sel, N, M, scale, blockIdx.x,
-                                           gridDim.x, blockIdx.y, blockIdx.z, -1);
+  __shared__ __align__(16) T Ks[2][TD::K_ELEMS];
+  __shared__ __align__(16) T Vt[DO_V ? 2 : 1][DO_V ? TD::V_ELEMS : 1];
+  score_chunk<T, D, WRITE_S, DO_V, SELECT>(&Ks[0][0], &Vt[0][0], q_lm, k, v, S, part_ml, part_o, sel, N, M, scale,
+                                           blockIdx.x, gridDim.x, blockIdx.y, blockIdx.z, -1);
 }
 
 // Score rows of listed landmark rows (fallback of the fused selection): work
@@ -197,15 +230,16 @@ __global__ __launch_bounds__(BLOCK) void scores_rows_kernel(const T *__restrict_
                                                             const int32_t *__restrict__ rows, int N, int M,
                                                             float scale, int nchunks) {
   using TD = TileDims<T, D>;
-  __shared__ __align__(16) T Ks[TD::K_ELEMS];
+  __shared__ __align__(16) T Ks[2][TD::K_ELEMS];
   const int64_t items = (int64_t)*nrows * nchunks;
   const SelectArgs none{nullptr, nullptr, nullptr};
   for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
     const int row = rows[it / nchunks];
     const int chunk = (int)(it % nchunks);
     const int lm = row % M;
-    score_chunk<T, D, true, false, false>(Ks, nullptr, q_lm, k, nullptr, S, nullptr, nullptr, none, N, M, scale,
-                                          chunk, nchunks, lm / 64, row / M, lm);
+    __syncthreads();  // the previous item's last reads of Ks are done
+    score_chunk<T, D, true, false, false>(&Ks[0][0], nullptr, q_lm, k, nullptr, S, nullptr, nullptr, none, N, M,
+                                          scale, chunk, nchunks, lm / 64, row / M, lm);
   }
 }
 

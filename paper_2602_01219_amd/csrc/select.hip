@@ -8,7 +8,7 @@
 //      key. r is chosen on the host so that at least k and far fewer than
 //      `cap` tokens of the row score >= pivot, except with negligible
 //      probability (r = k exactly when the sample is the whole row).
-//   3. the score pass lists every token scoring >= pivot (score key, token
+//   3. the score pass lists every token scoring >= pivot (score bits, token
 //      index), in token order, in one region per (row, key chunk).
 //   4. finalize_kernel: with k <= count <= cap the list holds the row's whole
 //      top-k, since every token left out scores below the pivot, which the
@@ -252,7 +252,8 @@ __global__ __launch_bounds__(256) void finalize_kernel(const uint2 *__restrict__
       else
         hi = mid - 1;
     }
-    lst[i] = cand[(row * nch + lo) * (int64_t)SCORE_NC + (i - (int)pre[lo])];
+    const uint2 e = cand[(row * nch + lo) * (int64_t)SCORE_NC + (i - (int)pre[lo])];
+    lst[i] = make_uint2(score_key(__uint_as_float(e.x)), e.y);  // listed as float bits
   }
   __syncthreads();
 
