@@ -173,6 +173,17 @@ template <typename T, int D, bool WITH_V = true> struct TileRegs {
       }
     }
   }
+  // a full tile: rows 0..63 all valid
+  __device__ __forceinline__ void load_full(const T *__restrict__ kb, const T *__restrict__ vb,
+                                            const int32_t *rowidx) {
+    const int r0 = row0(), ch = chunk();
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+      const int64_t src = rowidx ? (int64_t)rowidx[r0 + j] : (int64_t)(r0 + j);
+      k[j] = *reinterpret_cast<const uint4 *>(kb + src * D + ch * VE);
+      if (WITH_V) v[j] = *reinterpret_cast<const uint4 *>(vb + src * D + ch * VE);
+    }
+  }
   __device__ __forceinline__ void store(T *__restrict__ Ks, T *__restrict__ Vt) const {
     using TD = TileDims<T, D>;
     const int r0 = row0(), ch = chunk();

@@ -214,18 +214,42 @@ __global__ __launch_bounds__(1024) void worklist_kernel(const int32_t *__restric
 // ---------------------------------------------------------------------------
 // MiTA attention (Eq. mita with s = 1): each query attends, in one online
 // softmax, over the shared expert (keys q_lm, values v_lm; Eq. shared-expert)
-// and then over the k keys of its routed expert (Eq. mita-expert). Workgroup
-// = 64 queries of one expert (4 waves x 16), taken from the routing work list
+// and the k keys of its routed expert (Eq. mita-expert). Workgroup = 64
+// queries of one expert (4 waves x 16), taken from the routing work list
 // (Algorithm 1's varlen grouping); outputs are scattered back to token order.
 // With ROUTED, routed keys come from the expert tiles, or straight from the
-// K/V rows listed in idx (FUSED: the gather of Eq. gather done in place; the
-// expert's index list is staged in LDS first when it fits).
-// Key tiles are double-buffered in LDS: the next tile's global loads are in
-// flight while the current one is multiplied, one barrier per tile.
+// K/V rows listed in idx (FUSED: the gather of Eq. gather done in place; with
+// IDX_LDS the expert's index list is staged in LDS first).
+// The softmax is order-independent, so the full 64-key tiles (shared, then
+// routed) run first in a software-pipelined loop: tiles double-buffered in
+// LDS, the next tile's loads in flight while the current one is multiplied,
+// one barrier per tile, no masking. The partial tiles of either expert (when
+// M or k is not a multiple of 64) follow, masked.
+// Work-list tiles are spread so that consecutive tiles (usually of the same
+// expert) run on the same XCD and share its L2: with 8 XCDs taking workgroups
+// round robin, x -> (xcd = x % 8, slot = x / 8) covers tile xcd * C + slot,
+// C = ceil(tiles / 8); the grid's x extent is a multiple of 8.
 // ---------------------------------------------------------------------------
-constexpr int IDX_LDS = 1024;  // expert index lists up to this length are staged in LDS
+constexpr int NXCD = 8;
 
-template <typename T, int D, bool SHARED, bool ROUTED, bool FUSED>
+// Full tile i of the key sequence: shared rows first (nA tiles), then routed
+// ones, in place through the expert's index list (FUSED) or from its tile.
+template <typename T, int D, bool FUSED>
+__device__ __forceinline__ void load_full_tile(TileRegs<T, D> &R, int i, int nA, const T *__restrict__ sh_k,
+                                               const T *__restrict__ sh_v, const T *__restrict__ rk,
+                                               const T *__restrict__ rv, const int32_t *__restrict__ ridx) {
+  if (i < nA) {
+    R.load_full(sh_k + (int64_t)i * TK * D, sh_v + (int64_t)i * TK * D, nullptr);
+  } else {
+    const int u = i - nA;
+    if (FUSED)
+      R.load_full(rk, rv, ridx + u * TK);
+    else
+      R.load_full(rk + (int64_t)u * TK * D, rv + (int64_t)u * TK * D, nullptr);
+  }
+}
+
+template <typename T, int D, bool SHARED, bool ROUTED, bool FUSED, bool IDX_LDS>
 __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
                                                        const T *__restrict__ v_lm, const T *__restrict__ rk,
                                                        const T *__restrict__ rv, const int32_t *__restrict__ idx,
@@ -236,15 +260,18 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
   using TD = TileDims<T, D>;
   __shared__ __align__(16) T Ks[2][TD::K_ELEMS];
   __shared__ __align__(16) T Vt[2][TD::V_ELEMS];
-  __shared__ int32_t sidx[FUSED ? IDX_LDS : 1];
-  const int t = blockIdx.x;
+  extern __shared__ int32_t sidx[];  // k entries with FUSED && IDX_LDS
   const int64_t bh = blockIdx.y;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
 
   int e = 0, q_begin, q_end;
   if (ROUTED) {
     const int32_t *ts = tile_start + bh * (M + 1);
-    if (t >= ts[M]) return;  // uniform for the workgroup
+    const int ntl = ts[M];
+    const int C = (ntl + NXCD - 1) / NXCD;
+    const int slot = (int)blockIdx.x / NXCD;
+    const int t = ((int)blockIdx.x % NXCD) * C + slot;
+    if (slot >= C || t >= ntl) return;  // uniform for the workgroup
     int lo = 0, hi = M - 1;  // largest e with ts[e] <= t
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
@@ -258,46 +285,31 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
     q_begin = of[e] + (t - ts[e]) * ATT_TQ;
     q_end = min(of[e + 1], q_begin + ATT_TQ);
   } else {
-    q_begin = t * ATT_TQ;
+    q_begin = (int)blockIdx.x * ATT_TQ;
+    if (q_begin >= N) return;
     q_end = min(N, q_begin + ATT_TQ);
   }
 
-  // key tiles: shared ones first, then routed ones
-  const int nA = SHARED ? (M + TK - 1) / TK : 0;
-  const int nB = ROUTED ? (k + TK - 1) / TK : 0;
-  const int ntile = nA + nB;
-  const int32_t *gidx = FUSED ? idx + (bh * M + e) * (int64_t)k : nullptr;
-  const bool idx_in_lds = FUSED && k <= IDX_LDS;
-  if (idx_in_lds) {
+  // full tiles: nA shared, then nB routed; partial ones: pA shared rows, pB routed rows
+  const int nA = SHARED ? M / TK : 0, pA = SHARED ? M % TK : 0;
+  const int nB = ROUTED ? k / TK : 0, pB = ROUTED ? k % TK : 0;
+  const int nfull = nA + nB;
+  const T *sh_k = q_lm + bh * (int64_t)M * D, *sh_v = v_lm + bh * (int64_t)M * D;
+  const T *rkb, *rvb;
+  const int32_t *gidx = nullptr;
+  if (FUSED) {
+    rkb = rk + bh * (int64_t)N * D;
+    rvb = rv + bh * (int64_t)N * D;
+    gidx = idx + (bh * M + e) * (int64_t)k;
+  } else {
+    rkb = rk + (bh * M + e) * (int64_t)k * D;
+    rvb = rv + (bh * M + e) * (int64_t)k * D;
+  }
+  if (FUSED && IDX_LDS) {
     for (int i = threadIdx.x; i < k; i += BLOCK) sidx[i] = gidx[i];
     __syncthreads();
   }
-  // source of key tile i: K/V row bases, optional row list, valid rows
-  const T *kb_i, *vb_i;
-  const int32_t *ri_i;
-  int nr_i;
-  auto tile_src = [&](int i) {
-    if (SHARED && i < nA) {
-      const int64_t off = (bh * M + (int64_t)i * TK) * D;
-      kb_i = q_lm + off;
-      vb_i = v_lm + off;
-      ri_i = nullptr;
-      nr_i = min(TK, M - i * TK);
-    } else {
-      const int u = i - nA;
-      nr_i = min(TK, k - u * TK);
-      if (FUSED) {
-        kb_i = rk + bh * (int64_t)N * D;
-        vb_i = rv + bh * (int64_t)N * D;
-        ri_i = idx_in_lds ? sidx + u * TK : gidx + u * TK;
-      } else {
-        const int64_t off = ((bh * M + e) * (int64_t)k + (int64_t)u * TK) * D;
-        kb_i = rk + off;
-        vb_i = rv + off;
-        ri_i = nullptr;
-      }
-    }
-  };
+  const int32_t *ridx = IDX_LDS ? sidx : gidx;  // the routed tiles' row list (FUSED)
 
   const int qi = q_begin + w * 16 + p;
   const bool qvalid = qi < q_end;
@@ -315,28 +327,39 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
   const float sl2 = scale * LOG2E;
 
   TileRegs<T, D> R;
-  tile_src(0);
-  R.load(kb_i, vb_i, ri_i, nr_i);
-  R.store(Ks[0], Vt[0]);
+  if (nfull > 0) {
+    load_full_tile<T, D, FUSED>(R, 0, nA, sh_k, sh_v, rkb, rvb, ridx);
+    R.store(Ks[0], Vt[0]);
+  }
   __syncthreads();
-  int nvalid = nr_i;
-  for (int i = 0; i < ntile; ++i) {
+  for (int i = 0; i < nfull; ++i) {
     const int buf = i & 1;
-    const int nv = nvalid;
-    if (i + 1 < ntile) {
-      tile_src(i + 1);
-      R.load(kb_i, vb_i, ri_i, nr_i);
-      nvalid = nr_i;
-    }
+    if (i + 1 < nfull) load_full_tile<T, D, FUSED>(R, i + 1, nA, sh_k, sh_v, rkb, rvb, ridx);
     f32x4 acc[4];
     tile_scores<T, D>(acc, Ks[buf], qf);
-    if (nv == TK)
-      tile_softmax_pv<T, D, false>(st, acc, Vt[buf], TK, sl2);
-    else
-      tile_softmax_pv<T, D, true>(st, acc, Vt[buf], nv, sl2);
-    if (i + 1 < ntile) R.store(Ks[buf ^ 1], Vt[buf ^ 1]);
+    tile_softmax_pv<T, D, false>(st, acc, Vt[buf], TK, sl2);
+    if (i + 1 < nfull) R.store(Ks[buf ^ 1], Vt[buf ^ 1]);
     __syncthreads();
   }
+  // partial tiles (masked)
+  for (int part = 0; part < 2; ++part) {
+    const int nr = part == 0 ? pA : pB;
+    if (nr == 0) continue;  // uniform
+    if (part == 0) {
+      R.load(sh_k + (int64_t)nA * TK * D, sh_v + (int64_t)nA * TK * D, nullptr, nr);
+    } else if (FUSED) {
+      R.load(rkb, rvb, ridx + nB * TK, nr);
+    } else {
+      R.load(rkb + (int64_t)nB * TK * D, rvb + (int64_t)nB * TK * D, nullptr, nr);
+    }
+    R.store(Ks[0], Vt[0]);
+    __syncthreads();
+    f32x4 acc[4];
+    tile_scores<T, D>(acc, Ks[0], qf);
+    tile_softmax_pv<T, D, true>(st, acc, Vt[0], nr, sl2);
+    __syncthreads();
+  }
+
   const float l = column_sum(st.l);
   if (!qvalid) return;
   const float inv = 1.0f / l;
@@ -392,15 +415,27 @@ hipError_t launch_worklist(const mita_cfg_t &c, const int32_t *offsets, int32_t 
   return hipGetLastError();
 }
 
+constexpr int IDX_LDS_MAX = 4096;  // expert index lists up to this length are staged in LDS
+
 template <typename T, int D, bool SH, bool RT, bool FU>
 static hipError_t attend_t3(const mita_cfg_t &c, const void *q, const void *q_lm, const void *v_lm, const void *rk,
                             const void *rv, const int32_t *idx, const int32_t *perm, const int32_t *offsets,
                             const int32_t *tile_start, void *o, hipStream_t st) {
-  // routed: at most ceil(N/64) + M tiles (each expert adds at most one partial tile)
-  const int tiles = RT ? (c.N + ATT_TQ - 1) / ATT_TQ + c.M : (c.N + ATT_TQ - 1) / ATT_TQ;
-  hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU>), dim3(tiles, (unsigned)BH(c)), dim3(BLOCK), 0, st,
-                     (const T *)q, (const T *)q_lm, (const T *)v_lm, (const T *)rk, (const T *)rv, idx, perm, offsets,
-                     tile_start, (T *)o, c.N, c.M, c.k, eff_scale(c));
+  // routed: at most ceil(N/64) + M tiles (each expert adds at most one partial
+  // tile), rounded up to a multiple of the XCD count for the tile spreading
+  int tiles = (c.N + ATT_TQ - 1) / ATT_TQ;
+  if (RT) tiles = (tiles + c.M + NXCD - 1) / NXCD * NXCD;
+  const dim3 grid((unsigned)tiles, (unsigned)BH(c));
+  const bool in_lds = FU && c.k <= IDX_LDS_MAX;
+  const size_t lds = in_lds ? (size_t)c.k * sizeof(int32_t) : 0;
+  if (in_lds)
+    hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU, true>), grid, dim3(BLOCK), lds, st, (const T *)q,
+                       (const T *)q_lm, (const T *)v_lm, (const T *)rk, (const T *)rv, idx, perm, offsets, tile_start,
+                       (T *)o, c.N, c.M, c.k, eff_scale(c));
+  else
+    hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU, false>), grid, dim3(BLOCK), 0, st, (const T *)q,
+                       (const T *)q_lm, (const T *)v_lm, (const T *)rk, (const T *)rv, idx, perm, offsets, tile_start,
+                       (T *)o, c.N, c.M, c.k, eff_scale(c));
   return hipGetLastError();
 }
 
