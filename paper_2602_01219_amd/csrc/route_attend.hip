@@ -8,78 +8,112 @@ namespace mita {
 
 // ---------------------------------------------------------------------------
 // Routing logits and argmax (Sec. 3.2: logits Q^T Q_lm, rank-1 expert;
-// Algorithm 1 ArgMax). Workgroup = 4 waves x 16 queries = one 64-query tile.
-// Each wave forms L^T = Q_lm Q^T on MFMA one 16-landmark block at a time and
-// keeps a lane-local running (max, argmax) with strict '>' in increasing
-// landmark order, then merges the four lane groups preferring the lower
-// landmark on equal values. Also counts the tile's queries per expert and
-// adds them to the per-expert totals (zeroed beforehand).
+// Algorithm 1 ArgMax). Workgroup = 4 waves, wave = one 64-query routing tile
+// (4 column groups of 16 queries). The landmarks are staged in LDS 64 at a
+// time; each wave forms L^T = Q_lm Q^T on MFMA one 16-landmark block at a
+// time, every landmark fragment serving its 4 query groups, and keeps a
+// lane-local running (max, argmax) with strict '>' in increasing landmark
+// order, then merges the four lane groups of each query column preferring
+// the lower landmark on equal values. Each wave also counts its tile's
+// queries per expert and adds them to the per-expert totals (zeroed
+// beforehand).
 // ---------------------------------------------------------------------------
+constexpr int ROUTE_LB = 64;  // landmarks staged in LDS per step
+
 template <typename T, int D>
 __global__ __launch_bounds__(BLOCK) void route_logits_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
                                                              int32_t *__restrict__ expert,
                                                              int32_t *__restrict__ tile_cnt,
                                                              int32_t *__restrict__ counts, int N, int M,
-                                                             float scale) {
-  extern __shared__ uint32_t cnt[];  // [M]
-  const int tile = blockIdx.x, ntiles = gridDim.x;
+                                                             float scale, int ntiles) {
+  constexpr int VE = 16 / (int)sizeof(T);
+  constexpr int LSTR = D + VE;  // padded landmark row (elements)
+  __shared__ __align__(16) T lms[ROUTE_LB * LSTR];
+  extern __shared__ uint32_t cnt[];  // [4][M]
   const int64_t bh = blockIdx.y;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
-  for (int i = threadIdx.x; i < M; i += BLOCK) cnt[i] = 0u;
-  const int n = tile * ROUTE_TQ + w * 16 + p;
-  Frag<T> qf[D / 32];
+  const int tile = (int)blockIdx.x * 4 + w;
+  uint32_t *wc = cnt + w * M;
+  for (int i = lane; i < M; i += 64) wc[i] = 0u;
+  Frag<T> qf[4][D / 32];
 #pragma unroll
-  for (int ks = 0; ks < D / 32; ++ks) {
-    if (n < N)
-      qf[ks].load(q + (bh * N + n) * D + ks * 32 + g * 8);
-    else
-      qf[ks].zero();
-  }
-  const T *lmb = q_lm + bh * (int64_t)M * D;
-  float best = -INFINITY;
-  int arg = 0;
-  for (int m0 = 0; m0 < M; m0 += 16) {
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int mrow = m0 + p;
+  for (int c = 0; c < 4; ++c) {
+    const int n = tile * ROUTE_TQ + c * 16 + p;
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks) {
-      Frag<T> a;
-      if (mrow < M)
-        a.load(lmb + (int64_t)mrow * D + ks * 32 + g * 8);
+      if (n < N)
+        qf[c][ks].load(q + (bh * N + n) * D + ks * 32 + g * 8);
       else
-        a.zero();
-      acc = mma(a, qf[ks], acc);
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int lmi = m0 + 4 * g + r;
-      const float val = acc[r] * scale;
-      if (lmi < M && val > best) {
-        best = val;
-        arg = lmi;
-      }
+        qf[c][ks].zero();
     }
   }
+  const T *lmb = q_lm + bh * (int64_t)M * D;
+  float best[4];
+  int arg[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    best[c] = -INFINITY;
+    arg[c] = 0;
+  }
+  for (int l0 = 0; l0 < M; l0 += ROUTE_LB) {
+    const int nl = min(ROUTE_LB, M - l0);
+    __syncthreads();
+    for (int ch = threadIdx.x; ch < ROUTE_LB * (D / VE); ch += BLOCK) {
+      const int r = ch / (D / VE), cc = ch % (D / VE);
+      uint4 x = make_uint4(0, 0, 0, 0);
+      if (r < nl) x = *reinterpret_cast<const uint4 *>(lmb + (int64_t)(l0 + r) * D + cc * VE);
+      *reinterpret_cast<uint4 *>(lms + r * LSTR + cc * VE) = x;
+    }
+    __syncthreads();
+    if (tile >= ntiles) continue;
+    for (int sb = 0; sb < nl; sb += 16) {
+      f32x4 acc[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) {
+        Frag<T> a;
+        a.load(lms + (sb + p) * LSTR + ks * 32 + g * 8);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[c] = mma(a, qf[c][ks], acc[c]);
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int lmi = l0 + sb + 4 * g + r;
+          const float val = acc[c][r] * scale;
+          if (lmi < M && val > best[c]) {
+            best[c] = val;
+            arg[c] = lmi;
+          }
+        }
+    }
+  }
+  if (tile >= ntiles) return;  // no workgroup barriers below
   // merge the four lane groups of each query column (lower landmark wins ties)
 #pragma unroll
-  for (int o = 16; o <= 32; o <<= 1) {
-    const float ob = __shfl_xor(best, o);
-    const int oa = __shfl_xor(arg, o);
-    if (ob > best || (ob == best && oa < arg)) {
-      best = ob;
-      arg = oa;
+  for (int c = 0; c < 4; ++c) {
+#pragma unroll
+    for (int o = 16; o <= 32; o <<= 1) {
+      const float ob = __shfl_xor(best[c], o);
+      const int oa = __shfl_xor(arg[c], o);
+      if (ob > best[c] || (ob == best[c] && oa < arg[c])) {
+        best[c] = ob;
+        arg[c] = oa;
+      }
+    }
+    const int n = tile * ROUTE_TQ + c * 16 + p;
+    if (g == 0 && n < N) {
+      expert[bh * N + n] = arg[c];
+      atomicAdd(&wc[arg[c]], 1u);
     }
   }
-  __syncthreads();
-  if (g == 0 && n < N) {
-    expert[bh * N + n] = arg;
-    atomicAdd(&cnt[arg], 1u);
-  }
-  __syncthreads();
   int32_t *tc = tile_cnt + (bh * ntiles + tile) * (int64_t)M;
-  for (int i = threadIdx.x; i < M; i += BLOCK) {
-    tc[i] = (int32_t)cnt[i];
-    if (cnt[i]) atomicAdd(&counts[bh * M + i], (int32_t)cnt[i]);  // integer sums: order-independent
+  for (int i = lane; i < M; i += 64) {
+    const uint32_t x = wc[i];
+    tc[i] = (int32_t)x;
+    if (x) atomicAdd(&counts[bh * M + i], (int32_t)x);  // integer sums: order-independent
   }
 }
 
@@ -386,8 +420,8 @@ static hipError_t route_t(const mita_cfg_t &c, const void *q, const void *q_lm, 
                           int32_t *tile_start, hipStream_t st) {
   const int nt = route_tiles(c);
   const unsigned bh = (unsigned)BH(c);
-  hipLaunchKernelGGL((route_logits_kernel<T, D>), dim3(nt, bh), dim3(BLOCK), c.M * sizeof(uint32_t), st,
-                     (const T *)q, (const T *)q_lm, expert, tile_cnt, counts, c.N, c.M, eff_scale(c));
+  hipLaunchKernelGGL((route_logits_kernel<T, D>), dim3((nt + 3) / 4, bh), dim3(BLOCK), 4 * c.M * sizeof(uint32_t),
+                     st, (const T *)q, (const T *)q_lm, expert, tile_cnt, counts, c.N, c.M, eff_scale(c), nt);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(route_scan_kernel, dim3(c.M, bh), dim3(256), 0, st, tile_cnt, counts, tile_base, offsets,
