@@ -26,34 +26,32 @@ template <typename T, int D> struct TileDims {
   static constexpr int VSTR = TK + 4;
   static constexpr int K_ELEMS = TK * KSTR;
   static constexpr int V_ELEMS = D * VSTR;
+  // bf16, d = 64: key column c of V^T row R sits at c ^ (8 * ((R >> 4) & 3)).
+  // The transposing stores of a tile (8 chunks of 8 rows, 2-key words) then
+  // fall in 32 distinct banks instead of 8, and the P V fragment reads (16
+  // consecutive rows, one XOR value) stay conflict-free and 8-byte contiguous.
+  static constexpr bool VSWZ = sizeof(T) == 2 && D == 64;
+  __device__ __forceinline__ static int vcol(int row, int col) { return VSWZ ? col ^ (8 * ((row >> 4) & 3)) : col; }
 };
 
-// Cooperative load of up to 64 key/value rows into LDS: Ks row-major [64][D],
-// Vt transposed [D][64]. Rows >= nrows are zero-filled (masked keys must
-// contribute exact zeros to P V). Row r comes from row (rowidx ? rowidx[r] : r)
-// of kbase / vbase. LOAD_V = false stages keys only.
-template <typename T, int D, bool LOAD_V = true>
-__device__ __forceinline__ void load_kv_tile(T *__restrict__ Ks, T *__restrict__ Vt, const T *__restrict__ kbase,
-                                             const T *__restrict__ vbase, const int32_t *__restrict__ rowidx,
-                                             int nrows) {
+// Cooperative load of up to 64 key rows into LDS, Ks row-major [64][D]. Rows
+// >= nrows are zero-filled. Row r comes from row (rowidx ? rowidx[r] : r) of
+// kbase.
+template <typename T, int D>
+__device__ __forceinline__ void load_k_tile(T *__restrict__ Ks, const T *__restrict__ kbase,
+                                            const int32_t *__restrict__ rowidx, int nrows) {
   using TD = TileDims<T, D>;
   constexpr int VE = TD::VE;
   constexpr int CPR = D / VE;
 #pragma unroll
   for (int c = threadIdx.x; c < TK * CPR; c += BLOCK) {
     const int r = c / CPR, ch = c % CPR;
-    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+    uint4 kv = make_uint4(0, 0, 0, 0);
     if (r < nrows) {
       const int64_t src = rowidx ? (int64_t)rowidx[r] : (int64_t)r;
       kv = *reinterpret_cast<const uint4 *>(kbase + src * D + ch * VE);
-      if (LOAD_V) vv = *reinterpret_cast<const uint4 *>(vbase + src * D + ch * VE);
     }
     *reinterpret_cast<uint4 *>(Ks + r * TD::KSTR + ch * VE) = kv;
-    if (LOAD_V) {
-      const T *ve = reinterpret_cast<const T *>(&vv);
-#pragma unroll
-      for (int e = 0; e < VE; ++e) Vt[(ch * VE + e) * TD::VSTR + r] = ve[e];
-    }
   }
 }
 
@@ -136,9 +134,10 @@ __device__ __forceinline__ void tile_softmax_pv(Online<D> &st, const f32x4 (&acc
     b.from_f32(pv);
 #pragma unroll
     for (int db = 0; db < D / 16; ++db) {
-      const T *row = Vt + (db * 16 + p) * TD::VSTR + 32 * j + 4 * g;
+      const int vr = db * 16 + p, c = TD::vcol(vr, 32 * j + 4 * g);
+      const T *row = Vt + vr * TD::VSTR;
       Frag<T> a;
-      a.load2x4(row, row + 16);
+      a.load2x4(row + c, row + (c ^ 16));
       st.o[db] = mma(a, b, st.o[db]);
     }
   }
@@ -154,7 +153,28 @@ template <typename T, int D, bool WITH_V = true> struct TileRegs {
   static constexpr int VE = 16 / (int)sizeof(T);
   static constexpr int CPR = D / VE;           // 16-byte chunks per row
   static constexpr int CH = TK * CPR / BLOCK;  // rows per thread
-  uint4 k[CH], v[WITH_V ? CH : 1];
+  // the CH 16-byte chunks of K (and V) as one vector value each, so the
+  // compiler keeps them in registers (arrays of them could end up in scratch)
+  typedef uint32_t vec_t __attribute__((ext_vector_type(4 * CH)));
+  vec_t kq, vq;
+  __device__ __forceinline__ uint4 kget(int j) const {
+    return make_uint4(kq[4 * j], kq[4 * j + 1], kq[4 * j + 2], kq[4 * j + 3]);
+  }
+  __device__ __forceinline__ uint4 vget(int j) const {
+    return make_uint4(vq[4 * j], vq[4 * j + 1], vq[4 * j + 2], vq[4 * j + 3]);
+  }
+  __device__ __forceinline__ void kset(int j, uint4 x) {
+    kq[4 * j] = x.x;
+    kq[4 * j + 1] = x.y;
+    kq[4 * j + 2] = x.z;
+    kq[4 * j + 3] = x.w;
+  }
+  __device__ __forceinline__ void vset(int j, uint4 x) {
+    vq[4 * j] = x.x;
+    vq[4 * j + 1] = x.y;
+    vq[4 * j + 2] = x.z;
+    vq[4 * j + 3] = x.w;
+  }
   __device__ __forceinline__ int row0() const { return CH * ((int)threadIdx.x / CPR); }
   __device__ __forceinline__ int chunk() const { return (int)threadIdx.x % CPR; }
   // row r of the tile is source row (rowidx ? rowidx[r] : r); rows >= nrows load zeros
@@ -164,13 +184,14 @@ template <typename T, int D, bool WITH_V = true> struct TileRegs {
 #pragma unroll
     for (int j = 0; j < CH; ++j) {
       const int r = r0 + j;
-      k[j] = make_uint4(0, 0, 0, 0);
-      if (WITH_V) v[j] = make_uint4(0, 0, 0, 0);
+      uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
       if (r < nrows) {
         const int64_t src = rowidx ? (int64_t)rowidx[r] : (int64_t)r;
-        k[j] = *reinterpret_cast<const uint4 *>(kb + src * D + ch * VE);
-        if (WITH_V) v[j] = *reinterpret_cast<const uint4 *>(vb + src * D + ch * VE);
+        a = *reinterpret_cast<const uint4 *>(kb + src * D + ch * VE);
+        if (WITH_V) b = *reinterpret_cast<const uint4 *>(vb + src * D + ch * VE);
       }
+      kset(j, a);
+      if (WITH_V) vset(j, b);
     }
   }
   // a full tile: rows 0..63 all valid
@@ -180,36 +201,42 @@ template <typename T, int D, bool WITH_V = true> struct TileRegs {
 #pragma unroll
     for (int j = 0; j < CH; ++j) {
       const int64_t src = rowidx ? (int64_t)rowidx[r0 + j] : (int64_t)(r0 + j);
-      k[j] = *reinterpret_cast<const uint4 *>(kb + src * D + ch * VE);
-      if (WITH_V) v[j] = *reinterpret_cast<const uint4 *>(vb + src * D + ch * VE);
+      kset(j, *reinterpret_cast<const uint4 *>(kb + src * D + ch * VE));
+      if (WITH_V) vset(j, *reinterpret_cast<const uint4 *>(vb + src * D + ch * VE));
     }
   }
   __device__ __forceinline__ void store(T *__restrict__ Ks, T *__restrict__ Vt) const {
     using TD = TileDims<T, D>;
     const int r0 = row0(), ch = chunk();
 #pragma unroll
-    for (int j = 0; j < CH; ++j) *reinterpret_cast<uint4 *>(Ks + (r0 + j) * TD::KSTR + ch * VE) = k[j];
-    if constexpr (WITH_V) store_vt(Vt + (ch * VE) * TD::VSTR + r0);
+    for (int j = 0; j < CH; ++j) *reinterpret_cast<uint4 *>(Ks + (r0 + j) * TD::KSTR + ch * VE) = kget(j);
+    if constexpr (WITH_V) store_vt(Vt, ch * VE, r0);
   }
-  // V^T: dimension ch*VE + e, keys r0 .. r0+CH-1
-  __device__ __forceinline__ void store_vt(T *__restrict__ dst) const;
+  // V^T rows row .. row+VE-1 (one 8-aligned group, so one swizzle), keys r0 .. r0+CH-1
+  __device__ __forceinline__ void store_vt(T *__restrict__ Vt, int row, int r0) const;
 };
 
-template <> __device__ __forceinline__ void TileRegs<bf16_t, 64, true>::store_vt(bf16_t *__restrict__ dst) const {
+template <> __device__ __forceinline__ void TileRegs<bf16_t, 64, true>::store_vt(bf16_t *__restrict__ Vt, int row,
+                                                                               int r0) const {
   // CH = 2: keys r0, r0+1 of dims 2m, 2m+1 from the two rows' words m
   using TD = TileDims<bf16_t, 64>;
-  const uint32_t r0w[4] = {v[0].x, v[0].y, v[0].z, v[0].w}, r1w[4] = {v[1].x, v[1].y, v[1].z, v[1].w};
+  bf16_t *dst = Vt + row * TD::VSTR + TD::vcol(row, r0);
+  const uint4 v0 = vget(0), v1 = vget(1);
+  const uint32_t r0w[4] = {v0.x, v0.y, v0.z, v0.w}, r1w[4] = {v1.x, v1.y, v1.z, v1.w};
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
     *reinterpret_cast<uint32_t *>(dst + (2 * m) * TD::VSTR) = __builtin_amdgcn_perm(r1w[m], r0w[m], 0x05040100u);
     *reinterpret_cast<uint32_t *>(dst + (2 * m + 1) * TD::VSTR) = __builtin_amdgcn_perm(r1w[m], r0w[m], 0x07060302u);
   }
 }
-template <> __device__ __forceinline__ void TileRegs<bf16_t, 128, true>::store_vt(bf16_t *__restrict__ dst) const {
+template <> __device__ __forceinline__ void TileRegs<bf16_t, 128, true>::store_vt(bf16_t *__restrict__ Vt, int row,
+                                                                               int r0) const {
+  bf16_t *dst = Vt + row * TileDims<bf16_t, 128>::VSTR + r0;
   // CH = 4: keys r0 .. r0+3 of dims 2m, 2m+1 as one 8-byte word each
   using TD = TileDims<bf16_t, 128>;
-  const uint32_t w0[4] = {v[0].x, v[0].y, v[0].z, v[0].w}, w1[4] = {v[1].x, v[1].y, v[1].z, v[1].w};
-  const uint32_t w2[4] = {v[2].x, v[2].y, v[2].z, v[2].w}, w3[4] = {v[3].x, v[3].y, v[3].z, v[3].w};
+  const uint4 v0 = vget(0), v1 = vget(1), v2 = vget(2), v3 = vget(3);
+  const uint32_t w0[4] = {v0.x, v0.y, v0.z, v0.w}, w1[4] = {v1.x, v1.y, v1.z, v1.w};
+  const uint32_t w2[4] = {v2.x, v2.y, v2.z, v2.w}, w3[4] = {v3.x, v3.y, v3.z, v3.w};
 #pragma unroll
   for (int m = 0; m < 4; ++m) {
     *reinterpret_cast<uint2 *>(dst + (2 * m) * TD::VSTR) =
@@ -218,23 +245,28 @@ template <> __device__ __forceinline__ void TileRegs<bf16_t, 128, true>::store_v
         make_uint2(__builtin_amdgcn_perm(w1[m], w0[m], 0x07060302u), __builtin_amdgcn_perm(w3[m], w2[m], 0x07060302u));
   }
 }
-template <> __device__ __forceinline__ void TileRegs<float, 64, true>::store_vt(float *__restrict__ dst) const {
+template <> __device__ __forceinline__ void TileRegs<float, 64, true>::store_vt(float *__restrict__ Vt, int row,
+                                                                               int r0) const {
+  float *dst = Vt + row * TileDims<float, 64>::VSTR + r0;
   // CH = 4: keys r0 .. r0+3 of each of the 4 dims as one 16-byte word
   using TD = TileDims<float, 64>;
-  const float *r[4] = {reinterpret_cast<const float *>(&v[0]), reinterpret_cast<const float *>(&v[1]),
-                       reinterpret_cast<const float *>(&v[2]), reinterpret_cast<const float *>(&v[3])};
+  // vq[4 j + e] = dim e of key r0 + j
 #pragma unroll
   for (int e = 0; e < 4; ++e)
-    *reinterpret_cast<float4 *>(dst + e * TD::VSTR) = make_float4(r[0][e], r[1][e], r[2][e], r[3][e]);
+    *reinterpret_cast<float4 *>(dst + e * TD::VSTR) =
+        make_float4(__uint_as_float(vq[e]), __uint_as_float(vq[4 + e]), __uint_as_float(vq[8 + e]),
+                    __uint_as_float(vq[12 + e]));
 }
-template <> __device__ __forceinline__ void TileRegs<float, 128, true>::store_vt(float *__restrict__ dst) const {
+template <> __device__ __forceinline__ void TileRegs<float, 128, true>::store_vt(float *__restrict__ Vt, int row,
+                                                                               int r0) const {
+  float *dst = Vt + row * TileDims<float, 128>::VSTR + r0;
   // CH = 8: keys r0 .. r0+7 of each of the 4 dims as two 16-byte words
   using TD = TileDims<float, 128>;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     float x[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) x[j] = reinterpret_cast<const float *>(&v[j])[e];
+    for (int j = 0; j < 8; ++j) x[j] = __uint_as_float(vq[4 * j + e]);
     *reinterpret_cast<float4 *>(dst + e * TD::VSTR) = make_float4(x[0], x[1], x[2], x[3]);
     *reinterpret_cast<float4 *>(dst + e * TD::VSTR + 4) = make_float4(x[4], x[5], x[6], x[7]);
   }

@@ -266,23 +266,6 @@ __global__ __launch_bounds__(1024) void worklist_kernel(const int32_t *__restric
 // ---------------------------------------------------------------------------
 constexpr int NXCD = 8;
 
-// Full tile i of the key sequence: shared rows first (nA tiles), then routed
-// ones, in place through the expert's index list (FUSED) or from its tile.
-template <typename T, int D, bool FUSED>
-__device__ __forceinline__ void load_full_tile(TileRegs<T, D> &R, int i, int nA, const T *__restrict__ sh_k,
-                                               const T *__restrict__ sh_v, const T *__restrict__ rk,
-                                               const T *__restrict__ rv, const int32_t *__restrict__ ridx) {
-  if (i < nA) {
-    R.load_full(sh_k + (int64_t)i * TK * D, sh_v + (int64_t)i * TK * D, nullptr);
-  } else {
-    const int u = i - nA;
-    if (FUSED)
-      R.load_full(rk, rv, ridx + u * TK);
-    else
-      R.load_full(rk + (int64_t)u * TK * D, rv + (int64_t)u * TK * D, nullptr);
-  }
-}
-
 template <typename T, int D, bool SHARED, bool ROUTED, bool FUSED, bool IDX_LDS>
 __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
                                                        const T *__restrict__ v_lm, const T *__restrict__ rk,
@@ -294,7 +277,7 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
   using TD = TileDims<T, D>;
   __shared__ __align__(16) T Ks[2][TD::K_ELEMS];
   __shared__ __align__(16) T Vt[2][TD::V_ELEMS];
-  extern __shared__ int32_t sidx[];  // k entries with FUSED && IDX_LDS
+  extern __shared__ int32_t sidx[];  // with IDX_LDS: M + k row indices
   const int64_t bh = blockIdx.y;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
 
@@ -339,11 +322,26 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
     rkb = rk + (bh * M + e) * (int64_t)k * D;
     rvb = rv + (bh * M + e) * (int64_t)k * D;
   }
-  if (FUSED && IDX_LDS) {
-    for (int i = threadIdx.x; i < k; i += BLOCK) sidx[i] = gidx[i];
+  // With IDX_LDS, one row list in LDS covers every key: entries [0, M) are
+  // the shared rows (identity), entries [M, M + k) the routed rows (the
+  // expert's index list, or identity into its tile). Every tile then loads
+  // through the same code, its base pointer picked by a scalar select.
+  const int32_t *rows = nullptr;
+  if (IDX_LDS) {
+    const int nsh = SHARED ? M : 0;
+    for (int i = threadIdx.x; i < nsh; i += BLOCK) sidx[i] = i;
+    if (ROUTED)
+      for (int i = threadIdx.x; i < k; i += BLOCK) sidx[nsh + i] = FUSED ? gidx[i] : i;
     __syncthreads();
+    rows = sidx;
   }
-  const int32_t *ridx = IDX_LDS ? sidx : gidx;  // the routed tiles' row list (FUSED)
+  const int rbase = SHARED ? M : 0;  // list offset of the routed rows
+  auto tile_base = [&](int i, const T *&kb, const T *&vb, int &off) {
+    const bool sh = i < nA;
+    kb = sh ? sh_k : rkb;
+    vb = sh ? sh_v : rvb;
+    off = sh ? i * TK : rbase + (i - nA) * TK;
+  };
 
   const int qi = q_begin + w * 16 + p;
   const bool qvalid = qi < q_end;
@@ -360,33 +358,70 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
   st.init();
   const float sl2 = scale * LOG2E;
 
-  TileRegs<T, D> R;
-  if (nfull > 0) {
-    load_full_tile<T, D, FUSED>(R, 0, nA, sh_k, sh_v, rkb, rvb, ridx);
-    R.store(Ks[0], Vt[0]);
-  }
-  __syncthreads();
-  for (int i = 0; i < nfull; ++i) {
-    const int buf = i & 1;
-    if (i + 1 < nfull) load_full_tile<T, D, FUSED>(R, i + 1, nA, sh_k, sh_v, rkb, rvb, ridx);
-    f32x4 acc[4];
-    tile_scores<T, D>(acc, Ks[buf], qf);
-    tile_softmax_pv<T, D, false>(st, acc, Vt[buf], TK, sl2);
-    if (i + 1 < nfull) R.store(Ks[buf ^ 1], Vt[buf ^ 1]);
+  TileRegs<T, D> Ra;
+  if (IDX_LDS) {
+    // one tile ahead: tile i + 1 is loaded into registers while tile i is
+    // multiplied, then stored to the other LDS buffer
+    const T *kb, *vb;
+    int off;
+    if (nfull > 0) {
+      tile_base(0, kb, vb, off);
+      Ra.load_full(kb, vb, rows + off);
+      Ra.store(Ks[0], Vt[0]);
+    }
     __syncthreads();
+    for (int i = 0; i < nfull; ++i) {
+      const int buf = i & 1;
+      if (i + 1 < nfull) {
+        tile_base(i + 1, kb, vb, off);
+        Ra.load_full(kb, vb, rows + off);
+      }
+      f32x4 acc[4];
+      tile_scores<T, D>(acc, Ks[buf], qf);
+      tile_softmax_pv<T, D, false>(st, acc, Vt[buf], TK, sl2);
+      if (i + 1 < nfull) Ra.store(Ks[buf ^ 1], Vt[buf ^ 1]);
+      __syncthreads();
+    }
+  } else {
+    // long index lists stay in memory: one register set, one tile ahead
+    for (int i = 0; i < nfull; ++i) {
+      if (i == 0) {
+        if (i < nA)
+          Ra.load_full(sh_k, sh_v, nullptr);
+        else
+          Ra.load_full(rkb, rvb, FUSED ? gidx : nullptr);
+        Ra.store(Ks[0], Vt[0]);
+        __syncthreads();
+      }
+      const int buf = i & 1;
+      if (i + 1 < nfull) {
+        const int j = i + 1;
+        if (j < nA)
+          Ra.load_full(sh_k + (int64_t)j * TK * D, sh_v + (int64_t)j * TK * D, nullptr);
+        else if (FUSED)
+          Ra.load_full(rkb, rvb, gidx + (j - nA) * TK);
+        else
+          Ra.load_full(rkb + (int64_t)(j - nA) * TK * D, rvb + (int64_t)(j - nA) * TK * D, nullptr);
+      }
+      f32x4 acc[4];
+      tile_scores<T, D>(acc, Ks[buf], qf);
+      tile_softmax_pv<T, D, false>(st, acc, Vt[buf], TK, sl2);
+      if (i + 1 < nfull) Ra.store(Ks[buf ^ 1], Vt[buf ^ 1]);
+      __syncthreads();
+    }
   }
   // partial tiles (masked)
   for (int part = 0; part < 2; ++part) {
     const int nr = part == 0 ? pA : pB;
     if (nr == 0) continue;  // uniform
     if (part == 0) {
-      R.load(sh_k + (int64_t)nA * TK * D, sh_v + (int64_t)nA * TK * D, nullptr, nr);
+      Ra.load(sh_k + (int64_t)nA * TK * D, sh_v + (int64_t)nA * TK * D, nullptr, nr);
     } else if (FUSED) {
-      R.load(rkb, rvb, ridx + nB * TK, nr);
+      Ra.load(rkb, rvb, IDX_LDS ? rows + rbase + nB * TK : gidx + nB * TK, nr);
     } else {
-      R.load(rkb + (int64_t)nB * TK * D, rvb + (int64_t)nB * TK * D, nullptr, nr);
+      Ra.load(rkb + (int64_t)nB * TK * D, rvb + (int64_t)nB * TK * D, nullptr, nr);
     }
-    R.store(Ks[0], Vt[0]);
+    Ra.store(Ks[0], Vt[0]);
     __syncthreads();
     f32x4 acc[4];
     tile_scores<T, D>(acc, Ks[0], qf);
@@ -449,7 +484,7 @@ hipError_t launch_worklist(const mita_cfg_t &c, const int32_t *offsets, int32_t 
   return hipGetLastError();
 }
 
-constexpr int IDX_LDS_MAX = 4096;  // expert index lists up to this length are staged in LDS
+constexpr int IDX_LDS_MAX = 8192;  // key row lists up to this length are staged in LDS
 
 template <typename T, int D, bool SH, bool RT, bool FU>
 static hipError_t attend_t3(const mita_cfg_t &c, const void *q, const void *q_lm, const void *v_lm, const void *rk,
@@ -460,8 +495,9 @@ static hipError_t attend_t3(const mita_cfg_t &c, const void *q, const void *q_lm
   int tiles = (c.N + ATT_TQ - 1) / ATT_TQ;
   if (RT) tiles = (tiles + c.M + NXCD - 1) / NXCD * NXCD;
   const dim3 grid((unsigned)tiles, (unsigned)BH(c));
-  const bool in_lds = FU && c.k <= IDX_LDS_MAX;
-  const size_t lds = in_lds ? (size_t)c.k * sizeof(int32_t) : 0;
+  const int nlist = (SH ? c.M : 0) + (RT ? c.k : 0);
+  const bool in_lds = nlist <= IDX_LDS_MAX;
+  const size_t lds = in_lds ? (size_t)nlist * sizeof(int32_t) : 0;
   if (in_lds)
     hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU, true>), grid, dim3(BLOCK), lds, st, (const T *)q,
                        (const T *)q_lm, (const T *)v_lm, (const T *)rk, (const T *)rv, idx, perm, offsets, tile_start,

@@ -106,7 +106,7 @@ __global__ __launch_bounds__(BLOCK) void sample_kernel(const T *__restrict__ q_l
     __syncthreads();
     if (threadIdx.x < TK) pos[threadIdx.x] = (int)threadIdx.x < nvalid ? sample_pos(j0 + threadIdx.x, N, ns) : 0;
     __syncthreads();
-    load_kv_tile<T, D, false>(Ks, nullptr, kb_, nullptr, pos, nvalid);
+    load_k_tile<T, D>(Ks, kb_, pos, nvalid);
     __syncthreads();
     if (lm0 >= M) continue;
     f32x4 acc[4];
