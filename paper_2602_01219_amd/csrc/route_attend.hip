@@ -148,57 +148,92 @@ __device__ __forceinline__ uint32_t block_sum256(uint32_t x, uint32_t *wsum) {
   return t;
 }
 
-// One workgroup per (expert e, b*h): offsets[e] = sum of the sizes of experts
-// before e (Algorithm 1 BinCount of the argmax and CumSum), the attention work
-// list tile_start[e] = sum of ceil(size / 64) before e, and, by an exclusive
-// scan over the routing tiles, where each tile's first query of expert e goes.
+// Offsets and scatter bases (Algorithm 1 BinCount of the argmax and CumSum).
+// One workgroup per (b*h, block of SCAN_EB experts): offsets[e] = sum of the
+// sizes of experts before e, the attention work list tile_start[e] = sum of
+// ceil(size / 64) before e, and tile_base[tile][e] = offsets[e] + the queries
+// of expert e in earlier routing tiles (an exclusive scan over tiles). 256
+// tiles at a time are staged in LDS as [tile][expert] (each thread reads its
+// tile's SCAN_EB consecutive counts); wave w then scans experts 4w .. 4w+3,
+// lane l taking tiles 4l .. 4l+3, and the bases go back through LDS so each
+// thread writes its tile's row.
+constexpr int SCAN_EB = 16;
+
 __global__ __launch_bounds__(256) void route_scan_kernel(const int32_t *__restrict__ tile_cnt,
                                                          const int32_t *__restrict__ counts,
                                                          int32_t *__restrict__ tile_base,
                                                          int32_t *__restrict__ offsets,
                                                          int32_t *__restrict__ tile_start, int ntiles, int M,
                                                          int N) {
+  __shared__ uint32_t cnt[256][SCAN_EB + 1];
   __shared__ uint32_t wsum[2][4];
-  const int e = blockIdx.x;
+  __shared__ uint32_t eoff[SCAN_EB];
+  const int e0 = blockIdx.x * SCAN_EB;
+  const int ne = min(SCAN_EB, M - e0);
   const int64_t bh = blockIdx.y;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int32_t *cn = counts + bh * M;
+
+  // exclusive prefixes of the expert sizes (and of their tile counts) at e0 .. e0+ne-1
   uint32_t a = 0, t = 0;
-  for (int i = tid; i < e; i += 256) {
+  for (int i = tid; i < e0; i += 256) {
     const uint32_t c = (uint32_t)cn[i];
     a += c;
     t += (c + ATT_TQ - 1) / ATT_TQ;
   }
-  const uint32_t off = block_sum256(a, wsum[0]);
-  const uint32_t ts = block_sum256(t, wsum[1]);
+  uint32_t off = block_sum256(a, wsum[0]);
+  uint32_t ts = block_sum256(t, wsum[1]);
   if (tid == 0) {
-    const uint32_t mine = (uint32_t)cn[e];
-    offsets[bh * (M + 1) + e] = (int32_t)off;
-    tile_start[bh * (M + 1) + e] = (int32_t)ts;
-    if (e == M - 1) {
-      offsets[bh * (M + 1) + M] = (int32_t)(off + mine);
-      tile_start[bh * (M + 1) + M] = (int32_t)(ts + (mine + ATT_TQ - 1) / ATT_TQ);
+    for (int j = 0; j < ne; ++j) {
+      const uint32_t c = (uint32_t)cn[e0 + j];
+      eoff[j] = off;
+      offsets[bh * (M + 1) + e0 + j] = (int32_t)off;
+      tile_start[bh * (M + 1) + e0 + j] = (int32_t)ts;
+      off += c;
+      ts += (c + ATT_TQ - 1) / ATT_TQ;
+    }
+    if (e0 + ne == M) {
+      offsets[bh * (M + 1) + M] = (int32_t)off;
+      tile_start[bh * (M + 1) + M] = (int32_t)ts;
     }
   }
-  const int32_t *tc = tile_cnt + bh * ntiles * (int64_t)M + e;
-  int32_t *tb = tile_base + bh * ntiles * (int64_t)M + e;
-  uint32_t run = off;
-  int par = 0;
+  __syncthreads();
+  // running totals of wave w's experts 4w .. 4w+3 over the tiles done so far
+  uint32_t carry[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) carry[q] = 4 * w + q < ne ? eoff[4 * w + q] : 0u;
+  const int32_t *tc = tile_cnt + bh * ntiles * (int64_t)M + e0;
+  int32_t *tb = tile_base + bh * ntiles * (int64_t)M + e0;
   for (int t0 = 0; t0 < ntiles; t0 += 256) {
     const int tt = t0 + tid;
-    const uint32_t c = tt < ntiles ? (uint32_t)tc[(int64_t)tt * M] : 0u;
-    const uint32_t incl = wave_inclusive_scan(c);
-    if (lane == 63) wsum[par][w] = incl;
-    __syncthreads();
-    uint32_t before = run + incl - c, tot = 0;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      before += i < w ? wsum[par][i] : 0u;
-      tot += wsum[par][i];
+    for (int j = 0; j < SCAN_EB; ++j) cnt[tid][j] = tt < ntiles && j < ne ? (uint32_t)tc[(int64_t)tt * M + j] : 0u;
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = 4 * w + q;
+      uint32_t v[4], part = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v[i] = cnt[4 * lane + i][j];
+        part += v[i];
+      }
+      const uint32_t incl = wave_inclusive_scan(part);
+      uint32_t run = carry[q] + incl - part;
+      carry[q] += (uint32_t)__shfl((int)incl, 63);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t c = v[i];
+        v[i] = run;
+        run += c;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) cnt[4 * lane + i][j] = v[i];  // only this wave touches column j
     }
-    if (tt < ntiles) tb[(int64_t)tt * M] = (int32_t)before;
-    run += tot;
-    par ^= 1;
+    __syncthreads();
+    if (tt < ntiles)
+      for (int j = 0; j < ne; ++j) tb[(int64_t)tt * M + j] = (int32_t)cnt[tid][j];
+    __syncthreads();
   }
 }
 
@@ -459,8 +494,8 @@ static hipError_t route_t(const mita_cfg_t &c, const void *q, const void *q_lm, 
                      st, (const T *)q, (const T *)q_lm, expert, tile_cnt, counts, c.N, c.M, eff_scale(c), nt);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(route_scan_kernel, dim3(c.M, bh), dim3(256), 0, st, tile_cnt, counts, tile_base, offsets,
-                     tile_start, nt, c.M, c.N);
+  hipLaunchKernelGGL(route_scan_kernel, dim3((c.M + SCAN_EB - 1) / SCAN_EB, bh), dim3(256), 0, st, tile_cnt, counts,
+                     tile_base, offsets, tile_start, nt, c.M, c.N);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   int ebits = 0;
   while ((1 << ebits) < c.M) ++ebits;

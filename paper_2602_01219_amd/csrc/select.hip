@@ -133,9 +133,13 @@ __global__ __launch_bounds__(BLOCK) void sample_kernel(const T *__restrict__ q_l
 
 // ---------------------------------------------------------------------------
 // Pivots: one wave per landmark row, its ns (<= SEL_NS) sampled keys in
-// registers; the r-th largest by radix rounds over a 256-bin LDS histogram of
-// the current key range (bins span (hi - lo + 1) / 256 keys, so each round
-// shrinks the range by 2^8 and at most 4 rounds run).
+// registers. Radix rounds over a 256-bin LDS histogram of the current key
+// range (bins span (hi - lo + 1) / 256 keys, so each round shrinks the range
+// by 2^8) narrow down on the r-th largest sample; after two rounds the lower
+// edge of the bin holding it is taken. That edge is at most the r-th largest
+// sample, so at least r samples are >= pivot, and its bin spans at most
+// 2^16 keys (a relative step of 2^-7 within one binade), which lists only a
+// few more tokens than the exact sample statistic would.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void pivot_kernel(const uint32_t *__restrict__ samp, uint32_t *__restrict__ plo,
                                                     int64_t rows, int ns, int r) {
@@ -174,7 +178,7 @@ __global__ __launch_bounds__(256) void pivot_kernel(const uint32_t *__restrict__
   }
   uint32_t lo = wave_min_u32(mn), hi = wave_max_u32(mx);
   uint32_t need = (uint32_t)r;
-  while (lo < hi) {
+  for (int round = 0; round < 2 && lo < hi; ++round) {
     const uint32_t span = hi - lo;
     const int bits = 32 - __clz((int)span);
     const int shift = bits > 8 ? bits - 8 : 0;
