@@ -140,7 +140,7 @@ def main():
 
     q, k, v = dev(inp.q), dev(inp.k), dev(inp.v)
     cfg = mita.Config.from_workload(wl, staged_gather=a.staged_gather, full_scores=a.full_scores)
-    fused = (not a.full_scores) and bool(wl.use_routed) and (wl.N <= 2048 or 4 * wl.k <= 4096)
+    fused = (not a.full_scores) and bool(wl.use_routed) and (wl.N <= 1024 or 4 * wl.k <= 4096)
     o = torch.empty_like(q)
     ws = torch.empty(mita.workspace_size(cfg), dtype=torch.uint8, device="cuda")
     eprint(f"[bench] workspace {ws.numel() / 2**20:.1f} MiB")

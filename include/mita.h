@@ -120,7 +120,7 @@ const char *mita_last_error(void);
  * only the scores above it, and the exact selection runs on that list. A row
  * whose list turns out too short or too long is recomputed in full and
  * selected exactly (see mita_forward_fallbacks). Without MITA_FLAG_FULL_SCORES
- * this applies when N <= 2048 or k <= 1024.
+ * this applies when N <= 1024 or k <= 1024.
  */
 int mita_forward(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, void *o,
                  void *ws, size_t ws_bytes, mita_stream_t stream);

@@ -17,7 +17,7 @@ constexpr int ATT_TQ = 64;     // queries per attention workgroup
 constexpr int ROUTE_TQ = 64;   // queries per routing tile (one wave)
 constexpr int SCORE_NC = 512;  // keys per score/landmark-value workgroup chunk
 // Top-k selection fused with the score pass of the forward.
-constexpr int SEL_NS = 2048;   // sampled keys per landmark row (pivot estimate)
+constexpr int SEL_NS = 1024;   // sampled keys per landmark row (pivot estimate)
 constexpr int SEL_CAP = 4096;  // most candidates the exact selection of one row takes
 constexpr int SAMPLE_NC = 64;  // sampled keys per sample-kernel workgroup
 
@@ -31,7 +31,7 @@ inline float eff_scale(const mita_cfg_t &c) { return c.scale != 0.f ? c.scale : 
 inline int sel_ns(const mita_cfg_t &c) { return c.N < SEL_NS ? c.N : SEL_NS; }
 // Does the forward select the top-k sets inside the score pass? Rows whose
 // sample covers the whole row always fit their list; otherwise the expected
-// list length, at most k + 5 sqrt(32 k) + 64 for N / ns <= 32, must stay well
+// list length, at most k + 5 sqrt(64 k) + 128 for N / ns <= 64, must stay
 // inside SEL_CAP, which k <= SEL_CAP / 4 ensures.
 inline bool fused_select(const mita_cfg_t &c) {
   return c.use_routed && !(c.flags & MITA_FLAG_FULL_SCORES) && (c.N <= SEL_NS || 4 * (int64_t)c.k <= SEL_CAP);

@@ -64,11 +64,11 @@ int main() {
   mita::FwdLayout L2 = mita::forward_layout(c);
   assert(L2.vx - L2.kx == (size_t)24 * 128 * 512 * 64 * 2);
   assert(mita::workspace_size(&c, MITA_WS_TOPK) == 0);
-  // fused selection: sample of 2048 keys, pivot rank 64 + 5 * sqrt(64 * 31 / 32) + 1
-  // -> 105 at N = 16384, k = 512; expected count bound (105 + 6 sqrt(105)) * 8 -> cap 2048
-  assert(mita::fused_select(c) && mita::sel_ns(c) == 2048 && mita::sel_cap(c) == 2048);
-  assert(mita::sel_rank(c) == 105);
-  assert(L2.plo - L2.samp == (size_t)24 * 128 * 2048 * 4);
+  // fused selection: sample of 1024 keys, pivot rank 32 + 5 * sqrt(32 * 31 / 32) + 1
+  // -> 61 at N = 16384, k = 512; expected count bound (61 + 6 sqrt(61)) * 16 -> cap 2048
+  assert(mita::fused_select(c) && mita::sel_ns(c) == 1024 && mita::sel_cap(c) == 2048);
+  assert(mita::sel_rank(c) == 61);
+  assert(L2.plo - L2.samp == (size_t)24 * 128 * 1024 * 4);
   assert(L2.cand - L2.ccnt == (size_t)24 * 128 * 32 * 4);
   assert(L2.fail - L2.cand == (size_t)24 * 128 * 32 * 512 * 8);
   assert(L2.total - L2.fail >= (size_t)(24 * 128 + 1) * 4);
@@ -77,10 +77,12 @@ int main() {
   c.flags = 0;
   c.k = 1025;
   assert(!mita::fused_select(c));
-  c.grid_h = 32; c.grid_w = 64; c.N = 2048; c.k = 2048;  // the sample is the whole row: rank = k
-  assert(mita::fused_select(c) && mita::sel_rank(c) == 2048 && mita::sel_cap(c) == 2048);
-  c.grid_h = 256; c.grid_w = 256; c.N = 65536; c.k = 1024;  // rank 62, bound (62 + 47) * 32 -> cap 4096
-  assert(mita::fused_select(c) && mita::sel_rank(c) == 62 && mita::sel_cap(c) == 4096);
+  c.grid_h = 32; c.grid_w = 32; c.N = 1024; c.k = 1024;  // the sample is the whole row: rank = k
+  assert(mita::fused_select(c) && mita::sel_rank(c) == 1024 && mita::sel_cap(c) == 1024);
+  c.grid_h = 32; c.grid_w = 64; c.N = 2048; c.k = 2048;  // 4 k above the list capacity: stored-S path
+  assert(!mita::fused_select(c));
+  c.grid_h = 256; c.grid_w = 256; c.N = 65536; c.k = 1024;  // rank 37, bound (37 + 36.5) * 64 -> cap 4096
+  assert(mita::fused_select(c) && mita::sel_rank(c) == 37 && mita::sel_cap(c) == 4096);
   c = base();
   c.d = 96;
   assert(mita::workspace_size(&c, MITA_WS_FORWARD) == 0);

@@ -395,12 +395,15 @@ def test_fused_selection_rows_beyond_the_list_fall_back():
     _fallback_case(K, cfg, q, v, expect_fb=cfg.M)
 
 
+SELECT_SAMPLE = 1024  # keys the forward samples per landmark row for its top-k pivot
+
+
 def test_fused_selection_unrepresentative_sample_falls_back():
-    """Keys at exactly the sampled positions (the middle of each of 2048 equal
+    """Keys at exactly the sampled positions (the middle of each of 1024 equal
     parts of the row) scaled up 8x: the pivot from the sample then lies above
     all but about r of the row's scores, fewer than k, so every row falls back."""
     inp, cfg, (q, k, v) = _small_dense(H=1)
-    ns = min(cfg.N, 2048)
+    ns = min(cfg.N, SELECT_SAMPLE)
     pos = ((2 * np.arange(ns) + 1) * cfg.N) // (2 * ns)
     K = k.clone()
     K[0, 0, torch.from_numpy(pos).cuda()] *= 8
@@ -408,10 +411,10 @@ def test_fused_selection_unrepresentative_sample_falls_back():
 
 
 def test_fused_selection_exact_ties_within_the_list():
-    """N = 2048 (the sample is the whole row, a list holds it all) with
+    """N = 1024 (the sample is the whole row, a list holds it all) with
     all-zero keys: every score ties, every token is listed and the selection
     is the first k."""
-    wl = synth.WORKLOADS["dense_pred_bf16"].with_(B=1, H=1, grid_h=32, grid_w=64)
+    wl = synth.WORKLOADS["dense_pred_bf16"].with_(B=1, H=1, grid_h=32, grid_w=32)
     inp = synth.generate(wl)
     cfg = mita.Config.from_workload(wl)
     q, k, v = (to_dev(x, "bf16") for x in (inp.q, inp.k, inp.v))
