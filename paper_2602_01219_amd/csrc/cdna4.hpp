@@ -165,6 +165,15 @@ __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
   }
   return x;
 }
+// Wait until every global load this wave issued so far has landed. Placed
+// after the loads that precede a software-pipelined loop (fragments kept in
+// registers for the whole loop), it lets the compiler's wait placement inside
+// the loop count only the loop's own in-flight loads instead of draining them
+// before the first use of those fragments.
+// (s_waitcnt fields on gfx9: vmcnt bits 3:0 and 15:14 = 0, expcnt 6:4 = 7 and
+// lgkmcnt 11:8 = 15, i.e. no wait on those.)
+__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0f70); }
+
 // Number of set bits of `mask` in lanes below this one.
 __device__ __forceinline__ uint32_t lanes_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));

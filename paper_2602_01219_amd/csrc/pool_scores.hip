@@ -115,6 +115,7 @@ __device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ 
   }
   const bool write_row = WRITE_S && lm < M && (only_lm < 0 || lm == only_lm);
   uint32_t listed = 0;  // SELECT: candidates of this landmark listed so far in the chunk
+  wait_loads();  // landmark fragments and pivot are in registers before the pipelined loop
   Online<D> st;
   st.init();
   const float sl2 = scale * LOG2E;
@@ -136,34 +137,21 @@ __device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ 
     if (t + 1 < ntile)
       R.load(kb_ + (int64_t)(k0 + TK) * D, DO_V ? vb_ + (int64_t)(k0 + TK) * D : nullptr, nullptr,
              min(TK, key_end - k0 - TK));
+    // The tile's global stores (S or candidates) are issued after the next
+    // tile's LDS store: on gfx9 one counter tracks loads and stores, so the
+    // wait for the prefetched loads would otherwise also wait for them.
+    f32x4 acc[4];
+    uint32_t m[4] = {0u, 0u, 0u, 0u}, pos = 0u, tot = 0u;
     if (active) {
-      f32x4 acc[4];
       tile_scores<T, D>(acc, Kc, qf);
-      if (write_row) {
-        float *srow = S + row * (int64_t)N + k0;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-          const int key = kb * 16 + 4 * g;
-          if (key + 3 < nvalid) {
-            *reinterpret_cast<float4 *>(srow + key) =
-                make_float4(acc[kb][0] * scale, acc[kb][1] * scale, acc[kb][2] * scale, acc[kb][3] * scale);
-          } else {
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (key + r < nvalid) srow[key + r] = acc[kb][r] * scale;
-          }
-        }
-      }
       if (SELECT) {
-        float x[4][4];
-        uint32_t m[4], packed = 0;  // per-kb candidate bits (r); per-kb counts in bytes
+        uint32_t packed = 0;  // per-kb candidate bits m[kb] (bit r); per-kb counts in bytes
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
-          m[kb] = 0;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            x[kb][r] = acc[kb][r] * scale;
-            const bool c = x[kb][r] >= piv || (nan_in && x[kb][r] != x[kb][r]);
+            const float x = acc[kb][r] * scale;
+            const bool c = x >= piv || (nan_in && x != x);
             if (c && kb * 16 + 4 * g + r < nvalid) m[kb] |= 1u << r;
           }
           packed |= (uint32_t)__popc(m[kb]) << (8 * kb);
@@ -174,26 +162,43 @@ __device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ 
         if (g >= 1) incl += y;
         y = (uint32_t)__shfl_up((int)incl, 32);
         if (g >= 2) incl += y;
-        const uint32_t tot = (uint32_t)__shfl((int)incl, 48 + p);  // per-kb totals of the landmark
+        tot = (uint32_t)__shfl((int)incl, 48 + p);  // per-kb totals of the landmark
         // byte kb of pos: candidates of the landmark before this lane's block kb
-        const uint32_t pos = (incl - packed) + (tot << 8) + (tot << 16) + (tot << 24);
-        uint2 *list = sel.cand + (row * nchunks + chunk) * (int64_t)SCORE_NC + listed;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-          if (!__ballot(m[kb] != 0u)) continue;  // no candidate of this block in the wave
-          uint32_t at = (pos >> (8 * kb)) & 255u;
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (m[kb] & (1u << r)) {
-              list[at] = make_uint2(__float_as_uint(x[kb][r]), (uint32_t)(k0 + kb * 16 + 4 * g + r));
-              ++at;
-            }
-        }
-        listed += (tot * 0x01010101u) >> 24;
+        pos = (incl - packed) + (tot << 8) + (tot << 16) + (tot << 24);
       }
       if (DO_V) tile_softmax_pv<T, D>(st, acc, Vc, nvalid, sl2);
     }
     if (t + 1 < ntile) R.store(Ks + (buf ^ 1) * TD::K_ELEMS, DO_V ? Vt + (buf ^ 1) * TD::V_ELEMS : Vt);
+    if (active && write_row) {
+      float *srow = S + row * (int64_t)N + k0;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const int key = kb * 16 + 4 * g;
+        if (key + 3 < nvalid) {
+          *reinterpret_cast<float4 *>(srow + key) =
+              make_float4(acc[kb][0] * scale, acc[kb][1] * scale, acc[kb][2] * scale, acc[kb][3] * scale);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (key + r < nvalid) srow[key + r] = acc[kb][r] * scale;
+        }
+      }
+    }
+    if (SELECT && active) {
+      uint2 *list = sel.cand + (row * nchunks + chunk) * (int64_t)SCORE_NC + listed;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        if (!__ballot(m[kb] != 0u)) continue;  // no candidate of this block in the wave
+        uint32_t at = (pos >> (8 * kb)) & 255u;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (m[kb] & (1u << r)) {
+            list[at] = make_uint2(__float_as_uint(acc[kb][r] * scale), (uint32_t)(k0 + kb * 16 + 4 * g + r));
+            ++at;
+          }
+      }
+      listed += (tot * 0x01010101u) >> 24;
+    }
     __syncthreads();
   }
   if (SELECT && active && lm < M && g == 0) sel.ccnt[row * nchunks + chunk] = listed;

@@ -389,6 +389,7 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
     else
       qf[ks].zero();
   }
+  wait_loads();  // the query fragments are in registers before the pipelined loop
   Online<D> st;
   st.init();
   const float sl2 = scale * LOG2E;
