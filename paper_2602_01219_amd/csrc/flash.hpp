@@ -24,14 +24,15 @@ template <typename T, int D> struct TileDims {
   // padded V^T row: 136 bytes (bf16) / 272 bytes (fp32) keep the 8 / 16-byte
   // fragment reads aligned and spread the transposing writes over the banks
   static constexpr int VSTR = TK + 4;
+  // bf16, d = 64: V^T row R starts at R * VSTR + 8 * ((R >> 4) & 3). With that
+  // shift per 16-row group the transposing stores of a tile (8 chunks of 8
+  // rows, 2-key words) fall in 32 distinct banks instead of 8, while the P V
+  // fragment reads (16 consecutive rows, one shift) stay conflict-free and in
+  // ascending address order.
+  static constexpr bool VSHIFT = sizeof(T) == 2 && D == 64;
   static constexpr int K_ELEMS = TK * KSTR;
-  static constexpr int V_ELEMS = D * VSTR;
-  // bf16, d = 64: key column c of V^T row R sits at c ^ (8 * ((R >> 4) & 3)).
-  // The transposing stores of a tile (8 chunks of 8 rows, 2-key words) then
-  // fall in 32 distinct banks instead of 8, and the P V fragment reads (16
-  // consecutive rows, one XOR value) stay conflict-free and 8-byte contiguous.
-  static constexpr bool VSWZ = sizeof(T) == 2 && D == 64;
-  __device__ __forceinline__ static int vcol(int row, int col) { return VSWZ ? col ^ (8 * ((row >> 4) & 3)) : col; }
+  static constexpr int V_ELEMS = D * VSTR + (VSHIFT ? 24 : 0);
+  __device__ __forceinline__ static int vrow(int row) { return row * VSTR + (VSHIFT ? 8 * ((row >> 4) & 3) : 0); }
 };
 
 // Cooperative load of up to 64 key rows into LDS, Ks row-major [64][D]. Rows
@@ -72,17 +73,36 @@ __device__ __forceinline__ void tile_scores(f32x4 (&acc)[4], const T *__restrict
   }
 }
 
-// Running state of one wave (16 query columns). m is in the log2 domain.
+// Running state of one wave (16 query columns). m is in the log2 domain. The
+// running sum of the weights is an MFMA accumulator (an all-ones A operand
+// against the same P^T as the values), so every element of lsum holds the
+// full sum for its lane's query column, of the very weights (as rounded for
+// the MFMA) that multiply V.
 template <int D> struct Online {
   f32x4 o[D / 16];
-  float m, l;
+  f32x4 lsum;
+  float m;
   __device__ __forceinline__ void init() {
 #pragma unroll
     for (int i = 0; i < D / 16; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    lsum = f32x4{0.f, 0.f, 0.f, 0.f};
     m = -INFINITY;
-    l = 0.f;
   }
+  __device__ __forceinline__ float l() const { return lsum[0]; }
 };
+
+template <typename T> __device__ __forceinline__ Frag<T> ones_frag();
+template <> __device__ __forceinline__ Frag<bf16_t> ones_frag<bf16_t>() {
+  Frag<bf16_t> f;
+  f.v = make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);  // bf16 1.0 x 8
+  return f;
+}
+template <> __device__ __forceinline__ Frag<float> ones_frag<float>() {
+  Frag<float> f;
+  f.a = make_float4(1.f, 1.f, 1.f, 1.f);
+  f.b = f.a;
+  return f;
+}
 
 // Online-softmax update with the tile's scores (acc, unscaled dot products) and
 // O^T += V^T P^T. sl2 = scale * log2(e); the running max is kept in scaled
@@ -109,7 +129,6 @@ __device__ __forceinline__ void tile_softmax_pv(Online<D> &st, const f32x4 (&acc
   const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
   st.m = m_new;
   float t[4][4];
-  float ls = 0.f;
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -117,14 +136,14 @@ __device__ __forceinline__ void tile_softmax_pv(Online<D> &st, const f32x4 (&acc
       float e = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[kb][r], sl2, -m_new));
       if (MASKED && kb * 16 + 4 * g + r >= nvalid) e = 0.f;
       t[kb][r] = e;
-      ls += e;
     }
-  st.l = st.l * alpha + ls;
   // rescale only when some column's max moved (alpha == 1 exactly otherwise)
   if (__ballot(alpha != 1.0f)) {
 #pragma unroll
     for (int i = 0; i < D / 16; ++i) st.o[i] *= alpha;
+    st.lsum *= alpha;
   }
+  const Frag<T> ones = ones_frag<T>();
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     // reduction slice of group g: keys 32j + 4g + (0..3) and 32j + 16 + 4g + (0..3)
@@ -132,12 +151,12 @@ __device__ __forceinline__ void tile_softmax_pv(Online<D> &st, const f32x4 (&acc
                          t[2 * j + 1][0], t[2 * j + 1][1], t[2 * j + 1][2], t[2 * j + 1][3]};
     Frag<T> b;
     b.from_f32(pv);
+    st.lsum = mma(ones, b, st.lsum);
 #pragma unroll
     for (int db = 0; db < D / 16; ++db) {
-      const int vr = db * 16 + p, c = TD::vcol(vr, 32 * j + 4 * g);
-      const T *row = Vt + vr * TD::VSTR;
+      const T *row = Vt + TD::vrow(db * 16 + p) + 32 * j + 4 * g;
       Frag<T> a;
-      a.load2x4(row + c, row + (c ^ 16));
+      a.load2x4(row, row + 16);
       st.o[db] = mma(a, b, st.o[db]);
     }
   }
@@ -220,7 +239,7 @@ template <> __device__ __forceinline__ void TileRegs<bf16_t, 64, true>::store_vt
                                                                                int r0) const {
   // CH = 2: keys r0, r0+1 of dims 2m, 2m+1 from the two rows' words m
   using TD = TileDims<bf16_t, 64>;
-  bf16_t *dst = Vt + row * TD::VSTR + TD::vcol(row, r0);
+  bf16_t *dst = Vt + TD::vrow(row) + r0;
   const uint4 v0 = vget(0), v1 = vget(1);
   const uint32_t r0w[4] = {v0.x, v0.y, v0.z, v0.w}, r1w[4] = {v1.x, v1.y, v1.z, v1.w};
 #pragma unroll
@@ -272,11 +291,5 @@ template <> __device__ __forceinline__ void TileRegs<float, 128, true>::store_vt
   }
 }
 
-// Sum of the per-lane running sums over the four lane groups of a column.
-__device__ __forceinline__ float column_sum(float x) {
-  x += __shfl_xor(x, 16);
-  x += __shfl_xor(x, 32);
-  return x;
-}
 
 }  // namespace mita

@@ -203,7 +203,7 @@ __device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ 
   }
   if (SELECT && active && lm < M && g == 0) sel.ccnt[row * nchunks + chunk] = listed;
   if (!DO_V || !active) return;
-  const float l = column_sum(st.l);
+  const float l = st.l();
   if (lm < M) {
     const int64_t prow = (bh * nchunks + chunk) * M + lm;
     if (g == 0) part_ml[prow] = make_float2(st.m, l);

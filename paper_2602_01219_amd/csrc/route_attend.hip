@@ -465,7 +465,7 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
     __syncthreads();
   }
 
-  const float l = column_sum(st.l);
+  const float l = st.l();
   if (!qvalid) return;
   const float inv = 1.0f / l;
   T *orow = o + (bh * N + token) * D;
