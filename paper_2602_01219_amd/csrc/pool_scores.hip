@@ -145,17 +145,25 @@ __device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ 
     if (active) {
       tile_scores<T, D>(acc, Kc, qf);
       if (SELECT) {
-        uint32_t packed = 0;  // per-kb candidate bits m[kb] (bit r); per-kb counts in bytes
+        // per-kb candidate bits m[kb] (bit r); per-kb counts in bytes
+        if (nvalid == TK && !__ballot(nan_in)) {  // full tile, no -inf pivot in the wave
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
+          for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float x = acc[kb][r] * scale;
-            const bool c = x >= piv || (nan_in && x != x);
-            if (c && kb * 16 + 4 * g + r < nvalid) m[kb] |= 1u << r;
-          }
-          packed |= (uint32_t)__popc(m[kb]) << (8 * kb);
+            for (int r = 0; r < 4; ++r) m[kb] |= (acc[kb][r] * scale >= piv) ? 1u << r : 0u;
+        } else {
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float x = acc[kb][r] * scale;
+              const bool c = x >= piv || (nan_in && x != x);
+              if (c && kb * 16 + 4 * g + r < nvalid) m[kb] |= 1u << r;
+            }
         }
+        uint32_t packed = 0;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) packed |= (uint32_t)__popc(m[kb]) << (8 * kb);
         // inclusive scan over the lane groups of landmark p (bytes stay below 17)
         uint32_t incl = packed;
         uint32_t y = (uint32_t)__shfl_up((int)incl, 16);
