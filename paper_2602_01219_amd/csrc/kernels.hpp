@@ -29,7 +29,8 @@ struct SelectBufs {
 // Scores S = fl(q_lm . k) * scale (optional) and landmark values (optional):
 // split over key chunks, partials in `partial`, merged into v_lm. With sel,
 // the candidates of the fused selection are listed instead of storing S
-// (launch_select_pivots must have run).
+// (launch_select_pivots must have run) and the landmark-value merge is left to
+// launch_select_finish.
 hipError_t launch_scores(const mita_cfg_t &c, const void *q_lm, const void *k, const void *v, float *scores,
                          void *v_lm, void *partial, const SelectBufs *sel, hipStream_t st);
 
@@ -40,9 +41,11 @@ hipError_t launch_select_pivots(const mita_cfg_t &c, const void *q_lm, const voi
 
 // Fused selection, after the score pass: exact top-k from the candidate
 // lists into idx; rows whose list is unusable get their score row recomputed
-// into S (same arithmetic as the score pass) and the exact top-k of it.
+// into S (same arithmetic as the score pass) and the exact top-k of it. With
+// v_lm, also merges the score pass's landmark-value partials into v_lm (the
+// score pass then leaves that merge out).
 hipError_t launch_select_finish(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sel,
-                                float *S, int32_t *idx, hipStream_t st);
+                                float *S, int32_t *idx, const void *partial, void *v_lm, hipStream_t st);
 
 // Score rows of the listed landmark rows only (fallback of the fused selection).
 hipError_t launch_scores_rows(const mita_cfg_t &c, const void *q_lm, const void *k, float *S,

@@ -121,7 +121,7 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
                  "scores"));
   TRY(mark(2));
   if (fused)
-    TRY(hip_status(launch_select_finish(*c, q_lm, k, sel, S, idx, st), "topk"));
+    TRY(hip_status(launch_select_finish(*c, q_lm, k, sel, S, idx, w + L.partial, v_lm, st), "topk"));
   else if (c->use_routed)
     TRY(hip_status(launch_topk(*c, S, idx, st), "topk"));
   TRY(mark(3));

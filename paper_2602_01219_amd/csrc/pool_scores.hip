@@ -256,29 +256,14 @@ __global__ __launch_bounds__(BLOCK) void scores_rows_kernel(const T *__restrict_
   }
 }
 
-// Log-sum-exp merge of the per-chunk landmark-value partials (online softmax
-// across chunks, in one pass: the loads do not depend on the running state,
-// so they stay in flight). 256 threads = 256 / D landmarks x D dimensions.
+// Log-sum-exp merge of the per-chunk landmark-value partials, one workgroup
+// per landmark row (the same merge, in the same order, as the fused
+// selection's finish applies).
 template <typename T, int D>
 __global__ __launch_bounds__(256) void merge_kernel(const float2 *__restrict__ part_ml, const float *__restrict__ part_o,
                                                     T *__restrict__ v_lm, int M, int nchunks) {
-  constexpr int LPB = 256 / D;
-  const int lm = blockIdx.x * LPB + threadIdx.x / D, dim = threadIdx.x % D;
-  const int64_t bh = blockIdx.y;
-  if (lm >= M) return;
-  float mx = -INFINITY, L = 0.f, acc = 0.f;
-#pragma unroll 8
-  for (int c = 0; c < nchunks; ++c) {
-    const int64_t row = (bh * nchunks + c) * M + lm;
-    const float2 ml = part_ml[row];
-    const float o = part_o[row * D + dim];
-    const float m_new = fmaxf(mx, ml.x);
-    const float a = __builtin_amdgcn_exp2f(mx - m_new), b = __builtin_amdgcn_exp2f(ml.x - m_new);
-    L = L * a + ml.y * b;
-    acc = acc * a + o * b;
-    mx = m_new;
-  }
-  v_lm[(bh * M + lm) * D + dim] = from_f32<T>(acc / L);
+  __shared__ float red[256 / D][3][D];
+  merge_landmark_value<T, D>(part_ml, part_o, v_lm, blockIdx.y, blockIdx.x, M, nchunks, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -359,10 +344,9 @@ static hipError_t scores_t(const mita_cfg_t &c, const void *q_lm, const void *k,
   }
 #undef MITA_SCORES
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !v_lm) return e;
-  constexpr int LPB = 256 / D;
-  hipLaunchKernelGGL((merge_kernel<T, D>), dim3((c.M + LPB - 1) / LPB, (unsigned)BH(c)), dim3(256), 0, st, ml, po,
-                     (T *)v_lm, c.M, nch);
+  if (e != hipSuccess || !v_lm || sb) return e;  // with sel the merge runs in the selection's finish
+  hipLaunchKernelGGL((merge_kernel<T, D>), dim3((unsigned)c.M, (unsigned)BH(c)), dim3(256), 0, st, ml, po, (T *)v_lm,
+                     c.M, nch);
   return hipGetLastError();
 }
 

@@ -380,6 +380,10 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
 
   const int qi = q_begin + w * 16 + p;
   const bool qvalid = qi < q_end;
+  // a wave whose 16 queries all lie past the tile's end (the last tile of an
+  // expert is usually partial) still stages tiles and meets the barriers but
+  // skips the arithmetic
+  const bool wave_busy = q_begin + w * 16 < q_end;
   const int token = qvalid ? (ROUTED ? perm[bh * N + qi] : qi) : 0;
   Frag<T> qf[D / 32];
 #pragma unroll
@@ -412,9 +416,11 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
         tile_base(i + 1, kb, vb, off);
         Ra.load_full(kb, vb, rows + off);
       }
-      f32x4 acc[4];
-      tile_scores<T, D>(acc, Ks[buf], qf);
-      tile_softmax_pv<T, D, false>(st, acc, Vt[buf], TK, sl2);
+      if (wave_busy) {
+        f32x4 acc[4];
+        tile_scores<T, D>(acc, Ks[buf], qf);
+        tile_softmax_pv<T, D, false>(st, acc, Vt[buf], TK, sl2);
+      }
       if (i + 1 < nfull) Ra.store(Ks[buf ^ 1], Vt[buf ^ 1]);
       __syncthreads();
     }
@@ -439,9 +445,11 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
         else
           Ra.load_full(rkb + (int64_t)(j - nA) * TK * D, rvb + (int64_t)(j - nA) * TK * D, nullptr);
       }
-      f32x4 acc[4];
-      tile_scores<T, D>(acc, Ks[buf], qf);
-      tile_softmax_pv<T, D, false>(st, acc, Vt[buf], TK, sl2);
+      if (wave_busy) {
+        f32x4 acc[4];
+        tile_scores<T, D>(acc, Ks[buf], qf);
+        tile_softmax_pv<T, D, false>(st, acc, Vt[buf], TK, sl2);
+      }
       if (i + 1 < nfull) Ra.store(Ks[buf ^ 1], Vt[buf ^ 1]);
       __syncthreads();
     }
@@ -459,14 +467,16 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
     }
     Ra.store(Ks[0], Vt[0]);
     __syncthreads();
-    f32x4 acc[4];
-    tile_scores<T, D>(acc, Ks[0], qf);
-    tile_softmax_pv<T, D, true>(st, acc, Vt[0], nr, sl2);
+    if (wave_busy) {
+      f32x4 acc[4];
+      tile_scores<T, D>(acc, Ks[0], qf);
+      tile_softmax_pv<T, D, true>(st, acc, Vt[0], nr, sl2);
+    }
     __syncthreads();
   }
 
-  const float l = st.l();
   if (!qvalid) return;
+  const float l = st.l();
   const float inv = 1.0f / l;
   T *orow = o + (bh * N + token) * D;
 #pragma unroll

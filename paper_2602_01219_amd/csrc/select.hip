@@ -213,11 +213,14 @@ __device__ __forceinline__ uint64_t composite(uint2 e) {
 
 constexpr int MAX_CHUNKS = MITA_MAX_N / SCORE_NC;
 
-template <int CAP>
+template <typename T, int D, int CAP, bool MERGE>
 __global__ __launch_bounds__(256) void finalize_kernel(const uint2 *__restrict__ cand,
                                                        const uint32_t *__restrict__ ccnt, int32_t *__restrict__ idx,
                                                        uint32_t *__restrict__ fail_cnt,
-                                                       int32_t *__restrict__ fail_list, int k, int cap, int nch) {
+                                                       int32_t *__restrict__ fail_list, int k, int cap, int nch,
+                                                       const float2 *__restrict__ part_ml,
+                                                       const float *__restrict__ part_o, T *__restrict__ v_lm, int M) {
+  __shared__ float red[MERGE ? 256 / D : 1][3][D];
   __shared__ uint2 lst[CAP];
   __shared__ uint32_t pre[MAX_CHUNKS + 1];
   __shared__ uint32_t hist[256];
@@ -243,6 +246,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(const uint2 *__restrict__
   if (tid <= nch) pre[tid] = before + wincl - cc;
   if (total < (uint32_t)k || total > (uint32_t)cap) {  // uniform
     if (tid == 0) fail_list[atomicAdd(fail_cnt, 1u)] = (int32_t)row;
+    if (MERGE) merge_landmark_value<T, D>(part_ml, part_o, v_lm, row / M, (int)(row % M), M, nch, red);
     return;
   }
   __syncthreads();
@@ -366,6 +370,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(const uint2 *__restrict__
     run += tot;
     par ^= 1;  // double-buffered counts: the next step's write cannot race this read
   }
+  if (MERGE) merge_landmark_value<T, D>(part_ml, part_o, v_lm, row / M, (int)(row % M), M, nch, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -394,18 +399,38 @@ hipError_t launch_select_pivots(const mita_cfg_t &c, const void *q_lm, const voi
 }
 
 hipError_t launch_select_finish(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sb, float *S,
-                                int32_t *idx, hipStream_t st) {
+                                int32_t *idx, const void *partial, void *v_lm, hipStream_t st) {
   const unsigned rows = (unsigned)(BH(c) * c.M);
   const int nch = score_chunks(c);
-#define MITA_FINALIZE(CAP)                                                                                   \
-  hipLaunchKernelGGL((finalize_kernel<CAP>), dim3(rows), dim3(256), 0, st, sb.cand, sb.ccnt, idx, sb.fail_cnt, \
-                     sb.fail_list, c.k, sb.cap, nch)
-  if (sb.cap <= 1024)
-    MITA_FINALIZE(1024);
-  else if (sb.cap <= 2048)
-    MITA_FINALIZE(2048);
-  else
-    MITA_FINALIZE(SEL_CAP);
+  const float2 *ml = (const float2 *)partial;
+  const float *po = v_lm ? (const float *)((const char *)partial + align_up((size_t)BH(c) * nch * c.M * sizeof(float2)))
+                         : nullptr;
+#define MITA_FINALIZE(TT, DD, CAP, MG)                                                                          \
+  hipLaunchKernelGGL((finalize_kernel<TT, DD, CAP, MG>), dim3(rows), dim3(256), 0, st, sb.cand, sb.ccnt, idx,   \
+                     sb.fail_cnt, sb.fail_list, c.k, sb.cap, nch, ml, po, (TT *)v_lm, c.M)
+#define MITA_FINALIZE_CAP(TT, DD, MG)     \
+  if (sb.cap <= 1024)                     \
+    MITA_FINALIZE(TT, DD, 1024, MG);      \
+  else if (sb.cap <= 2048)                \
+    MITA_FINALIZE(TT, DD, 2048, MG);      \
+  else                                    \
+    MITA_FINALIZE(TT, DD, SEL_CAP, MG);
+  if (!v_lm) {
+    MITA_FINALIZE_CAP(float, 64, false)
+  } else if (c.dtype == MITA_F32) {
+    if (c.d == 64) {
+      MITA_FINALIZE_CAP(float, 64, true)
+    } else {
+      MITA_FINALIZE_CAP(float, 128, true)
+    }
+  } else {
+    if (c.d == 64) {
+      MITA_FINALIZE_CAP(bf16_t, 64, true)
+    } else {
+      MITA_FINALIZE_CAP(bf16_t, 128, true)
+    }
+  }
+#undef MITA_FINALIZE_CAP
 #undef MITA_FINALIZE
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
