@@ -155,6 +155,16 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
   for (int o = 32; o > 0; o >>= 1) x = max(x, (uint32_t)__shfl_xor((int)x, o));
   return x;
 }
+// Maximum over the four 16-lane groups at the same position (lanes p, p+16,
+// p+32, p+48), without LDS: v_permlane16_swap(x, x) yields groups (0,0,2,2)
+// and (1,1,3,3), v_permlane32_swap the low and high halves.
+__device__ __forceinline__ float max_lane_groups(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 // Inclusive prefix sum over the 64 lanes.
 __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
   const int lane = threadIdx.x & 63;

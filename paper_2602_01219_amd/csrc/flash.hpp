@@ -123,8 +123,7 @@ __device__ __forceinline__ void tile_softmax_pv(Online<D> &st, const f32x4 (&acc
       const bool ok = !MASKED || kb * 16 + 4 * g + r < nvalid;
       mx = fmaxf(mx, ok ? acc[kb][r] : -INFINITY);
     }
-  mx = fmaxf(mx, __shfl_xor(mx, 16));
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  mx = max_lane_groups(mx);
   const float m_new = fmaxf(st.m, mx * sl2);
   const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
   st.m = m_new;
