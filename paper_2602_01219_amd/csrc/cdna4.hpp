@@ -157,12 +157,13 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
 }
 // Maximum over the four 16-lane groups at the same position (lanes p, p+16,
 // p+32, p+48), without LDS: v_permlane16_swap(x, x) yields groups (0,0,2,2)
-// and (1,1,3,3), v_permlane32_swap the low and high halves.
+// and (1,1,3,3), v_permlane32_swap the low and high halves. The pairwise
+// max is med3(a, b, +inf), which needs no quieting of its inputs.
 __device__ __forceinline__ float max_lane_groups(float x) {
   const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  x = __builtin_amdgcn_fmed3f(__uint_as_float(a[0]), __uint_as_float(a[1]), INFINITY);
   const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+  return __builtin_amdgcn_fmed3f(__uint_as_float(b[0]), __uint_as_float(b[1]), INFINITY);
 }
 
 // Inclusive prefix sum over the 64 lanes.

@@ -17,6 +17,12 @@ namespace mita {
 constexpr int TK = 64;        // keys per tile
 constexpr int BLOCK = 256;    // 4 waves per workgroup
 constexpr float LOG2E = 1.4426950408889634f;
+// The running max of the online softmax is a reference value only: it is
+// raised when some query's tile max exceeds it by more than this (log2
+// units), so weights stay below 2^8 and the accumulators are rescaled only
+// a few times per query instead of on most tiles. Any reference gives the
+// same softmax; the weights and sums just carry a common factor.
+constexpr float RESCALE_LOG2 = 8.f;
 
 template <typename T, int D> struct TileDims {
   static constexpr int VE = 16 / (int)sizeof(T);  // elements per 16-byte chunk
@@ -73,7 +79,10 @@ __device__ __forceinline__ void tile_scores(f32x4 (&acc)[4], const T *__restrict
   }
 }
 
-// Running state of one wave (16 query columns). m is in the log2 domain. The
+// Running state of one wave (16 query columns). m is in the log2 domain and
+// at most RESCALE_LOG2 below the largest scaled score seen so far; thr is
+// (m + RESCALE_LOG2) / (scale * log2 e), the raw dot product above which m
+// has to be raised. The
 // running sum of the weights is an MFMA accumulator (an all-ones A operand
 // against the same P^T as the values), so every element of lsum holds the
 // full sum for its lane's query column, of the very weights (as rounded for
@@ -81,12 +90,13 @@ __device__ __forceinline__ void tile_scores(f32x4 (&acc)[4], const T *__restrict
 template <int D> struct Online {
   f32x4 o[D / 16];
   f32x4 lsum;
-  float m;
+  float m, thr;
   __device__ __forceinline__ void init() {
 #pragma unroll
     for (int i = 0; i < D / 16; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     lsum = f32x4{0.f, 0.f, 0.f, 0.f};
     m = -INFINITY;
+    thr = -INFINITY;
   }
   __device__ __forceinline__ float l() const { return lsum[0]; }
 };
@@ -105,9 +115,11 @@ template <> __device__ __forceinline__ Frag<float> ones_frag<float>() {
 }
 
 // Online-softmax update with the tile's scores (acc, unscaled dot products) and
-// O^T += V^T P^T. sl2 = scale * log2(e); the running max is kept in scaled
-// log2 units, the tile max is taken on the raw dots (a positive scale keeps
-// the order) and p = exp2(dot * sl2 - m) is one FMA. With MASKED, keys
+// O^T += V^T P^T. sl2 = scale * log2(e) > 0; the reference max is kept in
+// scaled log2 units and p = exp2(dot * sl2 - m) is one FMA. Whether the
+// reference has to move is decided on each lane's own 16 raw dots against
+// thr (a positive scale keeps the order); only then is the column max over
+// the four lane groups formed. With MASKED, keys
 // kb*16 + 4g + r >= nvalid are excluded (only the last tile of a key range is
 // partial). The tile must hold at least one valid key.
 template <typename T, int D, bool MASKED = true>
@@ -123,25 +135,27 @@ __device__ __forceinline__ void tile_softmax_pv(Online<D> &st, const f32x4 (&acc
       const bool ok = !MASKED || kb * 16 + 4 * g + r < nvalid;
       mx = fmaxf(mx, ok ? acc[kb][r] : -INFINITY);
     }
-  mx = max_lane_groups(mx);
-  const float m_new = fmaxf(st.m, mx * sl2);
-  const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
-  st.m = m_new;
+  // a new reference max only when some column's tile max is more than
+  // RESCALE_LOG2 above it (always on the first tile: m = -inf)
+  if (__ballot(mx > st.thr)) {
+    const float m_new = fmaxf(st.m, max_lane_groups(mx) * sl2);
+    const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
+    st.m = m_new;
+    st.thr = (m_new + RESCALE_LOG2) * __builtin_amdgcn_rcpf(sl2);
+#pragma unroll
+    for (int i = 0; i < D / 16; ++i) st.o[i] *= alpha;
+    st.lsum *= alpha;
+  }
+  const float m_ref = st.m;
   float t[4][4];
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      float e = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[kb][r], sl2, -m_new));
+      float e = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[kb][r], sl2, -m_ref));
       if (MASKED && kb * 16 + 4 * g + r >= nvalid) e = 0.f;
       t[kb][r] = e;
     }
-  // rescale only when some column's max moved (alpha == 1 exactly otherwise)
-  if (__ballot(alpha != 1.0f)) {
-#pragma unroll
-    for (int i = 0; i < D / 16; ++i) st.o[i] *= alpha;
-    st.lsum *= alpha;
-  }
   const Frag<T> ones = ones_frag<T>();
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
@@ -221,6 +235,36 @@ template <typename T, int D, bool WITH_V = true> struct TileRegs {
       const int64_t src = rowidx ? (int64_t)rowidx[r0 + j] : (int64_t)(r0 + j);
       kset(j, *reinterpret_cast<const uint4 *>(kb + src * D + ch * VE));
       if (WITH_V) vset(j, *reinterpret_cast<const uint4 *>(vb + src * D + ch * VE));
+    }
+  }
+  // the same from byte offsets: row r of the tile starts offs[r] bytes past
+  // kb (and vb); kb and vb are the same for every lane, so the loads take a
+  // scalar base and a 32-bit lane offset
+  __device__ __forceinline__ void load_off(const T *__restrict__ kb, const T *__restrict__ vb,
+                                           const uint32_t *offs, int nrows) {
+    const int r0 = row0();
+    const uint32_t cb = (uint32_t)chunk() * 16u;
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+      uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
+      if (r0 + j < nrows) {
+        const uint32_t o = offs[r0 + j] + cb;
+        a = *reinterpret_cast<const uint4 *>(reinterpret_cast<const char *>(kb) + o);
+        if (WITH_V) b = *reinterpret_cast<const uint4 *>(reinterpret_cast<const char *>(vb) + o);
+      }
+      kset(j, a);
+      if (WITH_V) vset(j, b);
+    }
+  }
+  __device__ __forceinline__ void load_full_off(const T *__restrict__ kb, const T *__restrict__ vb,
+                                                const uint32_t *offs) {
+    const int r0 = row0();
+    const uint32_t cb = (uint32_t)chunk() * 16u;
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+      const uint32_t o = offs[r0 + j] + cb;
+      kset(j, *reinterpret_cast<const uint4 *>(reinterpret_cast<const char *>(kb) + o));
+      if (WITH_V) vset(j, *reinterpret_cast<const uint4 *>(reinterpret_cast<const char *>(vb) + o));
     }
   }
   __device__ __forceinline__ void store(T *__restrict__ Ks, T *__restrict__ Vt) const {

@@ -312,7 +312,7 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
   using TD = TileDims<T, D>;
   __shared__ __align__(16) T Ks[2][TD::K_ELEMS];
   __shared__ __align__(16) T Vt[2][TD::V_ELEMS];
-  extern __shared__ int32_t sidx[];  // with IDX_LDS: M + k row indices
+  extern __shared__ uint32_t sidx[];  // with IDX_LDS: byte offsets of the M + k key rows
   const int64_t bh = blockIdx.y;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
 
@@ -359,14 +359,16 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
   }
   // With IDX_LDS, one row list in LDS covers every key: entries [0, M) are
   // the shared rows (identity), entries [M, M + k) the routed rows (the
-  // expert's index list, or identity into its tile). Every tile then loads
-  // through the same code, its base pointer picked by a scalar select.
-  const int32_t *rows = nullptr;
+  // expert's index list, or identity into its tile), each as the byte offset
+  // of the row. Every tile then loads through the same code, its base pointer
+  // picked by a scalar select and each row addressed by a 32-bit offset.
+  const uint32_t *rows = nullptr;
+  constexpr uint32_t ROWB = D * sizeof(T);
   if (IDX_LDS) {
     const int nsh = SHARED ? M : 0;
-    for (int i = threadIdx.x; i < nsh; i += BLOCK) sidx[i] = i;
+    for (int i = threadIdx.x; i < nsh; i += BLOCK) sidx[i] = (uint32_t)i * ROWB;
     if (ROUTED)
-      for (int i = threadIdx.x; i < k; i += BLOCK) sidx[nsh + i] = FUSED ? gidx[i] : i;
+      for (int i = threadIdx.x; i < k; i += BLOCK) sidx[nsh + i] = (uint32_t)(FUSED ? gidx[i] : i) * ROWB;
     __syncthreads();
     rows = sidx;
   }
@@ -401,29 +403,36 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
   TileRegs<T, D> Ra;
   if (IDX_LDS) {
     // one tile ahead: tile i + 1 is loaded into registers while tile i is
-    // multiplied, then stored to the other LDS buffer
+    // multiplied, then stored to the other LDS buffer; the loop is unrolled
+    // by two so that both buffers have fixed LDS addresses
     const T *kb, *vb;
     int off;
-    if (nfull > 0) {
-      tile_base(0, kb, vb, off);
-      Ra.load_full(kb, vb, rows + off);
-      Ra.store(Ks[0], Vt[0]);
-    }
-    __syncthreads();
-    for (int i = 0; i < nfull; ++i) {
-      const int buf = i & 1;
-      if (i + 1 < nfull) {
+    auto step = [&](int i, const T *Kc, const T *Vc, T *Kn, T *Vn) {
+      const bool more = i + 1 < nfull;
+      if (more) {
         tile_base(i + 1, kb, vb, off);
-        Ra.load_full(kb, vb, rows + off);
+        Ra.load_full_off(kb, vb, rows + off);
       }
       if (wave_busy) {
         f32x4 acc[4];
-        tile_scores<T, D>(acc, Ks[buf], qf);
-        tile_softmax_pv<T, D, false>(st, acc, Vt[buf], TK, sl2);
+        tile_scores<T, D>(acc, Kc, qf);
+        tile_softmax_pv<T, D, false>(st, acc, Vc, TK, sl2);
       }
-      if (i + 1 < nfull) Ra.store(Ks[buf ^ 1], Vt[buf ^ 1]);
+      if (more) Ra.store(Kn, Vn);
       __syncthreads();
+    };
+    if (nfull > 0) {
+      tile_base(0, kb, vb, off);
+      Ra.load_full_off(kb, vb, rows + off);
+      Ra.store(Ks[0], Vt[0]);
     }
+    __syncthreads();
+    int i = 0;
+    for (; i + 1 < nfull; i += 2) {
+      step(i, Ks[0], Vt[0], Ks[1], Vt[1]);
+      step(i + 1, Ks[1], Vt[1], Ks[0], Vt[0]);
+    }
+    if (i < nfull) step(i, Ks[0], Vt[0], Ks[1], Vt[1]);
   } else {
     // long index lists stay in memory: one register set, one tile ahead
     for (int i = 0; i < nfull; ++i) {
@@ -460,8 +469,10 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
     if (nr == 0) continue;  // uniform
     if (part == 0) {
       Ra.load(sh_k + (int64_t)nA * TK * D, sh_v + (int64_t)nA * TK * D, nullptr, nr);
+    } else if (IDX_LDS) {
+      Ra.load_off(rkb, rvb, rows + rbase + nB * TK, nr);
     } else if (FUSED) {
-      Ra.load(rkb, rvb, IDX_LDS ? rows + rbase + nB * TK : gidx + nB * TK, nr);
+      Ra.load(rkb, rvb, gidx + nB * TK, nr);
     } else {
       Ra.load(rkb + (int64_t)nB * TK * D, rvb + (int64_t)nB * TK * D, nullptr, nr);
     }
