@@ -175,6 +175,102 @@ __device__ __forceinline__ void tile_softmax_pv(Online<D> &st, const f32x4 (&acc
   }
 }
 
+// Running state of a wave that owns 32 queries: two 16-column groups, each
+// kept as in Online (reference max m, its raw-dot threshold thr, weight sums
+// as an MFMA accumulator).
+template <int D> struct Online2 {
+  f32x4 o[2][D / 16];
+  f32x4 lsum[2];
+  float m[2], thr[2];
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+#pragma unroll
+      for (int i = 0; i < D / 16; ++i) o[c][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+      lsum[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+      m[c] = -INFINITY;
+      thr[c] = -INFINITY;
+    }
+  }
+  __device__ __forceinline__ float l(int c) const { return lsum[c][0]; }
+};
+
+// One wave's online-softmax step over one 32-key half of an LDS tile (keys
+// 32h .. 32h + 31) for its 32 queries (fragments qf[c], c = column group):
+// S^T = K Q^T for both groups from the same key fragments, then the same
+// update as tile_softmax_pv on 8 dots per lane and group, and O^T += V^T P^T
+// with every V^T fragment serving both groups. Splitting a tile's keys
+// between two waves halves the LDS bytes each wave reads per score. With
+// MASKED only keys 32h + i, i < nvalid (>= 1) count.
+template <typename T, int D, bool MASKED = false>
+__device__ __forceinline__ void half_tile_attend(Online2<D> &st, const T *__restrict__ Ks, const T *__restrict__ Vt,
+                                                 int h, const Frag<T> (&qf)[2][D / 32], int nvalid, float sl2) {
+  using TD = TileDims<T, D>;
+  const int lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
+  f32x4 acc[2][2];  // [group][16-key block]
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    acc[0][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    acc[1][kb] = acc[0][kb];
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      Frag<T> a;
+      a.load(Ks + (32 * h + kb * 16 + p) * TD::KSTR + ks * 32 + g * 8);
+      acc[0][kb] = mma(a, qf[0][ks], acc[0][kb]);
+      acc[1][kb] = mma(a, qf[1][ks], acc[1][kb]);
+    }
+  }
+  float mx[2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    mx[c] = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool ok = !MASKED || kb * 16 + 4 * g + r < nvalid;
+        mx[c] = fmaxf(mx[c], ok ? acc[c][kb][r] : -INFINITY);
+      }
+  }
+  if (__ballot(mx[0] > st.thr[0] || mx[1] > st.thr[1])) {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const float m_new = fmaxf(st.m[c], max_lane_groups(mx[c]) * sl2);
+      const float alpha = __builtin_amdgcn_exp2f(st.m[c] - m_new);
+      st.m[c] = m_new;
+      st.thr[c] = (m_new + RESCALE_LOG2) * __builtin_amdgcn_rcpf(sl2);
+#pragma unroll
+      for (int i = 0; i < D / 16; ++i) st.o[c][i] *= alpha;
+      st.lsum[c] *= alpha;
+    }
+  }
+  const Frag<T> ones = ones_frag<T>();
+  Frag<T> b[2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    // reduction slice of group g: keys 32h + 4g + (0..3) and 32h + 16 + 4g + (0..3)
+    float pv[8];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float e = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[c][kb][r], sl2, -st.m[c]));
+        if (MASKED && kb * 16 + 4 * g + r >= nvalid) e = 0.f;
+        pv[4 * kb + r] = e;
+      }
+    b[c].from_f32(pv);
+    st.lsum[c] = mma(ones, b[c], st.lsum[c]);
+  }
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db) {
+    const T *row = Vt + TD::vrow(db * 16 + p) + 32 * h + 4 * g;
+    Frag<T> a;
+    a.load2x4(row, row + 16);
+    st.o[0][db] = mma(a, b[0], st.o[0][db]);
+    st.o[1][db] = mma(a, b[1], st.o[1][db]);
+  }
+}
+
 // Register-staged copy of one 64-row K/V tile (software pipelining: the
 // global loads of the next tile are issued before the current tile is
 // processed, the LDS stores after). Thread t owns rows CH*(t / CPR) + j,

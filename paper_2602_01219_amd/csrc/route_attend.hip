@@ -284,8 +284,12 @@ __global__ __launch_bounds__(1024) void worklist_kernel(const int32_t *__restric
 // MiTA attention (Eq. mita with s = 1): each query attends, in one online
 // softmax, over the shared expert (keys q_lm, values v_lm; Eq. shared-expert)
 // and the k keys of its routed expert (Eq. mita-expert). Workgroup = 64
-// queries of one expert (4 waves x 16), taken from the routing work list
-// (Algorithm 1's varlen grouping); outputs are scattered back to token order.
+// queries of one expert, taken from the routing work list (Algorithm 1's
+// varlen grouping); outputs are scattered back to token order. Wave w owns
+// queries 32 (w / 2) .. + 31 and the key half w % 2 of every 64-key tile, so
+// each wave reads half of each staged tile; the two waves of a query half
+// merge their partial softmax states through LDS at the end (log-sum-exp),
+// each finishing one of the two 16-query groups.
 // With ROUTED, routed keys come from the expert tiles, or straight from the
 // K/V rows listed in idx (FUSED: the gather of Eq. gather done in place; with
 // IDX_LDS the expert's index list is staged in LDS first).
@@ -380,23 +384,29 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
     off = sh ? i * TK : rbase + (i - nA) * TK;
   };
 
-  const int qi = q_begin + w * 16 + p;
-  const bool qvalid = qi < q_end;
-  // a wave whose 16 queries all lie past the tile's end (the last tile of an
+  const int qh = w >> 1, kh = w & 1;  // query half, key half
+  // a wave whose 32 queries all lie past the tile's end (the last tile of an
   // expert is usually partial) still stages tiles and meets the barriers but
   // skips the arithmetic
-  const bool wave_busy = q_begin + w * 16 < q_end;
-  const int token = qvalid ? (ROUTED ? perm[bh * N + qi] : qi) : 0;
-  Frag<T> qf[D / 32];
+  const bool wave_busy = q_begin + qh * 32 < q_end;
+  bool qvalid[2];
+  int token[2];
+  Frag<T> qf[2][D / 32];
 #pragma unroll
-  for (int ks = 0; ks < D / 32; ++ks) {
-    if (qvalid)
-      qf[ks].load(q + (bh * N + token) * D + ks * 32 + g * 8);
-    else
-      qf[ks].zero();
+  for (int c = 0; c < 2; ++c) {
+    const int qi = q_begin + qh * 32 + c * 16 + p;
+    qvalid[c] = qi < q_end;
+    token[c] = qvalid[c] ? (ROUTED ? perm[bh * N + qi] : qi) : 0;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      if (qvalid[c])
+        qf[c][ks].load(q + (bh * N + token[c]) * D + ks * 32 + g * 8);
+      else
+        qf[c][ks].zero();
+    }
   }
   wait_loads();  // the query fragments are in registers before the pipelined loop
-  Online<D> st;
+  Online2<D> st;
   st.init();
   const float sl2 = scale * LOG2E;
 
@@ -413,11 +423,7 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
         tile_base(i + 1, kb, vb, off);
         Ra.load_full_off(kb, vb, rows + off);
       }
-      if (wave_busy) {
-        f32x4 acc[4];
-        tile_scores<T, D>(acc, Kc, qf);
-        tile_softmax_pv<T, D, false>(st, acc, Vc, TK, sl2);
-      }
+      if (wave_busy) half_tile_attend<T, D>(st, Kc, Vc, kh, qf, 32, sl2);
       if (more) Ra.store(Kn, Vn);
       __syncthreads();
     };
@@ -454,11 +460,7 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
         else
           Ra.load_full(rkb + (int64_t)(j - nA) * TK * D, rvb + (int64_t)(j - nA) * TK * D, nullptr);
       }
-      if (wave_busy) {
-        f32x4 acc[4];
-        tile_scores<T, D>(acc, Ks[buf], qf);
-        tile_softmax_pv<T, D, false>(st, acc, Vt[buf], TK, sl2);
-      }
+      if (wave_busy) half_tile_attend<T, D>(st, Ks[buf], Vt[buf], kh, qf, 32, sl2);
       if (i + 1 < nfull) Ra.store(Ks[buf ^ 1], Vt[buf ^ 1]);
       __syncthreads();
     }
@@ -478,23 +480,44 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
     }
     Ra.store(Ks[0], Vt[0]);
     __syncthreads();
-    if (wave_busy) {
-      f32x4 acc[4];
-      tile_scores<T, D>(acc, Ks[0], qf);
-      tile_softmax_pv<T, D, true>(st, acc, Vt[0], nr, sl2);
-    }
+    const int nh = min(32, nr - 32 * kh);  // keys of this wave's half
+    if (wave_busy && nh > 0) half_tile_attend<T, D, true>(st, Ks[0], Vt[0], kh, qf, nh, sl2);
     __syncthreads();
   }
 
-  if (!qvalid) return;
-  const float l = st.l();
+  // merge the two key halves: wave (qh, kh) finishes query group kh and hands
+  // group 1 - kh to its partner (qh, 1 - kh) through LDS (the K tiles are
+  // free after the last barrier); a half that saw no key has m = -inf, l = 0
+  constexpr int XN = D / 4 + 2;  // o values, m, l per lane
+  static_assert(sizeof(Ks) >= sizeof(float) * 4 * XN * 64, "exchange buffer");
+  float *xb = reinterpret_cast<float *>(&Ks[0][0]);
+  // (kh selects by value: register arrays indexed at run time would go to scratch)
+  const bool k1 = kh != 0;
+  {
+    float *mine = xb + w * XN * 64 + lane;
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) mine[(db * 4 + r) * 64] = k1 ? st.o[0][db][r] : st.o[1][db][r];
+    mine[(D / 4) * 64] = k1 ? st.m[0] : st.m[1];
+    mine[(D / 4 + 1) * 64] = k1 ? st.l(0) : st.l(1);
+  }
+  __syncthreads();
+  if (!(k1 ? qvalid[1] : qvalid[0])) return;
+  const float *theirs = xb + (w ^ 1) * XN * 64 + lane;
+  const float m0 = k1 ? st.m[1] : st.m[0], m1 = theirs[(D / 4) * 64];
+  const float mm = fmaxf(m0, m1);
+  const float a0 = __builtin_amdgcn_exp2f(m0 - mm), a1 = __builtin_amdgcn_exp2f(m1 - mm);
+  const float l = (k1 ? st.l(1) : st.l(0)) * a0 + theirs[(D / 4 + 1) * 64] * a1;
   const float inv = 1.0f / l;
-  T *orow = o + (bh * N + token) * D;
+  const float s0 = a0 * inv, s1 = a1 * inv;
+  T *orow = o + (bh * N + (k1 ? token[1] : token[0])) * D;
 #pragma unroll
   for (int db = 0; db < D / 16; ++db) {
     T vals[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) vals[r] = from_f32<T>(st.o[db][r] * inv);
+    for (int r = 0; r < 4; ++r)
+      vals[r] = from_f32<T>((k1 ? st.o[1][db][r] : st.o[0][db][r]) * s0 + theirs[(db * 4 + r) * 64] * s1);
     T *dst = orow + db * 16 + 4 * g;
     if (sizeof(T) == 2)
       *reinterpret_cast<uint2 *>(dst) = *reinterpret_cast<const uint2 *>(vals);
