@@ -434,44 +434,74 @@ template <> __device__ __forceinline__ void TileRegs<float, 128, true>::store_vt
 // Landmark value of one row (Eq. landmark-value) from the score pass's
 // per-chunk partials (running max in log2 units, running sum, unnormalised
 // accumulator): a log-sum-exp merge over the chunks, by the whole workgroup:
-// thread t takes dimension t % D and every (256 / D)-th chunk from t / D on;
-// the groups' partial merges are combined through LDS.
+// thread t takes dimension t % D and every (256 / D)-th chunk from t / D on,
+// in increasing chunk order; the groups' partial merges are combined through
+// LDS. prefetch() issues the loads of a thread's first PF chunks, so that a
+// caller can overlap them with other work before finish().
+template <typename T, int D, int PF = 8> struct LandmarkMerge {
+  static constexpr int NG = 256 / D;
+  float2 ml[PF];
+  float ov[PF];
+  __device__ __forceinline__ void prefetch(const float2 *__restrict__ part_ml, const float *__restrict__ part_o,
+                                           int64_t bh, int lm, int M, int nch) {
+    const int dim = threadIdx.x % D, grp = threadIdx.x / D;
+#pragma unroll
+    for (int j = 0; j < PF; ++j) {
+      const int c = grp + NG * j;
+      if (c < nch) {
+        const int64_t prow = (bh * nch + c) * M + lm;
+        ml[j] = part_ml[prow];
+        ov[j] = part_o[prow * D + dim];
+      }
+    }
+  }
+  __device__ __forceinline__ static void step(float &mx, float &L, float &acc, float2 m, float o) {
+    const float m_new = fmaxf(mx, m.x);
+    const float a = __builtin_amdgcn_exp2f(mx - m_new), b = __builtin_amdgcn_exp2f(m.x - m_new);
+    L = L * a + m.y * b;
+    acc = acc * a + o * b;
+    mx = m_new;
+  }
+  __device__ __forceinline__ void finish(const float2 *__restrict__ part_ml, const float *__restrict__ part_o,
+                                         T *__restrict__ v_lm, int64_t bh, int lm, int M, int nch,
+                                         float (*red)[3][D]) const {
+    const int dim = threadIdx.x % D, grp = threadIdx.x / D;
+    float mx = -INFINITY, L = 0.f, acc = 0.f;
+#pragma unroll
+    for (int j = 0; j < PF; ++j)
+      if (grp + NG * j < nch) step(mx, L, acc, ml[j], ov[j]);
+#pragma unroll 4
+    for (int c = grp + NG * PF; c < nch; c += NG) {
+      const int64_t prow = (bh * nch + c) * M + lm;
+      step(mx, L, acc, part_ml[prow], part_o[prow * D + dim]);
+    }
+    red[grp][0][dim] = mx;
+    red[grp][1][dim] = L;
+    red[grp][2][dim] = acc;
+    __syncthreads();
+    if (grp == 0) {
+      float m2 = -INFINITY;
+#pragma unroll
+      for (int g2 = 0; g2 < NG; ++g2) m2 = fmaxf(m2, red[g2][0][dim]);
+      float L2 = 0.f, a2 = 0.f;
+#pragma unroll
+      for (int g2 = 0; g2 < NG; ++g2) {
+        const float f = __builtin_amdgcn_exp2f(red[g2][0][dim] - m2);  // a group with no chunk: exp2(-inf) = 0
+        L2 += red[g2][1][dim] * f;
+        a2 += red[g2][2][dim] * f;
+      }
+      v_lm[(bh * M + lm) * D + dim] = from_f32<T>(a2 / L2);
+    }
+  }
+};
+
 template <typename T, int D>
 __device__ __forceinline__ void merge_landmark_value(const float2 *__restrict__ part_ml,
                                                      const float *__restrict__ part_o, T *__restrict__ v_lm,
                                                      int64_t bh, int lm, int M, int nch, float (*red)[3][D]) {
-  constexpr int NG = 256 / D;
-  const int tid = threadIdx.x, dim = tid % D, grp = tid / D;
-  float mx = -INFINITY, L = 0.f, acc = 0.f;
-#pragma unroll 4
-  for (int c = grp; c < nch; c += NG) {
-    const int64_t prow = (bh * nch + c) * M + lm;
-    const float2 ml = part_ml[prow];
-    const float o = part_o[prow * D + dim];
-    const float m_new = fmaxf(mx, ml.x);
-    const float a = __builtin_amdgcn_exp2f(mx - m_new), b = __builtin_amdgcn_exp2f(ml.x - m_new);
-    L = L * a + ml.y * b;
-    acc = acc * a + o * b;
-    mx = m_new;
-  }
-  red[grp][0][dim] = mx;
-  red[grp][1][dim] = L;
-  red[grp][2][dim] = acc;
-  __syncthreads();
-  if (grp == 0) {
-    float m2 = -INFINITY;
-#pragma unroll
-    for (int g2 = 0; g2 < NG; ++g2) m2 = fmaxf(m2, red[g2][0][dim]);
-    float L2 = 0.f, a2 = 0.f;
-#pragma unroll
-    for (int g2 = 0; g2 < NG; ++g2) {
-      const float f = __builtin_amdgcn_exp2f(red[g2][0][dim] - m2);  // a group with no chunk: exp2(-inf) = 0
-      L2 += red[g2][1][dim] * f;
-      a2 += red[g2][2][dim] * f;
-    }
-    v_lm[(bh * M + lm) * D + dim] = from_f32<T>(a2 / L2);
-  }
+  LandmarkMerge<T, D> m;
+  m.prefetch(part_ml, part_o, bh, lm, M, nch);
+  m.finish(part_ml, part_o, v_lm, bh, lm, M, nch, red);
 }
-
 
 }  // namespace mita

@@ -231,6 +231,9 @@ __global__ __launch_bounds__(256) void finalize_kernel(const uint2 *__restrict__
   __shared__ uint32_t bc[3];
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int64_t row = blockIdx.x;
+  // the landmark-value partials are loaded first; the merge uses them last
+  LandmarkMerge<T, D> lmm;
+  if (MERGE) lmm.prefetch(part_ml, part_o, row / M, (int)(row % M), M, nch);
 
   // chunk counts -> exclusive prefix (nch <= 256: one chunk per thread)
   const uint32_t cc = tid < nch ? ccnt[row * nch + tid] : 0u;
@@ -246,29 +249,26 @@ __global__ __launch_bounds__(256) void finalize_kernel(const uint2 *__restrict__
   if (tid <= nch) pre[tid] = before + wincl - cc;
   if (total < (uint32_t)k || total > (uint32_t)cap) {  // uniform
     if (tid == 0) fail_list[atomicAdd(fail_cnt, 1u)] = (int32_t)row;
-    if (MERGE) merge_landmark_value<T, D>(part_ml, part_o, v_lm, row / M, (int)(row % M), M, nch, red);
+    if (MERGE) lmm.finish(part_ml, part_o, v_lm, row / M, (int)(row % M), M, nch, red);
     return;
   }
   __syncthreads();
+  // compaction into LDS, with the composite range of the list
   const int L = (int)total;
-  for (int i = tid; i < L; i += 256) {
-    int lo = 0, hi = nch - 1;  // last chunk c with pre[c] <= i
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (pre[mid] <= (uint32_t)i)
-        lo = mid;
-      else
-        hi = mid - 1;
-    }
-    const uint2 e = cand[(row * nch + lo) * (int64_t)SCORE_NC + (i - (int)pre[lo])];
-    lst[i] = make_uint2(score_key(__uint_as_float(e.x)), e.y);  // listed as float bits
-  }
-  __syncthreads();
-
-  // composite range of the list
   uint64_t lo = ~0ull, hi = 0ull;
   for (int i = tid; i < L; i += 256) {
-    const uint64_t c = composite(lst[i]);
+    int a = 0, b = nch - 1;  // last chunk c with pre[c] <= i
+    while (a < b) {
+      const int mid = (a + b + 1) >> 1;
+      if (pre[mid] <= (uint32_t)i)
+        a = mid;
+      else
+        b = mid - 1;
+    }
+    const uint2 e = cand[(row * nch + a) * (int64_t)SCORE_NC + (i - (int)pre[a])];
+    const uint2 x = make_uint2(score_key(__uint_as_float(e.x)), e.y);  // listed as float bits
+    lst[i] = x;
+    const uint64_t c = composite(x);
     lo = c < lo ? c : lo;
     hi = c > hi ? c : hi;
   }
@@ -345,32 +345,27 @@ __global__ __launch_bounds__(256) void finalize_kernel(const uint2 *__restrict__
     __syncthreads();  // bc and hist are rewritten by the next round
   }
 
-  // ordered scan: the list is in ascending token order
+  // ordered output: the list is in ascending token order; thread t takes
+  // entries [t E, t E + E) and one block scan places its selected ones
   int32_t *out = idx + row * (int64_t)k;
-  uint32_t run = 0;
-  int par = 0;
-  for (int i0 = 0; i0 < L; i0 += 256) {
-    const int i = i0 + tid;
-    uint2 e = make_uint2(0u, 0u);
-    bool sel = false;
-    if (i < L) {
-      e = lst[i];
-      sel = composite(e) >= ck;
-    }
-    const uint64_t m = __ballot(sel);
-    if (lane == 0) wsum[par][w] = (uint32_t)__popcll(m);
-    __syncthreads();
-    uint32_t at = run + lanes_below(m), tot = 0;
+  const int E = (L + 255) / 256;
+  const int i0 = tid * E, i1 = min(L, i0 + E);
+  uint32_t nsel = 0;
+  for (int i = i0; i < i1; ++i) nsel += composite(lst[i]) >= ck;
+  const uint32_t sincl = wave_inclusive_scan(nsel);
+  if (lane == 63) wsum[0][w] = sincl;  // wsum[0] was last read before the compaction
+  __syncthreads();
+  uint32_t at = sincl - nsel;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      at += j < w ? wsum[par][j] : 0u;
-      tot += wsum[par][j];
+  for (int j = 0; j < 4; ++j) at += j < w ? wsum[0][j] : 0u;
+  for (int i = i0; i < i1; ++i) {
+    const uint2 e = lst[i];
+    if (composite(e) >= ck) {
+      if (at < (uint32_t)k) out[at] = (int32_t)e.y;
+      ++at;
     }
-    if (sel && at < (uint32_t)k) out[at] = (int32_t)e.y;
-    run += tot;
-    par ^= 1;  // double-buffered counts: the next step's write cannot race this read
   }
-  if (MERGE) merge_landmark_value<T, D>(part_ml, part_o, v_lm, row / M, (int)(row % M), M, nch, red);
+  if (MERGE) lmm.finish(part_ml, part_o, v_lm, row / M, (int)(row % M), M, nch, red);
 }
 
 // ---------------------------------------------------------------------------
