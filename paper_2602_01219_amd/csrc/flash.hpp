@@ -193,6 +193,7 @@ template <int D> struct Online2 {
     }
   }
   __device__ __forceinline__ float l(int c) const { return lsum[c][0]; }
+  __device__ __forceinline__ float mval(int c) const { return m[c]; }
 };
 
 // One wave's online-softmax step over one 32-key half of an LDS tile (keys
@@ -266,6 +267,169 @@ __device__ __forceinline__ void half_tile_attend(Online2<D> &st, const T *__rest
     const T *row = Vt + TD::vrow(db * 16 + p) + 32 * h + 4 * g;
     Frag<T> a;
     a.load2x4(row, row + 16);
+    st.o[0][db] = mma(a, b[0], st.o[0][db]);
+    st.o[1][db] = mma(a, b[1], st.o[1][db]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 tiles staged by LDS DMA (global_load_lds_dwordx4: each lane's 16
+// bytes land at consecutive LDS addresses, 1 KB per wave instruction, with no
+// registers involved). K and V are both kept row-major, rows of D elements
+// without padding; 16-byte slot s of row r holds chunk s ^ swz(r). The
+// swizzle spreads the K fragment reads (8 rows at one chunk) and the V
+// transpose reads (16 rows, 4 pieces each) evenly over the LDS banks. The
+// A operand of O^T += V^T P^T comes from ds_read_b64_tr_b16: in each 16-lane
+// group, lane 4e + c addresses piece c (4 elements) of row e of a 4 x 16
+// block and lane i receives column i, i.e. 4 consecutive keys of one
+// dimension.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+
+template <int D> struct DmaTile {
+  static constexpr int CPR = D / 8;        // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;     // rows per wave instruction
+  static constexpr int NI = TK / RPI;      // instructions per 64-row matrix
+  static constexpr int PW = NI / 4;        // per wave of a 4-wave workgroup
+  static constexpr int BYTES = TK * D * 2; // one 64-row matrix
+};
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
+
+// Issue the DMA of one tile: rows r < 64 of K and V from byte offsets offs[r]
+// past kb and vb (rows >= nrows take offset offs[0]: real data, masked later).
+template <int D>
+__device__ __forceinline__ void dma_tile(bf16_t *Kl, bf16_t *Vl, const bf16_t *kb, const bf16_t *vb,
+                                         const uint32_t *offs, int nrows) {
+  using DT = DmaTile<D>;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int j = 0; j < DT::PW; ++j) {
+    const int ins = w * DT::PW + j;
+    const int r = ins * DT::RPI + lane / DT::CPR;
+    const int sl = lane % DT::CPR;
+    const uint32_t go = offs[r < nrows ? r : 0] + (uint32_t)((sl ^ swz(r)) << 4);
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(kb) + go,
+                                     (lds_void_t *)(reinterpret_cast<char *>(Kl) + ins * 1024), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vb) + go,
+                                     (lds_void_t *)(reinterpret_cast<char *>(Vl) + ins * 1024), 16, 0, 0);
+  }
+}
+
+// Softmax state of a wave with 32 queries for the DMA path: as Online2, the
+// reference max m kept also as the negated splat nm that initialises the
+// score accumulators, so the MFMA yields dot * scale * log2 e - m directly
+// (the query fragments are pre-scaled by scale * log2 e).
+template <int D> struct OnlineDma {
+  f32x4 o[2][D / 16];
+  f32x4 lsum[2];
+  f32x4 nm[2];
+  bool started;
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+#pragma unroll
+      for (int i = 0; i < D / 16; ++i) o[c][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+      lsum[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+      nm[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    started = false;
+  }
+  // a half that saw no key has no reference: -inf, with zero sums
+  __device__ __forceinline__ float mval(int c) const { return started ? -nm[c][0] : -INFINITY; }
+  __device__ __forceinline__ float l(int c) const { return lsum[c][0]; }
+};
+
+// One wave's step over the 32-key half h of a DMA-staged tile for its 32
+// queries (pre-scaled fragments qf[c]). The reference max starts at the first
+// tile's column max; later it moves only when a column's shifted scores
+// exceed RESCALE_LOG2 (then the tile's values, accumulators and sums shift
+// with it). With MASKED only keys 32h + i, i < nvalid (>= 1), count.
+template <int D, bool MASKED = false>
+__device__ __forceinline__ void half_tile_dma(OnlineDma<D> &st, const bf16_t *Kl, const bf16_t *Vl, int h,
+                                              const Frag<bf16_t> (&qf)[2][D / 32], int nvalid) {
+  constexpr int RB = 2 * D;  // bytes per row
+  const int lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
+  const char *kbase = reinterpret_cast<const char *>(Kl);
+  f32x4 acc[2][2];  // [group][16-key block]: shifted scores
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    acc[0][kb] = st.nm[0];
+    acc[1][kb] = st.nm[1];
+    const int R = 32 * h + kb * 16 + p;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      Frag<bf16_t> a;
+      a.v = *reinterpret_cast<const uint4 *>(kbase + R * RB + (((4 * ks + g) ^ swz(R)) << 4));
+      acc[0][kb] = mma(a, qf[0][ks], acc[0][kb]);
+      acc[1][kb] = mma(a, qf[1][ks], acc[1][kb]);
+    }
+  }
+  float mx[2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    mx[c] = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool ok = !MASKED || kb * 16 + 4 * g + r < nvalid;
+        mx[c] = fmaxf(mx[c], ok ? acc[c][kb][r] : -INFINITY);
+      }
+  }
+  if (__ballot(!st.started || mx[0] > RESCALE_LOG2 || mx[1] > RESCALE_LOG2)) {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const float cm = max_lane_groups(mx[c]);
+      // first tile: the reference becomes the column max (the accumulators
+      // are still zero); later: raised by the excess only
+      const float d = st.started ? fmaxf(cm, 0.f) : cm;
+      st.nm[c] -= d;
+      if (st.started) {
+        const float alpha = __builtin_amdgcn_exp2f(-d);
+#pragma unroll
+        for (int i = 0; i < D / 16; ++i) st.o[c][i] *= alpha;
+        st.lsum[c] *= alpha;
+      }
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) acc[c][kb] -= d;
+    }
+    st.started = true;
+  }
+  const Frag<bf16_t> ones = ones_frag<bf16_t>();
+  Frag<bf16_t> b[2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    // reduction slice of group g: keys 32h + 4g + (0..3) and 32h + 16 + 4g + (0..3)
+    float pv[8];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float e = __builtin_amdgcn_exp2f(acc[c][kb][r]);
+        if (MASKED && kb * 16 + 4 * g + r >= nvalid) e = 0.f;
+        pv[4 * kb + r] = e;
+      }
+    b[c].from_f32(pv);
+    st.lsum[c] = mma(ones, b[c], st.lsum[c]);
+  }
+  // V^T fragments by transpose reads: lane (g, i = 4e + c) addresses piece c
+  // of key row 32h + 16 h2 + 4g + e, dimensions 16 db + 4c .. + 3
+  const char *vbase = reinterpret_cast<const char *>(Vl);
+  const int e = p >> 2, c4 = p & 3;
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db) {
+    uint2 half[2];
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      const int Rv = 32 * h + 16 * h2 + 4 * g + e;
+      const char *addr = vbase + Rv * RB + (((2 * db + (c4 >> 1)) ^ swz(Rv)) << 4) + ((c4 & 1) << 3);
+      half[h2] = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)addr));
+    }
+    Frag<bf16_t> a;
+    a.v = make_uint4(half[0].x, half[0].y, half[1].x, half[1].y);
     st.o[0][db] = mma(a, b[0], st.o[0][db]);
     st.o[1][db] = mma(a, b[1], st.o[1][db]);
   }

@@ -1,4 +1,6 @@
 // route_attend.hip - routing of queries to landmarks and the MiTA attention.
+#include <type_traits>
+
 #include "cdna4.hpp"
 #include "flash.hpp"
 #include "kernels.hpp"
@@ -304,9 +306,11 @@ __global__ __launch_bounds__(1024) void worklist_kernel(const int32_t *__restric
 // C = ceil(tiles / 8); the grid's x extent is a multiple of 8.
 // ---------------------------------------------------------------------------
 constexpr int NXCD = 8;
+// bf16, d = 64 with the DMA staging: registers within four waves per SIMD
+#define ATTEND_OCCUPANCY __attribute__((amdgpu_waves_per_eu(sizeof(T) == 2 && D == 64 && IDX_LDS ? 4 : 1)))
 
 template <typename T, int D, bool SHARED, bool ROUTED, bool FUSED, bool IDX_LDS>
-__global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
+__global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
                                                        const T *__restrict__ v_lm, const T *__restrict__ rk,
                                                        const T *__restrict__ rv, const int32_t *__restrict__ idx,
                                                        const int32_t *__restrict__ perm,
@@ -314,8 +318,17 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
                                                        const int32_t *__restrict__ tile_start, T *__restrict__ o,
                                                        int N, int M, int k, float scale) {
   using TD = TileDims<T, D>;
-  __shared__ __align__(16) T Ks[2][TD::K_ELEMS];
-  __shared__ __align__(16) T Vt[2][TD::V_ELEMS];
+  // bf16 tiles listed in LDS go by LDS DMA (K and V row-major, swizzled);
+  // otherwise through registers (K row-major, V transposed, padded rows)
+  constexpr bool DMA = sizeof(T) == 2 && IDX_LDS;
+  constexpr int KBYTES = DMA ? DmaTile<D>::BYTES : TD::K_ELEMS * (int)sizeof(T);
+  constexpr int TBYTES = KBYTES + (DMA ? DmaTile<D>::BYTES : TD::V_ELEMS * (int)sizeof(T));
+  // two separate arrays, so that the compiler sees the DMA into one buffer
+  // and the reads of the other as disjoint (no wait for the DMA in between)
+  __shared__ __align__(16) char tiles0[TBYTES];
+  __shared__ __align__(16) char tiles1[TBYTES];
+  auto Ks = [&](int b) { return reinterpret_cast<T *>(b ? tiles1 : tiles0); };
+  auto Vt = [&](int b) { return reinterpret_cast<T *>((b ? tiles1 : tiles0) + KBYTES); };
   extern __shared__ uint32_t sidx[];  // with IDX_LDS: byte offsets of the M + k key rows
   const int64_t bh = blockIdx.y;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
@@ -405,11 +418,67 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
         qf[c][ks].zero();
     }
   }
-  wait_loads();  // the query fragments are in registers before the pipelined loop
-  Online2<D> st;
-  st.init();
   const float sl2 = scale * LOG2E;
+  if constexpr (DMA) {
+    // the DMA path's score MFMAs take q * scale * log2 e (rounded to bf16)
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) {
+        float x[8];
+        unpack16(qf[c][ks].v, x, (const bf16_t *)nullptr);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[i] *= sl2;
+        qf[c][ks].from_f32(x);
+      }
+  }
+  wait_loads();  // the query fragments are in registers before the pipelined loop
+  std::conditional_t<DMA, OnlineDma<D>, Online2<D>> st;
+  st.init();
 
+  if constexpr (DMA) {
+    // one tile ahead: the DMA of tile i + 1 into the other buffer is issued,
+    // tile i is multiplied, then the wave waits for its DMA and the workgroup
+    // meets at the barrier; unrolled by two so both buffers have fixed
+    // addresses
+    const T *kb, *vb;
+    int off;
+    auto step = [&](int i, const T *Kc, const T *Vc, T *Kn, T *Vn) {
+      if (i + 1 < nfull) {
+        tile_base(i + 1, kb, vb, off);
+        dma_tile<D>(Kn, Vn, kb, vb, rows + off, TK);
+      }
+      if (wave_busy) half_tile_dma<D>(st, Kc, Vc, kh, qf, 32);
+      wait_loads();
+      __syncthreads();
+    };
+    if (nfull > 0) {
+      tile_base(0, kb, vb, off);
+      dma_tile<D>(Ks(0), Vt(0), kb, vb, rows + off, TK);
+    }
+    wait_loads();
+    __syncthreads();
+    int i = 0;
+    for (; i + 1 < nfull; i += 2) {
+      step(i, Ks(0), Vt(0), Ks(1), Vt(1));
+      step(i + 1, Ks(1), Vt(1), Ks(0), Vt(0));
+    }
+    if (i < nfull) step(i, Ks(0), Vt(0), Ks(1), Vt(1));
+    // partial tiles (masked)
+    for (int part = 0; part < 2; ++part) {
+      const int nr = part == 0 ? pA : pB;
+      if (nr == 0) continue;  // uniform
+      if (part == 0)
+        dma_tile<D>(Ks(0), Vt(0), sh_k, sh_v, rows + nA * TK, nr);
+      else
+        dma_tile<D>(Ks(0), Vt(0), rkb, rvb, rows + rbase + nB * TK, nr);
+      wait_loads();
+      __syncthreads();
+      const int nh = min(32, nr - 32 * kh);  // keys of this wave's half
+      if (wave_busy && nh > 0) half_tile_dma<D, true>(st, Ks(0), Vt(0), kh, qf, nh);
+      __syncthreads();
+    }
+  } else {
   TileRegs<T, D> Ra;
   if (IDX_LDS) {
     // one tile ahead: tile i + 1 is loaded into registers while tile i is
@@ -430,15 +499,15 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
     if (nfull > 0) {
       tile_base(0, kb, vb, off);
       Ra.load_full_off(kb, vb, rows + off);
-      Ra.store(Ks[0], Vt[0]);
+      Ra.store(Ks(0), Vt(0));
     }
     __syncthreads();
     int i = 0;
     for (; i + 1 < nfull; i += 2) {
-      step(i, Ks[0], Vt[0], Ks[1], Vt[1]);
-      step(i + 1, Ks[1], Vt[1], Ks[0], Vt[0]);
+      step(i, Ks(0), Vt(0), Ks(1), Vt(1));
+      step(i + 1, Ks(1), Vt(1), Ks(0), Vt(0));
     }
-    if (i < nfull) step(i, Ks[0], Vt[0], Ks[1], Vt[1]);
+    if (i < nfull) step(i, Ks(0), Vt(0), Ks(1), Vt(1));
   } else {
     // long index lists stay in memory: one register set, one tile ahead
     for (int i = 0; i < nfull; ++i) {
@@ -447,7 +516,7 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
           Ra.load_full(sh_k, sh_v, nullptr);
         else
           Ra.load_full(rkb, rvb, FUSED ? gidx : nullptr);
-        Ra.store(Ks[0], Vt[0]);
+        Ra.store(Ks(0), Vt(0));
         __syncthreads();
       }
       const int buf = i & 1;
@@ -460,8 +529,8 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
         else
           Ra.load_full(rkb + (int64_t)(j - nA) * TK * D, rvb + (int64_t)(j - nA) * TK * D, nullptr);
       }
-      if (wave_busy) half_tile_attend<T, D>(st, Ks[buf], Vt[buf], kh, qf, 32, sl2);
-      if (i + 1 < nfull) Ra.store(Ks[buf ^ 1], Vt[buf ^ 1]);
+      if (wave_busy) half_tile_attend<T, D>(st, Ks(buf), Vt(buf), kh, qf, 32, sl2);
+      if (i + 1 < nfull) Ra.store(Ks(buf ^ 1), Vt(buf ^ 1));
       __syncthreads();
     }
   }
@@ -478,19 +547,23 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
     } else {
       Ra.load(rkb + (int64_t)nB * TK * D, rvb + (int64_t)nB * TK * D, nullptr, nr);
     }
-    Ra.store(Ks[0], Vt[0]);
+    Ra.store(Ks(0), Vt(0));
     __syncthreads();
     const int nh = min(32, nr - 32 * kh);  // keys of this wave's half
-    if (wave_busy && nh > 0) half_tile_attend<T, D, true>(st, Ks[0], Vt[0], kh, qf, nh, sl2);
+    if (wave_busy && nh > 0) half_tile_attend<T, D, true>(st, Ks(0), Vt(0), kh, qf, nh, sl2);
     __syncthreads();
+  }
   }
 
   // merge the two key halves: wave (qh, kh) finishes query group kh and hands
-  // group 1 - kh to its partner (qh, 1 - kh) through LDS (the K tiles are
-  // free after the last barrier); a half that saw no key has m = -inf, l = 0
-  constexpr int XN = D / 4 + 2;  // o values, m, l per lane
-  static_assert(sizeof(Ks) >= sizeof(float) * 4 * XN * 64, "exchange buffer");
-  float *xb = reinterpret_cast<float *>(&Ks[0][0]);
+  // group 1 - kh to its partner (qh, 1 - kh) through LDS (the tile buffers
+  // are free after the last barrier: o values in one, m and l in the other);
+  // a half that saw no key has m = -inf, l = 0
+  constexpr int XN = D / 4;  // o values per lane
+  static_assert(sizeof(tiles0) >= sizeof(float) * 4 * XN * 64 && sizeof(tiles1) >= sizeof(float) * 4 * 2 * 64,
+                "exchange buffers");
+  float *xb = reinterpret_cast<float *>(tiles0);
+  float *xm = reinterpret_cast<float *>(tiles1);
   // (kh selects by value: register arrays indexed at run time would go to scratch)
   const bool k1 = kh != 0;
   {
@@ -499,16 +572,16 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
     for (int db = 0; db < D / 16; ++db)
 #pragma unroll
       for (int r = 0; r < 4; ++r) mine[(db * 4 + r) * 64] = k1 ? st.o[0][db][r] : st.o[1][db][r];
-    mine[(D / 4) * 64] = k1 ? st.m[0] : st.m[1];
-    mine[(D / 4 + 1) * 64] = k1 ? st.l(0) : st.l(1);
+    xm[w * 128 + lane] = k1 ? st.mval(0) : st.mval(1);
+    xm[w * 128 + 64 + lane] = k1 ? st.l(0) : st.l(1);
   }
   __syncthreads();
   if (!(k1 ? qvalid[1] : qvalid[0])) return;
   const float *theirs = xb + (w ^ 1) * XN * 64 + lane;
-  const float m0 = k1 ? st.m[1] : st.m[0], m1 = theirs[(D / 4) * 64];
+  const float m0 = k1 ? st.mval(1) : st.mval(0), m1 = xm[(w ^ 1) * 128 + lane];
   const float mm = fmaxf(m0, m1);
   const float a0 = __builtin_amdgcn_exp2f(m0 - mm), a1 = __builtin_amdgcn_exp2f(m1 - mm);
-  const float l = (k1 ? st.l(1) : st.l(0)) * a0 + theirs[(D / 4 + 1) * 64] * a1;
+  const float l = (k1 ? st.l(1) : st.l(0)) * a0 + xm[(w ^ 1) * 128 + 64 + lane] * a1;
   const float inv = 1.0f / l;
   const float s0 = a0 * inv, s1 = a1 * inv;
   T *orow = o + (bh * N + (k1 ? token[1] : token[0])) * D;
