@@ -115,6 +115,13 @@ __device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ 
   }
   const bool write_row = WRITE_S && lm < M && (only_lm < 0 || lm == only_lm);
   uint32_t listed = 0;  // SELECT: candidates of this landmark listed so far in the chunk
+  // SELECT: the candidate regions of this wave's landmarks start here (the
+  // wave index is uniform; readfirstlane lets the compiler keep it scalar)
+  char *cand_w = nullptr;
+  if (SELECT) {
+    const int lmw = (lmblock * 4 + __builtin_amdgcn_readfirstlane(w)) * 16;
+    cand_w = reinterpret_cast<char *>(sel.cand + ((bh * M + lmw) * nchunks + chunk) * (int64_t)SCORE_NC);
+  }
   wait_loads();  // landmark fragments and pivot are in registers before the pipelined loop
   Online<D> st;
   st.init();
@@ -193,16 +200,20 @@ __device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ 
       }
     }
     if (SELECT && active) {
-      uint2 *list = sel.cand + (row * nchunks + chunk) * (int64_t)SCORE_NC + listed;
+      // a lane's candidates of block kb take consecutive entries; addresses
+      // are a 32-bit byte offset from the wave's base (its 16 landmarks'
+      // regions of this chunk)
+      const uint32_t lane_off = ((uint32_t)p * (uint32_t)nchunks * SCORE_NC + listed) * 8u;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
         if (!__ballot(m[kb] != 0u)) continue;  // no candidate of this block in the wave
-        uint32_t at = (pos >> (8 * kb)) & 255u;
+        uint32_t at = lane_off + ((pos >> (8 * kb)) & 255u) * 8u;
+        const uint32_t ib = (uint32_t)(k0 + kb * 16 + 4 * g);
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           if (m[kb] & (1u << r)) {
-            list[at] = make_uint2(__float_as_uint(acc[kb][r] * scale), (uint32_t)(k0 + kb * 16 + 4 * g + r));
-            ++at;
+            *reinterpret_cast<uint2 *>(cand_w + at) = make_uint2(__float_as_uint(acc[kb][r] * scale), ib + r);
+            at += 8u;
           }
       }
       listed += (tot * 0x01010101u) >> 24;
