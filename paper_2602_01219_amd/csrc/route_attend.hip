@@ -419,20 +419,7 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
     }
   }
   const float sl2 = scale * LOG2E;
-  if constexpr (DMA) {
-    // the DMA path's score MFMAs take q * scale * log2 e (rounded to bf16)
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-      for (int ks = 0; ks < D / 32; ++ks) {
-        float x[8];
-        unpack16(qf[c][ks].v, x, (const bf16_t *)nullptr);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) x[i] *= sl2;
-        qf[c][ks].from_f32(x);
-      }
-  }
-  wait_loads();  // the query fragments are in registers before the pipelined loop
+  if constexpr (!DMA) wait_loads();  // the query fragments are in registers before the pipelined loop
   std::conditional_t<DMA, OnlineDma<D>, Online2<D>> st;
   st.init();
 
@@ -456,6 +443,18 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
       tile_base(0, kb, vb, off);
       dma_tile<D>(Ks(0), Vt(0), kb, vb, rows + off, TK);
     }
+    // the score MFMAs take q * scale * log2 e (rounded to bf16); the query
+    // loads were issued before the first tile's DMA, which stays in flight
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) {
+        float x[8];
+        unpack16(qf[c][ks].v, x, (const bf16_t *)nullptr);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] *= sl2;
+        qf[c][ks].from_f32(x);
+      }
     wait_loads();
     __syncthreads();
     int i = 0;
