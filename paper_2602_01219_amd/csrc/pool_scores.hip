@@ -4,6 +4,7 @@
 #include "flash.hpp"
 #include "kernels.hpp"
 #include "check.hpp"
+#include "scores.hpp"
 
 namespace mita {
 
@@ -53,186 +54,6 @@ __global__ __launch_bounds__(256) void pool_kernel(const T *__restrict__ q, T *_
   }
 }
 
-// ---------------------------------------------------------------------------
-// Scores and landmark values. Workgroup = 4 waves x 16 landmarks over one
-// chunk of SCORE_NC keys, key tiles of 64 staged in LDS (K row-major, V
-// transposed). Each wave forms S^T for its landmarks on MFMA and, per mode:
-//  - WRITE_S: writes S = fl(dot) * scale (fp32, landmark-major);
-//  - SELECT: lists the keys whose score is >= the row's pivot, in ascending
-//    token order, in the (row, chunk) region of the candidate lists (score
-//    bits, token index) and writes the region's count. In a tile a
-//    landmark's 64 keys sit in 4 lanes (lane group g holds keys
-//    16 kb + 4 g + r): per 16-key block kb, a scan over the 4 lanes of
-//    per-block counts packed in bytes gives each candidate its position, and
-//    a running count carries over the tiles of the chunk (no atomics);
-//  - DO_V: runs an online softmax with P V on MFMA for the landmark values
-//    (Eq. landmark-value: the softmax runs over the keys of each landmark);
-//    per-chunk partials (running max in log2 units, running sum,
-//    unnormalised accumulator) go to `partial`.
-// only_lm >= 0 restricts the S write to that landmark (the arithmetic of
-// every score is the same whichever rows are written).
-// ---------------------------------------------------------------------------
-struct SelectArgs {
-  const uint32_t *plo;  // [rows] pivot keys
-  uint32_t *ccnt;       // [rows, chunks] candidates listed
-  uint2 *cand;          // [rows, chunks, SCORE_NC] (score bits, token index)
-};
-
-template <typename T, int D, bool WRITE_S, bool DO_V, bool SELECT>
-__device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ Vt, const T *__restrict__ q_lm,
-                                            const T *__restrict__ k, const T *__restrict__ v, float *__restrict__ S,
-                                            float2 *__restrict__ part_ml, float *__restrict__ part_o,
-                                            const SelectArgs &sel, int N, int M, float scale, int chunk, int nchunks,
-                                            int lmblock, int64_t bh, int only_lm) {
-  // Ks / Vt: two tile buffers each, K_ELEMS / V_ELEMS apart (Vt unused without DO_V)
-  using TD = TileDims<T, D>;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
-  const int lm0 = (lmblock * 4 + w) * 16;
-  const bool active = lm0 < M && (only_lm < 0 || (only_lm >= lm0 && only_lm < lm0 + 16));
-  const int lm = lm0 + p;
-  const int64_t row = bh * M + lm;
-  const T *kb_ = k + bh * (int64_t)N * D;
-  const T *vb_ = DO_V ? v + bh * (int64_t)N * D : nullptr;
-
-  Frag<T> qf[D / 32];
-#pragma unroll
-  for (int ks = 0; ks < D / 32; ++ks) {
-    if (lm < M)
-      qf[ks].load(q_lm + row * D + ks * 32 + g * 8);
-    else
-      qf[ks].zero();
-  }
-  // SELECT: a score x is listed iff score_key(x) >= plo, i.e. x >= key_to_float(plo)
-  // for x not NaN (the key order is the float order with -0 == +0), and for
-  // NaN (ranked as -inf) iff the pivot is -inf. plo = 0xffffffff (no row)
-  // gives a NaN bound that lists nothing.
-  float piv = 0.f;
-  bool nan_in = false;
-  if (SELECT) {
-    const uint32_t plo = lm < M ? sel.plo[row] : 0xffffffffu;
-    piv = key_to_float(plo);
-    nan_in = plo == ordered_key(-INFINITY);
-  }
-  const bool write_row = WRITE_S && lm < M && (only_lm < 0 || lm == only_lm);
-  uint32_t listed = 0;  // SELECT: candidates of this landmark listed so far in the chunk
-  // SELECT: the candidate regions of this wave's landmarks start here (the
-  // wave index is uniform; readfirstlane lets the compiler keep it scalar)
-  char *cand_w = nullptr;
-  if (SELECT) {
-    const int lmw = (lmblock * 4 + __builtin_amdgcn_readfirstlane(w)) * 16;
-    cand_w = reinterpret_cast<char *>(sel.cand + ((bh * M + lmw) * nchunks + chunk) * (int64_t)SCORE_NC);
-  }
-  wait_loads();  // landmark fragments and pivot are in registers before the pipelined loop
-  Online<D> st;
-  st.init();
-  const float sl2 = scale * LOG2E;
-  const int key_begin = chunk * SCORE_NC, key_end = min(N, key_begin + SCORE_NC);
-  const int ntile = (key_end - key_begin + TK - 1) / TK;
-
-  // key tiles double-buffered in LDS: the next tile's loads are in flight
-  // while the current one is used, one barrier per tile
-  TileRegs<T, D, DO_V> R;
-  R.load(kb_ + (int64_t)key_begin * D, DO_V ? vb_ + (int64_t)key_begin * D : nullptr, nullptr,
-         min(TK, key_end - key_begin));
-  R.store(Ks, Vt);
-  __syncthreads();
-  for (int t = 0; t < ntile; ++t) {
-    const int buf = t & 1;
-    T *Kc = Ks + buf * TD::K_ELEMS, *Vc = DO_V ? Vt + buf * TD::V_ELEMS : Vt;
-    const int k0 = key_begin + t * TK;
-    const int nvalid = min(TK, key_end - k0);
-    if (t + 1 < ntile)
-      R.load(kb_ + (int64_t)(k0 + TK) * D, DO_V ? vb_ + (int64_t)(k0 + TK) * D : nullptr, nullptr,
-             min(TK, key_end - k0 - TK));
-    // The tile's global stores (S or candidates) are issued after the next
-    // tile's LDS store: on gfx9 one counter tracks loads and stores, so the
-    // wait for the prefetched loads would otherwise also wait for them.
-    f32x4 acc[4];
-    uint32_t m[4] = {0u, 0u, 0u, 0u}, pos = 0u, tot = 0u;
-    if (active) {
-      tile_scores<T, D>(acc, Kc, qf);
-      if (SELECT) {
-        // per-kb candidate bits m[kb] (bit r); per-kb counts in bytes
-        if (nvalid == TK && !__ballot(nan_in)) {  // full tile, no -inf pivot in the wave
-#pragma unroll
-          for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) m[kb] |= (acc[kb][r] * scale >= piv) ? 1u << r : 0u;
-        } else {
-#pragma unroll
-          for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const float x = acc[kb][r] * scale;
-              const bool c = x >= piv || (nan_in && x != x);
-              if (c && kb * 16 + 4 * g + r < nvalid) m[kb] |= 1u << r;
-            }
-        }
-        uint32_t packed = 0;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) packed |= (uint32_t)__popc(m[kb]) << (8 * kb);
-        // inclusive scan over the lane groups of landmark p (bytes stay below 17)
-        uint32_t incl = packed;
-        uint32_t y = (uint32_t)__shfl_up((int)incl, 16);
-        if (g >= 1) incl += y;
-        y = (uint32_t)__shfl_up((int)incl, 32);
-        if (g >= 2) incl += y;
-        tot = (uint32_t)__shfl((int)incl, 48 + p);  // per-kb totals of the landmark
-        // byte kb of pos: candidates of the landmark before this lane's block kb
-        pos = (incl - packed) + (tot << 8) + (tot << 16) + (tot << 24);
-      }
-      if (DO_V) tile_softmax_pv<T, D>(st, acc, Vc, nvalid, sl2);
-    }
-    if (t + 1 < ntile) R.store(Ks + (buf ^ 1) * TD::K_ELEMS, DO_V ? Vt + (buf ^ 1) * TD::V_ELEMS : Vt);
-    if (active && write_row) {
-      float *srow = S + row * (int64_t)N + k0;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        const int key = kb * 16 + 4 * g;
-        if (key + 3 < nvalid) {
-          *reinterpret_cast<float4 *>(srow + key) =
-              make_float4(acc[kb][0] * scale, acc[kb][1] * scale, acc[kb][2] * scale, acc[kb][3] * scale);
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (key + r < nvalid) srow[key + r] = acc[kb][r] * scale;
-        }
-      }
-    }
-    if (SELECT && active) {
-      // a lane's candidates of block kb take consecutive entries; addresses
-      // are a 32-bit byte offset from the wave's base (its 16 landmarks'
-      // regions of this chunk)
-      const uint32_t lane_off = ((uint32_t)p * (uint32_t)nchunks * SCORE_NC + listed) * 8u;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        if (!__ballot(m[kb] != 0u)) continue;  // no candidate of this block in the wave
-        uint32_t at = lane_off + ((pos >> (8 * kb)) & 255u) * 8u;
-        const uint32_t ib = (uint32_t)(k0 + kb * 16 + 4 * g);
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (m[kb] & (1u << r)) {
-            *reinterpret_cast<uint2 *>(cand_w + at) = make_uint2(__float_as_uint(acc[kb][r] * scale), ib + r);
-            at += 8u;
-          }
-      }
-      listed += (tot * 0x01010101u) >> 24;
-    }
-    __syncthreads();
-  }
-  if (SELECT && active && lm < M && g == 0) sel.ccnt[row * nchunks + chunk] = listed;
-  if (!DO_V || !active) return;
-  const float l = st.l();
-  if (lm < M) {
-    const int64_t prow = (bh * nchunks + chunk) * M + lm;
-    if (g == 0) part_ml[prow] = make_float2(st.m, l);
-#pragma unroll
-    for (int db = 0; db < D / 16; ++db)
-      *reinterpret_cast<float4 *>(part_o + prow * D + db * 16 + 4 * g) =
-          make_float4(st.o[db][0], st.o[db][1], st.o[db][2], st.o[db][3]);
-  }
-}
-
 template <typename T, int D, bool WRITE_S, bool DO_V, bool SELECT>
 __global__ __launch_bounds__(BLOCK) void scores_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
                                                        const T *__restrict__ v, float *__restrict__ S,
@@ -245,9 +66,7 @@ __global__ __launch_bounds__(BLOCK) void scores_kernel(const T *__restrict__ q_l
                                            blockIdx.x, gridDim.x, blockIdx.y, blockIdx.z, -1);
 }
 
-// Score rows of listed landmark rows (fallback of the fused selection): work
-// item = (listed row, key chunk); each item recomputes the row's 64-landmark
-// block exactly as the score pass does and writes that row only.
+// Score rows of listed landmark rows (fallback of the fused selection).
 template <typename T, int D>
 __global__ __launch_bounds__(BLOCK) void scores_rows_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
                                                             float *__restrict__ S, const uint32_t *__restrict__ nrows,
@@ -255,16 +74,7 @@ __global__ __launch_bounds__(BLOCK) void scores_rows_kernel(const T *__restrict_
                                                             float scale, int nchunks) {
   using TD = TileDims<T, D>;
   __shared__ __align__(16) T Ks[2][TD::K_ELEMS];
-  const int64_t items = (int64_t)*nrows * nchunks;
-  const SelectArgs none{nullptr, nullptr, nullptr};
-  for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
-    const int row = rows[it / nchunks];
-    const int chunk = (int)(it % nchunks);
-    const int lm = row % M;
-    __syncthreads();  // the previous item's last reads of Ks are done
-    score_chunk<T, D, true, false, false>(&Ks[0][0], nullptr, q_lm, k, nullptr, S, nullptr, nullptr, none, N, M,
-                                          scale, chunk, nchunks, lm / 64, row / M, lm);
-  }
+  scores_rows_body<T, D>(&Ks[0][0], (int)blockIdx.x, (int)gridDim.x, q_lm, k, S, nrows, rows, N, M, scale, nchunks);
 }
 
 // Log-sum-exp merge of the per-chunk landmark-value partials, one workgroup

@@ -5,6 +5,8 @@
 #include "flash.hpp"
 #include "kernels.hpp"
 #include "check.hpp"
+#include "scores.hpp"
+#include "topk_row.hpp"
 
 namespace mita {
 
@@ -22,19 +24,24 @@ namespace mita {
 // ---------------------------------------------------------------------------
 constexpr int ROUTE_LB = 64;  // landmarks staged in LDS per step
 
+template <typename T, int D> struct RouteLds {
+  static constexpr int VE = 16 / (int)sizeof(T);
+  static constexpr int LSTR = D + VE;  // padded landmark row (elements)
+  static constexpr int BYTES = ROUTE_LB * LSTR * (int)sizeof(T);
+};
+
+// Workgroup (bx, by) of the routing grid; lms: RouteLds<T, D>::BYTES of LDS,
+// cnt: 4 M words of LDS.
 template <typename T, int D>
-__global__ __launch_bounds__(BLOCK) void route_logits_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
-                                                             int32_t *__restrict__ expert,
-                                                             int32_t *__restrict__ tile_cnt,
-                                                             int32_t *__restrict__ counts, int N, int M,
-                                                             float scale, int ntiles) {
-  constexpr int VE = 16 / (int)sizeof(T);
-  constexpr int LSTR = D + VE;  // padded landmark row (elements)
-  __shared__ __align__(16) T lms[ROUTE_LB * LSTR];
-  extern __shared__ uint32_t cnt[];  // [4][M]
-  const int64_t bh = blockIdx.y;
+__device__ __forceinline__ void route_logits_body(T *lms, uint32_t *cnt, int bx, int by, const T *__restrict__ q,
+                                                  const T *__restrict__ q_lm, int32_t *__restrict__ expert,
+                                                  int32_t *__restrict__ tile_cnt, int32_t *__restrict__ counts, int N,
+                                                  int M, float scale, int ntiles) {
+  constexpr int VE = RouteLds<T, D>::VE;
+  constexpr int LSTR = RouteLds<T, D>::LSTR;
+  const int64_t bh = by;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
-  const int tile = (int)blockIdx.x * 4 + w;
+  const int tile = bx * 4 + w;
   uint32_t *wc = cnt + w * M;
   for (int i = lane; i < M; i += 64) wc[i] = 0u;
   Frag<T> qf[4][D / 32];
@@ -119,6 +126,18 @@ __global__ __launch_bounds__(BLOCK) void route_logits_kernel(const T *__restrict
   }
 }
 
+template <typename T, int D>
+__global__ __launch_bounds__(BLOCK) void route_logits_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
+                                                             int32_t *__restrict__ expert,
+                                                             int32_t *__restrict__ tile_cnt,
+                                                             int32_t *__restrict__ counts, int N, int M,
+                                                             float scale, int ntiles) {
+  __shared__ __align__(16) T lms[RouteLds<T, D>::BYTES / sizeof(T)];
+  extern __shared__ uint32_t cnt[];  // [4][M]
+  route_logits_body<T, D>(lms, cnt, (int)blockIdx.x, (int)blockIdx.y, q, q_lm, expert, tile_cnt, counts, N, M, scale,
+                          ntiles);
+}
+
 // Block-wide exclusive scan of one value per thread (NT threads); returns the
 // exclusive prefix, *total gets the sum.
 template <int NT> __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t *wsum, uint32_t *total) {
@@ -161,18 +180,23 @@ __device__ __forceinline__ uint32_t block_sum256(uint32_t x, uint32_t *wsum) {
 // thread writes its tile's row.
 constexpr int SCAN_EB = 16;
 
-__global__ __launch_bounds__(256) void route_scan_kernel(const int32_t *__restrict__ tile_cnt,
-                                                         const int32_t *__restrict__ counts,
-                                                         int32_t *__restrict__ tile_base,
-                                                         int32_t *__restrict__ offsets,
-                                                         int32_t *__restrict__ tile_start, int ntiles, int M,
-                                                         int N) {
-  __shared__ uint32_t cnt[256][SCAN_EB + 1];
-  __shared__ uint32_t wsum[2][4];
-  __shared__ uint32_t eoff[SCAN_EB];
-  const int e0 = blockIdx.x * SCAN_EB;
+struct ScanLds {
+  uint32_t cnt[256][SCAN_EB + 1];
+  uint32_t wsum[2][4];
+  uint32_t eoff[SCAN_EB];
+};
+
+// Workgroup (bx, by) of the scan grid (ceil(M / SCAN_EB), BH).
+__device__ __forceinline__ void route_scan_body(ScanLds &sh, int bx, int by, const int32_t *__restrict__ tile_cnt,
+                                                const int32_t *__restrict__ counts, int32_t *__restrict__ tile_base,
+                                                int32_t *__restrict__ offsets, int32_t *__restrict__ tile_start,
+                                                int ntiles, int M, int N) {
+  auto &cnt = sh.cnt;
+  auto &wsum = sh.wsum;
+  auto &eoff = sh.eoff;
+  const int e0 = bx * SCAN_EB;
   const int ne = min(SCAN_EB, M - e0);
-  const int64_t bh = blockIdx.y;
+  const int64_t bh = by;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int32_t *cn = counts + bh * M;
 
@@ -237,6 +261,79 @@ __global__ __launch_bounds__(256) void route_scan_kernel(const int32_t *__restri
       for (int j = 0; j < ne; ++j) tb[(int64_t)tt * M + j] = (int32_t)cnt[tid][j];
     __syncthreads();
   }
+}
+
+__global__ __launch_bounds__(256) void route_scan_kernel(const int32_t *__restrict__ tile_cnt,
+                                                         const int32_t *__restrict__ counts,
+                                                         int32_t *__restrict__ tile_base,
+                                                         int32_t *__restrict__ offsets,
+                                                         int32_t *__restrict__ tile_start, int ntiles, int M,
+                                                         int N) {
+  __shared__ ScanLds sh;
+  route_scan_body(sh, (int)blockIdx.x, (int)blockIdx.y, tile_cnt, counts, tile_base, offsets, tile_start, ntiles, M,
+                  N);
+}
+
+// ---------------------------------------------------------------------------
+// The fallback rows of the fused selection combined with routing work in one
+// launch each (the two are independent; normally no row falls back and those
+// workgroups exit at once, so the fallback costs no launch of its own):
+//   rows_logits_kernel: fallback score rows, then the routing logits;
+//   topk_scan_kernel:   fallback top-k rows, then the routing scan.
+// Workgroups [0, nA) take the first part (nA of them, as that kernel's grid),
+// the rest the second (its 2-D grid flattened, x fastest). LDS is one buffer
+// that either part uses for its own layout.
+// ---------------------------------------------------------------------------
+template <typename T, int D> struct RowsLogitsLds {
+  static constexpr int ROWS = 2 * TileDims<T, D>::K_ELEMS * (int)sizeof(T);
+  static constexpr int BYTES = ROWS > RouteLds<T, D>::BYTES ? ROWS : RouteLds<T, D>::BYTES;
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(BLOCK) void rows_logits_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
+                                                            float *__restrict__ S, const uint32_t *__restrict__ nrows,
+                                                            const int32_t *__restrict__ rows, int nchunks, int nA,
+                                                            const T *__restrict__ q, int32_t *__restrict__ expert,
+                                                            int32_t *__restrict__ tile_cnt,
+                                                            int32_t *__restrict__ counts, int N, int M, float scale,
+                                                            int ntiles, int route_x) {
+  __shared__ __align__(16) char buf[RowsLogitsLds<T, D>::BYTES];
+  extern __shared__ uint32_t cnt[];  // routing: [4][M]
+  const int b = (int)blockIdx.x;
+  if (b < nA) {
+    scores_rows_body<T, D>(reinterpret_cast<T *>(buf), b, nA, q_lm, k, S, nrows, rows, N, M, scale, nchunks);
+    return;
+  }
+  const int rb = b - nA;
+  route_logits_body<T, D>(reinterpret_cast<T *>(buf), cnt, rb % route_x, rb / route_x, q, q_lm, expert, tile_cnt,
+                          counts, N, M, scale, ntiles);
+}
+
+template <int CAP, bool VEC, int ROWCAP> struct TopkScanLds {
+  static constexpr int TOPK = (int)((sizeof(TopkSmem<CAP>) + 15) / 16 * 16) + 4 * (ROWCAP > 0 ? ROWCAP : 1);
+  static constexpr int BYTES = TOPK > (int)sizeof(ScanLds) ? TOPK : (int)sizeof(ScanLds);
+};
+
+template <int CAP, bool VEC, int ROWCAP>
+__global__ __launch_bounds__(256) void topk_scan_kernel(const float *__restrict__ S, int32_t *__restrict__ idx, int kk,
+                                                        const uint32_t *__restrict__ nrows,
+                                                        const int32_t *__restrict__ rows, int nA,
+                                                        const int32_t *__restrict__ tile_cnt,
+                                                        const int32_t *__restrict__ counts,
+                                                        int32_t *__restrict__ tile_base, int32_t *__restrict__ offsets,
+                                                        int32_t *__restrict__ tile_start, int ntiles, int M, int N,
+                                                        int scan_x) {
+  __shared__ __align__(16) char buf[TopkScanLds<CAP, VEC, ROWCAP>::BYTES];
+  const int b = (int)blockIdx.x;
+  if (b < nA) {
+    constexpr int LROW = (int)((sizeof(TopkSmem<CAP>) + 15) / 16 * 16);
+    topk_listed_body<CAP, VEC, ROWCAP>(*reinterpret_cast<TopkSmem<CAP> *>(buf), reinterpret_cast<float *>(buf + LROW),
+                                       b, nA, S, idx, N, kk, nrows, rows);
+    return;
+  }
+  const int rb = b - nA;
+  route_scan_body(*reinterpret_cast<ScanLds *>(buf), rb % scan_x, rb / scan_x, tile_cnt, counts, tile_base, offsets,
+                  tile_start, ntiles, M, N);
 }
 
 // Stable grouping (Algorithm 1 ArgSort of the argmax): within a 64-query tile
@@ -629,6 +726,69 @@ hipError_t launch_route(const mita_cfg_t &c, const void *q, const void *q_lm, in
                      : route_t<float, 128>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st);
   return c.d == 64 ? route_t<bf16_t, 64>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st)
                    : route_t<bf16_t, 128>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st);
+}
+
+template <typename T, int D, int CAP, int ROWCAP>
+static hipError_t route_fb_t(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
+                             const SelectBufs &sb, float *S, int32_t *idx, int32_t *expert, int32_t *perm,
+                             int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, int32_t *counts,
+                             int32_t *tile_start, hipStream_t st) {
+  const int nt = route_tiles(c);
+  const int bh = (int)BH(c);
+  const int nch = score_chunks(c);
+  const int64_t rows = (int64_t)bh * c.M;
+  // the fallback grids of scores_rows_kernel and topk_kernel (listed mode)
+  const int nA = (int)(rows * nch < 1024 ? rows * nch : 1024);
+  const int nT = (int)(rows < 512 ? rows : 512);
+  const int route_x = (nt + 3) / 4, scan_x = (c.M + SCAN_EB - 1) / SCAN_EB;
+  hipLaunchKernelGGL((rows_logits_kernel<T, D>), dim3((unsigned)(nA + route_x * bh)), dim3(BLOCK),
+                     4 * c.M * sizeof(uint32_t), st, (const T *)q_lm, (const T *)k, S, sb.fail_cnt, sb.fail_list, nch,
+                     nA, (const T *)q, expert, tile_cnt, counts, c.N, c.M, eff_scale(c), nt, route_x);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  if (c.N % 4 == 0)
+    hipLaunchKernelGGL((topk_scan_kernel<CAP, true, ROWCAP>), dim3((unsigned)(nT + scan_x * bh)), dim3(256), 0, st, S,
+                       idx, c.k, sb.fail_cnt, sb.fail_list, nT, tile_cnt, counts, tile_base, offsets, tile_start, nt,
+                       c.M, c.N, scan_x);
+  else
+    hipLaunchKernelGGL((topk_scan_kernel<CAP, false, ROWCAP>), dim3((unsigned)(nT + scan_x * bh)), dim3(256), 0, st, S,
+                       idx, c.k, sb.fail_cnt, sb.fail_list, nT, tile_cnt, counts, tile_base, offsets, tile_start, nt,
+                       c.M, c.N, scan_x);
+  if ((err = hipGetLastError()) != hipSuccess) return err;
+  int ebits = 0;
+  while ((1 << ebits) < c.M) ++ebits;
+  hipLaunchKernelGGL(route_scatter_kernel, dim3((unsigned)route_x, (unsigned)bh), dim3(256), 0, st, expert, tile_base,
+                     perm, c.N, c.M, nt, ebits);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+static hipError_t route_fb_n(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
+                             const SelectBufs &sb, float *S, int32_t *idx, int32_t *expert, int32_t *perm,
+                             int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, int32_t *counts,
+                             int32_t *tile_start, hipStream_t st) {
+  // the fallback rows are streamed from memory (no LDS row copy), so the
+  // scan workgroups of the same launch keep a small LDS footprint
+  if (c.N <= 16384)
+    return route_fb_t<T, D, 512, 0>(c, q, q_lm, k, sb, S, idx, expert, perm, offsets, tile_cnt, tile_base, counts,
+                                    tile_start, st);
+  return route_fb_t<T, D, 2048, 0>(c, q, q_lm, k, sb, S, idx, expert, perm, offsets, tile_cnt, tile_base, counts,
+                                   tile_start, st);
+}
+
+hipError_t launch_route_fallbacks(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
+                                  const SelectBufs &sb, float *S, int32_t *idx, int32_t *expert, int32_t *perm,
+                                  int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, int32_t *counts,
+                                  int32_t *tile_start, hipStream_t st) {
+  if (c.dtype == MITA_F32)
+    return c.d == 64 ? route_fb_n<float, 64>(c, q, q_lm, k, sb, S, idx, expert, perm, offsets, tile_cnt, tile_base,
+                                             counts, tile_start, st)
+                     : route_fb_n<float, 128>(c, q, q_lm, k, sb, S, idx, expert, perm, offsets, tile_cnt, tile_base,
+                                              counts, tile_start, st);
+  return c.d == 64 ? route_fb_n<bf16_t, 64>(c, q, q_lm, k, sb, S, idx, expert, perm, offsets, tile_cnt, tile_base,
+                                            counts, tile_start, st)
+                   : route_fb_n<bf16_t, 128>(c, q, q_lm, k, sb, S, idx, expert, perm, offsets, tile_cnt, tile_base,
+                                             counts, tile_start, st);
 }
 
 hipError_t launch_worklist(const mita_cfg_t &c, const int32_t *offsets, int32_t *tile_start, hipStream_t st) {

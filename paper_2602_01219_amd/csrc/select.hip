@@ -393,8 +393,8 @@ hipError_t launch_select_pivots(const mita_cfg_t &c, const void *q_lm, const voi
   return hipGetLastError();
 }
 
-hipError_t launch_select_finish(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sb, float *S,
-                                int32_t *idx, const void *partial, void *v_lm, hipStream_t st) {
+hipError_t launch_select_finalize(const mita_cfg_t &c, const SelectBufs &sb, int32_t *idx, const void *partial,
+                                  void *v_lm, hipStream_t st) {
   const unsigned rows = (unsigned)(BH(c) * c.M);
   const int nch = score_chunks(c);
   const float2 *ml = (const float2 *)partial;
@@ -427,7 +427,12 @@ hipError_t launch_select_finish(const mita_cfg_t &c, const void *q_lm, const voi
   }
 #undef MITA_FINALIZE_CAP
 #undef MITA_FINALIZE
-  hipError_t e = hipGetLastError();
+  return hipGetLastError();
+}
+
+hipError_t launch_select_finish(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sb, float *S,
+                                int32_t *idx, const void *partial, void *v_lm, hipStream_t st) {
+  hipError_t e = launch_select_finalize(c, sb, idx, partial, v_lm, st);
   if (e != hipSuccess) return e;
   if ((e = launch_scores_rows(c, q_lm, k, S, sb.fail_cnt, sb.fail_list, st)) != hipSuccess) return e;
   return launch_topk(c, S, idx, st, sb.fail_cnt, sb.fail_list);
