@@ -47,13 +47,6 @@ hipError_t launch_select_pivots(const mita_cfg_t &c, const void *q_lm, const voi
 hipError_t launch_select_finish(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sel,
                                 float *S, int32_t *idx, const void *partial, void *v_lm, hipStream_t st);
 
-// The finalize step of launch_select_finish alone: exact top-k from the
-// candidate lists into idx, unusable rows appended to the fallback list, and
-// (with v_lm) the landmark-value merge. The fallback rows are then left to
-// launch_route_fallbacks.
-hipError_t launch_select_finalize(const mita_cfg_t &c, const SelectBufs &sel, int32_t *idx, const void *partial,
-                                  void *v_lm, hipStream_t st);
-
 // Score rows of the listed landmark rows only (fallback of the fused selection).
 hipError_t launch_scores_rows(const mita_cfg_t &c, const void *q_lm, const void *k, float *S,
                               const uint32_t *nrows, const int32_t *rows, hipStream_t st);
@@ -73,13 +66,13 @@ hipError_t launch_route(const mita_cfg_t &c, const void *q, const void *q_lm, in
                         int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, int32_t *counts,
                         int32_t *tile_start, hipStream_t st);
 
-// Routing (as launch_route) with the fallback rows of the fused selection
-// (after launch_select_finalize) done in the same launches: their score rows
-// into S and their exact top-k into idx.
-hipError_t launch_route_fallbacks(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
-                                  const SelectBufs &sel, float *S, int32_t *idx, int32_t *expert, int32_t *perm,
-                                  int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, int32_t *counts,
-                                  int32_t *tile_start, hipStream_t st);
+// The finish of the fused selection (launch_select_finish: top-k into idx,
+// fallback rows, landmark-value merge into v_lm when given) together with the
+// routing (launch_route), in three combined launches.
+hipError_t launch_select_route(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
+                               const SelectBufs &sel, float *S, int32_t *idx, const void *partial, void *v_lm,
+                               int32_t *expert, int32_t *perm, int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base,
+                               int32_t *counts, int32_t *tile_start, hipStream_t st);
 
 // Attention work list from offsets: tile_start [BH, M+1].
 hipError_t launch_worklist(const mita_cfg_t &c, const int32_t *offsets, int32_t *tile_start, hipStream_t st);

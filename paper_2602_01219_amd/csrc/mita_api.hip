@@ -120,21 +120,19 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
   TRY(hip_status(launch_scores(*c, q_lm, k, v, fused ? nullptr : S, v_lm, w + L.partial, fused ? &sel : nullptr, st),
                  "scores"));
   TRY(mark(2));
-  // with the fused selection and in-place gather, the selection's fallback
-  // rows ride in the routing launches (the "route" stage then includes them)
-  const bool fb_in_route = fused && c->use_routed && !staged;
-  if (fb_in_route)
-    TRY(hip_status(launch_select_finalize(*c, sel, idx, w + L.partial, v_lm, st), "topk"));
-  else if (fused)
+  // with the fused selection and in-place gather, the selection's finish
+  // shares launches with the routing (the "route" stage then includes it)
+  const bool sel_in_route = fused && c->use_routed && !staged;
+  if (fused && !sel_in_route)
     TRY(hip_status(launch_select_finish(*c, q_lm, k, sel, S, idx, w + L.partial, v_lm, st), "topk"));
-  else if (c->use_routed)
+  else if (!fused && c->use_routed)
     TRY(hip_status(launch_topk(*c, S, idx, st), "topk"));
   TRY(mark(3));
   if (staged) TRY(hip_status(launch_gather(*c, k, v, idx, kx, vx, st), "gather"));
   TRY(mark(4));
-  if (fb_in_route)
-    TRY(hip_status(launch_route_fallbacks(*c, q, q_lm, k, sel, S, idx, expert, perm, offsets, tile_cnt, tile_base,
-                                          counts, tile_start, st),
+  if (sel_in_route)
+    TRY(hip_status(launch_select_route(*c, q, q_lm, k, sel, S, idx, w + L.partial, v_lm, expert, perm, offsets,
+                                       tile_cnt, tile_base, counts, tile_start, st),
                    "route"));
   else if (c->use_routed)
     TRY(hip_status(launch_route(*c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st),

@@ -7,6 +7,7 @@
 #include "check.hpp"
 #include "scores.hpp"
 #include "topk_row.hpp"
+#include "finalize.hpp"
 
 namespace mita {
 
@@ -274,77 +275,14 @@ __global__ __launch_bounds__(256) void route_scan_kernel(const int32_t *__restri
                   N);
 }
 
-// ---------------------------------------------------------------------------
-// The fallback rows of the fused selection combined with routing work in one
-// launch each (the two are independent; normally no row falls back and those
-// workgroups exit at once, so the fallback costs no launch of its own):
-//   rows_logits_kernel: fallback score rows, then the routing logits;
-//   topk_scan_kernel:   fallback top-k rows, then the routing scan.
-// Workgroups [0, nA) take the first part (nA of them, as that kernel's grid),
-// the rest the second (its 2-D grid flattened, x fastest). LDS is one buffer
-// that either part uses for its own layout.
-// ---------------------------------------------------------------------------
-template <typename T, int D> struct RowsLogitsLds {
-  static constexpr int ROWS = 2 * TileDims<T, D>::K_ELEMS * (int)sizeof(T);
-  static constexpr int BYTES = ROWS > RouteLds<T, D>::BYTES ? ROWS : RouteLds<T, D>::BYTES;
-};
-
-template <typename T, int D>
-__global__ __launch_bounds__(BLOCK) void rows_logits_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
-                                                            float *__restrict__ S, const uint32_t *__restrict__ nrows,
-                                                            const int32_t *__restrict__ rows, int nchunks, int nA,
-                                                            const T *__restrict__ q, int32_t *__restrict__ expert,
-                                                            int32_t *__restrict__ tile_cnt,
-                                                            int32_t *__restrict__ counts, int N, int M, float scale,
-                                                            int ntiles, int route_x) {
-  __shared__ __align__(16) char buf[RowsLogitsLds<T, D>::BYTES];
-  extern __shared__ uint32_t cnt[];  // routing: [4][M]
-  const int b = (int)blockIdx.x;
-  if (b < nA) {
-    scores_rows_body<T, D>(reinterpret_cast<T *>(buf), b, nA, q_lm, k, S, nrows, rows, N, M, scale, nchunks);
-    return;
-  }
-  const int rb = b - nA;
-  route_logits_body<T, D>(reinterpret_cast<T *>(buf), cnt, rb % route_x, rb / route_x, q, q_lm, expert, tile_cnt,
-                          counts, N, M, scale, ntiles);
-}
-
-template <int CAP, bool VEC, int ROWCAP> struct TopkScanLds {
-  static constexpr int TOPK = (int)((sizeof(TopkSmem<CAP>) + 15) / 16 * 16) + 4 * (ROWCAP > 0 ? ROWCAP : 1);
-  static constexpr int BYTES = TOPK > (int)sizeof(ScanLds) ? TOPK : (int)sizeof(ScanLds);
-};
-
-template <int CAP, bool VEC, int ROWCAP>
-__global__ __launch_bounds__(256) void topk_scan_kernel(const float *__restrict__ S, int32_t *__restrict__ idx, int kk,
-                                                        const uint32_t *__restrict__ nrows,
-                                                        const int32_t *__restrict__ rows, int nA,
-                                                        const int32_t *__restrict__ tile_cnt,
-                                                        const int32_t *__restrict__ counts,
-                                                        int32_t *__restrict__ tile_base, int32_t *__restrict__ offsets,
-                                                        int32_t *__restrict__ tile_start, int ntiles, int M, int N,
-                                                        int scan_x) {
-  __shared__ __align__(16) char buf[TopkScanLds<CAP, VEC, ROWCAP>::BYTES];
-  const int b = (int)blockIdx.x;
-  if (b < nA) {
-    constexpr int LROW = (int)((sizeof(TopkSmem<CAP>) + 15) / 16 * 16);
-    topk_listed_body<CAP, VEC, ROWCAP>(*reinterpret_cast<TopkSmem<CAP> *>(buf), reinterpret_cast<float *>(buf + LROW),
-                                       b, nA, S, idx, N, kk, nrows, rows);
-    return;
-  }
-  const int rb = b - nA;
-  route_scan_body(*reinterpret_cast<ScanLds *>(buf), rb % scan_x, rb / scan_x, tile_cnt, counts, tile_base, offsets,
-                  tile_start, ntiles, M, N);
-}
-
 // Stable grouping (Algorithm 1 ArgSort of the argmax): within a 64-query tile
 // (one wave), a query's rank among earlier queries of the same expert comes
 // from matching expert ids bit by bit with ballots.
-__global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t *__restrict__ expert,
-                                                            const int32_t *__restrict__ tile_base,
-                                                            int32_t *__restrict__ perm, int N, int M, int ntiles,
-                                                            int ebits) {
-  const int64_t bh = blockIdx.y;
-  const int tile = blockIdx.x * 4 + (threadIdx.x >> 6);
+__device__ __forceinline__ void route_scatter_body(int bx, int by, const int32_t *__restrict__ expert,
+                                                   const int32_t *__restrict__ tile_base, int32_t *__restrict__ perm,
+                                                   int N, int M, int ntiles, int ebits) {
+  const int64_t bh = by;
+  const int tile = bx * 4 + (threadIdx.x >> 6);
   if (tile >= ntiles) return;
   const int n = tile * ROUTE_TQ + (threadIdx.x & 63);
   const bool valid = n < N;
@@ -359,6 +297,105 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t *__res
     const int pos = tile_base[(bh * ntiles + tile) * (int64_t)M + e] + (int)lanes_below(same);
     perm[bh * N + pos] = n;
   }
+}
+
+__global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t *__restrict__ expert,
+                                                            const int32_t *__restrict__ tile_base,
+                                                            int32_t *__restrict__ perm, int N, int M, int ntiles,
+                                                            int ebits) {
+  route_scatter_body((int)blockIdx.x, (int)blockIdx.y, expert, tile_base, perm, N, M, ntiles, ebits);
+}
+
+// ---------------------------------------------------------------------------
+// The finish of the fused selection and the routing, which do not depend on
+// each other, share launches, so that the latency-bound selection work and
+// the routing work fill one another's idle time and the fallback steps (which
+// normally have nothing to do) cost no launch of their own:
+//   finalize_logits_kernel: selection finalize rows | routing logits;
+//   rows_scan_kernel:       fallback score rows     | routing scan;
+//   topk_scatter_kernel:    fallback top-k rows     | routing scatter.
+// The routing part's 2-D grid is flattened (x fastest). LDS is one buffer
+// that either part lays out for itself.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int CAP, bool MERGE> struct FinalizeLogitsLds {
+  static constexpr int F = (int)sizeof(FinalizeLds<T, D, CAP, MERGE>);
+  static constexpr int BYTES = F > RouteLds<T, D>::BYTES ? F : RouteLds<T, D>::BYTES;
+};
+
+// Finalize rows and routing workgroups interleave one to one while both last,
+// so the two kinds run side by side.
+template <typename T, int D, int CAP, bool MERGE>
+__global__ __launch_bounds__(BLOCK) void finalize_logits_kernel(
+    const uint2 *__restrict__ cand, const uint32_t *__restrict__ ccnt, int32_t *__restrict__ idx,
+    uint32_t *__restrict__ fail_cnt, int32_t *__restrict__ fail_list, int k, int cap, int nch,
+    const float2 *__restrict__ part_ml, const float *__restrict__ part_o, T *__restrict__ v_lm, int nF,
+    const T *__restrict__ q, const T *__restrict__ q_lm, int32_t *__restrict__ expert, int32_t *__restrict__ tile_cnt,
+    int32_t *__restrict__ counts, int N, int M, float scale, int ntiles, int route_x, int nR) {
+  __shared__ __align__(16) char buf[FinalizeLogitsLds<T, D, CAP, MERGE>::BYTES];
+  extern __shared__ uint32_t cnt[];  // routing: [4][M]
+  const int b = (int)blockIdx.x, lo = min(nF, nR);
+  bool fin;
+  int i;
+  if (b < 2 * lo) {
+    fin = (b & 1) == 0;
+    i = b >> 1;
+  } else {
+    fin = nF > nR;
+    i = b - lo;
+  }
+  if (fin) {
+    finalize_row<T, D, CAP, MERGE>(*reinterpret_cast<FinalizeLds<T, D, CAP, MERGE> *>(buf), i, cand, ccnt, idx,
+                                   fail_cnt, fail_list, k, cap, nch, part_ml, part_o, v_lm, M);
+    return;
+  }
+  route_logits_body<T, D>(reinterpret_cast<T *>(buf), cnt, i % route_x, i / route_x, q, q_lm, expert, tile_cnt, counts,
+                          N, M, scale, ntiles);
+}
+
+template <typename T, int D> struct RowsScanLds {
+  static constexpr int ROWS = 2 * TileDims<T, D>::K_ELEMS * (int)sizeof(T);
+  static constexpr int BYTES = ROWS > (int)sizeof(ScanLds) ? ROWS : (int)sizeof(ScanLds);
+};
+
+// Workgroups [0, nA) walk the fallback score-row items, the rest scan.
+template <typename T, int D>
+__global__ __launch_bounds__(BLOCK) void rows_scan_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
+                                                          float *__restrict__ S, const uint32_t *__restrict__ nrows,
+                                                          const int32_t *__restrict__ rows, int nchunks, int nA,
+                                                          float scale, const int32_t *__restrict__ tile_cnt,
+                                                          const int32_t *__restrict__ counts,
+                                                          int32_t *__restrict__ tile_base,
+                                                          int32_t *__restrict__ offsets, int32_t *__restrict__ tile_start,
+                                                          int ntiles, int M, int N, int scan_x) {
+  __shared__ __align__(16) char buf[RowsScanLds<T, D>::BYTES];
+  const int b = (int)blockIdx.x;
+  if (b < nA) {
+    scores_rows_body<T, D>(reinterpret_cast<T *>(buf), b, nA, q_lm, k, S, nrows, rows, N, M, scale, nchunks);
+    return;
+  }
+  const int rb = b - nA;
+  route_scan_body(*reinterpret_cast<ScanLds *>(buf), rb % scan_x, rb / scan_x, tile_cnt, counts, tile_base, offsets,
+                  tile_start, ntiles, M, N);
+}
+
+// Workgroups [0, nT) walk the fallback rows' top-k (rows streamed from
+// memory: a small LDS footprint for the scatter workgroups), the rest scatter.
+template <int CAP, bool VEC>
+__global__ __launch_bounds__(256) void topk_scatter_kernel(const float *__restrict__ S, int32_t *__restrict__ idx,
+                                                           int kk, const uint32_t *__restrict__ nrows,
+                                                           const int32_t *__restrict__ rows, int nT,
+                                                           const int32_t *__restrict__ expert,
+                                                           const int32_t *__restrict__ tile_base,
+                                                           int32_t *__restrict__ perm, int N, int M, int ntiles,
+                                                           int ebits, int route_x) {
+  __shared__ TopkSmem<CAP> sh;
+  const int b = (int)blockIdx.x;
+  if (b < nT) {
+    topk_listed_body<CAP, VEC, 0>(sh, nullptr, b, nT, S, idx, N, kk, nrows, rows);
+    return;
+  }
+  const int rb = b - nT;
+  route_scatter_body(rb % route_x, rb / route_x, expert, tile_base, perm, N, M, ntiles, ebits);
 }
 
 // Attention work list: tile_start[e] = sum over e' < e of ceil(size(e') / 64),
@@ -728,67 +765,77 @@ hipError_t launch_route(const mita_cfg_t &c, const void *q, const void *q_lm, in
                    : route_t<bf16_t, 128>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st);
 }
 
-template <typename T, int D, int CAP, int ROWCAP>
-static hipError_t route_fb_t(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
-                             const SelectBufs &sb, float *S, int32_t *idx, int32_t *expert, int32_t *perm,
-                             int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, int32_t *counts,
-                             int32_t *tile_start, hipStream_t st) {
+template <typename T, int D, int CAP, bool MERGE>
+static hipError_t select_route_t(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
+                                 const SelectBufs &sb, float *S, int32_t *idx, const void *partial, void *v_lm,
+                                 int32_t *expert, int32_t *perm, int32_t *offsets, int32_t *tile_cnt,
+                                 int32_t *tile_base, int32_t *counts, int32_t *tile_start, hipStream_t st) {
   const int nt = route_tiles(c);
   const int bh = (int)BH(c);
   const int nch = score_chunks(c);
   const int64_t rows = (int64_t)bh * c.M;
+  const float2 *ml = (const float2 *)partial;
+  const float *po = MERGE ? (const float *)((const char *)partial + align_up((size_t)rows * nch * sizeof(float2)))
+                          : nullptr;
+  const int route_x = (nt + 3) / 4, scan_x = (c.M + SCAN_EB - 1) / SCAN_EB;
+  const int nF = (int)rows, nR = route_x * bh;
+  hipLaunchKernelGGL((finalize_logits_kernel<T, D, CAP, MERGE>), dim3((unsigned)(nF + nR)), dim3(BLOCK),
+                     4 * c.M * sizeof(uint32_t), st, sb.cand, sb.ccnt, idx, sb.fail_cnt, sb.fail_list, c.k, sb.cap,
+                     nch, ml, po, (T *)v_lm, nF, (const T *)q, (const T *)q_lm, expert, tile_cnt, counts, c.N, c.M,
+                     eff_scale(c), nt, route_x, nR);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
   // the fallback grids of scores_rows_kernel and topk_kernel (listed mode)
   const int nA = (int)(rows * nch < 1024 ? rows * nch : 1024);
   const int nT = (int)(rows < 512 ? rows : 512);
-  const int route_x = (nt + 3) / 4, scan_x = (c.M + SCAN_EB - 1) / SCAN_EB;
-  hipLaunchKernelGGL((rows_logits_kernel<T, D>), dim3((unsigned)(nA + route_x * bh)), dim3(BLOCK),
-                     4 * c.M * sizeof(uint32_t), st, (const T *)q_lm, (const T *)k, S, sb.fail_cnt, sb.fail_list, nch,
-                     nA, (const T *)q, expert, tile_cnt, counts, c.N, c.M, eff_scale(c), nt, route_x);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
-  if (c.N % 4 == 0)
-    hipLaunchKernelGGL((topk_scan_kernel<CAP, true, ROWCAP>), dim3((unsigned)(nT + scan_x * bh)), dim3(256), 0, st, S,
-                       idx, c.k, sb.fail_cnt, sb.fail_list, nT, tile_cnt, counts, tile_base, offsets, tile_start, nt,
-                       c.M, c.N, scan_x);
-  else
-    hipLaunchKernelGGL((topk_scan_kernel<CAP, false, ROWCAP>), dim3((unsigned)(nT + scan_x * bh)), dim3(256), 0, st, S,
-                       idx, c.k, sb.fail_cnt, sb.fail_list, nT, tile_cnt, counts, tile_base, offsets, tile_start, nt,
-                       c.M, c.N, scan_x);
+  hipLaunchKernelGGL((rows_scan_kernel<T, D>), dim3((unsigned)(nA + scan_x * bh)), dim3(BLOCK), 0, st,
+                     (const T *)q_lm, (const T *)k, S, sb.fail_cnt, sb.fail_list, nch, nA, eff_scale(c), tile_cnt,
+                     counts, tile_base, offsets, tile_start, nt, c.M, c.N, scan_x);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   int ebits = 0;
   while ((1 << ebits) < c.M) ++ebits;
-  hipLaunchKernelGGL(route_scatter_kernel, dim3((unsigned)route_x, (unsigned)bh), dim3(256), 0, st, expert, tile_base,
-                     perm, c.N, c.M, nt, ebits);
+  constexpr int TCAP = 512;
+  if (c.N % 4 == 0)
+    hipLaunchKernelGGL((topk_scatter_kernel<TCAP, true>), dim3((unsigned)(nT + nR)), dim3(256), 0, st, S, idx, c.k,
+                       sb.fail_cnt, sb.fail_list, nT, expert, tile_base, perm, c.N, c.M, nt, ebits, route_x);
+  else
+    hipLaunchKernelGGL((topk_scatter_kernel<TCAP, false>), dim3((unsigned)(nT + nR)), dim3(256), 0, st, S, idx, c.k,
+                       sb.fail_cnt, sb.fail_list, nT, expert, tile_base, perm, c.N, c.M, nt, ebits, route_x);
   return hipGetLastError();
 }
 
 template <typename T, int D>
-static hipError_t route_fb_n(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
-                             const SelectBufs &sb, float *S, int32_t *idx, int32_t *expert, int32_t *perm,
-                             int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, int32_t *counts,
-                             int32_t *tile_start, hipStream_t st) {
-  // the fallback rows are streamed from memory (no LDS row copy), so the
-  // scan workgroups of the same launch keep a small LDS footprint
-  if (c.N <= 16384)
-    return route_fb_t<T, D, 512, 0>(c, q, q_lm, k, sb, S, idx, expert, perm, offsets, tile_cnt, tile_base, counts,
-                                    tile_start, st);
-  return route_fb_t<T, D, 2048, 0>(c, q, q_lm, k, sb, S, idx, expert, perm, offsets, tile_cnt, tile_base, counts,
-                                   tile_start, st);
+static hipError_t select_route_n(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
+                                 const SelectBufs &sb, float *S, int32_t *idx, const void *partial, void *v_lm,
+                                 int32_t *expert, int32_t *perm, int32_t *offsets, int32_t *tile_cnt,
+                                 int32_t *tile_base, int32_t *counts, int32_t *tile_start, hipStream_t st) {
+#define MITA_SR(CAP, MG)                                                                                       \
+  return select_route_t<T, D, CAP, MG>(c, q, q_lm, k, sb, S, idx, partial, v_lm, expert, perm, offsets, tile_cnt, \
+                                       tile_base, counts, tile_start, st)
+  if (v_lm) {
+    if (sb.cap <= 1024) MITA_SR(1024, true);
+    if (sb.cap <= 2048) MITA_SR(2048, true);
+    MITA_SR(SEL_CAP, true);
+  }
+  if (sb.cap <= 1024) MITA_SR(1024, false);
+  if (sb.cap <= 2048) MITA_SR(2048, false);
+  MITA_SR(SEL_CAP, false);
+#undef MITA_SR
 }
 
-hipError_t launch_route_fallbacks(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
-                                  const SelectBufs &sb, float *S, int32_t *idx, int32_t *expert, int32_t *perm,
-                                  int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, int32_t *counts,
-                                  int32_t *tile_start, hipStream_t st) {
+hipError_t launch_select_route(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
+                               const SelectBufs &sb, float *S, int32_t *idx, const void *partial, void *v_lm,
+                               int32_t *expert, int32_t *perm, int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base,
+                               int32_t *counts, int32_t *tile_start, hipStream_t st) {
   if (c.dtype == MITA_F32)
-    return c.d == 64 ? route_fb_n<float, 64>(c, q, q_lm, k, sb, S, idx, expert, perm, offsets, tile_cnt, tile_base,
-                                             counts, tile_start, st)
-                     : route_fb_n<float, 128>(c, q, q_lm, k, sb, S, idx, expert, perm, offsets, tile_cnt, tile_base,
-                                              counts, tile_start, st);
-  return c.d == 64 ? route_fb_n<bf16_t, 64>(c, q, q_lm, k, sb, S, idx, expert, perm, offsets, tile_cnt, tile_base,
-                                            counts, tile_start, st)
-                   : route_fb_n<bf16_t, 128>(c, q, q_lm, k, sb, S, idx, expert, perm, offsets, tile_cnt, tile_base,
-                                             counts, tile_start, st);
+    return c.d == 64 ? select_route_n<float, 64>(c, q, q_lm, k, sb, S, idx, partial, v_lm, expert, perm, offsets,
+                                                 tile_cnt, tile_base, counts, tile_start, st)
+                     : select_route_n<float, 128>(c, q, q_lm, k, sb, S, idx, partial, v_lm, expert, perm, offsets,
+                                                  tile_cnt, tile_base, counts, tile_start, st);
+  return c.d == 64 ? select_route_n<bf16_t, 64>(c, q, q_lm, k, sb, S, idx, partial, v_lm, expert, perm, offsets,
+                                                tile_cnt, tile_base, counts, tile_start, st)
+                   : select_route_n<bf16_t, 128>(c, q, q_lm, k, sb, S, idx, partial, v_lm, expert, perm, offsets,
+                                                 tile_cnt, tile_base, counts, tile_start, st);
 }
 
 hipError_t launch_worklist(const mita_cfg_t &c, const int32_t *offsets, int32_t *tile_start, hipStream_t st) {

@@ -25,6 +25,7 @@
 #include "flash.hpp"
 #include "kernels.hpp"
 #include "check.hpp"
+#include "finalize.hpp"
 
 namespace mita {
 
@@ -197,22 +198,7 @@ __global__ __launch_bounds__(256) void pivot_kernel(const uint32_t *__restrict__
   if (lane == 0) plo[row] = lo;
 }
 
-// ---------------------------------------------------------------------------
-// Exact top-k from the candidate lists: one workgroup per landmark row. The
-// order is that of the composite C = key * 2^32 + (2^32 - 1 - index), larger
-// first; composites are distinct, so exactly k tokens have C >= C_k, the k-th
-// largest. The row's chunk regions are packed into LDS (token order kept);
-// radix rounds over a 256-bin histogram of the current composite range (each
-// round shrinks the range by 2^8) run until at most 64 candidates remain,
-// which one wave ranks directly; an ordered scan then writes the tokens with
-// C >= C_k.
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ uint64_t composite(uint2 e) {
-  return ((uint64_t)e.x << 32) | (uint64_t)(0xffffffffu - e.y);
-}
-
-constexpr int MAX_CHUNKS = MITA_MAX_N / SCORE_NC;
-
+// One workgroup per landmark row.
 template <typename T, int D, int CAP, bool MERGE>
 __global__ __launch_bounds__(256) void finalize_kernel(const uint2 *__restrict__ cand,
                                                        const uint32_t *__restrict__ ccnt, int32_t *__restrict__ idx,
@@ -220,152 +206,9 @@ __global__ __launch_bounds__(256) void finalize_kernel(const uint2 *__restrict__
                                                        int32_t *__restrict__ fail_list, int k, int cap, int nch,
                                                        const float2 *__restrict__ part_ml,
                                                        const float *__restrict__ part_o, T *__restrict__ v_lm, int M) {
-  __shared__ float red[MERGE ? 256 / D : 1][3][D];
-  __shared__ uint2 lst[CAP];
-  __shared__ uint32_t pre[MAX_CHUNKS + 1];
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t wsum[2][4];
-  __shared__ uint64_t wred[2][4];
-  __shared__ uint64_t rem[64];
-  __shared__ uint64_t bc64;
-  __shared__ uint32_t bc[3];
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-  const int64_t row = blockIdx.x;
-  // the landmark-value partials are loaded first; the merge uses them last
-  LandmarkMerge<T, D> lmm;
-  if (MERGE) lmm.prefetch(part_ml, part_o, row / M, (int)(row % M), M, nch);
-
-  // chunk counts -> exclusive prefix (nch <= 256: one chunk per thread)
-  const uint32_t cc = tid < nch ? ccnt[row * nch + tid] : 0u;
-  const uint32_t wincl = wave_inclusive_scan(cc);
-  if (lane == 63) wsum[0][w] = wincl;
-  __syncthreads();
-  uint32_t before = 0, total = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    before += i < w ? wsum[0][i] : 0u;
-    total += wsum[0][i];
-  }
-  if (tid <= nch) pre[tid] = before + wincl - cc;
-  if (total < (uint32_t)k || total > (uint32_t)cap) {  // uniform
-    if (tid == 0) fail_list[atomicAdd(fail_cnt, 1u)] = (int32_t)row;
-    if (MERGE) lmm.finish(part_ml, part_o, v_lm, row / M, (int)(row % M), M, nch, red);
-    return;
-  }
-  __syncthreads();
-  // compaction into LDS, with the composite range of the list
-  const int L = (int)total;
-  uint64_t lo = ~0ull, hi = 0ull;
-  for (int i = tid; i < L; i += 256) {
-    int a = 0, b = nch - 1;  // last chunk c with pre[c] <= i
-    while (a < b) {
-      const int mid = (a + b + 1) >> 1;
-      if (pre[mid] <= (uint32_t)i)
-        a = mid;
-      else
-        b = mid - 1;
-    }
-    const uint2 e = cand[(row * nch + a) * (int64_t)SCORE_NC + (i - (int)pre[a])];
-    const uint2 x = make_uint2(score_key(__uint_as_float(e.x)), e.y);  // listed as float bits
-    lst[i] = x;
-    const uint64_t c = composite(x);
-    lo = c < lo ? c : lo;
-    hi = c > hi ? c : hi;
-  }
-  lo = wave_min_u64(lo);
-  hi = wave_max_u64(hi);
-  if (lane == 0) {
-    wred[0][w] = lo;
-    wred[1][w] = hi;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    lo = wred[0][i] < lo ? wred[0][i] : lo;
-    hi = wred[1][i] > hi ? wred[1][i] : hi;
-  }
-  uint32_t need = (uint32_t)k, inrange = (uint32_t)L;
-  uint64_t ck = 0;
-  while (true) {
-    if (lo == hi) {  // a single composite left
-      ck = lo;
-      break;
-    }
-    if (inrange <= 64u) {
-      if (tid == 0) bc[0] = 0u;
-      __syncthreads();
-      for (int i = tid; i < L; i += 256) {
-        const uint64_t c = composite(lst[i]);
-        if (c >= lo && c <= hi) {
-          const uint32_t s = atomicAdd(&bc[0], 1u);
-          if (s < 64u) rem[s] = c;
-        }
-      }
-      __syncthreads();
-      if (w == 0) {
-        const uint64_t mine = lane < (int)inrange ? rem[lane] : 0ull;
-        uint32_t rank = 0;
-        for (uint32_t j = 0; j < inrange; ++j) rank += rem[j] > mine;
-        if (lane < (int)inrange && rank == need - 1u) bc64 = mine;
-      }
-      __syncthreads();
-      ck = bc64;
-      break;
-    }
-    const uint64_t span = hi - lo;
-    const int bits = 64 - __clzll((long long)span);
-    const int shift = bits > 8 ? bits - 8 : 0;
-    hist[tid] = 0u;
-    __syncthreads();
-    for (int i = tid; i < L; i += 256) {
-      const uint64_t c = composite(lst[i]);
-      if (c >= lo && c <= hi) atomicAdd(&hist[(uint32_t)((c - lo) >> shift)], 1u);
-    }
-    __syncthreads();
-    // thread t takes bin 255 - t: the scan runs from the top bin down
-    const uint32_t cnt = hist[255 - tid];
-    const uint32_t incl = wave_inclusive_scan(cnt);
-    if (lane == 63) wsum[1][w] = incl;
-    __syncthreads();
-    uint32_t ab = incl - cnt;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) ab += i < w ? wsum[1][i] : 0u;
-    if (ab < need && need <= ab + cnt) {
-      bc[0] = (uint32_t)(255 - tid);
-      bc[1] = ab;
-      bc[2] = cnt;
-    }
-    __syncthreads();
-    const uint32_t b = bc[0];
-    need -= bc[1];
-    inrange = bc[2];
-    lo += (uint64_t)b << shift;
-    const uint64_t width = (1ull << shift) - 1ull;
-    if (hi - lo > width) hi = lo + width;
-    __syncthreads();  // bc and hist are rewritten by the next round
-  }
-
-  // ordered output: the list is in ascending token order; thread t takes
-  // entries [t E, t E + E) and one block scan places its selected ones
-  int32_t *out = idx + row * (int64_t)k;
-  const int E = (L + 255) / 256;
-  const int i0 = tid * E, i1 = min(L, i0 + E);
-  uint32_t nsel = 0;
-  for (int i = i0; i < i1; ++i) nsel += composite(lst[i]) >= ck;
-  const uint32_t sincl = wave_inclusive_scan(nsel);
-  if (lane == 63) wsum[0][w] = sincl;  // wsum[0] was last read before the compaction
-  __syncthreads();
-  uint32_t at = sincl - nsel;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) at += j < w ? wsum[0][j] : 0u;
-  for (int i = i0; i < i1; ++i) {
-    const uint2 e = lst[i];
-    if (composite(e) >= ck) {
-      if (at < (uint32_t)k) out[at] = (int32_t)e.y;
-      ++at;
-    }
-  }
-  if (MERGE) lmm.finish(part_ml, part_o, v_lm, row / M, (int)(row % M), M, nch, red);
+  __shared__ FinalizeLds<T, D, CAP, MERGE> sh;
+  finalize_row<T, D, CAP, MERGE>(sh, blockIdx.x, cand, ccnt, idx, fail_cnt, fail_list, k, cap, nch, part_ml, part_o,
+                                 v_lm, M);
 }
 
 // ---------------------------------------------------------------------------
@@ -393,7 +236,8 @@ hipError_t launch_select_pivots(const mita_cfg_t &c, const void *q_lm, const voi
   return hipGetLastError();
 }
 
-hipError_t launch_select_finalize(const mita_cfg_t &c, const SelectBufs &sb, int32_t *idx, const void *partial,
+// The finalize kernel alone (one workgroup per landmark row).
+static hipError_t launch_select_finalize(const mita_cfg_t &c, const SelectBufs &sb, int32_t *idx, const void *partial,
                                   void *v_lm, hipStream_t st) {
   const unsigned rows = (unsigned)(BH(c) * c.M);
   const int nch = score_chunks(c);
