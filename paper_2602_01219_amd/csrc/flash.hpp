@@ -299,18 +299,20 @@ typedef short v4i16_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
 
 // Issue the DMA of one tile: rows r < 64 of K and V from byte offsets offs[r]
-// past kb and vb (rows >= nrows take offset offs[0]: real data, masked later).
-template <int D>
+// past kb and vb (without FULL, rows >= nrows take offset offs[0]: real
+// data, masked later).
+template <int D, bool FULL = false>
 __device__ __forceinline__ void dma_tile(bf16_t *Kl, bf16_t *Vl, const bf16_t *kb, const bf16_t *vb,
                                          const uint32_t *offs, int nrows) {
   using DT = DmaTile<D>;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  // the wave index as a scalar: the LDS destinations (M0) need no readfirstlane
+  const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6), lane = threadIdx.x & 63;
 #pragma unroll
   for (int j = 0; j < DT::PW; ++j) {
     const int ins = w * DT::PW + j;
     const int r = ins * DT::RPI + lane / DT::CPR;
     const int sl = lane % DT::CPR;
-    const uint32_t go = offs[r < nrows ? r : 0] + (uint32_t)((sl ^ swz(r)) << 4);
+    const uint32_t go = offs[FULL || r < nrows ? r : 0] + (uint32_t)((sl ^ swz(r)) << 4);
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(kb) + go,
                                      (lds_void_t *)(reinterpret_cast<char *>(Kl) + ins * 1024), 16, 0, 0);
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vb) + go,
@@ -379,7 +381,7 @@ __device__ __forceinline__ void half_tile_dma(OnlineDma<D> &st, const bf16_t *Kl
         mx[c] = fmaxf(mx[c], ok ? acc[c][kb][r] : -INFINITY);
       }
   }
-  if (__ballot(!st.started || mx[0] > RESCALE_LOG2 || mx[1] > RESCALE_LOG2)) {
+  if (!st.started || __ballot(mx[0] > RESCALE_LOG2 || mx[1] > RESCALE_LOG2)) {
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
       const float cm = max_lane_groups(mx[c]);

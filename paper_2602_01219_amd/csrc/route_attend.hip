@@ -567,7 +567,7 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
     auto step = [&](int i, const T *Kc, const T *Vc, T *Kn, T *Vn) {
       if (i + 1 < nfull) {
         tile_base(i + 1, kb, vb, off);
-        dma_tile<D>(Kn, Vn, kb, vb, rows + off, TK);
+        dma_tile<D, true>(Kn, Vn, kb, vb, rows + off, TK);
       }
       if (wave_busy) half_tile_dma<D>(st, Kc, Vc, kh, qf, 32);
       wait_loads();
@@ -575,7 +575,7 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
     };
     if (nfull > 0) {
       tile_base(0, kb, vb, off);
-      dma_tile<D>(Ks(0), Vt(0), kb, vb, rows + off, TK);
+      dma_tile<D, true>(Ks(0), Vt(0), kb, vb, rows + off, TK);
     }
     // the score MFMAs take q * scale * log2 e (rounded to bf16); the query
     // loads were issued before the first tile's DMA, which stays in flight
