@@ -166,6 +166,21 @@ __device__ __forceinline__ float max_lane_groups(float x) {
   return __builtin_amdgcn_fmed3f(__uint_as_float(b[0]), __uint_as_float(b[1]), INFINITY);
 }
 
+// Inclusive prefix sum `incl` over the four 16-lane groups at the same
+// position (lanes p, p+16, p+32, p+48; group g gets the sum over groups 0..g)
+// and their total `tot`, without LDS: v_permlane16_swap(x, x) hands each lane
+// the values of both groups of its pair (0,1) or (2,3), v_permlane32_swap
+// the sums of both pairs. Only sums of the pairs are used, so the order of
+// the two swap results does not matter.
+__device__ __forceinline__ void scan_lane_groups(uint32_t x, uint32_t &incl, uint32_t &tot) {
+  const int g = (threadIdx.x & 63) >> 4;
+  const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  const uint32_t pair = a[0] + a[1];
+  const auto b = __builtin_amdgcn_permlane32_swap(pair, pair, false, false);
+  tot = b[0] + b[1];
+  incl = ((g & 1) ? pair : x) + ((g & 2) ? tot - pair : 0u);
+}
+
 // Inclusive prefix sum over the 64 lanes.
 __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
   const int lane = threadIdx.x & 63;

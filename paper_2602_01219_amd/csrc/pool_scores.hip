@@ -54,8 +54,11 @@ __global__ __launch_bounds__(256) void pool_kernel(const T *__restrict__ q, T *_
   }
 }
 
+// The bf16 d=64 pass holds 3 waves per SIMD (at most 168 VGPRs).
+#define SCORES_OCCUPANCY __attribute__((amdgpu_waves_per_eu(sizeof(T) == 2 && D == 64 ? 3 : 1)))
+
 template <typename T, int D, bool WRITE_S, bool DO_V, bool SELECT>
-__global__ __launch_bounds__(BLOCK) void scores_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
+__global__ __launch_bounds__(BLOCK) SCORES_OCCUPANCY void scores_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
                                                        const T *__restrict__ v, float *__restrict__ S,
                                                        float2 *__restrict__ part_ml, float *__restrict__ part_o,
                                                        SelectArgs sel, int N, int M, float scale) {

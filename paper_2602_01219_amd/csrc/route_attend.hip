@@ -87,16 +87,18 @@ __device__ __forceinline__ void route_logits_body(T *lms, uint32_t *cnt, int bx,
 #pragma unroll
         for (int c = 0; c < 4; ++c) acc[c] = mma(a, qf[c][ks], acc[c]);
       }
+      // running argmax, branch-free (selects); the first maximum is kept, and
+      // landmarks are visited in increasing order, so ties go to the lower one
+      const bool full = sb + 16 <= nl;
 #pragma unroll
       for (int c = 0; c < 4; ++c)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int lmi = l0 + sb + 4 * g + r;
           const float val = acc[c][r] * scale;
-          if (lmi < M && val > best[c]) {
-            best[c] = val;
-            arg[c] = lmi;
-          }
+          const bool up = (full || lmi < M) && val > best[c];
+          best[c] = up ? val : best[c];
+          arg[c] = up ? lmi : arg[c];
         }
     }
   }

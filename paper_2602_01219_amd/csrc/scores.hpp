@@ -8,6 +8,45 @@
 
 namespace mita {
 
+// Neighbouring floats (a zero of either sign steps to the smallest subnormal).
+__device__ __forceinline__ float f32_next_down(float x) {
+  const uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) == 0u) return __uint_as_float(0x80000001u);
+  return __uint_as_float((u & 0x80000000u) ? u + 1u : u - 1u);
+}
+__device__ __forceinline__ float f32_next_up(float x) {
+  const uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) == 0u) return __uint_as_float(1u);
+  return __uint_as_float((u & 0x80000000u) ? u - 1u : u + 1u);
+}
+
+// Bound of a pivot on the unscaled dot: the smallest float t with
+// fl(t * scale) >= piv. A rounded product is monotonic in its operand, so for
+// scale > 0 and every non-NaN dot a, fl(a * scale) >= piv iff a >= t, and the
+// selection test can compare the MFMA dots without scaling them. piv / scale
+// lies within a few ulps of t for a normal piv; the walk is capped at 4 steps
+// and returns false if it has not settled (a subnormal piv), and then the
+// scaled test is used. A NaN piv (no row) gives t = NaN, which lists nothing.
+__device__ __forceinline__ bool dot_bound(float piv, float scale, float &t) {
+  t = piv / scale;
+  if (piv != piv) return true;
+  if (t * scale >= piv) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float d = f32_next_down(t);
+      if (!(d * scale >= piv)) return true;
+      t = d;
+    }
+    return false;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    t = f32_next_up(t);
+    if (t * scale >= piv) return true;
+  }
+  return false;
+}
+
 // ---------------------------------------------------------------------------
 // Scores and landmark values. Workgroup = 4 waves x 16 landmarks over one
 // chunk of SCORE_NC keys, key tiles of 64 staged in LDS (K row-major, V
@@ -61,12 +100,15 @@ __device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ 
   // for x not NaN (the key order is the float order with -0 == +0), and for
   // NaN (ranked as -inf) iff the pivot is -inf. plo = 0xffffffff (no row)
   // gives a NaN bound that lists nothing.
-  float piv = 0.f;
-  bool nan_in = false;
+  // dotpiv: piv as a bound on the unscaled dots (dot_bound); `scaled` marks
+  // the lanes that must test the scaled score instead.
+  float piv = 0.f, dotpiv = 0.f;
+  bool nan_in = false, scaled = false;
   if (SELECT) {
     const uint32_t plo = lm < M ? sel.plo[row] : 0xffffffffu;
     piv = key_to_float(plo);
     nan_in = plo == ordered_key(-INFINITY);
+    scaled = nan_in || !(scale > 0.f && scale < INFINITY) || !dot_bound(piv, scale, dotpiv);
   }
   const bool write_row = WRITE_S && lm < M && (only_lm < 0 || lm == only_lm);
   uint32_t listed = 0;  // SELECT: candidates of this landmark listed so far in the chunk
@@ -103,16 +145,16 @@ __device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ 
     // tile's LDS store: on gfx9 one counter tracks loads and stores, so the
     // wait for the prefetched loads would otherwise also wait for them.
     f32x4 acc[4];
-    uint32_t m[4] = {0u, 0u, 0u, 0u}, pos = 0u, tot = 0u;
+    uint32_t m[4] = {0u, 0u, 0u, 0u}, pos = 0u, tot = 0u, ntot = 0u;
     if (active) {
       tile_scores<T, D>(acc, Kc, qf);
       if (SELECT) {
         // per-kb candidate bits m[kb] (bit r); per-kb counts in bytes
-        if (nvalid == TK && !__ballot(nan_in)) {  // full tile, no -inf pivot in the wave
+        if (nvalid == TK && !__ballot(scaled)) {  // full tile, every lane has a dot bound
 #pragma unroll
           for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) m[kb] |= (acc[kb][r] * scale >= piv) ? 1u << r : 0u;
+            for (int r = 0; r < 4; ++r) m[kb] |= (acc[kb][r] >= dotpiv) ? 1u << r : 0u;
         } else {
 #pragma unroll
           for (int kb = 0; kb < 4; ++kb)
@@ -127,16 +169,18 @@ __device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ 
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) packed |= (uint32_t)__popc(m[kb]) << (8 * kb);
         // inclusive scan over the lane groups of landmark p (bytes stay below 17)
-        uint32_t incl = packed;
-        uint32_t y = (uint32_t)__shfl_up((int)incl, 16);
-        if (g >= 1) incl += y;
-        y = (uint32_t)__shfl_up((int)incl, 32);
-        if (g >= 2) incl += y;
-        tot = (uint32_t)__shfl((int)incl, 48 + p);  // per-kb totals of the landmark
+        uint32_t incl;
+        scan_lane_groups(packed, incl, tot);  // tot: per-kb totals of the landmark
         // byte kb of pos: candidates of the landmark before this lane's block kb
         pos = (incl - packed) + (tot << 8) + (tot << 16) + (tot << 24);
+        ntot = (tot * 0x01010101u) >> 24;  // candidates of the landmark in the tile
       }
-      if (DO_V) tile_softmax_pv<T, D>(st, acc, Vc, nvalid, sl2);
+      if (DO_V) {
+        if (nvalid == TK)
+          tile_softmax_pv<T, D, false>(st, acc, Vc, nvalid, sl2);
+        else
+          tile_softmax_pv<T, D, true>(st, acc, Vc, nvalid, sl2);
+      }
     }
     if (t + 1 < ntile) R.store(Ks + (buf ^ 1) * TD::K_ELEMS, DO_V ? Vt + (buf ^ 1) * TD::V_ELEMS : Vt);
     if (active && write_row) {
@@ -171,7 +215,7 @@ __device__ __forceinline__ void score_chunk(T *__restrict__ Ks, T *__restrict__ 
             at += 8u;
           }
       }
-      listed += (tot * 0x01010101u) >> 24;
+      listed += ntot;
     }
     __syncthreads();
   }
