@@ -76,24 +76,36 @@ __device__ __forceinline__ void finalize_row(FinalizeLds<T, D, CAP, MERGE> &sh, 
     return;
   }
   __syncthreads();
-  // compaction into LDS, with the composite range of the list
+  // compaction into LDS, with the composite range of the list: wave w copies
+  // chunks w, w + 4, ..., lane j taking entries j, j + 64, ...; the first 64
+  // entries of CU chunks are loaded together before any is stored
   const int L = (int)total;
   uint64_t lo = ~0ull, hi = 0ull;
-  for (int i = tid; i < L; i += 256) {
-    int a = 0, b = nch - 1;  // last chunk c with pre[c] <= i
-    while (a < b) {
-      const int mid = (a + b + 1) >> 1;
-      if (pre[mid] <= (uint32_t)i)
-        a = mid;
-      else
-        b = mid - 1;
-    }
-    const uint2 e = cand[(row * nch + a) * (int64_t)SCORE_NC + (i - (int)pre[a])];
+  auto put = [&](uint2 e, uint32_t at) {
     const uint2 x = make_uint2(score_key(__uint_as_float(e.x)), e.y);  // listed as float bits
-    lst[i] = x;
+    lst[at] = x;
     const uint64_t c = composite(x);
     lo = c < lo ? c : lo;
     hi = c > hi ? c : hi;
+  };
+  constexpr int CU = 4;
+  const uint2 *crow = cand + row * nch * (int64_t)SCORE_NC;
+  for (int c0 = w; c0 < nch; c0 += 4 * CU) {
+    uint2 e[CU];
+    uint32_t b[CU], n[CU];
+#pragma unroll
+    for (int u = 0; u < CU; ++u) {
+      const int c = c0 + 4 * u;
+      b[u] = c < nch ? pre[c] : 0u;
+      n[u] = c < nch ? pre[c + 1] - b[u] : 0u;
+      e[u] = (uint32_t)lane < n[u] ? crow[(int64_t)c * SCORE_NC + lane] : make_uint2(0u, 0u);
+    }
+#pragma unroll
+    for (int u = 0; u < CU; ++u)
+      if ((uint32_t)lane < n[u]) put(e[u], b[u] + lane);
+#pragma unroll
+    for (int u = 0; u < CU; ++u)
+      for (uint32_t j = lane + 64; j < n[u]; j += 64) put(crow[(int64_t)(c0 + 4 * u) * SCORE_NC + j], b[u] + j);
   }
   lo = wave_min_u64(lo);
   hi = wave_max_u64(hi);
