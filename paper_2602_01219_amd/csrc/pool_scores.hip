@@ -36,20 +36,44 @@ __global__ __launch_bounds__(256) void pool_kernel(const T *__restrict__ q, T *_
 #pragma unroll
   for (int e = 0; e < VE; ++e) acc[e] = 0.f;
   const T *base = q + bh * (int64_t)N * D;
-  for (int t = slot; t < count; t += P) {
-    const int r = r0 + t / cols, c = c0 + t % cols;
-    const uint4 u = *reinterpret_cast<const uint4 *>(base + ((int64_t)r * gw + c) * D + ch * VE);
-    float x[VE];
-    unpack16(u, x, (const T *)nullptr);
+  constexpr int U = 4;  // token rows per thread loaded before any is summed
+  for (int t0 = slot; t0 < count; t0 += U * P) {
+    uint4 u[U];
 #pragma unroll
-    for (int e = 0; e < VE; ++e) acc[e] += x[e];
+    for (int j = 0; j < U; ++j) {
+      const int t = t0 + j * P;
+      u[j] = make_uint4(0u, 0u, 0u, 0u);
+      if (t < count) {
+        const int r = r0 + t / cols, c = c0 + t % cols;
+        u[j] = *reinterpret_cast<const uint4 *>(base + ((int64_t)r * gw + c) * D + ch * VE);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      float x[VE];
+      unpack16(u[j], x, (const T *)nullptr);
+#pragma unroll
+      for (int e = 0; e < VE; ++e) acc[e] += x[e];
+    }
   }
 #pragma unroll
   for (int e = 0; e < VE; ++e) red[slot][ch * VE + e] = acc[e];
   __syncthreads();
+  // the P slot sums of each column: NQ partial sums per column (one per
+  // thread), then their sum
+  constexpr int NQ = 256 / D, PQ = P / NQ;
+  static_assert(NQ >= 1 && P % NQ == 0, "pool reduction layout");
+  const int col = threadIdx.x % D, part_i = threadIdx.x / D;
+  float part = 0.f;
+#pragma unroll
+  for (int j = 0; j < PQ; ++j) part += red[part_i * PQ + j][col];
+  __syncthreads();
+  red[part_i][col] = part;
+  __syncthreads();
   if (threadIdx.x < D) {
     float s = 0.f;
-    for (int j = 0; j < P; ++j) s += red[j][threadIdx.x];
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) s += red[j][threadIdx.x];
     q_lm[(bh * M + i) * D + threadIdx.x] = from_f32<T>(s / (float)count);
   }
 }
