@@ -19,7 +19,6 @@ constexpr int SCORE_NC = 512;  // keys per score/landmark-value workgroup chunk
 // Top-k selection fused with the score pass of the forward.
 constexpr int SEL_NS = 1024;   // sampled keys per landmark row (pivot estimate)
 constexpr int SEL_CAP = 4096;  // most candidates the exact selection of one row takes
-constexpr int SAMPLE_NC = 64;  // sampled keys per sample-kernel workgroup
 
 inline size_t align_up(size_t x) { return (x + WS_ALIGN - 1) / WS_ALIGN * WS_ALIGN; }
 inline size_t elem_bytes(const mita_cfg_t &c) { return c.dtype == MITA_F32 ? 4 : 2; }
@@ -99,7 +98,7 @@ inline int check_cfg(const mita_cfg_t *c, std::string *err) {
 // Workspace layout of mita_forward (offsets in bytes; 0-sized pieces allowed).
 struct FwdLayout {
   size_t q_lm, v_lm, scores, partial, idx, kx, vx, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start,
-      samp, plo, ccnt, cand, fail, total;
+      plo, ccnt, cand, fail, total;
 };
 
 inline size_t scores_ws_bytes(const mita_cfg_t &c) {
@@ -143,10 +142,9 @@ inline FwdLayout forward_layout(const mita_cfg_t &c) {
   L.tile_base = take(c.use_routed ? bh * route_tiles(c) * c.M * 4 : 0);
   L.counts = take(c.use_routed ? bh * c.M * 4 : 0);
   L.tile_start = take(c.use_routed ? bh * (c.M + 1) * 4 : 0);
-  // fused selection: sampled score keys, pivots, candidate counts and lists,
+  // fused selection: pivots, candidate counts and lists,
   // then the fallback counter followed by the fallback row list
   const bool fs = fused_select(c);
-  L.samp = take(fs ? bh * c.M * (size_t)sel_ns(c) * 4 : 0);
   L.plo = take(fs ? bh * c.M * 4 : 0);
   // per (row, key chunk): candidate count and a list region of SCORE_NC entries
   L.ccnt = take(fs ? bh * c.M * (size_t)score_chunks(c) * 4 : 0);

@@ -17,7 +17,6 @@ hipError_t launch_zero(int32_t *p, int64_t n, hipStream_t st);
 
 // Buffers of the top-k selection fused with the score pass (rows = BH*M).
 struct SelectBufs {
-  uint32_t *samp;       // [rows, ns] ordered keys of the sampled scores
   uint32_t *plo;        // [rows] pivot keys
   uint32_t *ccnt;       // [rows, chunks] candidates listed per key chunk
   uint2 *cand;          // [rows, chunks, SCORE_NC] (score bits, token index) lists

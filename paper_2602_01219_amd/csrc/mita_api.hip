@@ -102,7 +102,6 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
   const bool fused = fused_select(*c);
   SelectBufs sel{};
   if (fused) {
-    sel.samp = (uint32_t *)(w + L.samp);
     sel.plo = (uint32_t *)(w + L.plo);
     sel.ccnt = (uint32_t *)(w + L.ccnt);
     sel.cand = (uint2 *)(w + L.cand);

@@ -1,13 +1,13 @@
 // select.hip - the top-k selection of the forward (Eq. top-k), fused with the
 // landmark-key score pass so that the M x N score matrix is never stored.
 //
-//   1. sample_kernel: the scores of every landmark against ns evenly spaced
-//      keys, as order-preserving keys (the same tile arithmetic as the score
-//      pass, so the same values).
-//   2. pivot_kernel: per landmark row, the pivot = the r-th largest sampled
-//      key. r is chosen on the host so that at least k and far fewer than
-//      `cap` tokens of the row score >= pivot, except with negligible
-//      probability (r = k exactly when the sample is the whole row).
+//   1-2. sample_pivot_kernel: the scores of every landmark against ns evenly
+//      spaced keys, as order-preserving keys (the same tile arithmetic as the
+//      score pass, so the same values), kept in LDS; per landmark row, the
+//      pivot = the r-th largest sampled key. r is chosen on the host so that
+//      at least k and far fewer than `cap` tokens of the row score >= pivot,
+//      except with negligible probability (r = k exactly when the sample is
+//      the whole row).
 //   3. the score pass lists every token scoring >= pivot (score bits, token
 //      index), in token order, in one region per (row, key chunk).
 //   4. finalize_kernel: with k <= count <= cap the list holds the row's whole
@@ -74,106 +74,24 @@ __device__ __forceinline__ int wave_find_bin(const uint32_t *hist, uint32_t need
 }  // namespace
 
 // ---------------------------------------------------------------------------
-// Sampled scores. Workgroup = 4 waves x 16 landmarks over SAMPLE_NC sampled
-// keys, tiles of 64 gathered into LDS; keys = score_key(fl(dot) * scale).
-// Workgroup (0, 0, 0) also zeroes the fallback counter.
+// Pivot of one landmark row from its ns (<= SEL_NS) sampled keys, held by one
+// wave: lane l holds keys 4 l + 256 i + (0..3) in v[4 i .. 4 i + 3], 0 marking
+// a slot past ns (no score has key 0, so it lies below every range). Radix
+// rounds over a 256-bin LDS histogram of the current key range (bins span
+// (hi - lo + 1) / 256 keys, so each round shrinks the range by 2^8) narrow
+// down on the r-th largest sample; after two rounds the lower edge of the bin
+// holding it is taken. That edge is at most the r-th largest sample, so at
+// least r samples are >= pivot, and its bin spans at most 2^16 keys (a
+// relative step of 2^-7 within one binade), which lists only a few more
+// tokens than the exact sample statistic would.
 // ---------------------------------------------------------------------------
-template <typename T, int D>
-__global__ __launch_bounds__(BLOCK) void sample_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
-                                                       uint32_t *__restrict__ samp, uint32_t *__restrict__ fail_cnt,
-                                                       int N, int M, int ns, float scale) {
-  using TD = TileDims<T, D>;
-  __shared__ __align__(16) T Ks[TD::K_ELEMS];
-  __shared__ int32_t pos[TK];
-  const int64_t bh = blockIdx.z;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
-  const int lm0 = (blockIdx.y * 4 + w) * 16;
-  const int lm = lm0 + p;
-  const int64_t row = bh * M + lm;
-  if (blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0) *fail_cnt = 0;
+constexpr int PIVOT_PER = SEL_NS / 64;
 
-  Frag<T> qf[D / 32];
-#pragma unroll
-  for (int ks = 0; ks < D / 32; ++ks) {
-    if (lm < M)
-      qf[ks].load(q_lm + row * D + ks * 32 + g * 8);
-    else
-      qf[ks].zero();
-  }
-  const T *kb_ = k + bh * (int64_t)N * D;
-  const int j_begin = blockIdx.x * SAMPLE_NC, j_end = min(ns, j_begin + SAMPLE_NC);
-  for (int j0 = j_begin; j0 < j_end; j0 += TK) {
-    const int nvalid = min(TK, j_end - j0);
-    __syncthreads();
-    if (threadIdx.x < TK) pos[threadIdx.x] = (int)threadIdx.x < nvalid ? sample_pos(j0 + threadIdx.x, N, ns) : 0;
-    __syncthreads();
-    load_k_tile<T, D>(Ks, kb_, pos, nvalid);
-    __syncthreads();
-    if (lm0 >= M) continue;
-    f32x4 acc[4];
-    tile_scores<T, D>(acc, Ks, qf);
-    if (lm < M) {
-      uint32_t *srow = samp + row * (int64_t)ns + j0;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        const int j = kb * 16 + 4 * g;
-        uint32_t key[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) key[r] = score_key(acc[kb][r] * scale);
-        if ((ns & 3) == 0 && j + 3 < nvalid) {
-          *reinterpret_cast<uint4 *>(srow + j) = make_uint4(key[0], key[1], key[2], key[3]);
-        } else {
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (j + r < nvalid) srow[j + r] = key[r];
-        }
-      }
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Pivots: one wave per landmark row, its ns (<= SEL_NS) sampled keys in
-// registers. Radix rounds over a 256-bin LDS histogram of the current key
-// range (bins span (hi - lo + 1) / 256 keys, so each round shrinks the range
-// by 2^8) narrow down on the r-th largest sample; after two rounds the lower
-// edge of the bin holding it is taken. That edge is at most the r-th largest
-// sample, so at least r samples are >= pivot, and its bin spans at most
-// 2^16 keys (a relative step of 2^-7 within one binade), which lists only a
-// few more tokens than the exact sample statistic would.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void pivot_kernel(const uint32_t *__restrict__ samp, uint32_t *__restrict__ plo,
-                                                    int64_t rows, int ns, int r) {
-  constexpr int PER = SEL_NS / 64;
-  __shared__ uint32_t hist_all[4][256];
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * 4 + w;
-  if (row >= rows) return;  // a whole wave; no workgroup barriers below
-  uint32_t *hist = hist_all[w];
-  const uint32_t *s = samp + row * (int64_t)ns;
-  // lane l holds keys 4 l + 256 i + (0..3); 0 marks a slot past ns (no score
-  // has key 0, so it lies below every range)
-  uint32_t v[PER];
-  if ((ns & 255) == 0) {
-#pragma unroll
-    for (int i = 0; i < PER / 4; ++i) {
-      uint4 x = make_uint4(0u, 0u, 0u, 0u);
-      if (256 * i < ns) x = *reinterpret_cast<const uint4 *>(s + 256 * i + 4 * lane);
-      v[4 * i] = x.x;
-      v[4 * i + 1] = x.y;
-      v[4 * i + 2] = x.z;
-      v[4 * i + 3] = x.w;
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int j = 256 * (i / 4) + 4 * lane + (i % 4);
-      v[i] = j < ns ? s[j] : 0u;
-    }
-  }
+static __device__ __forceinline__ uint32_t pivot_of(const uint32_t (&v)[PIVOT_PER], uint32_t *hist, int r) {
+  const int lane = threadIdx.x & 63;
   uint32_t mn = 0xffffffffu, mx = 0u;
 #pragma unroll
-  for (int i = 0; i < PER; ++i) {
+  for (int i = 0; i < PIVOT_PER; ++i) {
     if (v[i]) mn = min(mn, v[i]);
     mx = max(mx, v[i]);
   }
@@ -186,7 +104,7 @@ __global__ __launch_bounds__(256) void pivot_kernel(const uint32_t *__restrict__
 #pragma unroll
     for (int q = 0; q < 4; ++q) hist[lane + 64 * q] = 0u;
 #pragma unroll
-    for (int i = 0; i < PER; ++i)
+    for (int i = 0; i < PIVOT_PER; ++i)
       if (v[i] >= lo && v[i] <= hi) atomicAdd(hist + ((v[i] - lo) >> shift), 1u);
     uint32_t above;
     const int b = wave_find_bin(hist, need, &above);
@@ -195,10 +113,86 @@ __global__ __launch_bounds__(256) void pivot_kernel(const uint32_t *__restrict__
     const uint32_t width = (1u << shift) - 1u;
     if (hi - lo > width) hi = lo + width;
   }
-  if (lane == 0) plo[row] = lo;
+  return lo;
 }
 
-// One workgroup per landmark row.
+// ---------------------------------------------------------------------------
+// Sampled scores and pivots in one launch. Workgroup = NW waves over 16
+// landmark rows of one head (one MFMA column block); wave w scores them
+// against the sampled keys [SEL_NS/NW w, SEL_NS/NW (w + 1)) in tiles of 64,
+// the A fragments loaded straight from the sampled key rows (tile arithmetic
+// as in the score pass, so the same values), keys = score_key(fl(dot) * scale)
+// into LDS; then wave w takes the pivots of rows 16/NW w .. 16/NW (w + 1) - 1,
+// its histogram in the first 256 words of its own row's keys once they are in
+// registers (the wave's LDS accesses are in order). Workgroup (0, 0) also
+// zeroes the fallback counter.
+// ---------------------------------------------------------------------------
+constexpr int SP_PITCH = SEL_NS + 4;  // keys per LDS row: rows start 4 banks apart
+
+template <typename T, int D, int NW>
+__global__ __launch_bounds__(64 * NW) void sample_pivot_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
+                                                               uint32_t *__restrict__ plo,
+                                                               uint32_t *__restrict__ fail_cnt, int N, int M, int ns,
+                                                               int r, float scale) {
+  static_assert(16 % NW == 0 && SEL_NS % (NW * TK) == 0, "sample/pivot split");
+  constexpr int PERW = SEL_NS / NW;  // samples per wave
+  constexpr int RPW = 16 / NW;       // rows per wave
+  __shared__ __align__(16) uint32_t keys[16][SP_PITCH];
+  const int64_t bh = blockIdx.y;
+  const int lm0 = blockIdx.x * 16;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
+  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *fail_cnt = 0;
+  Frag<T> qf[D / 32];
+#pragma unroll
+  for (int ks = 0; ks < D / 32; ++ks) {
+    if (lm0 + p < M)
+      qf[ks].load(q_lm + (bh * M + lm0 + p) * D + ks * 32 + g * 8);
+    else
+      qf[ks].zero();
+  }
+  const T *kb_ = k + bh * (int64_t)N * D;
+  for (int j0 = w * PERW; j0 < min(ns, (w + 1) * PERW); j0 += TK) {
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const int j = j0 + kb * 16 + p;  // A row p of block kb: sample j
+      const int64_t pos = j < ns ? sample_pos(j, N, ns) : 0;
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) {
+        Frag<T> a;
+        a.load(kb_ + pos * D + ks * 32 + g * 8);
+        acc = mma(a, qf[ks], acc);
+      }
+      // lane (g, p) holds samples j0 + 16 kb + 4 g + (0..3) of row p
+      const int jb = j0 + kb * 16 + 4 * g;
+      uint32_t key[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) key[q] = jb + q < ns ? score_key(acc[q] * scale) : 0u;
+      *reinterpret_cast<uint4 *>(&keys[p][jb]) = make_uint4(key[0], key[1], key[2], key[3]);
+    }
+  }
+  // slots past ns stay 0 (below every key) for the selection
+  for (int j = ns + (int)threadIdx.x; j < SEL_NS; j += 64 * NW)
+#pragma unroll
+    for (int row = 0; row < 16; ++row) keys[row][j] = 0u;
+  __syncthreads();
+  for (int q = 0; q < RPW; ++q) {
+    const int rl = RPW * w + q;
+    if (lm0 + rl >= M) break;  // uniform for the wave; no workgroup barriers below
+    uint32_t v[PIVOT_PER];
+#pragma unroll
+    for (int i = 0; i < PIVOT_PER / 4; ++i) {
+      const uint4 x = *reinterpret_cast<const uint4 *>(&keys[rl][256 * i + 4 * lane]);
+      v[4 * i] = x.x;
+      v[4 * i + 1] = x.y;
+      v[4 * i + 2] = x.z;
+      v[4 * i + 3] = x.w;
+    }
+    const uint32_t lo = pivot_of(v, &keys[rl][0], r);
+    if (lane == 0) plo[bh * M + lm0 + rl] = lo;
+  }
+}
+
 template <typename T, int D, int CAP, bool MERGE>
 __global__ __launch_bounds__(256) void finalize_kernel(const uint2 *__restrict__ cand,
                                                        const uint32_t *__restrict__ ccnt, int32_t *__restrict__ idx,
@@ -215,25 +209,23 @@ __global__ __launch_bounds__(256) void finalize_kernel(const uint2 *__restrict__
 // launchers
 // ---------------------------------------------------------------------------
 template <typename T, int D>
-static hipError_t sample_t(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sb, hipStream_t st) {
-  dim3 grid((sb.ns + SAMPLE_NC - 1) / SAMPLE_NC, (c.M + 63) / 64, (unsigned)BH(c));
-  hipLaunchKernelGGL((sample_kernel<T, D>), grid, dim3(BLOCK), 0, st, (const T *)q_lm, (const T *)k, sb.samp,
-                     sb.fail_cnt, c.N, c.M, sb.ns, eff_scale(c));
+static hipError_t sample_pivot_t(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sb,
+                                 hipStream_t st) {
+  // bf16: one sample tile and one row per wave (16 waves); fp32 (more
+  // registers per fragment): four waves, four tiles and four rows each
+  constexpr int NW = sizeof(T) == 2 ? 16 : 4;
+  const dim3 grid((unsigned)((c.M + 15) / 16), (unsigned)BH(c));
+  hipLaunchKernelGGL((sample_pivot_kernel<T, D, NW>), grid, dim3(64 * NW), 0, st, (const T *)q_lm, (const T *)k,
+                     sb.plo, sb.fail_cnt, c.N, c.M, sb.ns, sb.rank, eff_scale(c));
   return hipGetLastError();
 }
 
 hipError_t launch_select_pivots(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sb,
                                 hipStream_t st) {
-  hipError_t e;
+  if (sb.ns > SEL_NS) return hipErrorInvalidValue;  // the workgroup holds SEL_NS keys per row
   if (c.dtype == MITA_F32)
-    e = c.d == 64 ? sample_t<float, 64>(c, q_lm, k, sb, st) : sample_t<float, 128>(c, q_lm, k, sb, st);
-  else
-    e = c.d == 64 ? sample_t<bf16_t, 64>(c, q_lm, k, sb, st) : sample_t<bf16_t, 128>(c, q_lm, k, sb, st);
-  if (e != hipSuccess) return e;
-  const int64_t rows = BH(c) * c.M;
-  hipLaunchKernelGGL(pivot_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st, sb.samp, sb.plo, rows, sb.ns,
-                     sb.rank);
-  return hipGetLastError();
+    return c.d == 64 ? sample_pivot_t<float, 64>(c, q_lm, k, sb, st) : sample_pivot_t<float, 128>(c, q_lm, k, sb, st);
+  return c.d == 64 ? sample_pivot_t<bf16_t, 64>(c, q_lm, k, sb, st) : sample_pivot_t<bf16_t, 128>(c, q_lm, k, sb, st);
 }
 
 // The finalize kernel alone (one workgroup per landmark row).
