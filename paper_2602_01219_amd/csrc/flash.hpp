@@ -348,10 +348,12 @@ template <int D> struct OnlineDma {
 // queries (pre-scaled fragments qf[c]). The reference max starts at the first
 // tile's column max; later it moves only when a column's shifted scores
 // exceed RESCALE_LOG2 (then the tile's values, accumulators and sums shift
-// with it). With MASKED only keys 32h + i, i < nvalid (>= 1), count.
-template <int D, bool MASKED = false>
+// with it). With MASKED only keys 32h + i, i < nvalid (>= 1), count. NG = 1
+// computes the first 16-query group only (the second holds no query).
+template <int D, bool MASKED = false, int NG = 2>
 __device__ __forceinline__ void half_tile_dma(OnlineDma<D> &st, const bf16_t *Kl, const bf16_t *Vl, int h,
                                               const Frag<bf16_t> (&qf)[2][D / 32], int nvalid) {
+  static_assert(NG == 1 || NG == 2, "one or two query groups");
   constexpr int RB = 2 * D;  // bytes per row
   const int lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
   const char *kbase = reinterpret_cast<const char *>(Kl);
@@ -366,12 +368,12 @@ __device__ __forceinline__ void half_tile_dma(OnlineDma<D> &st, const bf16_t *Kl
       Frag<bf16_t> a;
       a.v = *reinterpret_cast<const uint4 *>(kbase + R * RB + (((4 * ks + g) ^ swz(R)) << 4));
       acc[0][kb] = mma(a, qf[0][ks], acc[0][kb]);
-      acc[1][kb] = mma(a, qf[1][ks], acc[1][kb]);
+      if (NG > 1) acc[1][kb] = mma(a, qf[1][ks], acc[1][kb]);
     }
   }
-  float mx[2];
+  float mx[2] = {-INFINITY, -INFINITY};
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
+  for (int c = 0; c < NG; ++c) {
     mx[c] = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -383,7 +385,7 @@ __device__ __forceinline__ void half_tile_dma(OnlineDma<D> &st, const bf16_t *Kl
   }
   if (!st.started || __ballot(mx[0] > RESCALE_LOG2 || mx[1] > RESCALE_LOG2)) {
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
+    for (int c = 0; c < NG; ++c) {
       const float cm = max_lane_groups(mx[c]);
       // first tile: the reference becomes the column max (the accumulators
       // are still zero); later: raised by the excess only
@@ -403,7 +405,7 @@ __device__ __forceinline__ void half_tile_dma(OnlineDma<D> &st, const bf16_t *Kl
   const Frag<bf16_t> ones = ones_frag<bf16_t>();
   Frag<bf16_t> b[2];
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
+  for (int c = 0; c < NG; ++c) {
     // reduction slice of group g: keys 32h + 4g + (0..3) and 32h + 16 + 4g + (0..3)
     float pv[8];
 #pragma unroll
@@ -433,7 +435,7 @@ __device__ __forceinline__ void half_tile_dma(OnlineDma<D> &st, const bf16_t *Kl
     Frag<bf16_t> a;
     a.v = make_uint4(half[0].x, half[0].y, half[1].x, half[1].y);
     st.o[0][db] = mma(a, b[0], st.o[0][db]);
-    st.o[1][db] = mma(a, b[1], st.o[1][db]);
+    if (NG > 1) st.o[1][db] = mma(a, b[1], st.o[1][db]);
   }
 }
 

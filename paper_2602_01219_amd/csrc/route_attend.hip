@@ -566,15 +566,6 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
     // addresses
     const T *kb, *vb;
     int off;
-    auto step = [&](int i, const T *Kc, const T *Vc, T *Kn, T *Vn) {
-      if (i + 1 < nfull) {
-        tile_base(i + 1, kb, vb, off);
-        dma_tile<D, true>(Kn, Vn, kb, vb, rows + off, TK);
-      }
-      if (wave_busy) half_tile_dma<D>(st, Kc, Vc, kh, qf, 32);
-      wait_loads();
-      __syncthreads();
-    };
     if (nfull > 0) {
       tile_base(0, kb, vb, off);
       dma_tile<D, true>(Ks(0), Vt(0), kb, vb, rows + off, TK);
@@ -593,26 +584,45 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
       }
     wait_loads();
     __syncthreads();
-    int i = 0;
-    for (; i + 1 < nfull; i += 2) {
-      step(i, Ks(0), Vt(0), Ks(1), Vt(1));
-      step(i + 1, Ks(1), Vt(1), Ks(0), Vt(0));
-    }
-    if (i < nfull) step(i, Ks(0), Vt(0), Ks(1), Vt(1));
-    // partial tiles (masked)
-    for (int part = 0; part < 2; ++part) {
-      const int nr = part == 0 ? pA : pB;
-      if (nr == 0) continue;  // uniform
-      if (part == 0)
-        dma_tile<D>(Ks(0), Vt(0), sh_k, sh_v, rows + nA * TK, nr);
-      else
-        dma_tile<D>(Ks(0), Vt(0), rkb, rvb, rows + rbase + nB * TK, nr);
-      wait_loads();
-      __syncthreads();
-      const int nh = min(32, nr - 32 * kh);  // keys of this wave's half
-      if (wave_busy && nh > 0) half_tile_dma<D, true>(st, Ks(0), Vt(0), kh, qf, nh);
-      __syncthreads();
-    }
+    // the tile loop, for a wave whose second 16-query group holds queries
+    // (NG = 2) or not (NG = 1: half the arithmetic); both versions stage the
+    // same tiles and meet the same barriers
+    auto run = [&](auto ng) {
+      constexpr int NG = decltype(ng)::value;
+      auto step = [&](int i, const T *Kc, const T *Vc, T *Kn, T *Vn) {
+        if (i + 1 < nfull) {
+          tile_base(i + 1, kb, vb, off);
+          dma_tile<D, true>(Kn, Vn, kb, vb, rows + off, TK);
+        }
+        if (wave_busy) half_tile_dma<D, false, NG>(st, Kc, Vc, kh, qf, 32);
+        wait_loads();
+        __syncthreads();
+      };
+      int i = 0;
+      for (; i + 1 < nfull; i += 2) {
+        step(i, Ks(0), Vt(0), Ks(1), Vt(1));
+        step(i + 1, Ks(1), Vt(1), Ks(0), Vt(0));
+      }
+      if (i < nfull) step(i, Ks(0), Vt(0), Ks(1), Vt(1));
+      // partial tiles (masked)
+      for (int part = 0; part < 2; ++part) {
+        const int nr = part == 0 ? pA : pB;
+        if (nr == 0) continue;  // uniform
+        if (part == 0)
+          dma_tile<D>(Ks(0), Vt(0), sh_k, sh_v, rows + nA * TK, nr);
+        else
+          dma_tile<D>(Ks(0), Vt(0), rkb, rvb, rows + rbase + nB * TK, nr);
+        wait_loads();
+        __syncthreads();
+        const int nh = min(32, nr - 32 * kh);  // keys of this wave's half
+        if (wave_busy && nh > 0) half_tile_dma<D, true, NG>(st, Ks(0), Vt(0), kh, qf, nh);
+        __syncthreads();
+      }
+    };
+    if (q_begin + qh * 32 + 16 < q_end)
+      run(std::integral_constant<int, 2>{});
+    else
+      run(std::integral_constant<int, 1>{});
   } else {
   TileRegs<T, D> Ra;
   if (IDX_LDS) {
