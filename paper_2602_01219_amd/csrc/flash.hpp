@@ -276,15 +276,17 @@ __device__ __forceinline__ void half_tile_attend(Online2<D> &st, const T *__rest
 // bf16 tiles staged by LDS DMA (global_load_lds_dwordx4: each lane's 16
 // bytes land at consecutive LDS addresses, 1 KB per wave instruction, with no
 // registers involved). K and V are both kept row-major, rows of D elements
-// without padding; 16-byte slot s of row r holds chunk s ^ swz(r). The
-// swizzle spreads the K fragment reads (8 rows at one chunk) and the V
-// transpose reads (16 rows, 4 pieces each) evenly over the LDS banks. The
+// without padding; 16-byte slot s of row r holds chunk s ^ swz(r). The LDS
+// serves 256 bytes per cycle from 64 banks: 16 lanes of a 16-byte read, 32
+// lanes of an 8-byte one. The swizzle makes both the K fragment reads (16
+// consecutive rows at one chunk) and the V transpose reads (8 rows, 4 pieces
+// each, per 32 lanes) touch every bank once per cycle (d = 64). The
 // A operand of O^T += V^T P^T comes from ds_read_b64_tr_b16: in each 16-lane
 // group, lane 4e + c addresses piece c (4 elements) of row e of a 4 x 16
 // block and lane i receives column i, i.e. 4 consecutive keys of one
 // dimension.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+__device__ __forceinline__ int swz(int r) { return (r & 6) | ((r >> 3) & 1); }
 
 template <int D> struct DmaTile {
   static constexpr int CPR = D / 8;        // 16-byte chunks per row
@@ -437,6 +439,20 @@ __device__ __forceinline__ void half_tile_dma(OnlineDma<D> &st, const bf16_t *Kl
     st.o[0][db] = mma(a, b[0], st.o[0][db]);
     if (NG > 1) st.o[1][db] = mma(a, b[1], st.o[1][db]);
   }
+}
+
+// One step of the DMA-staged tile loop: the DMA of the next tile into (Kn,
+// Vn) is issued (if `more`), then the wave's half of the current tile (Kc, Vc)
+// is multiplied (if `busy`). The buffers come in as restrict pointers, so the
+// compiler's alias information shows the reads of the current tile to be
+// disjoint from the DMA in flight and no wait for it is placed before them.
+template <int D, int NG>
+__device__ __forceinline__ void dma_step(OnlineDma<D> &st, const bf16_t *__restrict__ Kc,
+                                         const bf16_t *__restrict__ Vc, bf16_t *__restrict__ Kn,
+                                         bf16_t *__restrict__ Vn, bool more, const bf16_t *kb, const bf16_t *vb,
+                                         const uint32_t *offs, bool busy, int h, const Frag<bf16_t> (&qf)[2][D / 32]) {
+  if (more) dma_tile<D, true>(Kn, Vn, kb, vb, offs, TK);
+  if (busy) half_tile_dma<D, false, NG>(st, Kc, Vc, h, qf, 32);
 }
 
 // Register-staged copy of one 64-row K/V tile (software pipelining: the

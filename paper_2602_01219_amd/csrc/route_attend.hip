@@ -590,11 +590,9 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
     auto run = [&](auto ng) {
       constexpr int NG = decltype(ng)::value;
       auto step = [&](int i, const T *Kc, const T *Vc, T *Kn, T *Vn) {
-        if (i + 1 < nfull) {
-          tile_base(i + 1, kb, vb, off);
-          dma_tile<D, true>(Kn, Vn, kb, vb, rows + off, TK);
-        }
-        if (wave_busy) half_tile_dma<D, false, NG>(st, Kc, Vc, kh, qf, 32);
+        const bool more = i + 1 < nfull;
+        if (more) tile_base(i + 1, kb, vb, off);
+        dma_step<D, NG>(st, Kc, Vc, Kn, Vn, more, kb, vb, rows + off, wave_busy, kh, qf);
         wait_loads();
         __syncthreads();
       };
