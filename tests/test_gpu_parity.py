@@ -436,6 +436,22 @@ def test_fused_selection_quantised_keys():
     assert _same(a, b)
 
 
+@pytest.mark.parametrize("scale", [0.3, 1.0 / 3.0, 0.0884])
+def test_fused_selection_with_scales_off_a_power_of_two(scale):
+    """The score pass tests candidates on the unscaled dot products against a
+    per-row bound derived from the pivot and the scale; with scales whose
+    products round (not powers of two) the lists must still be exactly those
+    of the scaled scores, so the outputs equal the full-score path's."""
+    inp, cfg, (q, k, v) = _small_dense()
+    cfg = dataclasses.replace(cfg, scale=scale)
+    ws = torch.empty(mita.workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    a = mita.forward(cfg, q, k, v, ws=ws)
+    fb = mita.forward_fallbacks(cfg, ws)
+    b = mita.forward(dataclasses.replace(cfg, full_scores=True), q, k, v)
+    log(f"  scale {scale}: fallback rows {fb}")
+    assert _same(a, b)
+
+
 def test_staged_gather_equals_in_place_gather():
     name = "vitb_hr_bf16"
     cfg = mita.Config.from_workload(_inputs(name).wl)
