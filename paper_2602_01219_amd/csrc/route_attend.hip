@@ -235,8 +235,14 @@ __device__ __forceinline__ void route_scan_body(ScanLds &sh, int bx, int by, con
   int32_t *tb = tile_base + bh * ntiles * (int64_t)M + e0;
   for (int t0 = 0; t0 < ntiles; t0 += 256) {
     const int tt = t0 + tid;
+    // all SCAN_EB loads issued before any is used: addresses clamped into the
+    // tile row's expert block (always valid), values masked afterwards
+    const int64_t trow = (int64_t)(tt < ntiles ? tt : 0) * M;
+    uint32_t c[SCAN_EB];
 #pragma unroll
-    for (int j = 0; j < SCAN_EB; ++j) cnt[tid][j] = tt < ntiles && j < ne ? (uint32_t)tc[(int64_t)tt * M + j] : 0u;
+    for (int j = 0; j < SCAN_EB; ++j) c[j] = (uint32_t)tc[trow + min(j, ne - 1)];
+#pragma unroll
+    for (int j = 0; j < SCAN_EB; ++j) cnt[tid][j] = tt < ntiles && j < ne ? c[j] : 0u;
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < 4; ++q) {

@@ -152,17 +152,20 @@ __global__ __launch_bounds__(64 * NW) void sample_pivot_kernel(const T *__restri
   }
   const T *kb_ = k + bh * (int64_t)N * D;
   for (int j0 = w * PERW; j0 < min(ns, (w + 1) * PERW); j0 += TK) {
+    // the tile's A fragments, all loads issued before the first is used
+    Frag<T> a[4][D / 32];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       const int j = j0 + kb * 16 + p;  // A row p of block kb: sample j
       const int64_t pos = j < ns ? sample_pos(j, N, ns) : 0;
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) a[kb][ks].load(kb_ + pos * D + ks * 32 + g * 8);
+    }
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
       f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ks = 0; ks < D / 32; ++ks) {
-        Frag<T> a;
-        a.load(kb_ + pos * D + ks * 32 + g * 8);
-        acc = mma(a, qf[ks], acc);
-      }
+      for (int ks = 0; ks < D / 32; ++ks) acc = mma(a[kb][ks], qf[ks], acc);
       // lane (g, p) holds samples j0 + 16 kb + 4 g + (0..3) of row p
       const int jb = j0 + kb * 16 + 4 * g;
       uint32_t key[4];
