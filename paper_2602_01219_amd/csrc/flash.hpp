@@ -236,7 +236,10 @@ __device__ __forceinline__ void half_tile_attend(Online2<D> &st, const T *__rest
   if (__ballot(mx[0] > st.thr[0] || mx[1] > st.thr[1])) {
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      const float m_new = fmaxf(st.m[c], max_lane_groups(mx[c]) * sl2);
+      // only a column past its own threshold moves its reference, so a
+      // query's arithmetic does not depend on the other queries of the tile
+      const float cmx = max_lane_groups(mx[c]);
+      const float m_new = cmx > st.thr[c] ? fmaxf(st.m[c], cmx * sl2) : st.m[c];
       const float alpha = __builtin_amdgcn_exp2f(st.m[c] - m_new);
       st.m[c] = m_new;
       st.thr[c] = (m_new + RESCALE_LOG2) * __builtin_amdgcn_rcpf(sl2);
@@ -390,8 +393,10 @@ __device__ __forceinline__ void half_tile_dma(OnlineDma<D> &st, const bf16_t *Kl
     for (int c = 0; c < NG; ++c) {
       const float cm = max_lane_groups(mx[c]);
       // first tile: the reference becomes the column max (the accumulators
-      // are still zero); later: raised by the excess only
-      const float d = st.started ? fmaxf(cm, 0.f) : cm;
+      // are still zero); later: raised by the excess, only in a column past
+      // the threshold, so a query's arithmetic does not depend on the other
+      // queries of the tile
+      const float d = st.started ? (cm > RESCALE_LOG2 ? cm : 0.f) : cm;
       st.nm[c] -= d;
       if (st.started) {
         const float alpha = __builtin_amdgcn_exp2f(-d);

@@ -33,7 +33,7 @@ template <typename T, int D> struct RouteLds {
 
 // Workgroup (bx, by) of the routing grid; lms: RouteLds<T, D>::BYTES of LDS,
 // cnt: 4 M words of LDS.
-template <typename T, int D>
+template <typename T, int D, bool TILES = true>
 __device__ __forceinline__ void route_logits_body(T *lms, uint32_t *cnt, int bx, int by, const T *__restrict__ q,
                                                   const T *__restrict__ q_lm, int32_t *__restrict__ expert,
                                                   int32_t *__restrict__ tile_cnt, int32_t *__restrict__ counts, int N,
@@ -121,10 +121,10 @@ __device__ __forceinline__ void route_logits_body(T *lms, uint32_t *cnt, int bx,
       atomicAdd(&wc[arg[c]], 1u);
     }
   }
-  int32_t *tc = tile_cnt + (bh * ntiles + tile) * (int64_t)M;
+  int32_t *tc = TILES ? tile_cnt + (bh * ntiles + tile) * (int64_t)M : nullptr;
   for (int i = lane; i < M; i += 64) {
     const uint32_t x = wc[i];
-    tc[i] = (int32_t)x;
+    if (TILES) tc[i] = (int32_t)x;
     if (x) atomicAdd(&counts[bh * M + i], (int32_t)x);  // integer sums: order-independent
   }
 }
@@ -307,6 +307,71 @@ __device__ __forceinline__ void route_scatter_body(int bx, int by, const int32_t
   }
 }
 
+// Grouping without a stable order inside an expert (the forward's own
+// routing: each query's output does not depend on which queries share its
+// attention tile, so any order within an expert gives the same result).
+// route_place_body, one workgroup per head: offsets[e] = sizes of the experts
+// before e, the work list tile_start, and cursor[e] = offsets[e];
+// route_scatter_atomic_body: each wave takes, per expert among its 64
+// queries, one block of positions with one atomic add on the cursor and
+// places its queries there in lane order.
+__device__ __forceinline__ void route_place_body(uint32_t *wsum, int by, const int32_t *__restrict__ counts,
+                                                 int32_t *__restrict__ offsets, int32_t *__restrict__ tile_start,
+                                                 int32_t *__restrict__ cursor, int M) {
+  constexpr int EPT = (1024 + 255) / 256;  // experts per thread (M <= 1024)
+  const int64_t bh = by;
+  const int tid = threadIdx.x;
+  uint32_t sz[EPT], a = 0, t = 0;
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    const int e = tid * EPT + u;
+    sz[u] = e < M ? (uint32_t)counts[bh * M + e] : 0u;
+    a += sz[u];
+    t += (sz[u] + ATT_TQ - 1) / ATT_TQ;
+  }
+  uint32_t atot, ttot;
+  uint32_t off = block_exclusive_scan<256>(a, wsum, &atot);
+  uint32_t ts = block_exclusive_scan<256>(t, wsum, &ttot);
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    const int e = tid * EPT + u;
+    if (e < M) {
+      offsets[bh * (M + 1) + e] = (int32_t)off;
+      cursor[bh * M + e] = (int32_t)off;
+      tile_start[bh * (M + 1) + e] = (int32_t)ts;
+    }
+    off += sz[u];
+    ts += (sz[u] + ATT_TQ - 1) / ATT_TQ;
+  }
+  if (tid == 0) {
+    offsets[bh * (M + 1) + M] = (int32_t)atot;
+    tile_start[bh * (M + 1) + M] = (int32_t)ttot;
+  }
+}
+
+__device__ __forceinline__ void route_scatter_atomic_body(int bx, int by, const int32_t *__restrict__ expert,
+                                                          int32_t *__restrict__ cursor, int32_t *__restrict__ perm,
+                                                          int N, int M, int ntiles, int ebits) {
+  const int64_t bh = by;
+  const int tile = bx * 4 + (threadIdx.x >> 6);
+  if (tile >= ntiles) return;
+  const int lane = threadIdx.x & 63;
+  const int n = tile * ROUTE_TQ + lane;
+  const bool valid = n < N;
+  const int e = valid ? expert[bh * N + n] : 0;
+  uint64_t same = __ballot(valid);
+  for (int b = 0; b < ebits; ++b) {
+    const bool bit = (e >> b) & 1;
+    const uint64_t ones = __ballot(bit);
+    same &= bit ? ones : ~ones;
+  }
+  const int leader = valid ? __ffsll((unsigned long long)same) - 1 : lane;
+  int base = 0;
+  if (valid && lane == leader) base = atomicAdd(&cursor[bh * M + e], __popcll(same));
+  base = __shfl(base, leader);
+  if (valid) perm[bh * N + base + (int)lanes_below(same)] = n;
+}
+
 __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t *__restrict__ expert,
                                                             const int32_t *__restrict__ tile_base,
                                                             int32_t *__restrict__ perm, int N, int M, int ntiles,
@@ -320,8 +385,10 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t *__res
 // the routing work fill one another's idle time and the fallback steps (which
 // normally have nothing to do) cost no launch of their own:
 //   finalize_logits_kernel: selection finalize rows | routing logits;
-//   rows_scan_kernel:       fallback score rows     | routing scan;
+//   rows_place_kernel:      fallback score rows     | expert placement;
 //   topk_scatter_kernel:    fallback top-k rows     | routing scatter.
+// Here the queries of an expert are grouped without a stable order (see
+// route_place_body); mita_route keeps the stable grouping.
 // The routing part's 2-D grid is flattened (x fastest). LDS is one buffer
 // that either part lays out for itself.
 // ---------------------------------------------------------------------------
@@ -356,34 +423,32 @@ __global__ __launch_bounds__(BLOCK) void finalize_logits_kernel(
                                    fail_cnt, fail_list, k, cap, nch, part_ml, part_o, v_lm, M);
     return;
   }
-  route_logits_body<T, D>(reinterpret_cast<T *>(buf), cnt, i % route_x, i / route_x, q, q_lm, expert, tile_cnt, counts,
+  route_logits_body<T, D, false>(reinterpret_cast<T *>(buf), cnt, i % route_x, i / route_x, q, q_lm, expert, tile_cnt, counts,
                           N, M, scale, ntiles);
 }
 
-template <typename T, int D> struct RowsScanLds {
-  static constexpr int ROWS = 2 * TileDims<T, D>::K_ELEMS * (int)sizeof(T);
-  static constexpr int BYTES = ROWS > (int)sizeof(ScanLds) ? ROWS : (int)sizeof(ScanLds);
+template <typename T, int D> struct RowsPlaceLds {
+  static constexpr int ROWS = 2 * TileDims<T, D>::K_ELEMS * (int)sizeof(T);  // two K tiles
+  static constexpr int BYTES = ROWS > 64 ? ROWS : 64;                        // or the placement's scan words
 };
 
-// Workgroups [0, nA) walk the fallback score-row items, the rest scan.
+// Workgroups [0, nA) walk the fallback score-row items, the rest (one per
+// head) place the experts.
 template <typename T, int D>
-__global__ __launch_bounds__(BLOCK) void rows_scan_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
-                                                          float *__restrict__ S, const uint32_t *__restrict__ nrows,
-                                                          const int32_t *__restrict__ rows, int nchunks, int nA,
-                                                          float scale, const int32_t *__restrict__ tile_cnt,
-                                                          const int32_t *__restrict__ counts,
-                                                          int32_t *__restrict__ tile_base,
-                                                          int32_t *__restrict__ offsets, int32_t *__restrict__ tile_start,
-                                                          int ntiles, int M, int N, int scan_x) {
-  __shared__ __align__(16) char buf[RowsScanLds<T, D>::BYTES];
+__global__ __launch_bounds__(BLOCK) void rows_place_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
+                                                           float *__restrict__ S, const uint32_t *__restrict__ nrows,
+                                                           const int32_t *__restrict__ rows, int nchunks, int nA,
+                                                           float scale, const int32_t *__restrict__ counts,
+                                                           int32_t *__restrict__ offsets,
+                                                           int32_t *__restrict__ tile_start,
+                                                           int32_t *__restrict__ cursor, int M, int N) {
+  __shared__ __align__(16) char buf[RowsPlaceLds<T, D>::BYTES];
   const int b = (int)blockIdx.x;
   if (b < nA) {
     scores_rows_body<T, D>(reinterpret_cast<T *>(buf), b, nA, q_lm, k, S, nrows, rows, N, M, scale, nchunks);
     return;
   }
-  const int rb = b - nA;
-  route_scan_body(*reinterpret_cast<ScanLds *>(buf), rb % scan_x, rb / scan_x, tile_cnt, counts, tile_base, offsets,
-                  tile_start, ntiles, M, N);
+  route_place_body(reinterpret_cast<uint32_t *>(buf), b - nA, counts, offsets, tile_start, cursor, M);
 }
 
 // Workgroups [0, nT) walk the fallback rows' top-k (rows streamed from
@@ -393,9 +458,8 @@ __global__ __launch_bounds__(256) void topk_scatter_kernel(const float *__restri
                                                            int kk, const uint32_t *__restrict__ nrows,
                                                            const int32_t *__restrict__ rows, int nT,
                                                            const int32_t *__restrict__ expert,
-                                                           const int32_t *__restrict__ tile_base,
-                                                           int32_t *__restrict__ perm, int N, int M, int ntiles,
-                                                           int ebits, int route_x) {
+                                                           int32_t *__restrict__ cursor, int32_t *__restrict__ perm,
+                                                           int N, int M, int ntiles, int ebits, int route_x) {
   __shared__ TopkSmem<CAP> sh;
   const int b = (int)blockIdx.x;
   if (b < nT) {
@@ -403,7 +467,7 @@ __global__ __launch_bounds__(256) void topk_scatter_kernel(const float *__restri
     return;
   }
   const int rb = b - nT;
-  route_scatter_body(rb % route_x, rb / route_x, expert, tile_base, perm, N, M, ntiles, ebits);
+  route_scatter_atomic_body(rb % route_x, rb / route_x, expert, cursor, perm, N, M, ntiles, ebits);
 }
 
 // Attention work list: tile_start[e] = sum over e' < e of ceil(size(e') / 64),
@@ -726,11 +790,17 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
   }
   __syncthreads();
   if (!(k1 ? qvalid[1] : qvalid[0])) return;
+  // The two key halves are combined in a fixed order (half 0, then half 1)
+  // whichever wave does it, so a query's result does not depend on the
+  // column group it was given (with fused multiply-adds, a * b + c * d and
+  // c * d + a * b can round differently).
   const float *theirs = xb + (w ^ 1) * XN * 64 + lane;
-  const float m0 = k1 ? st.mval(1) : st.mval(0), m1 = xm[(w ^ 1) * 128 + lane];
+  const float m_mine = k1 ? st.mval(1) : st.mval(0), m_theirs = xm[(w ^ 1) * 128 + lane];
+  const float l_mine = k1 ? st.l(1) : st.l(0), l_theirs = xm[(w ^ 1) * 128 + 64 + lane];
+  const float m0 = k1 ? m_theirs : m_mine, m1 = k1 ? m_mine : m_theirs;  // halves 0 and 1
   const float mm = fmaxf(m0, m1);
   const float a0 = __builtin_amdgcn_exp2f(m0 - mm), a1 = __builtin_amdgcn_exp2f(m1 - mm);
-  const float l = (k1 ? st.l(1) : st.l(0)) * a0 + xm[(w ^ 1) * 128 + 64 + lane] * a1;
+  const float l = (k1 ? l_theirs : l_mine) * a0 + (k1 ? l_mine : l_theirs) * a1;
   const float inv = 1.0f / l;
   const float s0 = a0 * inv, s1 = a1 * inv;
   T *orow = o + (bh * N + (k1 ? token[1] : token[0])) * D;
@@ -738,8 +808,10 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
   for (int db = 0; db < D / 16; ++db) {
     T vals[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      vals[r] = from_f32<T>((k1 ? st.o[1][db][r] : st.o[0][db][r]) * s0 + theirs[(db * 4 + r) * 64] * s1);
+    for (int r = 0; r < 4; ++r) {
+      const float om = k1 ? st.o[1][db][r] : st.o[0][db][r], ot = theirs[(db * 4 + r) * 64];
+      vals[r] = from_f32<T>((k1 ? ot : om) * s0 + (k1 ? om : ot) * s1);
+    }
     T *dst = orow + db * 16 + 4 * g;
     if (sizeof(T) == 2)
       *reinterpret_cast<uint2 *>(dst) = *reinterpret_cast<const uint2 *>(vals);
@@ -793,7 +865,7 @@ static hipError_t select_route_t(const mita_cfg_t &c, const void *q, const void 
   const float2 *ml = (const float2 *)partial;
   const float *po = MERGE ? (const float *)((const char *)partial + align_up((size_t)rows * nch * sizeof(float2)))
                           : nullptr;
-  const int route_x = (nt + 3) / 4, scan_x = (c.M + SCAN_EB - 1) / SCAN_EB;
+  const int route_x = (nt + 3) / 4;
   const int nF = (int)rows, nR = route_x * bh;
   hipLaunchKernelGGL((finalize_logits_kernel<T, D, CAP, MERGE>), dim3((unsigned)(nF + nR)), dim3(BLOCK),
                      4 * c.M * sizeof(uint32_t), st, sb.cand, sb.ccnt, idx, sb.fail_cnt, sb.fail_list, c.k, sb.cap,
@@ -804,19 +876,21 @@ static hipError_t select_route_t(const mita_cfg_t &c, const void *q, const void 
   // the fallback grids of scores_rows_kernel and topk_kernel (listed mode)
   const int nA = (int)(rows * nch < 1024 ? rows * nch : 1024);
   const int nT = (int)(rows < 512 ? rows : 512);
-  hipLaunchKernelGGL((rows_scan_kernel<T, D>), dim3((unsigned)(nA + scan_x * bh)), dim3(BLOCK), 0, st,
-                     (const T *)q_lm, (const T *)k, S, sb.fail_cnt, sb.fail_list, nch, nA, eff_scale(c), tile_cnt,
-                     counts, tile_base, offsets, tile_start, nt, c.M, c.N, scan_x);
+  // the expert placement cursors live in the (here unused) tile_base buffer
+  int32_t *cursor = tile_base;
+  hipLaunchKernelGGL((rows_place_kernel<T, D>), dim3((unsigned)(nA + bh)), dim3(BLOCK), 0, st, (const T *)q_lm,
+                     (const T *)k, S, sb.fail_cnt, sb.fail_list, nch, nA, eff_scale(c), counts, offsets, tile_start,
+                     cursor, c.M, c.N);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   int ebits = 0;
   while ((1 << ebits) < c.M) ++ebits;
   constexpr int TCAP = 512;
   if (c.N % 4 == 0)
     hipLaunchKernelGGL((topk_scatter_kernel<TCAP, true>), dim3((unsigned)(nT + nR)), dim3(256), 0, st, S, idx, c.k,
-                       sb.fail_cnt, sb.fail_list, nT, expert, tile_base, perm, c.N, c.M, nt, ebits, route_x);
+                       sb.fail_cnt, sb.fail_list, nT, expert, cursor, perm, c.N, c.M, nt, ebits, route_x);
   else
     hipLaunchKernelGGL((topk_scatter_kernel<TCAP, false>), dim3((unsigned)(nT + nR)), dim3(256), 0, st, S, idx, c.k,
-                       sb.fail_cnt, sb.fail_list, nT, expert, tile_base, perm, c.N, c.M, nt, ebits, route_x);
+                       sb.fail_cnt, sb.fail_list, nT, expert, cursor, perm, c.N, c.M, nt, ebits, route_x);
   return hipGetLastError();
 }
 

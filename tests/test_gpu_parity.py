@@ -452,6 +452,31 @@ def test_fused_selection_with_scales_off_a_power_of_two(scale):
     assert _same(a, b)
 
 
+@pytest.mark.parametrize("name", ["vits_bf16", "vitb_hr_bf16"])
+def test_attention_does_not_depend_on_query_order_within_experts(name):
+    """Each query's output is its own: shuffling the queries inside every
+    expert's segment of perm (which changes the attention tiles they share
+    and the MFMA columns they take) gives bit-identical outputs. The forward
+    relies on this when it groups the queries of an expert in arrival order."""
+    cfg = mita.Config.from_workload(_inputs(name).wl)
+    q, k, v = _dev_inputs(name)
+    q_lm = mita.landmarks(cfg, q)
+    S, v_lm = mita.scores(cfg, q_lm, k, v, want_scores=True, want_v_lm=True)
+    idx = mita.topk(cfg, S)
+    kx, vx = mita.gather(cfg, k, v, idx)
+    expert, perm, offsets = mita.route(cfg, q, q_lm)
+    o1 = mita.attend(cfg, q, q_lm, v_lm, kx, vx, perm, offsets)
+    P, OF = perm.cpu().numpy().copy(), offsets.cpu().numpy()
+    r = np.random.default_rng(5)
+    for b in range(P.shape[0]):
+        for h in range(P.shape[1]):
+            for e in range(cfg.M):
+                seg = P[b, h, OF[b, h, e]:OF[b, h, e + 1]]
+                r.shuffle(seg)
+    o2 = mita.attend(cfg, q, q_lm, v_lm, kx, vx, torch.from_numpy(P).cuda(), offsets)
+    assert _same(o1, o2)
+
+
 def test_staged_gather_equals_in_place_gather():
     name = "vitb_hr_bf16"
     cfg = mita.Config.from_workload(_inputs(name).wl)
