@@ -52,7 +52,7 @@ int main() {
   mita::FwdLayout L = mita::forward_layout(c);
   const size_t offs[] = {L.q_lm,      L.v_lm,   L.scores, L.partial, L.idx,     L.kx,   L.vx,
                          L.expert,    L.perm,   L.offsets, L.tile_cnt, L.tile_base, L.counts, L.tile_start,
-                         L.samp,      L.plo,    L.ccnt,   L.cand,    L.fail,    L.total};
+                         L.plo,    L.ccnt,   L.cand,    L.fail,    L.total};
   for (size_t i = 0; i + 1 < sizeof offs / sizeof offs[0]; ++i) {
     assert(offs[i] % 256 == 0);
     assert(offs[i] <= offs[i + 1]);
@@ -68,12 +68,12 @@ int main() {
   // -> 61 at N = 16384, k = 512; expected count bound (61 + 6 sqrt(61)) * 16 -> cap 2048
   assert(mita::fused_select(c) && mita::sel_ns(c) == 1024 && mita::sel_cap(c) == 2048);
   assert(mita::sel_rank(c) == 61);
-  assert(L2.plo - L2.samp == (size_t)24 * 128 * 1024 * 4);
+  assert(L2.ccnt - L2.plo == (size_t)24 * 128 * 4);
   assert(L2.cand - L2.ccnt == (size_t)24 * 128 * 32 * 4);
   assert(L2.fail - L2.cand == (size_t)24 * 128 * 32 * 512 * 8);
   assert(L2.total - L2.fail >= (size_t)(24 * 128 + 1) * 4);
   c.flags = MITA_FLAG_FULL_SCORES;
-  assert(!mita::fused_select(c) && mita::forward_layout(c).samp == mita::forward_layout(c).total);
+  assert(!mita::fused_select(c) && mita::forward_layout(c).plo == mita::forward_layout(c).total);
   c.flags = 0;
   c.k = 1025;
   assert(!mita::fused_select(c));
