@@ -9,8 +9,10 @@
 namespace mita {
 
 // Landmark pooling (Sec. 3.2; Algorithm 1 AdaptiveAvgPool): q [BH,N,d] -> q_lm [BH,M,d].
-// If zero_counts is not NULL its BH*M entries are set to 0 (routing totals).
-hipError_t launch_pool(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *zero_counts, hipStream_t st);
+// If zero_counts (zero_cursor) is not NULL its BH*M entries are set to 0
+// (routing totals; the forward's placement cursors).
+hipError_t launch_pool(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *zero_counts, int32_t *zero_cursor,
+                       hipStream_t st);
 
 // Set n int32 entries to 0.
 hipError_t launch_zero(int32_t *p, int64_t n, hipStream_t st);

@@ -112,16 +112,18 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
     sel.rank = sel_rank(*c);
   }
 
+  // with the fused selection and in-place gather, the selection's finish
+  // shares launches with the routing (the "route" stage then includes it),
+  // whose placement cursors (in the tile_base buffer) start at zero
+  const bool sel_in_route = fused && c->use_routed && !staged;
   TRY(mark(0));
-  TRY(hip_status(launch_pool(*c, q, q_lm, c->use_routed ? counts : nullptr, st), "landmarks"));
+  TRY(hip_status(launch_pool(*c, q, q_lm, c->use_routed ? counts : nullptr, sel_in_route ? tile_base : nullptr, st),
+                 "landmarks"));
   TRY(mark(1));
   if (fused) TRY(hip_status(launch_select_pivots(*c, q_lm, k, sel, st), "select pivots"));
   TRY(hip_status(launch_scores(*c, q_lm, k, v, fused ? nullptr : S, v_lm, w + L.partial, fused ? &sel : nullptr, st),
                  "scores"));
   TRY(mark(2));
-  // with the fused selection and in-place gather, the selection's finish
-  // shares launches with the routing (the "route" stage then includes it)
-  const bool sel_in_route = fused && c->use_routed && !staged;
   if (fused && !sel_in_route)
     TRY(hip_status(launch_select_finish(*c, q_lm, k, sel, S, idx, w + L.partial, v_lm, st), "topk"));
   else if (!fused && c->use_routed)
@@ -200,7 +202,7 @@ int mita_landmarks(const mita_cfg_t *cfg, const void *q, void *q_lm, mita_stream
   TRY(validate(cfg));
   TRY(need_ptr(q, "q"));
   TRY(need_ptr(q_lm, "q_lm"));
-  return hip_status(launch_pool(*cfg, q, q_lm, nullptr, (hipStream_t)stream), "landmarks");
+  return hip_status(launch_pool(*cfg, q, q_lm, nullptr, nullptr, (hipStream_t)stream), "landmarks");
 }
 
 int mita_scores(const mita_cfg_t *cfg, const void *q_lm, const void *k, const void *v, float *scores, void *v_lm,

@@ -17,8 +17,8 @@ namespace mita {
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 __global__ __launch_bounds__(256) void pool_kernel(const T *__restrict__ q, T *__restrict__ q_lm,
-                                                   int32_t *__restrict__ zero_counts, int N, int gh, int gw, int lh,
-                                                   int lw) {
+                                                   int32_t *__restrict__ zero_counts, int32_t *__restrict__ zero_cursor,
+                                                   int N, int gh, int gw, int lh, int lw) {
   constexpr int VE = 16 / (int)sizeof(T);
   constexpr int CPT = D / VE;   // chunks per token row
   constexpr int P = 256 / CPT;  // token slots
@@ -31,6 +31,7 @@ __global__ __launch_bounds__(256) void pool_kernel(const T *__restrict__ q, T *_
   const int c0 = (int)(((int64_t)b * gw) / lw), c1 = (int)(((int64_t)(b + 1) * gw + lw - 1) / lw);
   const int cols = c1 - c0, count = (r1 - r0) * cols;
   if (zero_counts && threadIdx.x == 0) zero_counts[bh * M + i] = 0;
+  if (zero_cursor && threadIdx.x == 0) zero_cursor[bh * M + i] = 0;
   const int ch = threadIdx.x % CPT, slot = threadIdx.x / CPT;
   float acc[VE];
 #pragma unroll
@@ -140,17 +141,18 @@ __global__ __launch_bounds__(256) void gather_kernel(const T *__restrict__ k, co
 // launchers
 // ---------------------------------------------------------------------------
 template <typename T, int D>
-static hipError_t pool_t(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *zc, hipStream_t st) {
+static hipError_t pool_t(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *zc, int32_t *zcur,
+                         hipStream_t st) {
   dim3 grid(c.M, (unsigned)BH(c));
-  hipLaunchKernelGGL((pool_kernel<T, D>), grid, dim3(256), 0, st, (const T *)q, (T *)q_lm, zc, c.N, c.grid_h,
+  hipLaunchKernelGGL((pool_kernel<T, D>), grid, dim3(256), 0, st, (const T *)q, (T *)q_lm, zc, zcur, c.N, c.grid_h,
                      c.grid_w, c.lm_h, c.lm_w);
   return hipGetLastError();
 }
 
-hipError_t launch_pool(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *zc, hipStream_t st) {
+hipError_t launch_pool(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *zc, int32_t *zcur, hipStream_t st) {
   if (c.dtype == MITA_F32)
-    return c.d == 64 ? pool_t<float, 64>(c, q, q_lm, zc, st) : pool_t<float, 128>(c, q, q_lm, zc, st);
-  return c.d == 64 ? pool_t<bf16_t, 64>(c, q, q_lm, zc, st) : pool_t<bf16_t, 128>(c, q, q_lm, zc, st);
+    return c.d == 64 ? pool_t<float, 64>(c, q, q_lm, zc, zcur, st) : pool_t<float, 128>(c, q, q_lm, zc, zcur, st);
+  return c.d == 64 ? pool_t<bf16_t, 64>(c, q, q_lm, zc, zcur, st) : pool_t<bf16_t, 128>(c, q, q_lm, zc, zcur, st);
 }
 
 __global__ __launch_bounds__(256) void zero_kernel(int32_t *__restrict__ p, int64_t n) {

@@ -308,16 +308,22 @@ __device__ __forceinline__ void route_scatter_body(int bx, int by, const int32_t
 }
 
 // Grouping without a stable order inside an expert (the forward's own
-// routing: each query's output does not depend on which queries share its
-// attention tile, so any order within an expert gives the same result).
-// route_place_body, one workgroup per head: offsets[e] = sizes of the experts
-// before e, the work list tile_start, and cursor[e] = offsets[e];
-// route_scatter_atomic_body: each wave takes, per expert among its 64
-// queries, one block of positions with one atomic add on the cursor and
-// places its queries there in lane order.
-__device__ __forceinline__ void route_place_body(uint32_t *wsum, int by, const int32_t *__restrict__ counts,
-                                                 int32_t *__restrict__ offsets, int32_t *__restrict__ tile_start,
-                                                 int32_t *__restrict__ cursor, int M) {
+// routing: the attention gives each query the same result whatever its
+// position in the grouping, so any order within an expert gives the same
+// output). Workgroup (bx, by) of the scatter grid: the head's expert sizes
+// become offsets (a block scan every workgroup of the head does for itself,
+// into LDS; workgroup 0 of the head also writes offsets and the attention
+// work list tile_start); each wave then takes, per expert among its 64
+// queries, one block of positions with one atomic add on that expert's
+// cursor (zeroed by the pooling) and places its queries there in lane order.
+// pre: M + 1 words of LDS, wsum: 4 words.
+__device__ __forceinline__ void route_scatter_place_body(uint32_t *pre, uint32_t *wsum, int bx, int by,
+                                                         const int32_t *__restrict__ expert,
+                                                         const int32_t *__restrict__ counts,
+                                                         int32_t *__restrict__ cursor, int32_t *__restrict__ perm,
+                                                         int32_t *__restrict__ offsets,
+                                                         int32_t *__restrict__ tile_start, int N, int M, int ntiles,
+                                                         int ebits) {
   constexpr int EPT = (1024 + 255) / 256;  // experts per thread (M <= 1024)
   const int64_t bh = by;
   const int tid = threadIdx.x;
@@ -331,31 +337,28 @@ __device__ __forceinline__ void route_place_body(uint32_t *wsum, int by, const i
   }
   uint32_t atot, ttot;
   uint32_t off = block_exclusive_scan<256>(a, wsum, &atot);
-  uint32_t ts = block_exclusive_scan<256>(t, wsum, &ttot);
+  uint32_t ts = bx == 0 ? block_exclusive_scan<256>(t, wsum, &ttot) : 0u;  // uniform for the workgroup
 #pragma unroll
   for (int u = 0; u < EPT; ++u) {
     const int e = tid * EPT + u;
     if (e < M) {
-      offsets[bh * (M + 1) + e] = (int32_t)off;
-      cursor[bh * M + e] = (int32_t)off;
-      tile_start[bh * (M + 1) + e] = (int32_t)ts;
+      pre[e] = off;
+      if (bx == 0) {
+        offsets[bh * (M + 1) + e] = (int32_t)off;
+        tile_start[bh * (M + 1) + e] = (int32_t)ts;
+      }
     }
     off += sz[u];
     ts += (sz[u] + ATT_TQ - 1) / ATT_TQ;
   }
-  if (tid == 0) {
+  if (bx == 0 && tid == 0) {
     offsets[bh * (M + 1) + M] = (int32_t)atot;
     tile_start[bh * (M + 1) + M] = (int32_t)ttot;
   }
-}
-
-__device__ __forceinline__ void route_scatter_atomic_body(int bx, int by, const int32_t *__restrict__ expert,
-                                                          int32_t *__restrict__ cursor, int32_t *__restrict__ perm,
-                                                          int N, int M, int ntiles, int ebits) {
-  const int64_t bh = by;
-  const int tile = bx * 4 + (threadIdx.x >> 6);
-  if (tile >= ntiles) return;
-  const int lane = threadIdx.x & 63;
+  __syncthreads();
+  const int tile = bx * 4 + (tid >> 6);
+  if (tile >= ntiles) return;  // no workgroup barriers below
+  const int lane = tid & 63;
   const int n = tile * ROUTE_TQ + lane;
   const bool valid = n < N;
   const int e = valid ? expert[bh * N + n] : 0;
@@ -367,7 +370,7 @@ __device__ __forceinline__ void route_scatter_atomic_body(int bx, int by, const 
   }
   const int leader = valid ? __ffsll((unsigned long long)same) - 1 : lane;
   int base = 0;
-  if (valid && lane == leader) base = atomicAdd(&cursor[bh * M + e], __popcll(same));
+  if (valid && lane == leader) base = (int)pre[e] + atomicAdd(&cursor[bh * M + e], __popcll(same));
   base = __shfl(base, leader);
   if (valid) perm[bh * N + base + (int)lanes_below(same)] = n;
 }
@@ -385,10 +388,10 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t *__res
 // the routing work fill one another's idle time and the fallback steps (which
 // normally have nothing to do) cost no launch of their own:
 //   finalize_logits_kernel: selection finalize rows | routing logits;
-//   rows_place_kernel:      fallback score rows     | expert placement;
-//   topk_scatter_kernel:    fallback top-k rows     | routing scatter.
+//   topk_scatter_kernel:    fallback rows (scored in full, then their top-k)
+//                           | routing placement and scatter.
 // Here the queries of an expert are grouped without a stable order (see
-// route_place_body); mita_route keeps the stable grouping.
+// route_scatter_place_body); mita_route keeps the stable grouping.
 // The routing part's 2-D grid is flattened (x fastest). LDS is one buffer
 // that either part lays out for itself.
 // ---------------------------------------------------------------------------
@@ -427,47 +430,52 @@ __global__ __launch_bounds__(BLOCK) void finalize_logits_kernel(
                           N, M, scale, ntiles);
 }
 
-template <typename T, int D> struct RowsPlaceLds {
-  static constexpr int ROWS = 2 * TileDims<T, D>::K_ELEMS * (int)sizeof(T);  // two K tiles
-  static constexpr int BYTES = ROWS > 64 ? ROWS : 64;                        // or the placement's scan words
+// Workgroups [0, nT) take the fallback rows: each scores its rows in full
+// with the score pass's own arithmetic (one key chunk at a time), then
+// selects their top-k from those rows (the barrier between orders the stores
+// before the reads: the waves of a workgroup share one L1); the rest scatter.
+template <typename T, int D, int CAP, bool VEC> struct TopkScatterLds {
+  static constexpr int A = (int)sizeof(TopkSmem<CAP>);
+  static constexpr int B = 2 * TileDims<T, D>::K_ELEMS * (int)sizeof(T);  // two K tiles
+  static constexpr int BYTES = A > B ? A : B;
 };
 
-// Workgroups [0, nA) walk the fallback score-row items, the rest (one per
-// head) place the experts.
-template <typename T, int D>
-__global__ __launch_bounds__(BLOCK) void rows_place_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
-                                                           float *__restrict__ S, const uint32_t *__restrict__ nrows,
-                                                           const int32_t *__restrict__ rows, int nchunks, int nA,
-                                                           float scale, const int32_t *__restrict__ counts,
-                                                           int32_t *__restrict__ offsets,
-                                                           int32_t *__restrict__ tile_start,
-                                                           int32_t *__restrict__ cursor, int M, int N) {
-  __shared__ __align__(16) char buf[RowsPlaceLds<T, D>::BYTES];
-  const int b = (int)blockIdx.x;
-  if (b < nA) {
-    scores_rows_body<T, D>(reinterpret_cast<T *>(buf), b, nA, q_lm, k, S, nrows, rows, N, M, scale, nchunks);
-    return;
-  }
-  route_place_body(reinterpret_cast<uint32_t *>(buf), b - nA, counts, offsets, tile_start, cursor, M);
-}
-
-// Workgroups [0, nT) walk the fallback rows' top-k (rows streamed from
-// memory: a small LDS footprint for the scatter workgroups), the rest scatter.
-template <int CAP, bool VEC>
-__global__ __launch_bounds__(256) void topk_scatter_kernel(const float *__restrict__ S, int32_t *__restrict__ idx,
-                                                           int kk, const uint32_t *__restrict__ nrows,
+template <typename T, int D, int CAP, bool VEC>
+__global__ __launch_bounds__(256) void topk_scatter_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
+                                                           float *__restrict__ S, float scale, int nchunks,
+                                                           int32_t *__restrict__ idx, int kk,
+                                                           const uint32_t *__restrict__ nrows,
                                                            const int32_t *__restrict__ rows, int nT,
                                                            const int32_t *__restrict__ expert,
+                                                           const int32_t *__restrict__ counts,
                                                            int32_t *__restrict__ cursor, int32_t *__restrict__ perm,
-                                                           int N, int M, int ntiles, int ebits, int route_x) {
-  __shared__ TopkSmem<CAP> sh;
+                                                           int32_t *__restrict__ offsets,
+                                                           int32_t *__restrict__ tile_start, int N, int M, int ntiles,
+                                                           int ebits, int route_x) {
+  __shared__ __align__(16) char buf[TopkScatterLds<T, D, CAP, VEC>::BYTES];
   const int b = (int)blockIdx.x;
   if (b < nT) {
-    topk_listed_body<CAP, VEC, 0>(sh, nullptr, b, nT, S, idx, N, kk, nrows, rows);
+    const uint32_t nr = *nrows;
+    const SelectArgs none{nullptr, nullptr, nullptr};
+    for (uint32_t f = (uint32_t)b; f < nr; f += (uint32_t)nT) {
+      const int row = rows[f];
+      const int lm = row % M;
+      for (int chunk = 0; chunk < nchunks; ++chunk) {
+        __syncthreads();  // the previous use of the LDS is done
+        score_chunk<T, D, true, false, false>(reinterpret_cast<T *>(buf), nullptr, q_lm, k, nullptr, S, nullptr,
+                                              nullptr, none, N, M, scale, chunk, nchunks, lm / 64, row / M, lm);
+      }
+      __syncthreads();  // the row's scores are stored and visible to the workgroup
+      topk_row<CAP, VEC, 0>(*reinterpret_cast<TopkSmem<CAP> *>(buf), nullptr, S + (int64_t)row * N,
+                            idx + (int64_t)row * kk, N, kk);
+    }
     return;
   }
   const int rb = b - nT;
-  route_scatter_atomic_body(rb % route_x, rb / route_x, expert, cursor, perm, N, M, ntiles, ebits);
+  uint32_t *pre = reinterpret_cast<uint32_t *>(buf);
+  __shared__ uint32_t wsum[4];
+  route_scatter_place_body(pre, wsum, rb % route_x, rb / route_x, expert, counts, cursor, perm, offsets, tile_start,
+                           N, M, ntiles, ebits);
 }
 
 // Attention work list: tile_start[e] = sum over e' < e of ceil(size(e') / 64),
@@ -873,24 +881,20 @@ static hipError_t select_route_t(const mita_cfg_t &c, const void *q, const void 
                      eff_scale(c), nt, route_x, nR);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  // the fallback grids of scores_rows_kernel and topk_kernel (listed mode)
-  const int nA = (int)(rows * nch < 1024 ? rows * nch : 1024);
+  // the fallback workgroups of the last launch (listed rows, scored in full and selected)
   const int nT = (int)(rows < 512 ? rows : 512);
-  // the expert placement cursors live in the (here unused) tile_base buffer
-  int32_t *cursor = tile_base;
-  hipLaunchKernelGGL((rows_place_kernel<T, D>), dim3((unsigned)(nA + bh)), dim3(BLOCK), 0, st, (const T *)q_lm,
-                     (const T *)k, S, sb.fail_cnt, sb.fail_list, nch, nA, eff_scale(c), counts, offsets, tile_start,
-                     cursor, c.M, c.N);
-  if ((err = hipGetLastError()) != hipSuccess) return err;
+  int32_t *cursor = tile_base;  // the placement cursors live in the (here unused) tile_base buffer
   int ebits = 0;
   while ((1 << ebits) < c.M) ++ebits;
   constexpr int TCAP = 512;
   if (c.N % 4 == 0)
-    hipLaunchKernelGGL((topk_scatter_kernel<TCAP, true>), dim3((unsigned)(nT + nR)), dim3(256), 0, st, S, idx, c.k,
-                       sb.fail_cnt, sb.fail_list, nT, expert, cursor, perm, c.N, c.M, nt, ebits, route_x);
+    hipLaunchKernelGGL((topk_scatter_kernel<T, D, TCAP, true>), dim3((unsigned)(nT + nR)), dim3(256), 0, st,
+                       (const T *)q_lm, (const T *)k, S, eff_scale(c), nch, idx, c.k, sb.fail_cnt, sb.fail_list, nT,
+                       expert, counts, cursor, perm, offsets, tile_start, c.N, c.M, nt, ebits, route_x);
   else
-    hipLaunchKernelGGL((topk_scatter_kernel<TCAP, false>), dim3((unsigned)(nT + nR)), dim3(256), 0, st, S, idx, c.k,
-                       sb.fail_cnt, sb.fail_list, nT, expert, cursor, perm, c.N, c.M, nt, ebits, route_x);
+    hipLaunchKernelGGL((topk_scatter_kernel<T, D, TCAP, false>), dim3((unsigned)(nT + nR)), dim3(256), 0, st,
+                       (const T *)q_lm, (const T *)k, S, eff_scale(c), nch, idx, c.k, sb.fail_cnt, sb.fail_list, nT,
+                       expert, counts, cursor, perm, offsets, tile_start, c.N, c.M, nt, ebits, route_x);
   return hipGetLastError();
 }
 
