@@ -785,47 +785,60 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
                 "exchange buffers");
   float *xb = reinterpret_cast<float *>(tiles0);
   float *xm = reinterpret_cast<float *>(tiles1);
-  // (kh selects by value: register arrays indexed at run time would go to scratch)
-  const bool k1 = kh != 0;
-  {
+  // The two key halves are combined in a fixed order (half 0, then half 1)
+  // whichever wave does it, so a query's result does not depend on the
+  // column group it was given (with fused multiply-adds, a * b + c * d and
+  // c * d + a * b can round differently). The key half is a compile-time
+  // constant in each branch (it is uniform over the wave), so no selects.
+  auto hand_over = [&](auto khc) {
+    constexpr int KH = decltype(khc)::value;
     float *mine = xb + w * XN * 64 + lane;
 #pragma unroll
     for (int db = 0; db < D / 16; ++db)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) mine[(db * 4 + r) * 64] = k1 ? st.o[0][db][r] : st.o[1][db][r];
-    xm[w * 128 + lane] = k1 ? st.mval(0) : st.mval(1);
-    xm[w * 128 + 64 + lane] = k1 ? st.l(0) : st.l(1);
-  }
-  __syncthreads();
-  if (!(k1 ? qvalid[1] : qvalid[0])) return;
-  // The two key halves are combined in a fixed order (half 0, then half 1)
-  // whichever wave does it, so a query's result does not depend on the
-  // column group it was given (with fused multiply-adds, a * b + c * d and
-  // c * d + a * b can round differently).
-  const float *theirs = xb + (w ^ 1) * XN * 64 + lane;
-  const float m_mine = k1 ? st.mval(1) : st.mval(0), m_theirs = xm[(w ^ 1) * 128 + lane];
-  const float l_mine = k1 ? st.l(1) : st.l(0), l_theirs = xm[(w ^ 1) * 128 + 64 + lane];
-  const float m0 = k1 ? m_theirs : m_mine, m1 = k1 ? m_mine : m_theirs;  // halves 0 and 1
-  const float mm = fmaxf(m0, m1);
-  const float a0 = __builtin_amdgcn_exp2f(m0 - mm), a1 = __builtin_amdgcn_exp2f(m1 - mm);
-  const float l = (k1 ? l_theirs : l_mine) * a0 + (k1 ? l_mine : l_theirs) * a1;
-  const float inv = 1.0f / l;
-  const float s0 = a0 * inv, s1 = a1 * inv;
-  T *orow = o + (bh * N + (k1 ? token[1] : token[0])) * D;
+      for (int r = 0; r < 4; ++r) mine[(db * 4 + r) * 64] = st.o[1 - KH][db][r];
+    xm[w * 128 + lane] = st.mval(1 - KH);
+    xm[w * 128 + 64 + lane] = st.l(1 - KH);
+  };
+  auto finish = [&](auto khc) {
+    constexpr int KH = decltype(khc)::value;
+    if (!qvalid[KH]) return;
+    const float *theirs = xb + (w ^ 1) * XN * 64 + lane;
+    const float m_mine = st.mval(KH), m_theirs = xm[(w ^ 1) * 128 + lane];
+    const float l_mine = st.l(KH), l_theirs = xm[(w ^ 1) * 128 + 64 + lane];
+    const float m0 = KH ? m_theirs : m_mine, m1 = KH ? m_mine : m_theirs;  // halves 0 and 1
+    const float mm = fmaxf(m0, m1);
+    const float a0 = __builtin_amdgcn_exp2f(m0 - mm), a1 = __builtin_amdgcn_exp2f(m1 - mm);
+    // explicit fused multiply-adds: the two branches must round alike
+    const float l = __builtin_fmaf(KH ? l_mine : l_theirs, a1, (KH ? l_theirs : l_mine) * a0);
+    const float inv = __builtin_amdgcn_rcpf(l);
+    const float s0 = a0 * inv, s1 = a1 * inv;
+    T *orow = o + (bh * N + token[KH]) * D;
 #pragma unroll
-  for (int db = 0; db < D / 16; ++db) {
-    T vals[4];
+    for (int db = 0; db < D / 16; ++db) {
+      T vals[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float om = k1 ? st.o[1][db][r] : st.o[0][db][r], ot = theirs[(db * 4 + r) * 64];
-      vals[r] = from_f32<T>((k1 ? ot : om) * s0 + (k1 ? om : ot) * s1);
+      for (int r = 0; r < 4; ++r) {
+        const float om = st.o[KH][db][r], ot = theirs[(db * 4 + r) * 64];
+        vals[r] = from_f32<T>(__builtin_fmaf(KH ? om : ot, s1, (KH ? ot : om) * s0));
+      }
+      T *dst = orow + db * 16 + 4 * g;
+      if (sizeof(T) == 2)
+        *reinterpret_cast<uint2 *>(dst) = *reinterpret_cast<const uint2 *>(vals);
+      else
+        *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(vals);
     }
-    T *dst = orow + db * 16 + 4 * g;
-    if (sizeof(T) == 2)
-      *reinterpret_cast<uint2 *>(dst) = *reinterpret_cast<const uint2 *>(vals);
-    else
-      *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(vals);
-  }
+  };
+  const bool k1 = __builtin_amdgcn_readfirstlane(kh) != 0;  // uniform over the wave
+  if (k1)
+    hand_over(std::integral_constant<int, 1>{});
+  else
+    hand_over(std::integral_constant<int, 0>{});
+  __syncthreads();
+  if (k1)
+    finish(std::integral_constant<int, 1>{});
+  else
+    finish(std::integral_constant<int, 0>{});
 }
 
 // ---------------------------------------------------------------------------
