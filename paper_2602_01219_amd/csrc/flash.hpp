@@ -291,25 +291,26 @@ __device__ __forceinline__ void half_tile_attend(Online2<D> &st, const T *__rest
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int swz(int r) { return (r & 6) | ((r >> 3) & 1); }
 
-template <int D> struct DmaTile {
-  static constexpr int CPR = D / 8;        // 16-byte chunks per row
-  static constexpr int RPI = 64 / CPR;     // rows per wave instruction
-  static constexpr int NI = TK / RPI;      // instructions per 64-row matrix
-  static constexpr int PW = NI / 4;        // per wave of a 4-wave workgroup
-  static constexpr int BYTES = TK * D * 2; // one 64-row matrix
+template <int D, int ROWS = TK> struct DmaTile {
+  static constexpr int CPR = D / 8;          // 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;       // rows per wave instruction
+  static constexpr int NI = ROWS / RPI;      // instructions per ROWS-row matrix
+  static constexpr int PW = NI / 4;          // per wave of a 4-wave workgroup
+  static constexpr int BYTES = ROWS * D * 2; // one ROWS-row matrix
+  static_assert(PW >= 1 && NI % 4 == 0, "whole instructions per wave");
 };
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
 
-// Issue the DMA of one tile: rows r < 64 of K and V from byte offsets offs[r]
-// past kb and vb (without FULL, rows >= nrows take offset offs[0]: real
-// data, masked later).
-template <int D, bool FULL = false>
+// Issue the DMA of one tile: rows r < ROWS of K and V from byte offsets
+// offs[r] past kb and vb (without FULL, rows >= nrows take offset offs[0]:
+// real data, masked later).
+template <int D, bool FULL = false, int ROWS = TK>
 __device__ __forceinline__ void dma_tile(bf16_t *Kl, bf16_t *Vl, const bf16_t *kb, const bf16_t *vb,
                                          const uint32_t *offs, int nrows) {
-  using DT = DmaTile<D>;
+  using DT = DmaTile<D, ROWS>;
   // the wave index as a scalar: the LDS destinations (M0) need no readfirstlane
   const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6), lane = threadIdx.x & 63;
 #pragma unroll
@@ -451,12 +452,12 @@ __device__ __forceinline__ void half_tile_dma(OnlineDma<D> &st, const bf16_t *Kl
 // is multiplied (if `busy`). The buffers come in as restrict pointers, so the
 // compiler's alias information shows the reads of the current tile to be
 // disjoint from the DMA in flight and no wait for it is placed before them.
-template <int D, int NG>
+template <int D, int NG, int ROWS = TK>
 __device__ __forceinline__ void dma_step(OnlineDma<D> &st, const bf16_t *__restrict__ Kc,
                                          const bf16_t *__restrict__ Vc, bf16_t *__restrict__ Kn,
                                          bf16_t *__restrict__ Vn, bool more, const bf16_t *kb, const bf16_t *vb,
                                          const uint32_t *offs, bool busy, int h, const Frag<bf16_t> (&qf)[2][D / 32]) {
-  if (more) dma_tile<D, true>(Kn, Vn, kb, vb, offs, TK);
+  if (more) dma_tile<D, true, ROWS>(Kn, Vn, kb, vb, offs, ROWS);
   if (busy) half_tile_dma<D, false, NG>(st, Kc, Vc, h, qf, 32);
 }
 

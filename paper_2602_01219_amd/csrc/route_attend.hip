@@ -326,12 +326,31 @@ __device__ __forceinline__ void route_scatter_place_body(uint32_t *pre, uint32_t
                                                          int ebits) {
   constexpr int EPT = (1024 + 255) / 256;  // experts per thread (M <= 1024)
   const int64_t bh = by;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // the wave's queries and their experts first: the block of positions is
+  // taken (one atomic add per expert among the 64) while the sizes are
+  // scanned, so the two latencies overlap
+  const int tile = bx * 4 + (tid >> 6);
+  const int n = tile * ROUTE_TQ + lane;
+  const bool valid = tile < ntiles && n < N;
+  const int e = valid ? expert[bh * N + n] : 0;
   uint32_t sz[EPT], a = 0, t = 0;
 #pragma unroll
   for (int u = 0; u < EPT; ++u) {
-    const int e = tid * EPT + u;
-    sz[u] = e < M ? (uint32_t)counts[bh * M + e] : 0u;
+    const int x = tid * EPT + u;
+    sz[u] = x < M ? (uint32_t)counts[bh * M + x] : 0u;
+  }
+  uint64_t same = __ballot(valid);
+  for (int b = 0; b < ebits; ++b) {
+    const bool bit = (e >> b) & 1;
+    const uint64_t ones = __ballot(bit);
+    same &= bit ? ones : ~ones;
+  }
+  const int leader = valid ? __ffsll((unsigned long long)same) - 1 : lane;
+  int rel = 0;
+  if (valid && lane == leader) rel = atomicAdd(&cursor[bh * M + e], __popcll(same));
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
     a += sz[u];
     t += (sz[u] + ATT_TQ - 1) / ATT_TQ;
   }
@@ -340,12 +359,12 @@ __device__ __forceinline__ void route_scatter_place_body(uint32_t *pre, uint32_t
   uint32_t ts = bx == 0 ? block_exclusive_scan<256>(t, wsum, &ttot) : 0u;  // uniform for the workgroup
 #pragma unroll
   for (int u = 0; u < EPT; ++u) {
-    const int e = tid * EPT + u;
-    if (e < M) {
-      pre[e] = off;
+    const int x = tid * EPT + u;
+    if (x < M) {
+      pre[x] = off;
       if (bx == 0) {
-        offsets[bh * (M + 1) + e] = (int32_t)off;
-        tile_start[bh * (M + 1) + e] = (int32_t)ts;
+        offsets[bh * (M + 1) + x] = (int32_t)off;
+        tile_start[bh * (M + 1) + x] = (int32_t)ts;
       }
     }
     off += sz[u];
@@ -356,21 +375,7 @@ __device__ __forceinline__ void route_scatter_place_body(uint32_t *pre, uint32_t
     tile_start[bh * (M + 1) + M] = (int32_t)ttot;
   }
   __syncthreads();
-  const int tile = bx * 4 + (tid >> 6);
-  if (tile >= ntiles) return;  // no workgroup barriers below
-  const int lane = tid & 63;
-  const int n = tile * ROUTE_TQ + lane;
-  const bool valid = n < N;
-  const int e = valid ? expert[bh * N + n] : 0;
-  uint64_t same = __ballot(valid);
-  for (int b = 0; b < ebits; ++b) {
-    const bool bit = (e >> b) & 1;
-    const uint64_t ones = __ballot(bit);
-    same &= bit ? ones : ~ones;
-  }
-  const int leader = valid ? __ffsll((unsigned long long)same) - 1 : lane;
-  int base = 0;
-  if (valid && lane == leader) base = (int)pre[e] + atomicAdd(&cursor[bh * M + e], __popcll(same));
+  int base = (valid && lane == leader) ? (int)pre[e] + rel : 0;
   base = __shfl(base, leader);
   if (valid) perm[bh * N + base + (int)lanes_below(same)] = n;
 }
@@ -505,7 +510,9 @@ __global__ __launch_bounds__(1024) void worklist_kernel(const int32_t *__restric
 // queries 32 (w / 2) .. + 31 and the key half w % 2 of every 64-key tile, so
 // each wave reads half of each staged tile; the two waves of a query half
 // merge their partial softmax states through LDS at the end (log-sum-exp),
-// each finishing one of the two 16-query groups.
+// each finishing one of the two 16-query groups. Tiles are staged through
+// registers; this kernel serves fp32 inputs, and bf16 ones whose key row list
+// is too long for LDS (bf16 with the list in LDS goes to attend16_kernel).
 // With ROUTED, routed keys come from the expert tiles, or straight from the
 // K/V rows listed in idx (FUSED: the gather of Eq. gather done in place; with
 // IDX_LDS the expert's index list is staged in LDS first).
@@ -520,41 +527,21 @@ __global__ __launch_bounds__(1024) void worklist_kernel(const int32_t *__restric
 // C = ceil(tiles / 8); the grid's x extent is a multiple of 8.
 // ---------------------------------------------------------------------------
 constexpr int NXCD = 8;
-// bf16, d = 64 with the DMA staging: registers within four waves per SIMD
-#define ATTEND_OCCUPANCY __attribute__((amdgpu_waves_per_eu(sizeof(T) == 2 && D == 64 && IDX_LDS ? 4 : 1)))
 
-template <typename T, int D, bool SHARED, bool ROUTED, bool FUSED, bool IDX_LDS>
-__global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
-                                                       const T *__restrict__ v_lm, const T *__restrict__ rk,
-                                                       const T *__restrict__ rv, const int32_t *__restrict__ idx,
-                                                       const int32_t *__restrict__ perm,
-                                                       const int32_t *__restrict__ offsets,
-                                                       const int32_t *__restrict__ tile_start, T *__restrict__ o,
-                                                       int N, int M, int k, float scale) {
-  using TD = TileDims<T, D>;
-  // bf16 tiles listed in LDS go by LDS DMA (K and V row-major, swizzled);
-  // otherwise through registers (K row-major, V transposed, padded rows)
-  constexpr bool DMA = sizeof(T) == 2 && IDX_LDS;
-  constexpr int KBYTES = DMA ? DmaTile<D>::BYTES : TD::K_ELEMS * (int)sizeof(T);
-  constexpr int TBYTES = KBYTES + (DMA ? DmaTile<D>::BYTES : TD::V_ELEMS * (int)sizeof(T));
-  // two separate arrays, so that the compiler sees the DMA into one buffer
-  // and the reads of the other as disjoint (no wait for the DMA in between)
-  __shared__ __align__(16) char tiles0[TBYTES];
-  __shared__ __align__(16) char tiles1[TBYTES];
-  auto Ks = [&](int b) { return reinterpret_cast<T *>(b ? tiles1 : tiles0); };
-  auto Vt = [&](int b) { return reinterpret_cast<T *>((b ? tiles1 : tiles0) + KBYTES); };
-  extern __shared__ uint32_t sidx[];  // with IDX_LDS: byte offsets of the M + k key rows
-  const int64_t bh = blockIdx.y;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
-
-  int e = 0, q_begin, q_end;
+// The workgroup's queries [q_begin, q_end) (positions in perm) and their
+// expert e, from the work list; false for a workgroup past its end.
+template <bool ROUTED>
+__device__ __forceinline__ bool attend_queries(const int32_t *__restrict__ tile_start,
+                                               const int32_t *__restrict__ offsets, int64_t bh, int N, int M, int &e,
+                                               int &q_begin, int &q_end) {
+  e = 0;
   if (ROUTED) {
     const int32_t *ts = tile_start + bh * (M + 1);
     const int ntl = ts[M];
     const int C = (ntl + NXCD - 1) / NXCD;
     const int slot = (int)blockIdx.x / NXCD;
     const int t = ((int)blockIdx.x % NXCD) * C + slot;
-    if (slot >= C || t >= ntl) return;  // uniform for the workgroup
+    if (slot >= C || t >= ntl) return false;
     int lo = 0, hi = M - 1;  // largest e with ts[e] <= t
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
@@ -569,9 +556,34 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
     q_end = min(of[e + 1], q_begin + ATT_TQ);
   } else {
     q_begin = (int)blockIdx.x * ATT_TQ;
-    if (q_begin >= N) return;
+    if (q_begin >= N) return false;
     q_end = min(N, q_begin + ATT_TQ);
   }
+  return true;
+}
+
+template <typename T, int D, bool SHARED, bool ROUTED, bool FUSED, bool IDX_LDS>
+__global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
+                                                       const T *__restrict__ v_lm, const T *__restrict__ rk,
+                                                       const T *__restrict__ rv, const int32_t *__restrict__ idx,
+                                                       const int32_t *__restrict__ perm,
+                                                       const int32_t *__restrict__ offsets,
+                                                       const int32_t *__restrict__ tile_start, T *__restrict__ o,
+                                                       int N, int M, int k, float scale) {
+  using TD = TileDims<T, D>;
+  // tiles staged through registers (K row-major, V transposed, padded rows)
+  constexpr int KBYTES = TD::K_ELEMS * (int)sizeof(T);
+  constexpr int TBYTES = KBYTES + TD::V_ELEMS * (int)sizeof(T);
+  __shared__ __align__(16) char tiles0[TBYTES];
+  __shared__ __align__(16) char tiles1[TBYTES];
+  auto Ks = [&](int b) { return reinterpret_cast<T *>(b ? tiles1 : tiles0); };
+  auto Vt = [&](int b) { return reinterpret_cast<T *>((b ? tiles1 : tiles0) + KBYTES); };
+  extern __shared__ uint32_t sidx[];  // with IDX_LDS: byte offsets of the M + k key rows
+  const int64_t bh = blockIdx.y;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
+
+  int e = 0, q_begin, q_end;
+  if (!attend_queries<ROUTED>(tile_start, offsets, bh, N, M, e, q_begin, q_end)) return;  // uniform
 
   // full tiles: nA shared, then nB routed; partial ones: pA shared rows, pB routed rows
   const int nA = SHARED ? M / TK : 0, pA = SHARED ? M % TK : 0;
@@ -633,73 +645,10 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
     }
   }
   const float sl2 = scale * LOG2E;
-  if constexpr (!DMA) wait_loads();  // the query fragments are in registers before the pipelined loop
-  std::conditional_t<DMA, OnlineDma<D>, Online2<D>> st;
+  wait_loads();  // the query fragments are in registers before the pipelined loop
+  Online2<D> st;
   st.init();
 
-  if constexpr (DMA) {
-    // one tile ahead: the DMA of tile i + 1 into the other buffer is issued,
-    // tile i is multiplied, then the wave waits for its DMA and the workgroup
-    // meets at the barrier; unrolled by two so both buffers have fixed
-    // addresses
-    const T *kb, *vb;
-    int off;
-    if (nfull > 0) {
-      tile_base(0, kb, vb, off);
-      dma_tile<D, true>(Ks(0), Vt(0), kb, vb, rows + off, TK);
-    }
-    // the score MFMAs take q * scale * log2 e (rounded to bf16); the query
-    // loads were issued before the first tile's DMA, which stays in flight
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-      for (int ks = 0; ks < D / 32; ++ks) {
-        float x[8];
-        unpack16(qf[c][ks].v, x, (const bf16_t *)nullptr);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) x[j] *= sl2;
-        qf[c][ks].from_f32(x);
-      }
-    wait_loads();
-    __syncthreads();
-    // the tile loop, for a wave whose second 16-query group holds queries
-    // (NG = 2) or not (NG = 1: half the arithmetic); both versions stage the
-    // same tiles and meet the same barriers
-    auto run = [&](auto ng) {
-      constexpr int NG = decltype(ng)::value;
-      auto step = [&](int i, const T *Kc, const T *Vc, T *Kn, T *Vn) {
-        const bool more = i + 1 < nfull;
-        if (more) tile_base(i + 1, kb, vb, off);
-        dma_step<D, NG>(st, Kc, Vc, Kn, Vn, more, kb, vb, rows + off, wave_busy, kh, qf);
-        wait_loads();
-        __syncthreads();
-      };
-      int i = 0;
-      for (; i + 1 < nfull; i += 2) {
-        step(i, Ks(0), Vt(0), Ks(1), Vt(1));
-        step(i + 1, Ks(1), Vt(1), Ks(0), Vt(0));
-      }
-      if (i < nfull) step(i, Ks(0), Vt(0), Ks(1), Vt(1));
-      // partial tiles (masked)
-      for (int part = 0; part < 2; ++part) {
-        const int nr = part == 0 ? pA : pB;
-        if (nr == 0) continue;  // uniform
-        if (part == 0)
-          dma_tile<D>(Ks(0), Vt(0), sh_k, sh_v, rows + nA * TK, nr);
-        else
-          dma_tile<D>(Ks(0), Vt(0), rkb, rvb, rows + rbase + nB * TK, nr);
-        wait_loads();
-        __syncthreads();
-        const int nh = min(32, nr - 32 * kh);  // keys of this wave's half
-        if (wave_busy && nh > 0) half_tile_dma<D, true, NG>(st, Ks(0), Vt(0), kh, qf, nh);
-        __syncthreads();
-      }
-    };
-    if (q_begin + qh * 32 + 16 < q_end)
-      run(std::integral_constant<int, 2>{});
-    else
-      run(std::integral_constant<int, 1>{});
-  } else {
   TileRegs<T, D> Ra;
   if (IDX_LDS) {
     // one tile ahead: tile i + 1 is loaded into registers while tile i is
@@ -774,7 +723,6 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
     if (wave_busy && nh > 0) half_tile_attend<T, D, true>(st, Ks(0), Vt(0), kh, qf, nh, sl2);
     __syncthreads();
   }
-  }
 
   // merge the two key halves: wave (qh, kh) finishes query group kh and hands
   // group 1 - kh to its partner (qh, 1 - kh) through LDS (the tile buffers
@@ -839,6 +787,147 @@ __global__ __launch_bounds__(BLOCK) ATTEND_OCCUPANCY void attend_kernel(const T 
     finish(std::integral_constant<int, 1>{});
   else
     finish(std::integral_constant<int, 0>{});
+}
+
+// ---------------------------------------------------------------------------
+// Attention with one 16-query group per wave (bf16, key row list in LDS).
+// The workgroup takes the same 64 queries as attend_kernel, but each of its
+// four waves owns 16 of them and every key, so nothing is merged across
+// waves; the keys come in 32-row tiles (K and V: 8 KB at d = 64) by LDS DMA,
+// double buffered with one barrier per tile. The smaller LDS footprint and
+// register set let more workgroups share a CU than the 2 x 2 split of
+// attend_kernel, at twice the LDS reads per MFMA (each K/V fragment serves
+// one query group).
+// ---------------------------------------------------------------------------
+constexpr int TK32 = 32;
+// d = 64: registers for seven waves per SIMD (two values spill, outside the
+// tile loop); seven workgroups of 16 + 2.5 KB LDS fit a CU at M + k = 640
+#define ATTEND16_OCCUPANCY __attribute__((amdgpu_waves_per_eu(D == 64 ? 7 : 4)))
+
+template <int D, bool SHARED, bool ROUTED, bool FUSED>
+__global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
+    const bf16_t *__restrict__ q, const bf16_t *__restrict__ q_lm, const bf16_t *__restrict__ v_lm,
+    const bf16_t *__restrict__ rk, const bf16_t *__restrict__ rv, const int32_t *__restrict__ idx,
+    const int32_t *__restrict__ perm, const int32_t *__restrict__ offsets, const int32_t *__restrict__ tile_start,
+    bf16_t *__restrict__ o, int N, int M, int k, float scale) {
+  using DT = DmaTile<D, TK32>;
+  // two separate arrays (see attend_kernel): K then V of one tile each
+  __shared__ __align__(16) char tiles0[2 * DT::BYTES];
+  __shared__ __align__(16) char tiles1[2 * DT::BYTES];
+  auto Ks = [&](int b) { return reinterpret_cast<bf16_t *>(b ? tiles1 : tiles0); };
+  auto Vt = [&](int b) { return reinterpret_cast<bf16_t *>((b ? tiles1 : tiles0) + DT::BYTES); };
+  extern __shared__ uint32_t sidx[];  // byte offsets of the M + k key rows
+  const int64_t bh = blockIdx.y;
+  // the wave index as a scalar, so that the wave's busy flag and the softmax
+  // state's flags are scalar too (no exec-masked branches around the tile)
+  const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
+  int e, q_begin, q_end;
+  if (!attend_queries<ROUTED>(tile_start, offsets, bh, N, M, e, q_begin, q_end)) return;  // uniform
+
+  // full 32-row tiles: nA shared, then nB routed; partial ones: pA, pB rows
+  const int nA = SHARED ? M / TK32 : 0, pA = SHARED ? M % TK32 : 0;
+  const int nB = ROUTED ? k / TK32 : 0, pB = ROUTED ? k % TK32 : 0;
+  const int nfull = nA + nB;
+  const bf16_t *sh_k = q_lm + bh * (int64_t)M * D, *sh_v = v_lm + bh * (int64_t)M * D;
+  const bf16_t *rkb, *rvb;
+  const int32_t *gidx = nullptr;
+  if (FUSED) {
+    rkb = rk + bh * (int64_t)N * D;
+    rvb = rv + bh * (int64_t)N * D;
+    gidx = idx + (bh * M + e) * (int64_t)k;
+  } else {
+    rkb = rk + (bh * M + e) * (int64_t)k * D;
+    rvb = rv + (bh * M + e) * (int64_t)k * D;
+  }
+  constexpr uint32_t ROWB = D * sizeof(bf16_t);
+  const int nsh = SHARED ? M : 0;
+  for (int i = threadIdx.x; i < nsh; i += BLOCK) sidx[i] = (uint32_t)i * ROWB;
+  if (ROUTED)
+    for (int i = threadIdx.x; i < k; i += BLOCK) sidx[nsh + i] = (uint32_t)(FUSED ? gidx[i] : i) * ROWB;
+  __syncthreads();
+  const uint32_t *rows = sidx;
+  auto tile_base = [&](int i, const bf16_t *&kb, const bf16_t *&vb, int &off) {
+    const bool sh = i < nA;
+    kb = sh ? sh_k : rkb;
+    vb = sh ? sh_v : rvb;
+    off = sh ? i * TK32 : nsh + (i - nA) * TK32;
+  };
+
+  // this wave's 16 queries; a wave with none still stages tiles and meets
+  // the barriers but skips the arithmetic
+  const int qi = q_begin + 16 * w + p;
+  const bool qvalid = qi < q_end;
+  const int token = qvalid ? (ROUTED ? perm[bh * N + qi] : qi) : 0;
+  const bool busy = q_begin + 16 * w < q_end;
+  Frag<bf16_t> qf[2][D / 32];  // group 1 stays empty (one group per wave)
+#pragma unroll
+  for (int ks = 0; ks < D / 32; ++ks) {
+    if (qvalid)
+      qf[0][ks].load(q + (bh * N + token) * D + ks * 32 + g * 8);
+    else
+      qf[0][ks].zero();
+    qf[1][ks].zero();
+  }
+  OnlineDma<D> st;
+  st.init();
+  const bf16_t *kb, *vb;
+  int off;
+  if (nfull > 0) {
+    tile_base(0, kb, vb, off);
+    dma_tile<D, true, TK32>(Ks(0), Vt(0), kb, vb, rows + off, TK32);
+  }
+
+  // the score MFMAs take q * scale * log2 e (rounded to bf16)
+  const float sl2 = scale * LOG2E;
+#pragma unroll
+  for (int ks = 0; ks < D / 32; ++ks) {
+    float x[8];
+    unpack16(qf[0][ks].v, x, (const bf16_t *)nullptr);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] *= sl2;
+    qf[0][ks].from_f32(x);
+  }
+  wait_loads();
+  __syncthreads();
+  // step i: the DMA of tile i + 1 into the other buffer is issued, tile i is
+  // multiplied, then the wave waits for its DMA and the workgroup meets
+  auto step = [&](int i, const bf16_t *Kc, const bf16_t *Vc, bf16_t *Kn, bf16_t *Vn) {
+    const bool more = i + 1 < nfull;
+    if (more) tile_base(i + 1, kb, vb, off);
+    dma_step<D, 1, TK32>(st, Kc, Vc, Kn, Vn, more, kb, vb, rows + off, busy, 0, qf);
+    wait_loads();
+    __syncthreads();
+  };
+  int i = 0;
+  for (; i + 1 < nfull; i += 2) {  // unrolled by two: fixed buffer addresses
+    step(i, Ks(0), Vt(0), Ks(1), Vt(1));
+    step(i + 1, Ks(1), Vt(1), Ks(0), Vt(0));
+  }
+  if (i < nfull) step(i, Ks(0), Vt(0), Ks(1), Vt(1));
+  // partial tiles (masked)
+  for (int part = 0; part < 2; ++part) {
+    const int nr = part == 0 ? pA : pB;
+    if (nr == 0) continue;  // uniform
+    if (part == 0)
+      dma_tile<D, false, TK32>(Ks(0), Vt(0), sh_k, sh_v, rows + nA * TK32, nr);
+    else
+      dma_tile<D, false, TK32>(Ks(0), Vt(0), rkb, rvb, rows + nsh + nB * TK32, nr);
+    wait_loads();
+    __syncthreads();
+    if (busy) half_tile_dma<D, true, 1>(st, Ks(0), Vt(0), 0, qf, nr);
+    __syncthreads();
+  }
+  if (!qvalid) return;
+  const float inv = __builtin_amdgcn_rcpf(st.l(0));
+  bf16_t *orow = o + (bh * N + token) * D;
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db) {
+    bf16_t vals[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) vals[r] = from_f32<bf16_t>(st.o[0][db][r] * inv);
+    *reinterpret_cast<uint2 *>(orow + db * 16 + 4 * g) = *reinterpret_cast<const uint2 *>(vals);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -964,7 +1053,11 @@ static hipError_t attend_t3(const mita_cfg_t &c, const void *q, const void *q_lm
   const int nlist = (SH ? c.M : 0) + (RT ? c.k : 0);
   const bool in_lds = nlist <= IDX_LDS_MAX;
   const size_t lds = in_lds ? (size_t)nlist * sizeof(int32_t) : 0;
-  if (in_lds)
+  if (in_lds && sizeof(T) == 2)
+    hipLaunchKernelGGL((attend16_kernel<D, SH, RT, FU>), grid, dim3(BLOCK), lds, st, (const bf16_t *)q,
+                       (const bf16_t *)q_lm, (const bf16_t *)v_lm, (const bf16_t *)rk, (const bf16_t *)rv, idx, perm,
+                       offsets, tile_start, (bf16_t *)o, c.N, c.M, c.k, eff_scale(c));
+  else if (in_lds)
     hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU, true>), grid, dim3(BLOCK), lds, st, (const T *)q,
                        (const T *)q_lm, (const T *)v_lm, (const T *)rk, (const T *)rv, idx, perm, offsets, tile_start,
                        (T *)o, c.N, c.M, c.k, eff_scale(c));
