@@ -70,6 +70,16 @@ def stage_work(wl, staged: bool, fused: bool):
 # Kernel names (as rocprofv3 reports them) of the single-kernel stages.
 KERNEL_OF_STAGE = {"topk": "topk_kernel", "attend": "attend_kernel", "gather": "gather_kernel",
                    "landmarks": "pool_kernel"}
+IDX_LDS_MAX = 8192  # key row lists up to this length are staged in LDS by the attention
+
+
+def kernel_of(stage, wl):
+    """The kernel a single-kernel stage runs for this workload: bf16 attention
+    with its key row list in LDS uses the 16-query-per-wave kernel."""
+    if stage == "attend" and wl.dtype == "bf16":
+        if wl.M * wl.use_shared + wl.k * wl.use_routed <= IDX_LDS_MAX:
+            return "attend16_kernel"
+    return KERNEL_OF_STAGE.get(stage, stage)
 
 
 def cpu_baseline(wl, inp, budget_s: float):
@@ -209,13 +219,13 @@ def main():
     traffic = None
     try:
         tr = json.load(open(TRAFFIC_FILE))
-        ent = tr.get(f"{KERNEL_OF_STAGE.get(dom, dom)}@{name}")
+        ent = tr.get(f"{kernel_of(dom, wl)}@{name}")
         if ent and ent.get("source_digest") == source_digest():
             traffic = ent["bytes_per_launch"]
     except (OSError, ValueError):
         pass
     roofline = {"bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
-                "frac": round(ach / peak, 5), "traffic": traffic, "kernel": KERNEL_OF_STAGE.get(dom, dom),
+                "frac": round(ach / peak, 5), "traffic": traffic, "kernel": kernel_of(dom, wl),
                 "stage": dom, "launch_us": round(stage_ms[dom] * 1e3, 2),
                 "algorithmic_bytes": by, "algorithmic_flops": fl}
 
