@@ -920,7 +920,10 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
   }
   if (!qvalid) return;
   const float inv = __builtin_amdgcn_rcpf(st.l(0));
-  bf16_t *orow = o + (bh * N + token) * D;
+  // the token is read again (the barriers in between keep the compiler from
+  // reusing the first read), so no address stays live across the tile loop
+  const int tok = ROUTED ? perm[bh * N + qi] : qi;
+  bf16_t *orow = o + (bh * N + tok) * D;
 #pragma unroll
   for (int db = 0; db < D / 16; ++db) {
     bf16_t vals[4];
