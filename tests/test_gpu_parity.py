@@ -329,6 +329,10 @@ EDGE = [
     (16, 16, 4, 4, 40, 128, "f32", 0, 1),
     (32, 33, 8, 11, 100, 64, "bf16", 1, 1),   # M = 88 (two partial landmark blocks), ragged N = 1056
     (9, 8, 9, 8, 5, 64, "bf16", 1, 1),        # M = N
+    # key row lists longer than the attention stages in LDS (M + k > 8192):
+    # register-staged tiles, row indices read from memory
+    (96, 96, 4, 4, 8200, 64, "bf16", 1, 1),
+    (96, 96, 2, 2, 8190, 64, "f32", 1, 1),
 ]
 
 
@@ -342,7 +346,10 @@ def test_forward_edge_cases(case):
     cfg = mita.Config.from_workload(wl)
     q, k, v = (to_dev(x, dtype) for x in (inp.q, inp.k, inp.v))
     log(f"[edge] {case}")
-    _end_to_end(cfg, inp, q, k, v, [(0, 0), (1, 1)], row_limit=10 ** 9, exact_sets=(dtype == "f32"))
+    # the long-list cases check a sample of output rows (the oracle's attention
+    # over 8k keys for every token would take minutes)
+    big = gh * gw * (lh * lw * sh + kk * rt) > 10 ** 7
+    _end_to_end(cfg, inp, q, k, v, [(0, 0), (1, 1)], row_limit=256 if big else 10 ** 9, exact_sets=(dtype == "f32"))
 
 
 # ------------------------------------------------------------------ fused top-k selection
