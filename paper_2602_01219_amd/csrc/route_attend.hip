@@ -307,15 +307,18 @@ __device__ __forceinline__ void route_scatter_body(int bx, int by, const int32_t
   }
 }
 
+constexpr int SCATTER_TPW = 4;  // 64-query tiles per wave of the forward's scatter
+
 // Grouping without a stable order inside an expert (the forward's own
 // routing: the attention gives each query the same result whatever its
 // position in the grouping, so any order within an expert gives the same
 // output). Workgroup (bx, by) of the scatter grid: the head's expert sizes
 // become offsets (a block scan every workgroup of the head does for itself,
 // into LDS; workgroup 0 of the head also writes offsets and the attention
-// work list tile_start); each wave then takes, per expert among its 64
-// queries, one block of positions with one atomic add on that expert's
-// cursor (zeroed by the pooling) and places its queries there in lane order.
+// work list tile_start); each wave takes, per 64-query tile and expert among
+// the tile's queries, one block of positions with one atomic add on that
+// expert's cursor (zeroed by the pooling) and places the queries there in
+// lane order. A workgroup covers 4 * SCATTER_TPW tiles.
 // pre: M + 1 words of LDS, wsum: 4 words.
 __device__ __forceinline__ void route_scatter_place_body(uint32_t *pre, uint32_t *wsum, int bx, int by,
                                                          const int32_t *__restrict__ expert,
@@ -327,28 +330,38 @@ __device__ __forceinline__ void route_scatter_place_body(uint32_t *pre, uint32_t
   constexpr int EPT = (1024 + 255) / 256;  // experts per thread (M <= 1024)
   const int64_t bh = by;
   const int tid = threadIdx.x, lane = tid & 63;
-  // the wave's queries and their experts first: the block of positions is
-  // taken (one atomic add per expert among the 64) while the sizes are
-  // scanned, so the two latencies overlap
-  const int tile = bx * 4 + (tid >> 6);
-  const int n = tile * ROUTE_TQ + lane;
-  const bool valid = tile < ntiles && n < N;
-  const int e = valid ? expert[bh * N + n] : 0;
+  // the wave's queries (SCATTER_TPW tiles of 64) and their experts first:
+  // the blocks of positions are taken (one atomic add per expert among a
+  // tile's 64) while the sizes are scanned, so the two latencies overlap
+  int ej[SCATTER_TPW], rel[SCATTER_TPW], leader[SCATTER_TPW], nj[SCATTER_TPW];
+  bool vj[SCATTER_TPW];
+  uint64_t same[SCATTER_TPW];
+#pragma unroll
+  for (int j = 0; j < SCATTER_TPW; ++j) {
+    const int tile = (bx * SCATTER_TPW + j) * 4 + (tid >> 6);
+    nj[j] = tile * ROUTE_TQ + lane;
+    vj[j] = tile < ntiles && nj[j] < N;
+    ej[j] = vj[j] ? expert[bh * N + nj[j]] : 0;
+  }
   uint32_t sz[EPT], a = 0, t = 0;
 #pragma unroll
   for (int u = 0; u < EPT; ++u) {
     const int x = tid * EPT + u;
     sz[u] = x < M ? (uint32_t)counts[bh * M + x] : 0u;
   }
-  uint64_t same = __ballot(valid);
-  for (int b = 0; b < ebits; ++b) {
-    const bool bit = (e >> b) & 1;
-    const uint64_t ones = __ballot(bit);
-    same &= bit ? ones : ~ones;
+#pragma unroll
+  for (int j = 0; j < SCATTER_TPW; ++j) {
+    uint64_t sm = __ballot(vj[j]);
+    for (int b = 0; b < ebits; ++b) {
+      const bool bit = (ej[j] >> b) & 1;
+      const uint64_t ones = __ballot(bit);
+      sm &= bit ? ones : ~ones;
+    }
+    same[j] = sm;
+    leader[j] = vj[j] ? __ffsll((unsigned long long)sm) - 1 : lane;
+    rel[j] = 0;
+    if (vj[j] && lane == leader[j]) rel[j] = atomicAdd(&cursor[bh * M + ej[j]], __popcll(sm));
   }
-  const int leader = valid ? __ffsll((unsigned long long)same) - 1 : lane;
-  int rel = 0;
-  if (valid && lane == leader) rel = atomicAdd(&cursor[bh * M + e], __popcll(same));
 #pragma unroll
   for (int u = 0; u < EPT; ++u) {
     a += sz[u];
@@ -375,9 +388,12 @@ __device__ __forceinline__ void route_scatter_place_body(uint32_t *pre, uint32_t
     tile_start[bh * (M + 1) + M] = (int32_t)ttot;
   }
   __syncthreads();
-  int base = (valid && lane == leader) ? (int)pre[e] + rel : 0;
-  base = __shfl(base, leader);
-  if (valid) perm[bh * N + base + (int)lanes_below(same)] = n;
+#pragma unroll
+  for (int j = 0; j < SCATTER_TPW; ++j) {
+    int base = (vj[j] && lane == leader[j]) ? (int)pre[ej[j]] + rel[j] : 0;
+    base = __shfl(base, leader[j]);
+    if (vj[j]) perm[bh * N + base + (int)lanes_below(same[j])] = nj[j];
+  }
 }
 
 __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t *__restrict__ expert,
@@ -456,7 +472,7 @@ __global__ __launch_bounds__(256) void topk_scatter_kernel(const T *__restrict__
                                                            int32_t *__restrict__ cursor, int32_t *__restrict__ perm,
                                                            int32_t *__restrict__ offsets,
                                                            int32_t *__restrict__ tile_start, int N, int M, int ntiles,
-                                                           int ebits, int route_x) {
+                                                           int ebits, int scat_x) {
   __shared__ __align__(16) char buf[TopkScatterLds<T, D, CAP, VEC>::BYTES];
   const int b = (int)blockIdx.x;
   if (b < nT) {
@@ -479,7 +495,7 @@ __global__ __launch_bounds__(256) void topk_scatter_kernel(const T *__restrict__
   const int rb = b - nT;
   uint32_t *pre = reinterpret_cast<uint32_t *>(buf);
   __shared__ uint32_t wsum[4];
-  route_scatter_place_body(pre, wsum, rb % route_x, rb / route_x, expert, counts, cursor, perm, offsets, tile_start,
+  route_scatter_place_body(pre, wsum, rb % scat_x, rb / scat_x, expert, counts, cursor, perm, offsets, tile_start,
                            N, M, ntiles, ebits);
 }
 
@@ -989,17 +1005,19 @@ static hipError_t select_route_t(const mita_cfg_t &c, const void *q, const void 
   // the fallback workgroups of the last launch (listed rows, scored in full and selected)
   const int nT = (int)(rows < 512 ? rows : 512);
   int32_t *cursor = tile_base;  // the placement cursors live in the (here unused) tile_base buffer
+  const int scat_x = (nt + 4 * SCATTER_TPW - 1) / (4 * SCATTER_TPW);
+  const int nS = scat_x * bh;
   int ebits = 0;
   while ((1 << ebits) < c.M) ++ebits;
   constexpr int TCAP = 512;
   if (c.N % 4 == 0)
-    hipLaunchKernelGGL((topk_scatter_kernel<T, D, TCAP, true>), dim3((unsigned)(nT + nR)), dim3(256), 0, st,
+    hipLaunchKernelGGL((topk_scatter_kernel<T, D, TCAP, true>), dim3((unsigned)(nT + nS)), dim3(256), 0, st,
                        (const T *)q_lm, (const T *)k, S, eff_scale(c), nch, idx, c.k, sb.fail_cnt, sb.fail_list, nT,
-                       expert, counts, cursor, perm, offsets, tile_start, c.N, c.M, nt, ebits, route_x);
+                       expert, counts, cursor, perm, offsets, tile_start, c.N, c.M, nt, ebits, scat_x);
   else
-    hipLaunchKernelGGL((topk_scatter_kernel<T, D, TCAP, false>), dim3((unsigned)(nT + nR)), dim3(256), 0, st,
+    hipLaunchKernelGGL((topk_scatter_kernel<T, D, TCAP, false>), dim3((unsigned)(nT + nS)), dim3(256), 0, st,
                        (const T *)q_lm, (const T *)k, S, eff_scale(c), nch, idx, c.k, sb.fail_cnt, sb.fail_list, nT,
-                       expert, counts, cursor, perm, offsets, tile_start, c.N, c.M, nt, ebits, route_x);
+                       expert, counts, cursor, perm, offsets, tile_start, c.N, c.M, nt, ebits, scat_x);
   return hipGetLastError();
 }
 
