@@ -326,7 +326,8 @@ __device__ __forceinline__ void dma_tile(bf16_t *Kl, bf16_t *Vl, const bf16_t *k
   }
 }
 
-// Softmax state of a wave with 32 queries for the DMA path: as Online2, the
+// Softmax state of a wave with up to two 16-query groups for the DMA path
+// (the attention uses one group per wave): as Online2, the
 // reference max m kept also as the negated splat nm that initialises the
 // score accumulators, so the MFMA yields dot * scale * log2 e - m directly
 // (the query fragments are pre-scaled by scale * log2 e).
@@ -350,8 +351,9 @@ template <int D> struct OnlineDma {
   __device__ __forceinline__ float l(int c) const { return lsum[c][0]; }
 };
 
-// One wave's step over the 32-key half h of a DMA-staged tile for its 32
-// queries (pre-scaled fragments qf[c]). The reference max starts at the first
+// One wave's step over the 32 keys at rows 32h .. 32h + 31 of a DMA-staged
+// tile for its query groups (pre-scaled fragments qf[c]; the attention's
+// tiles are 32 rows, h = 0, one group). The reference max starts at the first
 // tile's column max; later it moves only when a column's shifted scores
 // exceed RESCALE_LOG2 (then the tile's values, accumulators and sums shift
 // with it). With MASKED only keys 32h + i, i < nvalid (>= 1), count. NG = 1
@@ -448,8 +450,8 @@ __device__ __forceinline__ void half_tile_dma(OnlineDma<D> &st, const bf16_t *Kl
 }
 
 // One step of the DMA-staged tile loop: the DMA of the next tile into (Kn,
-// Vn) is issued (if `more`), then the wave's half of the current tile (Kc, Vc)
-// is multiplied (if `busy`). The buffers come in as restrict pointers, so the
+// Vn) is issued (if `more`), then the wave's 32 keys of the current tile (Kc,
+// Vc) are multiplied (if `busy`). The buffers come in as restrict pointers, so the
 // compiler's alias information shows the reads of the current tile to be
 // disjoint from the DMA in flight and no wait for it is placed before them.
 template <int D, int NG, int ROWS = TK>
