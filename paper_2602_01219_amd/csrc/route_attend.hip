@@ -1003,7 +1003,9 @@ static hipError_t select_route_t(const mita_cfg_t &c, const void *q, const void 
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   // the fallback workgroups of the last launch (listed rows, scored in full and selected)
-  const int nT = (int)(rows < 512 ? rows : 512);
+  // (few: the rows normally all pass and these workgroups exit at once; each
+  // takes rows b, b + nT, ... when some do not)
+  const int nT = (int)(rows < 64 ? rows : 64);
   int32_t *cursor = tile_base;  // the placement cursors live in the (here unused) tile_base buffer
   const int scat_x = (nt + 4 * SCATTER_TPW - 1) / (4 * SCATTER_TPW);
   const int nS = scat_x * bh;
