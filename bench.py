@@ -1,24 +1,31 @@
 #!/usr/bin/env python3
 """Benchmark of the MiTA forward on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--dense]
+    python bench.py --sweep            # the paper's operating points, MiTA and dense
 
 One step = one whole forward (landmarks, scores + landmark values, top-k,
 [gather], routing, attention) over one batch of synthetic inputs that are
-resident in HBM before the timed region starts. Prints ONE JSON line on
-stdout: tokens/s (a token is one sequence position across all heads) over the
-timed region of plain forwards; the roofline of the dominant kernel, its
-launch time measured live with HIP events on the launch stream in a second
-pass of as many forwards with stage events; and the CPU oracle timed on a
-bounded sample of the same workload. Per-stage details go to stderr.
+resident in HBM before the timed region starts. Prints ONE JSON line on stdout
+(one per run with --sweep): tokens/s (a token is one sequence position across
+all heads) over the timed region of plain forwards; per-kernel times from a
+second pass of as many forwards with one HIP event behind each launch (on the
+launch stream), each kernel priced against its algorithmic bytes and flops;
+the roofline of the dominant kernel; and the CPU oracle timed on a bounded
+sample of the same workload. Details go to stderr.
+
+--dense runs the dense reference on the same inputs instead: route-only with
+one landmark and k = N, so every query attends over every key (full softmax
+attention) on the same kernels; PyTorch's flash SDPA is timed beside it as
+context.
 """
 from __future__ import annotations
 
 import argparse
 import hashlib
 import json
-import math
 import os
+import platform
 import sys
 import time
 
@@ -30,6 +37,11 @@ PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 CSRC = os.path.join(ROOT, "paper_2602_01219_amd", "csrc")
+SCORE_NC = 512        # keys per score-pass chunk
+ROUTE_TQ = 64         # queries per routing tile
+# kernels priced against MFMA whatever their byte count (the attention: its
+# algorithmic bytes count every expert's k rows, most of which come from L2)
+MFMA_KERNELS = ("attend16_kernel", "attend_kernel")
 
 
 def eprint(*a):
@@ -45,134 +57,177 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def stage_work(wl, staged: bool, fused: bool):
-    """Algorithmic work per stage launch: (bound, bytes, flops).
-
-    bytes: what the stage must read and write at least (inputs once, outputs
-    once); flops: its multiply-adds x 2 on the MFMA path. With the fused
-    selection the score matrix is neither written nor read back."""
+def kernel_work(name: str, wl, plan: dict, staged: bool):
+    """Algorithmic (bytes, flops) of one launch of kernel `name`: the tensors
+    its step must read and write at least (inputs once, outputs once) and its
+    multiply-adds x 2. Intermediate buffers of this design (score-pass
+    partials, candidate lists) are not counted."""
     e = 4 if wl.dtype == "f32" else 2
     BH, N, d, M, k = wl.BH, wl.N, wl.d, wl.M, wl.k
     sh, rt = wl.use_shared, wl.use_routed
-    lm = ("hbm", BH * N * d * e + BH * M * d * e, 0)
-    s_bytes = 4 * BH * M * N if (rt and not fused) else 0
-    sc_bytes = BH * N * d * e * (1 + sh) + s_bytes + BH * M * d * e * (1 + sh)
-    sc = ("hbm", sc_bytes, 2 * M * N * d * BH * (1 + sh))
-    tk = ("hbm", s_bytes + 4 * BH * M * k, 0) if rt else ("hbm", 0, 0)
-    ga = ("hbm", BH * M * k * (4 + 4 * d * e), 0) if (rt and staged) else ("hbm", 0, 0)
-    ro = ("mfma", BH * N * d * e + BH * M * d * e + 4 * 3 * BH * N, 2 * N * M * d * BH) if rt else ("hbm", 0, 0)
-    keys = M * sh + k * rt
-    at = ("mfma", 2 * BH * N * d * e + 2 * BH * M * k * d * e * rt + 2 * BH * M * d * e * sh,
-          4 * N * keys * d * BH)
-    return dict(landmarks=lm, scores=sc, topk=tk, gather=ga, route=ro, attend=at)
+    rows = BH * M
+    tens = BH * N * d * e            # one of q, k, v, o
+    lmt = BH * M * d * e             # q_lm or v_lm
+    nch = -(-N // SCORE_NC)
+    ntiles = -(-N // ROUTE_TQ)
+    ns = plan.get("ns") or 0
+    stored_s = rt and not plan.get("fused")
+    w = {
+        "pool_kernel": (tens + lmt, 0),
+        "sample_pivot_kernel": (BH * ns * d * e + lmt + 4 * rows, 2 * M * ns * d * BH),
+        "scores_kernel": (tens * (1 + sh) + lmt + 4 * BH * M * N * stored_s, 2 * M * N * d * BH * (1 + sh)),
+        "merge_kernel": (BH * nch * M * (d + 2) * 4 + lmt, 0),
+        "finalize_kernel": (4 * rows * k + lmt * sh, 0),
+        "finalize_logits_kernel": (4 * rows * k + lmt * sh + tens + lmt + 4 * BH * N, 2 * N * M * d * BH),
+        "topk_scatter_kernel": (8 * BH * N + 8 * BH * (M + 1), 0),
+        "scores_rows_kernel": (0, 0),
+        "topk_kernel": (4 * BH * M * N + 4 * rows * k, 0),
+        "gather_kernel": (rows * k * (4 + 4 * d * e), 0),
+        "route_logits_kernel": (tens + lmt + 4 * BH * N, 2 * N * M * d * BH),
+        "route_scan_kernel": (8 * BH * ntiles * M, 0),
+        "route_scatter_kernel": (8 * BH * N + 4 * BH * ntiles * M, 0),
+        "worklist_kernel": (8 * BH * (M + 1), 0),
+        "zero_kernel": (4 * BH * M, 0),
+    }
+    att = (2 * tens + 2 * BH * M * k * d * e * rt + 2 * lmt * sh, 4 * N * (M * sh + k * rt) * d * BH)
+    w["attend16_kernel"] = att
+    w["attend_kernel"] = att
+    return w.get(name, (0, 0))
 
 
-# Kernel names (as rocprofv3 reports them) of the single-kernel stages.
-KERNEL_OF_STAGE = {"topk": "topk_kernel", "attend": "attend_kernel", "gather": "gather_kernel",
-                   "landmarks": "pool_kernel"}
-IDX_LDS_MAX = 8192  # key row lists up to this length are staged in LDS by the attention
+def price(name, us, by, fl, dtype):
+    """Roofline of one kernel: achieved rates and fractions of both peaks;
+    `bound` is the roof whose ideal time is longer (MFMA for the attention)."""
+    t = us * 1e-6
+    peak_f = PEAK_TFLOPS[dtype]
+    t_hbm = by / (PEAK_HBM_GBS * 1e9)
+    t_mfma = fl / (peak_f * 1e12)
+    bound = "mfma" if (name in MFMA_KERNELS or t_mfma > t_hbm) else "hbm"
+    gbs = by / t / 1e9 if t > 0 else 0.0
+    tfs = fl / t / 1e12 if t > 0 else 0.0
+    return {"kernel": name, "us": round(us, 2), "bound": bound, "algorithmic_bytes": by, "algorithmic_flops": fl,
+            "gb_s": round(gbs, 1), "tflop_s": round(tfs, 2),
+            "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "frac_mfma": round(tfs / peak_f, 4),
+            "frac": round((tfs / peak_f) if bound == "mfma" else (gbs / PEAK_HBM_GBS), 4)}
 
 
-def kernel_of(stage, wl):
-    """The kernel a single-kernel stage runs for this workload: bf16 attention
-    with its key row list in LDS uses the 16-query-per-wave kernel."""
-    if stage == "attend" and wl.dtype == "bf16":
-        if wl.M * wl.use_shared + wl.k * wl.use_routed <= IDX_LDS_MAX:
-            return "attend16_kernel"
-    return KERNEL_OF_STAGE.get(stage, stage)
+def cpu_info():
+    model = platform.processor() or "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    blas, threads = "unknown", 1
+    try:
+        from threadpoolctl import threadpool_info
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')}"
+            threads = max(i.get("num_threads", 1) for i in info)
+    except Exception:
+        pass
+    return model, blas, threads
 
 
 def cpu_baseline(wl, inp, budget_s: float):
     """Time the CPU oracle (as it stands) on whole (b, h) slices until about
-    budget_s seconds are spent; scale to tokens/s of the full workload."""
+    budget_s seconds are spent, once with float32 inputs (the oracle then
+    computes in float32) and once in float64 (its parity precision) on half
+    the budget; scale to tokens/s of the full workload."""
     import numpy as np
     from oracle import mita_oracle as O
     from paper_2602_01219_amd import synth
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = 1
-    done, spent = 0, 0.0
+    model, blas, threads = cpu_info()
     order = [(b, h) for b in range(wl.B) for h in range(wl.H)]
-    while done < len(order) and (spent < budget_s or done == 0):
-        b, h = order[done]
-        if wl.dtype == "f32":
-            q, k, v = (x[b, h].astype(np.float64) for x in (inp.q, inp.k, inp.v))
-        else:
-            q, k, v = (synth.bf16_bits_to_f32(x[b, h]).astype(np.float64) for x in (inp.q, inp.k, inp.v))
-        t0 = time.perf_counter()
-        O.forward_slice(q, k, v, wl.grid_h, wl.grid_w, wl.lm_h, wl.lm_w, wl.k, None, wl.use_shared, wl.use_routed)
-        spent += time.perf_counter() - t0
-        done += 1
-    per_slice = spent / done
-    full_s = per_slice * wl.BH
-    return {"value": wl.tokens / full_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} of {wl.BH} (b,h) slices of the same workload, float64 numpy oracle, "
-                      f"{spent:.1f} s; scaled by {wl.BH}/{done} slices"}
+
+    def run(dtype, budget):
+        done, spent = 0, 0.0
+        while done < len(order) and (spent < budget or done == 0):
+            b, h = order[done]
+            if wl.dtype == "f32":
+                q, k, v = (x[b, h].astype(dtype) for x in (inp.q, inp.k, inp.v))
+            else:
+                q, k, v = (synth.bf16_bits_to_f32(x[b, h]).astype(dtype) for x in (inp.q, inp.k, inp.v))
+            t0 = time.perf_counter()
+            O.forward_slice(q, k, v, wl.grid_h, wl.grid_w, wl.lm_h, wl.lm_w, wl.k, None, wl.use_shared,
+                            wl.use_routed)
+            spent += time.perf_counter() - t0
+            done += 1
+        return wl.tokens / (spent / done * wl.BH), done, spent
+
+    v32, n32, s32 = run(np.float32, budget_s)
+    v64, n64, s64 = run(np.float64, budget_s / 2)
+    return {"value": v32, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n32} of {wl.BH} (b,h) slices of the same workload, numpy oracle on float32 inputs, "
+                      f"{s32:.1f} s; scaled by {wl.BH}/{n32} slices",
+            "value_f64": v64, "sample_f64": f"{n64} slices in float64 (the parity precision), {s64:.1f} s",
+            "cpu_model": model, "blas": blas, "affinity_cpus": len(os.sched_getaffinity(0))}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default=None)
-    ap.add_argument("--staged-gather", action="store_true", help="materialise expert tiles (flag path)")
-    ap.add_argument("--full-scores", action="store_true",
-                    help="store the score matrix and select from it (flag path) instead of the fused selection")
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle time for cpu_baseline")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--calib-copy-mib", type=int, default=0,
-                    help="after the timed region, run one device copy of this many MiB (counter calibration)")
-    a = ap.parse_args()
+def sdpa_ms(q, k, v, steps, warmup):
+    """PyTorch's flash SDPA on the same tensors (context only): the flash
+    backend is forced, so no other kernel is timed; None if it is unavailable."""
+    import torch
+    try:
+        from torch.nn.attention import SDPBackend, sdpa_kernel
+        with sdpa_kernel(SDPBackend.FLASH_ATTENTION):
+            for _ in range(warmup):
+                torch.nn.functional.scaled_dot_product_attention(q, k, v)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                torch.nn.functional.scaled_dot_product_attention(q, k, v)
+            torch.cuda.synchronize()
+            return (time.perf_counter() - t0) * 1e3 / steps
+    except RuntimeError as ex:
+        eprint(f"[bench] flash SDPA unavailable: {str(ex).splitlines()[0][:120]}")
+        return None
 
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if a.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build measures one GPU only: run with --gpus 1",
-                          "n_gpus": a.gpus}), flush=True)
-        sys.exit(2)
 
+def run(wl, name, a, dense: bool):
+    import numpy as np
     import torch
     from paper_2602_01219_amd import mita, synth
 
-    name = a.workload or synth.HEADLINE
-    wl = synth.WORKLOADS[name]
-    eprint(f"[bench] workload {name}: B={wl.B} H={wl.H} N={wl.N} d={wl.d} M={wl.M} k={wl.k} {wl.dtype}")
     inp = synth.generate(wl)
-    torch.cuda.set_device(0)
+    if dense:
+        wl = synth.dense_reference(wl)
+    eprint(f"[bench] workload {name}{' (dense reference)' if dense else ''}: B={wl.B} H={wl.H} N={wl.N} d={wl.d} "
+           f"M={wl.M} k={wl.k} shared={wl.use_shared} routed={wl.use_routed} {wl.dtype}")
     dt = torch.float32 if wl.dtype == "f32" else torch.bfloat16
 
     def dev(x):
-        import numpy as np
         if wl.dtype == "f32":
             return torch.from_numpy(x).cuda()
         return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda()
 
     q, k, v = dev(inp.q), dev(inp.k), dev(inp.v)
     cfg = mita.Config.from_workload(wl, staged_gather=a.staged_gather, full_scores=a.full_scores)
-    fused = (not a.full_scores) and bool(wl.use_routed) and (wl.N <= 1024 or 4 * wl.k <= 4096)
+    plan = mita.select_plan(cfg)
     o = torch.empty_like(q)
     ws = torch.empty(mita.workspace_size(cfg), dtype=torch.uint8, device="cuda")
-    eprint(f"[bench] workspace {ws.numel() / 2**20:.1f} MiB")
+    eprint(f"[bench] workspace {ws.numel() / 2**20:.1f} MiB; selection {plan}")
     for _ in range(a.warmup):
         mita.forward(cfg, q, k, v, o=o, ws=ws)
     torch.cuda.synchronize()
 
     # timed region: plain forwards, as a caller runs them
-    torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(a.steps):
         mita.forward(cfg, q, k, v, o=o, ws=ws)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    # per-stage times: the same number of forwards right after, with HIP events
-    # recorded on the launch stream between the stages (the events add a few
+    fallbacks = mita.forward_fallbacks(cfg, ws)
+    # per-kernel times: the same number of forwards right after, with one HIP
+    # event behind each launch on the launch stream (the events add a few
     # microseconds per forward, so they stay out of the timed region above)
     timer = mita.Timer(a.steps)
     for _ in range(a.steps):
         mita.forward(cfg, q, k, v, o=o, ws=ws, timer=timer)
-    per_call = timer.read()
+    per_call = timer.launches()
     timer.close()
     # cold caches (secondary figure): before each forward, reading 512 MiB
     # evicts the inputs from L2 and the 256 MiB MALL; each forward is timed
@@ -189,6 +244,9 @@ def main():
     torch.cuda.synchronize()
     cold_ms = sorted(e0.elapsed_time(e1) for e0, e1 in pairs)[len(pairs) // 2]
     del flush
+    sdpa = None
+    if dense:
+        sdpa = sdpa_ms(q, k, v, a.steps, a.warmup)
     if a.calib_copy_mib:
         src = torch.empty(a.calib_copy_mib * 2**20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
@@ -197,59 +255,119 @@ def main():
 
     ms_per_step = wall * 1e3 / a.steps
     value = wl.tokens * a.steps / wall
-    stage_ms = {s: sum(c[i] for c in per_call) / len(per_call) for i, s in enumerate(mita.STAGES)}
-    work = stage_work(wl, a.staged_gather, fused)
-    eprint(f"[bench] {ms_per_step:.3f} ms/step, {value / 1e6:.2f} M tokens/s; "
-           f"cold caches {cold_ms:.3f} ms/forward ({wl.tokens / cold_ms / 1e3:.2f} M tokens/s)")
-    for s in mita.STAGES:
-        bound, by, fl = work[s]
-        t = stage_ms[s] * 1e-3
-        extra = ""
-        if t > 0 and (by or fl):
-            extra = f"  {by / t / 1e9:8.1f} GB/s  {fl / t / 1e12:8.2f} TFLOP/s"
-        eprint(f"[bench]   {s:10s} {stage_ms[s] * 1e3:9.1f} us{extra}")
+    # per kernel: average time per forward (launches of one kernel in a forward summed)
+    per_kernel, launches, stage_us = {}, {}, [0.0] * mita.NUM_STAGES
+    for call in per_call:
+        seen = {}
+        for kname, stage, ms in call:
+            seen[kname] = seen.get(kname, 0.0) + ms * 1e3
+            launches[kname] = launches.get(kname, 0) + 1
+            stage_us[stage] += ms * 1e3
+        for kname, us in seen.items():
+            per_kernel[kname] = per_kernel.get(kname, 0.0) + us
+    ncalls = max(1, len(per_call))
+    kernels = []
+    for kname, us in sorted(per_kernel.items(), key=lambda x: -x[1]):
+        us /= ncalls
+        by, fl = kernel_work(kname, wl, plan, a.staged_gather)
+        ent = price(kname, us, by, fl, wl.dtype)
+        ent["launches_per_forward"] = round(launches[kname] / ncalls, 2)
+        kernels.append(ent)
+    stage_us = [u / ncalls for u in stage_us]
+    eprint(f"[bench] {ms_per_step:.4f} ms/step, {value / 1e6:.2f} M tokens/s; "
+           f"cold caches {cold_ms:.4f} ms/forward ({wl.tokens / cold_ms / 1e3:.2f} M tokens/s); "
+           f"fallback rows {fallbacks}")
+    for ent in kernels:
+        eprint(f"[bench]   {ent['kernel']:24s} {ent['us']:9.2f} us  {ent['gb_s']:8.1f} GB/s ({ent['frac_hbm']:.3f})"
+               f"  {ent['tflop_s']:8.2f} TFLOP/s ({ent['frac_mfma']:.3f})  bound {ent['bound']}")
+    for s, u in zip(mita.STAGES, stage_us):
+        eprint(f"[bench]   stage {s:10s} {u:9.2f} us" + ("" if u > 0 else "  (launches nothing)"))
 
-    dom = max(stage_ms, key=stage_ms.get)
-    bound, by, fl = work[dom]
-    t = stage_ms[dom] * 1e-3
-    if bound == "mfma":
-        ach, peak, unit = fl / t / 1e12, PEAK_TFLOPS[wl.dtype], "TFLOP/s"
-    else:
-        ach, peak, unit = by / t / 1e9, PEAK_HBM_GBS, "GB/s"
+    dom = kernels[0]
     traffic = None
     try:
         tr = json.load(open(TRAFFIC_FILE))
-        ent = tr.get(f"{kernel_of(dom, wl)}@{name}")
+        ent = tr.get(f"{dom['kernel']}@{name}{'@dense' if dense else ''}")
         if ent and ent.get("source_digest") == source_digest():
             traffic = ent["bytes_per_launch"]
     except (OSError, ValueError):
         pass
-    roofline = {"bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
-                "frac": round(ach / peak, 5), "traffic": traffic, "kernel": kernel_of(dom, wl),
-                "stage": dom, "launch_us": round(stage_ms[dom] * 1e3, 2),
-                "algorithmic_bytes": by, "algorithmic_flops": fl}
+    bound = dom["bound"]
+    roofline = {"bound": bound,
+                "achieved": dom["tflop_s"] if bound == "mfma" else dom["gb_s"],
+                "peak": PEAK_TFLOPS[wl.dtype] if bound == "mfma" else PEAK_HBM_GBS,
+                "unit": "TFLOP/s" if bound == "mfma" else "GB/s",
+                "frac": dom["frac"], "traffic": traffic, "kernel": dom["kernel"], "launch_us": dom["us"],
+                "algorithmic_bytes": dom["algorithmic_bytes"], "algorithmic_flops": dom["algorithmic_flops"]}
 
     cpu = None
-    if not a.no_cpu_baseline:
+    if not a.no_cpu_baseline and not dense:
         eprint("[bench] timing the CPU oracle on a sample ...")
         cpu = cpu_baseline(wl, inp, a.cpu_budget)
-        eprint(f"[bench] cpu oracle {cpu['value']:.1f} tokens/s ({cpu['sample']})")
+        eprint(f"[bench] cpu oracle {cpu['value']:.1f} tokens/s fp32, {cpu['value_f64']:.1f} fp64 "
+               f"({cpu['cores']} threads, {cpu['cpu_model']}, {cpu['blas']})")
 
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": a.steps,
         "warmup": a.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
-        "config": {"workload": name, "B": wl.B, "H": wl.H, "N": wl.N, "d": wl.d, "M": wl.M, "k": wl.k,
-                   "grid": [wl.grid_h, wl.grid_w], "use_shared": wl.use_shared, "use_routed": wl.use_routed,
+        "config": {"workload": name + (" dense reference" if dense else ""), "B": wl.B, "H": wl.H, "N": wl.N,
+                   "d": wl.d, "M": wl.M, "k": wl.k, "grid": [wl.grid_h, wl.grid_w],
+                   "use_shared": wl.use_shared, "use_routed": wl.use_routed,
                    "gather": "staged" if a.staged_gather else "in-place",
-                   "select": "fused" if fused else "full-scores", "parallelism": "none (1 GPU)"},
+                   "select": "fused" if plan["fused"] else "full-scores", "parallelism": "none (1 GPU)"},
         "roofline": roofline,
         "cpu_baseline": cpu,
-        "stages_us": {s: round(stage_ms[s] * 1e3, 2) for s in mita.STAGES},
+        "kernels": kernels,
+        "stages_us": {s: round(u, 2) for s, u in zip(mita.STAGES, stage_us)},
+        "fallback_rows": fallbacks,
         "cold": {"ms_per_forward": round(cold_ms, 4), "tokens_per_s": round(wl.tokens / cold_ms * 1e3, 1),
                  "note": "median single forward after reading 512 MiB (L2 and MALL evicted)"},
     }
-    print(json.dumps(out), flush=True)
+    if dense:
+        out["sdpa_flash_ms"] = None if sdpa is None else round(sdpa, 4)
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--dense", action="store_true",
+                    help="dense reference on the same inputs: route-only, one landmark, k = N")
+    ap.add_argument("--sweep", action="store_true",
+                    help="the paper's operating points, MiTA then the dense reference, one JSON line each")
+    ap.add_argument("--staged-gather", action="store_true", help="materialise expert tiles (flag path)")
+    ap.add_argument("--full-scores", action="store_true",
+                    help="store the score matrix and select from it (flag path) instead of the fused selection")
+    ap.add_argument("--cpu-budget", type=float, default=12.0,
+                    help="seconds of float32 oracle time for cpu_baseline (half as much again in float64)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after the timed region, run one device copy of this many MiB (counter calibration)")
+    a = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if a.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build measures one GPU only: run with --gpus 1",
+                          "n_gpus": a.gpus}), flush=True)
+        sys.exit(2)
+
+    import torch
+    from paper_2602_01219_amd import synth
+    torch.cuda.set_device(0)
+
+    if a.sweep:
+        a.no_cpu_baseline = True  # the oracle baseline belongs to the headline line
+        for name in synth.OPERATING_ORDER:
+            for dense in (False, True):
+                out = run(synth.WORKLOADS[name], name, a, dense)
+                print(json.dumps(out), flush=True)
+        return
+    name = a.workload or synth.HEADLINE
+    print(json.dumps(run(synth.WORKLOADS[name], name, a, a.dense)), flush=True)
 
 
 if __name__ == "__main__":

@@ -120,7 +120,10 @@ const char *mita_last_error(void);
  * only the scores above it, and the exact selection runs on that list. A row
  * whose list turns out too short or too long is recomputed in full and
  * selected exactly (see mita_forward_fallbacks). Without MITA_FLAG_FULL_SCORES
- * this applies when N <= 1024 or k <= 1024.
+ * this applies when mita_select_plan reports it: always for N <= 1024, else
+ * when a pivot rank and a list cap (at most 8192) exist for which each way a
+ * row's list can miss has probability <= 1e-9 per row on inputs whose scores
+ * are exchangeable over token positions (k up to about N / 8).
  */
 int mita_forward(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, void *o,
                  void *ws, size_t ws_bytes, mita_stream_t stream);
@@ -133,6 +136,15 @@ int mita_forward(const mita_cfg_t *cfg, const void *q, const void *k, const void
  */
 int mita_forward_fallbacks(const mita_cfg_t *cfg, const void *ws, size_t ws_bytes, int64_t *count,
                            mita_stream_t stream);
+
+/*
+ * Diagnostic, host only: how mita_forward selects the top-k sets for cfg.
+ * *fused = 1 if the selection runs inside the score pass (then *ns keys of
+ * each landmark row are sampled, the pivot is the *rank-th largest sampled
+ * score and the exact selection takes lists of up to *cap candidates), 0 if
+ * the whole score matrix is stored and selected from. Any output may be NULL.
+ */
+int mita_select_plan(const mita_cfg_t *cfg, int32_t *fused, int32_t *ns, int32_t *rank, int32_t *cap);
 
 /*
  * Landmark queries (Sec. 3.2: average pooling over uniformly spaced windows;
@@ -199,19 +211,31 @@ int mita_attend(const mita_cfg_t *cfg, const void *q, const void *q_lm, const vo
                 void *o, void *ws, size_t ws_bytes, mita_stream_t stream);
 
 /*
- * Per-stage timing of mita_forward with HIP events (profiling aid).
- * A timer holds event slots for up to max_calls forward calls; each
- * mita_forward_timed call records MITA_NUM_STAGES + 1 events on the stream
- * around the stages (landmarks, scores, top-k, gather, routing, attention; a
- * stage that does not run records an empty interval).
+ * Per-launch timing of mita_forward with HIP events (profiling aid).
+ * A timer holds event slots for up to max_calls forward calls. Each
+ * mita_forward_timed call records one event on the stream before its first
+ * kernel and one behind each kernel it launches (at most MITA_MAX_LAUNCHES),
+ * so the interval of a launch is that kernel's time on the stream. Every
+ * launch belongs to one of MITA_NUM_STAGES stages (0 landmarks, 1 scores,
+ * 2 top-k, 3 gather, 4 routing, 5 attention); a kernel that does the work of
+ * two stages (the forward's selection finish runs inside the routing
+ * launches) counts under the later one, and a stage that launches nothing
+ * takes no time.
  */
 #define MITA_NUM_STAGES 6
+#define MITA_MAX_LAUNCHES 16
 typedef struct mita_timer mita_timer_t;
 int mita_timer_create(mita_timer_t **timer, int max_calls);
 int mita_timer_destroy(mita_timer_t *timer);
 int mita_timer_reset(mita_timer_t *timer);
-/* Waits for the recorded events; fills ms[call * MITA_NUM_STAGES + stage]; *n_calls = calls recorded. */
+/* Waits for the recorded events; fills ms[call * MITA_NUM_STAGES + stage] with
+ * the summed launch times of each stage; *n_calls = calls recorded. */
 int mita_timer_read(mita_timer_t *timer, float *ms, int ms_len, int *n_calls);
+/* Waits for the recorded events; for recorded call `call`, fills the first
+ * *n_launches entries of kernels (static kernel names, owned by the library),
+ * stages and ms (each array holds at least cap entries). */
+int mita_timer_launches(mita_timer_t *timer, int call, int cap, const char **kernels, int32_t *stages, float *ms,
+                        int32_t *n_launches);
 int mita_forward_timed(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, void *o,
                        void *ws, size_t ws_bytes, mita_stream_t stream, mita_timer_t *timer);
 

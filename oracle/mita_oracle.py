@@ -6,7 +6,8 @@ leg use it. It shares no code with the HIP library (no kernels, headers,
 tables or helpers) and it never imports the package.
 
 Plain, slow and written to be checked by eye against the paper. Arithmetic is
-numpy float64 on the exact input values (bf16/fp32 inputs widened exactly).
+numpy float64 on the exact input values (bf16/fp32 inputs widened exactly);
+given float32 arrays it computes in float32 instead (the CPU timing baseline).
 Everything is per (batch, head) slice; nothing is shared across slices.
 
 Notation follows Sec. 3.2 with tokens as rows: q, k, v are [N, d] (the paper's
@@ -67,7 +68,7 @@ def landmarks(q: np.ndarray, grid_h: int, grid_w: int, lm_h: int, lm_w: int) -> 
     grid = q.reshape(grid_h, grid_w, d)
     rows = pool_windows(grid_h, lm_h)
     cols = pool_windows(grid_w, lm_w)
-    out = np.empty((lm_h * lm_w, d), dtype=np.float64)
+    out = np.empty((lm_h * lm_w, d), dtype=q.dtype)
     for a, (r0, r1) in enumerate(rows):
         for b, (c0, c1) in enumerate(cols):
             out[a * lm_w + b] = grid[r0:r1, c0:c1, :].reshape(-1, d).mean(axis=0)
@@ -153,7 +154,7 @@ def output_per_query(q, q_lm, v_lm, kx, vx, expert, scale, use_shared=1, use_rou
     """o_n = V* softmax(K*^T q_n * scale) with K* = [q_lm ; kx[e(n)]] and
     V* = [v_lm ; vx[e(n)]] (either part dropped by its flag)."""
     N, d = q.shape
-    o = np.empty((N, d), dtype=np.float64)
+    o = np.empty((N, d), dtype=q.dtype)
     for n in range(N):
         keys, vals = [], []
         if use_shared:
@@ -253,7 +254,7 @@ def forward_slice(q, k, v, grid_h, grid_w, lm_h, lm_w, topk, scale=None,
     (o is then [len(rows), d])."""
     N, d = q.shape
     if scale is None:
-        scale = 1.0 / np.sqrt(d)
+        scale = float(1.0 / np.sqrt(d))
     q_lm = landmarks(q, grid_h, grid_w, lm_h, lm_w)
     S = scores(q_lm, k, scale)
     idx = topk_indices(S, topk) if force_idx is None else np.asarray(force_idx, dtype=np.int64)

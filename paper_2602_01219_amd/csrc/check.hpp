@@ -18,7 +18,21 @@ constexpr int ROUTE_TQ = 64;   // queries per routing tile (one wave)
 constexpr int SCORE_NC = 512;  // keys per score/landmark-value workgroup chunk
 // Top-k selection fused with the score pass of the forward.
 constexpr int SEL_NS = 1024;   // sampled keys per landmark row (pivot estimate)
-constexpr int SEL_CAP = 4096;  // most candidates the exact selection of one row takes
+constexpr int SEL_CAP = 8192;  // most candidates the exact selection of one row takes
+// Per-row probability allowed for each of the two ways a row's candidate list
+// can miss (too short to hold the top-k, too long for the cap), under the
+// model below; such a row is still selected exactly, only slower.
+constexpr double SEL_EPS = 1e-9;
+
+// LDS one workgroup can hold on gfx950 (the whole 160 KB of a CU).
+constexpr size_t LDS_BYTES = 160 * 1024;
+// Longest key row list (shared plus routed rows, 4 bytes each) the attention
+// stages in LDS; longer ones are read from memory.
+constexpr int IDX_LDS_MAX = 8192;
+// Does a row list of nlist entries fit in LDS beside a kernel's static LDS?
+inline bool list_in_lds(int nlist, size_t static_bytes) {
+  return nlist <= IDX_LDS_MAX && static_bytes + (size_t)nlist * 4 <= LDS_BYTES;
+}
 
 inline size_t align_up(size_t x) { return (x + WS_ALIGN - 1) / WS_ALIGN * WS_ALIGN; }
 inline size_t elem_bytes(const mita_cfg_t &c) { return c.dtype == MITA_F32 ? 4 : 2; }
@@ -27,38 +41,135 @@ inline int score_chunks(const mita_cfg_t &c) { return (c.N + SCORE_NC - 1) / SCO
 inline int route_tiles(const mita_cfg_t &c) { return (c.N + ROUTE_TQ - 1) / ROUTE_TQ; }
 inline float eff_scale(const mita_cfg_t &c) { return c.scale != 0.f ? c.scale : 1.0f / std::sqrt((float)c.d); }
 
-inline int sel_ns(const mita_cfg_t &c) { return c.N < SEL_NS ? c.N : SEL_NS; }
-// Does the forward select the top-k sets inside the score pass? Rows whose
-// sample covers the whole row always fit their list; otherwise the expected
-// list length, at most k + 5 sqrt(64 k) + 128 for N / ns <= 64, must stay
-// inside SEL_CAP, which k <= SEL_CAP / 4 ensures.
+// ---------------------------------------------------------------------------
+// Plan of the fused selection. A row's pivot is the r-th largest of the
+// scores at ns evenly spaced keys; the score pass lists every token scoring
+// >= pivot and the exact selection runs on that list when it holds between k
+// and cap entries. Model: the row's scores are exchangeable over positions, so
+// the sampled positions are a uniform random ns-subset of the N tokens and,
+// for any fixed set of K tokens (the row's K first in the top-k order), the
+// number of samples among them is hypergeometric, X ~ H(N, K, ns).
+//  - The list is shorter than k only if at least r samples lie among the
+//    row's first k - 1 tokens: P = P(X >= r), K = k - 1. r is the smallest
+//    rank with P <= SEL_EPS.
+//  - The list is longer than cap only if fewer than r samples lie among the
+//    row's first cap tokens: P = P(X < r), K = cap. cap is the smallest power
+//    of two in [1024, SEL_CAP] (or N) with P <= SEL_EPS.
+// Both bounds are for the exact r-th sample; the pivot is the lower edge of
+// the 2^-7-relative bin holding it, which adds the few tokens inside that bin
+// to the list (inside the cap's margin). When the sample is the whole row
+// (N <= SEL_NS) the rank is k and the list cannot miss. A configuration with
+// no rank or cap meeting the bounds is not selected in the score pass.
+// ---------------------------------------------------------------------------
+inline double log_choose(double n, double x) { return std::lgamma(n + 1.0) - std::lgamma(x + 1.0) - std::lgamma(n - x + 1.0); }
+
+// log P(X = x), X ~ H(N, K, n)
+inline double hyper_log_pmf(int64_t N, int64_t K, int64_t n, int64_t x) {
+  return log_choose((double)K, (double)x) + log_choose((double)(N - K), (double)(n - x)) - log_choose((double)N, (double)n);
+}
+
+// Tails of X ~ H(N, K, n), each summed from its inner end on the side of the
+// mode where the terms shrink (so the first term cannot underflow while the
+// rest matter); the other side is the complement.
+//   upward:   P(x + 1) / P(x) = (K - x)(n - x) / ((x + 1)(N - K - n + x + 1))
+//   downward: P(x - 1) / P(x) = x (N - K - n + x) / ((K - x + 1)(n - x + 1))
+inline int64_t hyper_mode(int64_t N, int64_t K, int64_t n) { return (int64_t)(((double)(n + 1) * (K + 1)) / (N + 2)); }
+
+// sum of P(x) for x >= r, r above the mode
+inline double hyper_sum_up(int64_t N, int64_t K, int64_t n, int64_t r, int64_t hi) {
+  double t = std::exp(hyper_log_pmf(N, K, n, r)), s = 0.0;
+  for (int64_t x = r; x <= hi; ++x) {
+    s += t;
+    t *= (double)(K - x) * (double)(n - x) / ((double)(x + 1) * (double)(N - K - n + x + 1));
+    if (t <= s * 1e-18) break;
+  }
+  return s;
+}
+// sum of P(x) for x <= r, r below the mode
+inline double hyper_sum_down(int64_t N, int64_t K, int64_t n, int64_t r, int64_t lo) {
+  double t = std::exp(hyper_log_pmf(N, K, n, r)), s = 0.0;
+  for (int64_t x = r; x >= lo; --x) {
+    s += t;
+    t *= (double)x * (double)(N - K - n + x) / ((double)(K - x + 1) * (double)(n - x + 1));
+    if (t <= s * 1e-18) break;
+  }
+  return s;
+}
+
+// P(X >= r)
+inline double hyper_sf(int64_t N, int64_t K, int64_t n, int64_t r) {
+  const int64_t lo = n - (N - K) > 0 ? n - (N - K) : 0, hi = K < n ? K : n;
+  if (r <= lo) return 1.0;
+  if (r > hi) return 0.0;
+  const double p = r > hyper_mode(N, K, n) ? hyper_sum_up(N, K, n, r, hi) : 1.0 - hyper_sum_down(N, K, n, r - 1, lo);
+  return p < 0.0 ? 0.0 : (p > 1.0 ? 1.0 : p);
+}
+
+// P(X < r)
+inline double hyper_cdf_below(int64_t N, int64_t K, int64_t n, int64_t r) {
+  const int64_t lo = n - (N - K) > 0 ? n - (N - K) : 0, hi = K < n ? K : n;
+  if (r <= lo) return 0.0;
+  if (r > hi) return 1.0;
+  const double p = r - 1 < hyper_mode(N, K, n) ? hyper_sum_down(N, K, n, r - 1, lo) : 1.0 - hyper_sum_up(N, K, n, r, hi);
+  return p < 0.0 ? 0.0 : (p > 1.0 ? 1.0 : p);
+}
+
+struct SelPlan {
+  bool ok;   // the score pass can select this (N, k)
+  int ns;    // sampled keys per row
+  int rank;  // pivot rank among the samples
+  int cap;   // longest list the exact selection takes
+};
+
+inline SelPlan make_sel_plan(int N, int k) {
+  SelPlan p{false, N < SEL_NS ? N : SEL_NS, 0, 0};
+  if (N <= SEL_NS) {  // the sample is the row: exact pivot, list never misses
+    p.ok = true;
+    p.rank = k;
+    p.cap = N;
+    return p;
+  }
+  const int64_t ns = p.ns;
+  // smallest rank with P(at least r samples among the first k - 1 tokens) <= eps;
+  // below the mean of that count the probability is about 1/2 or more
+  int64_t r = (int64_t)std::floor((double)(k - 1) * ns / N) + 1;
+  while (r <= ns && hyper_sf(N, k - 1, ns, r) > SEL_EPS) ++r;
+  if (r > ns) return p;
+  p.rank = (int)r;
+  for (int64_t cap = 1024; cap <= SEL_CAP; cap *= 2) {
+    if (cap >= N) {
+      p.cap = N;
+      p.ok = true;
+      return p;
+    }
+    if (hyper_cdf_below(N, cap, ns, r) <= SEL_EPS) {
+      p.cap = (int)cap;
+      p.ok = true;
+      return p;
+    }
+  }
+  return p;
+}
+
+// The plan of cfg's (N, k), remembered per thread for the last (N, k) seen.
+inline SelPlan sel_plan(const mita_cfg_t &c) {
+  thread_local int last_n = -1, last_k = -1;
+  thread_local SelPlan last{};
+  if (c.N != last_n || c.k != last_k) {
+    last = make_sel_plan(c.N, c.k);
+    last_n = c.N;
+    last_k = c.k;
+  }
+  return last;
+}
+
+// Does the forward select the top-k sets inside the score pass?
 inline bool fused_select(const mita_cfg_t &c) {
-  return c.use_routed && !(c.flags & MITA_FLAG_FULL_SCORES) && (c.N <= SEL_NS || 4 * (int64_t)c.k <= SEL_CAP);
+  return c.use_routed && !(c.flags & MITA_FLAG_FULL_SCORES) && sel_plan(c).ok;
 }
-// Rank r of the pivot among the ns sampled scores of a row: the pivot is the
-// r-th largest sample score. With the sample equal to the row, r = k exactly;
-// otherwise r is the expected rank of the k-th token, k ns / N, plus five
-// binomial standard deviations (and one), so that at least k tokens of the
-// row score >= pivot except with negligible probability.
-inline int sel_rank(const mita_cfg_t &c) {
-  const int ns = sel_ns(c);
-  if (ns == c.N) return c.k;
-  const double f = (double)c.k * ns / c.N;
-  const double sd = std::sqrt(f * (1.0 - (double)c.k / c.N));
-  const int r = (int)std::ceil(f + 5.0 * sd) + 1;
-  return r < ns ? r : ns;
-}
-// Candidates one row may list before it falls back: a power of two in
-// [1024, SEL_CAP] above the count expected at the pivot rank plus six
-// standard deviations (the whole row when it is shorter).
-inline int sel_cap(const mita_cfg_t &c) {
-  const int ns = sel_ns(c);
-  const double r = sel_rank(c);
-  const double bound = ns == c.N ? c.N : (r + 6.0 * std::sqrt(r)) * ((double)c.N / ns);
-  int cap = 1024;
-  while (cap < SEL_CAP && cap < bound) cap *= 2;
-  return c.N < cap ? c.N : cap;
-}
+inline int sel_ns(const mita_cfg_t &c) { return sel_plan(c).ns; }
+inline int sel_rank(const mita_cfg_t &c) { return sel_plan(c).rank; }
+inline int sel_cap(const mita_cfg_t &c) { return sel_plan(c).cap; }
 
 // Validate a configuration. On failure, writes a message into err.
 inline int check_cfg(const mita_cfg_t *c, std::string *err) {

@@ -8,6 +8,12 @@
 
 namespace mita {
 
+// Per-launch timing of mita_forward_timed: every launcher calls
+// launched(kernel, st) right after enqueueing a kernel. It records an event on
+// st behind the launch when a timed forward is being enqueued on this thread
+// (nothing otherwise) and returns hipGetLastError().
+hipError_t launched(const char *kernel, hipStream_t st);
+
 // Landmark pooling (Sec. 3.2; Algorithm 1 AdaptiveAvgPool): q [BH,N,d] -> q_lm [BH,M,d].
 // If zero_counts (zero_cursor) is not NULL its BH*M entries are set to 0
 // (routing totals; the forward's placement cursors).

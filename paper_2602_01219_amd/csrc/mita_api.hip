@@ -57,11 +57,45 @@ size_t tensor_bytes(const mita_cfg_t *c) { return (size_t)BH(*c) * c->N * c->d *
 
 }  // namespace
 
+// Event slots of a timed forward: one event before its first launch and one
+// behind each launch, with the launch's kernel name and stage.
 struct mita_timer {
   int max_calls = 0;
   int used = 0;
-  std::vector<hipEvent_t> ev;  // max_calls * (MITA_NUM_STAGES + 1)
+  std::vector<hipEvent_t> ev;       // max_calls * (MITA_MAX_LAUNCHES + 1)
+  std::vector<const char *> name;   // max_calls * MITA_MAX_LAUNCHES
+  std::vector<int32_t> stage;       // max_calls * MITA_MAX_LAUNCHES
+  std::vector<int32_t> nlaunch;     // max_calls
 };
+
+namespace {
+
+// The timed forward being enqueued on this thread, if any.
+struct Recording {
+  mita_timer *t;
+  int call;
+  int stage;
+  hipError_t err;
+};
+thread_local Recording *g_rec = nullptr;
+
+}  // namespace
+
+hipError_t mita::launched(const char *kernel, hipStream_t st) {
+  const hipError_t e = hipGetLastError();
+  Recording *r = g_rec;
+  if (!r || e != hipSuccess) return e;
+  mita_timer *t = r->t;
+  int &n = t->nlaunch[r->call];
+  if (n >= MITA_MAX_LAUNCHES) return e;  // cannot happen: a forward launches fewer kernels
+  const size_t slot = (size_t)r->call * MITA_MAX_LAUNCHES + n;
+  t->name[slot] = kernel;
+  t->stage[slot] = r->stage;
+  const hipError_t er = hipEventRecord(t->ev[(size_t)r->call * (MITA_MAX_LAUNCHES + 1) + n + 1], st);
+  if (er != hipSuccess && r->err == hipSuccess) r->err = er;
+  ++n;
+  return e;
+}
 
 namespace {
 
@@ -76,15 +110,23 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
   if (overlaps(o, tb, q, tb) || overlaps(o, tb, k, tb) || overlaps(o, tb, v, tb))
     return set_err(MITA_ERR_INVALID_ARG, "o overlaps an input");
   TRY(need_ws(c, MITA_WS_FORWARD, ws, ws_bytes));
-  hipEvent_t *ev = nullptr;
+  Recording rec{timer, 0, 0, hipSuccess};
   if (timer) {
     if (timer->used >= timer->max_calls) return set_err(MITA_ERR_INVALID_ARG, "timer is full");
-    ev = &timer->ev[(size_t)timer->used * (MITA_NUM_STAGES + 1)];
-    timer->used++;
+    rec.call = timer->used++;
+    timer->nlaunch[rec.call] = 0;
+    TRY(hip_status(hipEventRecord(timer->ev[(size_t)rec.call * (MITA_MAX_LAUNCHES + 1)], st), "hipEventRecord"));
   }
-  auto mark = [&](int i) -> int {
-    if (!ev) return MITA_OK;
-    return hip_status(hipEventRecord(ev[i], st), "hipEventRecord");
+  // launches are attributed to the stage set last (a launch that does the
+  // work of two stages counts under the later one)
+  struct Scope {
+    Recording *prev;
+    explicit Scope(Recording *r) : prev(g_rec) { g_rec = r->t ? r : nullptr; }
+    ~Scope() { g_rec = prev; }
+  } scope(&rec);
+  auto mark = [&](int stage) -> int {
+    rec.stage = stage;
+    return MITA_OK;
   };
 
   const FwdLayout L = forward_layout(*c);
@@ -142,7 +184,7 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
   TRY(hip_status(launch_attend(*c, q, q_lm, v_lm, staged ? kx : k, staged ? vx : v, staged ? nullptr : idx, perm,
                                offsets, tile_start, o, st),
                  "attend"));
-  TRY(mark(6));
+  if (rec.err != hipSuccess) return hip_status(rec.err, "hipEventRecord");
   return MITA_OK;
 }
 
@@ -194,6 +236,18 @@ int mita_forward_fallbacks(const mita_cfg_t *cfg, const void *ws, size_t ws_byte
   TRY(hip_status(hipMemcpy(&n, (const char *)ws + forward_layout(*cfg).fail, sizeof n, hipMemcpyDeviceToHost),
                  "hipMemcpy"));
   *count = n;
+  return MITA_OK;
+}
+
+int mita_select_plan(const mita_cfg_t *cfg, int32_t *fused, int32_t *ns, int32_t *rank, int32_t *cap) {
+  g_err.clear();
+  TRY(validate(cfg));
+  const bool f = fused_select(*cfg);
+  const SelPlan p = sel_plan(*cfg);
+  if (fused) *fused = f ? 1 : 0;
+  if (ns) *ns = f ? p.ns : 0;
+  if (rank) *rank = f ? p.rank : 0;
+  if (cap) *cap = f ? p.cap : 0;
   return MITA_OK;
 }
 
@@ -296,7 +350,10 @@ int mita_timer_create(mita_timer_t **timer, int max_calls) {
   if (!timer || max_calls < 1) return set_err(MITA_ERR_INVALID_ARG, "bad timer arguments");
   mita_timer *t = new mita_timer();
   t->max_calls = max_calls;
-  t->ev.resize((size_t)max_calls * (MITA_NUM_STAGES + 1));
+  t->ev.resize((size_t)max_calls * (MITA_MAX_LAUNCHES + 1));
+  t->name.assign((size_t)max_calls * MITA_MAX_LAUNCHES, nullptr);
+  t->stage.assign((size_t)max_calls * MITA_MAX_LAUNCHES, 0);
+  t->nlaunch.assign((size_t)max_calls, 0);
   for (size_t i = 0; i < t->ev.size(); ++i) {
     hipError_t e = hipEventCreate(&t->ev[i]);
     if (e != hipSuccess) {
@@ -322,19 +379,50 @@ int mita_timer_reset(mita_timer_t *timer) {
   return MITA_OK;
 }
 
+namespace {
+// Waits for the last event of the last recorded call.
+int timer_wait(mita_timer *t) {
+  if (t->used == 0) return MITA_OK;
+  const int c = t->used - 1;
+  return hip_status(hipEventSynchronize(t->ev[(size_t)c * (MITA_MAX_LAUNCHES + 1) + t->nlaunch[c]]),
+                    "hipEventSynchronize");
+}
+}  // namespace
+
 int mita_timer_read(mita_timer_t *timer, float *ms, int ms_len, int *n_calls) {
   g_err.clear();
   if (!timer || !ms || !n_calls) return set_err(MITA_ERR_INVALID_ARG, "NULL argument");
   if (ms_len < timer->used * MITA_NUM_STAGES) return set_err(MITA_ERR_INVALID_ARG, "ms buffer too small");
   *n_calls = timer->used;
-  if (timer->used == 0) return MITA_OK;
-  TRY(hip_status(hipEventSynchronize(timer->ev[(size_t)timer->used * (MITA_NUM_STAGES + 1) - 1]),
-                 "hipEventSynchronize"));
+  TRY(timer_wait(timer));
   for (int c = 0; c < timer->used; ++c) {
-    hipEvent_t *ev = &timer->ev[(size_t)c * (MITA_NUM_STAGES + 1)];
-    for (int s = 0; s < MITA_NUM_STAGES; ++s)
-      TRY(hip_status(hipEventElapsedTime(&ms[c * MITA_NUM_STAGES + s], ev[s], ev[s + 1]), "hipEventElapsedTime"));
+    for (int s = 0; s < MITA_NUM_STAGES; ++s) ms[c * MITA_NUM_STAGES + s] = 0.f;
+    const hipEvent_t *ev = &timer->ev[(size_t)c * (MITA_MAX_LAUNCHES + 1)];
+    for (int i = 0; i < timer->nlaunch[c]; ++i) {
+      float t = 0.f;
+      TRY(hip_status(hipEventElapsedTime(&t, ev[i], ev[i + 1]), "hipEventElapsedTime"));
+      ms[c * MITA_NUM_STAGES + timer->stage[(size_t)c * MITA_MAX_LAUNCHES + i]] += t;
+    }
   }
+  return MITA_OK;
+}
+
+int mita_timer_launches(mita_timer_t *timer, int call, int cap, const char **kernels, int32_t *stages, float *ms,
+                        int32_t *n_launches) {
+  g_err.clear();
+  if (!timer || !kernels || !stages || !ms || !n_launches) return set_err(MITA_ERR_INVALID_ARG, "NULL argument");
+  if (call < 0 || call >= timer->used) return set_err(MITA_ERR_INVALID_ARG, "no such recorded call");
+  const int n = timer->nlaunch[call];
+  if (cap < n) return set_err(MITA_ERR_INVALID_ARG, "output arrays too small");
+  TRY(timer_wait(timer));
+  const hipEvent_t *ev = &timer->ev[(size_t)call * (MITA_MAX_LAUNCHES + 1)];
+  for (int i = 0; i < n; ++i) {
+    const size_t slot = (size_t)call * MITA_MAX_LAUNCHES + i;
+    kernels[i] = timer->name[slot];
+    stages[i] = timer->stage[slot];
+    TRY(hip_status(hipEventElapsedTime(&ms[i], ev[i], ev[i + 1]), "hipEventElapsedTime"));
+  }
+  *n_launches = n;
   return MITA_OK;
 }
 

@@ -80,7 +80,7 @@ __global__ __launch_bounds__(256) void pool_kernel(const T *__restrict__ q, T *_
 }
 
 // The bf16 d=64 pass holds 3 waves per SIMD (at most 168 VGPRs).
-#define SCORES_OCCUPANCY __attribute__((amdgpu_waves_per_eu(sizeof(T) == 2 && D == 64 ? 3 : 1)))
+#define SCORES_OCCUPANCY __attribute__((amdgpu_waves_per_eu(sizeof(T) == 2 && D == 64 ? 3 : (sizeof(T) == 2 ? 2 : 1))))
 
 template <typename T, int D, bool WRITE_S, bool DO_V, bool SELECT>
 __global__ __launch_bounds__(BLOCK) SCORES_OCCUPANCY void scores_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
@@ -146,7 +146,7 @@ static hipError_t pool_t(const mita_cfg_t &c, const void *q, void *q_lm, int32_t
   dim3 grid(c.M, (unsigned)BH(c));
   hipLaunchKernelGGL((pool_kernel<T, D>), grid, dim3(256), 0, st, (const T *)q, (T *)q_lm, zc, zcur, c.N, c.grid_h,
                      c.grid_w, c.lm_h, c.lm_w);
-  return hipGetLastError();
+  return launched("pool_kernel", st);
 }
 
 hipError_t launch_pool(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *zc, int32_t *zcur, hipStream_t st) {
@@ -163,7 +163,7 @@ __global__ __launch_bounds__(256) void zero_kernel(int32_t *__restrict__ p, int6
 hipError_t launch_zero(int32_t *p, int64_t n, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(zero_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p, n);
-  return hipGetLastError();
+  return launched("zero_kernel", st);
 }
 
 template <typename T, int D>
@@ -193,11 +193,11 @@ static hipError_t scores_t(const mita_cfg_t &c, const void *q_lm, const void *k,
     return hipSuccess;
   }
 #undef MITA_SCORES
-  hipError_t e = hipGetLastError();
+  hipError_t e = launched("scores_kernel", st);
   if (e != hipSuccess || !v_lm || sb) return e;  // with sel the merge runs in the selection's finish
   hipLaunchKernelGGL((merge_kernel<T, D>), dim3((unsigned)c.M, (unsigned)BH(c)), dim3(256), 0, st, ml, po, (T *)v_lm,
                      c.M, nch);
-  return hipGetLastError();
+  return launched("merge_kernel", st);
 }
 
 hipError_t launch_scores(const mita_cfg_t &c, const void *q_lm, const void *k, const void *v, float *S, void *v_lm,
@@ -219,7 +219,7 @@ static hipError_t scores_rows_t(const mita_cfg_t &c, const void *q_lm, const voi
   const unsigned grid = (unsigned)(most < 1024 ? most : 1024);
   hipLaunchKernelGGL((scores_rows_kernel<T, D>), dim3(grid), dim3(BLOCK), 0, st, (const T *)q_lm, (const T *)k, S,
                      nrows, rows, c.N, c.M, eff_scale(c), nch);
-  return hipGetLastError();
+  return launched("scores_rows_kernel", st);
 }
 
 hipError_t launch_scores_rows(const mita_cfg_t &c, const void *q_lm, const void *k, float *S, const uint32_t *nrows,
@@ -239,7 +239,7 @@ static hipError_t gather_t(const mita_cfg_t &c, const void *k, const void *v, co
   const int64_t blocks = (rows * CPR + 255) / 256;
   hipLaunchKernelGGL((gather_kernel<T, D>), dim3((unsigned)blocks), dim3(256), 0, st, (const T *)k, (const T *)v, idx,
                      (T *)kx, (T *)vx, rows, c.N, c.M * c.k);
-  return hipGetLastError();
+  return launched("gather_kernel", st);
 }
 
 hipError_t launch_gather(const mita_cfg_t &c, const void *k, const void *v, const int32_t *idx, void *kx, void *vx,

@@ -544,6 +544,13 @@ __global__ __launch_bounds__(1024) void worklist_kernel(const int32_t *__restric
 // ---------------------------------------------------------------------------
 constexpr int NXCD = 8;
 
+// Static LDS of the attention kernels (their double-buffered tiles); the key
+// row list comes on top as dynamic LDS when it is staged there.
+template <typename T, int D> constexpr size_t attend_tiles_lds() {
+  return 2 * (size_t)(TileDims<T, D>::K_ELEMS + TileDims<T, D>::V_ELEMS) * sizeof(T);
+}
+template <int D> constexpr size_t attend16_tiles_lds() { return 4 * (size_t)DmaTile<D, 32>::BYTES; }
+
 // The workgroup's queries [q_begin, q_end) (positions in perm) and their
 // expert e, from the work list; false for a workgroup past its end.
 template <bool ROUTED>
@@ -589,7 +596,8 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
   using TD = TileDims<T, D>;
   // tiles staged through registers (K row-major, V transposed, padded rows)
   constexpr int KBYTES = TD::K_ELEMS * (int)sizeof(T);
-  constexpr int TBYTES = KBYTES + TD::V_ELEMS * (int)sizeof(T);
+  constexpr int TBYTES = (int)attend_tiles_lds<T, D>() / 2;
+  static_assert(TBYTES == KBYTES + TD::V_ELEMS * (int)sizeof(T), "one K tile and one V^T tile per buffer");
   __shared__ __align__(16) char tiles0[TBYTES];
   __shared__ __align__(16) char tiles1[TBYTES];
   auto Ks = [&](int b) { return reinterpret_cast<T *>(b ? tiles1 : tiles0); };
@@ -827,6 +835,7 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
     const int32_t *__restrict__ perm, const int32_t *__restrict__ offsets, const int32_t *__restrict__ tile_start,
     bf16_t *__restrict__ o, int N, int M, int k, float scale) {
   using DT = DmaTile<D, TK32>;
+  static_assert(attend16_tiles_lds<D>() == 4 * DT::BYTES, "two buffers of one K and one V tile");
   // two separate arrays (see attend_kernel): K then V of one tile each
   __shared__ __align__(16) char tiles0[2 * DT::BYTES];
   __shared__ __align__(16) char tiles1[2 * DT::BYTES];
@@ -960,16 +969,16 @@ static hipError_t route_t(const mita_cfg_t &c, const void *q, const void *q_lm, 
   const unsigned bh = (unsigned)BH(c);
   hipLaunchKernelGGL((route_logits_kernel<T, D>), dim3((nt + 3) / 4, bh), dim3(BLOCK), 4 * c.M * sizeof(uint32_t),
                      st, (const T *)q, (const T *)q_lm, expert, tile_cnt, counts, c.N, c.M, eff_scale(c), nt);
-  hipError_t err = hipGetLastError();
+  hipError_t err = launched("route_logits_kernel", st);
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(route_scan_kernel, dim3((c.M + SCAN_EB - 1) / SCAN_EB, bh), dim3(256), 0, st, tile_cnt, counts,
                      tile_base, offsets, tile_start, nt, c.M, c.N);
-  if ((err = hipGetLastError()) != hipSuccess) return err;
+  if ((err = launched("route_scan_kernel", st)) != hipSuccess) return err;
   int ebits = 0;
   while ((1 << ebits) < c.M) ++ebits;
   hipLaunchKernelGGL(route_scatter_kernel, dim3((nt + 3) / 4, bh), dim3(256), 0, st, expert, tile_base, perm, c.N,
                      c.M, nt, ebits);
-  return hipGetLastError();
+  return launched("route_scatter_kernel", st);
 }
 
 hipError_t launch_route(const mita_cfg_t &c, const void *q, const void *q_lm, int32_t *expert, int32_t *perm,
@@ -1000,7 +1009,7 @@ static hipError_t select_route_t(const mita_cfg_t &c, const void *q, const void 
                      4 * c.M * sizeof(uint32_t), st, sb.cand, sb.ccnt, idx, sb.fail_cnt, sb.fail_list, c.k, sb.cap,
                      nch, ml, po, (T *)v_lm, nF, (const T *)q, (const T *)q_lm, expert, tile_cnt, counts, c.N, c.M,
                      eff_scale(c), nt, route_x, nR);
-  hipError_t err = hipGetLastError();
+  hipError_t err = launched("finalize_logits_kernel", st);
   if (err != hipSuccess) return err;
   // the fallback workgroups of the last launch (listed rows, scored in full and selected)
   // (few: the rows normally all pass and these workgroups exit at once; each
@@ -1020,7 +1029,7 @@ static hipError_t select_route_t(const mita_cfg_t &c, const void *q, const void 
     hipLaunchKernelGGL((topk_scatter_kernel<T, D, TCAP, false>), dim3((unsigned)(nT + nS)), dim3(256), 0, st,
                        (const T *)q_lm, (const T *)k, S, eff_scale(c), nch, idx, c.k, sb.fail_cnt, sb.fail_list, nT,
                        expert, counts, cursor, perm, offsets, tile_start, c.N, c.M, nt, ebits, scat_x);
-  return hipGetLastError();
+  return launched("topk_scatter_kernel", st);
 }
 
 template <typename T, int D>
@@ -1034,10 +1043,12 @@ static hipError_t select_route_n(const mita_cfg_t &c, const void *q, const void 
   if (v_lm) {
     if (sb.cap <= 1024) MITA_SR(1024, true);
     if (sb.cap <= 2048) MITA_SR(2048, true);
+    if (sb.cap <= 4096) MITA_SR(4096, true);
     MITA_SR(SEL_CAP, true);
   }
   if (sb.cap <= 1024) MITA_SR(1024, false);
   if (sb.cap <= 2048) MITA_SR(2048, false);
+  if (sb.cap <= 4096) MITA_SR(4096, false);
   MITA_SR(SEL_CAP, false);
 #undef MITA_SR
 }
@@ -1059,10 +1070,8 @@ hipError_t launch_select_route(const mita_cfg_t &c, const void *q, const void *q
 
 hipError_t launch_worklist(const mita_cfg_t &c, const int32_t *offsets, int32_t *tile_start, hipStream_t st) {
   hipLaunchKernelGGL(worklist_kernel, dim3((unsigned)BH(c)), dim3(1024), 0, st, offsets, tile_start, c.M);
-  return hipGetLastError();
+  return launched("worklist_kernel", st);
 }
-
-constexpr int IDX_LDS_MAX = 8192;  // key row lists up to this length are staged in LDS
 
 template <typename T, int D, bool SH, bool RT, bool FU>
 static hipError_t attend_t3(const mita_cfg_t &c, const void *q, const void *q_lm, const void *v_lm, const void *rk,
@@ -1074,21 +1083,28 @@ static hipError_t attend_t3(const mita_cfg_t &c, const void *q, const void *q_lm
   if (RT) tiles = (tiles + c.M + NXCD - 1) / NXCD * NXCD;
   const dim3 grid((unsigned)tiles, (unsigned)BH(c));
   const int nlist = (SH ? c.M : 0) + (RT ? c.k : 0);
-  const bool in_lds = nlist <= IDX_LDS_MAX;
-  const size_t lds = in_lds ? (size_t)nlist * sizeof(int32_t) : 0;
-  if (in_lds && sizeof(T) == 2)
-    hipLaunchKernelGGL((attend16_kernel<D, SH, RT, FU>), grid, dim3(BLOCK), lds, st, (const bf16_t *)q,
-                       (const bf16_t *)q_lm, (const bf16_t *)v_lm, (const bf16_t *)rk, (const bf16_t *)rv, idx, perm,
-                       offsets, tile_start, (bf16_t *)o, c.N, c.M, c.k, eff_scale(c));
-  else if (in_lds)
-    hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU, true>), grid, dim3(BLOCK), lds, st, (const T *)q,
-                       (const T *)q_lm, (const T *)v_lm, (const T *)rk, (const T *)rv, idx, perm, offsets, tile_start,
-                       (T *)o, c.N, c.M, c.k, eff_scale(c));
-  else
-    hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU, false>), grid, dim3(BLOCK), 0, st, (const T *)q,
-                       (const T *)q_lm, (const T *)v_lm, (const T *)rk, (const T *)rv, idx, perm, offsets, tile_start,
-                       (T *)o, c.N, c.M, c.k, eff_scale(c));
-  return hipGetLastError();
+  // the row list is staged in LDS when it and the kernel's tiles fit
+  if constexpr (sizeof(T) == 2) {
+    // bf16: lists of up to IDX_LDS_MAX rows beside the 16 / 32 KB DMA tiles
+    if (list_in_lds(nlist, attend16_tiles_lds<D>())) {
+      hipLaunchKernelGGL((attend16_kernel<D, SH, RT, FU>), grid, dim3(BLOCK), (size_t)nlist * sizeof(int32_t), st,
+                         (const bf16_t *)q, (const bf16_t *)q_lm, (const bf16_t *)v_lm, (const bf16_t *)rk,
+                         (const bf16_t *)rv, idx, perm, offsets, tile_start, (bf16_t *)o, c.N, c.M, c.k, eff_scale(c));
+      return launched("attend16_kernel", st);
+    }
+  } else {
+    if (list_in_lds(nlist, attend_tiles_lds<T, D>())) {
+      hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU, true>), grid, dim3(BLOCK), (size_t)nlist * sizeof(int32_t),
+                         st, (const T *)q, (const T *)q_lm, (const T *)v_lm, (const T *)rk, (const T *)rv, idx, perm,
+                         offsets, tile_start, (T *)o, c.N, c.M, c.k, eff_scale(c));
+      return launched("attend_kernel", st);
+    }
+  }
+  // the row list stays in memory
+  hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU, false>), grid, dim3(BLOCK), 0, st, (const T *)q,
+                     (const T *)q_lm, (const T *)v_lm, (const T *)rk, (const T *)rv, idx, perm, offsets, tile_start,
+                     (T *)o, c.N, c.M, c.k, eff_scale(c));
+  return launched("attend_kernel", st);
 }
 
 template <typename T, int D>

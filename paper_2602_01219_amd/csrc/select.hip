@@ -220,7 +220,7 @@ static hipError_t sample_pivot_t(const mita_cfg_t &c, const void *q_lm, const vo
   const dim3 grid((unsigned)((c.M + 15) / 16), (unsigned)BH(c));
   hipLaunchKernelGGL((sample_pivot_kernel<T, D, NW>), grid, dim3(64 * NW), 0, st, (const T *)q_lm, (const T *)k,
                      sb.plo, sb.fail_cnt, c.N, c.M, sb.ns, sb.rank, eff_scale(c));
-  return hipGetLastError();
+  return launched("sample_pivot_kernel", st);
 }
 
 hipError_t launch_select_pivots(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sb,
@@ -247,6 +247,8 @@ static hipError_t launch_select_finalize(const mita_cfg_t &c, const SelectBufs &
     MITA_FINALIZE(TT, DD, 1024, MG);      \
   else if (sb.cap <= 2048)                \
     MITA_FINALIZE(TT, DD, 2048, MG);      \
+  else if (sb.cap <= 4096)                \
+    MITA_FINALIZE(TT, DD, 4096, MG);      \
   else                                    \
     MITA_FINALIZE(TT, DD, SEL_CAP, MG);
   if (!v_lm) {
@@ -266,7 +268,7 @@ static hipError_t launch_select_finalize(const mita_cfg_t &c, const SelectBufs &
   }
 #undef MITA_FINALIZE_CAP
 #undef MITA_FINALIZE
-  return hipGetLastError();
+  return launched("finalize_kernel", st);
 }
 
 hipError_t launch_select_finish(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sb, float *S,

@@ -31,7 +31,7 @@ static hipError_t topk_t(const mita_cfg_t &c, const float *S, int32_t *idx, hipS
     hipLaunchKernelGGL((topk_kernel<CAP, true, ROWCAP>), dim3(grid), dim3(NT), 0, st, S, idx, c.N, c.k, nrows, rows);
   else
     hipLaunchKernelGGL((topk_kernel<CAP, false, ROWCAP>), dim3(grid), dim3(NT), 0, st, S, idx, c.N, c.k, nrows, rows);
-  return hipGetLastError();
+  return launched("topk_kernel", st);
 }
 
 // Rows up to 16384 scores (64 KiB) are copied into LDS once; longer rows are

@@ -27,13 +27,14 @@ MITA_FLAG_STAGED_GATHER = 0x1
 MITA_FLAG_FULL_SCORES = 0x2
 WS_FORWARD, WS_SCORES, WS_TOPK, WS_ROUTE, WS_ATTEND = range(5)
 NUM_STAGES = 6
+MAX_LAUNCHES = 16
 STAGES = ("landmarks", "scores", "topk", "gather", "route", "attend")
 MAX_N = 65536
 
 EXPORTED = ("mita_check", "mita_workspace_size", "mita_status_string", "mita_last_error", "mita_forward",
             "mita_landmarks", "mita_scores", "mita_topk", "mita_gather", "mita_route", "mita_attend",
             "mita_timer_create", "mita_timer_destroy", "mita_timer_reset", "mita_timer_read",
-            "mita_forward_timed", "mita_forward_fallbacks")
+            "mita_forward_timed", "mita_forward_fallbacks", "mita_select_plan", "mita_timer_launches")
 
 
 class CfgStruct(ctypes.Structure):
@@ -69,6 +70,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "mita_forward": (I, [cfgp, P, P, P, P, P, Z, P]),
         "mita_forward_timed": (I, [cfgp, P, P, P, P, P, Z, P, P]),
         "mita_forward_fallbacks": (I, [cfgp, P, Z, ctypes.POINTER(ctypes.c_int64), P]),
+        "mita_select_plan": (I, [cfgp] + [ctypes.POINTER(ctypes.c_int32)] * 4),
         "mita_landmarks": (I, [cfgp, P, P, P]),
         "mita_scores": (I, [cfgp, P, P, P, P, P, P, Z, P]),
         "mita_topk": (I, [cfgp, P, P, P, Z, P]),
@@ -79,6 +81,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "mita_timer_destroy": (I, [P]),
         "mita_timer_reset": (I, [P]),
         "mita_timer_read": (I, [P, ctypes.POINTER(ctypes.c_float), I, ctypes.POINTER(I)]),
+        "mita_timer_launches": (I, [P, I, I, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_int32),
+                                    ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -194,6 +198,15 @@ def forward_fallbacks(cfg: Config, ws, stream=None) -> int:
     return n.value
 
 
+def select_plan(cfg: Config) -> dict:
+    """How the forward selects the top-k sets (host only): fused in the score
+    pass (with its sample size, pivot rank and list cap) or from the stored
+    score matrix."""
+    v = [ctypes.c_int32() for _ in range(4)]
+    _check(load_library().mita_select_plan(ctypes.byref(cfg.struct()), *[ctypes.byref(x) for x in v]))
+    return dict(zip(("fused", "ns", "rank", "cap"), (x.value for x in v)))
+
+
 def landmarks(cfg: Config, q, q_lm=None, stream=None):
     lib = load_library()
     if q_lm is None:
@@ -268,8 +281,23 @@ class Timer:
     def reset(self):
         _check(self.lib.mita_timer_reset(self.handle))
 
+    def launches(self):
+        """Waits for the events; returns a list (one per call) of
+        (kernel name, stage index, ms) tuples, one per kernel launched."""
+        out = []
+        n_calls = len(self.read())
+        for c in range(n_calls):
+            names = (ctypes.c_char_p * MAX_LAUNCHES)()
+            stages = (ctypes.c_int32 * MAX_LAUNCHES)()
+            ms = (ctypes.c_float * MAX_LAUNCHES)()
+            n = ctypes.c_int32()
+            _check(self.lib.mita_timer_launches(self.handle, c, MAX_LAUNCHES, names, stages, ms, ctypes.byref(n)))
+            out.append([(names[i].decode(), stages[i], ms[i]) for i in range(n.value)])
+        return out
+
     def read(self):
-        """Waits for the events; returns a list (one per call) of per-stage ms lists."""
+        """Waits for the events; returns a list (one per call) of per-stage ms
+        lists (each stage the sum of its launches' times)."""
         n = ctypes.c_int()
         buf = (ctypes.c_float * (self.max_calls * NUM_STAGES))()
         _check(self.lib.mita_timer_read(self.handle, buf, len(buf), ctypes.byref(n)))

@@ -111,6 +111,46 @@ WORKLOADS = {
                             128, 0.5, "iid", use_shared=0,
                             note="route-only with k = N: equals full attention"),
 }
+
+def _wl1d(idx, name, B, H, N, d, M, k, dtype, clusters, std, **kw):
+    """A 1-D sequence (grid 1 x N, landmark grid 1 x M: 1-D pooling)."""
+    return Workload(name=name, B=B, H=H, grid_h=1, grid_w=N, d=d, lm_h=1, lm_w=M, k=k,
+                    dtype=dtype, clusters=clusters, std=std, cluster_map="iid",
+                    seed=BASE_SEED + idx, **kw)
+
+
+# The paper's own operating points (m = k), at batch sizes that fill one GPU:
+#  * image classification, 224 px / patch 16 (14 x 14 tokens), m = k = 25
+#    (Sec. 4.1, Tab. ablation default; 5 x 5 landmarks: windows overlap);
+#  * semantic segmentation at 512 px and 640 px (32 x 32 and 40 x 40 tokens),
+#    m = k = 49 (Sec. 4.2; 7 x 7 landmarks: windows overlap);
+#  * long sequences of 1K, 2K and 4K tokens, m = k = 128 (Sec. 4.3, the
+#    long-range setting and its wall-clock comparison; 1-D pooling), two heads
+#    of 64 (model width 128), B * N = 262144 tokens.
+OPERATING_POINTS = {
+    "vit_m25_bf16": _wl(7, "vit_m25_bf16", 64, 6, 14, 64, 25, 25, "bf16", 16, 0.5, "iid",
+                        note="ViT-S image shape, 14x14 grid, m = k = 25"),
+    "seg512_m49_bf16": _wl(8, "seg512_m49_bf16", 16, 6, 32, 64, 49, 49, "bf16", 32, 0.5,
+                           "voronoi", note="segmentation at 512 px, 32x32 grid, m = k = 49"),
+    "seg640_m49_bf16": _wl(9, "seg640_m49_bf16", 16, 6, 40, 64, 49, 49, "bf16", 32, 0.5,
+                           "voronoi", note="segmentation at 640 px, 40x40 grid, m = k = 49"),
+    "seq1k_m128_bf16": _wl1d(10, "seq1k_m128_bf16", 256, 2, 1024, 64, 128, 128, "bf16", 32, 0.5,
+                             note="1-D sequence of 1024 tokens, m = k = 128"),
+    "seq2k_m128_bf16": _wl1d(11, "seq2k_m128_bf16", 128, 2, 2048, 64, 128, 128, "bf16", 32, 0.5,
+                             note="1-D sequence of 2048 tokens, m = k = 128"),
+    "seq4k_m128_bf16": _wl1d(12, "seq4k_m128_bf16", 64, 2, 4096, 64, 128, 128, "bf16", 32, 0.5,
+                             note="1-D sequence of 4096 tokens, m = k = 128"),
+}
+OPERATING_ORDER = list(OPERATING_POINTS)
+WORKLOADS.update(OPERATING_POINTS)
+
+
+def dense_reference(wl: Workload) -> Workload:
+    """Route-only with one landmark and k = N on the same inputs: every query
+    attends over every key, i.e. full softmax attention."""
+    return wl.with_(lm_h=1, lm_w=1, k=wl.N, use_shared=0, use_routed=1)
+
+
 WORKLOAD_ORDER = ["tiny_f32", "vits_bf16", "vitb_hr_bf16", "dense_pred_bf16",
                   "long_bf16", "dense_equiv_bf16"]
 HEADLINE = "dense_pred_bf16"

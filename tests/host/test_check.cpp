@@ -1,5 +1,6 @@
 // Host-only test of the argument validation and workspace layout (no GPU).
 #include <cassert>
+#include <cmath>
 #include <cstdio>
 #include <string>
 
@@ -64,10 +65,19 @@ int main() {
   mita::FwdLayout L2 = mita::forward_layout(c);
   assert(L2.vx - L2.kx == (size_t)24 * 128 * 512 * 64 * 2);
   assert(mita::workspace_size(&c, MITA_WS_TOPK) == 0);
-  // fused selection: sample of 1024 keys, pivot rank 32 + 5 * sqrt(32 * 31 / 32) + 1
-  // -> 61 at N = 16384, k = 512; expected count bound (61 + 6 sqrt(61)) * 16 -> cap 2048
+  // fused selection: sample of 1024 keys; the smallest pivot rank with
+  // P(X >= r) <= 1e-9 for X ~ H(16384, 511, 1024) is 69, and the smallest
+  // power-of-two cap with P(Y < 69) <= 1e-9 for Y ~ H(16384, cap, 1024) is 2048
   assert(mita::fused_select(c) && mita::sel_ns(c) == 1024 && mita::sel_cap(c) == 2048);
-  assert(mita::sel_rank(c) == 61);
+  assert(mita::sel_rank(c) == 69);
+  assert(mita::hyper_sf(16384, 511, 1024, 69) <= mita::SEL_EPS && mita::hyper_sf(16384, 511, 1024, 68) > mita::SEL_EPS);
+  assert(mita::hyper_cdf_below(16384, 2048, 1024, 69) <= mita::SEL_EPS);
+  assert(mita::hyper_cdf_below(16384, 1024, 1024, 69) > mita::SEL_EPS);
+  // the two tails of one law add up to 1 (X >= r or X < r)
+  for (int r = 1; r < 200; r += 7) {
+    const double t = mita::hyper_sf(16384, 2048, 1024, r) + mita::hyper_cdf_below(16384, 2048, 1024, r);
+    assert(std::fabs(t - 1.0) < 1e-9);
+  }
   assert(L2.ccnt - L2.plo == (size_t)24 * 128 * 4);
   assert(L2.cand - L2.ccnt == (size_t)24 * 128 * 32 * 4);
   assert(L2.fail - L2.cand == (size_t)24 * 128 * 32 * 512 * 8);
@@ -75,14 +85,24 @@ int main() {
   c.flags = MITA_FLAG_FULL_SCORES;
   assert(!mita::fused_select(c) && mita::forward_layout(c).plo == mita::forward_layout(c).total);
   c.flags = 0;
-  c.k = 1025;
+  c.k = 4096;  // rank 340, cap 8192
+  assert(mita::fused_select(c) && mita::sel_rank(c) == 340 && mita::sel_cap(c) == 8192);
+  c.k = 6000;  // rank 467 would need a cap above 8192: stored-S path
   assert(!mita::fused_select(c));
   c.grid_h = 32; c.grid_w = 32; c.N = 1024; c.k = 1024;  // the sample is the whole row: rank = k
   assert(mita::fused_select(c) && mita::sel_rank(c) == 1024 && mita::sel_cap(c) == 1024);
-  c.grid_h = 32; c.grid_w = 64; c.N = 2048; c.k = 2048;  // 4 k above the list capacity: stored-S path
+  c.grid_h = 32; c.grid_w = 64; c.N = 2048; c.k = 2048;  // k = N > the sample: no rank meets the bound
   assert(!mita::fused_select(c));
-  c.grid_h = 256; c.grid_w = 256; c.N = 65536; c.k = 1024;  // rank 37, bound (37 + 36.5) * 64 -> cap 4096
-  assert(mita::fused_select(c) && mita::sel_rank(c) == 37 && mita::sel_cap(c) == 4096);
+  c.grid_h = 256; c.grid_w = 256; c.N = 65536; c.k = 1024;  // rank 45; cap 4096 misses, 8192 meets the bound
+  assert(mita::fused_select(c) && mita::sel_rank(c) == 45 && mita::sel_cap(c) == 8192);
+  c.grid_h = 64; c.grid_w = 64; c.N = 4096; c.k = 256;  // rank 107, cap 1024
+  assert(mita::fused_select(c) && mita::sel_rank(c) == 107 && mita::sel_cap(c) == 1024);
+  // attention row lists in LDS: fp32 d = 128 tiles take 137216 bytes, so at
+  // most 6656 rows fit beside them; the bf16 DMA tiles (16 KB at d = 64) leave
+  // room for the longest list staged in LDS (8192 rows)
+  assert(mita::list_in_lds(6656, 137216) && !mita::list_in_lds(6657, 137216));
+  assert(mita::list_in_lds(8192, 16384) && !mita::list_in_lds(8193, 16384));
+  assert(mita::list_in_lds(8192, 32768) && !mita::list_in_lds(8192, 163840 - 32767));
   c = base();
   c.d = 96;
   assert(mita::workspace_size(&c, MITA_WS_FORWARD) == 0);

@@ -45,11 +45,18 @@ def test_host_validation_without_gpu():
     assert mita.workspace_size(cfg, mita.WS_TOPK) == 0
 
 
-def test_check_header_host_program(tmp_path):
+@pytest.mark.parametrize("sanitize", [False, True], ids=["plain", "asan_ubsan"])
+def test_check_header_host_program(tmp_path, sanitize):
+    """The header-only validation, workspace layout, selection plan and LDS
+    dispatch rule, built with g++ (host code only), plainly and under
+    AddressSanitizer + UndefinedBehaviorSanitizer."""
     exe = tmp_path / "test_check"
     src = os.path.join(ROOT, "tests", "host", "test_check.cpp")
-    r = subprocess.run(["g++", "-std=c++17", "-O1", "-Wall", "-I", os.path.join(ROOT, "include"), src, "-o",
-                        str(exe)], capture_output=True, text=True)
+    flags = ["-std=c++17", "-O1", "-Wall", "-g"]
+    if sanitize:
+        flags += ["-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer"]
+    r = subprocess.run(["g++", *flags, "-I", os.path.join(ROOT, "include"), src, "-o", str(exe)],
+                       capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
     r = subprocess.run([str(exe)], capture_output=True, text=True)
     assert r.returncode == 0, r.stdout + r.stderr

@@ -65,6 +65,19 @@ def _rows(N, limit, seed=0):
     return rows
 
 
+def _same(a, b):
+    return torch.equal(a.view(torch.int16), b.view(torch.int16)) if a.dtype == torch.bfloat16 else torch.equal(a, b)
+
+
+def _all_slices(wl, limit=None):
+    sl = [(b, h) for b in range(wl.B) for h in range(wl.H)]
+    if limit is not None and len(sl) > limit:
+        r = np.random.default_rng(wl.seed)
+        pick = sorted(set([0, len(sl) - 1] + list(r.choice(len(sl), limit - 2, replace=False))))
+        sl = [sl[i] for i in pick]
+    return sl
+
+
 def _stages(cfg: mita.Config, q, k, v):
     """Run the stage entry points in the forward's order (staged gather)."""
     q_lm = mita.landmarks(cfg, q)
@@ -93,29 +106,46 @@ def _bounds(q, k, q_lm_ref, cfg, dtype):
     return tau_s, tau_r
 
 
-def _end_to_end(cfg: mita.Config, inp: synth.Inputs, q, k, v, slices, row_limit, exact_sets=False):
+def _end_to_end(cfg: mita.Config, inp: synth.Inputs, q, k, v, slices, row_limit, exact_sets=False,
+                grouped_slices=()):
+    """The forward against the oracle. On `slices`, sampled rows against the
+    per-query form (Eq. mita written out per token); on `grouped_slices`,
+    every row against the grouped form (Algorithm 1's shared attention,
+    per-expert attention and log-sum-exp combine), which the pins show equal
+    to the per-query form. Both take the GPU's top-k sets and routing after
+    validating them against the oracle's float64 scores and logits."""
+    import time
     o_fwd = mita.forward(cfg, q, k, v)
     st = _stages(cfg, q, k, v)
     torch.cuda.synchronize()
-    assert torch.equal(o_fwd.view(torch.int16) if o_fwd.dtype == torch.bfloat16 else o_fwd,
-                       st["o"].view(torch.int16) if o_fwd.dtype == torch.bfloat16 else st["o"]), \
-        "forward differs from the stage pipeline"
+    assert _same(o_fwd, st["o"]), "forward differs from the stage pipeline"
     tol = tol_for(cfg.dtype)
-    o_g = o_fwd
     worst = 0.0
+    o_all = from_dev(o_fwd)
+    idx_all = st["idx"].cpu().numpy().astype(np.int64) if cfg.use_routed else None
+    exp_all = st["expert"].cpu().numpy().astype(np.int64) if cfg.use_routed else None
+    t_oracle = 0.0
+
+    def discrete(b, h, qs, ks, q_lm_ref):
+        """The GPU's top-k sets and routing of slice (b, h), validated."""
+        if not cfg.use_routed:
+            return None, None, None
+        S_ref = O.scores(q_lm_ref, ks, cfg.eff_scale)
+        tau_s, tau_r = _bounds(qs, ks, q_lm_ref, cfg, cfg.dtype)
+        force_idx, force_exp = idx_all[b, h], exp_all[b, h]
+        same = check_selection(S_ref, tau_s, force_idx, cfg.k)
+        L_ref = (qs @ q_lm_ref.T) * cfg.eff_scale
+        agree = check_routing(L_ref, tau_r, force_exp)
+        return force_idx, force_exp, (S_ref, tau_s, same, agree)
+
     for (b, h) in slices:
         qs, ks, vs = _slice64(inp, b, h)
         rows = _rows(cfg.N, row_limit, seed=b * 131 + h)
+        t0 = time.perf_counter()
         q_lm_ref = O.landmarks(qs, cfg.grid_h, cfg.grid_w, cfg.lm_h, cfg.lm_w)
-        force_idx = force_exp = None
-        if cfg.use_routed:
-            S_ref = O.scores(q_lm_ref, ks, cfg.eff_scale)
-            tau_s, tau_r = _bounds(qs, ks, q_lm_ref, cfg, cfg.dtype)
-            force_idx = st["idx"][b, h].cpu().numpy().astype(np.int64)
-            same = check_selection(S_ref, tau_s, force_idx, cfg.k)
-            force_exp = st["expert"][b, h].cpu().numpy().astype(np.int64)
-            L_ref = (qs @ q_lm_ref.T) * cfg.eff_scale
-            agree = check_routing(L_ref, tau_r, force_exp)
+        force_idx, force_exp, info = discrete(b, h, qs, ks, q_lm_ref)
+        if info is not None:
+            S_ref, tau_s, same, agree = info
             log(f"  slice ({b},{h}): top-k sets equal to the oracle's {same}/{cfg.M}, routing agrees {agree}/{cfg.N}")
             if exact_sets:
                 # with every score gap above the budget the sets must be the oracle's own
@@ -126,12 +156,37 @@ def _end_to_end(cfg: mita.Config, inp: synth.Inputs, q, k, v, slices, row_limit,
                         assert (ref == force_idx[i]).all()
         r = O.forward_slice(qs, ks, vs, cfg.grid_h, cfg.grid_w, cfg.lm_h, cfg.lm_w, cfg.k, None, cfg.use_shared,
                             cfg.use_routed, force_idx, force_exp, rows=rows)
-        got = from_dev(o_g[b, h])[rows]
-        err = maxrel(got, r.o)
+        t_oracle += time.perf_counter() - t0
+        err = maxrel(o_all[b, h][rows], r.o)
         worst = max(worst, err)
-        log(f"  slice ({b},{h}) rows {len(rows)}: max-rel error {err:.3e} (tol {tol})")
+        log(f"  slice ({b},{h}) rows {len(rows)} (per-query form): max-rel error {err:.3e} (tol {tol})")
         assert err <= tol
-    return worst
+    worst_g = worst_el = 0.0
+    for (b, h) in grouped_slices:
+        qs, ks, vs = _slice64(inp, b, h)
+        t0 = time.perf_counter()
+        q_lm_ref = O.landmarks(qs, cfg.grid_h, cfg.grid_w, cfg.lm_h, cfg.lm_w)
+        force_idx, force_exp, _ = discrete(b, h, qs, ks, q_lm_ref)
+        S_ref = O.scores(q_lm_ref, ks, cfg.eff_scale)
+        v_lm_ref = O.landmark_values(S_ref, vs) if cfg.use_shared else None
+        if cfg.use_routed:
+            kx, vx = O.gather(ks, vs, force_idx)
+            routing = O.routing_from_expert(force_exp, cfg.M)
+        else:
+            kx = vx = routing = None
+        ref = O.output_grouped(qs, q_lm_ref, v_lm_ref, kx, vx, routing, cfg.eff_scale, cfg.use_shared,
+                               cfg.use_routed)
+        t_oracle += time.perf_counter() - t0
+        got = o_all[b, h]
+        err = maxrel(got, ref)
+        el = float(np.max(np.abs(got - ref) / (np.abs(ref) + 1e-3 * np.max(np.abs(ref)))))
+        worst_g, worst_el = max(worst_g, err), max(worst_el, el)
+        assert err <= tol, f"slice ({b},{h}) all rows: max-rel error {err:.3e} > {tol}"
+    if grouped_slices:
+        log(f"  {len(grouped_slices)} slices, every row (grouped form): worst normwise max-rel {worst_g:.3e}, "
+            f"worst elementwise |d|/(|ref| + 1e-3 max|ref|) {worst_el:.3e} (tol {tol})")
+    log(f"  oracle CPU time {t_oracle:.1f} s")
+    return max(worst, worst_g)
 
 
 # ------------------------------------------------------------------ stage parity
@@ -281,6 +336,14 @@ def test_attend_parity_identical_inputs(name):
 
 
 # ------------------------------------------------------------------ end to end
+# every row of every (b, h) slice against the grouped oracle form, except
+# where the oracle's time or memory would be out of proportion: the long
+# sequence (4 slices) and the dense-equivalence mode (per-query rows only;
+# compared with SDPA below)
+GROUPED_SLICES = {"tiny_f32": None, "vits_bf16": None, "vitb_hr_bf16": None, "dense_pred_bf16": None,
+                  "long_bf16": 4, "dense_equiv_bf16": 0}
+
+
 @pytest.mark.parametrize("name", ALL)
 def test_forward_end_to_end(name):
     inp = _inputs(name)
@@ -288,8 +351,41 @@ def test_forward_end_to_end(name):
     cfg = mita.Config.from_workload(wl)
     q, k, v = _dev_inputs(name)
     log(f"[forward] {name} B={wl.B} H={wl.H} N={wl.N} d={wl.d} M={wl.M} k={wl.k} {wl.dtype}")
+    lim = GROUPED_SLICES[name]
     _end_to_end(cfg, inp, q, k, v, _slices(wl), row_limit=256 if wl.N > 4096 else 512,
-                exact_sets=(wl.dtype == "f32"))
+                exact_sets=(wl.dtype == "f32"), grouped_slices=[] if lim == 0 else _all_slices(wl, lim))
+
+
+@pytest.mark.parametrize("name", synth.OPERATING_ORDER)
+def test_operating_points_end_to_end(name):
+    """The paper's own operating points (m = k = 25 at 14 x 14, 49 at 32 x 32
+    and 40 x 40 with overlapping windows, 128 on 1-D sequences of 1K-4K):
+    16 slices, every row, against the grouped oracle form."""
+    inp = _inputs(name)
+    wl = inp.wl
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = _dev_inputs(name)
+    log(f"[forward] {name} B={wl.B} H={wl.H} N={wl.N} d={wl.d} M={wl.M} k={wl.k} grid {wl.grid_h}x{wl.grid_w}")
+    _end_to_end(cfg, inp, q, k, v, _slices(wl), row_limit=256, grouped_slices=_all_slices(wl, 16))
+
+
+@pytest.mark.parametrize("name", synth.OPERATING_ORDER)
+def test_operating_points_dense_reference(name):
+    """The dense reference of the operating-point sweep (route-only, one
+    landmark, k = N on the same kernels) is full softmax attention."""
+    inp = _inputs(name)
+    wl = synth.dense_reference(inp.wl)
+    q, k, v = _dev_inputs(name)
+    o = mita.forward(mita.Config.from_workload(wl), q, k, v)
+    torch.cuda.synchronize()
+    for (b, h) in _slices(wl):
+        qs, ks, vs = _slice64(inp, b, h)
+        rows = _rows(wl.N, 256, seed=b + h)
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            torch.from_numpy(qs[rows])[None], torch.from_numpy(ks)[None], torch.from_numpy(vs)[None])[0].numpy()
+        err = maxrel(from_dev(o[b, h])[rows], ref)
+        log(f"  dense slice ({b},{h}) max-rel vs SDPA {err:.3e}")
+        assert err <= 2e-2
 
 
 def test_dense_equivalence_is_full_attention():
@@ -333,6 +429,8 @@ EDGE = [
     # register-staged tiles, row indices read from memory
     (96, 96, 4, 4, 8200, 64, "bf16", 1, 1),
     (96, 96, 2, 2, 8190, 64, "f32", 1, 1),
+    # fp32 d = 128: 6704 rows do not fit in LDS beside the 134 KB of tiles
+    (96, 72, 2, 2, 6700, 128, "f32", 1, 1),
 ]
 
 
@@ -353,8 +451,6 @@ def test_forward_edge_cases(case):
 
 
 # ------------------------------------------------------------------ fused top-k selection
-def _same(a, b):
-    return torch.equal(a.view(torch.int16), b.view(torch.int16)) if a.dtype == torch.bfloat16 else torch.equal(a, b)
 
 
 @pytest.mark.parametrize("name", ALL)
@@ -375,13 +471,18 @@ def test_fused_selection_equals_full_score_path(name):
 
 
 def _fallback_case(K, cfg, q, v, expect_fb):
+    """expect_fb: the exact number of rows that must fall back, or None for
+    'at least one'."""
     ws = torch.empty(mita.workspace_size(cfg), dtype=torch.uint8, device="cuda")
     a = mita.forward(cfg, q, K, v, ws=ws)
     fb = mita.forward_fallbacks(cfg, ws)
     b = mita.forward(dataclasses.replace(cfg, full_scores=True), q, K, v)
     torch.cuda.synchronize()
-    log(f"  fallback rows {fb} (expected {expect_fb})")
-    assert fb == expect_fb
+    log(f"  fallback rows {fb} (expected {'>= 1' if expect_fb is None else expect_fb})")
+    if expect_fb is None:
+        assert fb >= 1
+    else:
+        assert fb == expect_fb
     assert _same(a, b)
 
 
@@ -392,11 +493,35 @@ def _small_dense(H=2):
     return inp, cfg, tuple(to_dev(x, "bf16") for x in (inp.q, inp.k, inp.v))
 
 
-def test_fused_selection_rows_beyond_the_list_fall_back():
-    """Head 0 with all-zero keys: every score ties at 0, all N = 16384 tokens
-    reach the pivot, more than a list holds: those rows are recomputed in
-    full and selected exactly (the first k indices); head 1 stays fused."""
-    inp, cfg, (q, k, v) = _small_dense()
+# Shapes whose fused selection (and its fallback inside the routing launch)
+# takes different kernel instantiations: bf16 d = 64 (the headline shape),
+# bf16 d = 128 at N = 65536 (the long-sequence shape: list cap 8192, the
+# fallback's top-k streams its 65536 scores), and fp32 at d = 64 and 128 with
+# N > 1024 (a real sample).
+FALLBACK_SHAPES = {
+    "bf16_d64_n16384": lambda: synth.WORKLOADS["dense_pred_bf16"].with_(B=1, H=2),
+    "bf16_d128_n65536": lambda: synth.WORKLOADS["long_bf16"].with_(B=1, H=1),
+    "f32_d64_n16384": lambda: synth.WORKLOADS["dense_pred_bf16"].with_(B=1, H=1, dtype="f32"),
+    "f32_d128_n4096": lambda: synth.WORKLOADS["vitb_hr_bf16"].with_(B=1, H=1, d=128, dtype="f32"),
+}
+
+
+def _fallback_inputs(shape):
+    wl = FALLBACK_SHAPES[shape]()
+    inp = synth.generate(wl)
+    cfg = mita.Config.from_workload(wl)
+    plan = mita.select_plan(cfg)
+    log(f"[fallback] {shape}: N={wl.N} d={wl.d} M={wl.M} k={wl.k} {wl.dtype}, selection {plan}")
+    assert plan["fused"] and plan["ns"] < wl.N
+    return inp, cfg, tuple(to_dev(x, wl.dtype) for x in (inp.q, inp.k, inp.v))
+
+
+@pytest.mark.parametrize("shape", list(FALLBACK_SHAPES))
+def test_fused_selection_rows_beyond_the_list_fall_back(shape):
+    """Head 0 with all-zero keys: every score ties at 0, all N tokens reach
+    the pivot, more than a list holds: those rows are recomputed in full and
+    selected exactly (the first k indices); any other head stays fused."""
+    inp, cfg, (q, k, v) = _fallback_inputs(shape)
     K = k.clone()
     K[0, 0] = 0
     _fallback_case(K, cfg, q, v, expect_fb=cfg.M)
@@ -405,16 +530,18 @@ def test_fused_selection_rows_beyond_the_list_fall_back():
 SELECT_SAMPLE = 1024  # keys the forward samples per landmark row for its top-k pivot
 
 
-def test_fused_selection_unrepresentative_sample_falls_back():
+@pytest.mark.parametrize("shape", list(FALLBACK_SHAPES))
+def test_fused_selection_unrepresentative_sample_falls_back(shape):
     """Keys at exactly the sampled positions (the middle of each of 1024 equal
-    parts of the row) scaled up 8x: the pivot from the sample then lies above
-    all but about r of the row's scores, fewer than k, so every row falls back."""
-    inp, cfg, (q, k, v) = _small_dense(H=1)
+    parts of the row) scaled up 8x: the pivot from the sample then sits among
+    those scaled scores, away from the rest of the row, so rows list fewer
+    than k or more than the cap and fall back; the sets are still exact."""
+    inp, cfg, (q, k, v) = _fallback_inputs(shape)
     ns = min(cfg.N, SELECT_SAMPLE)
     pos = ((2 * np.arange(ns) + 1) * cfg.N) // (2 * ns)
     K = k.clone()
     K[0, 0, torch.from_numpy(pos).cuda()] *= 8
-    _fallback_case(K, cfg, q, v, expect_fb=cfg.M)
+    _fallback_case(K, cfg, q, v, expect_fb=cfg.M if shape == "bf16_d64_n16384" else None)
 
 
 def test_fused_selection_exact_ties_within_the_list():
@@ -502,7 +629,7 @@ def test_forward_is_deterministic():
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
-def test_timer_records_every_stage():
+def test_timer_records_every_launch():
     name = "vits_bf16"
     cfg = mita.Config.from_workload(_inputs(name).wl)
     q, k, v = _dev_inputs(name)
@@ -510,8 +637,18 @@ def test_timer_records_every_stage():
     o1 = mita.forward(cfg, q, k, v, timer=t)
     mita.forward(cfg, q, k, v, timer=t)
     ms = t.read()
+    launches = t.launches()
     assert len(ms) == 2 and all(len(x) == mita.NUM_STAGES for x in ms)
     assert all(x >= 0 for row in ms for x in row) and sum(ms[0]) > 0
+    for call, stages in zip(launches, ms):
+        names = [n for n, _, _ in call]
+        log(f"  launches {[(n, s, round(t_ * 1e3, 1)) for n, s, t_ in call]}")
+        assert names[0] == "pool_kernel" and names[-1] == "attend16_kernel"
+        assert "scores_kernel" in names
+        # stage times are sums of their launches; a stage that launches nothing takes 0
+        for s_ in range(mita.NUM_STAGES):
+            assert abs(stages[s_] - sum(t_ for _, st_, t_ in call if st_ == s_)) < 1e-6
+        assert stages[mita.STAGES.index("gather")] == 0.0
     o2 = mita.forward(cfg, q, k, v)
     assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
     t.close()
