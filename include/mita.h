@@ -129,6 +129,24 @@ int mita_forward(const mita_cfg_t *cfg, const void *q, const void *k, const void
                  void *ws, size_t ws_bytes, mita_stream_t stream);
 
 /*
+ * mita_forward for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same forward and results, with its workspace in a static device array of
+ * MITA_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends. It calls no hipMalloc, hipFree or other
+ * allocating routine. The calling thread's current device must be the one
+ * the stream and tensors belong to.
+ *   q, k, v, o : as mita_forward.
+ * Returns MITA_ERR_WORKSPACE (launching nothing) when the forward needs more
+ * workspace than the scratch holds (mita_workspace_size(cfg, MITA_WS_FORWARD)
+ * > MITA_NOALLOC_SCRATCH_BYTES). Every call on one GPU uses that GPU's one
+ * array: calls that overlap on one GPU (other streams or threads) race.
+ */
+#define MITA_NOALLOC_SCRATCH_BYTES (64u << 20)
+int mita_forward_noalloc(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, void *o,
+                         mita_stream_t stream);
+
+/*
  * Diagnostic: the number of landmark rows whose top-k selection in the last
  * mita_forward on workspace ws fell back to recomputing the full score row
  * (0 when that forward stored the whole score matrix). Waits for `stream`.

@@ -2,6 +2,7 @@
 // the launch sequence of the forward pass (Algorithm 1 order).
 #include <hip/hip_runtime.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -190,7 +191,52 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
 
 }  // namespace
 
+// Workspace of mita_forward_noalloc, for callers that cannot allocate: one
+// static device array per GPU the library runs on (held until the process
+// ends). In host code `scratch` is only a stand-in for the symbol; its device
+// address on the current GPU comes from hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[MITA_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[MAX_DEVICES] = {};
+
+// The device address of `scratch` on the current device, looked up once per
+// device (with that device current).
+int scratch_address(void **out) {
+  int dev = -1;
+  TRY(hip_status(hipGetDevice(&dev), "hipGetDevice"));
+  if (dev < 0 || dev >= MAX_DEVICES) return set_err(MITA_ERR_HIP, "device index out of range for the scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    TRY(hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)"));
+    if (!p) return set_err(MITA_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MITA_OK;
+}
+
+}  // namespace
+
 extern "C" {
+
+int mita_forward_noalloc(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, void *o,
+                         mita_stream_t stream) {
+  g_err.clear();
+  TRY(validate(cfg));
+  const size_t need = workspace_size(cfg, MITA_WS_FORWARD);
+  if (need > MITA_NOALLOC_SCRATCH_BYTES)
+    return set_err(MITA_ERR_WORKSPACE, "the forward needs " + std::to_string(need) +
+                                           " bytes of workspace; the static scratch of mita_forward_noalloc holds " +
+                                           std::to_string((size_t)MITA_NOALLOC_SCRATCH_BYTES));
+  void *ws = nullptr;
+  TRY(scratch_address(&ws));
+  return forward_impl(cfg, q, k, v, o, ws, MITA_NOALLOC_SCRATCH_BYTES, (hipStream_t)stream, nullptr);
+}
 
 int mita_check(const mita_cfg_t *cfg) { return validate(cfg); }
 

@@ -34,7 +34,8 @@ MAX_N = 65536
 EXPORTED = ("mita_check", "mita_workspace_size", "mita_status_string", "mita_last_error", "mita_forward",
             "mita_landmarks", "mita_scores", "mita_topk", "mita_gather", "mita_route", "mita_attend",
             "mita_timer_create", "mita_timer_destroy", "mita_timer_reset", "mita_timer_read",
-            "mita_forward_timed", "mita_forward_fallbacks", "mita_select_plan", "mita_timer_launches")
+            "mita_forward_timed", "mita_forward_fallbacks", "mita_select_plan", "mita_timer_launches",
+            "mita_forward_noalloc")
 
 
 class CfgStruct(ctypes.Structure):
@@ -69,6 +70,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "mita_last_error": (ctypes.c_char_p, []),
         "mita_forward": (I, [cfgp, P, P, P, P, P, Z, P]),
         "mita_forward_timed": (I, [cfgp, P, P, P, P, P, Z, P, P]),
+        "mita_forward_noalloc": (I, [cfgp, P, P, P, P, P]),
         "mita_forward_fallbacks": (I, [cfgp, P, Z, ctypes.POINTER(ctypes.c_int64), P]),
         "mita_select_plan": (I, [cfgp] + [ctypes.POINTER(ctypes.c_int32)] * 4),
         "mita_landmarks": (I, [cfgp, P, P, P]),
@@ -186,6 +188,22 @@ def forward(cfg: Config, q, k, v, o=None, ws=None, stream=None, timer: "Timer" =
         st = lib.mita_forward_timed(ctypes.byref(c), _p(q), _p(k), _p(v), _p(o), _p(ws), nws, _stream(stream),
                                     timer.handle)
     _check(st)
+    return o
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def forward_noalloc(cfg: Config, q, k, v, o=None, stream=None):
+    """MiTA forward with the library's static scratch as workspace (no
+    allocation by the library; only the output is allocated here if not
+    given). Raises MitaError(MITA_ERR_WORKSPACE) if the forward needs more
+    than NOALLOC_SCRATCH_BYTES of workspace."""
+    lib = load_library()
+    _dev(q)
+    if o is None:
+        o = torch.empty_like(q)
+    _check(lib.mita_forward_noalloc(ctypes.byref(cfg.struct()), _p(q), _p(k), _p(v), _p(o), _stream(stream)))
     return o
 
 
