@@ -304,6 +304,30 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 typedef short v4i16_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
 
+// Keep x in a register as computed here: the compiler may not recompute it
+// inside a loop (it does so to save registers, at a few VALU instructions per
+// use).
+template <typename T> __device__ __forceinline__ void pin(T &x) { asm volatile("" : "+v"(x)); }
+
+// Per-lane part of the DMA of one tile, fixed for every tile: the tile row r
+// this lane loads (rows start at multiples of 32, so the swizzle of r is the
+// same in every tile) and its 16-byte source chunk (sl ^ swz(r)) << 4.
+template <int D, int ROWS> struct DmaLane {
+  static constexpr int PW = DmaTile<D, ROWS>::PW;
+  uint32_t row[PW];    // r, per instruction of the wave
+  uint32_t chunk[PW];  // byte offset of the swizzled chunk within the row
+  __device__ __forceinline__ void init(int w, int lane) {
+    using DT = DmaTile<D, ROWS>;
+#pragma unroll
+    for (int j = 0; j < PW; ++j) {
+      const int r = (w * PW + j) * DT::RPI + lane / DT::CPR;
+      row[j] = (uint32_t)r;
+      chunk[j] = (uint32_t)(((lane % DT::CPR) ^ swz(r)) << 4);
+      pin(chunk[j]);
+    }
+  }
+};
+
 // Issue the DMA of one tile: rows r < ROWS of K and V from byte offsets
 // offs[r] past kb and vb (without FULL, rows >= nrows take offset offs[0]:
 // real data, masked later).
@@ -326,141 +350,220 @@ __device__ __forceinline__ void dma_tile(bf16_t *Kl, bf16_t *Vl, const bf16_t *k
   }
 }
 
-// Softmax state of a wave with up to two 16-query groups for the DMA path
-// (the attention uses one group per wave): as Online2, the
-// reference max m kept also as the negated splat nm that initialises the
-// score accumulators, so the MFMA yields dot * scale * log2 e - m directly
-// (the query fragments are pre-scaled by scale * log2 e).
-template <int D> struct OnlineDma {
-  f32x4 o[2][D / 16];
-  f32x4 lsum[2];
-  f32x4 nm[2];
-  bool started;
-  __device__ __forceinline__ void init() {
+// The same for a whole tile (every row valid) with the lane's precomputed
+// rows and chunks.
+template <int D, int ROWS>
+__device__ __forceinline__ void dma_tile_lane(bf16_t *Kl, bf16_t *Vl, const bf16_t *kb, const bf16_t *vb,
+                                              const uint32_t *offs, const DmaLane<D, ROWS> &dl) {
+  using DT = DmaTile<D, ROWS>;
+  const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-#pragma unroll
-      for (int i = 0; i < D / 16; ++i) o[c][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-      lsum[c] = f32x4{0.f, 0.f, 0.f, 0.f};
-      nm[c] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-    started = false;
+  for (int j = 0; j < DT::PW; ++j) {
+    const int ins = w * DT::PW + j;
+    const uint32_t go = offs[dl.row[j]] + dl.chunk[j];
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(kb) + go,
+                                     (lds_void_t *)(reinterpret_cast<char *>(Kl) + ins * 1024), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vb) + go,
+                                     (lds_void_t *)(reinterpret_cast<char *>(Vl) + ins * 1024), 16, 0, 0);
   }
-  // a half that saw no key has no reference: -inf, with zero sums
-  __device__ __forceinline__ float mval(int c) const { return started ? -nm[c][0] : -INFINITY; }
-  __device__ __forceinline__ float l(int c) const { return lsum[c][0]; }
+}
+
+// ---------------------------------------------------------------------------
+// One wave's online softmax over DMA-staged 32-key tiles for its 16 queries
+// (one MFMA column group; lane (g, p) holds column p). The score MFMAs start
+// from the splat -m of the column's reference max (log2 units; the query
+// fragments are pre-scaled by scale * log2 e), so they yield the exp2
+// argument directly. The reference is the first tile's column max and moves
+// only when a column's shifted scores exceed RESCALE_LOG2. The weight sum is
+// kept per lane over the lane's own 8 keys of each tile, from the very bf16
+// weights that multiply V (v_dot2c_f32_bf16 against a pair of ones); the
+// query's sum is the sum over the four lane groups of its column, formed
+// once at the end in a fixed order.
+// ---------------------------------------------------------------------------
+template <int D> struct Att16 {
+  f32x4 o[D / 16];  // O^T: dims 16 db + 4 g + r of query p
+  f32x4 nm;         // -m, splat
+  float l;          // this lane's part of the weight sum
 };
 
-// One wave's step over the 32 keys at rows 32h .. 32h + 31 of a DMA-staged
-// tile for its query groups (pre-scaled fragments qf[c]; the attention's
-// tiles are 32 rows, h = 0, one group). The reference max starts at the first
-// tile's column max; later it moves only when a column's shifted scores
-// exceed RESCALE_LOG2 (then the tile's values, accumulators and sums shift
-// with it). With MASKED only keys 32h + i, i < nvalid (>= 1), count. NG = 1
-// computes the first 16-query group only (the second holds no query).
-template <int D, bool MASKED = false, int NG = 2>
-__device__ __forceinline__ void half_tile_dma(OnlineDma<D> &st, const bf16_t *Kl, const bf16_t *Vl, int h,
-                                              const Frag<bf16_t> (&qf)[2][D / 32], int nvalid) {
-  static_assert(NG == 1 || NG == 2, "one or two query groups");
-  constexpr int RB = 2 * D;  // bytes per row
-  const int lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
+// Per-lane LDS byte offsets within one tile buffer, fixed for every tile:
+// K fragment of reduction step ks (row p of the first 16-key block; the
+// second block is 16 rows on, same swizzle) and the V^T transpose reads of
+// dimension block db (row 4 g + e of the first 16-key half; the second half
+// is 16 rows on).
+template <int D> struct Att16Addr {
+  uint32_t k[D / 32];
+  uint32_t v[D / 16];
+  __device__ __forceinline__ void init() {
+    constexpr int RB = 2 * D;  // bytes per row
+    const int lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      k[ks] = (uint32_t)(p * RB + (((4 * ks + g) ^ swz(p)) << 4));
+      pin(k[ks]);
+    }
+    const int e = p >> 2, c4 = p & 3, R = 4 * g + e;
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) {
+      v[db] = (uint32_t)(R * RB + (((2 * db + (c4 >> 1)) ^ swz(R)) << 4) + ((c4 & 1) << 3));
+      pin(v[db]);
+    }
+  }
+};
+
+// Shifted scores of the tile's 32 keys (acc[kb][r]: key 16 kb + 4 g + r of query p).
+template <int D>
+__device__ __forceinline__ void att16_scores(f32x4 (&acc)[2], const Att16<D> &st, const bf16_t *__restrict__ Kl,
+                                             const Att16Addr<D> &ad, const Frag<bf16_t> (&qf)[D / 32]) {
+  constexpr int RB = 2 * D;
   const char *kbase = reinterpret_cast<const char *>(Kl);
-  f32x4 acc[2][2];  // [group][16-key block]: shifted scores
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
-    acc[0][kb] = st.nm[0];
-    acc[1][kb] = st.nm[1];
-    const int R = 32 * h + kb * 16 + p;
+    acc[kb] = st.nm;
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks) {
       Frag<bf16_t> a;
-      a.v = *reinterpret_cast<const uint4 *>(kbase + R * RB + (((4 * ks + g) ^ swz(R)) << 4));
-      acc[0][kb] = mma(a, qf[0][ks], acc[0][kb]);
-      if (NG > 1) acc[1][kb] = mma(a, qf[1][ks], acc[1][kb]);
+      a.v = *reinterpret_cast<const uint4 *>(kbase + ad.k[ks] + kb * 16 * RB);
+      acc[kb] = mma(a, qf[ks], acc[kb]);
     }
   }
-  float mx[2] = {-INFINITY, -INFINITY};
+}
+
+// Weights of the tile (exp2 of the shifted scores; with MASKED keys i >=
+// nvalid weigh 0), the lane's weight sum, and O^T += V^T P^T.
+template <int D, bool MASKED>
+__device__ __forceinline__ void att16_pv(Att16<D> &st, const f32x4 (&acc)[2], const bf16_t *__restrict__ Vl,
+                                         const Att16Addr<D> &ad, int nvalid) {
+  constexpr int RB = 2 * D;
+  const int g = (threadIdx.x & 63) >> 4;
+  float pv[8];
 #pragma unroll
-  for (int c = 0; c < NG; ++c) {
-    mx[c] = -INFINITY;
+  for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const bool ok = !MASKED || kb * 16 + 4 * g + r < nvalid;
-        mx[c] = fmaxf(mx[c], ok ? acc[c][kb][r] : -INFINITY);
-      }
-  }
-  if (!st.started || __ballot(mx[0] > RESCALE_LOG2 || mx[1] > RESCALE_LOG2)) {
-#pragma unroll
-    for (int c = 0; c < NG; ++c) {
-      const float cm = max_lane_groups(mx[c]);
-      // first tile: the reference becomes the column max (the accumulators
-      // are still zero); later: raised by the excess, only in a column past
-      // the threshold, so a query's arithmetic does not depend on the other
-      // queries of the tile
-      const float d = st.started ? (cm > RESCALE_LOG2 ? cm : 0.f) : cm;
-      st.nm[c] -= d;
-      if (st.started) {
-        const float alpha = __builtin_amdgcn_exp2f(-d);
-#pragma unroll
-        for (int i = 0; i < D / 16; ++i) st.o[c][i] *= alpha;
-        st.lsum[c] *= alpha;
-      }
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) acc[c][kb] -= d;
+    for (int r = 0; r < 4; ++r) {
+      float x = __builtin_amdgcn_exp2f(acc[kb][r]);
+      if (MASKED && kb * 16 + 4 * g + r >= nvalid) x = 0.f;
+      pv[4 * kb + r] = x;
     }
-    st.started = true;
-  }
-  const Frag<bf16_t> ones = ones_frag<bf16_t>();
-  Frag<bf16_t> b[2];
-#pragma unroll
-  for (int c = 0; c < NG; ++c) {
-    // reduction slice of group g: keys 32h + 4g + (0..3) and 32h + 16 + 4g + (0..3)
-    float pv[8];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float e = __builtin_amdgcn_exp2f(acc[c][kb][r]);
-        if (MASKED && kb * 16 + 4 * g + r >= nvalid) e = 0.f;
-        pv[4 * kb + r] = e;
-      }
-    b[c].from_f32(pv);
-    st.lsum[c] = mma(ones, b[c], st.lsum[c]);
-  }
-  // V^T fragments by transpose reads: lane (g, i = 4e + c) addresses piece c
-  // of key row 32h + 16 h2 + 4g + e, dimensions 16 db + 4c .. + 3
+  Frag<bf16_t> b;
+  b.from_f32(pv);
+  // the sum of the rounded weights, two at a time (a bf16 pair of ones as the
+  // other operand)
+  st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b.v.x), __builtin_bit_cast(bf16x2, 0x3f803f80u),
+                                         st.l, false);
+  st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b.v.y), __builtin_bit_cast(bf16x2, 0x3f803f80u),
+                                         st.l, false);
+  st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b.v.z), __builtin_bit_cast(bf16x2, 0x3f803f80u),
+                                         st.l, false);
+  st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b.v.w), __builtin_bit_cast(bf16x2, 0x3f803f80u),
+                                         st.l, false);
   const char *vbase = reinterpret_cast<const char *>(Vl);
-  const int e = p >> 2, c4 = p & 3;
 #pragma unroll
   for (int db = 0; db < D / 16; ++db) {
     uint2 half[2];
 #pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      const int Rv = 32 * h + 16 * h2 + 4 * g + e;
-      const char *addr = vbase + Rv * RB + (((2 * db + (c4 >> 1)) ^ swz(Rv)) << 4) + ((c4 & 1) << 3);
-      half[h2] = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)addr));
-    }
+    for (int h2 = 0; h2 < 2; ++h2)
+      half[h2] = __builtin_bit_cast(
+          uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(vbase + ad.v[db] + h2 * 16 * RB)));
     Frag<bf16_t> a;
     a.v = make_uint4(half[0].x, half[0].y, half[1].x, half[1].y);
-    st.o[0][db] = mma(a, b[0], st.o[0][db]);
-    if (NG > 1) st.o[1][db] = mma(a, b[1], st.o[1][db]);
+    st.o[db] = mma(a, b, st.o[db]);
   }
 }
 
-// One step of the DMA-staged tile loop: the DMA of the next tile into (Kn,
-// Vn) is issued (if `more`), then the wave's 32 keys of the current tile (Kc,
-// Vc) are multiplied (if `busy`). The buffers come in as restrict pointers, so the
-// compiler's alias information shows the reads of the current tile to be
-// disjoint from the DMA in flight and no wait for it is placed before them.
-template <int D, int NG, int ROWS = TK>
-__device__ __forceinline__ void dma_step(OnlineDma<D> &st, const bf16_t *__restrict__ Kc,
-                                         const bf16_t *__restrict__ Vc, bf16_t *__restrict__ Kn,
-                                         bf16_t *__restrict__ Vn, bool more, const bf16_t *kb, const bf16_t *vb,
-                                         const uint32_t *offs, bool busy, int h, const Frag<bf16_t> (&qf)[2][D / 32]) {
-  if (more) dma_tile<D, true, ROWS>(Kn, Vn, kb, vb, offs, ROWS);
-  if (busy) half_tile_dma<D, false, NG>(st, Kc, Vc, h, qf, 32);
+// Maximum of the lane's 8 shifted scores (with MASKED only keys < nvalid).
+template <bool MASKED> __device__ __forceinline__ float att16_lane_max(const f32x4 (&acc)[2], int nvalid) {
+  const int g = (threadIdx.x & 63) >> 4;
+  float mx = -INFINITY;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) mx = fmaxf(mx, (!MASKED || kb * 16 + 4 * g + r < nvalid) ? acc[kb][r] : -INFINITY);
+  return mx;
+}
+
+// The first tile of a wave: its column maxima become the references.
+template <int D, bool MASKED>
+__device__ __forceinline__ void att16_first(Att16<D> &st, const bf16_t *__restrict__ Kl, const bf16_t *__restrict__ Vl,
+                                            const Att16Addr<D> &ad, const Frag<bf16_t> (&qf)[D / 32], int nvalid) {
+#pragma unroll
+  for (int i = 0; i < D / 16; ++i) st.o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  st.nm = f32x4{0.f, 0.f, 0.f, 0.f};
+  st.l = 0.f;
+  f32x4 acc[2];
+  att16_scores<D>(acc, st, Kl, ad, qf);
+  const float cm = max_lane_groups(att16_lane_max<MASKED>(acc, nvalid));
+  st.nm -= cm;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) acc[kb] -= cm;
+  att16_pv<D, MASKED>(st, acc, Vl, ad, nvalid);
+}
+
+// A later tile, in two parts: att16_scores and the lane max, then, when
+// some column of the wave needs it (att16_needs_rescale), att16_rescale,
+// then att16_pv. The reference of a column moves (by its excess) only when
+// the column's shifted scores exceed RESCALE_LOG2, so a query's arithmetic
+// does not depend on the other queries of the wave.
+__device__ __forceinline__ bool att16_needs_rescale(float mx) { return __ballot(mx > RESCALE_LOG2) != 0; }
+
+template <int D> __device__ __forceinline__ void att16_rescale(Att16<D> &st, f32x4 (&acc)[2], float mx) {
+  const float cm = max_lane_groups(mx);
+  const float d = cm > RESCALE_LOG2 ? cm : 0.f;
+  const float alpha = __builtin_amdgcn_exp2f(-d);
+  st.nm -= d;
+#pragma unroll
+  for (int i = 0; i < D / 16; ++i) st.o[i] *= alpha;
+  st.l *= alpha;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) acc[kb] -= d;
+}
+
+template <int D, bool MASKED>
+__device__ __forceinline__ void att16_next(Att16<D> &st, const bf16_t *__restrict__ Kl, const bf16_t *__restrict__ Vl,
+                                           const Att16Addr<D> &ad, const Frag<bf16_t> (&qf)[D / 32], int nvalid) {
+  f32x4 acc[2];
+  att16_scores<D>(acc, st, Kl, ad, qf);
+  const float mx = att16_lane_max<MASKED>(acc, nvalid);
+  if (att16_needs_rescale(mx)) att16_rescale<D>(st, acc, mx);
+  att16_pv<D, MASKED>(st, acc, Vl, ad, nvalid);
+}
+
+// A later tile without the reference check: the weights exp2(s - m) may
+// exceed 2^8 when a score overshoots the first tile's column max; they stay
+// finite while the overshoot is below about 2^7 (log2 units), and
+// att16_finite tells afterwards whether they did.
+template <int D, bool MASKED>
+__device__ __forceinline__ void att16_plain(Att16<D> &st, const bf16_t *__restrict__ Kl, const bf16_t *__restrict__ Vl,
+                                            const Att16Addr<D> &ad, const Frag<bf16_t> (&qf)[D / 32], int nvalid) {
+  f32x4 acc[2];
+  att16_scores<D>(acc, st, Kl, ad, qf);
+  att16_pv<D, MASKED>(st, acc, Vl, ad, nvalid);
+}
+
+// Are the query's weight sum and accumulators finite? This lane's parts,
+// and'ed over the four lane groups of its column (the same answer in every
+// lane of the column).
+template <int D> __device__ __forceinline__ bool att16_finite(const Att16<D> &st) {
+  bool ok = __builtin_isfinite(st.l);
+#pragma unroll
+  for (int i = 0; i < D / 16; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ok = ok && __builtin_isfinite(st.o[i][j]);
+  const uint32_t x = ok ? 1u : 0u;
+  const auto a = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  const uint32_t pair = a[0] & a[1];
+  const auto b = __builtin_amdgcn_permlane32_swap(pair, pair, false, false);
+  return (b[0] & b[1]) != 0u;
+}
+
+// The query's weight sum: the four lane groups of its column added in a
+// fixed order (pairs (0, 1) and (2, 3), then both pairs), the same in every
+// lane of the column.
+template <int D> __device__ __forceinline__ float att16_sum(const Att16<D> &st) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(st.l), __float_as_uint(st.l), false, false);
+  const float pair = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(pair), __float_as_uint(pair), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // Register-staged copy of one 64-row K/V tile (software pipelining: the

@@ -885,76 +885,140 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
   const bool qvalid = qi < q_end;
   const int token = qvalid ? (ROUTED ? perm[bh * N + qi] : qi) : 0;
   const bool busy = q_begin + 16 * w < q_end;
-  Frag<bf16_t> qf[2][D / 32];  // group 1 stays empty (one group per wave)
+  Frag<bf16_t> qf[D / 32];
 #pragma unroll
   for (int ks = 0; ks < D / 32; ++ks) {
     if (qvalid)
-      qf[0][ks].load(q + (bh * N + token) * D + ks * 32 + g * 8);
+      qf[ks].load(q + (bh * N + token) * D + ks * 32 + g * 8);
     else
-      qf[0][ks].zero();
-    qf[1][ks].zero();
+      qf[ks].zero();
   }
-  OnlineDma<D> st;
-  st.init();
+  DmaLane<D, TK32> dl;
+  dl.init(w, lane);
   const bf16_t *kb, *vb;
   int off;
-  if (nfull > 0) {
-    tile_base(0, kb, vb, off);
-    dma_tile<D, true, TK32>(Ks(0), Vt(0), kb, vb, rows + off, TK32);
-  }
 
   // the score MFMAs take q * scale * log2 e (rounded to bf16)
   const float sl2 = scale * LOG2E;
 #pragma unroll
   for (int ks = 0; ks < D / 32; ++ks) {
     float x[8];
-    unpack16(qf[0][ks].v, x, (const bf16_t *)nullptr);
+    unpack16(qf[ks].v, x, (const bf16_t *)nullptr);
 #pragma unroll
     for (int j = 0; j < 8; ++j) x[j] *= sl2;
-    qf[0][ks].from_f32(x);
+    qf[ks].from_f32(x);
   }
+  Att16Addr<D> ad;
+  ad.init();
+  Att16<D> st;
   wait_loads();
   __syncthreads();
   // step i: the DMA of tile i + 1 into the other buffer is issued, tile i is
-  // multiplied, then the wave waits for its DMA and the workgroup meets
-  auto step = [&](int i, const bf16_t *Kc, const bf16_t *Vc, bf16_t *Kn, bf16_t *Vn) {
-    const bool more = i + 1 < nfull;
-    if (more) tile_base(i + 1, kb, vb, off);
-    dma_step<D, 1, TK32>(st, Kc, Vc, Kn, Vn, more, kb, vb, rows + off, busy, 0, qf);
-    wait_loads();
-    __syncthreads();
+  // multiplied, then the wave waits for its DMA and the workgroup meets.
+  // Tile i lives in buffer i & 1; the loop is unrolled by two (fixed buffer
+  // addresses). The first tile's column maxima are the references for every
+  // later tile: no per-tile check, so the loop carries no branch (a branch
+  // that redefines the softmax state makes the compiler move the state
+  // between two register sets on every tile). A wave without queries runs
+  // the same steps without the arithmetic, in a loop of its own for the
+  // same reason. If some weight then overflowed (a later score above the
+  // first tile's maximum by more than about 2^7 in log2 units), the whole
+  // workgroup runs its tiles once more with the reference check on every
+  // tile.
+  auto issue_next = [&](int i, bf16_t *Kn, bf16_t *Vn) {
+    if (i + 1 < nfull) {
+      tile_base(i + 1, kb, vb, off);
+      dma_tile_lane<D, TK32>(Kn, Vn, kb, vb, rows + off, dl);
+    }
   };
-  int i = 0;
-  for (; i + 1 < nfull; i += 2) {  // unrolled by two: fixed buffer addresses
-    step(i, Ks(0), Vt(0), Ks(1), Vt(1));
-    step(i + 1, Ks(1), Vt(1), Ks(0), Vt(0));
+  // mode 0: no arithmetic; 1: fixed references; 2: reference check per tile
+  auto run_tiles = [&](auto mode_c) {
+    constexpr int MODE = decltype(mode_c)::value;
+    auto tile = [&](const bf16_t *__restrict__ Kc, const bf16_t *__restrict__ Vc, bool first, int nv, auto masked_c) {
+      constexpr bool MK = decltype(masked_c)::value;
+      if (MODE == 0) return;
+      if (first)
+        att16_first<D, MK>(st, Kc, Vc, ad, qf, nv);
+      else if (MODE == 1)
+        att16_plain<D, MK>(st, Kc, Vc, ad, qf, nv);
+      else
+        att16_next<D, MK>(st, Kc, Vc, ad, qf, nv);
+    };
+    auto step = [&](int i, const bf16_t *__restrict__ Kc, const bf16_t *__restrict__ Vc, bf16_t *__restrict__ Kn,
+                    bf16_t *__restrict__ Vn) {
+      issue_next(i, Kn, Vn);
+      tile(Kc, Vc, false, TK32, std::false_type{});
+      wait_loads();
+      __syncthreads();
+    };
+    if (nfull > 0) {
+      dma_tile_lane<D, TK32>(Ks(0), Vt(0), nA > 0 ? sh_k : rkb, nA > 0 ? sh_v : rvb, rows + (nA > 0 ? 0 : nsh), dl);
+      wait_loads();
+      __syncthreads();
+      issue_next(0, Ks(1), Vt(1));
+      tile(Ks(0), Vt(0), true, TK32, std::false_type{});
+      wait_loads();
+      __syncthreads();
+      int i = 1;
+      for (; i + 1 < nfull; i += 2) {
+        step(i, Ks(1), Vt(1), Ks(0), Vt(0));
+        step(i + 1, Ks(0), Vt(0), Ks(1), Vt(1));
+      }
+      if (i < nfull) step(i, Ks(1), Vt(1), Ks(0), Vt(0));
+    }
+    // partial tiles (masked)
+    for (int part = 0; part < 2; ++part) {
+      const int nr = part == 0 ? pA : pB;
+      if (nr == 0) continue;  // uniform
+      if (part == 0)
+        dma_tile<D, false, TK32>(Ks(0), Vt(0), sh_k, sh_v, rows + nA * TK32, nr);
+      else
+        dma_tile<D, false, TK32>(Ks(0), Vt(0), rkb, rvb, rows + nsh + nB * TK32, nr);
+      wait_loads();
+      __syncthreads();
+      tile(Ks(0), Vt(0), nfull == 0 && (part == 0 || pA == 0), nr, std::true_type{});
+      __syncthreads();
+    }
+  };
+  if (busy)
+    run_tiles(std::integral_constant<int, 1>{});
+  else
+    run_tiles(std::integral_constant<int, 0>{});
+  // A query whose weights all stayed finite is written now; if any query of
+  // the workgroup overflowed, the workgroup runs its tiles again with the
+  // reference check on every tile and those queries are written from that
+  // run (each query's result thus depends only on its own column).
+  uint32_t *redo = sidx + nsh + (ROUTED ? k : 0);  // one word past the row list
+  if (threadIdx.x == 0) *redo = 0u;
+  __syncthreads();
+  bool done = true;
+  if (busy) {
+    done = att16_finite<D>(st);
+    if (__ballot(!done) && lane == 0) atomicOr(redo, 1u);
   }
-  if (i < nfull) step(i, Ks(0), Vt(0), Ks(1), Vt(1));
-  // partial tiles (masked)
-  for (int part = 0; part < 2; ++part) {
-    const int nr = part == 0 ? pA : pB;
-    if (nr == 0) continue;  // uniform
-    if (part == 0)
-      dma_tile<D, false, TK32>(Ks(0), Vt(0), sh_k, sh_v, rows + nA * TK32, nr);
+  auto write_out = [&]() {
+    const float inv = __builtin_amdgcn_rcpf(att16_sum<D>(st));
+    // the token is read again (the barriers in between keep the compiler
+    // from reusing the first read), so no address stays live across the
+    // tile loop
+    const int tok = ROUTED ? perm[bh * N + qi] : qi;
+    bf16_t *orow = o + (bh * N + tok) * D;
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) {
+      bf16_t vals[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) vals[r] = from_f32<bf16_t>(st.o[db][r] * inv);
+      *reinterpret_cast<uint2 *>(orow + db * 16 + 4 * g) = *reinterpret_cast<const uint2 *>(vals);
+    }
+  };
+  if (qvalid && done) write_out();
+  __syncthreads();
+  if (*redo) {  // uniform for the workgroup
+    if (busy)
+      run_tiles(std::integral_constant<int, 2>{});
     else
-      dma_tile<D, false, TK32>(Ks(0), Vt(0), rkb, rvb, rows + nsh + nB * TK32, nr);
-    wait_loads();
-    __syncthreads();
-    if (busy) half_tile_dma<D, true, 1>(st, Ks(0), Vt(0), 0, qf, nr);
-    __syncthreads();
-  }
-  if (!qvalid) return;
-  const float inv = __builtin_amdgcn_rcpf(st.l(0));
-  // the token is read again (the barriers in between keep the compiler from
-  // reusing the first read), so no address stays live across the tile loop
-  const int tok = ROUTED ? perm[bh * N + qi] : qi;
-  bf16_t *orow = o + (bh * N + tok) * D;
-#pragma unroll
-  for (int db = 0; db < D / 16; ++db) {
-    bf16_t vals[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) vals[r] = from_f32<bf16_t>(st.o[0][db][r] * inv);
-    *reinterpret_cast<uint2 *>(orow + db * 16 + 4 * g) = *reinterpret_cast<const uint2 *>(vals);
+      run_tiles(std::integral_constant<int, 0>{});
+    if (qvalid && !done) write_out();
   }
 }
 
@@ -1085,9 +1149,10 @@ static hipError_t attend_t3(const mita_cfg_t &c, const void *q, const void *q_lm
   const int nlist = (SH ? c.M : 0) + (RT ? c.k : 0);
   // the row list is staged in LDS when it and the kernel's tiles fit
   if constexpr (sizeof(T) == 2) {
-    // bf16: lists of up to IDX_LDS_MAX rows beside the 16 / 32 KB DMA tiles
-    if (list_in_lds(nlist, attend16_tiles_lds<D>())) {
-      hipLaunchKernelGGL((attend16_kernel<D, SH, RT, FU>), grid, dim3(BLOCK), (size_t)nlist * sizeof(int32_t), st,
+    // bf16: lists of up to IDX_LDS_MAX - 1 rows (and the kernel's rerun flag)
+    // beside the 16 / 32 KB DMA tiles
+    if (list_in_lds(nlist + 1, attend16_tiles_lds<D>())) {
+      hipLaunchKernelGGL((attend16_kernel<D, SH, RT, FU>), grid, dim3(BLOCK), (size_t)(nlist + 1) * sizeof(int32_t), st,
                          (const bf16_t *)q, (const bf16_t *)q_lm, (const bf16_t *)v_lm, (const bf16_t *)rk,
                          (const bf16_t *)rv, idx, perm, offsets, tile_start, (bf16_t *)o, c.N, c.M, c.k, eff_scale(c));
       return launched("attend16_kernel", st);

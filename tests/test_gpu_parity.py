@@ -611,6 +611,28 @@ def test_attention_does_not_depend_on_query_order_within_experts(name):
     assert _same(o1, o2)
 
 
+def test_attention_scores_far_above_the_first_tile():
+    """The attention keeps each query's first-tile maximum as its softmax
+    reference; a later score above it by more than about 2^7 (log2 units)
+    overflows a weight, and the workgroup then redoes its tiles with a
+    reference check on every tile. Keys scaled up 1000x in head 0 give the
+    queries routed to their experts scores about 150 above the first (shared)
+    tile: the outputs must still be finite and match the oracle, every row."""
+    wl = synth.WORKLOADS["vits_bf16"].with_(B=2, H=2)
+    inp = synth.generate(wl)
+    r = np.random.default_rng(3)
+    hot = r.choice(wl.N, 4, replace=False)
+    kb = synth.bf16_bits_to_f32(inp.k)
+    kb[0, 0, hot] *= 1000.0
+    inp = synth.Inputs(wl, inp.q, synth.f32_to_bf16_bits(kb), inp.v)
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = (to_dev(x, "bf16") for x in (inp.q, inp.k, inp.v))
+    o = mita.forward(cfg, q, k, v)
+    torch.cuda.synchronize()
+    assert torch.isfinite(o.float()).all()
+    _end_to_end(cfg, inp, q, k, v, [(0, 0)], row_limit=10 ** 9, grouped_slices=_all_slices(wl))
+
+
 def test_staged_gather_equals_in_place_gather():
     name = "vitb_hr_bf16"
     cfg = mita.Config.from_workload(_inputs(name).wl)
