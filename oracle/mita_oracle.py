@@ -22,11 +22,14 @@ Steps, in the order of Algorithm 1 (Appendix B):
   4. K^(i) = K[:, I_i], V^(i) = V[:, I_i]           (Eq. gather)
   5. v_lm_i = Atten(q_lm_i, K, V)                   (Eq. landmark-value)
   6. e(q) = argmax_i q . q_lm_i (routing logits Q^T Q_lm, Sec. 3.2)
-  7. MiTA(q) = V* softmax(K*^T q / sqrt(d)),  K* = [Q_lm, K^(e(q))],
-     V* = [V_lm, V^(e(q))]                          (Eq. mita, s = 1)
+  7. MiTA(q) = V* softmax(K*^T q / sqrt(d)),  K* = [Q_lm, K^(e_1(q)), ...,
+     K^(e_s(q))], V* likewise                       (Eq. mita)
 A second formulation (Algorithm 1's grouped form: shared-expert attention,
-varlen attention over queries grouped by expert, log-sum-exp combine) is
-provided for cross-checking step 7.
+varlen attention over queries grouped by expert, log-sum-exp combine; for
+s > 1 the expert-wise form with one partial per (query, expert) pair that
+Sec. 3.2 allows) is provided for cross-checking step 7.
+Landmark queries may also come from random selection of M tokens (Tab. A1),
+the draw being an input.
 
 Readings where the paper is silent or ambiguous (listed in the design doc):
   * pooling windows: start = floor(i*G/g), end = ceil((i+1)*G/g) per axis
@@ -39,7 +42,12 @@ Readings where the paper is silent or ambiguous (listed in the design doc):
   * routing: e(q) is the lowest landmark index attaining the maximum of
     (q . q_lm_i) / sqrt(d); counts are the bincount of e (minlength M),
     offsets = [0, cumsum(counts)], grouping is stable.
-  * s = 1 only.
+  * s > 1: e_j(q) is the j-th landmark in the order (larger logit first,
+    equal logits by lower landmark index); K* concatenates the s experts' key
+    sets as Eq. mita writes them (m + k s columns), so a key selected by two
+    of the query's experts enters the softmax twice.
+  * random selection: landmark i is the query of token sel[i], sel being M
+    distinct token indices supplied by the caller.
 """
 from __future__ import annotations
 
@@ -73,6 +81,16 @@ def landmarks(q: np.ndarray, grid_h: int, grid_w: int, lm_h: int, lm_w: int) -> 
         for b, (c0, c1) in enumerate(cols):
             out[a * lm_w + b] = grid[r0:r1, c0:c1, :].reshape(-1, d).mean(axis=0)
     return out
+
+
+def landmarks_random(q: np.ndarray, sel) -> np.ndarray:
+    """Random selection (Tab. A1, landmark extraction): landmark i is the
+    query of token sel[i]; sel [M] holds distinct token indices drawn by the
+    caller. Returns q_lm [M, d]."""
+    sel = np.asarray(sel, dtype=np.int64)
+    assert sel.ndim == 1 and len(np.unique(sel)) == len(sel)
+    assert sel.min() >= 0 and sel.max() < q.shape[0]
+    return q[sel].copy()
 
 
 # ----------------------------------------------------------------------------
@@ -139,6 +157,33 @@ def route(q: np.ndarray, q_lm: np.ndarray, scale: float) -> Routing:
     return routing_from_expert(expert, q_lm.shape[0])
 
 
+def route_top(q: np.ndarray, q_lm: np.ndarray, scale: float, s: int) -> np.ndarray:
+    """The s experts of every query (Sec. 3.2: e_j(q) is the rank-j expert
+    under the logits Q^T Q_lm): landmarks ordered by larger logit first, equal
+    logits by lower landmark index. Returns int64 [N, s], rank order."""
+    logits = (q @ q_lm.T) * scale               # [N, M]
+    N, M = logits.shape
+    assert 1 <= s <= M
+    out = np.empty((N, s), dtype=np.int64)
+    lm = np.arange(M)
+    for n in range(N):
+        order = np.lexsort((lm, -logits[n]))    # primary: -logit; secondary: landmark index
+        out[n] = order[:s]
+    return out
+
+
+def pair_grouping(experts: np.ndarray, M: int) -> Routing:
+    """Grouping of the (query, rank) pairs of s > 1 routing for the
+    expert-wise computation: pair p = n * s + j goes to group e_j(n) when
+    j = 0 (the pairs that also carry the shared expert) and to group
+    M + e_j(n) otherwise; groups are stable in the pair id. Returns a Routing
+    over the 2 M groups whose expert field holds the group of each pair."""
+    experts = np.asarray(experts, dtype=np.int64)
+    N, s = experts.shape
+    group = experts + M * (np.arange(s)[None, :] > 0)
+    return routing_from_expert(group.reshape(-1), 2 * M)
+
+
 def routing_from_expert(expert: np.ndarray, M: int) -> Routing:
     expert = np.asarray(expert, dtype=np.int64)
     counts = np.bincount(expert, minlength=M)
@@ -148,12 +193,19 @@ def routing_from_expert(expert: np.ndarray, M: int) -> Routing:
 
 
 # ----------------------------------------------------------------------------
-# Step 7: the MiTA output (Eq. mita with s = 1), per query.
+# Step 7: the MiTA output (Eq. mita), per query.
 # ----------------------------------------------------------------------------
+def _experts_2d(expert) -> np.ndarray:
+    e = np.asarray(expert, dtype=np.int64)
+    return e[:, None] if e.ndim == 1 else e
+
+
 def output_per_query(q, q_lm, v_lm, kx, vx, expert, scale, use_shared=1, use_routed=1):
-    """o_n = V* softmax(K*^T q_n * scale) with K* = [q_lm ; kx[e(n)]] and
-    V* = [v_lm ; vx[e(n)]] (either part dropped by its flag)."""
+    """o_n = V* softmax(K*^T q_n * scale) with K* = [q_lm ; kx[e_1(n)] ; ... ;
+    kx[e_s(n)]] and V* likewise (either part dropped by its flag); expert is
+    [N] (s = 1) or [N, s] in rank order."""
     N, d = q.shape
+    ex = _experts_2d(expert)
     o = np.empty((N, d), dtype=q.dtype)
     for n in range(N):
         keys, vals = [], []
@@ -161,8 +213,9 @@ def output_per_query(q, q_lm, v_lm, kx, vx, expert, scale, use_shared=1, use_rou
             keys.append(q_lm)
             vals.append(v_lm)
         if use_routed:
-            keys.append(kx[expert[n]])
-            vals.append(vx[expert[n]])
+            for e in ex[n]:
+                keys.append(kx[e])
+                vals.append(vx[e])
         Ks = np.concatenate(keys, axis=0)
         Vs = np.concatenate(vals, axis=0)
         p = softmax_rows((Ks @ q[n]) * scale)
@@ -208,6 +261,46 @@ def output_grouped(q, q_lm, v_lm, kx, vx, routing: Routing, scale, use_shared=1,
     return (w1 * o1 + w2 * o2) / (w1 + w2)
 
 
+def output_pairs(q, q_lm, v_lm, kx, vx, experts, scale, use_shared=1, use_routed=1):
+    """The expert-wise form of Eq. mita for s >= 1 (Sec. 3.2: attention
+    computed per expert and combined by online softmax): for every expert,
+    attention of the (query, rank) pairs routed to it over its k keys, each
+    pair keeping its log-sum-exp; the shared-expert attention of every query
+    likewise; each query's s + 1 partials combined with weights
+    exp(lse - max lse). Returns o [N, d]."""
+    N, d = q.shape
+    ex = _experts_2d(experts)
+    s = ex.shape[1]
+    outs, lses = [], []
+    if use_shared:
+        z = (q @ q_lm.T) * scale
+        mx = z.max(axis=1, keepdims=True)
+        w = np.exp(z - mx)
+        sm = w.sum(axis=1, keepdims=True)
+        outs.append((w @ v_lm) / sm)
+        lses.append((mx + np.log(sm))[:, 0])
+    if use_routed:
+        for j in range(s):
+            o_j = np.empty((N, d))
+            l_j = np.empty(N)
+            for e in range(q_lm.shape[0]):
+                rows = np.nonzero(ex[:, j] == e)[0]
+                if len(rows) == 0:
+                    continue
+                z = (q[rows] @ kx[e].T) * scale
+                mx = z.max(axis=1, keepdims=True)
+                w = np.exp(z - mx)
+                sm = w.sum(axis=1, keepdims=True)
+                o_j[rows] = (w @ vx[e]) / sm
+                l_j[rows] = (mx + np.log(sm))[:, 0]
+            outs.append(o_j)
+            lses.append(l_j)
+    L = np.stack(lses, axis=1)                          # [N, parts]
+    wts = np.exp(L - L.max(axis=1, keepdims=True))
+    num = sum(wts[:, i:i + 1] * outs[i] for i in range(len(outs)))
+    return num / wts.sum(axis=1, keepdims=True)
+
+
 def effective_weights(q, k, q_lm, S, idx, expert, scale, use_shared=1, use_routed=1):
     """W [N, N] with o = W v: the shared part spreads landmark j's weight over
     the keys through softmax(S[j, :]) (Eq. landmark-value), the routed part puts
@@ -216,19 +309,23 @@ def effective_weights(q, k, q_lm, S, idx, expert, scale, use_shared=1, use_route
     A = softmax_rows(S)
     W = np.zeros((N, N))
     M = q_lm.shape[0]
+    ex = _experts_2d(expert)
     for n in range(N):
         z = []
         if use_shared:
             z.append((q_lm @ q[n]) * scale)
         if use_routed:
-            z.append((k[idx[expert[n]]] @ q[n]) * scale)
+            for e in ex[n]:
+                z.append((k[idx[e]] @ q[n]) * scale)
         p = softmax_rows(np.concatenate(z))
         j = 0
         if use_shared:
             W[n] += p[:M] @ A
             j = M
         if use_routed:
-            np.add.at(W[n], idx[expert[n]], p[j:])
+            for e in ex[n]:                              # repeated keys add up
+                np.add.at(W[n], idx[e], p[j:j + idx.shape[1]])
+                j += idx.shape[1]
     return W
 
 
@@ -241,49 +338,56 @@ class SliceResult:
     S: np.ndarray
     idx: np.ndarray
     v_lm: np.ndarray
-    routing: Routing
+    routing: Routing        # grouping by the rank-1 expert
     o: np.ndarray
+    experts: np.ndarray     # [N, s] routed experts in rank order
 
 
 def forward_slice(q, k, v, grid_h, grid_w, lm_h, lm_w, topk, scale=None,
                   use_shared=1, use_routed=1, force_idx=None, force_expert=None,
-                  rows=None) -> SliceResult:
+                  rows=None, s=1, lm_sel=None, q_lm=None) -> SliceResult:
     """One (b, h) slice of the forward. force_idx / force_expert replace the
     oracle's own selection / routing (to compare outputs given another
-    implementation's discrete choices). rows: compute o only for these tokens
-    (o is then [len(rows), d])."""
+    implementation's discrete choices; force_expert is [N] or [N, s]). rows:
+    compute o only for these tokens (o is then [len(rows), d]). s: routed
+    experts per query. Landmarks come from pooling, or from random selection
+    when lm_sel (the M drawn token indices) is given, or are q_lm when given."""
     N, d = q.shape
     if scale is None:
         scale = float(1.0 / np.sqrt(d))
-    q_lm = landmarks(q, grid_h, grid_w, lm_h, lm_w)
+    if q_lm is None:
+        q_lm = landmarks(q, grid_h, grid_w, lm_h, lm_w) if lm_sel is None else landmarks_random(q, lm_sel)
     S = scores(q_lm, k, scale)
     idx = topk_indices(S, topk) if force_idx is None else np.asarray(force_idx, dtype=np.int64)
     v_lm = landmark_values(S, v)
     if force_expert is None:
-        routing = route(q, q_lm, scale)
+        experts = route(q, q_lm, scale).expert[:, None] if s == 1 else route_top(q, q_lm, scale, s)
     else:
-        routing = routing_from_expert(force_expert, q_lm.shape[0])
+        experts = _experts_2d(force_expert)
+    routing = routing_from_expert(experts[:, 0], q_lm.shape[0])
     kx, vx = gather(k, v, idx)
     if rows is None:
-        o = output_per_query(q, q_lm, v_lm, kx, vx, routing.expert, scale, use_shared, use_routed)
+        o = output_per_query(q, q_lm, v_lm, kx, vx, experts, scale, use_shared, use_routed)
     else:
         rows = np.asarray(rows)
-        o = output_per_query(q[rows], q_lm, v_lm, kx, vx, routing.expert[rows], scale,
+        o = output_per_query(q[rows], q_lm, v_lm, kx, vx, experts[rows], scale,
                              use_shared, use_routed)
-    return SliceResult(q_lm, S, idx, v_lm, routing, o)
+    return SliceResult(q_lm, S, idx, v_lm, routing, o, experts)
 
 
 def forward(q, k, v, grid_h, grid_w, lm_h, lm_w, topk, scale=None, use_shared=1,
-            use_routed=1):
-    """q, k, v: [B, H, N, d] float64. Returns o [B, H, N, d] and the per-slice
-    results (a list in (b, h) order)."""
+            use_routed=1, s=1, lm_sel=None):
+    """q, k, v: [B, H, N, d] float64; lm_sel: [B, H, M] random-selection
+    draws or None (pooling). Returns o [B, H, N, d] and the per-slice results
+    (a list in (b, h) order)."""
     B, H, N, d = q.shape
     o = np.empty((B, H, N, d))
     res = []
     for b in range(B):
         for h in range(H):
             r = forward_slice(q[b, h], k[b, h], v[b, h], grid_h, grid_w, lm_h, lm_w,
-                              topk, scale, use_shared, use_routed)
+                              topk, scale, use_shared, use_routed, s=s,
+                              lm_sel=None if lm_sel is None else lm_sel[b, h])
             o[b, h] = r.o
             res.append(r)
     return o, res

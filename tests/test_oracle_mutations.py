@@ -77,3 +77,68 @@ def test_planted_mistake_is_caught(monkeypatch, name, mutant, pin):
     monkeypatch.setattr(O, name, mutant)
     with pytest.raises(AssertionError):
         pin()
+
+
+# ---------------------------------------------------------------- s > 1 and random landmarks
+from tests import test_oracle_pins_variants as PV  # noqa: E402
+
+
+def _route_top_ties_high(q, q_lm, scale, s):
+    z = (q @ q_lm.T) * scale
+    M = z.shape[1]
+    return np.stack([np.lexsort((-np.arange(M), -z[n]))[:s] for n in range(z.shape[0])])
+
+
+def _route_top_smallest(q, q_lm, scale, s):
+    z = (q @ q_lm.T) * scale
+    return np.argsort(z, axis=1, kind="stable")[:, :s]
+
+
+def _out_union_of_experts(q, q_lm, v_lm, kx, vx, expert, scale, use_shared=1, use_routed=1):
+    # a plausible misreading: the union of the experts' keys, duplicates dropped
+    e = np.asarray(expert)
+    if e.ndim == 1:
+        return _orig_out(q, q_lm, v_lm, kx, vx, expert, scale, use_shared, use_routed)
+    o = np.empty_like(q)
+    flat_k = kx.reshape(-1, kx.shape[-1])
+    for n in range(q.shape[0]):
+        rows = np.unique(np.concatenate([np.arange(kx.shape[1]) + kx.shape[1] * x for x in e[n]]))
+        keys = [q_lm] if use_shared else []
+        vals = [v_lm] if use_shared else []
+        kk = flat_k[rows]
+        keys.append(kk)
+        vals.append(vx.reshape(-1, vx.shape[-1])[rows])
+        # drop rows whose key vector repeats an earlier one
+        Ks = np.concatenate(keys)
+        _, first = np.unique(Ks, axis=0, return_index=True)
+        first = np.sort(first)
+        z = (Ks[first] @ q[n]) * scale
+        p = np.exp(z - z.max())
+        o[n] = (p / p.sum()) @ np.concatenate(vals)[first]
+    return o
+
+
+def _out_first_expert_only(q, q_lm, v_lm, kx, vx, expert, scale, use_shared=1, use_routed=1):
+    e = np.asarray(expert)
+    return _orig_out(q, q_lm, v_lm, kx, vx, e if e.ndim == 1 else e[:, 0], scale, use_shared, use_routed)
+
+
+def _landmarks_random_sorted(q, sel):
+    return q[np.sort(np.asarray(sel))].copy()
+
+
+MUTANTS_VARIANTS = [
+    ("route_top", _route_top_ties_high, lambda: PV.test_route_top_ties_go_to_the_lower_landmark()),
+    ("route_top", _route_top_smallest, lambda: PV.test_route_top_bruteforce(0, 2)),
+    ("output_per_query", _out_union_of_experts, lambda: PV.test_duplicate_keys_count_once_per_expert(2)),
+    ("output_per_query", _out_first_expert_only, lambda: PV.test_shared_and_routed_k_eq_N_weighs_keys_s_times(2)),
+    ("landmarks_random", _landmarks_random_sorted, lambda: PV.test_random_selection_picks_the_drawn_queries()),
+]
+
+
+@pytest.mark.parametrize("name,mutant,pin", MUTANTS_VARIANTS, ids=[m[1].__name__ for m in MUTANTS_VARIANTS])
+def test_planted_mistake_in_a_variant_is_caught(monkeypatch, name, mutant, pin):
+    pin()
+    monkeypatch.setattr(O, name, mutant)
+    with pytest.raises(AssertionError):
+        pin()
