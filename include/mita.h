@@ -2,16 +2,18 @@
  * mita.h - C ABI of the MI355X (gfx950) MiTA forward library.
  *
  * Mixture-of-Top-k Attention (arXiv 2602.01219, Sec. 3.2 and Algorithm 1 in
- * Appendix B), forward pass, one routed expert per query (s = 1):
+ * Appendix B), forward pass, s routed experts per query:
  *
  *   q_lm  = AdaptiveAvgPool(Q)                 landmark queries  (Sec. 3.2; Tab. A1)
  *   S     = K^T q_lm / sqrt(d)                 landmark-key scores (Eq. top-k; Alg. 1)
  *   I_i   = Top_k(S[i, :])                     expert key sets     (Eq. top-k)
  *   K^(i), V^(i) = K[:, I_i], V[:, I_i]        expert tiles        (Eq. gather)
  *   v_lm_i = Atten(q_lm_i, K, V)               landmark values     (Eq. landmark-value)
- *   e(q)  = argmax_i q . q_lm_i                routing             (Sec. 3.2, routing logits)
- *   o     = V* softmax(K*^T q / sqrt(d)),  K* = [q_lm, K^(e(q))],
- *           V* = [v_lm, V^(e(q))]              output              (Eq. mita; Eq. shared-expert)
+ *   e_j(q) = rank-j landmark under q . q_lm_i  routing             (Sec. 3.2, routing logits)
+ *   o     = V* softmax(K*^T q / sqrt(d)),  K* = [q_lm, K^(e_1(q)), ..., K^(e_s(q))],
+ *           V* likewise                        output              (Eq. mita; Eq. shared-expert)
+ * Landmark queries may instead be picked by random selection (Tab. A1) or be
+ * supplied by the caller (mita_landmarks_select, mita_forward_lm).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -53,7 +55,7 @@ extern "C" {
 /* Status codes. */
 #define MITA_OK 0
 #define MITA_ERR_INVALID_ARG 1   /* bad sizes/grids, k or M out of [1, N], null or misaligned pointer, o aliasing an input, both branches off */
-#define MITA_ERR_UNSUPPORTED 2   /* d not in {64, 128}; s != 1; unknown dtype; N beyond the supported maximum */
+#define MITA_ERR_UNSUPPORTED 2   /* d not in {64, 128}; s outside [1, MITA_MAX_S]; unknown dtype; N beyond the supported maximum */
 #define MITA_ERR_WORKSPACE 3     /* ws_bytes smaller than mita_workspace_size() */
 #define MITA_ERR_HIP 4           /* a HIP runtime or launch failure; see mita_last_error() */
 
@@ -71,19 +73,24 @@ extern "C" {
 
 /* Largest sequence length the library accepts. */
 #define MITA_MAX_N 65536
+/* Largest number of routed experts per query. */
+#define MITA_MAX_S 4
 
 typedef void *mita_stream_t; /* a hipStream_t */
 
 /*
  * Problem description (Algorithm 1 "Require": Q, K, V in R^{d x N}, the number of
- * landmark queries m, the expert width k, s = 1 routed expert per query).
+ * landmark queries m, the expert width k; s routed experts per query, Eq. mita).
  */
 typedef struct {
   int32_t B, H, N, d;      /* batch, heads, tokens, head dim; d in {64, 128} */
   int32_t grid_h, grid_w;  /* token grid, grid_h * grid_w == N; grid_h == 1 gives 1-D pooling */
   int32_t M, lm_h, lm_w;   /* landmarks (the paper's m), lm_h * lm_w == M, lm_h <= grid_h, lm_w <= grid_w */
   int32_t k;               /* expert width, 1 <= k <= N */
-  int32_t s;               /* routed experts per query; must be 1 (Sec. 3.2 implementation) */
+  int32_t s;               /* routed experts per query, 1 <= s <= MITA_MAX_S and s <= M (Eq. mita; the paper
+                              runs s = 1). With s > 1 the keys of the s experts are concatenated as
+                              Eq. mita writes them: a key two of a query's experts select counts twice.
+                              Ignored when use_routed == 0. */
   int32_t use_shared;      /* shared expert (Eq. shared-expert): landmarks as keys, landmark values as values */
   int32_t use_routed;      /* routed top-k expert (Eq. mita-expert); at least one of the two must be set */
   int32_t dtype;           /* MITA_F32 or MITA_BF16 */
@@ -111,9 +118,12 @@ const char *mita_status_string(int status);
 const char *mita_last_error(void);
 
 /*
- * The whole forward (Algorithm 1 with s = 1; output Eq. mita).
+ * The whole forward (Algorithm 1; output Eq. mita).
  *   q, k, v : [B, H, N, d] inputs;  o : [B, H, N, d] output (must not overlap q, k, v).
  *   ws      : >= mita_workspace_size(cfg, MITA_WS_FORWARD) bytes.
+ * With s > 1 the attention runs expert by expert and the s partial results of
+ * each query are merged by their log-sum-exp (the expert-wise evaluation of
+ * Eq. mita that Sec. 3.2 allows); the shared expert goes with the rank-1 one.
  * The top-k sets are those mita_topk computes from mita_scores' S (bit for
  * bit), but S is normally not stored: a pivot estimated from a sample of
  * each score row bounds the row's top-k from below, the score pass lists
@@ -174,6 +184,29 @@ int mita_select_plan(const mita_cfg_t *cfg, int32_t *fused, int32_t *ns, int32_t
 int mita_landmarks(const mita_cfg_t *cfg, const void *q, void *q_lm, mita_stream_t stream);
 
 /*
+ * Landmark queries by random selection (Tab. A1, landmark extraction): the
+ * caller draws the tokens, landmark i of slice (b, h) is the query of token
+ * sel[b, h, i].
+ *   q   : [B, H, N, d];  sel : [B, H, M] int32, entries in [0, N) (distinct, as
+ *         the selection draws them; repeats are not rejected);
+ *   q_lm : [B, H, M, d] output (copied rows). An entry outside [0, N) gives a
+ *         row of NaN (nothing is read for it).
+ */
+int mita_landmarks_select(const mita_cfg_t *cfg, const void *q, const int32_t *sel, void *q_lm,
+                          mita_stream_t stream);
+
+/*
+ * mita_forward with caller-supplied landmark queries (random selection, or any
+ * other extraction): every step of Algorithm 1 after AdaptiveAvgPool, with
+ * q_lm in its place. lm_h, lm_w, grid_h and grid_w are validated as for
+ * mita_forward but not otherwise used.
+ *   q_lm : [B, H, M, d] input;  q, k, v, o, ws : as mita_forward
+ *          (ws >= mita_workspace_size(cfg, MITA_WS_FORWARD) bytes).
+ */
+int mita_forward_lm(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, const void *q_lm,
+                    void *o, void *ws, size_t ws_bytes, mita_stream_t stream);
+
+/*
  * Landmark-key scores and landmark values, computed together (Sec. 3.2 notes
  * Eq. top-k and Eq. landmark-value share K^T q_lm).
  *   q_lm   : [B, H, M, d] landmark queries;  k, v : [B, H, N, d].
@@ -202,27 +235,37 @@ int mita_gather(const mita_cfg_t *cfg, const void *k, const void *v, const int32
                 void *k_x, void *v_x, mita_stream_t stream);
 
 /*
- * Routing (Sec. 3.2: logits Q^T q_lm, rank-1 expert e(q); Algorithm 1 ArgMax,
- * ArgSort, BinCount, CumSum). expert[n] is the lowest i attaining the maximum
- * of fl(q_n . q_lm_i) * scale. Queries are grouped by expert, stably.
+ * Routing (Sec. 3.2: logits Q^T q_lm, rank-j expert e_j(q); Algorithm 1 ArgMax,
+ * ArgSort, BinCount, CumSum). With s = 1, expert[n] is the lowest i attaining
+ * the maximum of fl(q_n . q_lm_i) * scale and queries are grouped by expert,
+ * stably:
  *   q : [B, H, N, d];  q_lm : [B, H, M, d].
  *   expert  : [B, H, N] int32 output;
  *   perm    : [B, H, N] int32 output, tokens of expert 0, then expert 1, ..., ascending inside a group;
  *   offsets : [B, H, M+1] int32 output, offsets[0] = 0, offsets[M] = N, group i = perm[offsets[i] : offsets[i+1]].
+ * With s > 1, expert[n, j] is the landmark of rank j when landmarks are
+ * ordered by larger fl(q_n . q_lm_i) * scale, equal values by lower i; the
+ * (query, rank) pairs p = n * s + j are grouped into 2 M groups: pair p goes
+ * to group expert[n, j] if j = 0 and to group M + expert[n, j] otherwise,
+ * stably in p:
+ *   expert  : [B, H, N, s] int32 output;
+ *   perm    : [B, H, N * s] int32 output, pair ids grouped as above;
+ *   offsets : [B, H, 2M+1] int32 output, offsets[2M] = N * s.
  *   ws      : >= mita_workspace_size(cfg, MITA_WS_ROUTE) bytes.
  */
 int mita_route(const mita_cfg_t *cfg, const void *q, const void *q_lm, int32_t *expert,
                int32_t *perm, int32_t *offsets, void *ws, size_t ws_bytes, mita_stream_t stream);
 
 /*
- * Attention of every query over the shared expert and its routed expert, as
- * one softmax over the concatenated keys (Eq. mita, s = 1; Algorithm 1's
+ * Attention of every query over the shared expert and its s routed experts,
+ * as one softmax over the concatenated keys (Eq. mita; Algorithm 1's
  * shared-expert attention, varlen expert attention and online-softmax combine).
  *   q : [B, H, N, d];  q_lm, v_lm : [B, H, M, d] (read if use_shared);
  *   k_x, v_x : [B, H, M, k, d] expert tiles (read if use_routed);
- *   perm, offsets : routing as produced by mita_route (read if use_routed);
+ *   perm, offsets : routing as produced by mita_route for the same s (read if use_routed);
  *   o : [B, H, N, d] output in token order.
- *   ws : >= mita_workspace_size(cfg, MITA_WS_ATTEND) bytes.
+ *   ws : >= mita_workspace_size(cfg, MITA_WS_ATTEND) bytes (with s > 1 it holds the
+ *        fp32 partial result and log-sum-exp of every (query, expert) pair).
  */
 int mita_attend(const mita_cfg_t *cfg, const void *q, const void *q_lm, const void *v_lm,
                 const void *k_x, const void *v_x, const int32_t *perm, const int32_t *offsets,

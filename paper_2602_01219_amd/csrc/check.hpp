@@ -38,7 +38,14 @@ inline size_t align_up(size_t x) { return (x + WS_ALIGN - 1) / WS_ALIGN * WS_ALI
 inline size_t elem_bytes(const mita_cfg_t &c) { return c.dtype == MITA_F32 ? 4 : 2; }
 inline int64_t BH(const mita_cfg_t &c) { return (int64_t)c.B * c.H; }
 inline int score_chunks(const mita_cfg_t &c) { return (c.N + SCORE_NC - 1) / SCORE_NC; }
-inline int route_tiles(const mita_cfg_t &c) { return (c.N + ROUTE_TQ - 1) / ROUTE_TQ; }
+// Routing items: the queries (s = 1) or the (query, rank) pairs n * s + j
+// (s > 1), grouped into M groups (s = 1) or 2 M (s > 1: group e holds the
+// rank-1 pairs of expert e, group M + e its other pairs).
+inline int route_s(const mita_cfg_t &c) { return c.use_routed ? c.s : 1; }
+inline bool multi_route(const mita_cfg_t &c) { return route_s(c) > 1; }
+inline int route_items(const mita_cfg_t &c) { return c.N * route_s(c); }
+inline int route_groups(const mita_cfg_t &c) { return multi_route(c) ? 2 * c.M : c.M; }
+inline int route_tiles(const mita_cfg_t &c) { return (route_items(c) + ROUTE_TQ - 1) / ROUTE_TQ; }
 inline float eff_scale(const mita_cfg_t &c) { return c.scale != 0.f ? c.scale : 1.0f / std::sqrt((float)c.d); }
 
 // ---------------------------------------------------------------------------
@@ -182,7 +189,7 @@ inline int check_cfg(const mita_cfg_t *c, std::string *err) {
   if (c->B < 1 || c->H < 1 || c->N < 1 || c->d < 1) return fail(MITA_ERR_INVALID_ARG, "B, H, N, d must be >= 1");
   if (c->dtype != MITA_F32 && c->dtype != MITA_BF16) return fail(MITA_ERR_UNSUPPORTED, "dtype must be MITA_F32 or MITA_BF16");
   if (c->d != 64 && c->d != 128) return fail(MITA_ERR_UNSUPPORTED, "d must be 64 or 128");
-  if (c->s != 1) return fail(MITA_ERR_UNSUPPORTED, "only s = 1 routed expert per query is supported");
+  if (c->s < 1 || c->s > MITA_MAX_S) return fail(MITA_ERR_UNSUPPORTED, "s must be in [1, MITA_MAX_S]");
   if (c->grid_h < 1 || c->grid_w < 1 || (int64_t)c->grid_h * c->grid_w != c->N)
     return fail(MITA_ERR_INVALID_ARG, "grid_h * grid_w must equal N");
   if (c->lm_h < 1 || c->lm_w < 1 || (int64_t)c->lm_h * c->lm_w != c->M)
@@ -194,6 +201,7 @@ inline int check_cfg(const mita_cfg_t *c, std::string *err) {
   if (c->use_routed != 0 && c->use_routed != 1) return fail(MITA_ERR_INVALID_ARG, "use_routed must be 0 or 1");
   if (!c->use_shared && !c->use_routed) return fail(MITA_ERR_INVALID_ARG, "use_shared and use_routed are both 0");
   if (c->k < 1 || c->k > c->N) return fail(MITA_ERR_INVALID_ARG, "k must be in [1, N]");
+  if (c->use_routed && c->s > c->M) return fail(MITA_ERR_INVALID_ARG, "s must not exceed M");
   if (c->N > MITA_MAX_N) {
     snprintf(buf, sizeof buf, "N = %d exceeds the supported maximum %d", c->N, MITA_MAX_N);
     return fail(MITA_ERR_UNSUPPORTED, buf);
@@ -209,7 +217,7 @@ inline int check_cfg(const mita_cfg_t *c, std::string *err) {
 // Workspace layout of mita_forward (offsets in bytes; 0-sized pieces allowed).
 struct FwdLayout {
   size_t q_lm, v_lm, scores, partial, idx, kx, vx, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start,
-      plo, ccnt, cand, fail, total;
+      group, pair_o, pair_lse, plo, ccnt, cand, fail, total;
 };
 
 inline size_t scores_ws_bytes(const mita_cfg_t &c) {
@@ -217,16 +225,35 @@ inline size_t scores_ws_bytes(const mita_cfg_t &c) {
   const size_t rows = (size_t)BH(c) * score_chunks(c) * c.M;
   return align_up(rows * 2 * sizeof(float)) + align_up(rows * c.d * sizeof(float));
 }
-// Routing scratch: per-tile expert counts, per-tile scatter bases, per-expert
-// totals and the attention work list, in that order.
+// Routing scratch: per-tile group counts, per-tile scatter bases, per-group
+// totals, the attention work list and (s > 1) the group of every pair, in
+// that order.
 inline size_t route_tiles_bytes(const mita_cfg_t &c) {
-  return align_up((size_t)BH(c) * route_tiles(c) * c.M * sizeof(int32_t));
+  return align_up((size_t)BH(c) * route_tiles(c) * route_groups(c) * sizeof(int32_t));
+}
+inline size_t route_counts_bytes(const mita_cfg_t &c) {
+  return align_up((size_t)BH(c) * route_groups(c) * sizeof(int32_t));
+}
+inline size_t route_start_bytes(const mita_cfg_t &c) {
+  return align_up((size_t)BH(c) * (route_groups(c) + 1) * sizeof(int32_t));
+}
+inline size_t route_group_bytes(const mita_cfg_t &c) {
+  return multi_route(c) ? align_up((size_t)BH(c) * route_items(c) * sizeof(int32_t)) : 0;
 }
 inline size_t route_ws_bytes(const mita_cfg_t &c) {
-  return 2 * route_tiles_bytes(c) + align_up((size_t)BH(c) * c.M * sizeof(int32_t)) +
-         align_up((size_t)BH(c) * (c.M + 1) * sizeof(int32_t));
+  return 2 * route_tiles_bytes(c) + route_counts_bytes(c) + route_start_bytes(c) + route_group_bytes(c);
 }
-inline size_t attend_ws_bytes(const mita_cfg_t &c) { return align_up((size_t)BH(c) * (c.M + 1) * sizeof(int32_t)); }
+// s > 1: the fp32 partial result and the log-sum-exp (log2 units) of every pair
+inline size_t pair_out_bytes(const mita_cfg_t &c) {
+  return multi_route(c) ? align_up((size_t)BH(c) * route_items(c) * c.d * sizeof(float)) : 0;
+}
+inline size_t pair_lse_bytes(const mita_cfg_t &c) {
+  return multi_route(c) ? align_up((size_t)BH(c) * route_items(c) * sizeof(float)) : 0;
+}
+// attention scratch: the work list, then (s > 1) the pair partials
+inline size_t attend_ws_bytes(const mita_cfg_t &c) {
+  return route_start_bytes(c) + pair_out_bytes(c) + pair_lse_bytes(c);
+}
 
 inline FwdLayout forward_layout(const mita_cfg_t &c) {
   FwdLayout L{};
@@ -246,13 +273,17 @@ inline FwdLayout forward_layout(const mita_cfg_t &c) {
   const bool staged = c.use_routed && (c.flags & MITA_FLAG_STAGED_GATHER);
   L.kx = take(staged ? bh * c.M * (size_t)c.k * c.d * e : 0);
   L.vx = take(staged ? bh * c.M * (size_t)c.k * c.d * e : 0);
-  L.expert = take(c.use_routed ? bh * c.N * 4 : 0);
-  L.perm = take(c.use_routed ? bh * c.N * 4 : 0);
-  L.offsets = take(c.use_routed ? bh * (c.M + 1) * 4 : 0);
-  L.tile_cnt = take(c.use_routed ? bh * route_tiles(c) * c.M * 4 : 0);
-  L.tile_base = take(c.use_routed ? bh * route_tiles(c) * c.M * 4 : 0);
-  L.counts = take(c.use_routed ? bh * c.M * 4 : 0);
-  L.tile_start = take(c.use_routed ? bh * (c.M + 1) * 4 : 0);
+  const size_t items = (size_t)route_items(c), groups = (size_t)route_groups(c);
+  L.expert = take(c.use_routed ? bh * items * 4 : 0);
+  L.perm = take(c.use_routed ? bh * items * 4 : 0);
+  L.offsets = take(c.use_routed ? bh * (groups + 1) * 4 : 0);
+  L.tile_cnt = take(c.use_routed ? bh * route_tiles(c) * groups * 4 : 0);
+  L.tile_base = take(c.use_routed ? bh * route_tiles(c) * groups * 4 : 0);
+  L.counts = take(c.use_routed ? bh * groups * 4 : 0);
+  L.tile_start = take(c.use_routed ? bh * (groups + 1) * 4 : 0);
+  L.group = take(route_group_bytes(c));
+  L.pair_o = take(pair_out_bytes(c));
+  L.pair_lse = take(pair_lse_bytes(c));
   // fused selection: pivots, candidate counts and lists,
   // then the fallback counter followed by the fallback row list
   const bool fs = fused_select(c);

@@ -69,9 +69,11 @@ hipError_t launch_gather(const mita_cfg_t &c, const void *k, const void *v, cons
 
 // Routing: expert [BH,N], per-tile counts and bases, offsets [BH,M+1], perm [BH,N],
 // attention work list tile_start [BH,M+1]. counts [BH,M] must be zero on entry.
+// With s > 1: expert [BH,N,s], the pairs' groups in group [BH,N*s], perm [BH,N*s],
+// offsets and tile_start [BH,2M+1], counts [BH,2M] (zeroed here).
 hipError_t launch_route(const mita_cfg_t &c, const void *q, const void *q_lm, int32_t *expert, int32_t *perm,
                         int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, int32_t *counts,
-                        int32_t *tile_start, hipStream_t st);
+                        int32_t *tile_start, int32_t *group, hipStream_t st);
 
 // The finish of the fused selection (launch_select_finish: top-k into idx,
 // fallback rows, landmark-value merge into v_lm when given) together with the
@@ -85,9 +87,16 @@ hipError_t launch_select_route(const mita_cfg_t &c, const void *q, const void *q
 hipError_t launch_worklist(const mita_cfg_t &c, const int32_t *offsets, int32_t *tile_start, hipStream_t st);
 
 // MiTA attention (Eq. mita). With idx != NULL the routed keys are read in place
-// from k/v rows idx[b,h,e,:]; otherwise from the expert tiles kx/vx.
+// from k/v rows idx[b,h,e,:]; otherwise from the expert tiles kx/vx. With
+// s > 1 the pairs' partials go to pair_o [BH,N*s,d] / pair_lse [BH,N*s] and a
+// combine launch merges them into o.
 hipError_t launch_attend(const mita_cfg_t &c, const void *q, const void *q_lm, const void *v_lm, const void *kv_k,
                          const void *kv_v, const int32_t *idx, const int32_t *perm, const int32_t *offsets,
-                         const int32_t *tile_start, void *o, hipStream_t st);
+                         const int32_t *tile_start, void *o, float *pair_o, float *pair_lse, hipStream_t st);
+
+// Random-selection landmarks: q_lm[bh, i] = q[bh, sel[bh, i]] (NaN row for an
+// index outside [0, N)).
+hipError_t launch_select_landmarks(const mita_cfg_t &c, const void *q, const int32_t *sel, void *q_lm,
+                                   hipStream_t st);
 
 }  // namespace mita

@@ -100,8 +100,9 @@ hipError_t mita::launched(const char *kernel, hipStream_t st) {
 
 namespace {
 
+// q_lm_in: caller-supplied landmark queries (mita_forward_lm), or NULL to pool them.
 int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *v, void *o, void *ws,
-                 size_t ws_bytes, hipStream_t st, mita_timer *timer) {
+                 size_t ws_bytes, hipStream_t st, mita_timer *timer, const void *q_lm_in = nullptr) {
   TRY(validate(c));
   TRY(need_ptr(q, "q"));
   TRY(need_ptr(k, "k"));
@@ -110,6 +111,8 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
   const size_t tb = tensor_bytes(c);
   if (overlaps(o, tb, q, tb) || overlaps(o, tb, k, tb) || overlaps(o, tb, v, tb))
     return set_err(MITA_ERR_INVALID_ARG, "o overlaps an input");
+  if (q_lm_in && overlaps(o, tb, q_lm_in, (size_t)BH(*c) * c->M * c->d * elem_bytes(*c)))
+    return set_err(MITA_ERR_INVALID_ARG, "o overlaps q_lm");
   TRY(need_ws(c, MITA_WS_FORWARD, ws, ws_bytes));
   Recording rec{timer, 0, 0, hipSuccess};
   if (timer) {
@@ -132,7 +135,8 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
 
   const FwdLayout L = forward_layout(*c);
   char *w = (char *)ws;
-  void *q_lm = w + L.q_lm;
+  void *q_lm_ws = w + L.q_lm;
+  const void *q_lm = q_lm_in ? q_lm_in : q_lm_ws;
   void *v_lm = c->use_shared ? (void *)(w + L.v_lm) : nullptr;
   float *S = c->use_routed ? (float *)(w + L.scores) : nullptr;
   int32_t *idx = (int32_t *)(w + L.idx);
@@ -158,10 +162,21 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
   // with the fused selection and in-place gather, the selection's finish
   // shares launches with the routing (the "route" stage then includes it),
   // whose placement cursors (in the tile_base buffer) start at zero
-  const bool sel_in_route = fused && c->use_routed && !staged;
+  // s > 1 routes through its own launches (stable grouping of the pairs)
+  const bool multi = multi_route(*c);
+  const bool sel_in_route = fused && c->use_routed && !staged && !multi;
+  int32_t *group = multi ? (int32_t *)(w + L.group) : nullptr;
+  float *pair_o = multi ? (float *)(w + L.pair_o) : nullptr;
+  float *pair_lse = multi ? (float *)(w + L.pair_lse) : nullptr;
   TRY(mark(0));
-  TRY(hip_status(launch_pool(*c, q, q_lm, c->use_routed ? counts : nullptr, sel_in_route ? tile_base : nullptr, st),
-                 "landmarks"));
+  int32_t *zero_counts = c->use_routed && !multi ? counts : nullptr;
+  int32_t *zero_cursor = sel_in_route ? tile_base : nullptr;
+  if (q_lm_in) {
+    TRY(hip_status(launch_zero(zero_counts, zero_counts ? BH(*c) * c->M : 0, st), "landmarks"));
+    TRY(hip_status(launch_zero(zero_cursor, zero_cursor ? BH(*c) * c->M : 0, st), "landmarks"));
+  } else {
+    TRY(hip_status(launch_pool(*c, q, q_lm_ws, zero_counts, zero_cursor, st), "landmarks"));
+  }
   TRY(mark(1));
   if (fused) TRY(hip_status(launch_select_pivots(*c, q_lm, k, sel, st), "select pivots"));
   TRY(hip_status(launch_scores(*c, q_lm, k, v, fused ? nullptr : S, v_lm, w + L.partial, fused ? &sel : nullptr, st),
@@ -179,11 +194,12 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
                                        tile_cnt, tile_base, counts, tile_start, st),
                    "route"));
   else if (c->use_routed)
-    TRY(hip_status(launch_route(*c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st),
-                   "route"));
+    TRY(hip_status(
+        launch_route(*c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, group, st),
+        "route"));
   TRY(mark(5));
   TRY(hip_status(launch_attend(*c, q, q_lm, v_lm, staged ? kx : k, staged ? vx : v, staged ? nullptr : idx, perm,
-                               offsets, tile_start, o, st),
+                               offsets, tile_start, o, pair_o, pair_lse, st),
                  "attend"));
   if (rec.err != hipSuccess) return hip_status(rec.err, "hipEventRecord");
   return MITA_OK;
@@ -305,6 +321,24 @@ int mita_landmarks(const mita_cfg_t *cfg, const void *q, void *q_lm, mita_stream
   return hip_status(launch_pool(*cfg, q, q_lm, nullptr, nullptr, (hipStream_t)stream), "landmarks");
 }
 
+int mita_landmarks_select(const mita_cfg_t *cfg, const void *q, const int32_t *sel, void *q_lm,
+                          mita_stream_t stream) {
+  g_err.clear();
+  TRY(validate(cfg));
+  TRY(need_ptr(q, "q"));
+  TRY(need_ptr(sel, "sel"));
+  TRY(need_ptr(q_lm, "q_lm"));
+  return hip_status(launch_select_landmarks(*cfg, q, sel, q_lm, (hipStream_t)stream), "landmarks");
+}
+
+int mita_forward_lm(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, const void *q_lm, void *o,
+                    void *ws, size_t ws_bytes, mita_stream_t stream) {
+  g_err.clear();
+  TRY(validate(cfg));
+  TRY(need_ptr(q_lm, "q_lm"));
+  return forward_impl(cfg, q, k, v, o, ws, ws_bytes, (hipStream_t)stream, nullptr, q_lm);
+}
+
 int mita_scores(const mita_cfg_t *cfg, const void *q_lm, const void *k, const void *v, float *scores, void *v_lm,
                 void *ws, size_t ws_bytes, mita_stream_t stream) {
   g_err.clear();
@@ -354,14 +388,19 @@ int mita_route(const mita_cfg_t *cfg, const void *q, const void *q_lm, int32_t *
   TRY(need_ptr(offsets, "offsets"));
   TRY(need_ws(cfg, MITA_WS_ROUTE, ws, ws_bytes));
   const size_t tb = route_tiles_bytes(*cfg);
-  int32_t *tile_cnt = (int32_t *)ws;
-  int32_t *tile_base = (int32_t *)((char *)ws + tb);
-  int32_t *counts = (int32_t *)((char *)ws + 2 * tb);
-  int32_t *tile_start = (int32_t *)((char *)ws + 2 * tb + align_up((size_t)BH(*cfg) * cfg->M * sizeof(int32_t)));
+  char *w = (char *)ws;
+  int32_t *tile_cnt = (int32_t *)w;
+  int32_t *tile_base = (int32_t *)(w + tb);
+  int32_t *counts = (int32_t *)(w + 2 * tb);
+  int32_t *tile_start = (int32_t *)(w + 2 * tb + route_counts_bytes(*cfg));
+  int32_t *group = multi_route(*cfg)
+                       ? (int32_t *)(w + 2 * tb + route_counts_bytes(*cfg) + route_start_bytes(*cfg))
+                       : nullptr;
   hipStream_t st = (hipStream_t)stream;
-  TRY(hip_status(launch_zero(counts, BH(*cfg) * cfg->M, st), "route"));
-  return hip_status(launch_route(*cfg, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st),
-                    "route");
+  if (!multi_route(*cfg)) TRY(hip_status(launch_zero(counts, BH(*cfg) * cfg->M, st), "route"));
+  return hip_status(
+      launch_route(*cfg, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, group, st),
+      "route");
 }
 
 int mita_attend(const mita_cfg_t *cfg, const void *q, const void *q_lm, const void *v_lm, const void *k_x,
@@ -385,10 +424,14 @@ int mita_attend(const mita_cfg_t *cfg, const void *q, const void *q_lm, const vo
   if (overlaps(o, tb, q, tb)) return set_err(MITA_ERR_INVALID_ARG, "o overlaps q");
   TRY(need_ws(cfg, MITA_WS_ATTEND, ws, ws_bytes));
   hipStream_t st = (hipStream_t)stream;
-  int32_t *tile_start = (int32_t *)ws;
+  char *w = (char *)ws;
+  int32_t *tile_start = (int32_t *)w;
+  float *pair_o = multi_route(*cfg) ? (float *)(w + route_start_bytes(*cfg)) : nullptr;
+  float *pair_lse = multi_route(*cfg) ? (float *)(w + route_start_bytes(*cfg) + pair_out_bytes(*cfg)) : nullptr;
   if (cfg->use_routed) TRY(hip_status(launch_worklist(*cfg, offsets, tile_start, st), "worklist"));
   return hip_status(
-      launch_attend(*cfg, q, q_lm, v_lm, k_x, v_x, nullptr, perm, offsets, tile_start, o, st), "attend");
+      launch_attend(*cfg, q, q_lm, v_lm, k_x, v_x, nullptr, perm, offsets, tile_start, o, pair_o, pair_lse, st),
+      "attend");
 }
 
 int mita_timer_create(mita_timer_t **timer, int max_calls) {

@@ -155,6 +155,49 @@ hipError_t launch_pool(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *
   return c.d == 64 ? pool_t<bf16_t, 64>(c, q, q_lm, zc, zcur, st) : pool_t<bf16_t, 128>(c, q, q_lm, zc, zcur, st);
 }
 
+// Random-selection landmarks (Tab. A1, landmark extraction): row i of slice
+// bh is the query of token sel[bh, i]; one thread per 16-byte chunk. An index
+// outside [0, N) is not read and gives a row of NaN.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void select_landmarks_kernel(const T *__restrict__ q, const int32_t *__restrict__ sel,
+                                                               T *__restrict__ q_lm, int N, int M, int64_t rows) {
+  constexpr int VE = 16 / (int)sizeof(T);
+  constexpr int C = D / VE;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t row = t / C;
+  const int c = (int)(t % C);
+  if (row >= rows) return;
+  const int64_t bh = row / M;
+  const int src = sel[row];
+  uint4 x;
+  if (src >= 0 && src < N) {
+    x = *reinterpret_cast<const uint4 *>(q + (bh * N + src) * D + c * VE);
+  } else {
+    const uint32_t nan = sizeof(T) == 4 ? 0x7fc00000u : 0x7fc07fc0u;
+    x = make_uint4(nan, nan, nan, nan);
+  }
+  *reinterpret_cast<uint4 *>(q_lm + row * D + c * VE) = x;
+}
+
+template <typename T, int D>
+static hipError_t select_landmarks_t(const mita_cfg_t &c, const void *q, const int32_t *sel, void *q_lm,
+                                     hipStream_t st) {
+  const int64_t rows = BH(c) * c.M;
+  const int64_t threads = rows * (D * (int64_t)sizeof(T) / 16);
+  hipLaunchKernelGGL((select_landmarks_kernel<T, D>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
+                     (const T *)q, sel, (T *)q_lm, c.N, c.M, rows);
+  return launched("select_landmarks_kernel", st);
+}
+
+hipError_t launch_select_landmarks(const mita_cfg_t &c, const void *q, const int32_t *sel, void *q_lm,
+                                   hipStream_t st) {
+  if (c.dtype == MITA_F32)
+    return c.d == 64 ? select_landmarks_t<float, 64>(c, q, sel, q_lm, st)
+                     : select_landmarks_t<float, 128>(c, q, sel, q_lm, st);
+  return c.d == 64 ? select_landmarks_t<bf16_t, 64>(c, q, sel, q_lm, st)
+                   : select_landmarks_t<bf16_t, 128>(c, q, sel, q_lm, st);
+}
+
 __global__ __launch_bounds__(256) void zero_kernel(int32_t *__restrict__ p, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i < n) p[i] = 0;

@@ -1,4 +1,5 @@
 // route_attend.hip - routing of queries to landmarks and the MiTA attention.
+#include <climits>
 #include <type_traits>
 
 #include "cdna4.hpp"
@@ -139,6 +140,165 @@ __global__ __launch_bounds__(BLOCK) void route_logits_kernel(const T *__restrict
   extern __shared__ uint32_t cnt[];  // [4][M]
   route_logits_body<T, D>(lms, cnt, (int)blockIdx.x, (int)blockIdx.y, q, q_lm, expert, tile_cnt, counts, N, M, scale,
                           ntiles);
+}
+
+// ---------------------------------------------------------------------------
+// Routing to S > 1 experts (Sec. 3.2: e_j(q), the rank-j expert under the
+// logits Q^T Q_lm). The logits are formed as in route_logits_body; each lane
+// keeps the S best (logit, landmark) pairs of the landmarks it sees, ordered
+// by larger logit, then lower landmark (a NaN logit counts as -inf). The
+// four lane groups of a query column then merge their lists: S rounds, each
+// taking the best head among the four lists (the owner's list advances;
+// landmarks are distinct, so the owner is unique). Writes expert[n * S + j]
+// and the pair's group: expert for j = 0, M + expert otherwise.
+// ---------------------------------------------------------------------------
+template <int S> struct TopS {
+  float v[S];
+  int a[S];
+  __device__ __forceinline__ void init() {
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      v[j] = -INFINITY;
+      a[j] = INT_MAX;  // sorts after every landmark
+    }
+  }
+  // insertion in order: (x, i) moves down the list past every entry it beats
+  __device__ __forceinline__ void insert(float x, int i) {
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      const bool up = x > v[j] || (x == v[j] && i < a[j]);
+      const float tv = v[j];
+      const int ta = a[j];
+      v[j] = up ? x : v[j];
+      a[j] = up ? i : a[j];
+      x = up ? tv : x;
+      i = up ? ta : i;
+    }
+  }
+  __device__ __forceinline__ void head(int h, float &x, int &i) const {
+    x = -INFINITY;
+    i = INT_MAX;
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      x = h == j ? v[j] : x;
+      i = h == j ? a[j] : i;
+    }
+  }
+};
+
+template <typename T, int D, int S>
+__global__ __launch_bounds__(BLOCK) void route_tops_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
+                                                           int32_t *__restrict__ expert, int32_t *__restrict__ group,
+                                                           int N, int M, float scale, int ntq) {
+  constexpr int VE = RouteLds<T, D>::VE;
+  constexpr int LSTR = RouteLds<T, D>::LSTR;
+  __shared__ __align__(16) T lms[RouteLds<T, D>::BYTES / sizeof(T)];
+  const int64_t bh = blockIdx.y;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
+  const int tile = blockIdx.x * 4 + w;
+  Frag<T> qf[4][D / 32];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int n = tile * ROUTE_TQ + c * 16 + p;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      if (tile < ntq && n < N)
+        qf[c][ks].load(q + (bh * N + n) * D + ks * 32 + g * 8);
+      else
+        qf[c][ks].zero();
+    }
+  }
+  const T *lmb = q_lm + bh * (int64_t)M * D;
+  TopS<S> top[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) top[c].init();
+  for (int l0 = 0; l0 < M; l0 += ROUTE_LB) {
+    const int nl = min(ROUTE_LB, M - l0);
+    __syncthreads();
+    for (int ch = threadIdx.x; ch < ROUTE_LB * (D / VE); ch += BLOCK) {
+      const int r = ch / (D / VE), cc = ch % (D / VE);
+      uint4 x = make_uint4(0, 0, 0, 0);
+      if (r < nl) x = *reinterpret_cast<const uint4 *>(lmb + (int64_t)(l0 + r) * D + cc * VE);
+      *reinterpret_cast<uint4 *>(lms + r * LSTR + cc * VE) = x;
+    }
+    __syncthreads();
+    if (tile >= ntq) continue;
+    for (int sb = 0; sb < nl; sb += 16) {
+      f32x4 acc[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) {
+        Frag<T> a;
+        a.load(lms + (sb + p) * LSTR + ks * 32 + g * 8);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[c] = mma(a, qf[c][ks], acc[c]);
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int lmi = l0 + sb + 4 * g + r;
+          float val = acc[c][r] * scale;
+          val = val != val ? -INFINITY : val;
+          if (lmi < l0 + nl) top[c].insert(val, lmi);
+        }
+    }
+  }
+  if (tile >= ntq) return;  // no workgroup barriers below
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int n = tile * ROUTE_TQ + c * 16 + p;
+    int h = 0;
+#pragma unroll
+    for (int j = 0; j < S; ++j) {
+      float x;
+      int i;
+      top[c].head(h, x, i);
+      float bx = x;
+      int bi = i;
+#pragma unroll
+      for (int o = 16; o <= 32; o <<= 1) {
+        const float ox = __shfl_xor(bx, o);
+        const int oi = __shfl_xor(bi, o);
+        if (ox > bx || (ox == bx && oi < bi)) {
+          bx = ox;
+          bi = oi;
+        }
+      }
+      h += i == bi ? 1 : 0;
+      if (g == 0 && n < N) {
+        const int64_t at = (bh * N + n) * S + j;
+        expert[at] = bi;
+        group[at] = j == 0 ? bi : M + bi;
+      }
+    }
+  }
+}
+
+// Per-tile group counts of the routing items (one wave per 64-item tile):
+// tile_cnt[tile][g] and the per-group totals (zeroed beforehand).
+// cnt: 4 G words of LDS.
+__global__ __launch_bounds__(256) void pair_count_kernel(const int32_t *__restrict__ group,
+                                                         int32_t *__restrict__ tile_cnt,
+                                                         int32_t *__restrict__ counts, int NP, int G, int ntiles) {
+  extern __shared__ uint32_t cnt[];
+  const int64_t bh = blockIdx.y;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int tile = blockIdx.x * 4 + w;
+  uint32_t *wc = cnt + w * G;
+  for (int i = lane; i < G; i += 64) wc[i] = 0u;
+  __syncthreads();
+  const int item = tile * ROUTE_TQ + lane;
+  if (tile < ntiles && item < NP) atomicAdd(&wc[group[bh * NP + item]], 1u);
+  __syncthreads();
+  if (tile >= ntiles) return;
+  int32_t *tc = tile_cnt + (bh * ntiles + tile) * (int64_t)G;
+  for (int i = lane; i < G; i += 64) {
+    const uint32_t x = wc[i];
+    tc[i] = (int32_t)x;
+    if (x) atomicAdd(&counts[bh * G + i], (int32_t)x);
+  }
 }
 
 // Block-wide exclusive scan of one value per thread (NT threads); returns the
@@ -500,21 +660,24 @@ __global__ __launch_bounds__(256) void topk_scatter_kernel(const T *__restrict__
 }
 
 // Attention work list: tile_start[e] = sum over e' < e of ceil(size(e') / 64),
-// tile_start[M] = total tiles. 1024 threads, one expert each.
+// tile_start[G] = total tiles, for G <= 2048 groups. 1024 threads, two
+// consecutive groups each.
 __global__ __launch_bounds__(1024) void worklist_kernel(const int32_t *__restrict__ offsets,
-                                                        int32_t *__restrict__ tile_start, int M) {
+                                                        int32_t *__restrict__ tile_start, int G) {
   __shared__ uint32_t wsum[16];
   const int64_t bh = blockIdx.x;
-  const int e = threadIdx.x;
-  uint32_t nt = 0;
-  if (e < M) {
-    const int sz = offsets[bh * (M + 1) + e + 1] - offsets[bh * (M + 1) + e];
-    nt = (uint32_t)((sz + ATT_TQ - 1) / ATT_TQ);
-  }
+  const int e0 = 2 * threadIdx.x;
+  const int32_t *of = offsets + bh * (G + 1);
+  uint32_t nt[2] = {0u, 0u};
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+    if (e0 + u < G) nt[u] = (uint32_t)((of[e0 + u + 1] - of[e0 + u] + ATT_TQ - 1) / ATT_TQ);
   uint32_t all;
-  const uint32_t before = block_exclusive_scan<1024>(nt, wsum, &all);
-  if (e < M) tile_start[bh * (M + 1) + e] = (int32_t)before;
-  if (e == 0) tile_start[bh * (M + 1) + M] = (int32_t)all;
+  const uint32_t before = block_exclusive_scan<1024>(nt[0] + nt[1], wsum, &all);
+  int32_t *ts = tile_start + bh * (G + 1);
+  if (e0 < G) ts[e0] = (int32_t)before;
+  if (e0 + 1 < G) ts[e0 + 1] = (int32_t)(before + nt[0]);
+  if (threadIdx.x == 0) ts[G] = (int32_t)all;
 }
 
 // ---------------------------------------------------------------------------
@@ -552,7 +715,7 @@ template <typename T, int D> constexpr size_t attend_tiles_lds() {
 template <int D> constexpr size_t attend16_tiles_lds() { return 4 * (size_t)DmaTile<D, 32>::BYTES; }
 
 // The workgroup's queries [q_begin, q_end) (positions in perm) and their
-// expert e, from the work list; false for a workgroup past its end.
+// group e (of G), from the work list; false for a workgroup past its end.
 template <bool ROUTED>
 __device__ __forceinline__ bool attend_queries(const int32_t *__restrict__ tile_start,
                                                const int32_t *__restrict__ offsets, int64_t bh, int N, int M, int &e,
@@ -585,14 +748,15 @@ __device__ __forceinline__ bool attend_queries(const int32_t *__restrict__ tile_
   return true;
 }
 
-template <typename T, int D, bool SHARED, bool ROUTED, bool FUSED, bool IDX_LDS>
+template <typename T, int D, bool SHARED, bool ROUTED, bool FUSED, bool IDX_LDS, bool MULTI>
 __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, const T *__restrict__ q_lm,
                                                        const T *__restrict__ v_lm, const T *__restrict__ rk,
                                                        const T *__restrict__ rv, const int32_t *__restrict__ idx,
                                                        const int32_t *__restrict__ perm,
                                                        const int32_t *__restrict__ offsets,
                                                        const int32_t *__restrict__ tile_start, T *__restrict__ o,
-                                                       int N, int M, int k, float scale) {
+                                                       int N, int M, int k, float scale, int s,
+                                                       float *__restrict__ pair_o, float *__restrict__ pair_lse) {
   using TD = TileDims<T, D>;
   // tiles staged through registers (K row-major, V transposed, padded rows)
   constexpr int KBYTES = TD::K_ELEMS * (int)sizeof(T);
@@ -607,10 +771,16 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
 
   int e = 0, q_begin, q_end;
-  if (!attend_queries<ROUTED>(tile_start, offsets, bh, N, M, e, q_begin, q_end)) return;  // uniform
+  if (!attend_queries<ROUTED>(tile_start, offsets, bh, N, MULTI ? 2 * M : M, e, q_begin, q_end)) return;  // uniform
+  // MULTI (s > 1): the items are (query, rank) pairs; group e < M holds rank-1
+  // pairs of expert e (these also take the shared expert), group M + e the
+  // other pairs of expert e
+  const bool with_sh = SHARED && (!MULTI || e < M);
+  if (MULTI && e >= M) e -= M;
+  const int NP = MULTI ? N * s : N;
 
   // full tiles: nA shared, then nB routed; partial ones: pA shared rows, pB routed rows
-  const int nA = SHARED ? M / TK : 0, pA = SHARED ? M % TK : 0;
+  const int nA = with_sh ? M / TK : 0, pA = with_sh ? M % TK : 0;
   const int nB = ROUTED ? k / TK : 0, pB = ROUTED ? k % TK : 0;
   const int nfull = nA + nB;
   const T *sh_k = q_lm + bh * (int64_t)M * D, *sh_v = v_lm + bh * (int64_t)M * D;
@@ -632,14 +802,14 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
   const uint32_t *rows = nullptr;
   constexpr uint32_t ROWB = D * sizeof(T);
   if (IDX_LDS) {
-    const int nsh = SHARED ? M : 0;
+    const int nsh = with_sh ? M : 0;
     for (int i = threadIdx.x; i < nsh; i += BLOCK) sidx[i] = (uint32_t)i * ROWB;
     if (ROUTED)
       for (int i = threadIdx.x; i < k; i += BLOCK) sidx[nsh + i] = (uint32_t)(FUSED ? gidx[i] : i) * ROWB;
     __syncthreads();
     rows = sidx;
   }
-  const int rbase = SHARED ? M : 0;  // list offset of the routed rows
+  const int rbase = with_sh ? M : 0;  // list offset of the routed rows
   auto tile_base = [&](int i, const T *&kb, const T *&vb, int &off) {
     const bool sh = i < nA;
     kb = sh ? sh_k : rkb;
@@ -653,13 +823,14 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
   // skips the arithmetic
   const bool wave_busy = q_begin + qh * 32 < q_end;
   bool qvalid[2];
-  int token[2];
+  int token[2], item[2];
   Frag<T> qf[2][D / 32];
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
     const int qi = q_begin + qh * 32 + c * 16 + p;
     qvalid[c] = qi < q_end;
-    token[c] = qvalid[c] ? (ROUTED ? perm[bh * N + qi] : qi) : 0;
+    item[c] = qvalid[c] ? (ROUTED ? perm[bh * NP + qi] : qi) : 0;
+    token[c] = MULTI ? item[c] / s : item[c];
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks) {
       if (qvalid[c])
@@ -785,6 +956,22 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
     const float l = __builtin_fmaf(KH ? l_mine : l_theirs, a1, (KH ? l_theirs : l_mine) * a0);
     const float inv = __builtin_amdgcn_rcpf(l);
     const float s0 = a0 * inv, s1 = a1 * inv;
+    if constexpr (MULTI) {
+      // the pair's normalised partial and its log-sum-exp (log2 units)
+      float *prow = pair_o + (bh * NP + item[KH]) * D;
+#pragma unroll
+      for (int db = 0; db < D / 16; ++db) {
+        float vals[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float om = st.o[KH][db][r], ot = theirs[(db * 4 + r) * 64];
+          vals[r] = __builtin_fmaf(KH ? om : ot, s1, (KH ? ot : om) * s0);
+        }
+        *reinterpret_cast<float4 *>(prow + db * 16 + 4 * g) = *reinterpret_cast<const float4 *>(vals);
+      }
+      if (g == 0) pair_lse[bh * NP + item[KH]] = mm + __log2f(l);
+      return;
+    }
     T *orow = o + (bh * N + token[KH]) * D;
 #pragma unroll
     for (int db = 0; db < D / 16; ++db) {
@@ -828,12 +1015,13 @@ constexpr int TK32 = 32;
 // tile loop); seven workgroups of 16 + 2.5 KB LDS fit a CU at M + k = 640
 #define ATTEND16_OCCUPANCY __attribute__((amdgpu_waves_per_eu(D == 64 ? 7 : 4)))
 
-template <int D, bool SHARED, bool ROUTED, bool FUSED>
+template <int D, bool SHARED, bool ROUTED, bool FUSED, bool MULTI>
 __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
     const bf16_t *__restrict__ q, const bf16_t *__restrict__ q_lm, const bf16_t *__restrict__ v_lm,
     const bf16_t *__restrict__ rk, const bf16_t *__restrict__ rv, const int32_t *__restrict__ idx,
     const int32_t *__restrict__ perm, const int32_t *__restrict__ offsets, const int32_t *__restrict__ tile_start,
-    bf16_t *__restrict__ o, int N, int M, int k, float scale) {
+    bf16_t *__restrict__ o, int N, int M, int k, float scale, int s, float *__restrict__ pair_o,
+    float *__restrict__ pair_lse) {
   using DT = DmaTile<D, TK32>;
   static_assert(attend16_tiles_lds<D>() == 4 * DT::BYTES, "two buffers of one K and one V tile");
   // two separate arrays (see attend_kernel): K then V of one tile each
@@ -848,10 +1036,15 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
   const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
   int e, q_begin, q_end;
-  if (!attend_queries<ROUTED>(tile_start, offsets, bh, N, M, e, q_begin, q_end)) return;  // uniform
+  if (!attend_queries<ROUTED>(tile_start, offsets, bh, N, MULTI ? 2 * M : M, e, q_begin, q_end)) return;  // uniform
+  // MULTI (s > 1): (query, rank) pairs; group e < M: rank-1 pairs of expert e
+  // (with the shared expert), group M + e: the other pairs of expert e
+  const bool with_sh = SHARED && (!MULTI || e < M);
+  if (MULTI && e >= M) e -= M;
+  const int NP = MULTI ? N * s : N;
 
   // full 32-row tiles: nA shared, then nB routed; partial ones: pA, pB rows
-  const int nA = SHARED ? M / TK32 : 0, pA = SHARED ? M % TK32 : 0;
+  const int nA = with_sh ? M / TK32 : 0, pA = with_sh ? M % TK32 : 0;
   const int nB = ROUTED ? k / TK32 : 0, pB = ROUTED ? k % TK32 : 0;
   const int nfull = nA + nB;
   const bf16_t *sh_k = q_lm + bh * (int64_t)M * D, *sh_v = v_lm + bh * (int64_t)M * D;
@@ -866,7 +1059,7 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
     rvb = rv + (bh * M + e) * (int64_t)k * D;
   }
   constexpr uint32_t ROWB = D * sizeof(bf16_t);
-  const int nsh = SHARED ? M : 0;
+  const int nsh = with_sh ? M : 0;
   for (int i = threadIdx.x; i < nsh; i += BLOCK) sidx[i] = (uint32_t)i * ROWB;
   if (ROUTED)
     for (int i = threadIdx.x; i < k; i += BLOCK) sidx[nsh + i] = (uint32_t)(FUSED ? gidx[i] : i) * ROWB;
@@ -883,7 +1076,8 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
   // the barriers but skips the arithmetic
   const int qi = q_begin + 16 * w + p;
   const bool qvalid = qi < q_end;
-  const int token = qvalid ? (ROUTED ? perm[bh * N + qi] : qi) : 0;
+  const int item = qvalid ? (ROUTED ? perm[bh * NP + qi] : qi) : 0;
+  const int token = MULTI ? item / s : item;
   const bool busy = q_begin + 16 * w < q_end;
   Frag<bf16_t> qf[D / 32];
 #pragma unroll
@@ -997,11 +1191,23 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
     if (__ballot(!done) && lane == 0) atomicOr(redo, 1u);
   }
   auto write_out = [&]() {
-    const float inv = __builtin_amdgcn_rcpf(att16_sum<D>(st));
+    const float lsum = att16_sum<D>(st);
+    const float inv = __builtin_amdgcn_rcpf(lsum);
     // the token is read again (the barriers in between keep the compiler
     // from reusing the first read), so no address stays live across the
     // tile loop
-    const int tok = ROUTED ? perm[bh * N + qi] : qi;
+    const int tok = ROUTED ? perm[bh * NP + qi] : qi;
+    if constexpr (MULTI) {
+      // the pair's normalised partial and its log-sum-exp (log2 units; the
+      // scores were pre-scaled by log2 e, the reference is -nm)
+      float *prow = pair_o + (bh * NP + tok) * D;
+#pragma unroll
+      for (int db = 0; db < D / 16; ++db)
+        *reinterpret_cast<float4 *>(prow + db * 16 + 4 * g) =
+            make_float4(st.o[db][0] * inv, st.o[db][1] * inv, st.o[db][2] * inv, st.o[db][3] * inv);
+      if (g == 0) pair_lse[bh * NP + tok] = __log2f(lsum) - st.nm[0];
+      return;
+    }
     bf16_t *orow = o + (bh * N + tok) * D;
 #pragma unroll
     for (int db = 0; db < D / 16; ++db) {
@@ -1020,6 +1226,51 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
       run_tiles(std::integral_constant<int, 0>{});
     if (qvalid && !done) write_out();
   }
+}
+
+// ---------------------------------------------------------------------------
+// s > 1: the s partial results of every query (the rank-1 one including the
+// shared expert) merged by their log-sum-exp (Sec. 3.2: expert-wise attention
+// combined by online softmax): o = sum_j w_j o_j / sum_j w_j with
+// w_j = 2^(lse_j - max_j lse_j), j in rank order. One thread per 4 dims.
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+__global__ __launch_bounds__(256) void combine_kernel(const float *__restrict__ pair_o,
+                                                      const float *__restrict__ pair_lse, T *__restrict__ o,
+                                                      int64_t nq, int s) {
+  constexpr int C = D / 4;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t n = t / C;
+  const int c = (int)(t % C);
+  if (n >= nq) return;
+  float lse[MITA_MAX_S];
+  float L = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < MITA_MAX_S; ++j) {
+    lse[j] = j < s ? pair_lse[n * s + j] : -INFINITY;
+    L = fmaxf(L, lse[j]);
+  }
+  float den = 0.f, acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < MITA_MAX_S; ++j) {
+    if (j >= s) break;
+    const float w = __builtin_amdgcn_exp2f(lse[j] - L);
+    const float4 x = *reinterpret_cast<const float4 *>(pair_o + (n * s + j) * D + 4 * c);
+    den += w;
+    acc[0] = __builtin_fmaf(w, x.x, acc[0]);
+    acc[1] = __builtin_fmaf(w, x.y, acc[1]);
+    acc[2] = __builtin_fmaf(w, x.z, acc[2]);
+    acc[3] = __builtin_fmaf(w, x.w, acc[3]);
+  }
+  const float inv = 1.f / den;
+  T vals[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) vals[r] = from_f32<T>(acc[r] * inv);
+  T *dst = o + n * D + 4 * c;
+  if (sizeof(T) == 2)
+    *reinterpret_cast<uint2 *>(dst) = *reinterpret_cast<const uint2 *>(vals);
+  else
+    *reinterpret_cast<uint4 *>(dst) = *reinterpret_cast<const uint4 *>(vals);
 }
 
 // ---------------------------------------------------------------------------
@@ -1045,9 +1296,55 @@ static hipError_t route_t(const mita_cfg_t &c, const void *q, const void *q_lm, 
   return launched("route_scatter_kernel", st);
 }
 
+// s > 1: top-s logits, per-tile pair counts, then the stable scan and
+// scatter of route_t over the N s pairs and 2 M groups.
+template <typename T, int D, int S>
+static hipError_t route_multi_t(const mita_cfg_t &c, const void *q, const void *q_lm, int32_t *expert, int32_t *group,
+                                int32_t *perm, int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base,
+                                int32_t *counts, int32_t *tile_start, hipStream_t st) {
+  const int G = route_groups(c), NP = route_items(c), nt = route_tiles(c);
+  const int ntq = (c.N + ROUTE_TQ - 1) / ROUTE_TQ;
+  const unsigned bh = (unsigned)BH(c);
+  hipError_t err = launch_zero(counts, (int64_t)bh * G, st);
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL((route_tops_kernel<T, D, S>), dim3((ntq + 3) / 4, bh), dim3(BLOCK), 0, st, (const T *)q,
+                     (const T *)q_lm, expert, group, c.N, c.M, eff_scale(c), ntq);
+  if ((err = launched("route_tops_kernel", st)) != hipSuccess) return err;
+  hipLaunchKernelGGL(pair_count_kernel, dim3((nt + 3) / 4, bh), dim3(256), 4 * (size_t)G * sizeof(uint32_t), st, group,
+                     tile_cnt, counts, NP, G, nt);
+  if ((err = launched("pair_count_kernel", st)) != hipSuccess) return err;
+  hipLaunchKernelGGL(route_scan_kernel, dim3((G + SCAN_EB - 1) / SCAN_EB, bh), dim3(256), 0, st, tile_cnt, counts,
+                     tile_base, offsets, tile_start, nt, G, NP);
+  if ((err = launched("route_scan_kernel", st)) != hipSuccess) return err;
+  int ebits = 0;
+  while ((1 << ebits) < G) ++ebits;
+  hipLaunchKernelGGL(route_scatter_kernel, dim3((nt + 3) / 4, bh), dim3(256), 0, st, group, tile_base, perm, NP, G, nt,
+                     ebits);
+  return launched("route_scatter_kernel", st);
+}
+
+template <typename T, int D>
+static hipError_t route_multi_s(const mita_cfg_t &c, const void *q, const void *q_lm, int32_t *expert, int32_t *group,
+                                int32_t *perm, int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base,
+                                int32_t *counts, int32_t *tile_start, hipStream_t st) {
+  static_assert(MITA_MAX_S == 4, "one instance per s");
+  switch (c.s) {
+    case 2: return route_multi_t<T, D, 2>(c, q, q_lm, expert, group, perm, offsets, tile_cnt, tile_base, counts, tile_start, st);
+    case 3: return route_multi_t<T, D, 3>(c, q, q_lm, expert, group, perm, offsets, tile_cnt, tile_base, counts, tile_start, st);
+    default: return route_multi_t<T, D, 4>(c, q, q_lm, expert, group, perm, offsets, tile_cnt, tile_base, counts, tile_start, st);
+  }
+}
+
 hipError_t launch_route(const mita_cfg_t &c, const void *q, const void *q_lm, int32_t *expert, int32_t *perm,
                         int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base, int32_t *counts,
-                        int32_t *tile_start, hipStream_t st) {
+                        int32_t *tile_start, int32_t *group, hipStream_t st) {
+  if (multi_route(c)) {
+    if (c.dtype == MITA_F32)
+      return c.d == 64 ? route_multi_s<float, 64>(c, q, q_lm, expert, group, perm, offsets, tile_cnt, tile_base, counts, tile_start, st)
+                       : route_multi_s<float, 128>(c, q, q_lm, expert, group, perm, offsets, tile_cnt, tile_base, counts, tile_start, st);
+    return c.d == 64 ? route_multi_s<bf16_t, 64>(c, q, q_lm, expert, group, perm, offsets, tile_cnt, tile_base, counts, tile_start, st)
+                     : route_multi_s<bf16_t, 128>(c, q, q_lm, expert, group, perm, offsets, tile_cnt, tile_base, counts, tile_start, st);
+  }
   if (c.dtype == MITA_F32)
     return c.d == 64 ? route_t<float, 64>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st)
                      : route_t<float, 128>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st);
@@ -1133,66 +1430,90 @@ hipError_t launch_select_route(const mita_cfg_t &c, const void *q, const void *q
 }
 
 hipError_t launch_worklist(const mita_cfg_t &c, const int32_t *offsets, int32_t *tile_start, hipStream_t st) {
-  hipLaunchKernelGGL(worklist_kernel, dim3((unsigned)BH(c)), dim3(1024), 0, st, offsets, tile_start, c.M);
+  hipLaunchKernelGGL(worklist_kernel, dim3((unsigned)BH(c)), dim3(1024), 0, st, offsets, tile_start, route_groups(c));
   return launched("worklist_kernel", st);
 }
 
-template <typename T, int D, bool SH, bool RT, bool FU>
+template <typename T, int D, bool SH, bool RT, bool FU, bool MU>
 static hipError_t attend_t3(const mita_cfg_t &c, const void *q, const void *q_lm, const void *v_lm, const void *rk,
                             const void *rv, const int32_t *idx, const int32_t *perm, const int32_t *offsets,
-                            const int32_t *tile_start, void *o, hipStream_t st) {
-  // routed: at most ceil(N/64) + M tiles (each expert adds at most one partial
-  // tile), rounded up to a multiple of the XCD count for the tile spreading
-  int tiles = (c.N + ATT_TQ - 1) / ATT_TQ;
-  if (RT) tiles = (tiles + c.M + NXCD - 1) / NXCD * NXCD;
+                            const int32_t *tile_start, void *o, float *pair_o, float *pair_lse, hipStream_t st) {
+  // routed: at most ceil(items / 64) + groups tiles (each group adds at most
+  // one partial tile), rounded up to a multiple of the XCD count for the tile
+  // spreading
+  int tiles = (route_items(c) + ATT_TQ - 1) / ATT_TQ;
+  if (RT) tiles = (tiles + route_groups(c) + NXCD - 1) / NXCD * NXCD;
   const dim3 grid((unsigned)tiles, (unsigned)BH(c));
   const int nlist = (SH ? c.M : 0) + (RT ? c.k : 0);
+  const int s = route_s(c);
+  hipError_t err = hipSuccess;
+  bool done = false;
   // the row list is staged in LDS when it and the kernel's tiles fit
   if constexpr (sizeof(T) == 2) {
     // bf16: lists of up to IDX_LDS_MAX - 1 rows (and the kernel's rerun flag)
     // beside the 16 / 32 KB DMA tiles
     if (list_in_lds(nlist + 1, attend16_tiles_lds<D>())) {
-      hipLaunchKernelGGL((attend16_kernel<D, SH, RT, FU>), grid, dim3(BLOCK), (size_t)(nlist + 1) * sizeof(int32_t), st,
-                         (const bf16_t *)q, (const bf16_t *)q_lm, (const bf16_t *)v_lm, (const bf16_t *)rk,
-                         (const bf16_t *)rv, idx, perm, offsets, tile_start, (bf16_t *)o, c.N, c.M, c.k, eff_scale(c));
-      return launched("attend16_kernel", st);
+      hipLaunchKernelGGL((attend16_kernel<D, SH, RT, FU, MU>), grid, dim3(BLOCK), (size_t)(nlist + 1) * sizeof(int32_t),
+                         st, (const bf16_t *)q, (const bf16_t *)q_lm, (const bf16_t *)v_lm, (const bf16_t *)rk,
+                         (const bf16_t *)rv, idx, perm, offsets, tile_start, (bf16_t *)o, c.N, c.M, c.k, eff_scale(c), s,
+                         pair_o, pair_lse);
+      err = launched("attend16_kernel", st);
+      done = true;
     }
   } else {
     if (list_in_lds(nlist, attend_tiles_lds<T, D>())) {
-      hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU, true>), grid, dim3(BLOCK), (size_t)nlist * sizeof(int32_t),
+      hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU, true, MU>), grid, dim3(BLOCK), (size_t)nlist * sizeof(int32_t),
                          st, (const T *)q, (const T *)q_lm, (const T *)v_lm, (const T *)rk, (const T *)rv, idx, perm,
-                         offsets, tile_start, (T *)o, c.N, c.M, c.k, eff_scale(c));
-      return launched("attend_kernel", st);
+                         offsets, tile_start, (T *)o, c.N, c.M, c.k, eff_scale(c), s, pair_o, pair_lse);
+      err = launched("attend_kernel", st);
+      done = true;
     }
   }
-  // the row list stays in memory
-  hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU, false>), grid, dim3(BLOCK), 0, st, (const T *)q,
-                     (const T *)q_lm, (const T *)v_lm, (const T *)rk, (const T *)rv, idx, perm, offsets, tile_start,
-                     (T *)o, c.N, c.M, c.k, eff_scale(c));
-  return launched("attend_kernel", st);
+  if (!done) {
+    // the row list stays in memory
+    hipLaunchKernelGGL((attend_kernel<T, D, SH, RT, FU, false, MU>), grid, dim3(BLOCK), 0, st, (const T *)q,
+                       (const T *)q_lm, (const T *)v_lm, (const T *)rk, (const T *)rv, idx, perm, offsets, tile_start,
+                       (T *)o, c.N, c.M, c.k, eff_scale(c), s, pair_o, pair_lse);
+    err = launched("attend_kernel", st);
+  }
+  if (!MU || err != hipSuccess) return err;
+  const int64_t nq = BH(c) * c.N;
+  const int64_t threads = nq * (D / 4);
+  hipLaunchKernelGGL((combine_kernel<T, D>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st, pair_o,
+                     pair_lse, (T *)o, nq, s);
+  return launched("combine_kernel", st);
+}
+
+template <typename T, int D, bool MU>
+static hipError_t attend_m(const mita_cfg_t &c, const void *q, const void *q_lm, const void *v_lm, const void *rk,
+                           const void *rv, const int32_t *idx, const int32_t *perm, const int32_t *offsets,
+                           const int32_t *tile_start, void *o, float *po, float *pl, hipStream_t st) {
+  if (idx) {
+    if (c.use_shared) return attend_t3<T, D, true, true, true, MU>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, po, pl, st);
+    return attend_t3<T, D, false, true, true, MU>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, po, pl, st);
+  }
+  if (c.use_shared) return attend_t3<T, D, true, true, false, MU>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, po, pl, st);
+  return attend_t3<T, D, false, true, false, MU>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, po, pl, st);
 }
 
 template <typename T, int D>
 static hipError_t attend_t(const mita_cfg_t &c, const void *q, const void *q_lm, const void *v_lm, const void *rk,
                            const void *rv, const int32_t *idx, const int32_t *perm, const int32_t *offsets,
-                           const int32_t *tile_start, void *o, hipStream_t st) {
-  if (!c.use_routed) return attend_t3<T, D, true, false, false>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
-  if (idx) {
-    if (c.use_shared) return attend_t3<T, D, true, true, true>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
-    return attend_t3<T, D, false, true, true>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
-  }
-  if (c.use_shared) return attend_t3<T, D, true, true, false>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
-  return attend_t3<T, D, false, true, false>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
+                           const int32_t *tile_start, void *o, float *po, float *pl, hipStream_t st) {
+  if (!c.use_routed)
+    return attend_t3<T, D, true, false, false, false>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, po, pl, st);
+  if (multi_route(c)) return attend_m<T, D, true>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, po, pl, st);
+  return attend_m<T, D, false>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, po, pl, st);
 }
 
 hipError_t launch_attend(const mita_cfg_t &c, const void *q, const void *q_lm, const void *v_lm, const void *rk,
                          const void *rv, const int32_t *idx, const int32_t *perm, const int32_t *offsets,
-                         const int32_t *tile_start, void *o, hipStream_t st) {
+                         const int32_t *tile_start, void *o, float *pair_o, float *pair_lse, hipStream_t st) {
   if (c.dtype == MITA_F32)
-    return c.d == 64 ? attend_t<float, 64>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st)
-                     : attend_t<float, 128>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
-  return c.d == 64 ? attend_t<bf16_t, 64>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st)
-                   : attend_t<bf16_t, 128>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, st);
+    return c.d == 64 ? attend_t<float, 64>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, pair_o, pair_lse, st)
+                     : attend_t<float, 128>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, pair_o, pair_lse, st);
+  return c.d == 64 ? attend_t<bf16_t, 64>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, pair_o, pair_lse, st)
+                   : attend_t<bf16_t, 128>(c, q, q_lm, v_lm, rk, rv, idx, perm, offsets, tile_start, o, pair_o, pair_lse, st);
 }
 
 }  // namespace mita

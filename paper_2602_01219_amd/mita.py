@@ -30,12 +30,13 @@ NUM_STAGES = 6
 MAX_LAUNCHES = 16
 STAGES = ("landmarks", "scores", "topk", "gather", "route", "attend")
 MAX_N = 65536
+MAX_S = 4
 
 EXPORTED = ("mita_check", "mita_workspace_size", "mita_status_string", "mita_last_error", "mita_forward",
             "mita_landmarks", "mita_scores", "mita_topk", "mita_gather", "mita_route", "mita_attend",
             "mita_timer_create", "mita_timer_destroy", "mita_timer_reset", "mita_timer_read",
             "mita_forward_timed", "mita_forward_fallbacks", "mita_select_plan", "mita_timer_launches",
-            "mita_forward_noalloc")
+            "mita_forward_noalloc", "mita_landmarks_select", "mita_forward_lm")
 
 
 class CfgStruct(ctypes.Structure):
@@ -74,6 +75,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "mita_forward_fallbacks": (I, [cfgp, P, Z, ctypes.POINTER(ctypes.c_int64), P]),
         "mita_select_plan": (I, [cfgp] + [ctypes.POINTER(ctypes.c_int32)] * 4),
         "mita_landmarks": (I, [cfgp, P, P, P]),
+        "mita_landmarks_select": (I, [cfgp, P, P, P, P]),
+        "mita_forward_lm": (I, [cfgp, P, P, P, P, P, P, Z, P]),
         "mita_scores": (I, [cfgp, P, P, P, P, P, P, Z, P]),
         "mita_topk": (I, [cfgp, P, P, P, Z, P]),
         "mita_gather": (I, [cfgp, P, P, P, P, P, P]),
@@ -174,14 +177,22 @@ def _dev(t):
     return t.device
 
 
-def forward(cfg: Config, q, k, v, o=None, ws=None, stream=None, timer: "Timer" = None):
-    """MiTA forward: o [B, H, N, d]."""
+def forward(cfg: Config, q, k, v, o=None, ws=None, stream=None, timer: "Timer" = None, q_lm=None):
+    """MiTA forward: o [B, H, N, d]. With q_lm [B, H, M, d] given (e.g. from
+    landmarks_select), the forward uses those landmark queries instead of
+    pooling them (mita_forward_lm)."""
     lib = load_library()
     dev = _dev(q)
     if o is None:
         o = torch.empty_like(q)
     ws, nws = _ws(cfg, WS_FORWARD, ws, dev)
     c = cfg.struct()
+    if q_lm is not None:
+        if timer is not None:
+            raise ValueError("the timed forward pools its landmarks")
+        _check(lib.mita_forward_lm(ctypes.byref(c), _p(q), _p(k), _p(v), _p(q_lm), _p(o), _p(ws), nws,
+                                   _stream(stream)))
+        return o
     if timer is None:
         st = lib.mita_forward(ctypes.byref(c), _p(q), _p(k), _p(v), _p(o), _p(ws), nws, _stream(stream))
     else:
@@ -233,6 +244,18 @@ def landmarks(cfg: Config, q, q_lm=None, stream=None):
     return q_lm
 
 
+def landmarks_select(cfg: Config, q, sel, q_lm=None, stream=None):
+    """Random-selection landmarks: q_lm[b, h, i] = q[b, h, sel[b, h, i]];
+    sel: [B, H, M] int32 device tensor of drawn token indices."""
+    lib = load_library()
+    if sel.dtype != torch.int32 or tuple(sel.shape) != (cfg.B, cfg.H, cfg.M) or not sel.is_contiguous():
+        raise ValueError("sel must be a contiguous [B, H, M] int32 tensor")
+    if q_lm is None:
+        q_lm = torch.empty((cfg.B, cfg.H, cfg.M, cfg.d), dtype=q.dtype, device=_dev(q))
+    _check(lib.mita_landmarks_select(ctypes.byref(cfg.struct()), _p(q), _p(sel), _p(q_lm), _stream(stream)))
+    return q_lm
+
+
 def scores(cfg: Config, q_lm, k, v=None, want_scores=True, want_v_lm=True, ws=None, stream=None):
     """Returns (scores [B,H,M,N] fp32 or None, v_lm [B,H,M,d] or None)."""
     lib = load_library()
@@ -263,12 +286,17 @@ def gather(cfg: Config, k, v, idx, stream=None):
 
 
 def route(cfg: Config, q, q_lm, ws=None, stream=None):
-    """Returns (expert [B,H,N], perm [B,H,N], offsets [B,H,M+1]) int32."""
+    """Returns (expert, perm, offsets) int32: with s = 1 expert [B,H,N],
+    perm [B,H,N], offsets [B,H,M+1]; with s > 1 expert [B,H,N,s] (rank
+    order), perm [B,H,N*s] (pair ids n*s+j grouped into 2M groups),
+    offsets [B,H,2M+1]."""
     lib = load_library()
     dev = _dev(q)
-    expert = torch.empty((cfg.B, cfg.H, cfg.N), dtype=torch.int32, device=dev)
-    perm = torch.empty((cfg.B, cfg.H, cfg.N), dtype=torch.int32, device=dev)
-    offsets = torch.empty((cfg.B, cfg.H, cfg.M + 1), dtype=torch.int32, device=dev)
+    s = cfg.s if cfg.use_routed else 1
+    G = 2 * cfg.M if s > 1 else cfg.M
+    expert = torch.empty((cfg.B, cfg.H, cfg.N) + ((s,) if s > 1 else ()), dtype=torch.int32, device=dev)
+    perm = torch.empty((cfg.B, cfg.H, cfg.N * s), dtype=torch.int32, device=dev)
+    offsets = torch.empty((cfg.B, cfg.H, G + 1), dtype=torch.int32, device=dev)
     ws, nws = _ws(cfg, WS_ROUTE, ws, dev)
     _check(lib.mita_route(ctypes.byref(cfg.struct()), _p(q), _p(q_lm), _p(expert), _p(perm), _p(offsets), _p(ws),
                           nws, _stream(stream)))

@@ -239,3 +239,15 @@ def generate(wl: Workload, seed: Optional[int] = None, B: Optional[int] = None,
 def small(wl: Workload, **kw) -> Workload:
     """A reduced copy of a workload for tests (same recipe, other sizes)."""
     return wl.with_(**kw)
+
+
+def landmark_draw(wl: Workload, seed: Optional[int] = None) -> np.ndarray:
+    """Random-selection landmark draw (the method's random numbers, passed in as
+    an input): for every (b, h) slice, M distinct token indices drawn uniformly
+    without replacement, in draw order. Returns int32 [B, H, M]."""
+    rng = np.random.Generator(np.random.PCG64((wl.seed if seed is None else seed) + 7919))
+    out = np.empty((wl.B, wl.H, wl.M), dtype=np.int32)
+    for b in range(wl.B):
+        for h in range(wl.H):
+            out[b, h] = rng.permutation(wl.N)[:wl.M]
+    return out

@@ -29,7 +29,12 @@ static mita_cfg_t base() {
 int main() {
   EXPECT((void)0, MITA_OK);
   EXPECT(c.d = 96, MITA_ERR_UNSUPPORTED);
-  EXPECT(c.s = 2, MITA_ERR_UNSUPPORTED);
+  EXPECT(c.s = 2, MITA_OK);
+  EXPECT(c.s = MITA_MAX_S, MITA_OK);
+  EXPECT(c.s = MITA_MAX_S + 1, MITA_ERR_UNSUPPORTED);
+  EXPECT(c.s = 0, MITA_ERR_UNSUPPORTED);
+  EXPECT((c.M = 2, c.lm_h = 1, c.lm_w = 2, c.s = 3), MITA_ERR_INVALID_ARG);  // s > M
+  EXPECT((c.M = 2, c.lm_h = 1, c.lm_w = 2, c.s = 3, c.use_routed = 0), MITA_OK);
   EXPECT(c.dtype = 7, MITA_ERR_UNSUPPORTED);
   EXPECT(c.N = 70000, MITA_ERR_INVALID_ARG);                       // grid no longer matches
   EXPECT((c.N = 131072, c.grid_h = 256, c.grid_w = 512), MITA_ERR_UNSUPPORTED);
@@ -53,7 +58,7 @@ int main() {
   mita::FwdLayout L = mita::forward_layout(c);
   const size_t offs[] = {L.q_lm,      L.v_lm,   L.scores, L.partial, L.idx,     L.kx,   L.vx,
                          L.expert,    L.perm,   L.offsets, L.tile_cnt, L.tile_base, L.counts, L.tile_start,
-                         L.plo,    L.ccnt,   L.cand,    L.fail,    L.total};
+                         L.group,  L.pair_o, L.pair_lse, L.plo,    L.ccnt,   L.cand,    L.fail,    L.total};
   for (size_t i = 0; i + 1 < sizeof offs / sizeof offs[0]; ++i) {
     assert(offs[i] % 256 == 0);
     assert(offs[i] <= offs[i + 1]);
@@ -103,6 +108,18 @@ int main() {
   assert(mita::list_in_lds(6656, 137216) && !mita::list_in_lds(6657, 137216));
   assert(mita::list_in_lds(8192, 16384) && !mita::list_in_lds(8193, 16384));
   assert(mita::list_in_lds(8192, 32768) && !mita::list_in_lds(8192, 163840 - 32767));
+  // s > 1: (query, rank) pairs in 2 M groups; the pairs' partials and log-sum-exps
+  c = base();
+  c.s = 2;
+  assert(mita::route_groups(c) == 256 && mita::route_items(c) == 32768 && mita::route_tiles(c) == 512);
+  mita::FwdLayout L3 = mita::forward_layout(c);
+  assert(L3.perm - L3.expert == (size_t)24 * 16384 * 2 * 4);
+  assert(L3.tile_start - L3.counts == (size_t)24 * 256 * 4);
+  assert(L3.pair_lse - L3.pair_o == (size_t)24 * 16384 * 2 * 64 * 4);
+  assert(mita::workspace_size(&c, MITA_WS_ATTEND) ==
+         mita::align_up((size_t)24 * 257 * 4) + (size_t)24 * 16384 * 2 * 64 * 4 + (size_t)24 * 16384 * 2 * 4);
+  c.use_routed = 0;  // s does not matter without routing
+  assert(!mita::multi_route(c) && mita::forward_layout(c).pair_o == mita::forward_layout(c).pair_lse);
   c = base();
   c.d = 96;
   assert(mita::workspace_size(&c, MITA_WS_FORWARD) == 0);

@@ -692,7 +692,7 @@ def test_invalid_arguments_launch_nothing():
                                 mita._p(ws_), ws_.numel() if nws is None else nws, st)
 
     assert call(dataclasses.replace(cfg, d=96)) == mita.MITA_ERR_UNSUPPORTED
-    assert call(dataclasses.replace(cfg, s=2)) == mita.MITA_ERR_UNSUPPORTED
+    assert call(dataclasses.replace(cfg, s=mita.MAX_S + 1)) == mita.MITA_ERR_UNSUPPORTED
     assert call(dataclasses.replace(cfg, k=cfg.N + 1)) == mita.MITA_ERR_INVALID_ARG
     assert call(dataclasses.replace(cfg, use_shared=0, use_routed=0)) == mita.MITA_ERR_INVALID_ARG
     assert call(cfg, nws=ws.numel() - 1) == mita.MITA_ERR_WORKSPACE

@@ -1,0 +1,275 @@
+"""GPU parity of the s > 1 routing and of random-selection landmarks, through
+the C ABI, against the CPU oracle.
+
+s > 1 (Sec. 3.2 e_j(q); Eq. mita with K* = [Q_lm, K^(e_1), ..., K^(e_s)]):
+the GPU's ranked experts are validated against the oracle's float64 logits
+within their rounding budget (the chosen s form a valid top-s, in
+non-increasing order, up to the budget), the pair grouping must equal the
+oracle's pair_grouping of those experts exactly, and the outputs are compared
+with the oracle given the GPU's discrete choices: every row of the compared
+slices against the expert-wise form (output_pairs) and sampled rows against
+the per-query form, max|o_gpu - o_ref| / max|o_ref| <= 1e-5 (fp32) / 2e-2
+(bf16).
+
+Random selection (Tab. A1): the drawn indices are an input (synth.landmark_draw);
+the landmark rows must be bit-identical copies, and the forward with them is
+compared like the pooled forward.
+"""
+from __future__ import annotations
+
+import dataclasses
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import mita_oracle as O
+from paper_2602_01219_amd import mita, synth
+from tests.gpu_helpers import U, check_selection, from_dev, log, maxrel, to_dev, tol_for
+from tests.test_gpu_parity import _bounds
+
+pytestmark = pytest.mark.gpu
+
+
+@functools.lru_cache(maxsize=None)
+def _inputs(name: str, B=None, H=None):
+    wl = synth.WORKLOADS[name]
+    return synth.generate(wl, B=B, H=H)
+
+
+def _dev(inp):
+    return tuple(to_dev(x, inp.wl.dtype) for x in (inp.q, inp.k, inp.v))
+
+
+def _slice64(inp, b, h):
+    if inp.wl.dtype == "f32":
+        return tuple(x[b, h].astype(np.float64) for x in (inp.q, inp.k, inp.v))
+    return tuple(synth.bf16_bits_to_f32(x[b, h]).astype(np.float64) for x in (inp.q, inp.k, inp.v))
+
+
+def _same(a, b):
+    return torch.equal(a.view(torch.int16), b.view(torch.int16)) if a.dtype == torch.bfloat16 else torch.equal(a, b)
+
+
+def check_top_routing(L, tau, ex):
+    """ex [N, s]: distinct landmarks; every chosen one within the budget of
+    every unchosen one; consecutive ranks non-increasing within the budget.
+    Returns the number of queries whose ranked list equals the oracle's."""
+    N, M = L.shape
+    s = ex.shape[1]
+    assert ex.min() >= 0 and ex.max() < M
+    rows = np.arange(N)[:, None]
+    srt = np.sort(ex, axis=1)
+    assert (np.diff(srt, axis=1) > 0).all(), "repeated expert"
+    chosen = np.zeros((N, M), dtype=bool)
+    chosen[rows, ex] = True
+    hi = np.where(chosen, L + tau, np.inf).min(axis=1)
+    lo = np.where(~chosen, L - tau, -np.inf).max(axis=1)
+    assert (hi >= lo).all(), f"top-s outside the rounding budget at {np.nonzero(hi < lo)[0][:5]}"
+    up = L[rows, ex[:, :-1]] + tau[rows, ex[:, :-1]]
+    dn = L[rows, ex[:, 1:]] - tau[rows, ex[:, 1:]]
+    assert (up >= dn).all(), "ranks out of order beyond the rounding budget"
+    ref = np.stack([np.lexsort((np.arange(M), -L[n]))[:s] for n in range(N)])
+    return int((ref == ex).all(axis=1).sum())
+
+
+S_CASES = [("tiny_f32", 2, None), ("tiny_f32", 4, None), ("vits_bf16", 2, 8), ("vits_bf16", 3, 8),
+           ("vitb_hr_bf16", 2, 2), ("dense_pred_bf16", 2, 1), ("dense_pred_bf16", 4, 1), ("long_bf16", 2, 1)]
+
+
+@pytest.mark.parametrize("name,s,B", S_CASES, ids=[f"{c[0]}_s{c[1]}" for c in S_CASES])
+def test_top_s_routing_parity(name, s, B):
+    inp = _inputs(name, B=B)
+    wl = inp.wl
+    cfg = dataclasses.replace(mita.Config.from_workload(wl), s=s)
+    q, k, v = _dev(inp)
+    q_lm = mita.landmarks(cfg, q)
+    expert, perm, offsets = mita.route(cfg, q, q_lm)
+    assert tuple(expert.shape) == (wl.B, wl.H, wl.N, s)
+    assert tuple(perm.shape) == (wl.B, wl.H, wl.N * s) and tuple(offsets.shape) == (wl.B, wl.H, 2 * wl.M + 1)
+    q_lm_g = from_dev(q_lm)
+    e_all, p_all, o_all = expert.cpu().numpy(), perm.cpu().numpy(), offsets.cpu().numpy()
+    for (b, h) in sorted({(0, 0), (wl.B - 1, wl.H - 1)}):
+        qs = _slice64(inp, b, h)[0]
+        L = (qs @ q_lm_g[b, h].T) * cfg.eff_scale               # identical landmark input
+        tau = cfg.eff_scale * 2.0 * (cfg.d + 2) * U * (np.abs(qs) @ np.abs(q_lm_g[b, h]).T) + 1e-30
+        agree = check_top_routing(L, tau, e_all[b, h].astype(np.int64))
+        log(f"  {name} s={s} slice ({b},{h}): ranked experts equal to the fp64 ranking on {agree}/{wl.N}")
+        g = O.pair_grouping(e_all[b, h], wl.M)
+        assert np.array_equal(p_all[b, h], g.perm)
+        assert np.array_equal(o_all[b, h], g.offsets)
+
+
+def _forward_check(cfg, inp, q, k, v, slices, row_limit, lm_sel=None):
+    """The forward (s >= 1, pooled or selected landmarks) against the oracle
+    given the GPU's discrete choices (validated first)."""
+    wl = inp.wl
+    sel_dev = None if lm_sel is None else torch.from_numpy(lm_sel).cuda()
+    q_lm = mita.landmarks(cfg, q) if sel_dev is None else mita.landmarks_select(cfg, q, sel_dev)
+    o_fwd = mita.forward(cfg, q, k, v) if sel_dev is None else mita.forward(cfg, q, k, v, q_lm=q_lm)
+    # the stage pipeline gives the same bits
+    S, v_lm = mita.scores(cfg, q_lm, k, v)
+    idx = mita.topk(cfg, S)
+    kx, vx = mita.gather(cfg, k, v, idx)
+    expert, perm, offsets = mita.route(cfg, q, q_lm)
+    o_st = mita.attend(cfg, q, q_lm, v_lm, kx, vx, perm, offsets)
+    torch.cuda.synchronize()
+    assert _same(o_fwd, o_st), "forward differs from the stage pipeline"
+    tol = tol_for(cfg.dtype)
+    o_all, idx_all = from_dev(o_fwd), idx.cpu().numpy().astype(np.int64)
+    ex_all = expert.cpu().numpy().astype(np.int64)
+    if ex_all.ndim == 3:
+        ex_all = ex_all[..., None]
+    q_lm_g = from_dev(q_lm)
+    worst = 0.0
+    for (b, h) in slices:
+        qs, ks, vs = _slice64(inp, b, h)
+        if lm_sel is None:
+            q_lm_ref = O.landmarks(qs, cfg.grid_h, cfg.grid_w, cfg.lm_h, cfg.lm_w)
+        else:
+            q_lm_ref = O.landmarks_random(qs, lm_sel[b, h])
+            assert np.array_equal(q_lm_g[b, h], q_lm_ref), "selected landmark rows are not exact copies"
+        S_ref = O.scores(q_lm_ref, ks, cfg.eff_scale)
+        if lm_sel is None:
+            # budgets with the rounding of the pooled landmarks (as for s = 1)
+            tau_s, tau_r = _bounds(qs, ks, q_lm_ref, cfg, cfg.dtype)
+        else:
+            # the selected landmarks are exact: dot-product rounding only
+            sc, d = cfg.eff_scale, cfg.d
+            tau_s = sc * 2.0 * (d + 2) * U * (np.abs(q_lm_ref) @ np.abs(ks).T) + 1e-30
+            tau_r = sc * 2.0 * (d + 2) * U * (np.abs(qs) @ np.abs(q_lm_ref).T) + 1e-30
+        check_selection(S_ref, tau_s, idx_all[b, h], cfg.k)
+        L = (qs @ q_lm_ref.T) * cfg.eff_scale
+        check_top_routing(L, tau_r, ex_all[b, h])
+        v_lm_ref = O.landmark_values(S_ref, vs)
+        kx_r, vx_r = O.gather(ks, vs, idx_all[b, h])
+        ref = O.output_pairs(qs, q_lm_ref, v_lm_ref, kx_r, vx_r, ex_all[b, h], cfg.eff_scale, cfg.use_shared,
+                             cfg.use_routed)
+        err = maxrel(o_all[b, h], ref)
+        rows = np.arange(wl.N) if wl.N <= row_limit else np.random.default_rng(b + h).choice(wl.N, row_limit, False)
+        ref_q = O.output_per_query(qs[rows], q_lm_ref, v_lm_ref, kx_r, vx_r, ex_all[b, h][rows], cfg.eff_scale,
+                                   cfg.use_shared, cfg.use_routed)
+        err_q = maxrel(o_all[b, h][rows], ref_q)
+        log(f"  slice ({b},{h}): every row (pair form) max-rel {err:.3e}; {len(rows)} rows (per-query form) "
+            f"{err_q:.3e} (tol {tol})")
+        worst = max(worst, err, err_q)
+        assert err <= tol and err_q <= tol
+    return worst
+
+
+F_CASES = [("tiny_f32", 2, None, 1), ("tiny_f32", 3, None, 1), ("vits_bf16", 2, 4, 4), ("vits_bf16", 4, 4, 4),
+           ("vitb_hr_bf16", 2, 1, 2), ("dense_pred_bf16", 2, 1, 1), ("dense_pred_bf16", 3, 1, 1)]
+
+
+@pytest.mark.parametrize("name,s,B,nsl", F_CASES, ids=[f"{c[0]}_s{c[1]}" for c in F_CASES])
+def test_forward_s_end_to_end(name, s, B, nsl):
+    inp = _inputs(name, B=B)
+    wl = inp.wl
+    cfg = dataclasses.replace(mita.Config.from_workload(wl), s=s)
+    q, k, v = _dev(inp)
+    log(f"[forward s={s}] {name} B={wl.B} H={wl.H} N={wl.N} M={wl.M} k={wl.k}")
+    slices = [(b, h) for b in range(wl.B) for h in range(wl.H)][:nsl]
+    _forward_check(cfg, inp, q, k, v, slices, row_limit=256)
+
+
+@pytest.mark.parametrize("flags", [(0, 1), (1, 0)])
+def test_forward_s_with_one_branch(flags):
+    inp = _inputs("vits_bf16", B=2)
+    cfg = dataclasses.replace(mita.Config.from_workload(inp.wl), s=3, use_shared=flags[0], use_routed=flags[1])
+    q, k, v = _dev(inp)
+    _forward_check(cfg, inp, q, k, v, [(0, 0), (1, 5)], row_limit=196)
+
+
+@pytest.mark.parametrize("s", [2, 4])
+def test_route_only_k_eq_N_with_s_experts_is_dense_attention(s):
+    # every expert holds every key, each key enters s times: dense attention
+    wl = synth.WORKLOADS["dense_equiv_bf16"].with_(H=4)
+    inp = synth.generate(wl)
+    cfg = dataclasses.replace(mita.Config.from_workload(wl), s=s)
+    q, k, v = _dev(inp)
+    o = mita.forward(cfg, q, k, v).float()
+    ref = torch.nn.functional.scaled_dot_product_attention(q.float(), k.float(), v.float())
+    err = ((o - ref).abs().amax() / ref.abs().amax()).item()
+    log(f"  s={s} route-only k=N vs SDPA (fp32): max-rel {err:.3e}")
+    assert err <= tol_for("bf16")
+
+
+@pytest.mark.parametrize("s", [2, 3])
+def test_forward_s_flag_paths_agree(s):
+    inp = _inputs("vitb_hr_bf16", B=1)
+    cfg = dataclasses.replace(mita.Config.from_workload(inp.wl), s=s)
+    q, k, v = _dev(inp)
+    o0 = mita.forward(cfg, q, k, v)
+    o1 = mita.forward(dataclasses.replace(cfg, staged_gather=True), q, k, v)
+    o2 = mita.forward(dataclasses.replace(cfg, full_scores=True), q, k, v)
+    o3 = mita.forward(cfg, q, k, v)
+    torch.cuda.synchronize()
+    assert _same(o0, o1) and _same(o0, o2) and _same(o0, o3)
+
+
+def test_s_one_and_multi_share_the_rank_one_expert():
+    # the s = 2 forward's rank-1 experts are the s = 1 routing's experts
+    inp = _inputs("vits_bf16", B=4)
+    cfg = mita.Config.from_workload(inp.wl)
+    q, k, v = _dev(inp)
+    q_lm = mita.landmarks(cfg, q)
+    e1, _, _ = mita.route(cfg, q, q_lm)
+    e2, _, _ = mita.route(dataclasses.replace(cfg, s=2), q, q_lm)
+    assert torch.equal(e1, e2[..., 0])
+
+
+# ------------------------------------------------------------------ random selection
+R_CASES = [("tiny_f32", None, 1), ("vits_bf16", 4, 4), ("vitb_hr_bf16", 1, 2), ("dense_pred_bf16", 1, 1)]
+
+
+@pytest.mark.parametrize("name,B,nsl", R_CASES, ids=[c[0] for c in R_CASES])
+def test_random_selection_forward(name, B, nsl):
+    inp = _inputs(name, B=B)
+    wl = inp.wl
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = _dev(inp)
+    sel = synth.landmark_draw(wl)
+    log(f"[random landmarks] {name} B={wl.B} H={wl.H} N={wl.N} M={wl.M}")
+    slices = [(b, h) for b in range(wl.B) for h in range(wl.H)][:nsl]
+    _forward_check(cfg, inp, q, k, v, slices, row_limit=256, lm_sel=sel)
+
+
+def test_random_selection_with_s_experts():
+    inp = _inputs("vits_bf16", B=2)
+    cfg = dataclasses.replace(mita.Config.from_workload(inp.wl), s=2)
+    q, k, v = _dev(inp)
+    _forward_check(cfg, inp, q, k, v, [(0, 0), (1, 5)], row_limit=196, lm_sel=synth.landmark_draw(inp.wl))
+
+
+def test_forward_with_pooled_landmarks_given_equals_forward():
+    inp = _inputs("vitb_hr_bf16", B=1)
+    cfg = mita.Config.from_workload(inp.wl)
+    q, k, v = _dev(inp)
+    o1 = mita.forward(cfg, q, k, v)
+    o2 = mita.forward(cfg, q, k, v, q_lm=mita.landmarks(cfg, q))
+    torch.cuda.synchronize()
+    assert _same(o1, o2)
+
+
+def test_selected_landmark_out_of_range_gives_nan_rows():
+    inp = _inputs("tiny_f32")
+    cfg = mita.Config.from_workload(inp.wl)
+    q, _, _ = _dev(inp)
+    sel = torch.from_numpy(synth.landmark_draw(inp.wl)).cuda()
+    sel[0, 0, 3] = cfg.N
+    sel[0, 0, 5] = -1
+    q_lm = mita.landmarks_select(cfg, q, sel).cpu()
+    assert torch.isnan(q_lm[0, 0, 3]).all() and torch.isnan(q_lm[0, 0, 5]).all()
+    ok = [i for i in range(cfg.M) if i not in (3, 5)]
+    assert torch.equal(q_lm[0, 0, ok], q.cpu()[0, 0, sel.cpu()[0, 0, ok].long()])
+
+
+def test_s_limits_are_rejected():
+    inp = _inputs("tiny_f32")
+    cfg = mita.Config.from_workload(inp.wl)
+    assert mita.check(dataclasses.replace(cfg, s=5)) == mita.MITA_ERR_UNSUPPORTED
+    assert mita.check(dataclasses.replace(cfg, s=0)) == mita.MITA_ERR_UNSUPPORTED
+    small = dataclasses.replace(cfg, M=2, lm_h=1, lm_w=2, s=3)
+    assert mita.check(small) == mita.MITA_ERR_INVALID_ARG
+    assert mita.check(dataclasses.replace(small, use_routed=0)) == mita.MITA_OK
