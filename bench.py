@@ -57,19 +57,25 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def kernel_work(name: str, wl, plan: dict, staged: bool):
+def kernel_work(name: str, wl, plan: dict, staged: bool, s: int = 1):
     """Algorithmic (bytes, flops) of one launch of kernel `name`: the tensors
     its step must read and write at least (inputs once, outputs once) and its
     multiply-adds x 2. Intermediate buffers of this design (score-pass
-    partials, candidate lists) are not counted."""
+    partials, candidate lists) are not counted, except, with s > 1 routed
+    experts, the pairs' partial results, which the expert-wise evaluation
+    must write and merge."""
     e = 4 if wl.dtype == "f32" else 2
     BH, N, d, M, k = wl.BH, wl.N, wl.d, wl.M, wl.k
     sh, rt = wl.use_shared, wl.use_routed
+    s = s if rt else 1
     rows = BH * M
     tens = BH * N * d * e            # one of q, k, v, o
     lmt = BH * M * d * e             # q_lm or v_lm
     nch = -(-N // SCORE_NC)
-    ntiles = -(-N // ROUTE_TQ)
+    G = 2 * M if s > 1 else M        # routing groups
+    NP = N * s                       # routing items
+    ntiles = -(-NP // ROUTE_TQ)
+    pairs = BH * NP * (d + 1) * 4 if s > 1 else 0  # fp32 partials and log-sum-exps
     ns = plan.get("ns") or 0
     stored_s = rt and not plan.get("fused")
     w = {
@@ -84,12 +90,17 @@ def kernel_work(name: str, wl, plan: dict, staged: bool):
         "topk_kernel": (4 * BH * M * N + 4 * rows * k, 0),
         "gather_kernel": (rows * k * (4 + 4 * d * e), 0),
         "route_logits_kernel": (tens + lmt + 4 * BH * N, 2 * N * M * d * BH),
-        "route_scan_kernel": (8 * BH * ntiles * M, 0),
-        "route_scatter_kernel": (8 * BH * N + 4 * BH * ntiles * M, 0),
-        "worklist_kernel": (8 * BH * (M + 1), 0),
-        "zero_kernel": (4 * BH * M, 0),
+        "route_scan_kernel": (8 * BH * ntiles * G, 0),
+        "route_scatter_kernel": (8 * BH * NP + 4 * BH * ntiles * G, 0),
+        "route_tops_kernel": (tens + lmt + 8 * BH * NP, 2 * N * M * d * BH),
+        "pair_count_kernel": (4 * BH * NP + 4 * BH * ntiles * G, 0),
+        "combine_kernel": (pairs + tens, 0),
+        "select_landmarks_kernel": (2 * lmt + 4 * rows, 0),
+        "worklist_kernel": (8 * BH * (G + 1), 0),
+        "zero_kernel": (4 * BH * G, 0),
     }
-    att = (2 * tens + 2 * BH * M * k * d * e * rt + 2 * lmt * sh, 4 * N * (M * sh + k * rt) * d * BH)
+    att = (2 * tens + 2 * BH * M * k * d * e * rt + 2 * lmt * sh + (pairs - tens if s > 1 else 0),
+           4 * N * (M * sh + k * s * rt) * d * BH)
     w["attend16_kernel"] = att
     w["attend_kernel"] = att
     return w.get(name, (0, 0))
@@ -205,30 +216,60 @@ def run(wl, name, a, dense: bool):
         return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda()
 
     q, k, v = dev(inp.q), dev(inp.k), dev(inp.v)
-    cfg = mita.Config.from_workload(wl, staged_gather=a.staged_gather, full_scores=a.full_scores)
+    s_exp = a.s if wl.use_routed else 1
+    cfg = mita.Config.from_workload(wl, staged_gather=a.staged_gather, full_scores=a.full_scores, s=s_exp)
     plan = mita.select_plan(cfg)
     o = torch.empty_like(q)
     ws = torch.empty(mita.workspace_size(cfg), dtype=torch.uint8, device="cuda")
-    eprint(f"[bench] workspace {ws.numel() / 2**20:.1f} MiB; selection {plan}")
+    eprint(f"[bench] s = {s_exp}, landmarks by {a.landmarks}; workspace {ws.numel() / 2**20:.1f} MiB; "
+           f"selection {plan}")
+    random_lm = a.landmarks == "random"
+    if random_lm:
+        # random selection: the draw is an input; a step selects the landmark
+        # rows, then runs the forward from them
+        sel = torch.from_numpy(synth.landmark_draw(wl)).cuda()
+        q_lm = torch.empty((wl.B, wl.H, wl.M, wl.d), dtype=q.dtype, device="cuda")
+
+    def step(timer=None):
+        if random_lm:
+            mita.landmarks_select(cfg, q, sel, q_lm=q_lm)
+            mita.forward(cfg, q, k, v, o=o, ws=ws, timer=timer, q_lm=q_lm)
+        else:
+            mita.forward(cfg, q, k, v, o=o, ws=ws, timer=timer)
+
     for _ in range(a.warmup):
-        mita.forward(cfg, q, k, v, o=o, ws=ws)
+        step()
     torch.cuda.synchronize()
 
-    # timed region: plain forwards, as a caller runs them
+    # timed region: whole steps, as a caller runs them
     t0 = time.perf_counter()
     for _ in range(a.steps):
-        mita.forward(cfg, q, k, v, o=o, ws=ws)
+        step()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     fallbacks = mita.forward_fallbacks(cfg, ws)
     # per-kernel times: the same number of forwards right after, with one HIP
     # event behind each launch on the launch stream (the events add a few
-    # microseconds per forward, so they stay out of the timed region above)
+    # microseconds per forward, so they stay out of the timed region above);
+    # random selection's landmark copy is timed with events of its own
     timer = mita.Timer(a.steps)
+    sel_ev = []
     for _ in range(a.steps):
-        mita.forward(cfg, q, k, v, o=o, ws=ws, timer=timer)
+        if random_lm:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            mita.landmarks_select(cfg, q, sel, q_lm=q_lm)
+            e1.record()
+            sel_ev.append((e0, e1))
+            mita.forward(cfg, q, k, v, o=o, ws=ws, timer=timer, q_lm=q_lm)
+        else:
+            mita.forward(cfg, q, k, v, o=o, ws=ws, timer=timer)
     per_call = timer.launches()
     timer.close()
+    if random_lm:
+        torch.cuda.synchronize()
+        per_call = [call + [("select_landmarks_kernel", 0, e0.elapsed_time(e1))]
+                    for call, (e0, e1) in zip(per_call, sel_ev)]
     # cold caches (secondary figure): before each forward, reading 512 MiB
     # evicts the inputs from L2 and the 256 MiB MALL; each forward is timed
     # alone with events on the launch stream and the median is reported
@@ -238,7 +279,7 @@ def run(wl, name, a, dense: bool):
         flush.sum()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        mita.forward(cfg, q, k, v, o=o, ws=ws)
+        step()
         e1.record()
         pairs.append((e0, e1))
     torch.cuda.synchronize()
@@ -269,7 +310,7 @@ def run(wl, name, a, dense: bool):
     kernels = []
     for kname, us in sorted(per_kernel.items(), key=lambda x: -x[1]):
         us /= ncalls
-        by, fl = kernel_work(kname, wl, plan, a.staged_gather)
+        by, fl = kernel_work(kname, wl, plan, a.staged_gather, s_exp)
         ent = price(kname, us, by, fl, wl.dtype)
         ent["launches_per_forward"] = round(launches[kname] / ncalls, 2)
         kernels.append(ent)
@@ -301,7 +342,7 @@ def run(wl, name, a, dense: bool):
                 "algorithmic_bytes": dom["algorithmic_bytes"], "algorithmic_flops": dom["algorithmic_flops"]}
 
     cpu = None
-    if not a.no_cpu_baseline and not dense:
+    if not a.no_cpu_baseline and not dense and s_exp == 1 and not random_lm:
         eprint("[bench] timing the CPU oracle on a sample ...")
         cpu = cpu_baseline(wl, inp, a.cpu_budget)
         eprint(f"[bench] cpu oracle {cpu['value']:.1f} tokens/s fp32, {cpu['value_f64']:.1f} fp64 "
@@ -315,7 +356,8 @@ def run(wl, name, a, dense: bool):
                    "d": wl.d, "M": wl.M, "k": wl.k, "grid": [wl.grid_h, wl.grid_w],
                    "use_shared": wl.use_shared, "use_routed": wl.use_routed,
                    "gather": "staged" if a.staged_gather else "in-place",
-                   "select": "fused" if plan["fused"] else "full-scores", "parallelism": "none (1 GPU)"},
+                   "select": "fused" if plan["fused"] else "full-scores", "s": s_exp, "landmarks": a.landmarks,
+                   "parallelism": "none (1 GPU)"},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kernels,
@@ -342,6 +384,9 @@ def main():
     ap.add_argument("--staged-gather", action="store_true", help="materialise expert tiles (flag path)")
     ap.add_argument("--full-scores", action="store_true",
                     help="store the score matrix and select from it (flag path) instead of the fused selection")
+    ap.add_argument("--s", type=int, default=1, help="routed experts per query (Eq. mita)")
+    ap.add_argument("--landmarks", choices=("pool", "random"), default="pool",
+                    help="landmark extraction: 2-D pooling (default) or random selection (Tab. A1)")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of float32 oracle time for cpu_baseline (half as much again in float64)")
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -299,6 +299,9 @@ int mita_timer_launches(mita_timer_t *timer, int call, int cap, const char **ker
                         int32_t *n_launches);
 int mita_forward_timed(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, void *o,
                        void *ws, size_t ws_bytes, mita_stream_t stream, mita_timer_t *timer);
+/* mita_forward_lm with the per-launch timing of mita_forward_timed. */
+int mita_forward_lm_timed(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, const void *q_lm,
+                          void *o, void *ws, size_t ws_bytes, mita_stream_t stream, mita_timer_t *timer);
 
 #ifdef __cplusplus
 }

@@ -284,6 +284,15 @@ int mita_forward_timed(const mita_cfg_t *cfg, const void *q, const void *k, cons
   return forward_impl(cfg, q, k, v, o, ws, ws_bytes, (hipStream_t)stream, timer);
 }
 
+int mita_forward_lm_timed(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, const void *q_lm,
+                          void *o, void *ws, size_t ws_bytes, mita_stream_t stream, mita_timer_t *timer) {
+  g_err.clear();
+  TRY(validate(cfg));
+  TRY(need_ptr(q_lm, "q_lm"));
+  if (!timer) return set_err(MITA_ERR_INVALID_ARG, "timer is NULL");
+  return forward_impl(cfg, q, k, v, o, ws, ws_bytes, (hipStream_t)stream, timer, q_lm);
+}
+
 int mita_forward_fallbacks(const mita_cfg_t *cfg, const void *ws, size_t ws_bytes, int64_t *count,
                            mita_stream_t stream) {
   g_err.clear();

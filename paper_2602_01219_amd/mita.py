@@ -36,7 +36,7 @@ EXPORTED = ("mita_check", "mita_workspace_size", "mita_status_string", "mita_las
             "mita_landmarks", "mita_scores", "mita_topk", "mita_gather", "mita_route", "mita_attend",
             "mita_timer_create", "mita_timer_destroy", "mita_timer_reset", "mita_timer_read",
             "mita_forward_timed", "mita_forward_fallbacks", "mita_select_plan", "mita_timer_launches",
-            "mita_forward_noalloc", "mita_landmarks_select", "mita_forward_lm")
+            "mita_forward_noalloc", "mita_landmarks_select", "mita_forward_lm", "mita_forward_lm_timed")
 
 
 class CfgStruct(ctypes.Structure):
@@ -77,6 +77,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "mita_landmarks": (I, [cfgp, P, P, P]),
         "mita_landmarks_select": (I, [cfgp, P, P, P, P]),
         "mita_forward_lm": (I, [cfgp, P, P, P, P, P, P, Z, P]),
+        "mita_forward_lm_timed": (I, [cfgp, P, P, P, P, P, P, Z, P, P]),
         "mita_scores": (I, [cfgp, P, P, P, P, P, P, Z, P]),
         "mita_topk": (I, [cfgp, P, P, P, Z, P]),
         "mita_gather": (I, [cfgp, P, P, P, P, P, P]),
@@ -188,10 +189,13 @@ def forward(cfg: Config, q, k, v, o=None, ws=None, stream=None, timer: "Timer" =
     ws, nws = _ws(cfg, WS_FORWARD, ws, dev)
     c = cfg.struct()
     if q_lm is not None:
-        if timer is not None:
-            raise ValueError("the timed forward pools its landmarks")
-        _check(lib.mita_forward_lm(ctypes.byref(c), _p(q), _p(k), _p(v), _p(q_lm), _p(o), _p(ws), nws,
-                                   _stream(stream)))
+        if timer is None:
+            st = lib.mita_forward_lm(ctypes.byref(c), _p(q), _p(k), _p(v), _p(q_lm), _p(o), _p(ws), nws,
+                                     _stream(stream))
+        else:
+            st = lib.mita_forward_lm_timed(ctypes.byref(c), _p(q), _p(k), _p(v), _p(q_lm), _p(o), _p(ws), nws,
+                                           _stream(stream), timer.handle)
+        _check(st)
         return o
     if timer is None:
         st = lib.mita_forward(ctypes.byref(c), _p(q), _p(k), _p(v), _p(o), _p(ws), nws, _stream(stream))
