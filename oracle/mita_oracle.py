@@ -30,6 +30,10 @@ s > 1 the expert-wise form with one partial per (query, expert) pair that
 Sec. 3.2 allows) is provided for cross-checking step 7.
 Landmark queries may also come from random selection of M tokens (Tab. A1),
 the draw being an input.
+The backward pass (backward_slice) gives the gradients of the output with
+respect to q, k and v by the chain rule through Eq. mita, Eq. landmark-value
+and the pooling, the top-k sets and the routing held fixed (they are
+piecewise constant in the inputs and take no gradient).
 
 Readings where the paper is silent or ambiguous (listed in the design doc):
   * pooling windows: start = floor(i*G/g), end = ceil((i+1)*G/g) per axis
@@ -391,3 +395,104 @@ def forward(q, k, v, grid_h, grid_w, lm_h, lm_w, topk, scale=None, use_shared=1,
             o[b, h] = r.o
             res.append(r)
     return o, res
+
+
+# ----------------------------------------------------------------------------
+# Backward pass: gradients of o with respect to q, k, v for an upstream
+# gradient dO, by the chain rule through step 7 (Eq. mita), step 5 (Eq.
+# landmark-value) and step 1 (pooling). The top-k sets I_i and the experts
+# e_j(q) are held fixed: they change only where a score or logit crosses
+# another, so the output is differentiable with them constant.
+# ----------------------------------------------------------------------------
+@dataclass
+class Grads:
+    dq: np.ndarray
+    dk: np.ndarray
+    dv: np.ndarray
+    dq_lm: np.ndarray      # gradient reaching the landmark queries (before pooling)
+    dv_lm: np.ndarray      # gradient reaching the landmark values
+
+
+def attention_backward(q, dO, q_lm, v_lm, k, v, idx, experts, scale, use_shared=1, use_routed=1):
+    """Step 7 backward, per query: z = K*^T q * scale, p = softmax(z),
+    o = V* p. Returns (dq [N, d], dk [N, d], dv [N, d], dq_lm [M, d],
+    dv_lm [M, d]): the routed keys' gradients land on their token rows, the
+    shared keys' on the landmark rows."""
+    N, d = q.shape
+    M = q_lm.shape[0]
+    dq, dk, dv = np.zeros((N, d)), np.zeros((N, d)), np.zeros((N, d))
+    dq_lm, dv_lm = np.zeros((M, d)), np.zeros((M, d))
+    for n in range(N):
+        keys, vals = [], []
+        if use_shared:
+            keys.append(q_lm)
+            vals.append(v_lm)
+        if use_routed:
+            for e in experts[n]:
+                keys.append(k[idx[e]])
+                vals.append(v[idx[e]])
+        Ks = np.concatenate(keys)
+        Vs = np.concatenate(vals)
+        p = softmax_rows((Ks @ q[n]) * scale)
+        dp = Vs @ dO[n]                         # dL/dp_j = dO . v*_j
+        dz = p * (dp - p @ dp)                  # softmax backward
+        dq[n] += scale * (dz @ Ks)
+        j = 0
+        if use_shared:
+            dq_lm += scale * np.outer(dz[:M], q[n])
+            dv_lm += np.outer(p[:M], dO[n])
+            j = M
+        if use_routed:
+            for e in experts[n]:
+                I = idx[e]
+                np.add.at(dk, I, scale * np.outer(dz[j:j + len(I)], q[n]))
+                np.add.at(dv, I, np.outer(p[j:j + len(I)], dO[n]))
+                j += len(I)
+    return dq, dk, dv, dq_lm, dv_lm
+
+
+def landmark_values_backward(S, q_lm, k, v, dv_lm, scale):
+    """Step 5 backward: v_lm = A v with A = softmax(S) over the N keys and
+    S = q_lm k^T * scale. Returns (dq_lm, dk, dv) contributions."""
+    A = softmax_rows(S)
+    dA = dv_lm @ v.T
+    dS = A * (dA - (A * dA).sum(axis=1, keepdims=True))
+    return scale * (dS @ k), scale * (dS.T @ q_lm), A.T @ dv_lm
+
+
+def pooling_backward(dq_lm, grid_h, grid_w, lm_h, lm_w):
+    """Step 1 backward: q_lm_i is the mean of q over window W_i, so each token
+    of W_i receives dq_lm_i / |W_i|. Returns dq [N, d]."""
+    M, d = dq_lm.shape
+    dq = np.zeros((grid_h * grid_w, d))
+    rows = pool_windows(grid_h, lm_h)
+    cols = pool_windows(grid_w, lm_w)
+    for a, (r0, r1) in enumerate(rows):
+        for b, (c0, c1) in enumerate(cols):
+            cnt = (r1 - r0) * (c1 - c0)
+            for rr in range(r0, r1):
+                dq[rr * grid_w + c0: rr * grid_w + c1] += dq_lm[a * lm_w + b] / cnt
+    return dq
+
+
+def backward_slice(q, k, v, dO, grid_h, grid_w, lm_h, lm_w, topk, scale=None,
+                   use_shared=1, use_routed=1, force_idx=None, force_expert=None,
+                   s=1, lm_sel=None) -> Grads:
+    """One (b, h) slice: dq, dk, dv [N, d] for upstream gradient dO [N, d]."""
+    N, d = q.shape
+    if scale is None:
+        scale = float(1.0 / np.sqrt(d))
+    r = forward_slice(q, k, v, grid_h, grid_w, lm_h, lm_w, topk, scale, use_shared, use_routed,
+                      force_idx, force_expert, s=s, lm_sel=lm_sel)
+    dq, dk, dv, dq_lm, dv_lm = attention_backward(q, dO, r.q_lm, r.v_lm, k, v, r.idx, r.experts, scale,
+                                                  use_shared, use_routed)
+    if use_shared:
+        a, b, c = landmark_values_backward(r.S, r.q_lm, k, v, dv_lm, scale)
+        dq_lm = dq_lm + a
+        dk = dk + b
+        dv = dv + c
+    if lm_sel is not None:                      # random selection: q_lm_i = q[sel_i]
+        np.add.at(dq, np.asarray(lm_sel, dtype=np.int64), dq_lm)
+    else:
+        dq = dq + pooling_backward(dq_lm, grid_h, grid_w, lm_h, lm_w)
+    return Grads(dq, dk, dv, dq_lm, dv_lm)

@@ -142,3 +142,53 @@ def test_planted_mistake_in_a_variant_is_caught(monkeypatch, name, mutant, pin):
     monkeypatch.setattr(O, name, mutant)
     with pytest.raises(AssertionError):
         pin()
+
+
+# ---------------------------------------------------------------- backward
+from tests import test_oracle_pins_backward as PB  # noqa: E402
+
+_orig_lvb = O.landmark_values_backward
+_orig_pb = O.pooling_backward
+_orig_ab = O.attention_backward
+
+
+def _lvb_uncentred(S, q_lm, k, v, dv_lm, scale):
+    A = O.softmax_rows(S)
+    dS = A * (dv_lm @ v.T)                      # softmax backward without the centring term
+    return scale * (dS @ k), scale * (dS.T @ q_lm), A.T @ dv_lm
+
+
+def _lvb_dk_unscaled(S, q_lm, k, v, dv_lm, scale):
+    a, b, c = _orig_lvb(S, q_lm, k, v, dv_lm, scale)
+    return a, b / scale, c
+
+
+def _pb_not_averaged(dq_lm, grid_h, grid_w, lm_h, lm_w):
+    rows, cols = O.pool_windows(grid_h, lm_h), O.pool_windows(grid_w, lm_w)
+    out = np.zeros((grid_h * grid_w, dq_lm.shape[1]))
+    for a, (r0, r1) in enumerate(rows):
+        for b, (c0, c1) in enumerate(cols):
+            for rr in range(r0, r1):
+                out[rr * grid_w + c0: rr * grid_w + c1] += dq_lm[a * lm_w + b]
+    return out
+
+
+def _ab_no_dv_lm(q, dO, q_lm, v_lm, k, v, idx, experts, scale, use_shared=1, use_routed=1):
+    dq, dk, dv, dq_lm, dv_lm = _orig_ab(q, dO, q_lm, v_lm, k, v, idx, experts, scale, use_shared, use_routed)
+    return dq, dk, dv, dq_lm, 0 * dv_lm         # the shared values' gradient dropped
+
+
+MUTANTS_BACKWARD = [
+    ("landmark_values_backward", _lvb_uncentred, lambda: PB.test_backward_matches_torch_autograd((1, 1), 1)),
+    ("landmark_values_backward", _lvb_dk_unscaled, lambda: PB.test_backward_matches_torch_autograd((1, 1), 1)),
+    ("pooling_backward", _pb_not_averaged, lambda: PB.test_pooling_backward_is_the_adjoint_of_pooling()),
+    ("attention_backward", _ab_no_dv_lm, lambda: PB.test_backward_matches_torch_autograd((1, 0), 1)),
+]
+
+
+@pytest.mark.parametrize("name,mutant,pin", MUTANTS_BACKWARD, ids=[m[1].__name__ for m in MUTANTS_BACKWARD])
+def test_planted_mistake_in_the_backward_is_caught(monkeypatch, name, mutant, pin):
+    pin()
+    monkeypatch.setattr(O, name, mutant)
+    with pytest.raises(AssertionError):
+        pin()
