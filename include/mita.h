@@ -104,6 +104,7 @@ typedef struct {
 #define MITA_WS_TOPK 2
 #define MITA_WS_ROUTE 3
 #define MITA_WS_ATTEND 4
+#define MITA_WS_BACKWARD 5
 
 /* Host-only validation of cfg (no device needed). Returns a status code. */
 int mita_check(const mita_cfg_t *cfg);
@@ -272,6 +273,27 @@ int mita_attend(const mita_cfg_t *cfg, const void *q, const void *q_lm, const vo
                 void *o, void *ws, size_t ws_bytes, mita_stream_t stream);
 
 /*
+ * Backward pass: the gradients of mita_forward's output o with respect to q,
+ * k and v for an upstream gradient dO, by the chain rule through Eq. mita (the
+ * softmax over the shared and routed keys), Eq. landmark-value (the softmax
+ * over all keys that forms the landmark values) and the pooling of the
+ * landmark queries (Sec. 3.2). The top-k sets (Eq. top-k) and the routing are
+ * held fixed: they change only where two scores or logits cross, so no
+ * gradient flows through a selection or an argmax. The call recomputes them
+ * (and the landmarks and landmark values) from q, k, v exactly as
+ * mita_forward does.
+ *   q, k, v : [B, H, N, d] the forward's inputs;  o : [B, H, N, d] its output;
+ *   dO : [B, H, N, d] upstream gradient;  dq, dk, dv : [B, H, N, d] outputs in
+ *        the io type (must not overlap the inputs or each other).
+ *   ws : >= mita_workspace_size(cfg, MITA_WS_BACKWARD) bytes.
+ * Requires s = 1 when use_routed is set (MITA_ERR_UNSUPPORTED otherwise). The
+ * key-side gradients are summed with fp32 atomic adds, whose order varies:
+ * dk, dv and dq are reproducible only to rounding, not bit for bit.
+ */
+int mita_backward(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, const void *o,
+                  const void *dO, void *dq, void *dk, void *dv, void *ws, size_t ws_bytes, mita_stream_t stream);
+
+/*
  * Per-launch timing of mita_forward with HIP events (profiling aid).
  * A timer holds event slots for up to max_calls forward calls. Each
  * mita_forward_timed call records one event on the stream before its first
@@ -299,6 +321,10 @@ int mita_timer_launches(mita_timer_t *timer, int call, int cap, const char **ker
                         int32_t *n_launches);
 int mita_forward_timed(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, void *o,
                        void *ws, size_t ws_bytes, mita_stream_t stream, mita_timer_t *timer);
+/* mita_backward with the per-launch timing of mita_forward_timed. */
+int mita_backward_timed(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, const void *o,
+                        const void *dO, void *dq, void *dk, void *dv, void *ws, size_t ws_bytes,
+                        mita_stream_t stream, mita_timer_t *timer);
 /* mita_forward_lm with the per-launch timing of mita_forward_timed. */
 int mita_forward_lm_timed(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, const void *q_lm,
                           void *o, void *ws, size_t ws_bytes, mita_stream_t stream, mita_timer_t *timer);

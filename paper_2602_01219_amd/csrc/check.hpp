@@ -296,6 +296,35 @@ inline FwdLayout forward_layout(const mita_cfg_t &c) {
   return L;
 }
 
+// Workspace of mita_backward: the forward's layout (its recomputation
+// fills the landmarks, landmark values, score-pass partials, top-k sets and
+// routing), then the landmark rows' log-sum-exp and the fp32 gradient
+// buffers.
+struct BwdLayout {
+  FwdLayout f;
+  size_t lse_lm, dq_direct, dk_acc, dv_acc, dq_lm_acc, dv_lm_acc, total;
+};
+
+inline BwdLayout backward_layout(const mita_cfg_t &c) {
+  BwdLayout L{};
+  L.f = forward_layout(c);
+  size_t off = L.f.total;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += align_up(bytes);
+    return o;
+  };
+  const size_t bh = (size_t)BH(c), nd = bh * c.N * c.d * 4, md = bh * c.M * c.d * 4;
+  L.lse_lm = take(bh * c.M * 4);
+  L.dq_direct = take(nd);
+  L.dk_acc = take(nd);
+  L.dv_acc = take(nd);
+  L.dq_lm_acc = take(md);
+  L.dv_lm_acc = take(md);
+  L.total = off;
+  return L;
+}
+
 inline size_t workspace_size(const mita_cfg_t *c, int which) {
   if (check_cfg(c, nullptr) != MITA_OK) return 0;
   switch (which) {
@@ -304,6 +333,7 @@ inline size_t workspace_size(const mita_cfg_t *c, int which) {
     case MITA_WS_TOPK: return 0;
     case MITA_WS_ROUTE: return route_ws_bytes(*c);
     case MITA_WS_ATTEND: return attend_ws_bytes(*c);
+    case MITA_WS_BACKWARD: return c->s == 1 || !c->use_routed ? backward_layout(*c).total : 0;
     default: return 0;
   }
 }

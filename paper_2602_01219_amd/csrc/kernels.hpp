@@ -99,4 +99,20 @@ hipError_t launch_attend(const mita_cfg_t &c, const void *q, const void *q_lm, c
 hipError_t launch_select_landmarks(const mita_cfg_t &c, const void *q, const int32_t *sel, void *q_lm,
                                    hipStream_t st);
 
+// Backward pass (gradients with the top-k sets and routing held fixed).
+// Inputs: the forward's tensors and the state its recomputation left in the
+// workspace; accumulators zeroed beforehand.
+struct BwdBufs {
+  const void *q, *k, *v, *o, *dO;  // [BH, N, d]
+  const void *q_lm, *v_lm;         // [BH, M, d]
+  const int32_t *idx, *perm, *offsets, *tile_start;
+  const void *part_ml;             // score-pass partials (max, sum) per key chunk
+  float *lse_lm;                   // [BH, M] (written)
+  float *dq_direct;                // [BH, N, d] (written)
+  float *dk_acc, *dv_acc;          // [BH, N, d] (zeroed)
+  float *dq_lm_acc, *dv_lm_acc;    // [BH, M, d] (zeroed)
+  void *dq, *dk, *dv;              // [BH, N, d] outputs (io type)
+};
+hipError_t launch_backward(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st);
+
 }  // namespace mita

@@ -205,6 +205,119 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
   return MITA_OK;
 }
 
+// The backward pass: the forward's landmarks, selection and routing
+// recomputed into the workspace, then the gradient kernels.
+int backward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *v, const void *o, const void *dO,
+                  void *dq, void *dk, void *dv, void *ws, size_t ws_bytes, hipStream_t st, mita_timer *timer) {
+  TRY(validate(c));
+  if (c->use_routed && c->s != 1) return set_err(MITA_ERR_UNSUPPORTED, "the backward pass supports s = 1 only");
+  for (auto pr : {std::make_pair(q, "q"), std::make_pair(k, "k"), std::make_pair(v, "v"), std::make_pair(o, "o"),
+                  std::make_pair(dO, "dO")})
+    TRY(need_ptr(pr.first, pr.second));
+  TRY(need_ptr(dq, "dq"));
+  TRY(need_ptr(dk, "dk"));
+  TRY(need_ptr(dv, "dv"));
+  const size_t tb = tensor_bytes(c);
+  for (const void *out : {(const void *)dq, (const void *)dk, (const void *)dv}) {
+    for (const void *in : {q, k, v, o, dO})
+      if (overlaps(out, tb, in, tb)) return set_err(MITA_ERR_INVALID_ARG, "a gradient output overlaps an input");
+  }
+  if (overlaps(dq, tb, dk, tb) || overlaps(dq, tb, dv, tb) || overlaps(dk, tb, dv, tb))
+    return set_err(MITA_ERR_INVALID_ARG, "the gradient outputs overlap");
+  TRY(need_ws(c, MITA_WS_BACKWARD, ws, ws_bytes));
+  Recording rec{timer, 0, 0, hipSuccess};
+  if (timer) {
+    if (timer->used >= timer->max_calls) return set_err(MITA_ERR_INVALID_ARG, "timer is full");
+    rec.call = timer->used++;
+    timer->nlaunch[rec.call] = 0;
+    TRY(hip_status(hipEventRecord(timer->ev[(size_t)rec.call * (MITA_MAX_LAUNCHES + 1)], st), "hipEventRecord"));
+  }
+  struct Scope {
+    Recording *prev;
+    explicit Scope(Recording *r) : prev(g_rec) { g_rec = r->t ? r : nullptr; }
+    ~Scope() { g_rec = prev; }
+  } scope(&rec);
+
+  const BwdLayout BL = backward_layout(*c);
+  const FwdLayout &L = BL.f;
+  char *w = (char *)ws;
+  void *q_lm = w + L.q_lm;
+  void *v_lm = c->use_shared ? (void *)(w + L.v_lm) : nullptr;
+  float *S = c->use_routed ? (float *)(w + L.scores) : nullptr;
+  int32_t *idx = (int32_t *)(w + L.idx);
+  int32_t *expert = (int32_t *)(w + L.expert), *perm = (int32_t *)(w + L.perm);
+  int32_t *offsets = (int32_t *)(w + L.offsets), *tile_cnt = (int32_t *)(w + L.tile_cnt);
+  int32_t *tile_base = (int32_t *)(w + L.tile_base), *tile_start = (int32_t *)(w + L.tile_start);
+  int32_t *counts = (int32_t *)(w + L.counts);
+  const bool fused = fused_select(*c);
+  SelectBufs sel{};
+  if (fused) {
+    sel.plo = (uint32_t *)(w + L.plo);
+    sel.ccnt = (uint32_t *)(w + L.ccnt);
+    sel.cand = (uint2 *)(w + L.cand);
+    sel.fail_cnt = (uint32_t *)(w + L.fail);
+    sel.fail_list = (int32_t *)(w + L.fail) + 1;
+    sel.ns = sel_ns(*c);
+    sel.cap = sel_cap(*c);
+    sel.rank = sel_rank(*c);
+  }
+  // recomputation (stages 0 to 4)
+  rec.stage = 0;
+  TRY(hip_status(launch_pool(*c, q, q_lm, c->use_routed ? counts : nullptr, nullptr, st), "landmarks"));
+  rec.stage = 1;
+  if (c->use_routed) {
+    if (fused) {
+      TRY(hip_status(launch_select_pivots(*c, q_lm, k, sel, st), "select pivots"));
+      TRY(hip_status(launch_scores(*c, q_lm, k, v, nullptr, v_lm, w + L.partial, &sel, st), "scores"));
+      rec.stage = 2;
+      TRY(hip_status(launch_select_finish(*c, q_lm, k, sel, S, idx, w + L.partial, v_lm, st), "topk"));
+    } else {
+      TRY(hip_status(launch_scores(*c, q_lm, k, v, S, v_lm, w + L.partial, nullptr, st), "scores"));
+      rec.stage = 2;
+      TRY(hip_status(launch_topk(*c, S, idx, st), "topk"));
+    }
+    rec.stage = 4;
+    TRY(hip_status(launch_route(*c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, nullptr,
+                                st),
+                   "route"));
+  } else {
+    TRY(hip_status(launch_scores(*c, q_lm, k, v, nullptr, v_lm, w + L.partial, nullptr, st), "scores"));
+  }
+  // gradients (stage 5)
+  rec.stage = 5;
+  const int64_t nd = BH(*c) * c->N * c->d, md = BH(*c) * c->M * c->d;
+  TRY(hip_status(launch_zero((int32_t *)(w + BL.dk_acc), nd, st), "backward"));
+  TRY(hip_status(launch_zero((int32_t *)(w + BL.dv_acc), nd, st), "backward"));
+  TRY(hip_status(launch_zero((int32_t *)(w + BL.dq_lm_acc), (int64_t)(BL.total - BL.dq_lm_acc) / 4, st),
+                 "backward"));  // dq_lm_acc and dv_lm_acc
+  BwdBufs b{};
+  b.q = q;
+  b.k = k;
+  b.v = v;
+  b.o = o;
+  b.dO = dO;
+  b.q_lm = q_lm;
+  b.v_lm = v_lm;
+  b.idx = idx;
+  b.perm = perm;
+  b.offsets = offsets;
+  b.tile_start = tile_start;
+  b.part_ml = w + L.partial;
+  b.lse_lm = (float *)(w + BL.lse_lm);
+  b.dq_direct = (float *)(w + BL.dq_direct);
+  b.dk_acc = (float *)(w + BL.dk_acc);
+  b.dv_acc = (float *)(w + BL.dv_acc);
+  b.dq_lm_acc = (float *)(w + BL.dq_lm_acc);
+  b.dv_lm_acc = (float *)(w + BL.dv_lm_acc);
+  b.dq = dq;
+  b.dk = dk;
+  b.dv = dv;
+  (void)md;
+  TRY(hip_status(launch_backward(*c, b, st), "backward"));
+  if (rec.err != hipSuccess) return hip_status(rec.err, "hipEventRecord");
+  return MITA_OK;
+}
+
 }  // namespace
 
 // Workspace of mita_forward_noalloc, for callers that cannot allocate: one
@@ -282,6 +395,20 @@ int mita_forward_timed(const mita_cfg_t *cfg, const void *q, const void *k, cons
   g_err.clear();
   if (!timer) return set_err(MITA_ERR_INVALID_ARG, "timer is NULL");
   return forward_impl(cfg, q, k, v, o, ws, ws_bytes, (hipStream_t)stream, timer);
+}
+
+int mita_backward(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, const void *o, const void *dO,
+                  void *dq, void *dk, void *dv, void *ws, size_t ws_bytes, mita_stream_t stream) {
+  g_err.clear();
+  return backward_impl(cfg, q, k, v, o, dO, dq, dk, dv, ws, ws_bytes, (hipStream_t)stream, nullptr);
+}
+
+int mita_backward_timed(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, const void *o,
+                        const void *dO, void *dq, void *dk, void *dv, void *ws, size_t ws_bytes,
+                        mita_stream_t stream, mita_timer_t *timer) {
+  g_err.clear();
+  if (!timer) return set_err(MITA_ERR_INVALID_ARG, "timer is NULL");
+  return backward_impl(cfg, q, k, v, o, dO, dq, dk, dv, ws, ws_bytes, (hipStream_t)stream, timer);
 }
 
 int mita_forward_lm_timed(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, const void *q_lm,

@@ -25,7 +25,7 @@ MITA_OK, MITA_ERR_INVALID_ARG, MITA_ERR_UNSUPPORTED, MITA_ERR_WORKSPACE, MITA_ER
 MITA_F32, MITA_BF16 = 0, 1
 MITA_FLAG_STAGED_GATHER = 0x1
 MITA_FLAG_FULL_SCORES = 0x2
-WS_FORWARD, WS_SCORES, WS_TOPK, WS_ROUTE, WS_ATTEND = range(5)
+WS_FORWARD, WS_SCORES, WS_TOPK, WS_ROUTE, WS_ATTEND, WS_BACKWARD = range(6)
 NUM_STAGES = 6
 MAX_LAUNCHES = 16
 STAGES = ("landmarks", "scores", "topk", "gather", "route", "attend")
@@ -36,7 +36,8 @@ EXPORTED = ("mita_check", "mita_workspace_size", "mita_status_string", "mita_las
             "mita_landmarks", "mita_scores", "mita_topk", "mita_gather", "mita_route", "mita_attend",
             "mita_timer_create", "mita_timer_destroy", "mita_timer_reset", "mita_timer_read",
             "mita_forward_timed", "mita_forward_fallbacks", "mita_select_plan", "mita_timer_launches",
-            "mita_forward_noalloc", "mita_landmarks_select", "mita_forward_lm", "mita_forward_lm_timed")
+            "mita_forward_noalloc", "mita_landmarks_select", "mita_forward_lm", "mita_forward_lm_timed",
+            "mita_backward", "mita_backward_timed")
 
 
 class CfgStruct(ctypes.Structure):
@@ -78,6 +79,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "mita_landmarks_select": (I, [cfgp, P, P, P, P]),
         "mita_forward_lm": (I, [cfgp, P, P, P, P, P, P, Z, P]),
         "mita_forward_lm_timed": (I, [cfgp, P, P, P, P, P, P, Z, P, P]),
+        "mita_backward": (I, [cfgp, P, P, P, P, P, P, P, P, P, Z, P]),
+        "mita_backward_timed": (I, [cfgp, P, P, P, P, P, P, P, P, P, Z, P, P]),
         "mita_scores": (I, [cfgp, P, P, P, P, P, P, Z, P]),
         "mita_topk": (I, [cfgp, P, P, P, Z, P]),
         "mita_gather": (I, [cfgp, P, P, P, P, P, P]),
@@ -204,6 +207,26 @@ def forward(cfg: Config, q, k, v, o=None, ws=None, stream=None, timer: "Timer" =
                                     timer.handle)
     _check(st)
     return o
+
+
+def backward(cfg: Config, q, k, v, o, dO, dq=None, dk=None, dv=None, ws=None, stream=None,
+             timer: "Timer" = None):
+    """Gradients (dq, dk, dv) [B, H, N, d] of the forward's output o for the
+    upstream gradient dO, the top-k sets and routing held fixed
+    (mita_backward)."""
+    lib = load_library()
+    dev = _dev(q)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    ws, nws = _ws(cfg, WS_BACKWARD, ws, dev)
+    c = cfg.struct()
+    args = [ctypes.byref(c), _p(q), _p(k), _p(v), _p(o), _p(dO), _p(dq), _p(dk), _p(dv), _p(ws), nws, _stream(stream)]
+    if timer is None:
+        _check(lib.mita_backward(*args))
+    else:
+        _check(lib.mita_backward_timed(*args, timer.handle))
+    return dq, dk, dv
 
 
 NOALLOC_SCRATCH_BYTES = 64 << 20

@@ -1,0 +1,133 @@
+"""GPU parity of the backward pass (mita_backward) against the oracle's
+backward_slice, through the C ABI.
+
+The GPU recomputes the forward's top-k sets and routing; they are read back
+through the stage entry points (which the forward tests show equal to the
+forward's own), validated against the oracle's float64 scores and logits
+within their rounding budget, and given to the oracle. dq, dk, dv are then
+compared per (b, h) slice, every row: max|g_gpu - g_ref| / max|g_ref| <= 1e-4
+(fp32) / 3e-2 (bf16). The bf16 bound: the softmax weights and their
+gradients enter the products rounded to bf16 (relative 2^-9 each), dZ = P (dP
+- D) can lose up to a few bits where dP is close to D, and the upstream
+gradient of the landmark values is rounded to bf16 for the landmark-value
+backward; the sums themselves are fp32.
+"""
+from __future__ import annotations
+
+import dataclasses
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import mita_oracle as O
+from paper_2602_01219_amd import mita, synth
+from tests.gpu_helpers import check_routing, check_selection, from_dev, log, maxrel, to_dev
+from tests.test_gpu_parity import _bounds
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 3e-2}
+
+
+@functools.lru_cache(maxsize=None)
+def _inputs(name, B=None, H=None):
+    return synth.generate(synth.WORKLOADS[name], B=B, H=H)
+
+
+def _slice64(inp, b, h):
+    if inp.wl.dtype == "f32":
+        return tuple(x[b, h].astype(np.float64) for x in (inp.q, inp.k, inp.v))
+    return tuple(synth.bf16_bits_to_f32(x[b, h]).astype(np.float64) for x in (inp.q, inp.k, inp.v))
+
+
+def _upstream(wl, seed=17):
+    r = np.random.default_rng(wl.seed + seed)
+    x = (r.standard_normal((wl.B, wl.H, wl.N, wl.d)) / np.sqrt(wl.d)).astype(np.float32)
+    return x if wl.dtype == "f32" else synth.f32_to_bf16_bits(x)
+
+
+def _check_backward(cfg, inp, slices):
+    wl = inp.wl
+    q, k, v = (to_dev(x, wl.dtype) for x in (inp.q, inp.k, inp.v))
+    dO_h = _upstream(wl)
+    dO = to_dev(dO_h, wl.dtype)
+    o = mita.forward(cfg, q, k, v)
+    dq, dk, dv = mita.backward(cfg, q, k, v, o, dO)
+    # the discrete choices the backward recomputed (equal to the forward's)
+    q_lm = mita.landmarks(cfg, q)
+    idx_all = exp_all = None
+    if cfg.use_routed:
+        S, _ = mita.scores(cfg, q_lm, k, v, want_v_lm=False)
+        idx_all = mita.topk(cfg, S).cpu().numpy().astype(np.int64)
+        exp_all = mita.route(cfg, q, q_lm)[0].cpu().numpy().astype(np.int64)
+    torch.cuda.synchronize()
+    g_all = [from_dev(t) for t in (dq, dk, dv)]
+    dO64 = dO_h.astype(np.float64) if wl.dtype == "f32" else synth.bf16_bits_to_f32(dO_h).astype(np.float64)
+    tol = TOL[wl.dtype]
+    worst = 0.0
+    for (b, h) in slices:
+        qs, ks, vs = _slice64(inp, b, h)
+        fi = fe = None
+        if cfg.use_routed:
+            q_lm_ref = O.landmarks(qs, cfg.grid_h, cfg.grid_w, cfg.lm_h, cfg.lm_w)
+            tau_s, tau_r = _bounds(qs, ks, q_lm_ref, cfg, wl.dtype)
+            check_selection(O.scores(q_lm_ref, ks, cfg.eff_scale), tau_s, idx_all[b, h], cfg.k)
+            check_routing((qs @ q_lm_ref.T) * cfg.eff_scale, tau_r, exp_all[b, h])
+            fi, fe = idx_all[b, h], exp_all[b, h]
+        ref = O.backward_slice(qs, ks, vs, dO64[b, h], cfg.grid_h, cfg.grid_w, cfg.lm_h, cfg.lm_w, cfg.k, None,
+                               cfg.use_shared, cfg.use_routed, force_idx=fi, force_expert=fe)
+        errs = [maxrel(g[b, h], r) for g, r in zip(g_all, (ref.dq, ref.dk, ref.dv))]
+        log(f"  slice ({b},{h}): max-rel dq {errs[0]:.3e} dk {errs[1]:.3e} dv {errs[2]:.3e} (tol {tol})")
+        worst = max(worst, *errs)
+        assert max(errs) <= tol, errs
+    return worst
+
+
+CASES = [("tiny_f32", None, None, (1, 1)), ("tiny_f32", None, None, (0, 1)), ("tiny_f32", None, None, (1, 0)),
+         ("vits_bf16", 2, 2, (1, 1)), ("vits_bf16", 2, 2, (0, 1)), ("vits_bf16", 2, 2, (1, 0)),
+         ("vitb_hr_bf16", 1, 2, (1, 1)), ("dense_pred_bf16", 1, 1, (1, 1)), ("long_bf16", 1, 1, (1, 1))]
+
+
+@pytest.mark.parametrize("name,B,H,flags", CASES, ids=[f"{c[0]}_f{c[3][0]}{c[3][1]}" for c in CASES])
+def test_backward_parity(name, B, H, flags):
+    inp = _inputs(name, B, H)
+    wl = inp.wl
+    cfg = mita.Config.from_workload(wl, use_shared=flags[0], use_routed=flags[1])
+    log(f"[backward] {name} B={wl.B} H={wl.H} N={wl.N} d={wl.d} M={wl.M} k={wl.k} flags={flags}")
+    sl = [(b, h) for b in range(wl.B) for h in range(wl.H)]
+    if wl.N > 4096:
+        sl = sl[:1]
+    _check_backward(cfg, inp, sl[:4])
+
+
+def test_backward_dense_equivalence_is_attention_backward():
+    # route-only, one landmark, k = N: the gradients of dense attention
+    wl = synth.WORKLOADS["dense_equiv_bf16"].with_(H=2)
+    inp = synth.generate(wl)
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = (to_dev(x, wl.dtype) for x in (inp.q, inp.k, inp.v))
+    dO = to_dev(_upstream(wl), wl.dtype)
+    o = mita.forward(cfg, q, k, v)
+    dq, dk, dv = mita.backward(cfg, q, k, v, o, dO)
+    tq, tk, tv = (x.float().detach().requires_grad_() for x in (q, k, v))
+    ref = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv)
+    (ref * dO.float()).sum().backward()
+    for name, got, r in (("dq", dq, tq.grad), ("dk", dk, tk.grad), ("dv", dv, tv.grad)):
+        err = ((got.float() - r).abs().amax() / r.abs().amax()).item()
+        log(f"  dense equivalence {name}: max-rel {err:.3e} vs SDPA autograd (fp32)")
+        assert err <= TOL["bf16"]
+
+
+def test_backward_rejects_s_above_one_and_overlaps():
+    inp = _inputs("tiny_f32")
+    cfg = mita.Config.from_workload(inp.wl)
+    q, k, v = (to_dev(x, "f32") for x in (inp.q, inp.k, inp.v))
+    o = mita.forward(cfg, q, k, v)
+    with pytest.raises(mita.MitaError) as ex:
+        mita.backward(dataclasses.replace(cfg, s=2), q, k, v, o, o)
+    assert ex.value.status == mita.MITA_ERR_UNSUPPORTED
+    with pytest.raises(mita.MitaError) as ex:
+        mita.backward(cfg, q, k, v, o, o, dq=q)
+    assert ex.value.status == mita.MITA_ERR_INVALID_ARG
