@@ -41,7 +41,8 @@ SCORE_NC = 512        # keys per score-pass chunk
 ROUTE_TQ = 64         # queries per routing tile
 # kernels priced against MFMA whatever their byte count (the attention: its
 # algorithmic bytes count every expert's k rows, most of which come from L2)
-MFMA_KERNELS = ("attend16_kernel", "attend_kernel")
+MFMA_KERNELS = ("attend16_kernel", "attend_kernel", "bwd_attend_kernel", "bwd_landmark_kernel", "bwd_kv_kernel",
+                "bwd_kv_shared_kernel")
 
 
 def eprint(*a):
@@ -101,6 +102,26 @@ def kernel_work(name: str, wl, plan: dict, staged: bool, s: int = 1):
     }
     att = (2 * tens + 2 * BH * M * k * d * e * rt + 2 * lmt * sh + (pairs - tens if s > 1 else 0),
            4 * N * (M * sh + k * s * rt) * d * BH)
+    # backward (s = 1): inputs once (q, o, dO, the keys and values each
+    # query attends, landmarks) and each gradient contribution once in fp32;
+    # flops of the five products S, dP, dQ, dK, dV (the log-sum-exp pass that
+    # recomputes S is this design's overhead and is not counted)
+    # (per kernel: the products it forms; S and dP are formed both by the
+    # dQ kernel and by the key-owned kernels, so their sum exceeds the
+    # backward's minimum of five products)
+    nkeys = M * sh + k * rt
+    w["bwd_attend_kernel"] = (3 * tens + 2 * BH * M * k * d * e * rt + 2 * lmt * sh + 4 * BH * N * d + 8 * BH * N,
+                              6 * N * nkeys * d * BH)
+    w["bwd_kv_kernel"] = (2 * BH * M * k * d * e + 2 * tens + 8 * BH * N + 8 * BH * M * k * d, 8 * N * k * d * BH * rt)
+    w["bwd_kv_shared_kernel"] = (2 * lmt + 2 * tens + 8 * BH * N + 8 * BH * M * d, 8 * N * M * d * BH * sh)
+    w["inv_count_kernel"] = (4 * BH * M * k + 4 * BH * N, 0)
+    w["inv_scan_kernel"] = (8 * BH * N, 0)
+    w["inv_place_kernel"] = (8 * BH * M * k + 8 * BH * N, 0)
+    w["inv_gather_kernel"] = (8 * BH * M * k * d + 4 * BH * M * k + 8 * BH * N + 8 * BH * N * d, 0)
+    w["bwd_landmark_kernel"] = (2 * lmt + 4 * BH * M * d + 2 * tens + 4 * rows + 8 * BH * N * d + 4 * BH * M * d,
+                                10 * M * N * d * BH * sh)
+    w["bwd_finish_kernel"] = (12 * BH * N * d + 4 * BH * M * d * sh + 3 * tens, 0)
+    w["lse_rows_kernel"] = (8 * BH * nch * M + 4 * rows, 0)
     w["attend16_kernel"] = att
     w["attend_kernel"] = att
     return w.get(name, (0, 0))
@@ -230,7 +251,20 @@ def run(wl, name, a, dense: bool):
         sel = torch.from_numpy(synth.landmark_draw(wl)).cuda()
         q_lm = torch.empty((wl.B, wl.H, wl.M, wl.d), dtype=q.dtype, device="cuda")
 
-    def step(timer=None):
+    if a.backward:
+        r = np.random.default_rng(wl.seed + 17)
+        dO = dev(synth.f32_to_bf16_bits((r.standard_normal((wl.B, wl.H, wl.N, wl.d)) / np.sqrt(wl.d)).astype(
+            np.float32)) if wl.dtype == "bf16" else (r.standard_normal((wl.B, wl.H, wl.N, wl.d)) /
+                                                        np.sqrt(wl.d)).astype(np.float32))
+        grads = tuple(torch.empty_like(x) for x in (q, k, v))
+        ws_b = torch.empty(mita.workspace_size(cfg, mita.WS_BACKWARD), dtype=torch.uint8, device="cuda")
+        eprint(f"[bench] backward workspace {ws_b.numel() / 2**20:.1f} MiB")
+
+    def step(timer=None, timer_b=None):
+        if a.backward:
+            mita.forward(cfg, q, k, v, o=o, ws=ws, timer=timer)
+            mita.backward(cfg, q, k, v, o, dO, *grads, ws=ws_b, timer=timer_b)
+            return
         if random_lm:
             mita.landmarks_select(cfg, q, sel, q_lm=q_lm)
             mita.forward(cfg, q, k, v, o=o, ws=ws, timer=timer, q_lm=q_lm)
@@ -253,9 +287,12 @@ def run(wl, name, a, dense: bool):
     # microseconds per forward, so they stay out of the timed region above);
     # random selection's landmark copy is timed with events of its own
     timer = mita.Timer(a.steps)
+    timer_b = mita.Timer(a.steps) if a.backward else None
     sel_ev = []
     for _ in range(a.steps):
-        if random_lm:
+        if a.backward:
+            step(timer, timer_b)
+        elif random_lm:
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
             mita.landmarks_select(cfg, q, sel, q_lm=q_lm)
@@ -266,6 +303,9 @@ def run(wl, name, a, dense: bool):
             mita.forward(cfg, q, k, v, o=o, ws=ws, timer=timer)
     per_call = timer.launches()
     timer.close()
+    if a.backward:
+        per_call = [f + b_ for f, b_ in zip(per_call, timer_b.launches())]
+        timer_b.close()
     if random_lm:
         torch.cuda.synchronize()
         per_call = [call + [("select_landmarks_kernel", 0, e0.elapsed_time(e1))]
@@ -342,7 +382,7 @@ def run(wl, name, a, dense: bool):
                 "algorithmic_bytes": dom["algorithmic_bytes"], "algorithmic_flops": dom["algorithmic_flops"]}
 
     cpu = None
-    if not a.no_cpu_baseline and not dense and s_exp == 1 and not random_lm:
+    if not a.no_cpu_baseline and not dense and s_exp == 1 and not random_lm and not a.backward:
         eprint("[bench] timing the CPU oracle on a sample ...")
         cpu = cpu_baseline(wl, inp, a.cpu_budget)
         eprint(f"[bench] cpu oracle {cpu['value']:.1f} tokens/s fp32, {cpu['value_f64']:.1f} fp64 "
@@ -352,7 +392,9 @@ def run(wl, name, a, dense: bool):
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": a.steps,
         "warmup": a.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
-        "config": {"workload": name + (" dense reference" if dense else ""), "B": wl.B, "H": wl.H, "N": wl.N,
+        "config": {"workload": name + (" dense reference" if dense else "") + (" forward+backward" if a.backward
+                                                                                  else ""), "B": wl.B, "H": wl.H,
+                   "N": wl.N,
                    "d": wl.d, "M": wl.M, "k": wl.k, "grid": [wl.grid_h, wl.grid_w],
                    "use_shared": wl.use_shared, "use_routed": wl.use_routed,
                    "gather": "staged" if a.staged_gather else "in-place",
@@ -385,6 +427,8 @@ def main():
     ap.add_argument("--full-scores", action="store_true",
                     help="store the score matrix and select from it (flag path) instead of the fused selection")
     ap.add_argument("--s", type=int, default=1, help="routed experts per query (Eq. mita)")
+    ap.add_argument("--backward", action="store_true",
+                    help="time forward + backward steps (gradients of q, k, v for a synthetic upstream gradient)")
     ap.add_argument("--landmarks", choices=("pool", "random"), default="pool",
                     help="landmark extraction: 2-D pooling (default) or random selection (Tab. A1)")
     ap.add_argument("--cpu-budget", type=float, default=12.0,

@@ -306,7 +306,7 @@ int mita_backward(const mita_cfg_t *cfg, const void *q, const void *k, const voi
  * takes no time.
  */
 #define MITA_NUM_STAGES 6
-#define MITA_MAX_LAUNCHES 16
+#define MITA_MAX_LAUNCHES 32
 typedef struct mita_timer mita_timer_t;
 int mita_timer_create(mita_timer_t **timer, int max_calls);
 int mita_timer_destroy(mita_timer_t *timer);

@@ -8,11 +8,9 @@
 //   ATT: a workgroup takes one tile of the forward's work list (64 queries
 //        of one expert); its keys are the shared landmarks (keys q_lm,
 //        values v_lm) and the expert's k routed rows. A first pass over the
-//        keys forms each query's log-sum-exp, a second one the gradients:
-//        dQ stays in registers (a query's keys are all seen here) and is
-//        written once; dK and dV of each key tile, summed over the 64
-//        queries, go by fp32 atomic adds to the keys' rows (token rows for
-//        routed keys, landmark rows for shared ones).
+//        keys forms each query's log-sum-exp (kept for the key side), a
+//        second one dQ, in registers (a query's keys are all seen here),
+//        written once.
 //   LMV: a workgroup takes 64 landmarks (as queries) and one chunk of the
 //        N keys; the upstream gradient is that of the landmark values, the
 //        log-sum-exp of each landmark row comes from the score pass. dQ (the
@@ -28,8 +26,17 @@
 // elements: Q and dO row-major (and, for bf16 at d = 64, transposed; else
 // their columns are read element by element), the key tile row-major and
 // transposed, P and dZ as [key][query] and dZ as [query][key].
-// Summation orders of the atomic adds vary from run to run, so the key-side
-// gradients are not bitwise reproducible (the rounding differs by a few ulp).
+// The keys' gradients of the MiTA attention come from bwd_kv_kernel, where a
+// workgroup owns 64 keys and streams the queries that attend them, so that
+// dK and dV stay in registers: a routed key block of one expert sees that
+// expert's queries (the per-expert sums are staged and then summed per token
+// through an inverse index of the top-k sets); a block of shared keys sees a
+// chunk of all queries (few atomic adds per chunk). fp32 atomic adds retire at
+// a few hundred G/s on the whole chip, so a design that adds every 64-query
+// tile's key gradients atomically is bound by them.
+// The landmark queries' gradient and the landmark-value backward use atomic
+// adds whose order varies from run to run, so dq, dk, dv are reproducible
+// only to rounding (a few ulp), not bit for bit.
 #include "cdna4.hpp"
 #include "check.hpp"
 #include "flash.hpp"
@@ -90,6 +97,7 @@ struct BwdArgs {
   float *dq;               // [BH, N, d] ATT: the queries' direct gradient (written)
   float *dk, *dv;          // [BH, N, d] accumulators (atomic adds)
   float *dq_lm, *dv_lm_out;  // [BH, M, d] accumulators (atomic adds)
+  float *q_lse, *q_D;      // [BH, N] ATT: each query's log-sum-exp (log2 units) and dO . o (written)
   int N, M, topk, chunk;
   float scale;
 };
@@ -101,15 +109,18 @@ __global__ __launch_bounds__(256) void bwd_kernel(BwdArgs a) {
   using L = BwdLds<T, D>;
   constexpr int VE = 16 / (int)sizeof(T);
   constexpr bool TRANS = L::TRANS;
+  // the key-side tiles ([key][query] P and dZ, transposed Q and dO) serve
+  // the LMV mode's dK and dV only
+  constexpr bool KEYS = MODE == BWD_LMV;
   __shared__ __align__(16) T Qs[L::NQ];
   __shared__ __align__(16) T dOs[L::NQ];
-  __shared__ __align__(16) T QT[L::NQT];
-  __shared__ __align__(16) T dOT[L::NQT];
+  __shared__ __align__(16) T QT[KEYS ? L::NQT : 1];
+  __shared__ __align__(16) T dOT[KEYS ? L::NQT : 1];
   __shared__ __align__(16) T Ks[L::NK];
   __shared__ __align__(16) T Vs[L::NK];
   __shared__ __align__(16) T KT[L::NKT];
-  __shared__ __align__(16) T Pkq[L::NP];
-  __shared__ __align__(16) T Zkq[L::NP];
+  __shared__ __align__(16) T Pkq[KEYS ? L::NP : 1];
+  __shared__ __align__(16) T Zkq[KEYS ? L::NP : 1];
   __shared__ __align__(16) T Zqk[L::NZ];
   __shared__ float Dq[BWD_TQ];
   __shared__ int32_t qrow[BWD_TQ];  // each query's row in its tensor (token or landmark), -1 if none
@@ -165,7 +176,7 @@ __global__ __launch_bounds__(256) void bwd_kernel(BwdArgs a) {
       }
       *reinterpret_cast<uint4 *>(Qs + row * L::QS + cc * VE) = xq;
       *reinterpret_cast<uint4 *>(dOs + row * L::QS + cc * VE) = xd;
-      if constexpr (TRANS) {
+      if constexpr (TRANS && KEYS) {
         const T *tq = reinterpret_cast<const T *>(&xq), *td = reinterpret_cast<const T *>(&xd);
 #pragma unroll
         for (int i = 0; i < VE; ++i) {
@@ -296,6 +307,10 @@ __global__ __launch_bounds__(256) void bwd_kernel(BwdArgs a) {
     lc += __shfl_xor(lc, 16);
     lc += __shfl_xor(lc, 32);
     lse = mc + __log2f(lc);
+    if (g == 0 && qok) {
+      a.q_lse[bh * N + qrow[myq]] = lse;
+      a.q_D[bh * N + qrow[myq]] = Dq[myq];
+    }
   } else {
     lse = qok ? a.lse_lm[bh * M + q_begin + myq] : 0.f;
   }
@@ -337,8 +352,10 @@ __global__ __launch_bounds__(256) void bwd_kernel(BwdArgs a) {
         const float pr = ok ? __builtin_amdgcn_exp2f(s[kb][r] * sl2 - lse) : 0.f;
         pz[r] = pr;
         zz[r] = pr * (dp[kb][r] - dq_row);
-        Pkq[key * L::PS + myq] = from_f32<T>(pz[r]);
-        Zkq[key * L::PS + myq] = from_f32<T>(zz[r]);
+        if constexpr (KEYS) {
+          Pkq[key * L::PS + myq] = from_f32<T>(pz[r]);
+          Zkq[key * L::PS + myq] = from_f32<T>(zz[r]);
+        }
       }
       T z4[4];
 #pragma unroll
@@ -358,8 +375,10 @@ __global__ __launch_bounds__(256) void bwd_kernel(BwdArgs a) {
       B.load(KT + (16 * db + p) * L::KTS + 8 * g);
       dqa[db] = mma(A, B, dqa[db]);
     }
-    // dK = dZ^T Q and dV = P^T dO over the 64 queries (two 32-long steps):
-    // block b = w * NBLK + j of D / 4: first half dK, second half dV
+    // LMV: dK = dZ^T Q and dV = P^T dO over the 64 queries (two 32-long
+    // steps), block b = w * NBLK + j of D / 4: first half dK, second half dV
+    // (in ATT mode the keys' gradients come from bwd_kv_kernel)
+    if constexpr (KEYS)
 #pragma unroll
     for (int j = 0; j < NBLK; ++j) {
       const int b = w * NBLK + j;
@@ -371,7 +390,7 @@ __global__ __launch_bounds__(256) void bwd_kernel(BwdArgs a) {
       for (int qs = 0; qs < 2; ++qs) {
         Frag<T> A, B;
         A.load((isv ? Pkq : Zkq) + (16 * kb + p) * L::PS + 32 * qs + 8 * g);
-        if constexpr (TRANS)
+        if constexpr (TRANS && KEYS)
           B.load((isv ? dOT : QT) + (16 * db + p) * L::TS + 32 * qs + 8 * g);
         else
           B = load_col<T>(isv ? dOs : Qs, L::QS, 32 * qs + 8 * g, 16 * db + p);
@@ -411,6 +430,282 @@ __global__ __launch_bounds__(256) void bwd_kernel(BwdArgs a) {
         unsafeAtomicAdd(a.dq_lm + (bh * M + row) * D + 16 * db + p, val);
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// Key-owned backward of the MiTA attention: a workgroup owns KB = 64 keys
+// (wave w the 16 keys 16 w ..), whose K and V fragments stay in registers,
+// and streams the queries that attend them in tiles of 64, with each query's
+// log-sum-exp and D = dO . o from the dQ pass. Per query tile:
+//   S^T = K Q^T, dP^T = V dO^T (keys x queries, one wave's 16 keys),
+//   P = exp2(S^T scale log2 e - lse), dZ = P (dP - D),
+//   dK += dZ^T Q, dV += P^T dO (reduction over the tile's 64 queries; P and
+//   dZ go through a per-wave LDS area to take the operand layout).
+//   ROUTED: block x = (expert e, key block b); keys idx[e][64 b ..], queries
+//           the expert's group (perm[offsets[e] ..]); the expert's sums are
+//           written to the staging rows [e][64 b ..] (plain stores).
+//   SHARED: block x = (landmark block, chunk of BWD_QCHUNK queries in token
+//           order); keys q_lm / v_lm rows; the sums are added atomically to
+//           the landmark rows.
+// Blocks are spread over the XCDs as the attention work list is, so the key
+// blocks of one expert (same queries) share an L2.
+// ---------------------------------------------------------------------------
+constexpr int BWD_KB = 64;
+constexpr int BWD_QCHUNK = 2048;
+
+template <typename T, int D> struct KvLds {
+  static constexpr int PAD = 16 / (int)sizeof(T);
+  static constexpr bool TRANS = sizeof(T) == 2 && D == 64;
+  static constexpr int QS = D + PAD, TS = BWD_TQ + PAD, WS = BWD_TQ + PAD;
+  static constexpr int NQ = BWD_TQ * QS, NQT = TRANS ? D * TS : 1, NW = 4 * 16 * WS;
+};
+
+struct KvArgs {
+  const void *q, *k, *v, *dO, *q_lm, *v_lm;
+  const int32_t *idx, *perm, *offsets;
+  const float *q_lse, *q_D;   // [BH, N]
+  float *stage_k, *stage_v;   // ROUTED: [BH, M, k, d]
+  float *dq_lm, *dv_lm;       // SHARED: [BH, M, d] accumulators
+  int N, M, topk, nblk;       // nblk: key blocks per expert (ROUTED) or landmark blocks (SHARED)
+  int ntotal;                 // blocks with work (the grid is rounded up to a multiple of 8)
+  float scale;
+};
+
+template <typename T, int D, bool ROUTED>
+__global__ __launch_bounds__(256) void bwd_kv_kernel(KvArgs a) {
+  using L = KvLds<T, D>;
+  constexpr int VE = 16 / (int)sizeof(T);
+  constexpr bool TRANS = L::TRANS;
+  __shared__ __align__(16) T Qs[L::NQ];
+  __shared__ __align__(16) T dOs[L::NQ];
+  __shared__ __align__(16) T QT[L::NQT];
+  __shared__ __align__(16) T dOT[L::NQT];
+  __shared__ __align__(16) T Pw[L::NW];
+  __shared__ __align__(16) T Zw[L::NW];
+  __shared__ float lse_s[BWD_TQ], D_s[BWD_TQ];
+  __shared__ int32_t qtok[BWD_TQ];
+  const int64_t bh = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63, g = lane >> 4, p = lane & 15;
+  const int N = a.N, M = a.M, K = a.topk;
+  const T *q = (const T *)a.q, *dO = (const T *)a.dO;
+  // the block, spread over the XCDs
+  const int nb = (int)gridDim.x;
+  const int C = (nb + NXCD - 1) / NXCD;
+  const int x = ((int)blockIdx.x % NXCD) * C + (int)blockIdx.x / NXCD;
+  if (x >= a.ntotal) return;  // uniform
+  int e = 0, kb0, nkeys, q0, nq;
+  if (ROUTED) {
+    e = x / a.nblk;
+    kb0 = (x % a.nblk) * BWD_KB;
+    nkeys = min(BWD_KB, K - kb0);
+    q0 = a.offsets[bh * (M + 1) + e];
+    nq = a.offsets[bh * (M + 1) + e + 1] - q0;
+  } else {
+    kb0 = (x % a.nblk) * BWD_KB;
+    nkeys = min(BWD_KB, M - kb0);
+    q0 = (x / a.nblk) * BWD_QCHUNK;
+    nq = min(BWD_QCHUNK, N - q0);
+  }
+  // (an expert without queries still writes its staging rows: zeros)
+  // this wave's 16 keys: K and V fragments (row p of the wave's block)
+  const int mykey = 16 * w + p;
+  const bool kvalid = mykey < nkeys;
+  int krow = 0;
+  if (kvalid) krow = ROUTED ? a.idx[(bh * M + e) * (int64_t)K + kb0 + mykey] : kb0 + mykey;
+  const T *kbase = ROUTED ? (const T *)a.k + bh * (int64_t)N * D : (const T *)a.q_lm + bh * (int64_t)M * D;
+  const T *vbase = ROUTED ? (const T *)a.v + bh * (int64_t)N * D : (const T *)a.v_lm + bh * (int64_t)M * D;
+  Frag<T> kf[D / 32], vf[D / 32];
+#pragma unroll
+  for (int ks = 0; ks < D / 32; ++ks) {
+    if (kvalid) {
+      kf[ks].load(kbase + (int64_t)krow * D + 32 * ks + 8 * g);
+      vf[ks].load(vbase + (int64_t)krow * D + 32 * ks + 8 * g);
+    } else {
+      kf[ks].zero();
+      vf[ks].zero();
+    }
+  }
+  const float sl2 = a.scale * LOG2E;
+  f32x4 dk[D / 16], dv[D / 16];
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db) {
+    dk[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    dv[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  T *pw = Pw + w * 16 * L::WS, *zw = Zw + w * 16 * L::WS;
+  for (int t0 = 0; t0 < nq; t0 += BWD_TQ) {
+    __syncthreads();
+    if (tid < BWD_TQ) {
+      int tok = -1;
+      if (t0 + tid < nq) tok = ROUTED ? a.perm[bh * N + q0 + t0 + tid] : q0 + t0 + tid;
+      qtok[tid] = tok;
+      lse_s[tid] = tok >= 0 ? a.q_lse[bh * N + tok] : 0.f;
+      D_s[tid] = tok >= 0 ? a.q_D[bh * N + tok] : 0.f;
+    }
+    __syncthreads();
+    for (int c = tid; c < BWD_TQ * (D / VE); c += 256) {
+      const int row = c / (D / VE), cc = c % (D / VE);
+      const int tok = qtok[row];
+      uint4 xq = make_uint4(0, 0, 0, 0), xd = make_uint4(0, 0, 0, 0);
+      if (tok >= 0) {
+        xq = *reinterpret_cast<const uint4 *>(q + (bh * N + tok) * D + cc * VE);
+        xd = *reinterpret_cast<const uint4 *>(dO + (bh * N + tok) * D + cc * VE);
+      }
+      *reinterpret_cast<uint4 *>(Qs + row * L::QS + cc * VE) = xq;
+      *reinterpret_cast<uint4 *>(dOs + row * L::QS + cc * VE) = xd;
+      if constexpr (TRANS) {
+        const T *tq = reinterpret_cast<const T *>(&xq), *td = reinterpret_cast<const T *>(&xd);
+#pragma unroll
+        for (int i = 0; i < VE; ++i) {
+          QT[(cc * VE + i) * L::TS + row] = tq[i];
+          dOT[(cc * VE + i) * L::TS + row] = td[i];
+        }
+      }
+    }
+    __syncthreads();
+    // P and dZ of (key 16 w + 4 g + r, query 16 qb + p) into the wave's LDS area
+#pragma unroll
+    for (int qb = 0; qb < 4; ++qb) {
+      f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f}, dp = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) {
+        Frag<T> B;
+        B.load(Qs + (16 * qb + p) * L::QS + 32 * ks + 8 * g);
+        s = mma(kf[ks], B, s);
+        B.load(dOs + (16 * qb + p) * L::QS + 32 * ks + 8 * g);
+        dp = mma(vf[ks], B, dp);
+      }
+      const int qq = 16 * qb + p;
+      const bool qok = qtok[qq] >= 0;
+      const float lq = lse_s[qq], dq = D_s[qq];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = 16 * w + 4 * g + r;
+        const bool ok = qok && key < nkeys;
+        const float pr = ok ? __builtin_amdgcn_exp2f(s[r] * sl2 - lq) : 0.f;
+        pw[(4 * g + r) * L::WS + qq] = from_f32<T>(pr);
+        zw[(4 * g + r) * L::WS + qq] = from_f32<T>(pr * (dp[r] - dq));
+      }
+    }
+    __syncthreads();
+    // dK += dZ^T Q, dV += P^T dO: rows = the wave's 16 keys, columns = dims
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) {
+#pragma unroll
+      for (int qs = 0; qs < 2; ++qs) {
+        Frag<T> A, B;
+        A.load(zw + p * L::WS + 32 * qs + 8 * g);
+        if constexpr (TRANS)
+          B.load(QT + (16 * db + p) * L::TS + 32 * qs + 8 * g);
+        else
+          B = load_col<T>(Qs, L::QS, 32 * qs + 8 * g, 16 * db + p);
+        dk[db] = mma(A, B, dk[db]);
+        A.load(pw + p * L::WS + 32 * qs + 8 * g);
+        if constexpr (TRANS)
+          B.load(dOT + (16 * db + p) * L::TS + 32 * qs + 8 * g);
+        else
+          B = load_col<T>(dOs, L::QS, 32 * qs + 8 * g, 16 * db + p);
+        dv[db] = mma(A, B, dv[db]);
+      }
+    }
+  }
+  // rows: key 16 w + 4 g + r of the block; column: dim 16 db + p
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int key = 16 * w + 4 * g + r;
+    if (key >= nkeys) continue;
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) {
+      if (ROUTED) {
+        const int64_t at = ((bh * M + e) * (int64_t)K + kb0 + key) * D + 16 * db + p;
+        a.stage_k[at] = dk[db][r] * a.scale;
+        a.stage_v[at] = dv[db][r];
+      } else {
+        const int64_t at = (bh * M + kb0 + key) * D + 16 * db + p;
+        unsafeAtomicAdd(a.dq_lm + at, dk[db][r] * a.scale);
+        unsafeAtomicAdd(a.dv_lm + at, dv[db][r]);
+      }
+    }
+  }
+}
+
+// Inverse index of the top-k sets: for each token, the (expert, position)
+// slots e * k + j with idx[e][j] = token, by a counting sort (count, scan,
+// place; the order of a token's slots is that of the atomic decrements).
+__global__ __launch_bounds__(256) void inv_count_kernel(const int32_t *__restrict__ idx, int32_t *__restrict__ cnt,
+                                                        int64_t total, int per_head, int N) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= total) return;
+  const int64_t bh = t / per_head;
+  atomicAdd(&cnt[bh * N + idx[t]], 1);
+}
+
+// Exclusive scan of cnt over each head's N tokens into start [BH, N + 1]
+// (1024 threads per head, consecutive runs per thread).
+__global__ __launch_bounds__(1024) void inv_scan_kernel(const int32_t *__restrict__ cnt, int32_t *__restrict__ start,
+                                                        int N) {
+  __shared__ uint32_t wsum[16];
+  const int64_t bh = blockIdx.x;
+  const int per = (N + 1023) / 1024;
+  const int b0 = threadIdx.x * per, b1 = min(N, b0 + per);
+  uint32_t sum = 0;
+  for (int i = b0; i < b1; ++i) sum += (uint32_t)cnt[bh * N + i];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const uint32_t incl = wave_inclusive_scan(sum);
+  if (lane == 63) wsum[w] = incl;
+  __syncthreads();
+  uint32_t before = incl - sum, all = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    before += i < w ? wsum[i] : 0u;
+    all += wsum[i];
+  }
+  for (int i = b0; i < b1; ++i) {
+    start[bh * (N + 1) + i] = (int32_t)before;
+    before += (uint32_t)cnt[bh * N + i];
+  }
+  if (threadIdx.x == 0) start[bh * (N + 1) + N] = (int32_t)all;
+}
+
+__global__ __launch_bounds__(256) void inv_place_kernel(const int32_t *__restrict__ idx, int32_t *__restrict__ cnt,
+                                                        const int32_t *__restrict__ start, int32_t *__restrict__ slot,
+                                                        int64_t total, int per_head, int N) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= total) return;
+  const int64_t bh = t / per_head;
+  const int tok = idx[t];
+  const int pos = atomicSub(&cnt[bh * N + tok], 1) - 1;
+  slot[bh * (int64_t)per_head + start[bh * (N + 1) + tok] + pos] = (int32_t)(t - bh * per_head);
+}
+
+// dk_acc, dv_acc of every token = the sum of its staged per-expert rows
+// (written, not added: the first contribution). One thread per 4 dims.
+template <int D>
+__global__ __launch_bounds__(256) void inv_gather_kernel(const float *__restrict__ stage_k,
+                                                         const float *__restrict__ stage_v,
+                                                         const int32_t *__restrict__ start,
+                                                         const int32_t *__restrict__ slot, float *__restrict__ dk,
+                                                         float *__restrict__ dv, int64_t rows, int N, int per_head) {
+  constexpr int C = D / 4;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t row = t / C;
+  const int c = (int)(t % C);
+  if (row >= rows) return;
+  const int64_t bh = row / N;
+  const int tok = (int)(row % N);
+  const int s0 = start[bh * (N + 1) + tok], s1 = start[bh * (N + 1) + tok + 1];
+  float4 xk = make_float4(0.f, 0.f, 0.f, 0.f), xv = xk;
+  for (int i = s0; i < s1; ++i) {
+    const int64_t src = (bh * (int64_t)per_head + slot[bh * (int64_t)per_head + i]) * D + 4 * c;
+    const float4 yk = *reinterpret_cast<const float4 *>(stage_k + src);
+    const float4 yv = *reinterpret_cast<const float4 *>(stage_v + src);
+    xk.x += yk.x; xk.y += yk.y; xk.z += yk.z; xk.w += yk.w;
+    xv.x += yv.x; xv.y += yv.y; xv.z += yv.z; xv.w += yv.w;
+  }
+  *reinterpret_cast<float4 *>(dk + row * D + 4 * c) = xk;
+  *reinterpret_cast<float4 *>(dv + row * D + 4 * c) = xv;
 }
 
 // Log-sum-exp (log2 units) of every landmark row's scores, from the score
@@ -509,6 +804,8 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
   a.dv = b.dv_acc;
   a.dq_lm = b.dq_lm_acc;
   a.dv_lm_out = b.dv_lm_acc;
+  a.q_lse = b.q_lse;
+  a.q_D = b.q_D;
   a.N = c.N;
   a.M = c.M;
   a.topk = c.k;
@@ -522,7 +819,7 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
                        b.lse_lm, rows, c.M, score_chunks(c));
     if ((err = launched("lse_rows_kernel", st)) != hipSuccess) return err;
   }
-  // the attention of Eq. mita
+  // dQ of the MiTA attention, and each query's log-sum-exp and D
   int tiles = (c.N + ATT_TQ - 1) / ATT_TQ;
   if (c.use_routed) tiles = (tiles + c.M + NXCD - 1) / NXCD * NXCD;
   const dim3 grid((unsigned)tiles, bh);
@@ -533,8 +830,57 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
   else
     hipLaunchKernelGGL((bwd_kernel<T, D, BWD_ATT, true, false>), grid, dim3(256), 0, st, a);
   if ((err = launched("bwd_attend_kernel", st)) != hipSuccess) return err;
-  // the landmark values (Eq. landmark-value), once their gradient is complete
+  KvArgs kv{};
+  kv.q = b.q;
+  kv.k = b.k;
+  kv.v = b.v;
+  kv.dO = b.dO;
+  kv.q_lm = b.q_lm;
+  kv.v_lm = b.v_lm;
+  kv.idx = b.idx;
+  kv.perm = b.perm;
+  kv.offsets = b.offsets;
+  kv.q_lse = b.q_lse;
+  kv.q_D = b.q_D;
+  kv.stage_k = b.stage_k;
+  kv.stage_v = b.stage_v;
+  kv.dq_lm = b.dq_lm_acc;
+  kv.dv_lm = b.dv_lm_acc;
+  kv.N = c.N;
+  kv.M = c.M;
+  kv.topk = c.k;
+  kv.scale = eff_scale(c);
+  if (c.use_routed) {
+    // routed keys: per-expert sums staged, then summed per token
+    kv.nblk = (c.k + BWD_KB - 1) / BWD_KB;
+    kv.ntotal = c.M * kv.nblk;
+    const unsigned nx = (unsigned)((kv.ntotal + NXCD - 1) / NXCD * NXCD);
+    hipLaunchKernelGGL((bwd_kv_kernel<T, D, true>), dim3(nx, bh), dim3(256), 0, st, kv);
+    if ((err = launched("bwd_kv_kernel", st)) != hipSuccess) return err;
+    const int per_head = c.M * c.k;
+    const int64_t total = BH(c) * per_head;
+    const unsigned gi = (unsigned)((total + 255) / 256);
+    if ((err = launch_zero(b.inv_cnt, BH(c) * c.N, st)) != hipSuccess) return err;
+    hipLaunchKernelGGL(inv_count_kernel, dim3(gi), dim3(256), 0, st, b.idx, b.inv_cnt, total, per_head, c.N);
+    if ((err = launched("inv_count_kernel", st)) != hipSuccess) return err;
+    hipLaunchKernelGGL(inv_scan_kernel, dim3(bh), dim3(1024), 0, st, b.inv_cnt, b.inv_start, c.N);
+    if ((err = launched("inv_scan_kernel", st)) != hipSuccess) return err;
+    hipLaunchKernelGGL(inv_place_kernel, dim3(gi), dim3(256), 0, st, b.idx, b.inv_cnt, b.inv_start, b.inv_slot, total,
+                       per_head, c.N);
+    if ((err = launched("inv_place_kernel", st)) != hipSuccess) return err;
+    const int64_t rows = BH(c) * c.N;
+    hipLaunchKernelGGL((inv_gather_kernel<D>), dim3((unsigned)((rows * (D / 4) + 255) / 256)), dim3(256), 0, st,
+                       b.stage_k, b.stage_v, b.inv_start, b.inv_slot, b.dk_acc, b.dv_acc, rows, c.N, per_head);
+    if ((err = launched("inv_gather_kernel", st)) != hipSuccess) return err;
+  }
   if (c.use_shared) {
+    // shared keys (the landmarks): atomic adds per landmark block and query chunk
+    kv.nblk = (c.M + BWD_KB - 1) / BWD_KB;
+    kv.ntotal = kv.nblk * ((c.N + BWD_QCHUNK - 1) / BWD_QCHUNK);
+    const unsigned nx = (unsigned)((kv.ntotal + NXCD - 1) / NXCD * NXCD);
+    hipLaunchKernelGGL((bwd_kv_kernel<T, D, false>), dim3(nx, bh), dim3(256), 0, st, kv);
+    if ((err = launched("bwd_kv_shared_kernel", st)) != hipSuccess) return err;
+    // the landmark values (Eq. landmark-value), once their gradient is complete
     const int nlb = (c.M + BWD_TQ - 1) / BWD_TQ, nch = (c.N + BWD_CHUNK - 1) / BWD_CHUNK;
     hipLaunchKernelGGL((bwd_kernel<T, D, BWD_LMV, true, false>), dim3((unsigned)(nlb * nch), bh), dim3(256), 0, st,
                        a);

@@ -111,6 +111,9 @@ struct BwdBufs {
   float *dq_direct;                // [BH, N, d] (written)
   float *dk_acc, *dv_acc;          // [BH, N, d] (zeroed)
   float *dq_lm_acc, *dv_lm_acc;    // [BH, M, d] (zeroed)
+  float *q_lse, *q_D;              // [BH, N] per-query log-sum-exp and dO . o (written)
+  float *stage_k, *stage_v;        // [BH, M, k, d] per-expert sums of the routed keys (written)
+  int32_t *inv_cnt, *inv_start, *inv_slot;  // inverse index of the top-k sets
   void *dq, *dk, *dv;              // [BH, N, d] outputs (io type)
 };
 hipError_t launch_backward(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st);

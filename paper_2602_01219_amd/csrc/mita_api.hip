@@ -88,7 +88,7 @@ hipError_t mita::launched(const char *kernel, hipStream_t st) {
   if (!r || e != hipSuccess) return e;
   mita_timer *t = r->t;
   int &n = t->nlaunch[r->call];
-  if (n >= MITA_MAX_LAUNCHES) return e;  // cannot happen: a forward launches fewer kernels
+  if (n >= MITA_MAX_LAUNCHES) return e;  // cannot happen: a forward or backward launches fewer kernels
   const size_t slot = (size_t)r->call * MITA_MAX_LAUNCHES + n;
   t->name[slot] = kernel;
   t->stage[slot] = r->stage;
@@ -286,10 +286,12 @@ int backward_impl(const mita_cfg_t *c, const void *q, const void *k, const void 
   // gradients (stage 5)
   rec.stage = 5;
   const int64_t nd = BH(*c) * c->N * c->d, md = BH(*c) * c->M * c->d;
-  TRY(hip_status(launch_zero((int32_t *)(w + BL.dk_acc), nd, st), "backward"));
-  TRY(hip_status(launch_zero((int32_t *)(w + BL.dv_acc), nd, st), "backward"));
-  TRY(hip_status(launch_zero((int32_t *)(w + BL.dq_lm_acc), (int64_t)(BL.total - BL.dq_lm_acc) / 4, st),
-                 "backward"));  // dq_lm_acc and dv_lm_acc
+  if (!c->use_routed) {  // with routing, the routed keys' gather writes dk_acc and dv_acc first
+    TRY(hip_status(launch_zero((int32_t *)(w + BL.dk_acc), nd, st), "backward"));
+    TRY(hip_status(launch_zero((int32_t *)(w + BL.dv_acc), nd, st), "backward"));
+  }
+  TRY(hip_status(launch_zero((int32_t *)(w + BL.dq_lm_acc), md, st), "backward"));
+  TRY(hip_status(launch_zero((int32_t *)(w + BL.dv_lm_acc), md, st), "backward"));
   BwdBufs b{};
   b.q = q;
   b.k = k;
@@ -309,10 +311,16 @@ int backward_impl(const mita_cfg_t *c, const void *q, const void *k, const void 
   b.dv_acc = (float *)(w + BL.dv_acc);
   b.dq_lm_acc = (float *)(w + BL.dq_lm_acc);
   b.dv_lm_acc = (float *)(w + BL.dv_lm_acc);
+  b.q_lse = (float *)(w + BL.q_lse);
+  b.q_D = (float *)(w + BL.q_D);
+  b.stage_k = (float *)(w + BL.stage_k);
+  b.stage_v = (float *)(w + BL.stage_v);
+  b.inv_cnt = (int32_t *)(w + BL.inv_cnt);
+  b.inv_start = (int32_t *)(w + BL.inv_start);
+  b.inv_slot = (int32_t *)(w + BL.inv_slot);
   b.dq = dq;
   b.dk = dk;
   b.dv = dv;
-  (void)md;
   TRY(hip_status(launch_backward(*c, b, st), "backward"));
   if (rec.err != hipSuccess) return hip_status(rec.err, "hipEventRecord");
   return MITA_OK;

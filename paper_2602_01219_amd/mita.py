@@ -27,7 +27,7 @@ MITA_FLAG_STAGED_GATHER = 0x1
 MITA_FLAG_FULL_SCORES = 0x2
 WS_FORWARD, WS_SCORES, WS_TOPK, WS_ROUTE, WS_ATTEND, WS_BACKWARD = range(6)
 NUM_STAGES = 6
-MAX_LAUNCHES = 16
+MAX_LAUNCHES = 32
 STAGES = ("landmarks", "scores", "topk", "gather", "route", "attend")
 MAX_N = 65536
 MAX_S = 4
