@@ -329,9 +329,12 @@ def run(wl, name, a, dense: bool):
     if dense:
         sdpa = sdpa_ms(q, k, v, a.steps, a.warmup)
     if a.calib_copy_mib:
-        src = torch.empty(a.calib_copy_mib * 2**20, dtype=torch.uint8, device="cuda")
+        # a plain elementwise kernel that reads and writes calib_copy_mib MiB
+        # each (torch's copy_ of contiguous tensors is a runtime blit, whose
+        # stores the counters need not see like an ordinary kernel's)
+        src = torch.ones(a.calib_copy_mib * 2**18, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
-        dst.copy_(src)
+        torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
 
     ms_per_step = wall * 1e3 / a.steps
