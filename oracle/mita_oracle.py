@@ -52,6 +52,8 @@ Readings where the paper is silent or ambiguous (listed in the design doc):
     of the query's experts enters the softmax twice.
   * random selection: landmark i is the query of token sel[i], sel being M
     distinct token indices supplied by the caller.
+  * token merging (ToMe) as landmark extraction (Tab. A1 names it; bipartite
+    soft matching, applied repeatedly): see landmarks_tome.
 """
 from __future__ import annotations
 
@@ -95,6 +97,77 @@ def landmarks_random(q: np.ndarray, sel) -> np.ndarray:
     assert sel.ndim == 1 and len(np.unique(sel)) == len(sel)
     assert sel.min() >= 0 and sel.max() < q.shape[0]
     return q[sel].copy()
+
+
+@dataclass
+class TomeResult:
+    q_lm: np.ndarray       # [M, d] landmark queries (means of their members)
+    assign: np.ndarray     # [N] landmark of every token
+    margins: list          # per round: (smallest gap between an A token's best and second-best
+                           # similarity, gap between the r-th and (r+1)-th edge), for parity budgets
+
+
+def tome_similarity(XA: np.ndarray, XB: np.ndarray) -> np.ndarray:
+    """Cosine similarity of every A token with every B token (rows: merged
+    queries)."""
+    na = XA / np.linalg.norm(XA, axis=1, keepdims=True)
+    nb = XB / np.linalg.norm(XB, axis=1, keepdims=True)
+    return na @ nb.T
+
+
+def landmarks_tome(q: np.ndarray, M: int) -> TomeResult:
+    """Token merging as landmark extraction (Tab. A1; bipartite soft matching
+    applied in rounds until M tokens remain). A round over the current
+    sequence of n merged tokens (each the mean of its original members, in
+    sequence order):
+      1. A = the tokens at even positions, B = those at odd positions;
+      2. each A token's match is the B token of largest cosine similarity of
+         the merged queries (ties: lower B position), its edge score that
+         similarity;
+      3. the r = min(n - M, |A|) edges of largest score (ties: lower A
+         position) merge: each of those A tokens joins its match;
+      4. the survivors (unmerged A tokens and all B tokens) keep their order.
+    The landmarks are the final tokens' means, in sequence order."""
+    N, d = q.shape
+    assert 1 <= M <= N
+    groups = [[t] for t in range(N)]            # members of each current token, in sequence order
+    margins = []
+    while len(groups) > M:
+        n = len(groups)
+        X = np.stack([q[g].mean(axis=0) for g in groups])
+        A = list(range(0, n, 2))
+        B = list(range(1, n, 2))
+        sim = tome_similarity(X[A], X[B])        # [|A|, |B|]
+        match = np.empty(len(A), dtype=np.int64)
+        score = np.empty(len(A))
+        gap_best = np.inf
+        for i in range(len(A)):
+            order = np.lexsort((np.arange(len(B)), -sim[i]))
+            match[i] = order[0]
+            score[i] = sim[i, order[0]]
+            if len(B) > 1:
+                gap_best = min(gap_best, sim[i, order[0]] - sim[i, order[1]])
+        r = min(n - M, len(A))
+        eorder = np.lexsort((np.arange(len(A)), -score))
+        merged = set(eorder[:r].tolist())
+        gap_edge = score[eorder[r - 1]] - score[eorder[r]] if r < len(A) else np.inf
+        margins.append((gap_best, gap_edge))
+        new_groups = {}
+        for i in sorted(merged):                 # A tokens join their matches, in A order
+            new_groups.setdefault(match[i], []).extend(groups[A[i]])
+        out = []
+        for j in range(n):
+            if j % 2 == 0:
+                if j // 2 not in merged:
+                    out.append(groups[j])
+            else:
+                out.append(groups[j] + new_groups.get(j // 2, []))
+        groups = out
+    assign = np.empty(N, dtype=np.int64)
+    for i, g in enumerate(groups):
+        assign[g] = i
+    q_lm = np.stack([q[g].mean(axis=0) for g in groups])
+    return TomeResult(q_lm, assign, margins)
 
 
 # ----------------------------------------------------------------------------

@@ -192,3 +192,37 @@ def test_planted_mistake_in_the_backward_is_caught(monkeypatch, name, mutant, pi
     monkeypatch.setattr(O, name, mutant)
     with pytest.raises(AssertionError):
         pin()
+
+
+# ---------------------------------------------------------------- token merging
+_orig_tome = O.landmarks_tome
+
+
+def _tome_sim_dot(XA, XB):
+    return XA @ XB.T                            # dot products instead of cosines
+
+
+def _tome_odd_as_A(q, M):
+    # A and B swapped (A = odd positions): emulated by reversing the order of pairs
+    N = q.shape[0]
+    perm = np.arange(N)
+    perm[0:N - N % 2:2], perm[1:N - N % 2:2] = np.arange(1, N - N % 2, 2), np.arange(0, N - N % 2, 2)
+    r = _orig_tome(q[perm], M)
+    assign = np.empty(N, dtype=np.int64)
+    assign[perm] = r.assign
+    means = np.stack([q[assign == i].mean(axis=0) for i in range(M)])
+    return O.TomeResult(means, assign, r.margins)
+
+
+MUTANTS_TOME = [
+    ("tome_similarity", _tome_sim_dot, lambda: PV.test_tome_merges_by_cosine_not_dot()),
+    ("landmarks_tome", _tome_odd_as_A, lambda: PV.test_tome_ties_go_to_the_lower_position()),
+]
+
+
+@pytest.mark.parametrize("name,mutant,pin", MUTANTS_TOME, ids=[m[1].__name__ for m in MUTANTS_TOME])
+def test_planted_mistake_in_token_merging_is_caught(monkeypatch, name, mutant, pin):
+    pin()
+    monkeypatch.setattr(O, name, mutant)
+    with pytest.raises(AssertionError):
+        pin()

@@ -169,3 +169,61 @@ def test_random_landmarks_forward_is_sdpa_over_shared_plus_routed_keys():
         I = r.idx[r.experts[n, 0]]
         ref = _sdpa_bias(q[n], np.concatenate([r.q_lm, k[I]]), np.concatenate([v_lm, v[I]]), sc, 0.0)[0]
         np.testing.assert_allclose(r.o[n], ref, atol=1e-12)
+
+
+# ---------------------------------------------------------------- token merging (ToMe)
+def test_tome_merges_by_cosine_not_dot():
+    # positions 0 (A), 1 (B), 2 (A), 3 (B); M = 3: one edge merges.
+    # A0 = (1, 0): cosine 0.707 with B1 = (10, 10), 0.994 with B3 = (0.9, 0.1)
+    # (a dot product would prefer B1); A2 = (0, 1): 0.707 with B1, 0.110 with B3.
+    # Edge scores 0.994 (A0) > 0.707 (A2): A0 joins B3.
+    q = np.array([[1, 0], [10, 10], [0, 1], [0.9, 0.1]], dtype=np.float64)
+    r = O.landmarks_tome(q, 3)
+    np.testing.assert_allclose(r.q_lm, [[10, 10], [0, 1], [0.95, 0.05]], atol=1e-15)
+    assert r.assign.tolist() == [2, 0, 1, 2]
+
+
+def test_tome_ties_go_to_the_lower_position():
+    # A0 = (1, 0) has cosine 1 with both B1 = (2, 0) and B3 = (3, 0): B1 (lower).
+    # A2 = (0, 1) has cosine 0 with both: B1. Edge scores 1 (A0), 0 (A2).
+    q = np.array([[1, 0], [2, 0], [0, 1], [3, 0]], dtype=np.float64)
+    r3 = O.landmarks_tome(q, 3)                 # one edge: A0 -> B1
+    np.testing.assert_allclose(r3.q_lm, [[1.5, 0], [0, 1], [3, 0]], atol=1e-15)
+    r2 = O.landmarks_tome(q, 2)                 # both edges: A0, A2 -> B1
+    np.testing.assert_allclose(r2.q_lm, [[1, 1 / 3], [3, 0]], atol=1e-15)
+    assert r2.assign.tolist() == [0, 0, 0, 1]
+
+
+def test_tome_twins_merge_with_each_other():
+    # tokens in identical pairs at (2i, 2i + 1), pairs far apart: one round
+    # with M = N / 2 merges every A token into its twin
+    r = _rng(31)
+    base = r.standard_normal((12, 16))
+    q = np.repeat(base, 2, axis=0)
+    t = O.landmarks_tome(q, 12)
+    np.testing.assert_allclose(t.q_lm, base, atol=1e-14)
+    assert t.assign.tolist() == [i // 2 for i in range(24)]
+
+
+def test_tome_with_M_eq_N_merges_nothing():
+    q = _rng(32).standard_normal((20, 5))
+    t = O.landmarks_tome(q, 20)
+    np.testing.assert_array_equal(t.q_lm, q)
+    assert t.assign.tolist() == list(range(20))
+
+
+@pytest.mark.parametrize("N,M", [(196, 25), (196, 16), (100, 7), (64, 63), (33, 1)])
+def test_tome_landmarks_are_means_of_a_partition(N, M):
+    q = _rng(N + M).standard_normal((N, 6))
+    t = O.landmarks_tome(q, M)
+    assert t.assign.min() == 0 and t.assign.max() == M - 1
+    assert (np.bincount(t.assign, minlength=M) > 0).all()
+    for i in range(M):
+        np.testing.assert_allclose(t.q_lm[i], q[t.assign == i].mean(axis=0), atol=1e-13)
+
+
+def test_tome_is_invariant_to_a_positive_scale():
+    q = _rng(33).standard_normal((64, 8))
+    a, b = O.landmarks_tome(q, 10), O.landmarks_tome(3.5 * q, 10)
+    np.testing.assert_array_equal(a.assign, b.assign)
+    np.testing.assert_allclose(b.q_lm, 3.5 * a.q_lm, atol=1e-13)
