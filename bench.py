@@ -245,11 +245,20 @@ def run(wl, name, a, dense: bool):
     eprint(f"[bench] s = {s_exp}, landmarks by {a.landmarks}; workspace {ws.numel() / 2**20:.1f} MiB; "
            f"selection {plan}")
     random_lm = a.landmarks == "random"
-    if random_lm:
-        # random selection: the draw is an input; a step selects the landmark
-        # rows, then runs the forward from them
-        sel = torch.from_numpy(synth.landmark_draw(wl)).cuda()
+    tome_lm = a.landmarks == "tome"
+    if random_lm or tome_lm:
+        # random selection (the draw is an input) or token merging: a step
+        # forms the landmarks, then runs the forward from them
+        sel = torch.from_numpy(synth.landmark_draw(wl)).cuda() if random_lm else None
         q_lm = torch.empty((wl.B, wl.H, wl.M, wl.d), dtype=q.dtype, device="cuda")
+        ws_t = (torch.empty(mita.workspace_size(cfg, mita.WS_TOME), dtype=torch.uint8, device="cuda")
+                if tome_lm else None)
+
+    def make_landmarks():
+        if random_lm:
+            mita.landmarks_select(cfg, q, sel, q_lm=q_lm)
+        else:
+            mita.landmarks_tome(cfg, q, q_lm=q_lm, want_assign=False, ws=ws_t)
 
     if a.backward:
         r = np.random.default_rng(wl.seed + 17)
@@ -265,8 +274,8 @@ def run(wl, name, a, dense: bool):
             mita.forward(cfg, q, k, v, o=o, ws=ws, timer=timer)
             mita.backward(cfg, q, k, v, o, dO, *grads, ws=ws_b, timer=timer_b)
             return
-        if random_lm:
-            mita.landmarks_select(cfg, q, sel, q_lm=q_lm)
+        if random_lm or tome_lm:
+            make_landmarks()
             mita.forward(cfg, q, k, v, o=o, ws=ws, timer=timer, q_lm=q_lm)
         else:
             mita.forward(cfg, q, k, v, o=o, ws=ws, timer=timer)
@@ -292,10 +301,10 @@ def run(wl, name, a, dense: bool):
     for _ in range(a.steps):
         if a.backward:
             step(timer, timer_b)
-        elif random_lm:
+        elif random_lm or tome_lm:
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
-            mita.landmarks_select(cfg, q, sel, q_lm=q_lm)
+            make_landmarks()
             e1.record()
             sel_ev.append((e0, e1))
             mita.forward(cfg, q, k, v, o=o, ws=ws, timer=timer, q_lm=q_lm)
@@ -306,10 +315,10 @@ def run(wl, name, a, dense: bool):
     if a.backward:
         per_call = [f + b_ for f, b_ in zip(per_call, timer_b.launches())]
         timer_b.close()
-    if random_lm:
+    if random_lm or tome_lm:
         torch.cuda.synchronize()
-        per_call = [call + [("select_landmarks_kernel", 0, e0.elapsed_time(e1))]
-                    for call, (e0, e1) in zip(per_call, sel_ev)]
+        lm_name = "select_landmarks_kernel" if random_lm else "token merging (all launches)"
+        per_call = [call + [(lm_name, 0, e0.elapsed_time(e1))] for call, (e0, e1) in zip(per_call, sel_ev)]
     # cold caches (secondary figure): before each forward, reading 512 MiB
     # evicts the inputs from L2 and the 256 MiB MALL; each forward is timed
     # alone with events on the launch stream and the median is reported
@@ -336,6 +345,24 @@ def run(wl, name, a, dense: bool):
         dst = torch.empty_like(src)
         torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
+
+    # the HBM rate a plain streaming kernel reaches on this machine (context for
+    # the fractions, which use the published 8 TB/s): torch.mul by 1 of 1 GiB
+    # of fp32 into another 1 GiB, median of 5 event-timed launches
+    hbm_src = torch.ones(2**28, dtype=torch.float32, device="cuda")
+    hbm_dst = torch.empty_like(hbm_src)
+    torch.mul(hbm_src, 1.0, out=hbm_dst)
+    hbm_ms = []
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        torch.mul(hbm_src, 1.0, out=hbm_dst)
+        e1.record()
+        torch.cuda.synchronize()
+        hbm_ms.append(e0.elapsed_time(e1))
+    measured_hbm = 2 * 2**30 / (sorted(hbm_ms)[2] * 1e-3) / 1e9
+    del hbm_src, hbm_dst
+    eprint(f"[bench] streaming kernel on this box: {measured_hbm:.0f} GB/s (1 GiB read + 1 GiB written)")
 
     ms_per_step = wall * 1e3 / a.steps
     value = wl.tokens * a.steps / wall
@@ -385,7 +412,7 @@ def run(wl, name, a, dense: bool):
                 "algorithmic_bytes": dom["algorithmic_bytes"], "algorithmic_flops": dom["algorithmic_flops"]}
 
     cpu = None
-    if not a.no_cpu_baseline and not dense and s_exp == 1 and not random_lm and not a.backward:
+    if not a.no_cpu_baseline and not dense and s_exp == 1 and a.landmarks == "pool" and not a.backward:
         eprint("[bench] timing the CPU oracle on a sample ...")
         cpu = cpu_baseline(wl, inp, a.cpu_budget)
         eprint(f"[bench] cpu oracle {cpu['value']:.1f} tokens/s fp32, {cpu['value_f64']:.1f} fp64 "
@@ -408,6 +435,7 @@ def run(wl, name, a, dense: bool):
         "kernels": kernels,
         "stages_us": {s: round(u, 2) for s, u in zip(mita.STAGES, stage_us)},
         "fallback_rows": fallbacks,
+        "measured_hbm_gb_s": round(measured_hbm, 1),
         "cold": {"ms_per_forward": round(cold_ms, 4), "tokens_per_s": round(wl.tokens / cold_ms * 1e3, 1),
                  "note": "median single forward after reading 512 MiB (L2 and MALL evicted)"},
     }
@@ -432,8 +460,8 @@ def main():
     ap.add_argument("--s", type=int, default=1, help="routed experts per query (Eq. mita)")
     ap.add_argument("--backward", action="store_true",
                     help="time forward + backward steps (gradients of q, k, v for a synthetic upstream gradient)")
-    ap.add_argument("--landmarks", choices=("pool", "random"), default="pool",
-                    help="landmark extraction: 2-D pooling (default) or random selection (Tab. A1)")
+    ap.add_argument("--landmarks", choices=("pool", "random", "tome"), default="pool",
+                    help="landmark extraction: 2-D pooling (default), random selection or token merging (Tab. A1)")
     ap.add_argument("--cpu-budget", type=float, default=12.0,
                     help="seconds of float32 oracle time for cpu_baseline (half as much again in float64)")
     ap.add_argument("--no-cpu-baseline", action="store_true")

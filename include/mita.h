@@ -105,6 +105,7 @@ typedef struct {
 #define MITA_WS_ROUTE 3
 #define MITA_WS_ATTEND 4
 #define MITA_WS_BACKWARD 5
+#define MITA_WS_TOME 6
 
 /* Host-only validation of cfg (no device needed). Returns a status code. */
 int mita_check(const mita_cfg_t *cfg);
@@ -195,6 +196,28 @@ int mita_landmarks(const mita_cfg_t *cfg, const void *q, void *q_lm, mita_stream
  */
 int mita_landmarks_select(const mita_cfg_t *cfg, const void *q, const int32_t *sel, void *q_lm,
                           mita_stream_t stream);
+
+/*
+ * Landmark queries by token merging (Tab. A1 lists ToMe among the landmark
+ * extractions): bipartite soft matching applied in rounds until M tokens
+ * remain. A round over the current sequence of n merged tokens (each the mean
+ * of its tokens' queries, in sequence order) splits it into A (even
+ * positions) and B (odd positions); each A token's match is its B token of
+ * largest cosine similarity (lower B position on ties); the r = min(n - M,
+ * |A|) edges of largest similarity (lower A position on ties) merge each of
+ * those A tokens into its match; the survivors keep their order. Landmark i
+ * is the mean of the queries of the tokens merged into the i-th final token.
+ *   q : [B, H, N, d];  q_lm : [B, H, M, d] output;
+ *   assign : [B, H, N] int32 output, the landmark of every token, or NULL;
+ *   ws : >= mita_workspace_size(cfg, MITA_WS_TOME) bytes.
+ * Member sums are exact in 64-bit fixed point (units of 2^-32), so the
+ * result does not depend on the order of the merge additions; the
+ * similarities are fp32. Queries whose window sums reach 2^31 in magnitude
+ * overflow that format (results then unspecified; every access stays in
+ * bounds). Feed q_lm to mita_forward_lm for the forward with these landmarks.
+ */
+int mita_landmarks_tome(const mita_cfg_t *cfg, const void *q, void *q_lm, int32_t *assign, void *ws,
+                        size_t ws_bytes, mita_stream_t stream);
 
 /*
  * mita_forward with caller-supplied landmark queries (random selection, or any

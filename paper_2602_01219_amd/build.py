@@ -21,7 +21,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmita.so")
 ARCH = "gfx950"
 
-SOURCES = ["mita_api.hip", "pool_scores.hip", "topk.hip", "select.hip", "route_attend.hip", "backward.hip"]
+SOURCES = ["mita_api.hip", "pool_scores.hip", "topk.hip", "select.hip", "route_attend.hip", "backward.hip", "tome.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

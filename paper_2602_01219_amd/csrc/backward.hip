@@ -898,6 +898,11 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
   return launched("bwd_finish_kernel", st);
 }
 
+hipError_t launch_scan_counts(const int32_t *cnt, int32_t *start, int n, int64_t bh, hipStream_t st) {
+  hipLaunchKernelGGL(inv_scan_kernel, dim3((unsigned)bh), dim3(1024), 0, st, cnt, start, n);
+  return launched("scan_counts_kernel", st);
+}
+
 hipError_t launch_backward(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
   if (c.dtype == MITA_F32) return c.d == 64 ? bwd_t<float, 64>(c, b, st) : bwd_t<float, 128>(c, b, st);
   return c.d == 64 ? bwd_t<bf16_t, 64>(c, b, st) : bwd_t<bf16_t, 128>(c, b, st);

@@ -334,6 +334,37 @@ inline BwdLayout backward_layout(const mita_cfg_t &c) {
   return L;
 }
 
+// Workspace of mita_landmarks_tome (the merge rounds' buffers, TomeBufs order).
+struct TomeLayout {
+  size_t S0, S1, cnt0, cnt1, rep0, rep1, X, score, match, sel, merged, alive, pos, total;
+};
+
+inline TomeLayout tome_layout(const mita_cfg_t &c) {
+  TomeLayout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += align_up(bytes);
+    return o;
+  };
+  const size_t bh = (size_t)BH(c), n = (size_t)c.N, h = (n + 1) / 2;
+  L.S0 = take(bh * n * c.d * 8);
+  L.S1 = take(bh * n * c.d * 8);
+  L.cnt0 = take(bh * n * 4);
+  L.cnt1 = take(bh * n * 4);
+  L.rep0 = take(bh * n * 4);
+  L.rep1 = take(bh * n * 4);
+  L.X = take(bh * n * c.d * 4);
+  L.score = take(bh * h * 4);
+  L.match = take(bh * h * 4);
+  L.sel = take(bh * h * 4);
+  L.merged = take(bh * h * 4);
+  L.alive = take(bh * n * 4);
+  L.pos = take(bh * (n + 1) * 4);
+  L.total = off;
+  return L;
+}
+
 inline size_t workspace_size(const mita_cfg_t *c, int which) {
   if (check_cfg(c, nullptr) != MITA_OK) return 0;
   switch (which) {
@@ -343,6 +374,7 @@ inline size_t workspace_size(const mita_cfg_t *c, int which) {
     case MITA_WS_ROUTE: return route_ws_bytes(*c);
     case MITA_WS_ATTEND: return attend_ws_bytes(*c);
     case MITA_WS_BACKWARD: return c->s == 1 || !c->use_routed ? backward_layout(*c).total : 0;
+    case MITA_WS_TOME: return tome_layout(*c).total;
     default: return 0;
   }
 }

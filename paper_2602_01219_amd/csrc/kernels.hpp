@@ -118,4 +118,21 @@ struct BwdBufs {
 };
 hipError_t launch_backward(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st);
 
+// Exclusive scan of n int32 counts per head (cnt [BH, n]) into start [BH, n + 1].
+hipError_t launch_scan_counts(const int32_t *cnt, int32_t *start, int n, int64_t bh, hipStream_t st);
+
+// Token merging as landmark extraction: q_lm [BH, M, d]; assign [BH, N] (the
+// landmark of every token) when not NULL. Buffers of the merge rounds:
+struct TomeBufs {
+  int64_t *S[2];           // [BH, N, d] member sums of the current tokens (fixed point), ping-pong
+  int32_t *cnt[2];         // [BH, N] member counts
+  int32_t *rep[2];         // [BH, N] every token's current position
+  float *X;                // [BH, N, d] unit vectors of the sums
+  float *score;            // [BH, ceil(N / 2)] edge scores
+  int32_t *match, *sel, *merged;  // [BH, ceil(N / 2)]
+  int32_t *alive, *pos;    // [BH, N], [BH, N + 1]
+};
+hipError_t launch_tome(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *assign, const TomeBufs &b,
+                       hipStream_t st);
+
 }  // namespace mita

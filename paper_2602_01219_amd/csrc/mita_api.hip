@@ -475,6 +475,33 @@ int mita_landmarks_select(const mita_cfg_t *cfg, const void *q, const int32_t *s
   return hip_status(launch_select_landmarks(*cfg, q, sel, q_lm, (hipStream_t)stream), "landmarks");
 }
 
+int mita_landmarks_tome(const mita_cfg_t *cfg, const void *q, void *q_lm, int32_t *assign, void *ws, size_t ws_bytes,
+                        mita_stream_t stream) {
+  g_err.clear();
+  TRY(validate(cfg));
+  TRY(need_ptr(q, "q"));
+  TRY(need_ptr(q_lm, "q_lm"));
+  if (assign) TRY(need_ptr(assign, "assign"));
+  TRY(need_ws(cfg, MITA_WS_TOME, ws, ws_bytes));
+  const TomeLayout L = tome_layout(*cfg);
+  char *w = (char *)ws;
+  TomeBufs b{};
+  b.S[0] = (int64_t *)(w + L.S0);
+  b.S[1] = (int64_t *)(w + L.S1);
+  b.cnt[0] = (int32_t *)(w + L.cnt0);
+  b.cnt[1] = (int32_t *)(w + L.cnt1);
+  b.rep[0] = (int32_t *)(w + L.rep0);
+  b.rep[1] = (int32_t *)(w + L.rep1);
+  b.X = (float *)(w + L.X);
+  b.score = (float *)(w + L.score);
+  b.match = (int32_t *)(w + L.match);
+  b.sel = (int32_t *)(w + L.sel);
+  b.merged = (int32_t *)(w + L.merged);
+  b.alive = (int32_t *)(w + L.alive);
+  b.pos = (int32_t *)(w + L.pos);
+  return hip_status(launch_tome(*cfg, q, q_lm, assign, b, (hipStream_t)stream), "landmarks (token merging)");
+}
+
 int mita_forward_lm(const mita_cfg_t *cfg, const void *q, const void *k, const void *v, const void *q_lm, void *o,
                     void *ws, size_t ws_bytes, mita_stream_t stream) {
   g_err.clear();

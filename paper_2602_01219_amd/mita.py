@@ -25,7 +25,7 @@ MITA_OK, MITA_ERR_INVALID_ARG, MITA_ERR_UNSUPPORTED, MITA_ERR_WORKSPACE, MITA_ER
 MITA_F32, MITA_BF16 = 0, 1
 MITA_FLAG_STAGED_GATHER = 0x1
 MITA_FLAG_FULL_SCORES = 0x2
-WS_FORWARD, WS_SCORES, WS_TOPK, WS_ROUTE, WS_ATTEND, WS_BACKWARD = range(6)
+WS_FORWARD, WS_SCORES, WS_TOPK, WS_ROUTE, WS_ATTEND, WS_BACKWARD, WS_TOME = range(7)
 NUM_STAGES = 6
 MAX_LAUNCHES = 32
 STAGES = ("landmarks", "scores", "topk", "gather", "route", "attend")
@@ -37,7 +37,7 @@ EXPORTED = ("mita_check", "mita_workspace_size", "mita_status_string", "mita_las
             "mita_timer_create", "mita_timer_destroy", "mita_timer_reset", "mita_timer_read",
             "mita_forward_timed", "mita_forward_fallbacks", "mita_select_plan", "mita_timer_launches",
             "mita_forward_noalloc", "mita_landmarks_select", "mita_forward_lm", "mita_forward_lm_timed",
-            "mita_backward", "mita_backward_timed")
+            "mita_backward", "mita_backward_timed", "mita_landmarks_tome")
 
 
 class CfgStruct(ctypes.Structure):
@@ -80,6 +80,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "mita_forward_lm": (I, [cfgp, P, P, P, P, P, P, Z, P]),
         "mita_forward_lm_timed": (I, [cfgp, P, P, P, P, P, P, Z, P, P]),
         "mita_backward": (I, [cfgp, P, P, P, P, P, P, P, P, P, Z, P]),
+        "mita_landmarks_tome": (I, [cfgp, P, P, P, P, Z, P]),
         "mita_backward_timed": (I, [cfgp, P, P, P, P, P, P, P, P, P, Z, P, P]),
         "mita_scores": (I, [cfgp, P, P, P, P, P, P, Z, P]),
         "mita_topk": (I, [cfgp, P, P, P, Z, P]),
@@ -281,6 +282,20 @@ def landmarks_select(cfg: Config, q, sel, q_lm=None, stream=None):
         q_lm = torch.empty((cfg.B, cfg.H, cfg.M, cfg.d), dtype=q.dtype, device=_dev(q))
     _check(lib.mita_landmarks_select(ctypes.byref(cfg.struct()), _p(q), _p(sel), _p(q_lm), _stream(stream)))
     return q_lm
+
+
+def landmarks_tome(cfg: Config, q, q_lm=None, want_assign=True, ws=None, stream=None):
+    """Token-merging landmarks: (q_lm [B, H, M, d], assign [B, H, N] int32 or
+    None), mita_landmarks_tome."""
+    lib = load_library()
+    dev = _dev(q)
+    if q_lm is None:
+        q_lm = torch.empty((cfg.B, cfg.H, cfg.M, cfg.d), dtype=q.dtype, device=dev)
+    assign = torch.empty((cfg.B, cfg.H, cfg.N), dtype=torch.int32, device=dev) if want_assign else None
+    ws, nws = _ws(cfg, WS_TOME, ws, dev)
+    _check(lib.mita_landmarks_tome(ctypes.byref(cfg.struct()), _p(q), _p(q_lm), _p(assign), _p(ws), nws,
+                                   _stream(stream)))
+    return q_lm, assign
 
 
 def scores(cfg: Config, q_lm, k, v=None, want_scores=True, want_v_lm=True, ws=None, stream=None):

@@ -101,13 +101,17 @@ def test_top_s_routing_parity(name, s, B):
         assert np.array_equal(o_all[b, h], g.offsets)
 
 
-def _forward_check(cfg, inp, q, k, v, slices, row_limit, lm_sel=None):
-    """The forward (s >= 1, pooled or selected landmarks) against the oracle
-    given the GPU's discrete choices (validated first)."""
+def _forward_check(cfg, inp, q, k, v, slices, row_limit, lm_sel=None, q_lm_given=None):
+    """The forward (s >= 1, pooled, selected or given landmarks) against the
+    oracle given the GPU's discrete choices (validated first)."""
     wl = inp.wl
     sel_dev = None if lm_sel is None else torch.from_numpy(lm_sel).cuda()
-    q_lm = mita.landmarks(cfg, q) if sel_dev is None else mita.landmarks_select(cfg, q, sel_dev)
-    o_fwd = mita.forward(cfg, q, k, v) if sel_dev is None else mita.forward(cfg, q, k, v, q_lm=q_lm)
+    if q_lm_given is not None:
+        q_lm = q_lm_given
+    else:
+        q_lm = mita.landmarks(cfg, q) if sel_dev is None else mita.landmarks_select(cfg, q, sel_dev)
+    pooled = sel_dev is None and q_lm_given is None
+    o_fwd = mita.forward(cfg, q, k, v) if pooled else mita.forward(cfg, q, k, v, q_lm=q_lm)
     # the stage pipeline gives the same bits
     S, v_lm = mita.scores(cfg, q_lm, k, v)
     idx = mita.topk(cfg, S)
@@ -125,13 +129,15 @@ def _forward_check(cfg, inp, q, k, v, slices, row_limit, lm_sel=None):
     worst = 0.0
     for (b, h) in slices:
         qs, ks, vs = _slice64(inp, b, h)
-        if lm_sel is None:
+        if q_lm_given is not None:
+            q_lm_ref = q_lm_g[b, h].astype(np.float64)  # the given landmarks, exactly
+        elif lm_sel is None:
             q_lm_ref = O.landmarks(qs, cfg.grid_h, cfg.grid_w, cfg.lm_h, cfg.lm_w)
         else:
             q_lm_ref = O.landmarks_random(qs, lm_sel[b, h])
             assert np.array_equal(q_lm_g[b, h], q_lm_ref), "selected landmark rows are not exact copies"
         S_ref = O.scores(q_lm_ref, ks, cfg.eff_scale)
-        if lm_sel is None:
+        if pooled:
             # budgets with the rounding of the pooled landmarks (as for s = 1)
             tau_s, tau_r = _bounds(qs, ks, q_lm_ref, cfg, cfg.dtype)
         else:
@@ -273,3 +279,60 @@ def test_s_limits_are_rejected():
     small = dataclasses.replace(cfg, M=2, lm_h=1, lm_w=2, s=3)
     assert mita.check(small) == mita.MITA_ERR_INVALID_ARG
     assert mita.check(dataclasses.replace(small, use_routed=0)) == mita.MITA_OK
+
+
+# ------------------------------------------------------------------ token merging
+T_CASES = [("tiny_f32", None, 1, None), ("vits_bf16", 2, 4, None), ("vit_m25_bf16", 1, 3, None),
+           ("seg512_m49_bf16", 1, 2, None), ("vitb_hr_bf16", 1, 1, None), ("dense_pred_bf16", 1, 1, None)]
+
+
+@pytest.mark.parametrize("name,B,nsl,_", T_CASES, ids=[c[0] for c in T_CASES])
+def test_tome_landmarks_parity(name, B, nsl, _):
+    inp = _inputs(name, B=B)
+    wl = inp.wl
+    cfg = mita.Config.from_workload(wl)
+    q, _k, _v = _dev(inp)
+    q_lm, assign = mita.landmarks_tome(cfg, q)
+    torch.cuda.synchronize()
+    q_lm_g, asg = from_dev(q_lm), assign.cpu().numpy().astype(np.int64)
+    tol = 1e-6 if wl.dtype == "f32" else 2.0 ** -8
+    slices = [(b, h) for b in range(wl.B) for h in range(wl.H)][:nsl]
+    exact = 0
+    for (b, h) in slices:
+        qs = _slice64(inp, b, h)[0]
+        a = asg[b, h]
+        # properties at any size: a partition into M non-empty groups, each landmark its members' mean
+        assert a.min() == 0 and a.max() == wl.M - 1
+        assert (np.bincount(a, minlength=wl.M) > 0).all()
+        means = np.stack([qs[a == i].mean(axis=0) for i in range(wl.M)])
+        err_m = maxrel(q_lm_g[b, h], means)
+        assert err_m <= tol, f"landmarks are not their members' means ({err_m:.3e})"
+        # against the oracle's merge rounds where every decision has room above fp32 rounding
+        ref = O.landmarks_tome(qs, wl.M)
+        margin = min(min(m) for m in ref.margins) if ref.margins else np.inf
+        if margin > 1e-5:
+            assert np.array_equal(a, ref.assign), "merge decisions differ from the oracle's"
+            assert maxrel(q_lm_g[b, h], ref.q_lm) <= tol
+            exact += 1
+        log(f"  {name} slice ({b},{h}): {len(ref.margins)} rounds, smallest decision margin {margin:.2e}; "
+            f"landmarks vs member means {err_m:.2e}" + ("; assignment equals the oracle's" if margin > 1e-5 else
+                                                        "; margin below the fp32 budget: properties only"))
+    assert exact > 0 or wl.N >= 4096  # the exact comparison does run on the small shapes
+
+
+def test_tome_forward_against_the_oracle():
+    inp = _inputs("vits_bf16", B=2)
+    cfg = mita.Config.from_workload(inp.wl)
+    q, k, v = _dev(inp)
+    q_lm, _ = mita.landmarks_tome(cfg, q, want_assign=False)
+    _forward_check(cfg, inp, q, k, v, [(0, 0), (1, 5)], row_limit=196, q_lm_given=q_lm)
+
+
+def test_tome_is_deterministic():
+    inp = _inputs("vitb_hr_bf16", B=1)
+    cfg = mita.Config.from_workload(inp.wl)
+    q = _dev(inp)[0]
+    a1, s1 = mita.landmarks_tome(cfg, q)
+    a2, s2 = mita.landmarks_tome(cfg, q)
+    torch.cuda.synchronize()
+    assert _same(a1, a2) and torch.equal(s1, s2)
