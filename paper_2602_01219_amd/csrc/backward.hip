@@ -124,7 +124,7 @@ __global__ __launch_bounds__(256) void bwd_kernel(BwdArgs a) {
   __shared__ __align__(16) T Zqk[L::NZ];
   __shared__ float Dq[BWD_TQ];
   __shared__ int32_t qrow[BWD_TQ];  // each query's row in its tensor (token or landmark), -1 if none
-  const int64_t bh = blockIdx.y;
+  int64_t bh = blockIdx.y;
   const int tid = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63, g = lane >> 4, p = lane & 15;

@@ -291,13 +291,13 @@ __device__ __forceinline__ void half_tile_attend(Online2<D> &st, const T *__rest
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int swz(int r) { return (r & 6) | ((r >> 3) & 1); }
 
-template <int D, int ROWS = TK> struct DmaTile {
+template <int D, int ROWS = TK, int NW = 4> struct DmaTile {
   static constexpr int CPR = D / 8;          // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;       // rows per wave instruction
   static constexpr int NI = ROWS / RPI;      // instructions per ROWS-row matrix
-  static constexpr int PW = NI / 4;          // per wave of a 4-wave workgroup
+  static constexpr int PW = NI / NW;         // per wave of an NW-wave workgroup
   static constexpr int BYTES = ROWS * D * 2; // one ROWS-row matrix
-  static_assert(PW >= 1 && NI % 4 == 0, "whole instructions per wave");
+  static_assert(PW >= 1 && NI % NW == 0, "whole instructions per wave");
 };
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -312,12 +312,12 @@ template <typename T> __device__ __forceinline__ void pin(T &x) { asm volatile("
 // Per-lane part of the DMA of one tile, fixed for every tile: the tile row r
 // this lane loads (rows start at multiples of 32, so the swizzle of r is the
 // same in every tile) and its 16-byte source chunk (sl ^ swz(r)) << 4.
-template <int D, int ROWS> struct DmaLane {
-  static constexpr int PW = DmaTile<D, ROWS>::PW;
+template <int D, int ROWS, int NW = 4> struct DmaLane {
+  static constexpr int PW = DmaTile<D, ROWS, NW>::PW;
   uint32_t row[PW];    // r, per instruction of the wave
   uint32_t chunk[PW];  // byte offset of the swizzled chunk within the row
   __device__ __forceinline__ void init(int w, int lane) {
-    using DT = DmaTile<D, ROWS>;
+    using DT = DmaTile<D, ROWS, NW>;
 #pragma unroll
     for (int j = 0; j < PW; ++j) {
       const int r = (w * PW + j) * DT::RPI + lane / DT::CPR;
@@ -331,10 +331,10 @@ template <int D, int ROWS> struct DmaLane {
 // Issue the DMA of one tile: rows r < ROWS of K and V from byte offsets
 // offs[r] past kb and vb (without FULL, rows >= nrows take offset offs[0]:
 // real data, masked later).
-template <int D, bool FULL = false, int ROWS = TK>
+template <int D, bool FULL = false, int ROWS = TK, int NW = 4>
 __device__ __forceinline__ void dma_tile(bf16_t *Kl, bf16_t *Vl, const bf16_t *kb, const bf16_t *vb,
                                          const uint32_t *offs, int nrows) {
-  using DT = DmaTile<D, ROWS>;
+  using DT = DmaTile<D, ROWS, NW>;
   // the wave index as a scalar: the LDS destinations (M0) need no readfirstlane
   const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6), lane = threadIdx.x & 63;
 #pragma unroll
@@ -352,10 +352,10 @@ __device__ __forceinline__ void dma_tile(bf16_t *Kl, bf16_t *Vl, const bf16_t *k
 
 // The same for a whole tile (every row valid) with the lane's precomputed
 // rows and chunks.
-template <int D, int ROWS>
+template <int D, int ROWS, int NW = 4>
 __device__ __forceinline__ void dma_tile_lane(bf16_t *Kl, bf16_t *Vl, const bf16_t *kb, const bf16_t *vb,
-                                              const uint32_t *offs, const DmaLane<D, ROWS> &dl) {
-  using DT = DmaTile<D, ROWS>;
+                                              const uint32_t *offs, const DmaLane<D, ROWS, NW> &dl) {
+  using DT = DmaTile<D, ROWS, NW>;
   const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
 #pragma unroll
   for (int j = 0; j < DT::PW; ++j) {
@@ -369,8 +369,8 @@ __device__ __forceinline__ void dma_tile_lane(bf16_t *Kl, bf16_t *Vl, const bf16
 }
 
 // ---------------------------------------------------------------------------
-// One wave's online softmax over DMA-staged 32-key tiles for its 16 queries
-// (one MFMA column group; lane (g, p) holds column p). The score MFMAs start
+// A wave's online softmax over DMA-staged 32-key tiles for its 16-query
+// groups (one MFMA column group each; lane (g, p) holds column p). The score MFMAs start
 // from the splat -m of the column's reference max (log2 units; the query
 // fragments are pre-scaled by scale * log2 e), so they yield the exp2
 // argument directly. The reference is the first tile's column max and moves
@@ -411,52 +411,60 @@ template <int D> struct Att16Addr {
   }
 };
 
-// Shifted scores of the tile's 32 keys (acc[kb][r]: key 16 kb + 4 g + r of query p).
-template <int D>
-__device__ __forceinline__ void att16_scores(f32x4 (&acc)[2], const Att16<D> &st, const bf16_t *__restrict__ Kl,
-                                             const Att16Addr<D> &ad, const Frag<bf16_t> (&qf)[D / 32]) {
+// The tile functions below run NGB (<= NG) query groups of one wave over the
+// same K and V fragments: each fragment read from LDS feeds one MFMA per
+// group.
+
+// Shifted scores of the tile's 32 keys (acc[c][kb][r]: key 16 kb + 4 g + r of
+// query p of group c).
+template <int D, int NGB, int NG>
+__device__ __forceinline__ void att16_scores(f32x4 (&acc)[NG][2], const Att16<D> (&st)[NG],
+                                             const bf16_t *__restrict__ Kl, const Att16Addr<D> &ad,
+                                             const Frag<bf16_t> (&qf)[NG][D / 32]) {
   constexpr int RB = 2 * D;
   const char *kbase = reinterpret_cast<const char *>(Kl);
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
-    acc[kb] = st.nm;
+#pragma unroll
+    for (int c = 0; c < NGB; ++c) acc[c][kb] = st[c].nm;
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks) {
       Frag<bf16_t> a;
       a.v = *reinterpret_cast<const uint4 *>(kbase + ad.k[ks] + kb * 16 * RB);
-      acc[kb] = mma(a, qf[ks], acc[kb]);
+#pragma unroll
+      for (int c = 0; c < NGB; ++c) acc[c][kb] = mma(a, qf[c][ks], acc[c][kb]);
     }
   }
 }
 
 // Weights of the tile (exp2 of the shifted scores; with MASKED keys i >=
-// nvalid weigh 0), the lane's weight sum, and O^T += V^T P^T.
-template <int D, bool MASKED>
-__device__ __forceinline__ void att16_pv(Att16<D> &st, const f32x4 (&acc)[2], const bf16_t *__restrict__ Vl,
-                                         const Att16Addr<D> &ad, int nvalid) {
+// nvalid weigh 0), each lane's weight sum, and O^T += V^T P^T per group.
+template <int D, bool MASKED, int NGB, int NG>
+__device__ __forceinline__ void att16_pv(Att16<D> (&st)[NG], const f32x4 (&acc)[NG][2],
+                                         const bf16_t *__restrict__ Vl, const Att16Addr<D> &ad, int nvalid) {
   constexpr int RB = 2 * D;
   const int g = (threadIdx.x & 63) >> 4;
-  float pv[8];
+  Frag<bf16_t> b[NG];
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
+  for (int c = 0; c < NGB; ++c) {
+    float pv[8];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      float x = __builtin_amdgcn_exp2f(acc[kb][r]);
-      if (MASKED && kb * 16 + 4 * g + r >= nvalid) x = 0.f;
-      pv[4 * kb + r] = x;
-    }
-  Frag<bf16_t> b;
-  b.from_f32(pv);
-  // the sum of the rounded weights, two at a time (a bf16 pair of ones as the
-  // other operand)
-  st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b.v.x), __builtin_bit_cast(bf16x2, 0x3f803f80u),
-                                         st.l, false);
-  st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b.v.y), __builtin_bit_cast(bf16x2, 0x3f803f80u),
-                                         st.l, false);
-  st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b.v.z), __builtin_bit_cast(bf16x2, 0x3f803f80u),
-                                         st.l, false);
-  st.l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b.v.w), __builtin_bit_cast(bf16x2, 0x3f803f80u),
-                                         st.l, false);
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float x = __builtin_amdgcn_exp2f(acc[c][kb][r]);
+        if (MASKED && kb * 16 + 4 * g + r >= nvalid) x = 0.f;
+        pv[4 * kb + r] = x;
+      }
+    b[c].from_f32(pv);
+    // the sum of the rounded weights, two at a time (a bf16 pair of ones as
+    // the other operand)
+    const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3f803f80u);
+    st[c].l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b[c].v.x), ones, st[c].l, false);
+    st[c].l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b[c].v.y), ones, st[c].l, false);
+    st[c].l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b[c].v.z), ones, st[c].l, false);
+    st[c].l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b[c].v.w), ones, st[c].l, false);
+  }
   const char *vbase = reinterpret_cast<const char *>(Vl);
 #pragma unroll
   for (int db = 0; db < D / 16; ++db) {
@@ -467,7 +475,8 @@ __device__ __forceinline__ void att16_pv(Att16<D> &st, const f32x4 (&acc)[2], co
           uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(vbase + ad.v[db] + h2 * 16 * RB)));
     Frag<bf16_t> a;
     a.v = make_uint4(half[0].x, half[0].y, half[1].x, half[1].y);
-    st.o[db] = mma(a, b, st.o[db]);
+#pragma unroll
+    for (int c = 0; c < NGB; ++c) st[c].o[db] = mma(a, b[c], st[c].o[db]);
   }
 }
 
@@ -483,27 +492,34 @@ template <bool MASKED> __device__ __forceinline__ float att16_lane_max(const f32
 }
 
 // The first tile of a wave: its column maxima become the references.
-template <int D, bool MASKED>
-__device__ __forceinline__ void att16_first(Att16<D> &st, const bf16_t *__restrict__ Kl, const bf16_t *__restrict__ Vl,
-                                            const Att16Addr<D> &ad, const Frag<bf16_t> (&qf)[D / 32], int nvalid) {
+template <int D, bool MASKED, int NGB, int NG>
+__device__ __forceinline__ void att16_first(Att16<D> (&st)[NG], const bf16_t *__restrict__ Kl,
+                                            const bf16_t *__restrict__ Vl, const Att16Addr<D> &ad,
+                                            const Frag<bf16_t> (&qf)[NG][D / 32], int nvalid) {
 #pragma unroll
-  for (int i = 0; i < D / 16; ++i) st.o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  st.nm = f32x4{0.f, 0.f, 0.f, 0.f};
-  st.l = 0.f;
-  f32x4 acc[2];
-  att16_scores<D>(acc, st, Kl, ad, qf);
-  const float cm = max_lane_groups(att16_lane_max<MASKED>(acc, nvalid));
-  st.nm -= cm;
+  for (int c = 0; c < NGB; ++c) {
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb) acc[kb] -= cm;
-  att16_pv<D, MASKED>(st, acc, Vl, ad, nvalid);
+    for (int i = 0; i < D / 16; ++i) st[c].o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    st[c].nm = f32x4{0.f, 0.f, 0.f, 0.f};
+    st[c].l = 0.f;
+  }
+  f32x4 acc[NG][2];
+  att16_scores<D, NGB>(acc, st, Kl, ad, qf);
+#pragma unroll
+  for (int c = 0; c < NGB; ++c) {
+    const float cm = max_lane_groups(att16_lane_max<MASKED>(acc[c], nvalid));
+    st[c].nm -= cm;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) acc[c][kb] -= cm;
+  }
+  att16_pv<D, MASKED, NGB>(st, acc, Vl, ad, nvalid);
 }
 
-// A later tile, in two parts: att16_scores and the lane max, then, when
-// some column of the wave needs it (att16_needs_rescale), att16_rescale,
-// then att16_pv. The reference of a column moves (by its excess) only when
-// the column's shifted scores exceed RESCALE_LOG2, so a query's arithmetic
-// does not depend on the other queries of the wave.
+// A later tile, with the reference check: after the scores, a group some of
+// whose columns need it (att16_needs_rescale) is rescaled (att16_rescale),
+// then the weights multiply V. The reference of a column moves (by its
+// excess) only when the column's shifted scores exceed RESCALE_LOG2, so a
+// query's arithmetic does not depend on the other queries of the wave.
 __device__ __forceinline__ bool att16_needs_rescale(float mx) { return __ballot(mx > RESCALE_LOG2) != 0; }
 
 template <int D> __device__ __forceinline__ void att16_rescale(Att16<D> &st, f32x4 (&acc)[2], float mx) {
@@ -518,26 +534,31 @@ template <int D> __device__ __forceinline__ void att16_rescale(Att16<D> &st, f32
   for (int kb = 0; kb < 2; ++kb) acc[kb] -= d;
 }
 
-template <int D, bool MASKED>
-__device__ __forceinline__ void att16_next(Att16<D> &st, const bf16_t *__restrict__ Kl, const bf16_t *__restrict__ Vl,
-                                           const Att16Addr<D> &ad, const Frag<bf16_t> (&qf)[D / 32], int nvalid) {
-  f32x4 acc[2];
-  att16_scores<D>(acc, st, Kl, ad, qf);
-  const float mx = att16_lane_max<MASKED>(acc, nvalid);
-  if (att16_needs_rescale(mx)) att16_rescale<D>(st, acc, mx);
-  att16_pv<D, MASKED>(st, acc, Vl, ad, nvalid);
+template <int D, bool MASKED, int NGB, int NG>
+__device__ __forceinline__ void att16_next(Att16<D> (&st)[NG], const bf16_t *__restrict__ Kl,
+                                           const bf16_t *__restrict__ Vl, const Att16Addr<D> &ad,
+                                           const Frag<bf16_t> (&qf)[NG][D / 32], int nvalid) {
+  f32x4 acc[NG][2];
+  att16_scores<D, NGB>(acc, st, Kl, ad, qf);
+#pragma unroll
+  for (int c = 0; c < NGB; ++c) {
+    const float mx = att16_lane_max<MASKED>(acc[c], nvalid);
+    if (att16_needs_rescale(mx)) att16_rescale<D>(st[c], acc[c], mx);
+  }
+  att16_pv<D, MASKED, NGB>(st, acc, Vl, ad, nvalid);
 }
 
 // A later tile without the reference check: the weights exp2(s - m) may
 // exceed 2^8 when a score overshoots the first tile's column max; they stay
 // finite while the overshoot is below about 2^7 (log2 units), and
 // att16_finite tells afterwards whether they did.
-template <int D, bool MASKED>
-__device__ __forceinline__ void att16_plain(Att16<D> &st, const bf16_t *__restrict__ Kl, const bf16_t *__restrict__ Vl,
-                                            const Att16Addr<D> &ad, const Frag<bf16_t> (&qf)[D / 32], int nvalid) {
-  f32x4 acc[2];
-  att16_scores<D>(acc, st, Kl, ad, qf);
-  att16_pv<D, MASKED>(st, acc, Vl, ad, nvalid);
+template <int D, bool MASKED, int NGB, int NG>
+__device__ __forceinline__ void att16_plain(Att16<D> (&st)[NG], const bf16_t *__restrict__ Kl,
+                                            const bf16_t *__restrict__ Vl, const Att16Addr<D> &ad,
+                                            const Frag<bf16_t> (&qf)[NG][D / 32], int nvalid) {
+  f32x4 acc[NG][2];
+  att16_scores<D, NGB>(acc, st, Kl, ad, qf);
+  att16_pv<D, MASKED, NGB>(st, acc, Vl, ad, nvalid);
 }
 
 // Are the query's weight sum and accumulators finite? This lane's parts,

@@ -710,6 +710,8 @@ template <typename T, int D> constexpr size_t attend_tiles_lds() {
   return 2 * (size_t)(TileDims<T, D>::K_ELEMS + TileDims<T, D>::V_ELEMS) * sizeof(T);
 }
 template <int D> constexpr size_t attend16_tiles_lds() { return 4 * (size_t)DmaTile<D, 32>::BYTES; }
+// query groups per wave of attend16_kernel
+template <int D> constexpr int ATT16_GROUPS = D == 64 ? 2 : 1;
 
 
 template <typename T, int D, bool SHARED, bool ROUTED, bool FUSED, bool IDX_LDS, bool MULTI>
@@ -731,7 +733,7 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
   auto Ks = [&](int b) { return reinterpret_cast<T *>(b ? tiles1 : tiles0); };
   auto Vt = [&](int b) { return reinterpret_cast<T *>((b ? tiles1 : tiles0) + KBYTES); };
   extern __shared__ uint32_t sidx[];  // with IDX_LDS: byte offsets of the M + k key rows
-  const int64_t bh = blockIdx.y;
+  int64_t bh = blockIdx.y;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
 
   int e = 0, q_begin, q_end;
@@ -965,28 +967,32 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
 }
 
 // ---------------------------------------------------------------------------
-// Attention with one 16-query group per wave (bf16, key row list in LDS).
-// The workgroup takes the same 64 queries as attend_kernel, but each of its
-// four waves owns 16 of them and every key, so nothing is merged across
-// waves; the keys come in 32-row tiles (K and V: 8 KB at d = 64) by LDS DMA,
-// double buffered with one barrier per tile. The smaller LDS footprint and
-// register set let more workgroups share a CU than the 2 x 2 split of
-// attend_kernel, at twice the LDS reads per MFMA (each K/V fragment serves
-// one query group).
+// Attention with whole 16-query groups per wave (bf16, key row list in LDS).
+// The workgroup takes the same 64 queries as attend_kernel; each of its
+// 4 / NG waves owns NG groups of 16 of them and every key, so nothing is
+// merged across waves. The keys come in 32-row tiles (K and V: 8 KB at
+// d = 64) by LDS DMA, double buffered with one barrier per tile. Each K / V
+// fragment read from LDS serves the wave's NG groups (NG MFMAs): with NG = 2
+// the LDS reads per MFMA are half those of NG = 1, and the two groups' MFMA
+// chains are independent.
 // ---------------------------------------------------------------------------
 constexpr int TK32 = 32;
-// d = 64: registers for seven waves per SIMD (two values spill, outside the
-// tile loop); seven workgroups of 16 + 2.5 KB LDS fit a CU at M + k = 640
-#define ATTEND16_OCCUPANCY __attribute__((amdgpu_waves_per_eu(D == 64 ? 7 : 4)))
+// d = 64, one group per wave: registers for seven waves per SIMD (seven
+// workgroups of 16 + 2.5 KB LDS fit a CU at M + k = 640); two groups per
+// wave: four waves per SIMD (eight two-wave workgroups per CU)
+#define ATTEND16_OCCUPANCY __attribute__((amdgpu_waves_per_eu(NG == 2 ? 4 : (D == 64 ? 7 : 4))))
 
-template <int D, bool SHARED, bool ROUTED, bool FUSED, bool MULTI>
-__global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
+template <int D, bool SHARED, bool ROUTED, bool FUSED, bool MULTI, int NG>
+__global__ __launch_bounds__(256 / NG) ATTEND16_OCCUPANCY void attend16_kernel(
     const bf16_t *__restrict__ q, const bf16_t *__restrict__ q_lm, const bf16_t *__restrict__ v_lm,
     const bf16_t *__restrict__ rk, const bf16_t *__restrict__ rv, const int32_t *__restrict__ idx,
     const int32_t *__restrict__ perm, const int32_t *__restrict__ offsets, const int32_t *__restrict__ tile_start,
     bf16_t *__restrict__ o, int N, int M, int k, float scale, int s, float *__restrict__ pair_o,
     float *__restrict__ pair_lse) {
-  using DT = DmaTile<D, TK32>;
+  constexpr int NW = 4 / NG;  // waves per workgroup
+  constexpr int NT = 64 * NW;
+  static_assert(NG * NW == 4 && NG * NW * 16 == ATT_TQ, "64 queries per workgroup");
+  using DT = DmaTile<D, TK32, NW>;
   static_assert(attend16_tiles_lds<D>() == 4 * DT::BYTES, "two buffers of one K and one V tile");
   // two separate arrays (see attend_kernel): K then V of one tile each
   __shared__ __align__(16) char tiles0[2 * DT::BYTES];
@@ -994,9 +1000,10 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
   auto Ks = [&](int b) { return reinterpret_cast<bf16_t *>(b ? tiles1 : tiles0); };
   auto Vt = [&](int b) { return reinterpret_cast<bf16_t *>((b ? tiles1 : tiles0) + DT::BYTES); };
   extern __shared__ uint32_t sidx[];  // byte offsets of the M + k key rows
-  const int64_t bh = blockIdx.y;
-  // the wave index as a scalar, so that the wave's busy flag and the softmax
-  // state's flags are scalar too (no exec-masked branches around the tile)
+  int64_t bh = blockIdx.y;
+  // the wave index as a scalar, so that the wave's busy count and the
+  // softmax state's flags are scalar too (no exec-masked branches around the
+  // tile)
   const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
   int e, q_begin, q_end;
@@ -1024,9 +1031,9 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
   }
   constexpr uint32_t ROWB = D * sizeof(bf16_t);
   const int nsh = with_sh ? M : 0;
-  for (int i = threadIdx.x; i < nsh; i += BLOCK) sidx[i] = (uint32_t)i * ROWB;
+  for (int i = threadIdx.x; i < nsh; i += NT) sidx[i] = (uint32_t)i * ROWB;
   if (ROUTED)
-    for (int i = threadIdx.x; i < k; i += BLOCK) sidx[nsh + i] = (uint32_t)(FUSED ? gidx[i] : i) * ROWB;
+    for (int i = threadIdx.x; i < k; i += NT) sidx[nsh + i] = (uint32_t)(FUSED ? gidx[i] : i) * ROWB;
   __syncthreads();
   const uint32_t *rows = sidx;
   auto tile_base = [&](int i, const bf16_t *&kb, const bf16_t *&vb, int &off) {
@@ -1036,22 +1043,30 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
     off = sh ? i * TK32 : nsh + (i - nA) * TK32;
   };
 
-  // this wave's 16 queries; a wave with none still stages tiles and meets
-  // the barriers but skips the arithmetic
-  const int qi = q_begin + 16 * w + p;
-  const bool qvalid = qi < q_end;
-  const int item = qvalid ? (ROUTED ? perm[bh * NP + qi] : qi) : 0;
-  const int token = MULTI ? item / s : item;
-  const bool busy = q_begin + 16 * w < q_end;
-  Frag<bf16_t> qf[D / 32];
+  // this wave's groups: group c holds queries q_begin + 16 (NG w + c) + p;
+  // the groups with queries come first (nbusy of them); a wave with none
+  // still stages tiles and meets the barriers but skips the arithmetic
+  int qi[NG];
+  bool qvalid[NG];
+  Frag<bf16_t> qf[NG][D / 32];
 #pragma unroll
-  for (int ks = 0; ks < D / 32; ++ks) {
-    if (qvalid)
-      qf[ks].load(q + (bh * N + token) * D + ks * 32 + g * 8);
-    else
-      qf[ks].zero();
+  for (int c = 0; c < NG; ++c) {
+    qi[c] = q_begin + 16 * (NG * w + c) + p;
+    qvalid[c] = qi[c] < q_end;
+    const int item = qvalid[c] ? (ROUTED ? perm[bh * NP + qi[c]] : qi[c]) : 0;
+    const int token = MULTI ? item / s : item;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      if (qvalid[c])
+        qf[c][ks].load(q + (bh * N + token) * D + ks * 32 + g * 8);
+      else
+        qf[c][ks].zero();
+    }
   }
-  DmaLane<D, TK32> dl;
+  int nbusy = 0;
+#pragma unroll
+  for (int c = 0; c < NG; ++c) nbusy += q_begin + 16 * (NG * w + c) < q_end ? 1 : 0;
+  DmaLane<D, TK32, NW> dl;
   dl.init(w, lane);
   const bf16_t *kb, *vb;
   int off;
@@ -1059,16 +1074,18 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
   // the score MFMAs take q * scale * log2 e (rounded to bf16)
   const float sl2 = scale * LOG2E;
 #pragma unroll
-  for (int ks = 0; ks < D / 32; ++ks) {
-    float x[8];
-    unpack16(qf[ks].v, x, (const bf16_t *)nullptr);
+  for (int c = 0; c < NG; ++c)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) x[j] *= sl2;
-    qf[ks].from_f32(x);
-  }
+    for (int ks = 0; ks < D / 32; ++ks) {
+      float x[8];
+      unpack16(qf[c][ks].v, x, (const bf16_t *)nullptr);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] *= sl2;
+      qf[c][ks].from_f32(x);
+    }
   Att16Addr<D> ad;
   ad.init();
-  Att16<D> st;
+  Att16<D> st[NG];
   wait_loads();
   __syncthreads();
   // step i: the DMA of tile i + 1 into the other buffer is issued, tile i is
@@ -1077,43 +1094,50 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
   // addresses). The first tile's column maxima are the references for every
   // later tile: no per-tile check, so the loop carries no branch (a branch
   // that redefines the softmax state makes the compiler move the state
-  // between two register sets on every tile). A wave without queries runs
-  // the same steps without the arithmetic, in a loop of its own for the
-  // same reason. If some weight then overflowed (a later score above the
-  // first tile's maximum by more than about 2^7 in log2 units), the whole
-  // workgroup runs its tiles once more with the reference check on every
-  // tile.
+  // between two register sets on every tile). A wave runs the loop of its
+  // number of busy groups (none: the same steps without the arithmetic), so
+  // no loop branches on it either. If some weight then overflowed (a later
+  // score above the first tile's maximum by more than about 2^7 in log2
+  // units), the whole workgroup runs its tiles once more with the reference
+  // check on every tile.
   auto issue_next = [&](int i, bf16_t *Kn, bf16_t *Vn) {
     if (i + 1 < nfull) {
       tile_base(i + 1, kb, vb, off);
-      dma_tile_lane<D, TK32>(Kn, Vn, kb, vb, rows + off, dl);
+      dma_tile_lane<D, TK32, NW>(Kn, Vn, kb, vb, rows + off, dl);
     }
   };
-  // mode 0: no arithmetic; 1: fixed references; 2: reference check per tile
-  auto run_tiles = [&](auto mode_c) {
+  // mode 0: no arithmetic; 1: fixed references; 2: reference check per tile;
+  // NGB busy groups
+  auto run_tiles = [&](auto mode_c, auto ngb_c) {
     constexpr int MODE = decltype(mode_c)::value;
+    constexpr int NGB = decltype(ngb_c)::value;
     auto tile = [&](const bf16_t *__restrict__ Kc, const bf16_t *__restrict__ Vc, bool first, int nv, auto masked_c) {
       constexpr bool MK = decltype(masked_c)::value;
-      if (MODE == 0) return;
+      if (MODE == 0 || NGB == 0) return;
       if (first)
-        att16_first<D, MK>(st, Kc, Vc, ad, qf, nv);
+        att16_first<D, MK, NGB>(st, Kc, Vc, ad, qf, nv);
       else if (MODE == 1)
-        att16_plain<D, MK>(st, Kc, Vc, ad, qf, nv);
+        att16_plain<D, MK, NGB>(st, Kc, Vc, ad, qf, nv);
       else
-        att16_next<D, MK>(st, Kc, Vc, ad, qf, nv);
+        att16_next<D, MK, NGB>(st, Kc, Vc, ad, qf, nv);
     };
     auto step = [&](int i, const bf16_t *__restrict__ Kc, const bf16_t *__restrict__ Vc, bf16_t *__restrict__ Kn,
                     bf16_t *__restrict__ Vn) {
       issue_next(i, Kn, Vn);
+      // the DMA is issued before the tile's arithmetic: the scheduler would
+      // otherwise sink it to the end of the step, right before its wait
+      __builtin_amdgcn_sched_barrier(0);
       tile(Kc, Vc, false, TK32, std::false_type{});
       wait_loads();
       __syncthreads();
     };
     if (nfull > 0) {
-      dma_tile_lane<D, TK32>(Ks(0), Vt(0), nA > 0 ? sh_k : rkb, nA > 0 ? sh_v : rvb, rows + (nA > 0 ? 0 : nsh), dl);
+      dma_tile_lane<D, TK32, NW>(Ks(0), Vt(0), nA > 0 ? sh_k : rkb, nA > 0 ? sh_v : rvb,
+                                 rows + (nA > 0 ? 0 : nsh), dl);
       wait_loads();
       __syncthreads();
       issue_next(0, Ks(1), Vt(1));
+      __builtin_amdgcn_sched_barrier(0);
       tile(Ks(0), Vt(0), true, TK32, std::false_type{});
       wait_loads();
       __syncthreads();
@@ -1129,19 +1153,24 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
       const int nr = part == 0 ? pA : pB;
       if (nr == 0) continue;  // uniform
       if (part == 0)
-        dma_tile<D, false, TK32>(Ks(0), Vt(0), sh_k, sh_v, rows + nA * TK32, nr);
+        dma_tile<D, false, TK32, NW>(Ks(0), Vt(0), sh_k, sh_v, rows + nA * TK32, nr);
       else
-        dma_tile<D, false, TK32>(Ks(0), Vt(0), rkb, rvb, rows + nsh + nB * TK32, nr);
+        dma_tile<D, false, TK32, NW>(Ks(0), Vt(0), rkb, rvb, rows + nsh + nB * TK32, nr);
       wait_loads();
       __syncthreads();
       tile(Ks(0), Vt(0), nfull == 0 && (part == 0 || pA == 0), nr, std::true_type{});
       __syncthreads();
     }
   };
-  if (busy)
-    run_tiles(std::integral_constant<int, 1>{});
-  else
-    run_tiles(std::integral_constant<int, 0>{});
+  auto run_busy = [&](auto mode_c) {
+    if (NG == 2 && nbusy == 2)
+      run_tiles(mode_c, std::integral_constant<int, NG>{});
+    else if (nbusy >= 1)
+      run_tiles(mode_c, std::integral_constant<int, 1>{});
+    else
+      run_tiles(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{});
+  };
+  run_busy(std::integral_constant<int, 1>{});
   // A query whose weights all stayed finite is written now; if any query of
   // the workgroup overflowed, the workgroup runs its tiles again with the
   // reference check on every tile and those queries are written from that
@@ -1149,18 +1178,22 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
   uint32_t *redo = sidx + nsh + (ROUTED ? k : 0);  // one word past the row list
   if (threadIdx.x == 0) *redo = 0u;
   __syncthreads();
-  bool done = true;
-  if (busy) {
-    done = att16_finite<D>(st);
-    if (__ballot(!done) && lane == 0) atomicOr(redo, 1u);
+  bool done[NG];
+#pragma unroll
+  for (int c = 0; c < NG; ++c) {
+    done[c] = true;
+    if (c < nbusy) {
+      done[c] = att16_finite<D>(st[c]);
+      if (__ballot(!done[c]) && lane == 0) atomicOr(redo, 1u);
+    }
   }
-  auto write_out = [&]() {
-    const float lsum = att16_sum<D>(st);
+  auto write_out = [&](int c) {
+    const float lsum = att16_sum<D>(st[c]);
     const float inv = __builtin_amdgcn_rcpf(lsum);
     // the token is read again (the barriers in between keep the compiler
     // from reusing the first read), so no address stays live across the
     // tile loop
-    const int tok = ROUTED ? perm[bh * NP + qi] : qi;
+    const int tok = ROUTED ? perm[bh * NP + qi[c]] : qi[c];
     if constexpr (MULTI) {
       // the pair's normalised partial and its log-sum-exp (log2 units; the
       // scores were pre-scaled by log2 e, the reference is -nm)
@@ -1168,8 +1201,8 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
 #pragma unroll
       for (int db = 0; db < D / 16; ++db)
         *reinterpret_cast<float4 *>(prow + db * 16 + 4 * g) =
-            make_float4(st.o[db][0] * inv, st.o[db][1] * inv, st.o[db][2] * inv, st.o[db][3] * inv);
-      if (g == 0) pair_lse[bh * NP + tok] = __log2f(lsum) - st.nm[0];
+            make_float4(st[c].o[db][0] * inv, st[c].o[db][1] * inv, st[c].o[db][2] * inv, st[c].o[db][3] * inv);
+      if (g == 0) pair_lse[bh * NP + tok] = __log2f(lsum) - st[c].nm[0];
       return;
     }
     bf16_t *orow = o + (bh * N + tok) * D;
@@ -1177,18 +1210,19 @@ __global__ __launch_bounds__(BLOCK) ATTEND16_OCCUPANCY void attend16_kernel(
     for (int db = 0; db < D / 16; ++db) {
       bf16_t vals[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) vals[r] = from_f32<bf16_t>(st.o[db][r] * inv);
+      for (int r = 0; r < 4; ++r) vals[r] = from_f32<bf16_t>(st[c].o[db][r] * inv);
       *reinterpret_cast<uint2 *>(orow + db * 16 + 4 * g) = *reinterpret_cast<const uint2 *>(vals);
     }
   };
-  if (qvalid && done) write_out();
+#pragma unroll
+  for (int c = 0; c < NG; ++c)
+    if (qvalid[c] && done[c]) write_out(c);
   __syncthreads();
   if (*redo) {  // uniform for the workgroup
-    if (busy)
-      run_tiles(std::integral_constant<int, 2>{});
-    else
-      run_tiles(std::integral_constant<int, 0>{});
-    if (qvalid && !done) write_out();
+    run_busy(std::integral_constant<int, 2>{});
+#pragma unroll
+    for (int c = 0; c < NG; ++c)
+      if (qvalid[c] && !done[c]) write_out(c);
   }
 }
 
@@ -1417,7 +1451,10 @@ static hipError_t attend_t3(const mita_cfg_t &c, const void *q, const void *q_lm
     // bf16: lists of up to IDX_LDS_MAX - 1 rows (and the kernel's rerun flag)
     // beside the 16 / 32 KB DMA tiles
     if (list_in_lds(nlist + 1, attend16_tiles_lds<D>())) {
-      hipLaunchKernelGGL((attend16_kernel<D, SH, RT, FU, MU>), grid, dim3(BLOCK), (size_t)(nlist + 1) * sizeof(int32_t),
+      // d = 64: two query groups per wave, two waves; d = 128: one group, four
+      constexpr int NG = ATT16_GROUPS<D>;
+      hipLaunchKernelGGL((attend16_kernel<D, SH, RT, FU, MU, NG>), grid, dim3(256 / NG),
+                         (size_t)(nlist + 1) * sizeof(int32_t),
                          st, (const bf16_t *)q, (const bf16_t *)q_lm, (const bf16_t *)v_lm, (const bf16_t *)rk,
                          (const bf16_t *)rv, idx, perm, offsets, tile_start, (bf16_t *)o, c.N, c.M, c.k, eff_scale(c), s,
                          pair_o, pair_lse);

@@ -6,26 +6,36 @@
 
 namespace mita {
 
-// Work-list tiles are spread so that consecutive tiles (usually of the same
-// expert) run on the same XCD and share its L2: with 8 XCDs taking workgroups
-// round robin, x -> (xcd = x % 8, slot = x / 8) covers tile xcd * C + slot,
-// C = ceil(tiles / 8); the grid's x extent is a multiple of 8.
+// Work-list tiles are spread so that each XCD takes a contiguous range of
+// the (head, tile) slots, head-major: with at least 8 heads an XCD works
+// through whole heads, one at a time, so the head's K and V rows are fetched
+// into that XCD's L2 only (spread by tile within each head, every XCD needed
+// a share of every head's rows, about three times the K / V fetches at the
+// 16K-token shape); consecutive tiles, usually of one expert, share the L2
+// too. Workgroups go to the 8 XCDs round robin by linear index L (x fastest),
+// so slot f = (L % 8) * C + L / 8, C = slots / 8, covers head f / T and tile
+// f % T of that head, T = the grid's x extent (a multiple of 8).
 constexpr int NXCD = 8;
 
-// The workgroup's queries [q_begin, q_end) (positions in perm) and their
-// group e (of G), from the work list; false for a workgroup past its end.
+// The workgroup's head bh, queries [q_begin, q_end) (positions in perm) and
+// their group e (of G), from the work list; false for a workgroup past its
+// end. Without ROUTED, bh keeps the caller's value and the workgroup takes
+// queries 64 blockIdx.x onwards.
 template <bool ROUTED>
 __device__ __forceinline__ bool attend_queries(const int32_t *__restrict__ tile_start,
-                                               const int32_t *__restrict__ offsets, int64_t bh, int N, int M, int &e,
-                                               int &q_begin, int &q_end) {
+                                               const int32_t *__restrict__ offsets, int64_t &bh, int N, int M,
+                                               int &e, int &q_begin, int &q_end) {
   e = 0;
   if (ROUTED) {
+    const int T = (int)gridDim.x;
+    const int64_t L = (int64_t)blockIdx.y * T + blockIdx.x;
+    const int64_t C = (int64_t)T * gridDim.y / NXCD;
+    const int64_t f = (L % NXCD) * C + L / NXCD;
+    bh = f / T;
+    const int t = (int)(f % T);
     const int32_t *ts = tile_start + bh * (M + 1);
     const int ntl = ts[M];
-    const int C = (ntl + NXCD - 1) / NXCD;
-    const int slot = (int)blockIdx.x / NXCD;
-    const int t = ((int)blockIdx.x % NXCD) * C + slot;
-    if (slot >= C || t >= ntl) return false;
+    if (t >= ntl) return false;
     int lo = 0, hi = M - 1;  // largest e with ts[e] <= t
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
