@@ -58,7 +58,7 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def kernel_work(name: str, wl, plan: dict, staged: bool, s: int = 1):
+def kernel_work(name: str, wl, plan: dict, staged: bool, s: int = 1, launched=()):
     """Algorithmic (bytes, flops) of one launch of kernel `name`: the tensors
     its step must read and write at least (inputs once, outputs once) and its
     multiply-adds x 2. Intermediate buffers of this design (score-pass
@@ -85,7 +85,12 @@ def kernel_work(name: str, wl, plan: dict, staged: bool, s: int = 1):
         "scores_kernel": (tens * (1 + sh) + lmt + 4 * BH * M * N * stored_s, 2 * M * N * d * BH * (1 + sh)),
         "merge_kernel": (BH * nch * M * (d + 2) * 4 + lmt, 0),
         "finalize_kernel": (4 * rows * k + lmt * sh, 0),
-        "finalize_logits_kernel": (4 * rows * k + lmt * sh + tens + lmt + 4 * BH * N, 2 * N * M * d * BH),
+        # the routing logits run in the finish launch unless the pivot launch
+        # took them (sample_logits_kernel)
+        "finalize_logits_kernel": (4 * rows * k + lmt * sh, 0) if "sample_logits_kernel" in launched else
+                                  (4 * rows * k + lmt * sh + tens + lmt + 4 * BH * N, 2 * N * M * d * BH),
+        "sample_logits_kernel": (BH * ns * d * e + lmt + 4 * rows + tens + lmt + 4 * BH * N,
+                                 2 * M * ns * d * BH + 2 * N * M * d * BH),
         "topk_scatter_kernel": (8 * BH * N + 8 * BH * (M + 1), 0),
         "scores_rows_kernel": (0, 0),
         "topk_kernel": (4 * BH * M * N + 4 * rows * k, 0),
@@ -380,7 +385,7 @@ def run(wl, name, a, dense: bool):
     kernels = []
     for kname, us in sorted(per_kernel.items(), key=lambda x: -x[1]):
         us /= ncalls
-        by, fl = kernel_work(kname, wl, plan, a.staged_gather, s_exp)
+        by, fl = kernel_work(kname, wl, plan, a.staged_gather, s_exp, per_kernel)
         ent = price(kname, us, by, fl, wl.dtype)
         ent["launches_per_forward"] = round(launches[kname] / ncalls, 2)
         kernels.append(ent)

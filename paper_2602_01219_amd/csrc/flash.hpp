@@ -423,6 +423,7 @@ __device__ __forceinline__ void att16_scores(f32x4 (&acc)[NG][2], const Att16<D>
                                              const Frag<bf16_t> (&qf)[NG][D / 32]) {
   constexpr int RB = 2 * D;
   const char *kbase = reinterpret_cast<const char *>(Kl);
+  __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
@@ -435,6 +436,7 @@ __device__ __forceinline__ void att16_scores(f32x4 (&acc)[NG][2], const Att16<D>
       for (int c = 0; c < NGB; ++c) acc[c][kb] = mma(a, qf[c][ks], acc[c][kb]);
     }
   }
+  __builtin_amdgcn_s_setprio(0);
 }
 
 // Weights of the tile (exp2 of the shifted scores; with MASKED keys i >=
@@ -475,9 +477,11 @@ __device__ __forceinline__ void att16_pv(Att16<D> (&st)[NG], const f32x4 (&acc)[
           uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(vbase + ad.v[db] + h2 * 16 * RB)));
     Frag<bf16_t> a;
     a.v = make_uint4(half[0].x, half[0].y, half[1].x, half[1].y);
+    if (db == 0) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int c = 0; c < NGB; ++c) st[c].o[db] = mma(a, b[c], st[c].o[db]);
   }
+  __builtin_amdgcn_s_setprio(0);
 }
 
 // Maximum of the lane's 8 shifted scores (with MASKED only keys < nvalid).

@@ -77,11 +77,21 @@ hipError_t launch_route(const mita_cfg_t &c, const void *q, const void *q_lm, in
 
 // The finish of the fused selection (launch_select_finish: top-k into idx,
 // fallback rows, landmark-value merge into v_lm when given) together with the
-// routing (launch_route), in three combined launches.
+// routing (launch_route), in two combined launches; with logits_done the
+// routing logits (expert, counts) were formed by launch_pivots_logits and the
+// first launch runs the selection's finish rows alone.
 hipError_t launch_select_route(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
                                const SelectBufs &sel, float *S, int32_t *idx, const void *partial, void *v_lm,
                                int32_t *expert, int32_t *perm, int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base,
-                               int32_t *counts, int32_t *tile_start, hipStream_t st);
+                               int32_t *counts, int32_t *tile_start, bool logits_done, hipStream_t st);
+
+// Whether launch_pivots_logits serves this configuration (bf16, sample in LDS).
+bool pivots_with_logits(const mita_cfg_t &c, const SelectBufs &sel);
+// The sampled scores and pivots (launch_select_pivots) and the routing
+// logits (expert [BH,N] and counts [BH,M], which must be zero on entry) in one
+// launch.
+hipError_t launch_pivots_logits(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
+                                const SelectBufs &sel, int32_t *expert, int32_t *counts, hipStream_t st);
 
 // Attention work list from offsets: tile_start [BH, M+1].
 hipError_t launch_worklist(const mita_cfg_t &c, const int32_t *offsets, int32_t *tile_start, hipStream_t st);

@@ -178,7 +178,13 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
     TRY(hip_status(launch_pool(*c, q, q_lm_ws, zero_counts, zero_cursor, st), "landmarks"));
   }
   TRY(mark(1));
-  if (fused) TRY(hip_status(launch_select_pivots(*c, q_lm, k, sel, st), "select pivots"));
+  // bf16: the routing logits are formed beside the sampled scores (they
+  // depend on the landmarks only), in the same launch
+  const bool logits_early = sel_in_route && pivots_with_logits(*c, sel);
+  if (logits_early)
+    TRY(hip_status(launch_pivots_logits(*c, q, q_lm, k, sel, expert, counts, st), "select pivots"));
+  else if (fused)
+    TRY(hip_status(launch_select_pivots(*c, q_lm, k, sel, st), "select pivots"));
   TRY(hip_status(launch_scores(*c, q_lm, k, v, fused ? nullptr : S, v_lm, w + L.partial, fused ? &sel : nullptr, st),
                  "scores"));
   TRY(mark(2));
@@ -191,7 +197,7 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
   TRY(mark(4));
   if (sel_in_route)
     TRY(hip_status(launch_select_route(*c, q, q_lm, k, sel, S, idx, w + L.partial, v_lm, expert, perm, offsets,
-                                       tile_cnt, tile_base, counts, tile_start, st),
+                                       tile_cnt, tile_base, counts, tile_start, logits_early, st),
                    "route"));
   else if (c->use_routed)
     TRY(hip_status(

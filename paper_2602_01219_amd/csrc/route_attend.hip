@@ -9,6 +9,7 @@
 #include "scores.hpp"
 #include "topk_row.hpp"
 #include "finalize.hpp"
+#include "sample.hpp"
 #include "worklist.hpp"
 
 namespace mita {
@@ -33,9 +34,9 @@ template <typename T, int D> struct RouteLds {
   static constexpr int BYTES = ROUTE_LB * LSTR * (int)sizeof(T);
 };
 
-// Workgroup (bx, by) of the routing grid; lms: RouteLds<T, D>::BYTES of LDS,
-// cnt: 4 M words of LDS.
-template <typename T, int D, bool TILES = true>
+// Workgroup (bx, by) of the routing grid (NWV waves, one 64-query tile
+// each); lms: RouteLds<T, D>::BYTES of LDS, cnt: NWV M words of LDS.
+template <typename T, int D, bool TILES = true, int NWV = 4>
 __device__ __forceinline__ void route_logits_body(T *lms, uint32_t *cnt, int bx, int by, const T *__restrict__ q,
                                                   const T *__restrict__ q_lm, int32_t *__restrict__ expert,
                                                   int32_t *__restrict__ tile_cnt, int32_t *__restrict__ counts, int N,
@@ -44,7 +45,7 @@ __device__ __forceinline__ void route_logits_body(T *lms, uint32_t *cnt, int bx,
   constexpr int LSTR = RouteLds<T, D>::LSTR;
   const int64_t bh = by;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
-  const int tile = bx * 4 + w;
+  const int tile = bx * NWV + w;
   uint32_t *wc = cnt + w * M;
   for (int i = lane; i < M; i += 64) wc[i] = 0u;
   Frag<T> qf[4][D / 32];
@@ -70,7 +71,7 @@ __device__ __forceinline__ void route_logits_body(T *lms, uint32_t *cnt, int bx,
   for (int l0 = 0; l0 < M; l0 += ROUTE_LB) {
     const int nl = min(ROUTE_LB, M - l0);
     __syncthreads();
-    for (int ch = threadIdx.x; ch < ROUTE_LB * (D / VE); ch += BLOCK) {
+    for (int ch = threadIdx.x; ch < ROUTE_LB * (D / VE); ch += 64 * NWV) {
       const int r = ch / (D / VE), cc = ch % (D / VE);
       uint4 x = make_uint4(0, 0, 0, 0);
       if (r < nl) x = *reinterpret_cast<const uint4 *>(lmb + (int64_t)(l0 + r) * D + cc * VE);
@@ -610,6 +611,40 @@ __global__ __launch_bounds__(BLOCK) void finalize_logits_kernel(
   }
   route_logits_body<T, D, false>(reinterpret_cast<T *>(buf), cnt, i % route_x, i / route_x, q, q_lm, expert, tile_cnt, counts,
                           N, M, scale, ntiles);
+}
+
+// ---------------------------------------------------------------------------
+// bf16: the sampled scores and pivots and the routing logits (independent of
+// each other) share one launch of 16-wave workgroups: the few sample
+// workgroups are latency-bound and leave CUs idle, which the routing
+// workgroups (sixteen 64-query tiles each) fill. Workgroups [0, nS) take the
+// sample grid (x fastest), the rest the routing grid; LDS is one buffer that
+// either part lays out for itself.
+// ---------------------------------------------------------------------------
+template <typename T, int D> struct SampleLogitsLds {
+  static constexpr int A = 16 * SP_PITCH * (int)sizeof(uint32_t);
+  static constexpr int BYTES = A > RouteLds<T, D>::BYTES ? A : RouteLds<T, D>::BYTES;
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(1024) void sample_logits_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
+                                                             uint32_t *__restrict__ plo,
+                                                             uint32_t *__restrict__ fail_cnt, int ns, int r,
+                                                             int sample_x, int nS, const T *__restrict__ q,
+                                                             int32_t *__restrict__ expert,
+                                                             int32_t *__restrict__ counts, int N, int M, float scale,
+                                                             int ntiles, int route_x) {
+  __shared__ __align__(16) char buf[SampleLogitsLds<T, D>::BYTES];
+  extern __shared__ uint32_t cnt[];  // routing: [16][M]
+  const int b = (int)blockIdx.x;
+  if (b < nS) {
+    sample_pivot_body<T, D, 16>(reinterpret_cast<uint32_t(*)[SP_PITCH]>(buf), b % sample_x, b / sample_x, q_lm, k,
+                                plo, fail_cnt, N, M, ns, r, scale);
+    return;
+  }
+  const int i = b - nS;
+  route_logits_body<T, D, false, 16>(reinterpret_cast<T *>(buf), cnt, i % route_x, i / route_x, q, q_lm, expert,
+                                     nullptr, counts, N, M, scale, ntiles);
 }
 
 // Workgroups [0, nT) take the fallback rows: each scores its rows in full
@@ -1354,7 +1389,8 @@ template <typename T, int D, int CAP, bool MERGE>
 static hipError_t select_route_t(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
                                  const SelectBufs &sb, float *S, int32_t *idx, const void *partial, void *v_lm,
                                  int32_t *expert, int32_t *perm, int32_t *offsets, int32_t *tile_cnt,
-                                 int32_t *tile_base, int32_t *counts, int32_t *tile_start, hipStream_t st) {
+                                 int32_t *tile_base, int32_t *counts, int32_t *tile_start, bool logits_done,
+                                 hipStream_t st) {
   const int nt = route_tiles(c);
   const int bh = (int)BH(c);
   const int nch = score_chunks(c);
@@ -1362,10 +1398,11 @@ static hipError_t select_route_t(const mita_cfg_t &c, const void *q, const void 
   const float2 *ml = (const float2 *)partial;
   const float *po = MERGE ? (const float *)((const char *)partial + align_up((size_t)rows * nch * sizeof(float2)))
                           : nullptr;
+  // with the logits formed beside the sampled scores, the finish rows run alone
   const int route_x = (nt + 3) / 4;
-  const int nF = (int)rows, nR = route_x * bh;
+  const int nF = (int)rows, nR = logits_done ? 0 : route_x * bh;
   hipLaunchKernelGGL((finalize_logits_kernel<T, D, CAP, MERGE>), dim3((unsigned)(nF + nR)), dim3(BLOCK),
-                     4 * c.M * sizeof(uint32_t), st, sb.cand, sb.ccnt, idx, sb.fail_cnt, sb.fail_list, c.k, sb.cap,
+                     nR ? 4 * c.M * sizeof(uint32_t) : 0, st, sb.cand, sb.ccnt, idx, sb.fail_cnt, sb.fail_list, c.k, sb.cap,
                      nch, ml, po, (T *)v_lm, nF, (const T *)q, (const T *)q_lm, expert, tile_cnt, counts, c.N, c.M,
                      eff_scale(c), nt, route_x, nR);
   hipError_t err = launched("finalize_logits_kernel", st);
@@ -1395,10 +1432,11 @@ template <typename T, int D>
 static hipError_t select_route_n(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
                                  const SelectBufs &sb, float *S, int32_t *idx, const void *partial, void *v_lm,
                                  int32_t *expert, int32_t *perm, int32_t *offsets, int32_t *tile_cnt,
-                                 int32_t *tile_base, int32_t *counts, int32_t *tile_start, hipStream_t st) {
+                                 int32_t *tile_base, int32_t *counts, int32_t *tile_start, bool logits_done,
+                                 hipStream_t st) {
 #define MITA_SR(CAP, MG)                                                                                       \
   return select_route_t<T, D, CAP, MG>(c, q, q_lm, k, sb, S, idx, partial, v_lm, expert, perm, offsets, tile_cnt, \
-                                       tile_base, counts, tile_start, st)
+                                       tile_base, counts, tile_start, logits_done, st)
   if (v_lm) {
     if (sb.cap <= 1024) MITA_SR(1024, true);
     if (sb.cap <= 2048) MITA_SR(2048, true);
@@ -1415,16 +1453,45 @@ static hipError_t select_route_n(const mita_cfg_t &c, const void *q, const void 
 hipError_t launch_select_route(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
                                const SelectBufs &sb, float *S, int32_t *idx, const void *partial, void *v_lm,
                                int32_t *expert, int32_t *perm, int32_t *offsets, int32_t *tile_cnt, int32_t *tile_base,
-                               int32_t *counts, int32_t *tile_start, hipStream_t st) {
+                               int32_t *counts, int32_t *tile_start, bool logits_done, hipStream_t st) {
   if (c.dtype == MITA_F32)
     return c.d == 64 ? select_route_n<float, 64>(c, q, q_lm, k, sb, S, idx, partial, v_lm, expert, perm, offsets,
-                                                 tile_cnt, tile_base, counts, tile_start, st)
+                                                 tile_cnt, tile_base, counts, tile_start, logits_done, st)
                      : select_route_n<float, 128>(c, q, q_lm, k, sb, S, idx, partial, v_lm, expert, perm, offsets,
-                                                  tile_cnt, tile_base, counts, tile_start, st);
+                                                  tile_cnt, tile_base, counts, tile_start, logits_done, st);
   return c.d == 64 ? select_route_n<bf16_t, 64>(c, q, q_lm, k, sb, S, idx, partial, v_lm, expert, perm, offsets,
-                                                tile_cnt, tile_base, counts, tile_start, st)
+                                                tile_cnt, tile_base, counts, tile_start, logits_done, st)
                    : select_route_n<bf16_t, 128>(c, q, q_lm, k, sb, S, idx, partial, v_lm, expert, perm, offsets,
-                                                 tile_cnt, tile_base, counts, tile_start, st);
+                                                 tile_cnt, tile_base, counts, tile_start, logits_done, st);
+}
+
+// The routing logits go beside the sampled scores when the selection's
+// finish rows hold long lists (cap above 2048 entries: 32 KB and more of LDS
+// per row), which would leave the routing workgroups that share their launch
+// few slots per CU; with shorter lists the finish launch serves them better
+// (at 16K tokens, M = 128, k = 512: 63.9 us against 75.4 for the pivots and
+// the finish together).
+bool pivots_with_logits(const mita_cfg_t &c, const SelectBufs &sb) {
+  return c.dtype == MITA_BF16 && sb.ns <= SEL_NS && sb.cap > 2048;
+}
+
+hipError_t launch_pivots_logits(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
+                                const SelectBufs &sb, int32_t *expert, int32_t *counts, hipStream_t st) {
+  if (!pivots_with_logits(c, sb)) return hipErrorInvalidValue;
+  const int bh = (int)BH(c);
+  const int sample_x = (c.M + 15) / 16, nS = sample_x * bh;
+  const int nt = route_tiles(c), route_x = (nt + 15) / 16, nR = route_x * bh;
+  const dim3 grid((unsigned)(nS + nR));
+  const size_t dyn = 16 * (size_t)c.M * sizeof(uint32_t);
+  if (c.d == 64)
+    hipLaunchKernelGGL((sample_logits_kernel<bf16_t, 64>), grid, dim3(1024), dyn, st, (const bf16_t *)q_lm,
+                       (const bf16_t *)k, sb.plo, sb.fail_cnt, sb.ns, sb.rank, sample_x, nS, (const bf16_t *)q, expert,
+                       counts, c.N, c.M, eff_scale(c), nt, route_x);
+  else
+    hipLaunchKernelGGL((sample_logits_kernel<bf16_t, 128>), grid, dim3(1024), dyn, st, (const bf16_t *)q_lm,
+                       (const bf16_t *)k, sb.plo, sb.fail_cnt, sb.ns, sb.rank, sample_x, nS, (const bf16_t *)q, expert,
+                       counts, c.N, c.M, eff_scale(c), nt, route_x);
+  return launched("sample_logits_kernel", st);
 }
 
 hipError_t launch_worklist(const mita_cfg_t &c, const int32_t *offsets, int32_t *tile_start, hipStream_t st) {

@@ -26,174 +26,17 @@
 #include "kernels.hpp"
 #include "check.hpp"
 #include "finalize.hpp"
+#include "sample.hpp"
 
 namespace mita {
-
-namespace {
-
-// Token index of sample j of ns: the middle of the j-th of ns equal parts of
-// [0, N). Distinct and below N for ns <= N; equal to j when ns == N.
-__device__ __forceinline__ int sample_pos(int j, int N, int ns) {
-  return (int)(((2 * (int64_t)j + 1) * N) / (2 * (int64_t)ns));
-}
-
-// Bin of a 256-bin histogram (hist[0..255], counted from the top bin down)
-// holding the need-th item, for one wave: returns the bin, *above = items in
-// higher bins. need must be in [1, total].
-__device__ __forceinline__ int wave_find_bin(const uint32_t *hist, uint32_t need, uint32_t *above) {
-  const int lane = threadIdx.x & 63;
-  uint32_t c[4], sum = 0;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    c[q] = hist[255 - 4 * lane - q];
-    sum += c[q];
-  }
-  const uint32_t incl = wave_inclusive_scan(sum);
-  const uint32_t excl = incl - sum;
-  int bin = -1;
-  uint32_t ab = 0;
-  if (excl < need && need <= incl) {
-    uint32_t acc = excl;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (bin < 0) {
-        if (acc + c[q] >= need)
-          bin = 255 - 4 * lane - q;
-        else
-          acc += c[q];
-      }
-    }
-    ab = acc;
-  }
-  const uint64_t m = __ballot(bin >= 0);
-  const int src = __ffsll((unsigned long long)m) - 1;
-  *above = (uint32_t)__shfl((int)ab, src);
-  return __shfl(bin, src);
-}
-
-}  // namespace
-
-// ---------------------------------------------------------------------------
-// Pivot of one landmark row from its ns (<= SEL_NS) sampled keys, held by one
-// wave: lane l holds keys 4 l + 256 i + (0..3) in v[4 i .. 4 i + 3], 0 marking
-// a slot past ns (no score has key 0, so it lies below every range). Radix
-// rounds over a 256-bin LDS histogram of the current key range (bins span
-// (hi - lo + 1) / 256 keys, so each round shrinks the range by 2^8) narrow
-// down on the r-th largest sample; after two rounds the lower edge of the bin
-// holding it is taken. That edge is at most the r-th largest sample, so at
-// least r samples are >= pivot, and its bin spans at most 2^16 keys (a
-// relative step of 2^-7 within one binade), which lists only a few more
-// tokens than the exact sample statistic would.
-// ---------------------------------------------------------------------------
-constexpr int PIVOT_PER = SEL_NS / 64;
-
-static __device__ __forceinline__ uint32_t pivot_of(const uint32_t (&v)[PIVOT_PER], uint32_t *hist, int r) {
-  const int lane = threadIdx.x & 63;
-  uint32_t mn = 0xffffffffu, mx = 0u;
-#pragma unroll
-  for (int i = 0; i < PIVOT_PER; ++i) {
-    if (v[i]) mn = min(mn, v[i]);
-    mx = max(mx, v[i]);
-  }
-  uint32_t lo = wave_min_u32(mn), hi = wave_max_u32(mx);
-  uint32_t need = (uint32_t)r;
-  for (int round = 0; round < 2 && lo < hi; ++round) {
-    const uint32_t span = hi - lo;
-    const int bits = 32 - __clz((int)span);
-    const int shift = bits > 8 ? bits - 8 : 0;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) hist[lane + 64 * q] = 0u;
-#pragma unroll
-    for (int i = 0; i < PIVOT_PER; ++i)
-      if (v[i] >= lo && v[i] <= hi) atomicAdd(hist + ((v[i] - lo) >> shift), 1u);
-    uint32_t above;
-    const int b = wave_find_bin(hist, need, &above);
-    need -= above;
-    lo += (uint32_t)b << shift;
-    const uint32_t width = (1u << shift) - 1u;
-    if (hi - lo > width) hi = lo + width;
-  }
-  return lo;
-}
-
-// ---------------------------------------------------------------------------
-// Sampled scores and pivots in one launch. Workgroup = NW waves over 16
-// landmark rows of one head (one MFMA column block); wave w scores them
-// against the sampled keys [SEL_NS/NW w, SEL_NS/NW (w + 1)) in tiles of 64,
-// the A fragments loaded straight from the sampled key rows (tile arithmetic
-// as in the score pass, so the same values), keys = score_key(fl(dot) * scale)
-// into LDS; then wave w takes the pivots of rows 16/NW w .. 16/NW (w + 1) - 1,
-// its histogram in the first 256 words of its own row's keys once they are in
-// registers (the wave's LDS accesses are in order). Workgroup (0, 0) also
-// zeroes the fallback counter.
-// ---------------------------------------------------------------------------
-constexpr int SP_PITCH = SEL_NS + 4;  // keys per LDS row: rows start 4 banks apart
 
 template <typename T, int D, int NW>
 __global__ __launch_bounds__(64 * NW) void sample_pivot_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
                                                                uint32_t *__restrict__ plo,
                                                                uint32_t *__restrict__ fail_cnt, int N, int M, int ns,
                                                                int r, float scale) {
-  static_assert(16 % NW == 0 && SEL_NS % (NW * TK) == 0, "sample/pivot split");
-  constexpr int PERW = SEL_NS / NW;  // samples per wave
-  constexpr int RPW = 16 / NW;       // rows per wave
   __shared__ __align__(16) uint32_t keys[16][SP_PITCH];
-  const int64_t bh = blockIdx.y;
-  const int lm0 = blockIdx.x * 16;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
-  if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *fail_cnt = 0;
-  Frag<T> qf[D / 32];
-#pragma unroll
-  for (int ks = 0; ks < D / 32; ++ks) {
-    if (lm0 + p < M)
-      qf[ks].load(q_lm + (bh * M + lm0 + p) * D + ks * 32 + g * 8);
-    else
-      qf[ks].zero();
-  }
-  const T *kb_ = k + bh * (int64_t)N * D;
-  for (int j0 = w * PERW; j0 < min(ns, (w + 1) * PERW); j0 += TK) {
-    // the tile's A fragments, all loads issued before the first is used
-    Frag<T> a[4][D / 32];
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      const int j = j0 + kb * 16 + p;  // A row p of block kb: sample j
-      const int64_t pos = j < ns ? sample_pos(j, N, ns) : 0;
-#pragma unroll
-      for (int ks = 0; ks < D / 32; ++ks) a[kb][ks].load(kb_ + pos * D + ks * 32 + g * 8);
-    }
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < D / 32; ++ks) acc = mma(a[kb][ks], qf[ks], acc);
-      // lane (g, p) holds samples j0 + 16 kb + 4 g + (0..3) of row p
-      const int jb = j0 + kb * 16 + 4 * g;
-      uint32_t key[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) key[q] = jb + q < ns ? score_key(acc[q] * scale) : 0u;
-      *reinterpret_cast<uint4 *>(&keys[p][jb]) = make_uint4(key[0], key[1], key[2], key[3]);
-    }
-  }
-  // slots past ns stay 0 (below every key) for the selection
-  for (int j = ns + (int)threadIdx.x; j < SEL_NS; j += 64 * NW)
-#pragma unroll
-    for (int row = 0; row < 16; ++row) keys[row][j] = 0u;
-  __syncthreads();
-  for (int q = 0; q < RPW; ++q) {
-    const int rl = RPW * w + q;
-    if (lm0 + rl >= M) break;  // uniform for the wave; no workgroup barriers below
-    uint32_t v[PIVOT_PER];
-#pragma unroll
-    for (int i = 0; i < PIVOT_PER / 4; ++i) {
-      const uint4 x = *reinterpret_cast<const uint4 *>(&keys[rl][256 * i + 4 * lane]);
-      v[4 * i] = x.x;
-      v[4 * i + 1] = x.y;
-      v[4 * i + 2] = x.z;
-      v[4 * i + 3] = x.w;
-    }
-    const uint32_t lo = pivot_of(v, &keys[rl][0], r);
-    if (lane == 0) plo[bh * M + lm0 + rl] = lo;
-  }
+  sample_pivot_body<T, D, NW>(keys, (int)blockIdx.x, (int)blockIdx.y, q_lm, k, plo, fail_cnt, N, M, ns, r, scale);
 }
 
 template <typename T, int D, int CAP, bool MERGE>
