@@ -433,6 +433,307 @@ __global__ __launch_bounds__(256) void bwd_kernel(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// The dQ pass for bf16 with the key row list in LDS, on the forward
+// attention's tile machinery (attend16_kernel): each wave owns NG 16-query
+// column groups of the workgroup's 64 queries and every key; 32-key tiles by
+// LDS DMA, double buffered, one barrier per tile, K and V row-major with the
+// 16-byte swizzle, K^T read by ds_read_b64_tr_b16 for dQ. Per group and key
+// tile (lane (g, p): keys 16 kb + 4 g + r of query p):
+//   pass 1 (K tiles only): S^T = K Q^T, each lane's running (max, sum) of
+//     exp2(S^T scale log2 e); the four lane groups merge into the query's
+//     log-sum-exp (log2 units);
+//   pass 2 (K and V tiles): P = exp2(S^T scale log2 e - lse), dP^T = V dO^T,
+//     dZ = P (dP - D) (rounded to bf16 for the MFMA), dQ^T += K^T dZ^T;
+// then dQ * scale, the log-sum-exp and D = dO . o (fp32, over the lane's 16
+// dimensions and then the four lane groups) are written per query, as
+// bwd_kernel does. S and P take the unscaled bf16 queries and an fp32
+// multiply by scale log2 e, as the key-owned kernel does.
+// ---------------------------------------------------------------------------
+constexpr int BWD16_TK = 32;
+template <int D> constexpr int BWD16_GROUPS = D == 64 ? 2 : 1;
+template <int D> constexpr size_t bwd16_tiles_lds() { return 4 * (size_t)DmaTile<D, BWD16_TK>::BYTES; }
+
+template <int D, bool SHARED, bool ROUTED, int NG>
+__global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(4))) void bwd_att16_kernel(BwdArgs a) {
+  constexpr int NW = 4 / NG;  // waves per workgroup
+  constexpr int NT = 64 * NW;
+  constexpr int TK = BWD16_TK;
+  static_assert(NG * NW * 16 == BWD_TQ, "64 queries per workgroup");
+  using DT = DmaTile<D, TK, NW>;
+  constexpr int RB = 2 * D;  // bytes per K / V row
+  __shared__ __align__(16) char tiles0[2 * DT::BYTES];
+  __shared__ __align__(16) char tiles1[2 * DT::BYTES];
+  auto Ks = [&](int b) { return reinterpret_cast<bf16_t *>(b ? tiles1 : tiles0); };
+  auto Vt = [&](int b) { return reinterpret_cast<bf16_t *>((b ? tiles1 : tiles0) + DT::BYTES); };
+  extern __shared__ uint32_t sidx[];  // byte offsets of the M + k key rows
+  int64_t bh = blockIdx.y;
+  const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
+  const int N = a.N, M = a.M, K = a.topk;
+  int e, q_begin, q_end;
+  if (!attend_queries<ROUTED>(a.tile_start, a.offsets, bh, N, M, e, q_begin, q_end)) return;  // uniform
+
+  const int nA = SHARED ? M / TK : 0, pA = SHARED ? M % TK : 0;
+  const int nB = ROUTED ? K / TK : 0, pB = ROUTED ? K % TK : 0;
+  const int nfull = nA + nB;
+  const bf16_t *sh_k = (const bf16_t *)a.q_lm + bh * (int64_t)M * D;
+  const bf16_t *sh_v = (const bf16_t *)a.v_lm + bh * (int64_t)M * D;
+  const bf16_t *rkb = (const bf16_t *)a.k + bh * (int64_t)N * D;
+  const bf16_t *rvb = (const bf16_t *)a.v + bh * (int64_t)N * D;
+  const int nsh = SHARED ? M : 0;
+  for (int i = threadIdx.x; i < nsh; i += NT) sidx[i] = (uint32_t)i * RB;
+  if (ROUTED) {
+    const int32_t *gidx = a.idx + (bh * M + e) * (int64_t)K;
+    for (int i = threadIdx.x; i < K; i += NT) sidx[nsh + i] = (uint32_t)gidx[i] * RB;
+  }
+  __syncthreads();
+  const uint32_t *rows = sidx;
+  auto tile_base = [&](int i, const bf16_t *&kb, const bf16_t *&vb, int &off) {
+    const bool sh = i < nA;
+    kb = sh ? sh_k : rkb;
+    vb = sh ? sh_v : rvb;
+    off = sh ? i * TK : nsh + (i - nA) * TK;
+  };
+
+  // this wave's groups: group c holds queries q_begin + 16 (NG w + c) + p
+  const bf16_t *qg = (const bf16_t *)a.q, *dOg = (const bf16_t *)a.dO, *og = (const bf16_t *)a.o;
+  int tok[NG];
+  bool qvalid[NG];
+  Frag<bf16_t> qf[NG][D / 32], df[NG][D / 32];
+  float Dq[NG];
+#pragma unroll
+  for (int c = 0; c < NG; ++c) {
+    const int qi = q_begin + 16 * (NG * w + c) + p;
+    qvalid[c] = qi < q_end;
+    tok[c] = qvalid[c] ? (ROUTED ? a.perm[bh * N + qi] : qi) : 0;
+    float dpart = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      const int64_t at = (bh * N + tok[c]) * D + ks * 32 + g * 8;
+      if (qvalid[c]) {
+        qf[c][ks].load(qg + at);
+        df[c][ks].load(dOg + at);
+        float ov[8], dv[8];
+        load16_f32(og + at, ov);
+        unpack16(df[c][ks].v, dv, (const bf16_t *)nullptr);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) dpart = __builtin_fmaf(ov[i], dv[i], dpart);
+      } else {
+        qf[c][ks].zero();
+        df[c][ks].zero();
+      }
+    }
+    // D = dO . o of query p: the four lane groups' parts, in a fixed order
+    const auto x = __builtin_amdgcn_permlane16_swap(__float_as_uint(dpart), __float_as_uint(dpart), false, false);
+    const float pair = __uint_as_float(x[0]) + __uint_as_float(x[1]);
+    const auto y = __builtin_amdgcn_permlane32_swap(__float_as_uint(pair), __float_as_uint(pair), false, false);
+    Dq[c] = __uint_as_float(y[0]) + __uint_as_float(y[1]);
+  }
+  int nbusy = 0;
+#pragma unroll
+  for (int c = 0; c < NG; ++c) nbusy += q_begin + 16 * (NG * w + c) < q_end ? 1 : 0;
+  DmaLane<D, TK, NW> dl;
+  dl.init(w, lane);
+  Att16Addr<D> ad;
+  ad.init();
+  const float sl2 = a.scale * LOG2E;
+  const bf16_t *kb, *vb;
+  int off;
+  wait_loads();
+  __syncthreads();
+
+  // S^T of the tile for the first NGB groups, from zero
+  auto scores = [&](f32x4 (&acc)[NG][2], const bf16_t *Kl, auto ngb_c) {
+    constexpr int NGB = decltype(ngb_c)::value;
+    const char *kbase = reinterpret_cast<const char *>(Kl);
+#pragma unroll
+    for (int kb2 = 0; kb2 < 2; ++kb2) {
+#pragma unroll
+      for (int c = 0; c < NGB; ++c) acc[c][kb2] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) {
+        Frag<bf16_t> A;
+        A.v = *reinterpret_cast<const uint4 *>(kbase + ad.k[ks] + kb2 * 16 * RB);
+#pragma unroll
+        for (int c = 0; c < NGB; ++c) acc[c][kb2] = mma(A, qf[c][ks], acc[c][kb2]);
+      }
+    }
+  };
+  // One sweep over the key tiles (DMA pipeline as in attend16_kernel);
+  // body(Kc, Vc, nvalid, masked_c) runs each tile's arithmetic.
+  auto sweep = [&](auto with_v_c, auto body) {
+    constexpr bool WV = decltype(with_v_c)::value;
+    auto issue = [&](int j, bf16_t *Kn, bf16_t *Vn) {
+      if (j < nfull) {
+        tile_base(j, kb, vb, off);
+        dma_tile_lane<D, TK, NW, WV>(Kn, Vn, kb, vb, rows + off, dl);
+      }
+    };
+    auto step = [&](int i, int b) {
+      issue(i + 1, Ks(b ^ 1), Vt(b ^ 1));
+      __builtin_amdgcn_sched_barrier(0);
+      body(Ks(b), Vt(b), TK, std::false_type{});
+      wait_loads();
+      __syncthreads();
+    };
+    if (nfull > 0) {
+      issue(0, Ks(0), Vt(0));
+      wait_loads();
+      __syncthreads();
+      int i = 0;
+      for (; i + 1 < nfull; i += 2) {
+        step(i, 0);
+        step(i + 1, 1);
+      }
+      if (i < nfull) step(i, 0);
+    }
+    for (int part = 0; part < 2; ++part) {
+      const int nr = part == 0 ? pA : pB;
+      if (nr == 0) continue;  // uniform
+      if (part == 0)
+        dma_tile<D, false, TK, NW, WV>(Ks(0), Vt(0), sh_k, sh_v, rows + nA * TK, nr);
+      else
+        dma_tile<D, false, TK, NW, WV>(Ks(0), Vt(0), rkb, rvb, rows + nsh + nB * TK, nr);
+      wait_loads();
+      __syncthreads();
+      body(Ks(0), Vt(0), nr, std::true_type{});
+      __syncthreads();
+    }
+  };
+
+  // ------------------------------------------------------------ pass 1: lse
+  float lm[NG], ll[NG];
+#pragma unroll
+  for (int c = 0; c < NG; ++c) {
+    lm[c] = -INFINITY;
+    ll[c] = 0.f;
+  }
+  auto pass1 = [&](auto ngb_c) {
+    constexpr int NGB = decltype(ngb_c)::value;
+    sweep(std::false_type{}, [&](const bf16_t *Kc, const bf16_t *, int nv, auto masked_c) {
+      constexpr bool MK = decltype(masked_c)::value;
+      if (NGB == 0) return;
+      f32x4 acc[NG][2];
+      scores(acc, Kc, ngb_c);
+#pragma unroll
+      for (int c = 0; c < NGB; ++c) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            mx = (!MK || 16 * kb2 + 4 * g + r < nv) ? fmaxf(mx, acc[c][kb2][r]) : mx;
+        const float mn = fmaxf(lm[c], mx * sl2);
+        float add = 0.f;
+#pragma unroll
+        for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            add += (!MK || 16 * kb2 + 4 * g + r < nv) ? __builtin_amdgcn_exp2f(__builtin_fmaf(acc[c][kb2][r], sl2, -mn))
+                                                      : 0.f;
+        ll[c] = (mn == -INFINITY ? 0.f : ll[c] * __builtin_amdgcn_exp2f(lm[c] - mn)) + add;
+        lm[c] = mn;
+      }
+    });
+  };
+  if (NG == 2 && nbusy == 2)
+    pass1(std::integral_constant<int, NG>{});
+  else if (nbusy >= 1)
+    pass1(std::integral_constant<int, 1>{});
+  else
+    pass1(std::integral_constant<int, 0>{});
+  float lse[NG];
+#pragma unroll
+  for (int c = 0; c < NG; ++c) {
+    const float mc = max_lane_groups(lm[c]);
+    const float lc = lm[c] == -INFINITY ? 0.f : ll[c] * __builtin_amdgcn_exp2f(lm[c] - mc);
+    const auto x = __builtin_amdgcn_permlane16_swap(__float_as_uint(lc), __float_as_uint(lc), false, false);
+    const float pair = __uint_as_float(x[0]) + __uint_as_float(x[1]);
+    const auto y = __builtin_amdgcn_permlane32_swap(__float_as_uint(pair), __float_as_uint(pair), false, false);
+    lse[c] = qvalid[c] ? mc + __log2f(__uint_as_float(y[0]) + __uint_as_float(y[1])) : 0.f;
+  }
+
+  // ------------------------------------------------------------ pass 2: dQ
+  f32x4 dqa[NG][D / 16];
+#pragma unroll
+  for (int c = 0; c < NG; ++c)
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) dqa[c][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto pass2 = [&](auto ngb_c) {
+    constexpr int NGB = decltype(ngb_c)::value;
+    sweep(std::true_type{}, [&](const bf16_t *Kc, const bf16_t *Vc, int nv, auto masked_c) {
+      constexpr bool MK = decltype(masked_c)::value;
+      if (NGB == 0) return;
+      f32x4 acc[NG][2], dp[NG][2];
+      scores(acc, Kc, ngb_c);
+      const char *vbase = reinterpret_cast<const char *>(Vc);
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2) {
+#pragma unroll
+        for (int c = 0; c < NGB; ++c) dp[c][kb2] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks) {
+          Frag<bf16_t> A;
+          A.v = *reinterpret_cast<const uint4 *>(vbase + ad.k[ks] + kb2 * 16 * RB);
+#pragma unroll
+          for (int c = 0; c < NGB; ++c) dp[c][kb2] = mma(A, df[c][ks], dp[c][kb2]);
+        }
+      }
+      Frag<bf16_t> z[NG];
+#pragma unroll
+      for (int c = 0; c < NGB; ++c) {
+        float zz[8];
+#pragma unroll
+        for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            float pr = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[c][kb2][r], sl2, -lse[c]));
+            if (MK && 16 * kb2 + 4 * g + r >= nv) pr = 0.f;
+            zz[4 * kb2 + r] = pr * (dp[c][kb2][r] - Dq[c]);
+          }
+        z[c].from_f32(zz);
+      }
+      // dQ^T += K^T dZ^T: the K^T operand by transposing reads of the K tile
+      const char *kbase = reinterpret_cast<const char *>(Kc);
+#pragma unroll
+      for (int db = 0; db < D / 16; ++db) {
+        uint2 half[2];
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2)
+          half[h2] = __builtin_bit_cast(
+              uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(kbase + ad.v[db] + h2 * 16 * RB)));
+        Frag<bf16_t> A;
+        A.v = make_uint4(half[0].x, half[0].y, half[1].x, half[1].y);
+#pragma unroll
+        for (int c = 0; c < NGB; ++c) dqa[c][db] = mma(A, z[c], dqa[c][db]);
+      }
+    });
+  };
+  if (NG == 2 && nbusy == 2)
+    pass2(std::integral_constant<int, NG>{});
+  else if (nbusy >= 1)
+    pass2(std::integral_constant<int, 1>{});
+  else
+    pass2(std::integral_constant<int, 0>{});
+
+  // ------------------------------------------------------------ outputs
+#pragma unroll
+  for (int c = 0; c < NG; ++c) {
+    if (!qvalid[c]) continue;
+    float *drow = a.dq + (bh * N + tok[c]) * D;
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db)
+      *reinterpret_cast<float4 *>(drow + db * 16 + 4 * g) =
+          make_float4(dqa[c][db][0] * a.scale, dqa[c][db][1] * a.scale, dqa[c][db][2] * a.scale,
+                      dqa[c][db][3] * a.scale);
+    if (g == 0) {
+      a.q_lse[bh * N + tok[c]] = lse[c];
+      a.q_D[bh * N + tok[c]] = Dq[c];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Key-owned backward of the MiTA attention: a workgroup owns KB = 64 keys
 // (wave w the 16 keys 16 w ..), whose K and V fragments stay in registers,
 // and streams the queries that attend them in tiles of 64, with each query's
@@ -823,12 +1124,31 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
   int tiles = (c.N + ATT_TQ - 1) / ATT_TQ;
   if (c.use_routed) tiles = (tiles + c.M + NXCD - 1) / NXCD * NXCD;
   const dim3 grid((unsigned)tiles, bh);
-  if (c.use_shared && c.use_routed)
-    hipLaunchKernelGGL((bwd_kernel<T, D, BWD_ATT, true, true>), grid, dim3(256), 0, st, a);
-  else if (c.use_routed)
-    hipLaunchKernelGGL((bwd_kernel<T, D, BWD_ATT, false, true>), grid, dim3(256), 0, st, a);
-  else
-    hipLaunchKernelGGL((bwd_kernel<T, D, BWD_ATT, true, false>), grid, dim3(256), 0, st, a);
+  const int nlist = (c.use_shared ? c.M : 0) + (c.use_routed ? c.k : 0);
+  bool done = false;
+  if constexpr (sizeof(T) == 2) {
+    // bf16 with the key row list in LDS: the DMA-tiled kernel
+    if (list_in_lds(nlist, bwd16_tiles_lds<D>())) {
+      constexpr int NG = BWD16_GROUPS<D>;
+      const dim3 blk(256 / NG);
+      const size_t dyn = (size_t)nlist * sizeof(uint32_t);
+      if (c.use_shared && c.use_routed)
+        hipLaunchKernelGGL((bwd_att16_kernel<D, true, true, NG>), grid, blk, dyn, st, a);
+      else if (c.use_routed)
+        hipLaunchKernelGGL((bwd_att16_kernel<D, false, true, NG>), grid, blk, dyn, st, a);
+      else
+        hipLaunchKernelGGL((bwd_att16_kernel<D, true, false, NG>), grid, blk, dyn, st, a);
+      done = true;
+    }
+  }
+  if (!done) {
+    if (c.use_shared && c.use_routed)
+      hipLaunchKernelGGL((bwd_kernel<T, D, BWD_ATT, true, true>), grid, dim3(256), 0, st, a);
+    else if (c.use_routed)
+      hipLaunchKernelGGL((bwd_kernel<T, D, BWD_ATT, false, true>), grid, dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL((bwd_kernel<T, D, BWD_ATT, true, false>), grid, dim3(256), 0, st, a);
+  }
   if ((err = launched("bwd_attend_kernel", st)) != hipSuccess) return err;
   KvArgs kv{};
   kv.q = b.q;

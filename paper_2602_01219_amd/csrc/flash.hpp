@@ -328,10 +328,10 @@ template <int D, int ROWS, int NW = 4> struct DmaLane {
   }
 };
 
-// Issue the DMA of one tile: rows r < ROWS of K and V from byte offsets
-// offs[r] past kb and vb (without FULL, rows >= nrows take offset offs[0]:
-// real data, masked later).
-template <int D, bool FULL = false, int ROWS = TK, int NW = 4>
+// Issue the DMA of one tile: rows r < ROWS of K (and, WITH_V, of V) from
+// byte offsets offs[r] past kb and vb (without FULL, rows >= nrows take
+// offset offs[0]: real data, masked later).
+template <int D, bool FULL = false, int ROWS = TK, int NW = 4, bool WITH_V = true>
 __device__ __forceinline__ void dma_tile(bf16_t *Kl, bf16_t *Vl, const bf16_t *kb, const bf16_t *vb,
                                          const uint32_t *offs, int nrows) {
   using DT = DmaTile<D, ROWS, NW>;
@@ -345,14 +345,15 @@ __device__ __forceinline__ void dma_tile(bf16_t *Kl, bf16_t *Vl, const bf16_t *k
     const uint32_t go = offs[FULL || r < nrows ? r : 0] + (uint32_t)((sl ^ swz(r)) << 4);
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(kb) + go,
                                      (lds_void_t *)(reinterpret_cast<char *>(Kl) + ins * 1024), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vb) + go,
-                                     (lds_void_t *)(reinterpret_cast<char *>(Vl) + ins * 1024), 16, 0, 0);
+    if (WITH_V)
+      __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vb) + go,
+                                       (lds_void_t *)(reinterpret_cast<char *>(Vl) + ins * 1024), 16, 0, 0);
   }
 }
 
 // The same for a whole tile (every row valid) with the lane's precomputed
 // rows and chunks.
-template <int D, int ROWS, int NW = 4>
+template <int D, int ROWS, int NW = 4, bool WITH_V = true>
 __device__ __forceinline__ void dma_tile_lane(bf16_t *Kl, bf16_t *Vl, const bf16_t *kb, const bf16_t *vb,
                                               const uint32_t *offs, const DmaLane<D, ROWS, NW> &dl) {
   using DT = DmaTile<D, ROWS, NW>;
@@ -363,8 +364,9 @@ __device__ __forceinline__ void dma_tile_lane(bf16_t *Kl, bf16_t *Vl, const bf16
     const uint32_t go = offs[dl.row[j]] + dl.chunk[j];
     __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(kb) + go,
                                      (lds_void_t *)(reinterpret_cast<char *>(Kl) + ins * 1024), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vb) + go,
-                                     (lds_void_t *)(reinterpret_cast<char *>(Vl) + ins * 1024), 16, 0, 0);
+    if (WITH_V)
+      __builtin_amdgcn_global_load_lds(reinterpret_cast<const char *>(vb) + go,
+                                       (lds_void_t *)(reinterpret_cast<char *>(Vl) + ins * 1024), 16, 0, 0);
   }
 }
 
