@@ -932,6 +932,233 @@ __global__ __launch_bounds__(256) void bwd_kv_kernel(KvArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// The key-owned backward for bf16 on the same tile machinery, with the roles
+// of queries and keys exchanged: each wave owns NG 16-key column groups of
+// the block's 64 keys (their K and V rows as MFMA B fragments in registers)
+// and streams the block's queries in 32-row tiles (Q and dO rows by LDS
+// DMA, double buffered, row-major with the 16-byte swizzle). Per group and
+// query tile (lane (g, p): queries 16 qb + 4 g + r of key p):
+//   S = Q K^T, dP = dO V^T; P = exp2(S scale log2 e - lse_q),
+//   dZ = P (dP - D_q) (both rounded to bf16 for the MFMA);
+//   dV^T += dO^T P, dK^T += Q^T dZ, with dO^T and Q^T read by transposing
+//   LDS reads of the tiles (the P and dZ fragments are already the B
+//   operand, in the key order of the transposing reads).
+// The queries' rows, log-sum-exps and D come in chunks of QC queries
+// (offsets and values staged in LDS per chunk). The sums go where
+// bwd_kv_kernel puts them (staging rows, or atomic adds for the landmarks).
+// ---------------------------------------------------------------------------
+constexpr int KV16_QC = 512;  // queries per staged chunk
+
+template <int D, bool ROUTED, int NG>
+__global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) void bwd_kv16_kernel(KvArgs a) {
+  constexpr int NW = 4 / NG;
+  constexpr int NT = 64 * NW;
+  constexpr int TQ = BWD16_TK;  // queries per tile
+  static_assert(NG * NW * 16 == BWD_KB, "64 keys per workgroup");
+  using DT = DmaTile<D, TQ, NW>;
+  constexpr int RB = 2 * D;
+  __shared__ __align__(16) char tiles0[2 * DT::BYTES];
+  __shared__ __align__(16) char tiles1[2 * DT::BYTES];
+  __shared__ uint32_t qoff[KV16_QC];
+  __shared__ float lse_s[KV16_QC], D_s[KV16_QC];
+  auto Qt = [&](int b) { return reinterpret_cast<bf16_t *>(b ? tiles1 : tiles0); };
+  auto Dt = [&](int b) { return reinterpret_cast<bf16_t *>((b ? tiles1 : tiles0) + DT::BYTES); };
+  const int64_t bh = blockIdx.y;
+  const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
+  const int N = a.N, M = a.M, K = a.topk;
+  // the block, spread over the XCDs
+  const int nb = (int)gridDim.x;
+  const int C = (nb + NXCD - 1) / NXCD;
+  const int x = ((int)blockIdx.x % NXCD) * C + (int)blockIdx.x / NXCD;
+  if (x >= a.ntotal) return;  // uniform
+  int e = 0, kb0, nkeys, q0, nq;
+  if (ROUTED) {
+    e = x / a.nblk;
+    kb0 = (x % a.nblk) * BWD_KB;
+    nkeys = min(BWD_KB, K - kb0);
+    q0 = a.offsets[bh * (M + 1) + e];
+    nq = a.offsets[bh * (M + 1) + e + 1] - q0;
+  } else {
+    kb0 = (x % a.nblk) * BWD_KB;
+    nkeys = min(BWD_KB, M - kb0);
+    q0 = (x / a.nblk) * BWD_QCHUNK;
+    nq = min(BWD_QCHUNK, N - q0);
+  }
+  // (an expert without queries still writes its staging rows: zeros)
+  const bf16_t *kbase = ROUTED ? (const bf16_t *)a.k + bh * (int64_t)N * D : (const bf16_t *)a.q_lm + bh * (int64_t)M * D;
+  const bf16_t *vbase = ROUTED ? (const bf16_t *)a.v + bh * (int64_t)N * D : (const bf16_t *)a.v_lm + bh * (int64_t)M * D;
+  Frag<bf16_t> kf[NG][D / 32], vf[NG][D / 32];
+#pragma unroll
+  for (int c = 0; c < NG; ++c) {
+    const int key = 16 * (NG * w + c) + p;
+    const bool kvalid = key < nkeys;
+    const int krow = kvalid ? (ROUTED ? a.idx[(bh * M + e) * (int64_t)K + kb0 + key] : kb0 + key) : 0;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      if (kvalid) {
+        kf[c][ks].load(kbase + (int64_t)krow * D + 32 * ks + 8 * g);
+        vf[c][ks].load(vbase + (int64_t)krow * D + 32 * ks + 8 * g);
+      } else {
+        kf[c][ks].zero();
+        vf[c][ks].zero();
+      }
+    }
+  }
+  f32x4 dka[NG][D / 16], dva[NG][D / 16];
+#pragma unroll
+  for (int c = 0; c < NG; ++c)
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) {
+      dka[c][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dva[c][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  DmaLane<D, TQ, NW> dl;
+  dl.init(w, lane);
+  Att16Addr<D> ad;
+  ad.init();
+  const float sl2 = a.scale * LOG2E;
+  const bf16_t *qg = (const bf16_t *)a.q + bh * (int64_t)N * D, *dOg = (const bf16_t *)a.dO + bh * (int64_t)N * D;
+
+  // one query tile: nv valid rows at chunk position j0
+  auto tile = [&](const bf16_t *Qc, const bf16_t *Dc, int j0, int nv, auto masked_c) {
+    constexpr bool MK = decltype(masked_c)::value;
+    const char *qbase = reinterpret_cast<const char *>(Qc), *dbase = reinterpret_cast<const char *>(Dc);
+    f32x4 s[NG][2], dp[NG][2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+#pragma unroll
+      for (int c = 0; c < NG; ++c) {
+        s[c][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        dp[c][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) {
+        Frag<bf16_t> A, B;
+        A.v = *reinterpret_cast<const uint4 *>(qbase + ad.k[ks] + qb * 16 * RB);
+        B.v = *reinterpret_cast<const uint4 *>(dbase + ad.k[ks] + qb * 16 * RB);
+#pragma unroll
+        for (int c = 0; c < NG; ++c) {
+          s[c][qb] = mma(A, kf[c][ks], s[c][qb]);
+          dp[c][qb] = mma(B, vf[c][ks], dp[c][qb]);
+        }
+      }
+    }
+    // the rows' log-sum-exps and D (queries 16 qb + 4 g + r of the tile)
+    float lq[2][4], dq[2][4];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const float4 l4 = *reinterpret_cast<const float4 *>(&lse_s[j0 + 16 * qb + 4 * g]);
+      const float4 d4 = *reinterpret_cast<const float4 *>(&D_s[j0 + 16 * qb + 4 * g]);
+      lq[qb][0] = l4.x; lq[qb][1] = l4.y; lq[qb][2] = l4.z; lq[qb][3] = l4.w;
+      dq[qb][0] = d4.x; dq[qb][1] = d4.y; dq[qb][2] = d4.z; dq[qb][3] = d4.w;
+    }
+    Frag<bf16_t> pf[NG], zf[NG];
+#pragma unroll
+    for (int c = 0; c < NG; ++c) {
+      float pp[8], zz[8];
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float pr = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][qb][r], sl2, -lq[qb][r]));
+          if (MK && 16 * qb + 4 * g + r >= nv) pr = 0.f;
+          pp[4 * qb + r] = pr;
+          zz[4 * qb + r] = pr * (dp[c][qb][r] - dq[qb][r]);
+        }
+      pf[c].from_f32(pp);
+      zf[c].from_f32(zz);
+    }
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) {
+      uint2 hq[2], hd[2];
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        hq[h2] = __builtin_bit_cast(
+            uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(qbase + ad.v[db] + h2 * 16 * RB)));
+        hd[h2] = __builtin_bit_cast(
+            uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(dbase + ad.v[db] + h2 * 16 * RB)));
+      }
+      Frag<bf16_t> AQ, AD;
+      AQ.v = make_uint4(hq[0].x, hq[0].y, hq[1].x, hq[1].y);
+      AD.v = make_uint4(hd[0].x, hd[0].y, hd[1].x, hd[1].y);
+#pragma unroll
+      for (int c = 0; c < NG; ++c) {
+        dva[c][db] = mma(AD, pf[c], dva[c][db]);
+        dka[c][db] = mma(AQ, zf[c], dka[c][db]);
+      }
+    }
+  };
+
+  for (int c0 = 0; c0 < nq; c0 += KV16_QC) {
+    const int nc = min(KV16_QC, nq - c0);
+    __syncthreads();  // the previous chunk's tiles and arrays are done
+    for (int j = threadIdx.x; j < nc; j += NT) {
+      const int tok = ROUTED ? a.perm[bh * N + q0 + c0 + j] : q0 + c0 + j;
+      qoff[j] = (uint32_t)tok * RB;
+      lse_s[j] = a.q_lse[bh * N + tok];
+      D_s[j] = a.q_D[bh * N + tok];
+    }
+    __syncthreads();
+    const int nfull = nc / TQ, part = nc % TQ;
+    auto issue = [&](int j, int b) {
+      if (j < nfull) dma_tile_lane<D, TQ, NW>(Qt(b), Dt(b), qg, dOg, qoff + j * TQ, dl);
+    };
+    auto step = [&](int i, int b) {
+      issue(i + 1, b ^ 1);
+      __builtin_amdgcn_sched_barrier(0);
+      tile(Qt(b), Dt(b), i * TQ, TQ, std::false_type{});
+      wait_loads();
+      __syncthreads();
+    };
+    if (nfull > 0) {
+      issue(0, 0);
+      wait_loads();
+      __syncthreads();
+      int i = 0;
+      for (; i + 1 < nfull; i += 2) {
+        step(i, 0);
+        step(i + 1, 1);
+      }
+      if (i < nfull) step(i, 0);
+    }
+    if (part > 0) {
+      dma_tile<D, false, TQ, NW>(Qt(0), Dt(0), qg, dOg, qoff + nfull * TQ, part);
+      wait_loads();
+      __syncthreads();
+      tile(Qt(0), Dt(0), nfull * TQ, part, std::true_type{});
+    }
+  }
+  // dK^T, dV^T: dims 16 db + 4 g + r of key p of group c
+#pragma unroll
+  for (int c = 0; c < NG; ++c) {
+    const int key = 16 * (NG * w + c) + p;
+    if (key >= nkeys) continue;
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) {
+      const float4 kq = make_float4(dka[c][db][0] * a.scale, dka[c][db][1] * a.scale, dka[c][db][2] * a.scale,
+                                    dka[c][db][3] * a.scale);
+      const float4 vq = make_float4(dva[c][db][0], dva[c][db][1], dva[c][db][2], dva[c][db][3]);
+      if (ROUTED) {
+        const int64_t at = ((bh * M + e) * (int64_t)K + kb0 + key) * D + 16 * db + 4 * g;
+        *reinterpret_cast<float4 *>(a.stage_k + at) = kq;
+        *reinterpret_cast<float4 *>(a.stage_v + at) = vq;
+      } else {
+        const int64_t at = (bh * M + kb0 + key) * D + 16 * db + 4 * g;
+        unsafeAtomicAdd(a.dq_lm + at, kq.x);
+        unsafeAtomicAdd(a.dq_lm + at + 1, kq.y);
+        unsafeAtomicAdd(a.dq_lm + at + 2, kq.z);
+        unsafeAtomicAdd(a.dq_lm + at + 3, kq.w);
+        unsafeAtomicAdd(a.dv_lm + at, vq.x);
+        unsafeAtomicAdd(a.dv_lm + at + 1, vq.y);
+        unsafeAtomicAdd(a.dv_lm + at + 2, vq.z);
+        unsafeAtomicAdd(a.dv_lm + at + 3, vq.w);
+      }
+    }
+  }
+}
+
 // Inverse index of the top-k sets: for each token, the (expert, position)
 // slots e * k + j with idx[e][j] = token, by a counting sort (count, scan,
 // place; the order of a token's slots is that of the atomic decrements).
@@ -1175,7 +1402,11 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
     kv.nblk = (c.k + BWD_KB - 1) / BWD_KB;
     kv.ntotal = c.M * kv.nblk;
     const unsigned nx = (unsigned)((kv.ntotal + NXCD - 1) / NXCD * NXCD);
-    hipLaunchKernelGGL((bwd_kv_kernel<T, D, true>), dim3(nx, bh), dim3(256), 0, st, kv);
+    if constexpr (sizeof(T) == 2)
+      hipLaunchKernelGGL((bwd_kv16_kernel<D, true, BWD16_GROUPS<D>>), dim3(nx, bh), dim3(256 / BWD16_GROUPS<D>), 0, st,
+                         kv);
+    else
+      hipLaunchKernelGGL((bwd_kv_kernel<T, D, true>), dim3(nx, bh), dim3(256), 0, st, kv);
     if ((err = launched("bwd_kv_kernel", st)) != hipSuccess) return err;
     const int per_head = c.M * c.k;
     const int64_t total = BH(c) * per_head;
@@ -1198,7 +1429,11 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
     kv.nblk = (c.M + BWD_KB - 1) / BWD_KB;
     kv.ntotal = kv.nblk * ((c.N + BWD_QCHUNK - 1) / BWD_QCHUNK);
     const unsigned nx = (unsigned)((kv.ntotal + NXCD - 1) / NXCD * NXCD);
-    hipLaunchKernelGGL((bwd_kv_kernel<T, D, false>), dim3(nx, bh), dim3(256), 0, st, kv);
+    if constexpr (sizeof(T) == 2)
+      hipLaunchKernelGGL((bwd_kv16_kernel<D, false, BWD16_GROUPS<D>>), dim3(nx, bh), dim3(256 / BWD16_GROUPS<D>), 0,
+                         st, kv);
+    else
+      hipLaunchKernelGGL((bwd_kv_kernel<T, D, false>), dim3(nx, bh), dim3(256), 0, st, kv);
     if ((err = launched("bwd_kv_shared_kernel", st)) != hipSuccess) return err;
     // the landmark values (Eq. landmark-value), once their gradient is complete
     const int nlb = (c.M + BWD_TQ - 1) / BWD_TQ, nch = (c.N + BWD_CHUNK - 1) / BWD_CHUNK;
