@@ -41,7 +41,8 @@ SCORE_NC = 512        # keys per score-pass chunk
 ROUTE_TQ = 64         # queries per routing tile
 # kernels priced against MFMA whatever their byte count (the attention: its
 # algorithmic bytes count every expert's k rows, most of which come from L2)
-MFMA_KERNELS = ("attend16_kernel", "attend_kernel", "bwd_attend_kernel", "bwd_landmark_kernel", "bwd_kv_kernel",
+MFMA_KERNELS = ("attend16_kernel", "attend_kernel", "bwd_attend_kernel", "bwd_landmark_kernel", "bwd_kv_landmark_kernel",
+                "bwd_kv_kernel",
                 "bwd_kv_shared_kernel")
 
 
@@ -123,8 +124,15 @@ def kernel_work(name: str, wl, plan: dict, staged: bool, s: int = 1, launched=()
     w["inv_scan_kernel"] = (8 * BH * N, 0)
     w["inv_place_kernel"] = (8 * BH * M * k + 8 * BH * N, 0)
     w["inv_gather_kernel"] = (8 * BH * M * k * d + 4 * BH * M * k + 8 * BH * N + 8 * BH * N * d, 0)
-    w["bwd_landmark_kernel"] = (2 * lmt + 4 * BH * M * d + 2 * tens + 4 * rows + 8 * BH * N * d + 4 * BH * M * d,
-                                10 * M * N * d * BH * sh)
+    if wl.dtype == "f32":
+        w["bwd_landmark_kernel"] = (2 * lmt + 4 * BH * M * d + 2 * tens + 4 * rows + 8 * BH * N * d + 4 * BH * M * d,
+                                    10 * M * N * d * BH * sh)
+    else:
+        # bf16: the landmark queries' gradient (S, dP, dQ~) and, in its own
+        # launch, the keys' (S, dP, dK, dV; each token row read and written once)
+        w["bwd_landmark_kernel"] = (2 * lmt + 2 * tens + 8 * rows + 4 * BH * M * d, 6 * M * N * d * BH * sh)
+        w["bwd_kv_landmark_kernel"] = (2 * tens + 2 * lmt + 8 * rows + 16 * BH * N * d, 8 * M * N * d * BH * sh)
+        w["lmv_prep_kernel"] = (4 * BH * M * d + 2 * lmt + 4 * rows, 0)
     w["bwd_finish_kernel"] = (12 * BH * N * d + 4 * BH * M * d * sh + 3 * tens, 0)
     w["lse_rows_kernel"] = (8 * BH * nch * M + 4 * rows, 0)
     w["attend16_kernel"] = att

@@ -98,6 +98,8 @@ struct BwdArgs {
   float *dk, *dv;          // [BH, N, d] accumulators (atomic adds)
   float *dq_lm, *dv_lm_out;  // [BH, M, d] accumulators (atomic adds)
   float *q_lse, *q_D;      // [BH, N] ATT: each query's log-sum-exp (log2 units) and dO . o (written)
+  const void *dv_lm16;     // [BH, M, d] bf16 copy of dv_lm (the DMA-tiled landmark-value pass)
+  const float *D_lm;       // [BH, M] dv_lm . v_lm (the DMA-tiled landmark-value pass)
   int N, M, topk, chunk;
   float scale;
 };
@@ -450,10 +452,11 @@ __global__ __launch_bounds__(256) void bwd_kernel(BwdArgs a) {
 // multiply by scale log2 e, as the key-owned kernel does.
 // ---------------------------------------------------------------------------
 constexpr int BWD16_TK = 32;
+constexpr int BWD16_LMV_CHUNK = 2048;  // keys per workgroup of the landmark queries' gradient
 template <int D> constexpr int BWD16_GROUPS = D == 64 ? 2 : 1;
 template <int D> constexpr size_t bwd16_tiles_lds() { return 4 * (size_t)DmaTile<D, BWD16_TK>::BYTES; }
 
-template <int D, bool SHARED, bool ROUTED, int NG>
+template <int D, bool SHARED, bool ROUTED, int NG, bool LMV = false>
 __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(4))) void bwd_att16_kernel(BwdArgs a) {
   constexpr int NW = 4 / NG;  // waves per workgroup
   constexpr int NT = 64 * NW;
@@ -470,19 +473,33 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(4))) v
   const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, g = lane >> 4, p = lane & 15;
   const int N = a.N, M = a.M, K = a.topk;
-  int e, q_begin, q_end;
-  if (!attend_queries<ROUTED>(a.tile_start, a.offsets, bh, N, M, e, q_begin, q_end)) return;  // uniform
-
-  const int nA = SHARED ? M / TK : 0, pA = SHARED ? M % TK : 0;
-  const int nB = ROUTED ? K / TK : 0, pB = ROUTED ? K % TK : 0;
+  int e = 0, q_begin, q_end, c0 = 0, nck = 0;
+  if (LMV) {
+    // landmark block lb (the queries) against key chunk ch
+    const int nlb = (M + BWD_TQ - 1) / BWD_TQ;
+    const int lb = (int)blockIdx.x % nlb, ch = (int)blockIdx.x / nlb;
+    q_begin = lb * BWD_TQ;
+    q_end = min(M, q_begin + BWD_TQ);
+    c0 = ch * a.chunk;
+    if (c0 >= N) return;  // uniform
+    nck = min(N - c0, a.chunk);
+  } else if (!attend_queries<ROUTED>(a.tile_start, a.offsets, bh, N, M, e, q_begin, q_end)) {
+    return;  // uniform
+  }
+  // LMV: the chunk's keys take the place of the routed ones
+  const int nrt = LMV ? nck : (ROUTED ? K : 0);
+  const int nA = SHARED && !LMV ? M / TK : 0, pA = SHARED && !LMV ? M % TK : 0;
+  const int nB = nrt / TK, pB = nrt % TK;
   const int nfull = nA + nB;
   const bf16_t *sh_k = (const bf16_t *)a.q_lm + bh * (int64_t)M * D;
   const bf16_t *sh_v = (const bf16_t *)a.v_lm + bh * (int64_t)M * D;
   const bf16_t *rkb = (const bf16_t *)a.k + bh * (int64_t)N * D;
   const bf16_t *rvb = (const bf16_t *)a.v + bh * (int64_t)N * D;
-  const int nsh = SHARED ? M : 0;
+  const int nsh = SHARED && !LMV ? M : 0;
   for (int i = threadIdx.x; i < nsh; i += NT) sidx[i] = (uint32_t)i * RB;
-  if (ROUTED) {
+  if (LMV) {
+    for (int i = threadIdx.x; i < nck; i += NT) sidx[i] = (uint32_t)(c0 + i) * RB;
+  } else if (ROUTED) {
     const int32_t *gidx = a.idx + (bh * M + e) * (int64_t)K;
     for (int i = threadIdx.x; i < K; i += NT) sidx[nsh + i] = (uint32_t)gidx[i] * RB;
   }
@@ -496,7 +513,10 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(4))) v
   };
 
   // this wave's groups: group c holds queries q_begin + 16 (NG w + c) + p
-  const bf16_t *qg = (const bf16_t *)a.q, *dOg = (const bf16_t *)a.dO, *og = (const bf16_t *)a.o;
+  // (LMV: landmark rows of q_lm, their upstream gradient in bf16, D given)
+  const bf16_t *qg = LMV ? (const bf16_t *)a.q_lm : (const bf16_t *)a.q;
+  const bf16_t *dOg = LMV ? (const bf16_t *)a.dv_lm16 : (const bf16_t *)a.dO, *og = (const bf16_t *)a.o;
+  const int QN = LMV ? M : N;  // rows per head of the query tensors
   int tok[NG];
   bool qvalid[NG];
   Frag<bf16_t> qf[NG][D / 32], df[NG][D / 32];
@@ -505,12 +525,20 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(4))) v
   for (int c = 0; c < NG; ++c) {
     const int qi = q_begin + 16 * (NG * w + c) + p;
     qvalid[c] = qi < q_end;
-    tok[c] = qvalid[c] ? (ROUTED ? a.perm[bh * N + qi] : qi) : 0;
+    tok[c] = qvalid[c] ? (ROUTED && !LMV ? a.perm[bh * N + qi] : qi) : 0;
     float dpart = 0.f;
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks) {
-      const int64_t at = (bh * N + tok[c]) * D + ks * 32 + g * 8;
-      if (qvalid[c]) {
+      const int64_t at = (bh * QN + tok[c]) * D + ks * 32 + g * 8;
+      if (LMV) {
+        if (qvalid[c]) {
+          qf[c][ks].load(qg + at);
+          df[c][ks].load(dOg + at);
+        } else {
+          qf[c][ks].zero();
+          df[c][ks].zero();
+        }
+      } else if (qvalid[c]) {
         qf[c][ks].load(qg + at);
         df[c][ks].load(dOg + at);
         float ov[8], dv[8];
@@ -528,6 +556,7 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(4))) v
     const float pair = __uint_as_float(x[0]) + __uint_as_float(x[1]);
     const auto y = __builtin_amdgcn_permlane32_swap(__float_as_uint(pair), __float_as_uint(pair), false, false);
     Dq[c] = __uint_as_float(y[0]) + __uint_as_float(y[1]);
+    if (LMV) Dq[c] = qvalid[c] ? a.D_lm[bh * M + tok[c]] : 0.f;
   }
   int nbusy = 0;
 #pragma unroll
@@ -636,7 +665,10 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(4))) v
       }
     });
   };
-  if (NG == 2 && nbusy == 2)
+  // (LMV: each landmark row's log-sum-exp comes from the score pass)
+  if (LMV)
+    ;
+  else if (NG == 2 && nbusy == 2)
     pass1(std::integral_constant<int, NG>{});
   else if (nbusy >= 1)
     pass1(std::integral_constant<int, 1>{});
@@ -645,6 +677,10 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(4))) v
   float lse[NG];
 #pragma unroll
   for (int c = 0; c < NG; ++c) {
+    if (LMV) {
+      lse[c] = qvalid[c] ? a.lse_lm[bh * M + tok[c]] : 0.f;
+      continue;
+    }
     const float mc = max_lane_groups(lm[c]);
     const float lc = lm[c] == -INFINITY ? 0.f : ll[c] * __builtin_amdgcn_exp2f(lm[c] - mc);
     const auto x = __builtin_amdgcn_permlane16_swap(__float_as_uint(lc), __float_as_uint(lc), false, false);
@@ -717,6 +753,18 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(4))) v
     pass2(std::integral_constant<int, 0>{});
 
   // ------------------------------------------------------------ outputs
+  if (LMV) {  // the chunk's part of the landmark queries' gradient
+#pragma unroll
+    for (int c = 0; c < NG; ++c) {
+      if (!qvalid[c]) continue;
+      float *drow = a.dq_lm + (bh * M + tok[c]) * D;
+#pragma unroll
+      for (int db = 0; db < D / 16; ++db)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) unsafeAtomicAdd(drow + db * 16 + 4 * g + r, dqa[c][db][r] * a.scale);
+    }
+    return;
+  }
 #pragma unroll
   for (int c = 0; c < NG; ++c) {
     if (!qvalid[c]) continue;
@@ -765,6 +813,9 @@ struct KvArgs {
   const void *q, *k, *v, *dO, *q_lm, *v_lm;
   const int32_t *idx, *perm, *offsets;
   const float *q_lse, *q_D;   // [BH, N]
+  const void *dv_lm16;        // LMV keys: [BH, M, d] bf16 gradient of the landmark values
+  const float *lse_lm, *D_lm; // LMV keys: [BH, M] the landmark rows' log-sum-exp and dV~ . V~
+  float *dk_acc, *dv_acc;     // LMV keys: [BH, N, d] accumulators (read, added to, written)
   float *stage_k, *stage_v;   // ROUTED: [BH, M, k, d]
   float *dq_lm, *dv_lm;       // SHARED: [BH, M, d] accumulators
   int N, M, topk, nblk;       // nblk: key blocks per expert (ROUTED) or landmark blocks (SHARED)
@@ -949,9 +1000,15 @@ __global__ __launch_bounds__(256) void bwd_kv_kernel(KvArgs a) {
 // bwd_kv_kernel puts them (staging rows, or atomic adds for the landmarks).
 // ---------------------------------------------------------------------------
 constexpr int KV16_QC = 512;  // queries per staged chunk
+// key blocks of bwd_kv16_kernel: an expert's routed keys (its queries),
+// landmark keys (a chunk of all queries), or tokens as the keys of the
+// landmark values (the landmark rows as queries; each token row is owned by
+// one block, so the sums are added to the accumulators without atomics)
+constexpr int KV_ROUTED = 0, KV_SHARED = 1, KV_LMV = 2;
 
-template <int D, bool ROUTED, int NG>
+template <int D, int KM, int NG>
 __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) void bwd_kv16_kernel(KvArgs a) {
+  constexpr bool ROUTED = KM == KV_ROUTED;
   constexpr int NW = 4 / NG;
   constexpr int NT = 64 * NW;
   constexpr int TQ = BWD16_TK;  // queries per tile
@@ -974,21 +1031,27 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) v
   const int x = ((int)blockIdx.x % NXCD) * C + (int)blockIdx.x / NXCD;
   if (x >= a.ntotal) return;  // uniform
   int e = 0, kb0, nkeys, q0, nq;
-  if (ROUTED) {
+  if (KM == KV_ROUTED) {
     e = x / a.nblk;
     kb0 = (x % a.nblk) * BWD_KB;
     nkeys = min(BWD_KB, K - kb0);
     q0 = a.offsets[bh * (M + 1) + e];
     nq = a.offsets[bh * (M + 1) + e + 1] - q0;
-  } else {
+  } else if (KM == KV_SHARED) {
     kb0 = (x % a.nblk) * BWD_KB;
     nkeys = min(BWD_KB, M - kb0);
     q0 = (x / a.nblk) * BWD_QCHUNK;
     nq = min(BWD_QCHUNK, N - q0);
+  } else {
+    kb0 = x * BWD_KB;
+    nkeys = min(BWD_KB, N - kb0);
+    q0 = 0;
+    nq = M;
   }
   // (an expert without queries still writes its staging rows: zeros)
-  const bf16_t *kbase = ROUTED ? (const bf16_t *)a.k + bh * (int64_t)N * D : (const bf16_t *)a.q_lm + bh * (int64_t)M * D;
-  const bf16_t *vbase = ROUTED ? (const bf16_t *)a.v + bh * (int64_t)N * D : (const bf16_t *)a.v_lm + bh * (int64_t)M * D;
+  const bool tok_keys = KM != KV_SHARED;  // keys are token rows of k, v
+  const bf16_t *kbase = tok_keys ? (const bf16_t *)a.k + bh * (int64_t)N * D : (const bf16_t *)a.q_lm + bh * (int64_t)M * D;
+  const bf16_t *vbase = tok_keys ? (const bf16_t *)a.v + bh * (int64_t)N * D : (const bf16_t *)a.v_lm + bh * (int64_t)M * D;
   Frag<bf16_t> kf[NG][D / 32], vf[NG][D / 32];
 #pragma unroll
   for (int c = 0; c < NG; ++c) {
@@ -1019,7 +1082,12 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) v
   Att16Addr<D> ad;
   ad.init();
   const float sl2 = a.scale * LOG2E;
-  const bf16_t *qg = (const bf16_t *)a.q + bh * (int64_t)N * D, *dOg = (const bf16_t *)a.dO + bh * (int64_t)N * D;
+  // the streamed queries: tokens (q, dO), or for LMV keys the landmark rows
+  // (q_lm and the landmark values' gradient)
+  const bf16_t *qg = KM == KV_LMV ? (const bf16_t *)a.q_lm + bh * (int64_t)M * D
+                                  : (const bf16_t *)a.q + bh * (int64_t)N * D;
+  const bf16_t *dOg = KM == KV_LMV ? (const bf16_t *)a.dv_lm16 + bh * (int64_t)M * D
+                                   : (const bf16_t *)a.dO + bh * (int64_t)N * D;
 
   // one query tile: nv valid rows at chunk position j0
   auto tile = [&](const bf16_t *Qc, const bf16_t *Dc, int j0, int nv, auto masked_c) {
@@ -1097,8 +1165,8 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) v
     for (int j = threadIdx.x; j < nc; j += NT) {
       const int tok = ROUTED ? a.perm[bh * N + q0 + c0 + j] : q0 + c0 + j;
       qoff[j] = (uint32_t)tok * RB;
-      lse_s[j] = a.q_lse[bh * N + tok];
-      D_s[j] = a.q_D[bh * N + tok];
+      lse_s[j] = KM == KV_LMV ? a.lse_lm[bh * M + tok] : a.q_lse[bh * N + tok];
+      D_s[j] = KM == KV_LMV ? a.D_lm[bh * M + tok] : a.q_D[bh * N + tok];
     }
     __syncthreads();
     const int nfull = nc / TQ, part = nc % TQ;
@@ -1140,10 +1208,18 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) v
       const float4 kq = make_float4(dka[c][db][0] * a.scale, dka[c][db][1] * a.scale, dka[c][db][2] * a.scale,
                                     dka[c][db][3] * a.scale);
       const float4 vq = make_float4(dva[c][db][0], dva[c][db][1], dva[c][db][2], dva[c][db][3]);
-      if (ROUTED) {
+      if (KM == KV_ROUTED) {
         const int64_t at = ((bh * M + e) * (int64_t)K + kb0 + key) * D + 16 * db + 4 * g;
         *reinterpret_cast<float4 *>(a.stage_k + at) = kq;
         *reinterpret_cast<float4 *>(a.stage_v + at) = vq;
+      } else if (KM == KV_LMV) {
+        const int64_t at = (bh * N + kb0 + key) * D + 16 * db + 4 * g;
+        float4 k4 = *reinterpret_cast<const float4 *>(a.dk_acc + at);
+        float4 v4 = *reinterpret_cast<const float4 *>(a.dv_acc + at);
+        k4.x += kq.x; k4.y += kq.y; k4.z += kq.z; k4.w += kq.w;
+        v4.x += vq.x; v4.y += vq.y; v4.z += vq.z; v4.w += vq.w;
+        *reinterpret_cast<float4 *>(a.dk_acc + at) = k4;
+        *reinterpret_cast<float4 *>(a.dv_acc + at) = v4;
       } else {
         const int64_t at = (bh * M + kb0 + key) * D + 16 * db + 4 * g;
         unsafeAtomicAdd(a.dq_lm + at, kq.x);
@@ -1157,6 +1233,34 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) v
       }
     }
   }
+}
+
+// The landmark values' gradient in bf16 (the MFMA operand of the DMA-tiled
+// landmark-value kernels) and each landmark row's D = dV~ . V~ (fp32), one
+// thread per row.
+template <int D>
+__global__ __launch_bounds__(256) void lmv_prep_kernel(const float *__restrict__ dv_lm, const bf16_t *__restrict__ v_lm,
+                                                       bf16_t *__restrict__ dv16, float *__restrict__ D_lm,
+                                                       int64_t rows) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= rows) return;
+  float dsum = 0.f;
+#pragma unroll
+  for (int c = 0; c < D; c += 8) {
+    const float4 f0 = *reinterpret_cast<const float4 *>(dv_lm + t * D + c);
+    const float4 f1 = *reinterpret_cast<const float4 *>(dv_lm + t * D + c + 4);
+    const float f[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+    float vv[8];
+    load16_f32(v_lm + t * D + c, vv);
+    bf16_t tt[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      dsum = __builtin_fmaf(vv[i], f[i], dsum);
+      tt[i] = from_f32<bf16_t>(f[i]);
+    }
+    *reinterpret_cast<uint4 *>(dv16 + t * D + c) = *reinterpret_cast<const uint4 *>(tt);
+  }
+  D_lm[t] = dsum;
 }
 
 // Inverse index of the top-k sets: for each token, the (expert, position)
@@ -1403,7 +1507,7 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
     kv.ntotal = c.M * kv.nblk;
     const unsigned nx = (unsigned)((kv.ntotal + NXCD - 1) / NXCD * NXCD);
     if constexpr (sizeof(T) == 2)
-      hipLaunchKernelGGL((bwd_kv16_kernel<D, true, BWD16_GROUPS<D>>), dim3(nx, bh), dim3(256 / BWD16_GROUPS<D>), 0, st,
+      hipLaunchKernelGGL((bwd_kv16_kernel<D, KV_ROUTED, BWD16_GROUPS<D>>), dim3(nx, bh), dim3(256 / BWD16_GROUPS<D>), 0, st,
                          kv);
     else
       hipLaunchKernelGGL((bwd_kv_kernel<T, D, true>), dim3(nx, bh), dim3(256), 0, st, kv);
@@ -1430,16 +1534,45 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
     kv.ntotal = kv.nblk * ((c.N + BWD_QCHUNK - 1) / BWD_QCHUNK);
     const unsigned nx = (unsigned)((kv.ntotal + NXCD - 1) / NXCD * NXCD);
     if constexpr (sizeof(T) == 2)
-      hipLaunchKernelGGL((bwd_kv16_kernel<D, false, BWD16_GROUPS<D>>), dim3(nx, bh), dim3(256 / BWD16_GROUPS<D>), 0,
+      hipLaunchKernelGGL((bwd_kv16_kernel<D, KV_SHARED, BWD16_GROUPS<D>>), dim3(nx, bh), dim3(256 / BWD16_GROUPS<D>), 0,
                          st, kv);
     else
       hipLaunchKernelGGL((bwd_kv_kernel<T, D, false>), dim3(nx, bh), dim3(256), 0, st, kv);
     if ((err = launched("bwd_kv_shared_kernel", st)) != hipSuccess) return err;
     // the landmark values (Eq. landmark-value), once their gradient is complete
     const int nlb = (c.M + BWD_TQ - 1) / BWD_TQ, nch = (c.N + BWD_CHUNK - 1) / BWD_CHUNK;
-    hipLaunchKernelGGL((bwd_kernel<T, D, BWD_LMV, true, false>), dim3((unsigned)(nlb * nch), bh), dim3(256), 0, st,
-                       a);
-    if ((err = launched("bwd_landmark_kernel", st)) != hipSuccess) return err;
+    if constexpr (sizeof(T) == 2) {
+      // bf16: the landmark queries' gradient by landmark blocks and key
+      // chunks (atomic adds per chunk), then the keys' gradient by token
+      // blocks with all landmark rows streamed (each row added once)
+      const int64_t mrows = BH(c) * c.M;
+      hipLaunchKernelGGL((lmv_prep_kernel<D>), dim3((unsigned)((mrows + 255) / 256)), dim3(256), 0, st, b.dv_lm_acc,
+                         (const bf16_t *)b.v_lm, (bf16_t *)b.dv_lm16, b.D_lm, mrows);
+      if ((err = launched("lmv_prep_kernel", st)) != hipSuccess) return err;
+      a.dv_lm16 = b.dv_lm16;
+      a.D_lm = b.D_lm;
+      constexpr int NG = BWD16_GROUPS<D>;
+      // longer key chunks than the fp32 kernel's: fewer atomic adds of the
+      // partial sums, which all chunks of a landmark block add to the same rows
+      a.chunk = BWD16_LMV_CHUNK;
+      const int nch16 = (c.N + BWD16_LMV_CHUNK - 1) / BWD16_LMV_CHUNK;
+      hipLaunchKernelGGL((bwd_att16_kernel<D, false, false, NG, true>), dim3((unsigned)(nlb * nch16), bh),
+                         dim3(256 / NG), (size_t)BWD16_LMV_CHUNK * sizeof(uint32_t), st, a);
+      if ((err = launched("bwd_landmark_kernel", st)) != hipSuccess) return err;
+      kv.dv_lm16 = b.dv_lm16;
+      kv.lse_lm = b.lse_lm;
+      kv.D_lm = b.D_lm;
+      kv.dk_acc = b.dk_acc;
+      kv.dv_acc = b.dv_acc;
+      kv.ntotal = (c.N + BWD_KB - 1) / BWD_KB;
+      const unsigned nxl = (unsigned)((kv.ntotal + NXCD - 1) / NXCD * NXCD);
+      hipLaunchKernelGGL((bwd_kv16_kernel<D, KV_LMV, NG>), dim3(nxl, bh), dim3(256 / NG), 0, st, kv);
+      if ((err = launched("bwd_kv_landmark_kernel", st)) != hipSuccess) return err;
+    } else {
+      hipLaunchKernelGGL((bwd_kernel<T, D, BWD_LMV, true, false>), dim3((unsigned)(nlb * nch), bh), dim3(256), 0,
+                         st, a);
+      if ((err = launched("bwd_landmark_kernel", st)) != hipSuccess) return err;
+    }
   }
   const int64_t rows = BH(c) * c.N;
   const int64_t threads = rows * (D / 4);

@@ -303,7 +303,7 @@ inline FwdLayout forward_layout(const mita_cfg_t &c) {
 struct BwdLayout {
   FwdLayout f;
   size_t lse_lm, dq_direct, dk_acc, dv_acc, dq_lm_acc, dv_lm_acc, q_lse, q_D, stage_k, stage_v, inv_cnt, inv_start,
-      inv_slot, total;
+      inv_slot, dv_lm16, D_lm, total;
 };
 
 inline BwdLayout backward_layout(const mita_cfg_t &c) {
@@ -330,6 +330,9 @@ inline BwdLayout backward_layout(const mita_cfg_t &c) {
   L.inv_cnt = take(c.use_routed ? bh * c.N * 4 : 0);
   L.inv_start = take(c.use_routed ? bh * (c.N + 1) * 4 : 0);
   L.inv_slot = take(c.use_routed ? bh * c.M * (size_t)c.k * 4 : 0);
+  // the landmark values' gradient in bf16 and each landmark row's dV~ . V~
+  L.dv_lm16 = take(c.use_shared ? bh * c.M * c.d * 2 : 0);
+  L.D_lm = take(c.use_shared ? bh * c.M * 4 : 0);
   L.total = off;
   return L;
 }

@@ -324,6 +324,8 @@ int backward_impl(const mita_cfg_t *c, const void *q, const void *k, const void 
   b.inv_cnt = (int32_t *)(w + BL.inv_cnt);
   b.inv_start = (int32_t *)(w + BL.inv_start);
   b.inv_slot = (int32_t *)(w + BL.inv_slot);
+  b.dv_lm16 = w + BL.dv_lm16;
+  b.D_lm = (float *)(w + BL.D_lm);
   b.dq = dq;
   b.dk = dk;
   b.dv = dv;
