@@ -815,7 +815,12 @@ struct KvArgs {
   const float *q_lse, *q_D;   // [BH, N]
   const void *dv_lm16;        // LMV keys: [BH, M, d] bf16 gradient of the landmark values
   const float *lse_lm, *D_lm; // LMV keys: [BH, M] the landmark rows' log-sum-exp and dV~ . V~
-  float *dk_acc, *dv_acc;     // LMV keys: [BH, N, d] accumulators (read, added to, written)
+  float *dk_acc, *dv_acc;     // LMV keys without the fused finish: [BH, N, d] accumulators (added to)
+  // LMV keys with the fused finish (dk_out != NULL): the routed keys' staged
+  // per-expert rows (inverse index inv_start / inv_slot, NULL without
+  // routing) are summed in, and dk, dv written in bf16
+  const int32_t *inv_start, *inv_slot;
+  void *dk_out, *dv_out;
   float *stage_k, *stage_v;   // ROUTED: [BH, M, k, d]
   float *dq_lm, *dv_lm;       // SHARED: [BH, M, d] accumulators
   int N, M, topk, nblk;       // nblk: key blocks per expert (ROUTED) or landmark blocks (SHARED)
@@ -1198,6 +1203,56 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) v
       tile(Qt(0), Dt(0), nfull * TQ, part, std::true_type{});
     }
   }
+  // LMV keys with the fused finish: each key's staged per-expert rows (the
+  // first FS slots loaded together: the index, then every row's dims) are
+  // added to the landmark-value sums, and dk, dv written in bf16
+  if (KM == KV_LMV && a.dk_out) {
+    constexpr int FS = 8;
+    const int64_t per_head = (int64_t)M * K;
+#pragma unroll
+    for (int c = 0; c < NG; ++c) {
+      const int key = 16 * (NG * w + c) + p;
+      if (key >= nkeys) continue;
+      float4 k4[D / 16], v4[D / 16];
+#pragma unroll
+      for (int db = 0; db < D / 16; ++db) {
+        k4[db] = make_float4(dka[c][db][0] * a.scale, dka[c][db][1] * a.scale, dka[c][db][2] * a.scale,
+                             dka[c][db][3] * a.scale);
+        v4[db] = make_float4(dva[c][db][0], dva[c][db][1], dva[c][db][2], dva[c][db][3]);
+      }
+      if (a.inv_start) {
+        const int s0 = a.inv_start[bh * (N + 1) + kb0 + key], s1 = a.inv_start[bh * (N + 1) + kb0 + key + 1];
+        const int n = s1 - s0;
+        int64_t src[FS];
+#pragma unroll
+        for (int i = 0; i < FS; ++i) src[i] = i < n ? (bh * per_head + a.inv_slot[bh * per_head + s0 + i]) * D : 0;
+        auto add = [&](int64_t sr) {
+#pragma unroll
+          for (int db = 0; db < D / 16; ++db) {
+            const float4 yk = *reinterpret_cast<const float4 *>(a.stage_k + sr + 16 * db + 4 * g);
+            const float4 yv = *reinterpret_cast<const float4 *>(a.stage_v + sr + 16 * db + 4 * g);
+            k4[db].x += yk.x; k4[db].y += yk.y; k4[db].z += yk.z; k4[db].w += yk.w;
+            v4[db].x += yv.x; v4[db].y += yv.y; v4[db].z += yv.z; v4[db].w += yv.w;
+          }
+        };
+#pragma unroll
+        for (int i = 0; i < FS; ++i)
+          if (i < n) add(src[i]);
+        for (int i = FS; i < n; ++i) add((bh * per_head + a.inv_slot[bh * per_head + s0 + i]) * D);
+      }
+      const int64_t at = (bh * N + kb0 + key) * D + 4 * g;
+#pragma unroll
+      for (int db = 0; db < D / 16; ++db) {
+        const bf16_t kb4[4] = {from_f32<bf16_t>(k4[db].x), from_f32<bf16_t>(k4[db].y), from_f32<bf16_t>(k4[db].z),
+                               from_f32<bf16_t>(k4[db].w)};
+        const bf16_t vb4[4] = {from_f32<bf16_t>(v4[db].x), from_f32<bf16_t>(v4[db].y), from_f32<bf16_t>(v4[db].z),
+                               from_f32<bf16_t>(v4[db].w)};
+        *reinterpret_cast<uint2 *>((bf16_t *)a.dk_out + at + 16 * db) = *reinterpret_cast<const uint2 *>(kb4);
+        *reinterpret_cast<uint2 *>((bf16_t *)a.dv_out + at + 16 * db) = *reinterpret_cast<const uint2 *>(vb4);
+      }
+    }
+    return;
+  }
   // dK^T, dV^T: dims 16 db + 4 g + r of key p of group c
 #pragma unroll
   for (int c = 0; c < NG; ++c) {
@@ -1214,10 +1269,11 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) v
         *reinterpret_cast<float4 *>(a.stage_v + at) = vq;
       } else if (KM == KV_LMV) {
         const int64_t at = (bh * N + kb0 + key) * D + 16 * db + 4 * g;
-        float4 k4 = *reinterpret_cast<const float4 *>(a.dk_acc + at);
-        float4 v4 = *reinterpret_cast<const float4 *>(a.dv_acc + at);
-        k4.x += kq.x; k4.y += kq.y; k4.z += kq.z; k4.w += kq.w;
-        v4.x += vq.x; v4.y += vq.y; v4.z += vq.z; v4.w += vq.w;
+        float4 k4 = kq, v4 = vq;
+        const float4 ak = *reinterpret_cast<const float4 *>(a.dk_acc + at);
+        const float4 av = *reinterpret_cast<const float4 *>(a.dv_acc + at);
+        k4.x += ak.x; k4.y += ak.y; k4.z += ak.z; k4.w += ak.w;
+        v4.x += av.x; v4.y += av.y; v4.z += av.z; v4.w += av.w;
         *reinterpret_cast<float4 *>(a.dk_acc + at) = k4;
         *reinterpret_cast<float4 *>(a.dv_acc + at) = v4;
       } else {
@@ -1364,7 +1420,7 @@ __global__ __launch_bounds__(256) void lse_rows_kernel(const float2 *__restrict_
 // dq_lm_i / |W_i|), dk, dv from their accumulators. One thread per 4 dims.
 // Along each axis a position lies in at most two adaptive windows, among
 // floor(pos * g / G) - 1 .. + 1.
-template <typename T, int D, bool POOL>
+template <typename T, int D, bool POOL, bool KV = true>
 __global__ __launch_bounds__(256) void bwd_finish_kernel(const float *__restrict__ dq_direct,
                                                          const float *__restrict__ dq_lm,
                                                          const float *__restrict__ dk_acc,
@@ -1398,8 +1454,6 @@ __global__ __launch_bounds__(256) void bwd_finish_kernel(const float *__restrict
       }
     }
   }
-  const float4 yk = *reinterpret_cast<const float4 *>(dk_acc + at);
-  const float4 yv = *reinterpret_cast<const float4 *>(dv_acc + at);
   auto put = [&](T *dst, float4 f) {
     T vals[4] = {from_f32<T>(f.x), from_f32<T>(f.y), from_f32<T>(f.z), from_f32<T>(f.w)};
     if (sizeof(T) == 2)
@@ -1408,8 +1462,10 @@ __global__ __launch_bounds__(256) void bwd_finish_kernel(const float *__restrict
       *reinterpret_cast<uint4 *>(dst + at) = *reinterpret_cast<const uint4 *>(vals);
   };
   put(dq, x);
-  put(dk, yk);
-  put(dv, yv);
+  if (KV) {  // (else the landmark-value key pass wrote dk and dv)
+    put(dk, *reinterpret_cast<const float4 *>(dk_acc + at));
+    put(dv, *reinterpret_cast<const float4 *>(dv_acc + at));
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1501,6 +1557,10 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
   kv.M = c.M;
   kv.topk = c.k;
   kv.scale = eff_scale(c);
+  // bf16 with the landmark values: their key pass owns every token row, so it
+  // also sums the routed keys' staged rows and writes dk, dv (no gather pass,
+  // no fp32 accumulators of the keys)
+  const bool fused_finish = sizeof(T) == 2 && c.use_shared;
   if (c.use_routed) {
     // routed keys: per-expert sums staged, then summed per token
     kv.nblk = (c.k + BWD_KB - 1) / BWD_KB;
@@ -1523,10 +1583,12 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
     hipLaunchKernelGGL(inv_place_kernel, dim3(gi), dim3(256), 0, st, b.idx, b.inv_cnt, b.inv_start, b.inv_slot, total,
                        per_head, c.N);
     if ((err = launched("inv_place_kernel", st)) != hipSuccess) return err;
-    const int64_t rows = BH(c) * c.N;
-    hipLaunchKernelGGL((inv_gather_kernel<D>), dim3((unsigned)((rows * (D / 4) + 255) / 256)), dim3(256), 0, st,
-                       b.stage_k, b.stage_v, b.inv_start, b.inv_slot, b.dk_acc, b.dv_acc, rows, c.N, per_head);
-    if ((err = launched("inv_gather_kernel", st)) != hipSuccess) return err;
+    if (!fused_finish) {  // (else the landmark-value key pass sums the staged rows)
+      const int64_t rows = BH(c) * c.N;
+      hipLaunchKernelGGL((inv_gather_kernel<D>), dim3((unsigned)((rows * (D / 4) + 255) / 256)), dim3(256), 0, st,
+                         b.stage_k, b.stage_v, b.inv_start, b.inv_slot, b.dk_acc, b.dv_acc, rows, c.N, per_head);
+      if ((err = launched("inv_gather_kernel", st)) != hipSuccess) return err;
+    }
   }
   if (c.use_shared) {
     // shared keys (the landmarks): atomic adds per landmark block and query chunk
@@ -1564,6 +1626,10 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
       kv.D_lm = b.D_lm;
       kv.dk_acc = b.dk_acc;
       kv.dv_acc = b.dv_acc;
+      kv.inv_start = c.use_routed ? b.inv_start : nullptr;
+      kv.inv_slot = c.use_routed ? b.inv_slot : nullptr;
+      kv.dk_out = b.dk;
+      kv.dv_out = b.dv;
       kv.ntotal = (c.N + BWD_KB - 1) / BWD_KB;
       const unsigned nxl = (unsigned)((kv.ntotal + NXCD - 1) / NXCD * NXCD);
       hipLaunchKernelGGL((bwd_kv16_kernel<D, KV_LMV, NG>), dim3(nxl, bh), dim3(256 / NG), 0, st, kv);
@@ -1577,7 +1643,11 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
   const int64_t rows = BH(c) * c.N;
   const int64_t threads = rows * (D / 4);
   const dim3 fg((unsigned)((threads + 255) / 256));
-  if (c.use_shared)
+  if (fused_finish)
+    hipLaunchKernelGGL((bwd_finish_kernel<T, D, true, false>), fg, dim3(256), 0, st, b.dq_direct, b.dq_lm_acc,
+                       b.dk_acc, b.dv_acc, (T *)b.dq, (T *)b.dk, (T *)b.dv, rows, c.N, c.M, c.grid_h, c.grid_w,
+                       c.lm_h, c.lm_w);
+  else if (c.use_shared)
     hipLaunchKernelGGL((bwd_finish_kernel<T, D, true>), fg, dim3(256), 0, st, b.dq_direct, b.dq_lm_acc, b.dk_acc,
                        b.dv_acc, (T *)b.dq, (T *)b.dk, (T *)b.dv, rows, c.N, c.M, c.grid_h, c.grid_w, c.lm_h, c.lm_w);
   else
