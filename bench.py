@@ -131,7 +131,10 @@ def kernel_work(name: str, wl, plan: dict, staged: bool, s: int = 1, launched=()
         # bf16: the landmark queries' gradient (S, dP, dQ~) and, in its own
         # launch, the keys' (S, dP, dK, dV; each token row read and written once)
         w["bwd_landmark_kernel"] = (2 * lmt + 2 * tens + 8 * rows + 4 * BH * M * d, 6 * M * N * d * BH * sh)
-        w["bwd_kv_landmark_kernel"] = (2 * tens + 2 * lmt + 8 * rows + 16 * BH * N * d, 8 * M * N * d * BH * sh)
+        # (with the routed keys' staged rows summed in and dk, dv written)
+        w["bwd_kv_landmark_kernel"] = (2 * tens + 2 * lmt + 8 * rows
+                                       + (8 * BH * M * k * d + 4 * BH * M * k + 4 * BH * N) * rt + 2 * tens,
+                                       8 * M * N * d * BH * sh)
         w["lmv_prep_kernel"] = (4 * BH * M * d + 2 * lmt + 4 * rows, 0)
     w["bwd_finish_kernel"] = (12 * BH * N * d + 4 * BH * M * d * sh + 3 * tens, 0)
     w["lse_rows_kernel"] = (8 * BH * nch * M + 4 * rows, 0)

@@ -22,6 +22,8 @@ hipError_t launch_pool(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *
 
 // Set n int32 entries to 0.
 hipError_t launch_zero(int32_t *p, int64_t n, hipStream_t st);
+// The same for two arrays in one launch (either may be NULL or empty).
+hipError_t launch_zero2(int32_t *p, int64_t n, int32_t *p2, int64_t n2, hipStream_t st);
 
 // Buffers of the top-k selection fused with the score pass (rows = BH*M).
 struct SelectBufs {

@@ -172,8 +172,9 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
   int32_t *zero_counts = c->use_routed && !multi ? counts : nullptr;
   int32_t *zero_cursor = sel_in_route ? tile_base : nullptr;
   if (q_lm_in) {
-    TRY(hip_status(launch_zero(zero_counts, zero_counts ? BH(*c) * c->M : 0, st), "landmarks"));
-    TRY(hip_status(launch_zero(zero_cursor, zero_cursor ? BH(*c) * c->M : 0, st), "landmarks"));
+    TRY(hip_status(launch_zero2(zero_counts, zero_counts ? BH(*c) * c->M : 0, zero_cursor,
+                                zero_cursor ? BH(*c) * c->M : 0, st),
+                   "landmarks"));
   } else {
     TRY(hip_status(launch_pool(*c, q, q_lm_ws, zero_counts, zero_cursor, st), "landmarks"));
   }
@@ -293,11 +294,10 @@ int backward_impl(const mita_cfg_t *c, const void *q, const void *k, const void 
   rec.stage = 5;
   const int64_t nd = BH(*c) * c->N * c->d, md = BH(*c) * c->M * c->d;
   if (!c->use_routed) {  // with routing, the routed keys' gather writes dk_acc and dv_acc first
-    TRY(hip_status(launch_zero((int32_t *)(w + BL.dk_acc), nd, st), "backward"));
-    TRY(hip_status(launch_zero((int32_t *)(w + BL.dv_acc), nd, st), "backward"));
+    TRY(hip_status(launch_zero2((int32_t *)(w + BL.dk_acc), nd, (int32_t *)(w + BL.dv_acc), nd, st), "backward"));
   }
-  TRY(hip_status(launch_zero((int32_t *)(w + BL.dq_lm_acc), md, st), "backward"));
-  TRY(hip_status(launch_zero((int32_t *)(w + BL.dv_lm_acc), md, st), "backward"));
+  TRY(hip_status(launch_zero2((int32_t *)(w + BL.dq_lm_acc), md, (int32_t *)(w + BL.dv_lm_acc), md, st),
+                 "backward"));
   BwdBufs b{};
   b.q = q;
   b.k = k;

@@ -198,14 +198,27 @@ hipError_t launch_select_landmarks(const mita_cfg_t &c, const void *q, const int
                    : select_landmarks_t<bf16_t, 128>(c, q, sel, q_lm, st);
 }
 
-__global__ __launch_bounds__(256) void zero_kernel(int32_t *__restrict__ p, int64_t n) {
+// Zeroes p[0, n) and (when p2 is given) p2[0, n2): one launch for both.
+__global__ __launch_bounds__(256) void zero_kernel(int32_t *__restrict__ p, int64_t n, int32_t *__restrict__ p2,
+                                                   int64_t n2) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i < n) p[i] = 0;
+  if (p2 && i < n2) p2[i] = 0;
 }
 
-hipError_t launch_zero(int32_t *p, int64_t n, hipStream_t st) {
-  if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(zero_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p, n);
+hipError_t launch_zero(int32_t *p, int64_t n, hipStream_t st) { return launch_zero2(p, n, nullptr, 0, st); }
+
+hipError_t launch_zero2(int32_t *p, int64_t n, int32_t *p2, int64_t n2, hipStream_t st) {
+  if (!p || n <= 0) {  // the second array alone, or nothing
+    p = p2;
+    n = n2;
+    p2 = nullptr;
+    n2 = 0;
+  }
+  if (!p || n <= 0) return hipSuccess;
+  if (!p2) n2 = 0;
+  const int64_t m = n > n2 ? n : n2;
+  hipLaunchKernelGGL(zero_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, st, p, n, p2, n2);
   return launched("zero_kernel", st);
 }
 
