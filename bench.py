@@ -136,7 +136,10 @@ def kernel_work(name: str, wl, plan: dict, staged: bool, s: int = 1, launched=()
                                        + (8 * BH * M * k * d + 4 * BH * M * k + 4 * BH * N) * rt + 2 * tens,
                                        8 * M * N * d * BH * sh)
         w["lmv_prep_kernel"] = (4 * BH * M * d + 2 * lmt + 4 * rows, 0)
-    w["bwd_finish_kernel"] = (12 * BH * N * d + 4 * BH * M * d * sh + 3 * tens, 0)
+    # (bf16 with the landmark values: dk, dv come from the landmark-value
+    # key pass, the finish forms dq only)
+    w["bwd_finish_kernel"] = ((4 * BH * N * d + 4 * BH * M * d + tens, 0) if "bwd_kv_landmark_kernel" in launched
+                              else (12 * BH * N * d + 4 * BH * M * d * sh + 3 * tens, 0))
     w["lse_rows_kernel"] = (8 * BH * nch * M + 4 * rows, 0)
     w["attend16_kernel"] = att
     w["attend_kernel"] = att

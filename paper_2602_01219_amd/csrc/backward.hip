@@ -1437,14 +1437,19 @@ __global__ __launch_bounds__(256) void bwd_finish_kernel(const float *__restrict
   const int64_t at = row * D + 4 * c;
   float4 x = *reinterpret_cast<const float4 *>(dq_direct + at);
   if (POOL) {
-    const int pr = tok / gw, pc = tok % gw;
-    const int ar = (int)((int64_t)pr * lh / gh), ac = (int)((int64_t)pc * lw / gw);
+    // 32-bit index arithmetic: positions stay below 2^16 (N <= 65536) and
+    // window counts at most 1024 (M <= 1024), so every product below is
+    // under 2^27
+    const uint32_t pr = (uint32_t)tok / (uint32_t)gw, pc = (uint32_t)tok % (uint32_t)gw;
+    const int ar = (int)(pr * (uint32_t)lh / (uint32_t)gh), ac = (int)(pc * (uint32_t)lw / (uint32_t)gw);
     for (int a = max(0, ar - 1); a <= min(lh - 1, ar + 1); ++a) {
-      const int r0 = (int)((int64_t)a * gh / lh), r1 = (int)(((int64_t)(a + 1) * gh + lh - 1) / lh);
-      if (pr < r0 || pr >= r1) continue;
+      const int r0 = (int)((uint32_t)a * (uint32_t)gh / (uint32_t)lh);
+      const int r1 = (int)(((uint32_t)(a + 1) * (uint32_t)gh + (uint32_t)lh - 1u) / (uint32_t)lh);
+      if ((int)pr < r0 || (int)pr >= r1) continue;
       for (int b = max(0, ac - 1); b <= min(lw - 1, ac + 1); ++b) {
-        const int s0 = (int)((int64_t)b * gw / lw), s1 = (int)(((int64_t)(b + 1) * gw + lw - 1) / lw);
-        if (pc < s0 || pc >= s1) continue;
+        const int s0 = (int)((uint32_t)b * (uint32_t)gw / (uint32_t)lw);
+        const int s1 = (int)(((uint32_t)(b + 1) * (uint32_t)gw + (uint32_t)lw - 1u) / (uint32_t)lw);
+        if ((int)pc < s0 || (int)pc >= s1) continue;
         const float inv = 1.f / (float)((r1 - r0) * (s1 - s0));
         const float4 y = *reinterpret_cast<const float4 *>(dq_lm + (bh * M + a * lw + b) * D + 4 * c);
         x.x += y.x * inv;
