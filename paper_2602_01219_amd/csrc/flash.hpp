@@ -385,7 +385,7 @@ __device__ __forceinline__ void dma_tile_lane(bf16_t *Kl, bf16_t *Vl, const bf16
 template <int D> struct Att16 {
   f32x4 o[D / 16];  // O^T: dims 16 db + 4 g + r of query p
   f32x4 nm;         // -m, splat
-  float l;          // this lane's part of the weight sum
+  f32x4 l;          // the weight sum of query p (an all-ones MFMA row block; every element)
 };
 
 // Per-lane LDS byte offsets within one tile buffer, fixed for every tile:
@@ -461,13 +461,9 @@ __device__ __forceinline__ void att16_pv(Att16<D> (&st)[NG], const f32x4 (&acc)[
         pv[4 * kb + r] = x;
       }
     b[c].from_f32(pv);
-    // the sum of the rounded weights, two at a time (a bf16 pair of ones as
-    // the other operand)
-    const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3f803f80u);
-    st[c].l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b[c].v.x), ones, st[c].l, false);
-    st[c].l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b[c].v.y), ones, st[c].l, false);
-    st[c].l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b[c].v.z), ones, st[c].l, false);
-    st[c].l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, b[c].v.w), ones, st[c].l, false);
+    // the sum of the rounded weights: an all-ones A operand against the same
+    // P^T (every row of the result holds the column sum)
+    st[c].l = mma(ones_frag<bf16_t>(), b[c], st[c].l);
   }
   const char *vbase = reinterpret_cast<const char *>(Vl);
 #pragma unroll
@@ -507,7 +503,7 @@ __device__ __forceinline__ void att16_first(Att16<D> (&st)[NG], const bf16_t *__
 #pragma unroll
     for (int i = 0; i < D / 16; ++i) st[c].o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     st[c].nm = f32x4{0.f, 0.f, 0.f, 0.f};
-    st[c].l = 0.f;
+    st[c].l = f32x4{0.f, 0.f, 0.f, 0.f};
   }
   f32x4 acc[NG][2];
   att16_scores<D, NGB>(acc, st, Kl, ad, qf);
@@ -571,7 +567,7 @@ __device__ __forceinline__ void att16_plain(Att16<D> (&st)[NG], const bf16_t *__
 // and'ed over the four lane groups of its column (the same answer in every
 // lane of the column).
 template <int D> __device__ __forceinline__ bool att16_finite(const Att16<D> &st) {
-  bool ok = __builtin_isfinite(st.l);
+  bool ok = __builtin_isfinite(st.l[0]);
 #pragma unroll
   for (int i = 0; i < D / 16; ++i)
 #pragma unroll
@@ -586,12 +582,7 @@ template <int D> __device__ __forceinline__ bool att16_finite(const Att16<D> &st
 // The query's weight sum: the four lane groups of its column added in a
 // fixed order (pairs (0, 1) and (2, 3), then both pairs), the same in every
 // lane of the column.
-template <int D> __device__ __forceinline__ float att16_sum(const Att16<D> &st) {
-  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(st.l), __float_as_uint(st.l), false, false);
-  const float pair = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(pair), __float_as_uint(pair), false, false);
-  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
-}
+template <int D> __device__ __forceinline__ float att16_sum(const Att16<D> &st) { return st.l[0]; }
 
 // Register-staged copy of one 64-row K/V tile (software pipelining: the
 // global loads of the next tile are issued before the current tile is
