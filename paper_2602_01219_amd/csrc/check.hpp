@@ -62,11 +62,10 @@ inline float eff_scale(const mita_cfg_t &c) { return c.scale != 0.f ? c.scale : 
 //  - The list is longer than cap only if fewer than r samples lie among the
 //    row's first cap tokens: P = P(X < r), K = cap. cap is the smallest power
 //    of two in [1024, SEL_CAP] (or N) with P <= SEL_EPS.
-// Both bounds are for the exact r-th sample; the pivot is the lower edge of
-// the 2^-7-relative bin holding it, which adds the few tokens inside that bin
-// to the list (inside the cap's margin). When the sample is the whole row
-// (N <= SEL_NS) the rank is k and the list cannot miss. A configuration with
-// no rank or cap meeting the bounds is not selected in the score pass.
+// Both bounds are for the exact r-th sample, which is the pivot. When the
+// sample is the whole row (N <= SEL_NS) the rank is k and the list cannot
+// miss. A configuration with no rank or cap meeting the bounds is not
+// selected in the score pass.
 // ---------------------------------------------------------------------------
 inline double log_choose(double n, double x) { return std::lgamma(n + 1.0) - std::lgamma(x + 1.0) - std::lgamma(n - x + 1.0); }
 

@@ -53,18 +53,52 @@ __device__ __forceinline__ int wave_find_bin(const uint32_t *hist, uint32_t need
 // ---------------------------------------------------------------------------
 // Pivot of one landmark row from its ns (<= SEL_NS) sampled keys, held by one
 // wave: lane l holds keys 4 l + 256 i + (0..3) in v[4 i .. 4 i + 3], 0 marking
-// a slot past ns (no score has key 0, so it lies below every range). Radix
-// rounds over a 256-bin LDS histogram of the current key range (bins span
-// (hi - lo + 1) / 256 keys, so each round shrinks the range by 2^8) narrow
-// down on the r-th largest sample; after two rounds the lower edge of the bin
-// holding it is taken. That edge is at most the r-th largest sample, so at
-// least r samples are >= pivot, and its bin spans at most 2^16 keys (a
-// relative step of 2^-7 within one binade), which lists only a few more
-// tokens than the exact sample statistic would.
+// a slot past ns (no score has key 0). The pivot is the exact r-th largest
+// sampled key, found in two steps:
+//  1. a 256-bin LDS histogram over the VALUE range [fmin, fmax] of the row's
+//     samples (bin = floor((x - fmin) * 255.5 / (fmax - fmin)), a
+//     non-decreasing function of the key, so every key in a higher bin is
+//     larger than every key in a lower one) gives the bin holding the r-th
+//     largest and the number of samples above it. Linear bins keep the
+//     counts per bin small for bell-shaped scores (bins by key bits would put
+//     a third of the samples into the one bin of a binade, and its LDS
+//     atomics would serialise);
+//  2. that bin's keys (at most 64 of them) are compacted into one register
+//     per lane and an MSB-first bisection over the 32 key bits, counting by
+//     ballots, finds the exact rank among them.
+// Rows whose samples span a non-finite range or crowd more than 64 into the
+// bin (clustered scores) take the bisection over all samples instead.
+// Uses words 0..383 of the LDS row at `lds`.
 // ---------------------------------------------------------------------------
 constexpr int PIVOT_PER = SEL_NS / 64;
 
-__device__ __forceinline__ uint32_t pivot_of(const uint32_t (&v)[PIVOT_PER], uint32_t *hist, int r) {
+// need-th largest of the keys x, one per lane (0 = none); 1 <= need <= count
+// of nonzero keys. Bit b of the result is set iff at least `need` keys reach
+// the result's higher bits with b set.
+__device__ __forceinline__ uint32_t wave_kth_key(uint32_t x, uint32_t need) {
+  uint32_t t = 0;
+#pragma unroll
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t c = t | (1u << bit);
+    if ((uint32_t)__popcll(__ballot(x >= c)) >= need) t = c;
+  }
+  return t;
+}
+// The same over P keys per lane.
+template <int P>
+__device__ __forceinline__ uint32_t wave_kth_key(const uint32_t (&x)[P], uint32_t need) {
+  uint32_t t = 0;
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t c = t | (1u << bit);
+    uint32_t n = 0;
+#pragma unroll
+    for (int i = 0; i < P; ++i) n += (uint32_t)__popcll(__ballot(x[i] >= c));
+    if (n >= need) t = c;
+  }
+  return t;
+}
+
+__device__ __forceinline__ uint32_t pivot_of(const uint32_t (&v)[PIVOT_PER], uint32_t *lds, int r) {
   const int lane = threadIdx.x & 63;
   uint32_t mn = 0xffffffffu, mx = 0u;
 #pragma unroll
@@ -72,25 +106,35 @@ __device__ __forceinline__ uint32_t pivot_of(const uint32_t (&v)[PIVOT_PER], uin
     if (v[i]) mn = min(mn, v[i]);
     mx = max(mx, v[i]);
   }
-  uint32_t lo = wave_min_u32(mn), hi = wave_max_u32(mx);
-  uint32_t need = (uint32_t)r;
-  for (int round = 0; round < 2 && lo < hi; ++round) {
-    const uint32_t span = hi - lo;
-    const int bits = 32 - __clz((int)span);
-    const int shift = bits > 8 ? bits - 8 : 0;
+  const uint32_t kmin = wave_min_u32(mn), kmax = wave_max_u32(mx);
+  if (kmin == kmax) return kmin;  // all samples equal
+  const float fmin = key_to_float(kmin), span = key_to_float(kmax) - fmin;
+  const float inv = 255.5f / span;
+  if (!(span < INFINITY) || !(inv < INFINITY)) return wave_kth_key(v, (uint32_t)r);
+  // (x - fmin) <= span after rounding, so (x - fmin) * inv < 256: bins 0..255;
+  // empty slots go to words 256 + lane (distinct, never read as counts)
+  uint32_t bin[PIVOT_PER];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) hist[lane + 64 * q] = 0u;
+  for (int q = 0; q < 4; ++q) lds[lane + 64 * q] = 0u;
 #pragma unroll
-    for (int i = 0; i < PIVOT_PER; ++i)
-      if (v[i] >= lo && v[i] <= hi) atomicAdd(hist + ((v[i] - lo) >> shift), 1u);
-    uint32_t above;
-    const int b = wave_find_bin(hist, need, &above);
-    need -= above;
-    lo += (uint32_t)b << shift;
-    const uint32_t width = (1u << shift) - 1u;
-    if (hi - lo > width) hi = lo + width;
+  for (int i = 0; i < PIVOT_PER; ++i) {
+    const uint32_t b = min((uint32_t)((key_to_float(v[i]) - fmin) * inv), 255u);
+    bin[i] = v[i] ? b : 256u + (uint32_t)lane;
+    atomicAdd(lds + bin[i], 1u);
   }
-  return lo;
+  uint32_t above;
+  const uint32_t b = (uint32_t)wave_find_bin(lds, (uint32_t)r, &above);
+  const uint32_t cnt = lds[b];
+  if (cnt > 64u) return wave_kth_key(v, (uint32_t)r);
+  uint32_t *slot = lds + 320;
+  uint32_t base = 0;
+#pragma unroll
+  for (int i = 0; i < PIVOT_PER; ++i) {
+    const uint64_t m = __ballot(bin[i] == b);
+    if (bin[i] == b) slot[base + lanes_below(m)] = v[i];
+    base += (uint32_t)__popcll(m);
+  }
+  return wave_kth_key((uint32_t)lane < cnt ? slot[lane] : 0u, (uint32_t)r - above);
 }
 
 // ---------------------------------------------------------------------------
@@ -100,8 +144,8 @@ __device__ __forceinline__ uint32_t pivot_of(const uint32_t (&v)[PIVOT_PER], uin
 // the A fragments loaded straight from the sampled key rows (tile arithmetic
 // as in the score pass, so the same values), keys = score_key(fl(dot) * scale)
 // into LDS; then wave w takes the pivots of rows 16/NW w .. 16/NW (w + 1) - 1,
-// its histogram in the first 256 words of its own row's keys once they are in
-// registers (the wave's LDS accesses are in order). Workgroup (0, 0) also
+// its histogram and compaction slots in the first 384 words of its own row's
+// keys once they are in registers (the wave's LDS accesses are in order). Workgroup (0, 0) also
 // zeroes the fallback counter.
 // ---------------------------------------------------------------------------
 constexpr int SP_PITCH = SEL_NS + 4;  // keys per LDS row: rows start 4 banks apart

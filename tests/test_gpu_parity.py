@@ -544,6 +544,26 @@ def test_fused_selection_unrepresentative_sample_falls_back(shape):
     _fallback_case(K, cfg, q, v, expect_fb=cfg.M if shape == "bf16_d64_n16384" else None)
 
 
+@pytest.mark.parametrize("shape", list(FALLBACK_SHAPES))
+def test_fused_selection_clustered_sample(shape):
+    """Head 0's keys all one vector u, except 8 sampled positions at 2u and 8
+    at -u: each row's samples take three values, all but 16 of them equal,
+    so the pivot's value histogram puts the rank's bin far above 64 samples
+    and the pivot is found by bisection over every sample. It is the shared
+    score (the rank exceeds 8 here), so nearly every token is listed, beyond
+    the cap: head 0's rows fall back, and the sets are still exact."""
+    inp, cfg, (q, k, v) = _fallback_inputs(shape)
+    assert mita.select_plan(cfg)["rank"] > 8 and mita.select_plan(cfg)["cap"] < cfg.N - 16
+    ns = min(cfg.N, SELECT_SAMPLE)
+    pos = torch.from_numpy(((2 * np.arange(ns) + 1) * cfg.N) // (2 * ns)).cuda()
+    K = k.clone()
+    u = k[0, 0, 0].clone()
+    K[0, 0] = u
+    K[0, 0, pos[:8]] = 2 * u
+    K[0, 0, pos[8:16]] = -u
+    _fallback_case(K, cfg, q, v, expect_fb=cfg.M)
+
+
 def test_fused_selection_exact_ties_within_the_list():
     """N = 1024 (the sample is the whole row, a list holds it all) with
     all-zero keys: every score ties, every token is listed and the selection
