@@ -141,6 +141,7 @@ def kernel_work(name: str, wl, plan: dict, staged: bool, s: int = 1, launched=()
     w["bwd_finish_kernel"] = ((4 * BH * N * d + 4 * BH * M * d + tens, 0) if "bwd_kv_landmark_kernel" in launched
                               else (12 * BH * N * d + 4 * BH * M * d * sh + 3 * tens, 0))
     w["lse_rows_kernel"] = (8 * BH * nch * M + 4 * rows, 0)
+    w["scores16_kernel"] = w["scores_kernel"]
     w["attend16_kernel"] = att
     w["attend_kernel"] = att
     return w.get(name, (0, 0))

@@ -43,7 +43,7 @@ __device__ __forceinline__ void finalize_row(FinalizeLds<T, D, CAP, MERGE> &sh, 
                                              int32_t *__restrict__ idx, uint32_t *__restrict__ fail_cnt,
                                              int32_t *__restrict__ fail_list, int k, int cap, int nch,
                                              const float2 *__restrict__ part_ml, const float *__restrict__ part_o,
-                                             T *__restrict__ v_lm, int M) {
+                                             T *__restrict__ v_lm, int M, float scale) {
   auto &red = sh.red;
   auto &lst = sh.lst;
   auto &pre = sh.pre;
@@ -82,7 +82,8 @@ __device__ __forceinline__ void finalize_row(FinalizeLds<T, D, CAP, MERGE> &sh, 
   const int L = (int)total;
   uint64_t lo = ~0ull, hi = 0ull;
   auto put = [&](uint2 e, uint32_t at) {
-    const uint2 x = make_uint2(score_key(__uint_as_float(e.x)), e.y);  // listed as float bits
+    // listed as the bits of the unscaled dot: the score is fl(dot * scale)
+    const uint2 x = make_uint2(score_key(__uint_as_float(e.x) * scale), e.y);
     lst[at] = x;
     const uint64_t c = composite(x);
     lo = c < lo ? c : lo;

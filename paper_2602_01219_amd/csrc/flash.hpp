@@ -291,6 +291,8 @@ __device__ __forceinline__ void half_tile_attend(Online2<D> &st, const T *__rest
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int swz(int r) { return (r & 6) | ((r >> 3) & 1); }
 
+constexpr int TK32 = 32;  // rows of a DMA-staged tile
+
 template <int D, int ROWS = TK, int NW = 4> struct DmaTile {
   static constexpr int CPR = D / 8;          // 16-byte chunks per row
   static constexpr int RPI = 64 / CPR;       // rows per wave instruction

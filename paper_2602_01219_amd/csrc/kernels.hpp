@@ -29,7 +29,7 @@ hipError_t launch_zero2(int32_t *p, int64_t n, int32_t *p2, int64_t n2, hipStrea
 struct SelectBufs {
   uint32_t *plo;        // [rows] pivot keys
   uint32_t *ccnt;       // [rows, chunks] candidates listed per key chunk
-  uint2 *cand;          // [rows, chunks, SCORE_NC] (score bits, token index) lists
+  uint2 *cand;          // [rows, chunks, SCORE_NC] (unscaled dot bits, token index) lists
   uint32_t *fail_cnt;   // rows that fall back to the full score row
   int32_t *fail_list;   // [rows] their row numbers
   int ns, cap, rank;

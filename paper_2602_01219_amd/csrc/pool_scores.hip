@@ -94,6 +94,22 @@ __global__ __launch_bounds__(BLOCK) SCORES_OCCUPANCY void scores_kernel(const T 
                                            blockIdx.x, gridDim.x, blockIdx.y, blockIdx.z, -1);
 }
 
+// The bf16 score pass with landmark values on the DMA tiles (score16_chunk):
+// NW waves of NG landmark groups each; three waves per SIMD with four-wave
+// workgroups (two scratch spills outside the tile loop).
+template <int D, int NG, int NW, bool WRITE_S, bool SELECT>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(NW == 4 ? 3 : 2))) void scores16_kernel(
+    const bf16_t *__restrict__ q_lm, const bf16_t *__restrict__ k, const bf16_t *__restrict__ v,
+    float *__restrict__ S, float2 *__restrict__ part_ml, float *__restrict__ part_o, SelectArgs sel, int N, int M,
+    float scale) {
+  using DT = DmaTile<D, TK32, NW>;
+  // the two tile buffers (K then V each) as separate arrays
+  __shared__ __align__(16) char tiles0[2 * DT::BYTES];
+  __shared__ __align__(16) char tiles1[2 * DT::BYTES];
+  score16_chunk<D, NG, NW, WRITE_S, SELECT>(tiles0, tiles1, q_lm, k, v, S, part_ml, part_o, sel, N, M, scale,
+                                            (int)blockIdx.x, (int)gridDim.x, (int)blockIdx.y, (int64_t)blockIdx.z);
+}
+
 // Score rows of listed landmark rows (fallback of the fused selection).
 template <typename T, int D>
 __global__ __launch_bounds__(BLOCK) void scores_rows_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
@@ -232,6 +248,44 @@ static hipError_t scores_t(const mita_cfg_t &c, const void *q_lm, const void *k,
   const float sc = eff_scale(c);
   const SelectArgs sel = sb ? SelectArgs{sb->plo, sb->ccnt, sb->cand} : SelectArgs{nullptr, nullptr, nullptr};
   const T *ql = (const T *)q_lm, *kk = (const T *)k, *vv = (const T *)v;
+  // bf16, d = 128, with landmark values: every such pass (selection, stored
+  // scores or values alone) runs score16_chunk, so their landmark values
+  // agree. (At d = 64 the 64-key register-staged tiles of score_chunk are
+  // faster: per 32-key tile the listing's fixed steps weigh twice as much
+  // against the smaller products.)
+  if constexpr (sizeof(T) == 2 && D == 128) {
+    if (v_lm) {
+      constexpr int NG = 1;
+      const bool narrow = c.M <= 32 * NG;  // two waves cover the landmarks
+      const int per = 16 * NG * (narrow ? 2 : 4);
+      const dim3 g16(nch, (c.M + per - 1) / per, (unsigned)BH(c));
+      const bf16_t *qb = (const bf16_t *)q_lm, *kb = (const bf16_t *)k, *vb = (const bf16_t *)v;
+#define MITA_SCORES16(NW, W, SEL)                                                                                  \
+  hipLaunchKernelGGL((scores16_kernel<D, NG, NW, W, SEL>), g16, dim3(64 * NW), 0, st, qb, kb, vb, S, ml, po, sel, \
+                     c.N, c.M, sc)
+      if (narrow) {
+        if (sb)
+          MITA_SCORES16(2, false, true);
+        else if (S)
+          MITA_SCORES16(2, true, false);
+        else
+          MITA_SCORES16(2, false, false);
+      } else {
+        if (sb)
+          MITA_SCORES16(4, false, true);
+        else if (S)
+          MITA_SCORES16(4, true, false);
+        else
+          MITA_SCORES16(4, false, false);
+      }
+#undef MITA_SCORES16
+      hipError_t e = launched("scores16_kernel", st);
+      if (e != hipSuccess || sb) return e;  // with sel the merge runs in the selection's finish
+      hipLaunchKernelGGL((merge_kernel<T, D>), dim3((unsigned)c.M, (unsigned)BH(c)), dim3(256), 0, st, ml, po,
+                         (T *)v_lm, c.M, nch);
+      return launched("merge_kernel", st);
+    }
+  }
 #define MITA_SCORES(W, V, SEL) \
   hipLaunchKernelGGL((scores_kernel<T, D, W, V, SEL>), grid, dim3(BLOCK), 0, st, ql, kk, vv, S, ml, po, sel, c.N, c.M, sc)
   if (sb) {

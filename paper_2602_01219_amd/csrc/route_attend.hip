@@ -606,7 +606,7 @@ __global__ __launch_bounds__(BLOCK) void finalize_logits_kernel(
   }
   if (fin) {
     finalize_row<T, D, CAP, MERGE>(*reinterpret_cast<FinalizeLds<T, D, CAP, MERGE> *>(buf), i, cand, ccnt, idx,
-                                   fail_cnt, fail_list, k, cap, nch, part_ml, part_o, v_lm, M);
+                                   fail_cnt, fail_list, k, cap, nch, part_ml, part_o, v_lm, M, scale);
     return;
   }
   route_logits_body<T, D, false>(reinterpret_cast<T *>(buf), cnt, i % route_x, i / route_x, q, q_lm, expert, tile_cnt, counts,
@@ -1011,7 +1011,6 @@ __global__ __launch_bounds__(BLOCK) void attend_kernel(const T *__restrict__ q, 
 // the LDS reads per MFMA are half those of NG = 1, and the two groups' MFMA
 // chains are independent.
 // ---------------------------------------------------------------------------
-constexpr int TK32 = 32;
 // d = 64, one group per wave: registers for seven waves per SIMD (seven
 // workgroups of 16 + 2.5 KB LDS fit a CU at M + k = 640); two groups per
 // wave: four waves per SIMD (eight two-wave workgroups per CU)

@@ -8,8 +8,9 @@
 //      at least k and far fewer than `cap` tokens of the row score >= pivot,
 //      except with negligible probability (r = k exactly when the sample is
 //      the whole row).
-//   3. the score pass lists every token scoring >= pivot (score bits, token
-//      index), in token order, in one region per (row, key chunk).
+//   3. the score pass lists every token scoring >= pivot (bits of its
+//      unscaled dot, token index), in token order, in one region per (row,
+//      key chunk); the finish scales the dots as every score is scaled.
 //   4. finalize_kernel: with k <= count <= cap the list holds the row's whole
 //      top-k, since every token left out scores below the pivot, which the
 //      k-th listed score reaches. The row's regions are packed into LDS, an
@@ -45,10 +46,11 @@ __global__ __launch_bounds__(256) void finalize_kernel(const uint2 *__restrict__
                                                        uint32_t *__restrict__ fail_cnt,
                                                        int32_t *__restrict__ fail_list, int k, int cap, int nch,
                                                        const float2 *__restrict__ part_ml,
-                                                       const float *__restrict__ part_o, T *__restrict__ v_lm, int M) {
+                                                       const float *__restrict__ part_o, T *__restrict__ v_lm, int M,
+                                                       float scale) {
   __shared__ FinalizeLds<T, D, CAP, MERGE> sh;
   finalize_row<T, D, CAP, MERGE>(sh, blockIdx.x, cand, ccnt, idx, fail_cnt, fail_list, k, cap, nch, part_ml, part_o,
-                                 v_lm, M);
+                                 v_lm, M, scale);
 }
 
 // ---------------------------------------------------------------------------
@@ -84,7 +86,7 @@ static hipError_t launch_select_finalize(const mita_cfg_t &c, const SelectBufs &
                          : nullptr;
 #define MITA_FINALIZE(TT, DD, CAP, MG)                                                                          \
   hipLaunchKernelGGL((finalize_kernel<TT, DD, CAP, MG>), dim3(rows), dim3(256), 0, st, sb.cand, sb.ccnt, idx,   \
-                     sb.fail_cnt, sb.fail_list, c.k, sb.cap, nch, ml, po, (TT *)v_lm, c.M)
+                     sb.fail_cnt, sb.fail_list, c.k, sb.cap, nch, ml, po, (TT *)v_lm, c.M, eff_scale(c))
 #define MITA_FINALIZE_CAP(TT, DD, MG)     \
   if (sb.cap <= 1024)                     \
     MITA_FINALIZE(TT, DD, 1024, MG);      \
