@@ -617,9 +617,10 @@ __global__ __launch_bounds__(BLOCK) void finalize_logits_kernel(
 // bf16: the sampled scores and pivots and the routing logits (independent of
 // each other) share one launch of 16-wave workgroups: the few sample
 // workgroups are latency-bound and leave CUs idle, which the routing
-// workgroups (sixteen 64-query tiles each) fill. Workgroups [0, nS) take the
-// sample grid (x fastest), the rest the routing grid; LDS is one buffer that
-// either part lays out for itself.
+// workgroups (sixteen 64-query tiles each) fill. Workgroups [0, nSp) take
+// the nS sample slots (x fastest, spread over the XCDs by xcd_slot so that a
+// head's blocks share an L2; slots past nS exit), the rest the routing grid;
+// LDS is one buffer that either part lays out for itself.
 // ---------------------------------------------------------------------------
 template <typename T, int D> struct SampleLogitsLds {
   static constexpr int A = 16 * SP_PITCH * (int)sizeof(uint32_t);
@@ -630,19 +631,21 @@ template <typename T, int D>
 __global__ __launch_bounds__(1024) void sample_logits_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
                                                              uint32_t *__restrict__ plo,
                                                              uint32_t *__restrict__ fail_cnt, int ns, int r,
-                                                             int sample_x, int nS, const T *__restrict__ q,
+                                                             int sample_x, int nS, int nSp, const T *__restrict__ q,
                                                              int32_t *__restrict__ expert,
                                                              int32_t *__restrict__ counts, int N, int M, float scale,
                                                              int ntiles, int route_x) {
   __shared__ __align__(16) char buf[SampleLogitsLds<T, D>::BYTES];
   extern __shared__ uint32_t cnt[];  // routing: [16][M]
   const int b = (int)blockIdx.x;
-  if (b < nS) {
-    sample_pivot_body<T, D, 16>(reinterpret_cast<uint32_t(*)[SP_PITCH]>(buf), b % sample_x, b / sample_x, q_lm, k,
+  if (b < nSp) {  // nSp = nS rounded up to whole XCD ranges (xcd_slot)
+    const int f = xcd_slot(b, nSp / NXCD);
+    if (f >= nS) return;
+    sample_pivot_body<T, D, 16>(reinterpret_cast<uint32_t(*)[SP_PITCH]>(buf), f % sample_x, f / sample_x, q_lm, k,
                                 plo, fail_cnt, N, M, ns, r, scale);
     return;
   }
-  const int i = b - nS;
+  const int i = b - nSp;
   route_logits_body<T, D, false, 16>(reinterpret_cast<T *>(buf), cnt, i % route_x, i / route_x, q, q_lm, expert,
                                      nullptr, counts, N, M, scale, ntiles);
 }
@@ -1478,17 +1481,17 @@ hipError_t launch_pivots_logits(const mita_cfg_t &c, const void *q, const void *
                                 const SelectBufs &sb, int32_t *expert, int32_t *counts, hipStream_t st) {
   if (!pivots_with_logits(c, sb)) return hipErrorInvalidValue;
   const int bh = (int)BH(c);
-  const int sample_x = (c.M + 15) / 16, nS = sample_x * bh;
+  const int sample_x = (c.M + 15) / 16, nS = sample_x * bh, nSp = NXCD * ((nS + NXCD - 1) / NXCD);
   const int nt = route_tiles(c), route_x = (nt + 15) / 16, nR = route_x * bh;
-  const dim3 grid((unsigned)(nS + nR));
+  const dim3 grid((unsigned)(nSp + nR));
   const size_t dyn = 16 * (size_t)c.M * sizeof(uint32_t);
   if (c.d == 64)
     hipLaunchKernelGGL((sample_logits_kernel<bf16_t, 64>), grid, dim3(1024), dyn, st, (const bf16_t *)q_lm,
-                       (const bf16_t *)k, sb.plo, sb.fail_cnt, sb.ns, sb.rank, sample_x, nS, (const bf16_t *)q, expert,
+                       (const bf16_t *)k, sb.plo, sb.fail_cnt, sb.ns, sb.rank, sample_x, nS, nSp, (const bf16_t *)q, expert,
                        counts, c.N, c.M, eff_scale(c), nt, route_x);
   else
     hipLaunchKernelGGL((sample_logits_kernel<bf16_t, 128>), grid, dim3(1024), dyn, st, (const bf16_t *)q_lm,
-                       (const bf16_t *)k, sb.plo, sb.fail_cnt, sb.ns, sb.rank, sample_x, nS, (const bf16_t *)q, expert,
+                       (const bf16_t *)k, sb.plo, sb.fail_cnt, sb.ns, sb.rank, sample_x, nS, nSp, (const bf16_t *)q, expert,
                        counts, c.N, c.M, eff_scale(c), nt, route_x);
   return launched("sample_logits_kernel", st);
 }

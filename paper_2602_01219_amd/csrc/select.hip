@@ -28,16 +28,22 @@
 #include "check.hpp"
 #include "finalize.hpp"
 #include "sample.hpp"
+#include "worklist.hpp"
 
 namespace mita {
 
+// One workgroup per (16 landmarks, head) slot, slots spread over the XCDs in
+// contiguous ranges (xcd_slot): a head's landmark blocks share an XCD, so
+// its sampled key rows are fetched into one L2 instead of one per block.
 template <typename T, int D, int NW>
 __global__ __launch_bounds__(64 * NW) void sample_pivot_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
                                                                uint32_t *__restrict__ plo,
                                                                uint32_t *__restrict__ fail_cnt, int N, int M, int ns,
-                                                               int r, float scale) {
+                                                               int r, float scale, int nbx, int nslots) {
   __shared__ __align__(16) uint32_t keys[16][SP_PITCH];
-  sample_pivot_body<T, D, NW>(keys, (int)blockIdx.x, (int)blockIdx.y, q_lm, k, plo, fail_cnt, N, M, ns, r, scale);
+  const int f = xcd_slot((int)blockIdx.x, (int)gridDim.x / NXCD);
+  if (f >= nslots) return;  // the whole workgroup
+  sample_pivot_body<T, D, NW>(keys, f % nbx, f / nbx, q_lm, k, plo, fail_cnt, N, M, ns, r, scale);
 }
 
 template <typename T, int D, int CAP, bool MERGE>
@@ -62,9 +68,10 @@ static hipError_t sample_pivot_t(const mita_cfg_t &c, const void *q_lm, const vo
   // bf16: one sample tile and one row per wave (16 waves); fp32 (more
   // registers per fragment): four waves, four tiles and four rows each
   constexpr int NW = sizeof(T) == 2 ? 16 : 4;
-  const dim3 grid((unsigned)((c.M + 15) / 16), (unsigned)BH(c));
+  const int nbx = (c.M + 15) / 16, nslots = nbx * (int)BH(c);
+  const dim3 grid((unsigned)(NXCD * ((nslots + NXCD - 1) / NXCD)));
   hipLaunchKernelGGL((sample_pivot_kernel<T, D, NW>), grid, dim3(64 * NW), 0, st, (const T *)q_lm, (const T *)k,
-                     sb.plo, sb.fail_cnt, c.N, c.M, sb.ns, sb.rank, eff_scale(c));
+                     sb.plo, sb.fail_cnt, c.N, c.M, sb.ns, sb.rank, eff_scale(c), nbx, nslots);
   return launched("sample_pivot_kernel", st);
 }
 

@@ -17,6 +17,10 @@ namespace mita {
 // f % T of that head, T = the grid's x extent (a multiple of 8).
 constexpr int NXCD = 8;
 
+// Slot of workgroup L in a grid of NXCD * C workgroups whose slots the XCDs
+// take in contiguous ranges of C (XCD x: slots [x C, (x + 1) C)).
+__device__ __forceinline__ int xcd_slot(int L, int C) { return (L % NXCD) * C + L / NXCD; }
+
 // The workgroup's head bh, queries [q_begin, q_end) (positions in perm) and
 // their group e (of G), from the work list; false for a workgroup past its
 // end. Without ROUTED, bh keeps the caller's value and the workgroup takes
