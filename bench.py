@@ -82,14 +82,18 @@ def kernel_work(name: str, wl, plan: dict, staged: bool, s: int = 1, launched=()
     stored_s = rt and not plan.get("fused")
     w = {
         "pool_kernel": (tens + lmt, 0),
-        "sample_pivot_kernel": (BH * ns * d * e + lmt + 4 * rows, 2 * M * ns * d * BH),
+        "sample_pivot_kernel": (BH * ns * d * e + lmt + 4 * rows + (4 * rows * k if ns == N else 0),
+                                2 * M * ns * d * BH),
         "scores_kernel": (tens * (1 + sh) + lmt + 4 * BH * M * N * stored_s, 2 * M * N * d * BH * (1 + sh)),
         "merge_kernel": (BH * nch * M * (d + 2) * 4 + lmt, 0),
         "finalize_kernel": (4 * rows * k + lmt * sh, 0),
         # the routing logits run in the finish launch unless the pivot launch
         # took them (sample_logits_kernel)
+        # (with the sample the whole row, N <= 1024, the sample launch writes the
+        # sets and the finish launch forms the routing logits only)
         "finalize_logits_kernel": (4 * rows * k + lmt * sh, 0) if "sample_logits_kernel" in launched else
-                                  (4 * rows * k + lmt * sh + tens + lmt + 4 * BH * N, 2 * N * M * d * BH),
+                                  ((tens + lmt + 4 * BH * N, 2 * N * M * d * BH) if ns == N else
+                                   (4 * rows * k + lmt * sh + tens + lmt + 4 * BH * N, 2 * N * M * d * BH)),
         "sample_logits_kernel": (BH * ns * d * e + lmt + 4 * rows + tens + lmt + 4 * BH * N,
                                  2 * M * ns * d * BH + 2 * N * M * d * BH),
         "topk_scatter_kernel": (8 * BH * N + 8 * BH * (M + 1), 0),

@@ -33,6 +33,10 @@ struct SelectBufs {
   uint32_t *fail_cnt;   // rows that fall back to the full score row
   int32_t *fail_list;   // [rows] their row numbers
   int ns, cap, rank;
+  // non-null when the sample is the whole row (ns == N): the pivot launch
+  // writes the top-k sets here itself, the score pass lists nothing and the
+  // finish selects nothing (direct selection)
+  int32_t *idx;
 };
 
 // Scores S = fl(q_lm . k) * scale (optional) and landmark values (optional):

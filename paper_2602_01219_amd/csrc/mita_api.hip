@@ -157,7 +157,9 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
     sel.ns = sel_ns(*c);
     sel.cap = sel_cap(*c);
     sel.rank = sel_rank(*c);
+    sel.idx = sel.ns == c->N ? idx : nullptr;  // the sample is the row: the pivot launch writes the sets
   }
+  const bool direct = fused && sel.idx;
 
   // with the fused selection and in-place gather, the selection's finish
   // shares launches with the routing (the "route" stage then includes it),
@@ -181,12 +183,14 @@ int forward_impl(const mita_cfg_t *c, const void *q, const void *k, const void *
   TRY(mark(1));
   // bf16: the routing logits are formed beside the sampled scores (they
   // depend on the landmarks only), in the same launch
-  const bool logits_early = sel_in_route && pivots_with_logits(*c, sel);
+  const bool logits_early = sel_in_route && !direct && pivots_with_logits(*c, sel);
   if (logits_early)
     TRY(hip_status(launch_pivots_logits(*c, q, q_lm, k, sel, expert, counts, st), "select pivots"));
   else if (fused)
     TRY(hip_status(launch_select_pivots(*c, q_lm, k, sel, st), "select pivots"));
-  TRY(hip_status(launch_scores(*c, q_lm, k, v, fused ? nullptr : S, v_lm, w + L.partial, fused ? &sel : nullptr, st),
+  // (direct selection: the score pass forms the landmark values only)
+  TRY(hip_status(launch_scores(*c, q_lm, k, v, fused ? nullptr : S, v_lm, w + L.partial,
+                               fused && !direct ? &sel : nullptr, st),
                  "scores"));
   TRY(mark(2));
   if (fused && !sel_in_route)
@@ -267,6 +271,7 @@ int backward_impl(const mita_cfg_t *c, const void *q, const void *k, const void 
     sel.ns = sel_ns(*c);
     sel.cap = sel_cap(*c);
     sel.rank = sel_rank(*c);
+    sel.idx = sel.ns == c->N ? idx : nullptr;  // the sample is the row: the pivot launch writes the sets
   }
   // recomputation (stages 0 to 4)
   rec.stage = 0;
@@ -275,7 +280,8 @@ int backward_impl(const mita_cfg_t *c, const void *q, const void *k, const void 
   if (c->use_routed) {
     if (fused) {
       TRY(hip_status(launch_select_pivots(*c, q_lm, k, sel, st), "select pivots"));
-      TRY(hip_status(launch_scores(*c, q_lm, k, v, nullptr, v_lm, w + L.partial, &sel, st), "scores"));
+      TRY(hip_status(launch_scores(*c, q_lm, k, v, nullptr, v_lm, w + L.partial, sel.idx ? nullptr : &sel, st),
+                     "scores"));
       rec.stage = 2;
       TRY(hip_status(launch_select_finish(*c, q_lm, k, sel, S, idx, w + L.partial, v_lm, st), "topk"));
     } else {

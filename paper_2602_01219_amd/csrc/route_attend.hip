@@ -1400,9 +1400,12 @@ static hipError_t select_route_t(const mita_cfg_t &c, const void *q, const void 
   const float2 *ml = (const float2 *)partial;
   const float *po = MERGE ? (const float *)((const char *)partial + align_up((size_t)rows * nch * sizeof(float2)))
                           : nullptr;
-  // with the logits formed beside the sampled scores, the finish rows run alone
+  // with the logits formed beside the sampled scores, the finish rows run
+  // alone; with the sets written by the pivot launch (direct selection) the
+  // routing logits do
   const int route_x = (nt + 3) / 4;
-  const int nF = (int)rows, nR = logits_done ? 0 : route_x * bh;
+  const int nF = sb.idx ? 0 : (int)rows, nR = logits_done ? 0 : route_x * bh;
+  if (nF + nR == 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL((finalize_logits_kernel<T, D, CAP, MERGE>), dim3((unsigned)(nF + nR)), dim3(BLOCK),
                      nR ? 4 * c.M * sizeof(uint32_t) : 0, st, sb.cand, sb.ccnt, idx, sb.fail_cnt, sb.fail_list, c.k, sb.cap,
                      nch, ml, po, (T *)v_lm, nF, (const T *)q, (const T *)q_lm, expert, tile_cnt, counts, c.N, c.M,

@@ -152,11 +152,17 @@ constexpr int SP_PITCH = SEL_NS + 4;  // keys per LDS row: rows start 4 banks ap
 
 // Workgroup (bx, by) of the sample grid (16 landmarks of head by); keys: 16
 // LDS rows of SP_PITCH words.
+// With idx (only when the sample is the whole row, ns == N, and r == kk)
+// the rows' top-kk sets are written too, in ascending token order: every key
+// above the pivot and, in token order, as many keys equal to it as the set
+// still needs (the order of the top-k: larger score first, lower index first
+// among equal scores).
 template <typename T, int D, int NW>
 __device__ __forceinline__ void sample_pivot_body(uint32_t (*keys)[SP_PITCH], int bx, int by,
                                                   const T *__restrict__ q_lm, const T *__restrict__ k,
                                                   uint32_t *__restrict__ plo, uint32_t *__restrict__ fail_cnt, int N,
-                                                  int M, int ns, int r, float scale) {
+                                                  int M, int ns, int r, float scale, int32_t *__restrict__ idx = nullptr,
+                                                  int kk = 0) {
   static_assert(16 % NW == 0 && SEL_NS % (NW * TK) == 0, "sample/pivot split");
   constexpr int PERW = SEL_NS / NW;  // samples per wave
   constexpr int RPW = 16 / NW;       // rows per wave
@@ -215,6 +221,28 @@ __device__ __forceinline__ void sample_pivot_body(uint32_t (*keys)[SP_PITCH], in
     }
     const uint32_t lo = pivot_of(v, &keys[rl][0], r);
     if (lane == 0) plo[bh * M + lm0 + rl] = lo;
+    if (idx) {
+      // the row's keys back in LDS (pivot_of used its first words)
+#pragma unroll
+      for (int i = 0; i < PIVOT_PER / 4; ++i)
+        *reinterpret_cast<uint4 *>(&keys[rl][256 * i + 4 * lane]) = make_uint4(v[4 * i], v[4 * i + 1], v[4 * i + 2], v[4 * i + 3]);
+      uint32_t gt = 0;
+#pragma unroll
+      for (int i = 0; i < PIVOT_PER; ++i) gt += v[i] > lo ? 1u : 0u;
+      const uint32_t need_eq = (uint32_t)kk - wave_sum_u32(gt);  // >= 1: lo is the kk-th largest
+      int32_t *out = idx + (bh * M + lm0 + rl) * (int64_t)kk;
+      uint32_t taken = 0, eq_seen = 0;
+      for (int j0 = 0; j0 < ns; j0 += 64) {
+        const int j = j0 + lane;
+        const uint32_t key = j < ns ? keys[rl][j] : 0u;  // 0 lies below every key
+        const uint64_t be = __ballot(key == lo);
+        const bool take = key > lo || (key == lo && eq_seen + lanes_below(be) < need_eq);
+        const uint64_t bt = __ballot(take);
+        if (take) out[taken + lanes_below(bt)] = j;
+        taken += (uint32_t)__popcll(bt);
+        eq_seen += (uint32_t)__popcll(be);
+      }
+    }
   }
 }
 

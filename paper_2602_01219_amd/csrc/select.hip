@@ -39,11 +39,12 @@ template <typename T, int D, int NW>
 __global__ __launch_bounds__(64 * NW) void sample_pivot_kernel(const T *__restrict__ q_lm, const T *__restrict__ k,
                                                                uint32_t *__restrict__ plo,
                                                                uint32_t *__restrict__ fail_cnt, int N, int M, int ns,
-                                                               int r, float scale, int nbx, int nslots) {
+                                                               int r, float scale, int nbx, int nslots,
+                                                               int32_t *__restrict__ idx, int kk) {
   __shared__ __align__(16) uint32_t keys[16][SP_PITCH];
   const int f = xcd_slot((int)blockIdx.x, (int)gridDim.x / NXCD);
   if (f >= nslots) return;  // the whole workgroup
-  sample_pivot_body<T, D, NW>(keys, f % nbx, f / nbx, q_lm, k, plo, fail_cnt, N, M, ns, r, scale);
+  sample_pivot_body<T, D, NW>(keys, f % nbx, f / nbx, q_lm, k, plo, fail_cnt, N, M, ns, r, scale, idx, kk);
 }
 
 template <typename T, int D, int CAP, bool MERGE>
@@ -71,13 +72,14 @@ static hipError_t sample_pivot_t(const mita_cfg_t &c, const void *q_lm, const vo
   const int nbx = (c.M + 15) / 16, nslots = nbx * (int)BH(c);
   const dim3 grid((unsigned)(NXCD * ((nslots + NXCD - 1) / NXCD)));
   hipLaunchKernelGGL((sample_pivot_kernel<T, D, NW>), grid, dim3(64 * NW), 0, st, (const T *)q_lm, (const T *)k,
-                     sb.plo, sb.fail_cnt, c.N, c.M, sb.ns, sb.rank, eff_scale(c), nbx, nslots);
+                     sb.plo, sb.fail_cnt, c.N, c.M, sb.ns, sb.rank, eff_scale(c), nbx, nslots, sb.idx, c.k);
   return launched("sample_pivot_kernel", st);
 }
 
 hipError_t launch_select_pivots(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sb,
                                 hipStream_t st) {
   if (sb.ns > SEL_NS) return hipErrorInvalidValue;  // the workgroup holds SEL_NS keys per row
+  if (sb.idx && (sb.ns != c.N || sb.rank != c.k)) return hipErrorInvalidValue;  // direct sets need the whole row
   if (c.dtype == MITA_F32)
     return c.d == 64 ? sample_pivot_t<float, 64>(c, q_lm, k, sb, st) : sample_pivot_t<float, 128>(c, q_lm, k, sb, st);
   return c.d == 64 ? sample_pivot_t<bf16_t, 64>(c, q_lm, k, sb, st) : sample_pivot_t<bf16_t, 128>(c, q_lm, k, sb, st);
@@ -125,6 +127,7 @@ static hipError_t launch_select_finalize(const mita_cfg_t &c, const SelectBufs &
 
 hipError_t launch_select_finish(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sb, float *S,
                                 int32_t *idx, const void *partial, void *v_lm, hipStream_t st) {
+  if (sb.idx) return hipSuccess;  // the pivot launch wrote the sets; nothing is listed
   hipError_t e = launch_select_finalize(c, sb, idx, partial, v_lm, st);
   if (e != hipSuccess) return e;
   if ((e = launch_scores_rows(c, q_lm, k, S, sb.fail_cnt, sb.fail_list, st)) != hipSuccess) return e;
