@@ -146,6 +146,7 @@ def kernel_work(name: str, wl, plan: dict, staged: bool, s: int = 1, launched=()
                               else (12 * BH * N * d + 4 * BH * M * d * sh + 3 * tens, 0))
     w["lse_rows_kernel"] = (8 * BH * nch * M + 4 * rows, 0)
     w["scores16_kernel"] = w["scores_kernel"]
+    w["pool_small_kernel"] = w["pool_kernel"]
     w["attend16_kernel"] = att
     w["attend_kernel"] = att
     return w.get(name, (0, 0))

@@ -810,6 +810,40 @@ template <typename T, int D, int PF = 8> struct LandmarkMerge {
   }
 };
 
+// The same merge for one (row, dimension) by one thread: the 256 / D
+// groups' chunk sequences run one after the other (each in increasing chunk
+// order, from the empty state), then the groups are combined in group order,
+// with the arithmetic of LandmarkMerge, so the result is the same bit for bit.
+template <int D>
+__device__ __forceinline__ float merge_landmark_value_1(const float2 *__restrict__ part_ml,
+                                                        const float *__restrict__ part_o, int64_t bh, int lm, int M,
+                                                        int nch, int dim) {
+  constexpr int NG = 256 / D;
+  float gm[NG], gl[NG], ga[NG];
+#pragma unroll
+  for (int grp = 0; grp < NG; ++grp) {
+    float mx = -INFINITY, L = 0.f, acc = 0.f;
+    for (int c = grp; c < nch; c += NG) {
+      const int64_t prow = (bh * nch + c) * M + lm;
+      LandmarkMerge<float, D>::step(mx, L, acc, part_ml[prow], part_o[prow * D + dim]);
+    }
+    gm[grp] = mx;
+    gl[grp] = L;
+    ga[grp] = acc;
+  }
+  float m2 = -INFINITY;
+#pragma unroll
+  for (int g2 = 0; g2 < NG; ++g2) m2 = fmaxf(m2, gm[g2]);
+  float L2 = 0.f, a2 = 0.f;
+#pragma unroll
+  for (int g2 = 0; g2 < NG; ++g2) {
+    const float f = __builtin_amdgcn_exp2f(gm[g2] - m2);
+    L2 += gl[g2] * f;
+    a2 += ga[g2] * f;
+  }
+  return a2 / L2;
+}
+
 template <typename T, int D>
 __device__ __forceinline__ void merge_landmark_value(const float2 *__restrict__ part_ml,
                                                      const float *__restrict__ part_o, T *__restrict__ v_lm,

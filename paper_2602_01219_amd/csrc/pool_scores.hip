@@ -79,6 +79,57 @@ __global__ __launch_bounds__(256) void pool_kernel(const T *__restrict__ q, T *_
   }
 }
 
+// The same pooling for small windows (at most SMALL_WINDOW tokens): one wave
+// per landmark row, four rows per workgroup; lane = (token slot, 16-byte
+// chunk), the slots summed across lanes (sum order: each slot's tokens in
+// order, then the slots pairwise).
+constexpr int SMALL_WINDOW = 32;
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void pool_small_kernel(const T *__restrict__ q, T *__restrict__ q_lm,
+                                                         int32_t *__restrict__ zero_counts,
+                                                         int32_t *__restrict__ zero_cursor, int N, int gh, int gw,
+                                                         int lh, int lw, int64_t rows) {
+  constexpr int VE = 16 / (int)sizeof(T);
+  constexpr int CPT = D / VE;  // chunks per token row
+  constexpr int PS = 64 / CPT;  // token slots per wave
+  static_assert(PS >= 1 && 64 % CPT == 0, "whole token rows per wave");
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;  // the whole wave; no barriers below
+  const int M = lh * lw;
+  const int64_t bh = row / M;
+  const int i = (int)(row % M);
+  const int a = i / lw, b = i % lw;
+  const int r0 = (int)(((int64_t)a * gh) / lh), r1 = (int)(((int64_t)(a + 1) * gh + lh - 1) / lh);
+  const int c0 = (int)(((int64_t)b * gw) / lw), c1 = (int)(((int64_t)(b + 1) * gw + lw - 1) / lw);
+  const int cols = c1 - c0, count = (r1 - r0) * cols;
+  if (zero_counts && lane == 0) zero_counts[row] = 0;
+  if (zero_cursor && lane == 0) zero_cursor[row] = 0;
+  const int ch = lane % CPT, slot = lane / CPT;
+  float acc[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) acc[e] = 0.f;
+  const T *base = q + bh * (int64_t)N * D;
+  for (int t = slot; t < count; t += PS) {
+    const int r = r0 + t / cols, c = c0 + t % cols;
+    float x[VE];
+    unpack16(*reinterpret_cast<const uint4 *>(base + ((int64_t)r * gw + c) * D + ch * VE), x, (const T *)nullptr);
+#pragma unroll
+    for (int e = 0; e < VE; ++e) acc[e] += x[e];
+  }
+#pragma unroll
+  for (int o = CPT; o < 64; o <<= 1)
+#pragma unroll
+    for (int e = 0; e < VE; ++e) acc[e] += __shfl_xor(acc[e], o);
+  if (slot == 0) {
+    T out[VE];
+#pragma unroll
+    for (int e = 0; e < VE; ++e) out[e] = from_f32<T>(acc[e] / (float)count);
+    *reinterpret_cast<uint4 *>(q_lm + row * D + ch * VE) = *reinterpret_cast<const uint4 *>(out);
+  }
+}
+
 // The bf16 d=64 pass holds 3 waves per SIMD (at most 168 VGPRs).
 #define SCORES_OCCUPANCY __attribute__((amdgpu_waves_per_eu(sizeof(T) == 2 && D == 64 ? 3 : (sizeof(T) == 2 ? 2 : 1))))
 
@@ -121,14 +172,18 @@ __global__ __launch_bounds__(BLOCK) void scores_rows_kernel(const T *__restrict_
   scores_rows_body<T, D>(&Ks[0][0], (int)blockIdx.x, (int)gridDim.x, q_lm, k, S, nrows, rows, N, M, scale, nchunks);
 }
 
-// Log-sum-exp merge of the per-chunk landmark-value partials, one workgroup
-// per landmark row (the same merge, in the same order, as the fused
-// selection's finish applies).
+// Log-sum-exp merge of the per-chunk landmark-value partials, one thread per
+// (landmark row, dimension) (the same merge, in the same order, as the fused
+// selection's finish applies to a row with a whole workgroup).
 template <typename T, int D>
 __global__ __launch_bounds__(256) void merge_kernel(const float2 *__restrict__ part_ml, const float *__restrict__ part_o,
-                                                    T *__restrict__ v_lm, int M, int nchunks) {
-  __shared__ float red[256 / D][3][D];
-  merge_landmark_value<T, D>(part_ml, part_o, v_lm, blockIdx.y, blockIdx.x, M, nchunks, red);
+                                                    T *__restrict__ v_lm, int M, int nchunks, int64_t rows) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t row = t / D;
+  if (row >= rows) return;
+  const int dim = (int)(t % D);
+  v_lm[row * D + dim] =
+      from_f32<T>(merge_landmark_value_1<D>(part_ml, part_o, row / M, (int)(row % M), M, nchunks, dim));
 }
 
 // ---------------------------------------------------------------------------
@@ -159,6 +214,18 @@ __global__ __launch_bounds__(256) void gather_kernel(const T *__restrict__ k, co
 template <typename T, int D>
 static hipError_t pool_t(const mita_cfg_t &c, const void *q, void *q_lm, int32_t *zc, int32_t *zcur,
                          hipStream_t st) {
+  // the largest window: its most rows times its most columns
+  int wr = 0, wc = 0;
+  for (int a = 0; a < c.lm_h; ++a)
+    wr = std::max(wr, (int)(((int64_t)(a + 1) * c.grid_h + c.lm_h - 1) / c.lm_h - ((int64_t)a * c.grid_h) / c.lm_h));
+  for (int b = 0; b < c.lm_w; ++b)
+    wc = std::max(wc, (int)(((int64_t)(b + 1) * c.grid_w + c.lm_w - 1) / c.lm_w - ((int64_t)b * c.grid_w) / c.lm_w));
+  if ((int64_t)wr * wc <= SMALL_WINDOW) {
+    const int64_t rows = BH(c) * c.M;
+    hipLaunchKernelGGL((pool_small_kernel<T, D>), dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st, (const T *)q,
+                       (T *)q_lm, zc, zcur, c.N, c.grid_h, c.grid_w, c.lm_h, c.lm_w, rows);
+    return launched("pool_small_kernel", st);
+  }
   dim3 grid(c.M, (unsigned)BH(c));
   hipLaunchKernelGGL((pool_kernel<T, D>), grid, dim3(256), 0, st, (const T *)q, (T *)q_lm, zc, zcur, c.N, c.grid_h,
                      c.grid_w, c.lm_h, c.lm_w);
@@ -281,8 +348,8 @@ static hipError_t scores_t(const mita_cfg_t &c, const void *q_lm, const void *k,
 #undef MITA_SCORES16
       hipError_t e = launched("scores16_kernel", st);
       if (e != hipSuccess || sb) return e;  // with sel the merge runs in the selection's finish
-      hipLaunchKernelGGL((merge_kernel<T, D>), dim3((unsigned)c.M, (unsigned)BH(c)), dim3(256), 0, st, ml, po,
-                         (T *)v_lm, c.M, nch);
+      hipLaunchKernelGGL((merge_kernel<T, D>), dim3((unsigned)((BH(c) * c.M * D + 255) / 256)), dim3(256), 0, st, ml,
+                         po, (T *)v_lm, c.M, nch, (int64_t)BH(c) * c.M);
       return launched("merge_kernel", st);
     }
   }
@@ -305,8 +372,8 @@ static hipError_t scores_t(const mita_cfg_t &c, const void *q_lm, const void *k,
 #undef MITA_SCORES
   hipError_t e = launched("scores_kernel", st);
   if (e != hipSuccess || !v_lm || sb) return e;  // with sel the merge runs in the selection's finish
-  hipLaunchKernelGGL((merge_kernel<T, D>), dim3((unsigned)c.M, (unsigned)BH(c)), dim3(256), 0, st, ml, po, (T *)v_lm,
-                     c.M, nch);
+  hipLaunchKernelGGL((merge_kernel<T, D>), dim3((unsigned)((BH(c) * c.M * D + 255) / 256)), dim3(256), 0, st, ml, po,
+                     (T *)v_lm, c.M, nch, (int64_t)BH(c) * c.M);
   return launched("merge_kernel", st);
 }
 

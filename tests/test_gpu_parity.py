@@ -685,7 +685,7 @@ def test_timer_records_every_launch():
     for call, stages in zip(launches, ms):
         names = [n for n, _, _ in call]
         log(f"  launches {[(n, s, round(t_ * 1e3, 1)) for n, s, t_ in call]}")
-        assert names[0] == "pool_kernel" and names[-1] == "attend16_kernel"
+        assert names[0] in ("pool_kernel", "pool_small_kernel") and names[-1] == "attend16_kernel"
         assert "scores_kernel" in names or "scores16_kernel" in names
         # stage times are sums of their launches; a stage that launches nothing takes 0
         for s_ in range(mita.NUM_STAGES):
