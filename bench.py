@@ -147,6 +147,7 @@ def kernel_work(name: str, wl, plan: dict, staged: bool, s: int = 1, launched=()
     w["lse_rows_kernel"] = (8 * BH * nch * M + 4 * rows, 0)
     w["scores16_kernel"] = w["scores_kernel"]
     w["pool_small_kernel"] = w["pool_kernel"]
+    w["finalize_wave_kernel"] = w["finalize_kernel"]
     w["attend16_kernel"] = att
     w["attend_kernel"] = att
     return w.get(name, (0, 0))

@@ -6,6 +6,7 @@
 #include "cdna4.hpp"
 #include "flash.hpp"
 #include "check.hpp"
+#include "sample.hpp"
 
 namespace mita {
 
@@ -202,6 +203,97 @@ __device__ __forceinline__ void finalize_row(FinalizeLds<T, D, CAP, MERGE> &sh, 
     }
   }
   if (MERGE) lmm.finish(part_ml, part_o, v_lm, row / M, (int)(row % M), M, nch, red);
+}
+
+// ---------------------------------------------------------------------------
+// The same finish by one wave per row, for lists of at most SEL_NS entries
+// and at most 64 key chunks (no barriers; a workgroup takes four rows):
+// the chunk regions are packed into LDS in token order, the keys (score_key
+// of the scaled dot) read back 16 per lane (entry j = lane + 64 m, key 0
+// past the list), the k-th largest key K found exactly by pivot_of, and an
+// ordered scan over the entries writes every token with a key above K and,
+// in token order, as many with key K as the set still needs: the tokens with
+// composite >= C_k, in ascending order, as finalize_row writes them.
+// ---------------------------------------------------------------------------
+struct FinalizeWaveLds {
+  uint2 lst[SEL_NS];
+  uint32_t scratch[384];  // pivot_of's histogram and slots
+};
+
+template <typename T, int D, bool MERGE>
+__device__ __forceinline__ void finalize_row_wave(FinalizeWaveLds &sh, int64_t row, const uint2 *__restrict__ cand,
+                                                  const uint32_t *__restrict__ ccnt, int32_t *__restrict__ idx,
+                                                  uint32_t *__restrict__ fail_cnt, int32_t *__restrict__ fail_list,
+                                                  int k, int cap, int nch, const float2 *__restrict__ part_ml,
+                                                  const float *__restrict__ part_o, T *__restrict__ v_lm, int M,
+                                                  float scale) {
+  const int lane = threadIdx.x & 63;
+  // the landmark-value partials are loaded first; the merge uses them last
+  constexpr int DL = D / 64;  // dimensions per lane
+  LandmarkMerge1<D> lmm[DL];
+  if (MERGE)
+#pragma unroll
+    for (int u = 0; u < DL; ++u) lmm[u].prefetch(part_ml, part_o, row / M, (int)(row % M), M, nch, lane + 64 * u);
+  // chunk counts -> exclusive prefix (nch <= 64: one chunk per lane)
+  const uint32_t cc = lane < nch ? ccnt[row * nch + lane] : 0u;
+  const uint32_t incl = wave_inclusive_scan(cc);
+  const uint32_t total = (uint32_t)__shfl((int)incl, 63);
+  const uint32_t excl = incl - cc;
+  if (total >= (uint32_t)k && total <= (uint32_t)cap) {
+    // the list into LDS, the first 64 entries of four chunks loaded before any is stored
+    const uint2 *crow = cand + row * nch * (int64_t)SCORE_NC;
+    for (int c0 = 0; c0 < nch; c0 += 4) {
+      uint2 e[4];
+      uint32_t n[4], b[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int c = c0 + u < nch ? c0 + u : 0;
+        n[u] = c0 + u < nch ? (uint32_t)__shfl((int)cc, c) : 0u;
+        b[u] = (uint32_t)__shfl((int)excl, c);
+        e[u] = (uint32_t)lane < n[u] ? crow[(int64_t)c * SCORE_NC + lane] : make_uint2(0u, 0u);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if ((uint32_t)lane < n[u]) sh.lst[b[u] + lane] = make_uint2(score_key(__uint_as_float(e[u].x) * scale), e[u].y);
+        for (uint32_t j = lane + 64; j < n[u]; j += 64) {
+          const uint2 x = crow[(int64_t)(c0 + u) * SCORE_NC + j];
+          sh.lst[b[u] + j] = make_uint2(score_key(__uint_as_float(x.x) * scale), x.y);
+        }
+      }
+    }
+    uint32_t v[PIVOT_PER];
+    int32_t ix[PIVOT_PER];
+#pragma unroll
+    for (int m = 0; m < PIVOT_PER; ++m) {
+      const uint32_t j = (uint32_t)(lane + 64 * m);
+      const uint2 x = j < total ? sh.lst[j] : make_uint2(0u, 0u);
+      v[m] = x.x;
+      ix[m] = (int32_t)x.y;
+    }
+    const uint32_t K = pivot_of(v, sh.scratch, k);
+    uint32_t gt = 0;
+#pragma unroll
+    for (int m = 0; m < PIVOT_PER; ++m) gt += v[m] > K ? 1u : 0u;
+    const uint32_t need_eq = (uint32_t)k - wave_sum_u32(gt);  // >= 1: K is the k-th largest
+    int32_t *out = idx + row * (int64_t)k;
+    uint32_t taken = 0, eq_seen = 0;
+#pragma unroll
+    for (int m = 0; m < PIVOT_PER; ++m) {
+      const uint64_t be = __ballot(v[m] == K);
+      const bool take = v[m] > K || (v[m] == K && eq_seen + lanes_below(be) < need_eq);
+      const uint64_t bt = __ballot(take);
+      if (take) out[taken + lanes_below(bt)] = ix[m];
+      taken += (uint32_t)__popcll(bt);
+      eq_seen += (uint32_t)__popcll(be);
+    }
+  } else if (lane == 0) {
+    fail_list[atomicAdd(fail_cnt, 1u)] = (int32_t)row;
+  }
+  if (MERGE)
+#pragma unroll
+    for (int u = 0; u < DL; ++u)
+      v_lm[row * D + lane + 64 * u] =
+          from_f32<T>(lmm[u].finish(part_ml, part_o, row / M, (int)(row % M), M, nch, lane + 64 * u));
 }
 
 }  // namespace mita

@@ -814,6 +814,57 @@ template <typename T, int D, int PF = 8> struct LandmarkMerge {
 // groups' chunk sequences run one after the other (each in increasing chunk
 // order, from the empty state), then the groups are combined in group order,
 // with the arithmetic of LandmarkMerge, so the result is the same bit for bit.
+// prefetch() loads the first PF chunks' values (PF a multiple of 256 / D),
+// so that a caller can overlap them with other work before finish().
+template <int D, int PF = 8> struct LandmarkMerge1 {
+  static constexpr int NG = 256 / D;
+  static_assert(PF % NG == 0, "whole rounds of the groups prefetched");
+  float2 ml[PF];
+  float ov[PF];
+  __device__ __forceinline__ void prefetch(const float2 *__restrict__ part_ml, const float *__restrict__ part_o,
+                                           int64_t bh, int lm, int M, int nch, int dim) {
+#pragma unroll
+    for (int c = 0; c < PF; ++c)
+      if (c < nch) {
+        const int64_t prow = (bh * nch + c) * M + lm;
+        ml[c] = part_ml[prow];
+        ov[c] = part_o[prow * D + dim];
+      }
+  }
+  __device__ __forceinline__ float finish(const float2 *__restrict__ part_ml, const float *__restrict__ part_o,
+                                          int64_t bh, int lm, int M, int nch, int dim) const {
+    float gm[NG], gl[NG], ga[NG];
+#pragma unroll
+    for (int grp = 0; grp < NG; ++grp) {
+      float mx = -INFINITY, L = 0.f, acc = 0.f;
+#pragma unroll
+      for (int j = 0; j < PF / NG; ++j)
+        if (grp + NG * j < nch) LandmarkMerge<float, D>::step(mx, L, acc, ml[grp + NG * j], ov[grp + NG * j]);
+      for (int c = grp + PF; c < nch; c += NG) {
+        const int64_t prow = (bh * nch + c) * M + lm;
+        LandmarkMerge<float, D>::step(mx, L, acc, part_ml[prow], part_o[prow * D + dim]);
+      }
+      gm[grp] = mx;
+      gl[grp] = L;
+      ga[grp] = acc;
+    }
+    return combine(gm, gl, ga);
+  }
+  __device__ __forceinline__ static float combine(const float (&gm)[NG], const float (&gl)[NG], const float (&ga)[NG]) {
+    float m2 = -INFINITY;
+#pragma unroll
+    for (int g2 = 0; g2 < NG; ++g2) m2 = fmaxf(m2, gm[g2]);
+    float L2 = 0.f, a2 = 0.f;
+#pragma unroll
+    for (int g2 = 0; g2 < NG; ++g2) {
+      const float f = __builtin_amdgcn_exp2f(gm[g2] - m2);
+      L2 += gl[g2] * f;
+      a2 += ga[g2] * f;
+    }
+    return a2 / L2;
+  }
+};
+
 template <int D>
 __device__ __forceinline__ float merge_landmark_value_1(const float2 *__restrict__ part_ml,
                                                         const float *__restrict__ part_o, int64_t bh, int lm, int M,
@@ -831,18 +882,9 @@ __device__ __forceinline__ float merge_landmark_value_1(const float2 *__restrict
     gl[grp] = L;
     ga[grp] = acc;
   }
-  float m2 = -INFINITY;
-#pragma unroll
-  for (int g2 = 0; g2 < NG; ++g2) m2 = fmaxf(m2, gm[g2]);
-  float L2 = 0.f, a2 = 0.f;
-#pragma unroll
-  for (int g2 = 0; g2 < NG; ++g2) {
-    const float f = __builtin_amdgcn_exp2f(gm[g2] - m2);
-    L2 += gl[g2] * f;
-    a2 += ga[g2] * f;
-  }
-  return a2 / L2;
+  return LandmarkMerge1<D>::combine(gm, gl, ga);
 }
+
 
 template <typename T, int D>
 __device__ __forceinline__ void merge_landmark_value(const float2 *__restrict__ part_ml,

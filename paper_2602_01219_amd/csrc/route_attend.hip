@@ -578,21 +578,22 @@ __global__ __launch_bounds__(256) void route_scatter_kernel(const int32_t *__res
 // The routing part's 2-D grid is flattened (x fastest). LDS is one buffer
 // that either part lays out for itself.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int CAP, bool MERGE> struct FinalizeLogitsLds {
-  static constexpr int F = (int)sizeof(FinalizeLds<T, D, CAP, MERGE>);
+// WAVE: finish rows by finalize_row_wave, four per workgroup.
+template <typename T, int D, int CAP, bool MERGE, bool WAVE> struct FinalizeLogitsLds {
+  static constexpr int F = WAVE ? 4 * (int)sizeof(FinalizeWaveLds) : (int)sizeof(FinalizeLds<T, D, CAP, MERGE>);
   static constexpr int BYTES = F > RouteLds<T, D>::BYTES ? F : RouteLds<T, D>::BYTES;
 };
 
 // Finalize rows and routing workgroups interleave one to one while both last,
 // so the two kinds run side by side.
-template <typename T, int D, int CAP, bool MERGE>
+template <typename T, int D, int CAP, bool MERGE, bool WAVE>
 __global__ __launch_bounds__(BLOCK) void finalize_logits_kernel(
     const uint2 *__restrict__ cand, const uint32_t *__restrict__ ccnt, int32_t *__restrict__ idx,
     uint32_t *__restrict__ fail_cnt, int32_t *__restrict__ fail_list, int k, int cap, int nch,
     const float2 *__restrict__ part_ml, const float *__restrict__ part_o, T *__restrict__ v_lm, int nF,
     const T *__restrict__ q, const T *__restrict__ q_lm, int32_t *__restrict__ expert, int32_t *__restrict__ tile_cnt,
-    int32_t *__restrict__ counts, int N, int M, float scale, int ntiles, int route_x, int nR) {
-  __shared__ __align__(16) char buf[FinalizeLogitsLds<T, D, CAP, MERGE>::BYTES];
+    int32_t *__restrict__ counts, int N, int M, float scale, int ntiles, int route_x, int nR, int64_t nrows) {
+  __shared__ __align__(16) char buf[FinalizeLogitsLds<T, D, CAP, MERGE, WAVE>::BYTES];
   extern __shared__ uint32_t cnt[];  // routing: [4][M]
   const int b = (int)blockIdx.x, lo = min(nF, nR);
   bool fin;
@@ -605,8 +606,16 @@ __global__ __launch_bounds__(BLOCK) void finalize_logits_kernel(
     i = b - lo;
   }
   if (fin) {
-    finalize_row<T, D, CAP, MERGE>(*reinterpret_cast<FinalizeLds<T, D, CAP, MERGE> *>(buf), i, cand, ccnt, idx,
-                                   fail_cnt, fail_list, k, cap, nch, part_ml, part_o, v_lm, M, scale);
+    if constexpr (WAVE) {
+      const int w = (int)threadIdx.x >> 6;
+      const int64_t row = (int64_t)i * 4 + w;
+      if (row < nrows)  // the whole wave
+        finalize_row_wave<T, D, MERGE>(reinterpret_cast<FinalizeWaveLds *>(buf)[w], row, cand, ccnt, idx, fail_cnt,
+                                       fail_list, k, cap, nch, part_ml, part_o, v_lm, M, scale);
+    } else {
+      finalize_row<T, D, CAP, MERGE>(*reinterpret_cast<FinalizeLds<T, D, CAP, MERGE> *>(buf), i, cand, ccnt, idx,
+                                     fail_cnt, fail_list, k, cap, nch, part_ml, part_o, v_lm, M, scale);
+    }
     return;
   }
   route_logits_body<T, D, false>(reinterpret_cast<T *>(buf), cnt, i % route_x, i / route_x, q, q_lm, expert, tile_cnt, counts,
@@ -1387,7 +1396,7 @@ hipError_t launch_route(const mita_cfg_t &c, const void *q, const void *q_lm, in
                    : route_t<bf16_t, 128>(c, q, q_lm, expert, perm, offsets, tile_cnt, tile_base, counts, tile_start, st);
 }
 
-template <typename T, int D, int CAP, bool MERGE>
+template <typename T, int D, int CAP, bool MERGE, bool WAVE>
 static hipError_t select_route_t(const mita_cfg_t &c, const void *q, const void *q_lm, const void *k,
                                  const SelectBufs &sb, float *S, int32_t *idx, const void *partial, void *v_lm,
                                  int32_t *expert, int32_t *perm, int32_t *offsets, int32_t *tile_cnt,
@@ -1404,12 +1413,12 @@ static hipError_t select_route_t(const mita_cfg_t &c, const void *q, const void 
   // alone; with the sets written by the pivot launch (direct selection) the
   // routing logits do
   const int route_x = (nt + 3) / 4;
-  const int nF = sb.idx ? 0 : (int)rows, nR = logits_done ? 0 : route_x * bh;
+  const int nF = sb.idx ? 0 : (int)(WAVE ? (rows + 3) / 4 : rows), nR = logits_done ? 0 : route_x * bh;
   if (nF + nR == 0) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((finalize_logits_kernel<T, D, CAP, MERGE>), dim3((unsigned)(nF + nR)), dim3(BLOCK),
+  hipLaunchKernelGGL((finalize_logits_kernel<T, D, CAP, MERGE, WAVE>), dim3((unsigned)(nF + nR)), dim3(BLOCK),
                      nR ? 4 * c.M * sizeof(uint32_t) : 0, st, sb.cand, sb.ccnt, idx, sb.fail_cnt, sb.fail_list, c.k, sb.cap,
                      nch, ml, po, (T *)v_lm, nF, (const T *)q, (const T *)q_lm, expert, tile_cnt, counts, c.N, c.M,
-                     eff_scale(c), nt, route_x, nR);
+                     eff_scale(c), nt, route_x, nR, rows);
   hipError_t err = launched("finalize_logits_kernel", st);
   if (err != hipSuccess) return err;
   // the fallback workgroups of the last launch (listed rows, scored in full and selected)
@@ -1439,19 +1448,23 @@ static hipError_t select_route_n(const mita_cfg_t &c, const void *q, const void 
                                  int32_t *expert, int32_t *perm, int32_t *offsets, int32_t *tile_cnt,
                                  int32_t *tile_base, int32_t *counts, int32_t *tile_start, bool logits_done,
                                  hipStream_t st) {
-#define MITA_SR(CAP, MG)                                                                                       \
-  return select_route_t<T, D, CAP, MG>(c, q, q_lm, k, sb, S, idx, partial, v_lm, expert, perm, offsets, tile_cnt, \
-                                       tile_base, counts, tile_start, logits_done, st)
+#define MITA_SR(CAP, MG, W)                                                                                      \
+  return select_route_t<T, D, CAP, MG, W>(c, q, q_lm, k, sb, S, idx, partial, v_lm, expert, perm, offsets, tile_cnt, \
+                                          tile_base, counts, tile_start, logits_done, st)
+  // lists of at most SEL_NS entries over at most 64 chunks: one wave per row
+  const bool wave = sb.cap <= SEL_NS && score_chunks(c) <= 64;
   if (v_lm) {
-    if (sb.cap <= 1024) MITA_SR(1024, true);
-    if (sb.cap <= 2048) MITA_SR(2048, true);
-    if (sb.cap <= 4096) MITA_SR(4096, true);
-    MITA_SR(SEL_CAP, true);
+    if (wave) MITA_SR(SEL_NS, true, true);
+    if (sb.cap <= 1024) MITA_SR(1024, true, false);
+    if (sb.cap <= 2048) MITA_SR(2048, true, false);
+    if (sb.cap <= 4096) MITA_SR(4096, true, false);
+    MITA_SR(SEL_CAP, true, false);
   }
-  if (sb.cap <= 1024) MITA_SR(1024, false);
-  if (sb.cap <= 2048) MITA_SR(2048, false);
-  if (sb.cap <= 4096) MITA_SR(4096, false);
-  MITA_SR(SEL_CAP, false);
+  if (wave) MITA_SR(SEL_NS, false, true);
+  if (sb.cap <= 1024) MITA_SR(1024, false, false);
+  if (sb.cap <= 2048) MITA_SR(2048, false, false);
+  if (sb.cap <= 4096) MITA_SR(4096, false, false);
+  MITA_SR(SEL_CAP, false, false);
 #undef MITA_SR
 }
 

@@ -60,6 +60,23 @@ __global__ __launch_bounds__(256) void finalize_kernel(const uint2 *__restrict__
                                  v_lm, M, scale);
 }
 
+// The same with one wave per row (lists of at most SEL_NS, at most 64 chunks).
+template <typename T, int D, bool MERGE>
+__global__ __launch_bounds__(256) void finalize_wave_kernel(const uint2 *__restrict__ cand,
+                                                            const uint32_t *__restrict__ ccnt,
+                                                            int32_t *__restrict__ idx, uint32_t *__restrict__ fail_cnt,
+                                                            int32_t *__restrict__ fail_list, int k, int cap, int nch,
+                                                            const float2 *__restrict__ part_ml,
+                                                            const float *__restrict__ part_o, T *__restrict__ v_lm,
+                                                            int M, float scale, int64_t nrows) {
+  __shared__ FinalizeWaveLds sh[4];
+  const int w = (int)threadIdx.x >> 6;
+  const int64_t row = (int64_t)blockIdx.x * 4 + w;
+  if (row >= nrows) return;  // the whole wave
+  finalize_row_wave<T, D, MERGE>(sh[w], row, cand, ccnt, idx, fail_cnt, fail_list, k, cap, nch, part_ml, part_o,
+                                 v_lm, M, scale);
+}
+
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
@@ -96,8 +113,16 @@ static hipError_t launch_select_finalize(const mita_cfg_t &c, const SelectBufs &
 #define MITA_FINALIZE(TT, DD, CAP, MG)                                                                          \
   hipLaunchKernelGGL((finalize_kernel<TT, DD, CAP, MG>), dim3(rows), dim3(256), 0, st, sb.cand, sb.ccnt, idx,   \
                      sb.fail_cnt, sb.fail_list, c.k, sb.cap, nch, ml, po, (TT *)v_lm, c.M, eff_scale(c))
+#define MITA_FINALIZE_WAVE(TT, DD, MG)                                                                          \
+  hipLaunchKernelGGL((finalize_wave_kernel<TT, DD, MG>), dim3((rows + 3) / 4), dim3(256), 0, st, sb.cand, sb.ccnt, \
+                     idx, sb.fail_cnt, sb.fail_list, c.k, sb.cap, nch, ml, po, (TT *)v_lm, c.M, eff_scale(c),      \
+                     (int64_t)rows)
+  // lists of at most SEL_NS entries over at most 64 chunks: one wave per row
+  const bool wave = sb.cap <= SEL_NS && nch <= 64;
 #define MITA_FINALIZE_CAP(TT, DD, MG)     \
-  if (sb.cap <= 1024)                     \
+  if (wave)                               \
+    MITA_FINALIZE_WAVE(TT, DD, MG);       \
+  else if (sb.cap <= 1024)                \
     MITA_FINALIZE(TT, DD, 1024, MG);      \
   else if (sb.cap <= 2048)                \
     MITA_FINALIZE(TT, DD, 2048, MG);      \
@@ -121,8 +146,9 @@ static hipError_t launch_select_finalize(const mita_cfg_t &c, const SelectBufs &
     }
   }
 #undef MITA_FINALIZE_CAP
+#undef MITA_FINALIZE_WAVE
 #undef MITA_FINALIZE
-  return launched("finalize_kernel", st);
+  return launched(wave ? "finalize_wave_kernel" : "finalize_kernel", st);
 }
 
 hipError_t launch_select_finish(const mita_cfg_t &c, const void *q_lm, const void *k, const SelectBufs &sb, float *S,

@@ -575,10 +575,16 @@ def test_fused_selection_exact_ties_within_the_list():
     _fallback_case(torch.zeros_like(k), cfg, q, v, expect_fb=0)
 
 
-def test_fused_selection_quantised_keys():
+@pytest.mark.parametrize("name", ["dense_pred_bf16", "vitb_hr_bf16"])
+def test_fused_selection_quantised_keys(name):
     """Keys in {-1, 0, 1}: scores take few distinct values, so the k-th score
-    is shared by many tokens and the cut falls inside a run of ties."""
-    inp, cfg, (q, k, v) = _small_dense()
+    is shared by many tokens and the cut falls inside a run of ties (the
+    16K-token shape's lists take the workgroup finish, the 4K-token shape's
+    the one-wave finish)."""
+    wl = synth.WORKLOADS[name].with_(B=1, H=2)
+    inp = synth.generate(wl)
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = (to_dev(x, "bf16") for x in (inp.q, inp.k, inp.v))
     r = np.random.default_rng(11)
     kq = r.integers(-1, 2, size=k.shape).astype(np.float32)
     K = torch.from_numpy(kq).to(torch.bfloat16).cuda()
