@@ -453,10 +453,12 @@ def test_forward_edge_cases(case):
 # ------------------------------------------------------------------ fused top-k selection
 
 
-@pytest.mark.parametrize("name", ALL)
+@pytest.mark.parametrize("name", ALL + list(synth.OPERATING_ORDER))
 def test_fused_selection_equals_full_score_path(name):
     """The forward's selection inside the score pass gives the sets of the
-    exact top-k over the stored score matrix: identical outputs."""
+    exact top-k over the stored score matrix: identical outputs (the
+    operating points take the direct selection, N <= 1024, and the one-wave
+    finish of short lists)."""
     cfg = mita.Config.from_workload(_inputs(name).wl)
     q, k, v = _dev_inputs(name)
     ws = torch.empty(mita.workspace_size(cfg), dtype=torch.uint8, device="cuda")
