@@ -425,6 +425,10 @@ EDGE = [
     (16, 16, 4, 4, 40, 128, "f32", 0, 1),
     (32, 33, 8, 11, 100, 64, "bf16", 1, 1),   # M = 88 (two partial landmark blocks), ragged N = 1056
     (9, 8, 9, 8, 5, 64, "bf16", 1, 1),        # M = N
+    # lists of at most 1024 candidates over three key chunks: the one-wave
+    # finish (d = 128: two dimensions per lane in its merge)
+    (36, 36, 6, 6, 36, 64, "bf16", 1, 1),
+    (36, 36, 6, 6, 36, 128, "bf16", 1, 1),
     # key row lists longer than the attention stages in LDS (M + k > 8192):
     # register-staged tiles, row indices read from memory
     (96, 96, 4, 4, 8200, 64, "bf16", 1, 1),
