@@ -124,9 +124,8 @@ def kernel_work(name: str, wl, plan: dict, staged: bool, s: int = 1, launched=()
                               6 * N * nkeys * d * BH)
     w["bwd_kv_kernel"] = (2 * BH * M * k * d * e + 2 * tens + 8 * BH * N + 8 * BH * M * k * d, 8 * N * k * d * BH * rt)
     w["bwd_kv_shared_kernel"] = (2 * lmt + 2 * tens + 8 * BH * N + 8 * BH * M * d, 8 * N * M * d * BH * sh)
-    w["inv_count_kernel"] = (4 * BH * M * k + 4 * BH * N, 0)
-    w["inv_scan_kernel"] = (8 * BH * N, 0)
-    w["inv_place_kernel"] = (8 * BH * M * k + 8 * BH * N, 0)
+    # inverse index of the top-k sets: the sets read once, slots and starts written
+    w["inv_index_kernel"] = (8 * BH * M * k * rt + 4 * BH * (N + 1) * rt, 0)
     w["inv_gather_kernel"] = (8 * BH * M * k * d + 4 * BH * M * k + 8 * BH * N + 8 * BH * N * d, 0)
     if wl.dtype == "f32":
         w["bwd_landmark_kernel"] = (2 * lmt + 4 * BH * M * d + 2 * tens + 4 * rows + 8 * BH * N * d + 4 * BH * M * d,

@@ -1319,19 +1319,117 @@ __global__ __launch_bounds__(256) void lmv_prep_kernel(const float *__restrict__
   D_lm[t] = dsum;
 }
 
-// Inverse index of the top-k sets: for each token, the (expert, position)
-// slots e * k + j with idx[e][j] = token, by a counting sort (count, scan,
-// place; the order of a token's slots is that of the atomic decrements).
-__global__ __launch_bounds__(256) void inv_count_kernel(const int32_t *__restrict__ idx, int32_t *__restrict__ cnt,
-                                                        int64_t total, int per_head, int N) {
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= total) return;
-  const int64_t bh = t / per_head;
-  atomicAdd(&cnt[bh * N + idx[t]], 1);
+// Inverse index of the top-k sets: for each token, the slots e * k + j with
+// idx[e][j] = token, listed by start [BH, N + 1] and slot [BH, M * k] (a
+// counting sort). One workgroup per (head, range of T tokens), its counters
+// in LDS: it reads all of its head's sets, counting the slots of its own
+// tokens and those of the tokens below its range (the range's base), scans
+// its counts from that base, and places its slots on a second read. The
+// order of a token's slots is that of the LDS atomics. Entries outside
+// [0, N) are left out of the index.
+constexpr int INV_THREADS = 512, INV_WAVES = INV_THREADS / 64;
+constexpr int INV_TMAX = 15360;  // tokens per workgroup: 60 KiB of counters
+
+// f(i, idx[i]) for the head's per_head entries, strided over the workgroup:
+// four 16-byte loads in flight per thread where the rows allow it.
+template <class F>
+__device__ __forceinline__ void inv_entries(const int32_t *__restrict__ ih, int per_head, F &&f) {
+  int i = threadIdx.x;
+  if ((per_head & 3) == 0 && ((uintptr_t)ih & 15) == 0) {
+    const int4 *v = reinterpret_cast<const int4 *>(ih);
+    const int n4 = per_head >> 2;
+    for (; i + 3 * INV_THREADS < n4; i += 4 * INV_THREADS) {
+      int4 x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) x[u] = v[i + u * INV_THREADS];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int e = 4 * (i + u * INV_THREADS);
+        f(e, x[u].x);
+        f(e + 1, x[u].y);
+        f(e + 2, x[u].z);
+        f(e + 3, x[u].w);
+      }
+    }
+    for (; i < n4; i += INV_THREADS) {
+      const int4 x = v[i];
+      f(4 * i, x.x);
+      f(4 * i + 1, x.y);
+      f(4 * i + 2, x.z);
+      f(4 * i + 3, x.w);
+    }
+    return;
+  }
+  for (; i < per_head; i += INV_THREADS) f(i, ih[i]);
+}
+
+// Grid: NXCD * ceil(nwork / NXCD) workgroups of INV_THREADS, nwork = BH *
+// parts, parts = ceil(N / T); dynamic LDS (T + 2 * INV_WAVES) * 4 bytes.
+__global__ __launch_bounds__(INV_THREADS) void inv_index_kernel(const int32_t *__restrict__ idx,
+                                                                int32_t *__restrict__ start,
+                                                                int32_t *__restrict__ slot, int per_head, int N,
+                                                                int T, int parts, int64_t nwork) {
+  extern __shared__ uint32_t inv_lds[];
+  uint32_t *cnt = inv_lds, *wsum = inv_lds + T;
+  // a head's ranges on consecutive slots of one XCD, which share its sets in L2
+  const int64_t w = xcd_slot((int)blockIdx.x, (int)(gridDim.x / NXCD));
+  if (w >= nwork) return;
+  const int64_t bh = w / parts;
+  const int t0 = (int)(w % parts) * T;
+  const uint32_t nt = (uint32_t)min(N - t0, T);
+  const int32_t *ih = idx + bh * per_head;
+  for (uint32_t i = threadIdx.x; i < nt; i += INV_THREADS) cnt[i] = 0;
+  __syncthreads();
+  uint32_t below = 0;
+  inv_entries(ih, per_head, [&](int, int tok) {
+    const uint32_t r = (uint32_t)tok - (uint32_t)t0;
+    if ((uint32_t)tok < (uint32_t)t0)
+      ++below;
+    else if (r < nt)
+      atomicAdd(&cnt[r], 1u);
+  });
+  __syncthreads();
+  // exclusive scan of the counts from the base (consecutive runs per thread)
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const uint32_t per = (nt + INV_THREADS - 1) / INV_THREADS;
+  const uint32_t b0 = min(nt, threadIdx.x * per), b1 = min(nt, b0 + per);
+  uint32_t sum = 0;
+  for (uint32_t i = b0; i < b1; ++i) sum += cnt[i];
+  const uint32_t incl = wave_inclusive_scan(sum), bw = wave_sum_u32(below);
+  if (lane == 63) {
+    wsum[wv] = incl;
+    wsum[INV_WAVES + wv] = bw;
+  }
+  __syncthreads();
+  uint32_t before = incl - sum, base = 0, all = 0;
+#pragma unroll
+  for (int i = 0; i < INV_WAVES; ++i) {
+    before += i < wv ? wsum[i] : 0u;
+    all += wsum[i];
+    base += wsum[INV_WAVES + i];
+  }
+  before += base;
+  for (uint32_t i = b0; i < b1; ++i) {
+    const uint32_t c = cnt[i];
+    cnt[i] = before;
+    before += c;
+  }
+  __syncthreads();
+  int32_t *sh = start + bh * (N + 1) + t0;
+  for (uint32_t i = threadIdx.x; i < nt; i += INV_THREADS) sh[i] = (int32_t)cnt[i];
+  if (threadIdx.x == 0 && t0 + (int)nt == N) sh[nt] = (int32_t)(base + all);
+  __syncthreads();  // (the copy above reads the starts before the atomics move them)
+  // place: cnt holds each token's next free position (< base + all <= per_head)
+  int32_t *sl = slot + bh * per_head;
+  inv_entries(ih, per_head, [&](int e, int tok) {
+    const uint32_t r = (uint32_t)tok - (uint32_t)t0;
+    if (r < nt) sl[atomicAdd(&cnt[r], 1u)] = e;
+  });
 }
 
 // Exclusive scan of cnt over each head's N tokens into start [BH, N + 1]
-// (1024 threads per head, consecutive runs per thread).
+// (1024 threads per head, consecutive runs per thread; the merge rounds'
+// positions of the surviving tokens).
 __global__ __launch_bounds__(1024) void inv_scan_kernel(const int32_t *__restrict__ cnt, int32_t *__restrict__ start,
                                                         int N) {
   __shared__ uint32_t wsum[16];
@@ -1355,17 +1453,6 @@ __global__ __launch_bounds__(1024) void inv_scan_kernel(const int32_t *__restric
     before += (uint32_t)cnt[bh * N + i];
   }
   if (threadIdx.x == 0) start[bh * (N + 1) + N] = (int32_t)all;
-}
-
-__global__ __launch_bounds__(256) void inv_place_kernel(const int32_t *__restrict__ idx, int32_t *__restrict__ cnt,
-                                                        const int32_t *__restrict__ start, int32_t *__restrict__ slot,
-                                                        int64_t total, int per_head, int N) {
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= total) return;
-  const int64_t bh = t / per_head;
-  const int tok = idx[t];
-  const int pos = atomicSub(&cnt[bh * N + tok], 1) - 1;
-  slot[bh * (int64_t)per_head + start[bh * (N + 1) + tok] + pos] = (int32_t)(t - bh * per_head);
 }
 
 // dk_acc, dv_acc of every token = the sum of its staged per-expert rows
@@ -1578,16 +1665,19 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
       hipLaunchKernelGGL((bwd_kv_kernel<T, D, true>), dim3(nx, bh), dim3(256), 0, st, kv);
     if ((err = launched("bwd_kv_kernel", st)) != hipSuccess) return err;
     const int per_head = c.M * c.k;
-    const int64_t total = BH(c) * per_head;
-    const unsigned gi = (unsigned)((total + 255) / 256);
-    if ((err = launch_zero(b.inv_cnt, BH(c) * c.N, st)) != hipSuccess) return err;
-    hipLaunchKernelGGL(inv_count_kernel, dim3(gi), dim3(256), 0, st, b.idx, b.inv_cnt, total, per_head, c.N);
-    if ((err = launched("inv_count_kernel", st)) != hipSuccess) return err;
-    hipLaunchKernelGGL(inv_scan_kernel, dim3(bh), dim3(1024), 0, st, b.inv_cnt, b.inv_start, c.N);
-    if ((err = launched("inv_scan_kernel", st)) != hipSuccess) return err;
-    hipLaunchKernelGGL(inv_place_kernel, dim3(gi), dim3(256), 0, st, b.idx, b.inv_cnt, b.inv_start, b.inv_slot, total,
-                       per_head, c.N);
-    if ((err = launched("inv_place_kernel", st)) != hipSuccess) return err;
+    // token ranges per head: about one workgroup per CU over all heads (a
+    // head's ranges on one XCD), at least 256 tokens each, at most INV_TMAX
+    const int64_t heads = BH(c), per_xcd = (heads + NXCD - 1) / NXCD;
+    int parts = (int)std::max<int64_t>(1, 256 / (NXCD * per_xcd));
+    parts = std::min(parts, std::max(1, c.N / 256));
+    parts = std::max(parts, (c.N + INV_TMAX - 1) / INV_TMAX);
+    const int span = (c.N + parts - 1) / parts;
+    parts = (c.N + span - 1) / span;
+    const int64_t nwork = heads * parts;
+    hipLaunchKernelGGL(inv_index_kernel, dim3((unsigned)((nwork + NXCD - 1) / NXCD * NXCD)), dim3(INV_THREADS),
+                       (size_t)(span + 2 * INV_WAVES) * 4, st, b.idx, b.inv_start, b.inv_slot, per_head, c.N, span, parts,
+                       nwork);
+    if ((err = launched("inv_index_kernel", st)) != hipSuccess) return err;
     if (!fused_finish) {  // (else the landmark-value key pass sums the staged rows)
       const int64_t rows = BH(c) * c.N;
       hipLaunchKernelGGL((inv_gather_kernel<D>), dim3((unsigned)((rows * (D / 4) + 255) / 256)), dim3(256), 0, st,

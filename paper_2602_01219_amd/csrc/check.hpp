@@ -301,8 +301,8 @@ inline FwdLayout forward_layout(const mita_cfg_t &c) {
 // buffers.
 struct BwdLayout {
   FwdLayout f;
-  size_t lse_lm, dq_direct, dk_acc, dv_acc, dq_lm_acc, dv_lm_acc, q_lse, q_D, stage_k, stage_v, inv_cnt, inv_start,
-      inv_slot, dv_lm16, D_lm, total;
+  size_t lse_lm, dq_direct, dk_acc, dv_acc, dq_lm_acc, dv_lm_acc, q_lse, q_D, stage_k, stage_v, inv_start, inv_slot,
+      dv_lm16, D_lm, total;
 };
 
 inline BwdLayout backward_layout(const mita_cfg_t &c) {
@@ -326,7 +326,6 @@ inline BwdLayout backward_layout(const mita_cfg_t &c) {
   const size_t stage = c.use_routed ? bh * c.M * (size_t)c.k * c.d * 4 : 0;
   L.stage_k = take(stage);
   L.stage_v = take(stage);
-  L.inv_cnt = take(c.use_routed ? bh * c.N * 4 : 0);
   L.inv_start = take(c.use_routed ? bh * (c.N + 1) * 4 : 0);
   L.inv_slot = take(c.use_routed ? bh * c.M * (size_t)c.k * 4 : 0);
   // the landmark values' gradient in bf16 and each landmark row's dV~ . V~

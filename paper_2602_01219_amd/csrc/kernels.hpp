@@ -129,7 +129,7 @@ struct BwdBufs {
   float *dq_lm_acc, *dv_lm_acc;    // [BH, M, d] (zeroed)
   float *q_lse, *q_D;              // [BH, N] per-query log-sum-exp and dO . o (written)
   float *stage_k, *stage_v;        // [BH, M, k, d] per-expert sums of the routed keys (written)
-  int32_t *inv_cnt, *inv_start, *inv_slot;  // inverse index of the top-k sets
+  int32_t *inv_start, *inv_slot;   // inverse index of the top-k sets: [BH, N + 1], [BH, M * k]
   void *dv_lm16;                   // [BH, M, d] bf16 copy of the landmark values' gradient
   float *D_lm;                     // [BH, M] dV~ . V~ per landmark row
   void *dq, *dk, *dv;              // [BH, N, d] outputs (io type)

@@ -327,7 +327,6 @@ int backward_impl(const mita_cfg_t *c, const void *q, const void *k, const void 
   b.q_D = (float *)(w + BL.q_D);
   b.stage_k = (float *)(w + BL.stage_k);
   b.stage_v = (float *)(w + BL.stage_v);
-  b.inv_cnt = (int32_t *)(w + BL.inv_cnt);
   b.inv_start = (int32_t *)(w + BL.inv_start);
   b.inv_slot = (int32_t *)(w + BL.inv_slot);
   b.dv_lm16 = w + BL.dv_lm16;
