@@ -1327,49 +1327,75 @@ __global__ __launch_bounds__(256) void lmv_prep_kernel(const float *__restrict__
 // its counts from that base, and places its slots on a second read. The
 // order of a token's slots is that of the LDS atomics. Entries outside
 // [0, N) are left out of the index.
-constexpr int INV_THREADS = 512, INV_WAVES = INV_THREADS / 64;
-constexpr int INV_TMAX = 15360;  // tokens per workgroup: 60 KiB of counters
+constexpr int INV_THREADS = 1024, INV_WAVES = INV_THREADS / 64;
+constexpr int INV_TMAX = 15360;  // tokens per workgroup: 60 KiB of counters (+ 384 B)
 
-// f(i, idx[i]) for the head's per_head entries, strided over the workgroup:
-// four 16-byte loads in flight per thread where the rows allow it.
+// f(e, tok) for the head's per_head entries, strided over the workgroup, 16
+// per thread and call (e[i] the entry, tok[i] its token; -1 pads a short
+// batch): up to sixteen 16-byte loads in flight where the rows allow them,
+// and the callee's LDS atomics of a batch issued before their results are
+// used.
 template <class F>
 __device__ __forceinline__ void inv_entries(const int32_t *__restrict__ ih, int per_head, F &&f) {
+  int e[16], t[16];
   int i = threadIdx.x;
   if ((per_head & 3) == 0 && ((uintptr_t)ih & 15) == 0) {
     const int4 *v = reinterpret_cast<const int4 *>(ih);
     const int n4 = per_head >> 2;
+    // sixteen loads in flight (a whole head of 64Ki entries in one round trip)
+    for (; i + 15 * INV_THREADS < n4; i += 16 * INV_THREADS) {
+      int4 x[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) x[u] = v[i + u * INV_THREADS];
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int e0 = 4 * (i + (4 * b + u) * INV_THREADS);
+          const int4 y = x[4 * b + u];
+          e[4 * u] = e0, e[4 * u + 1] = e0 + 1, e[4 * u + 2] = e0 + 2, e[4 * u + 3] = e0 + 3;
+          t[4 * u] = y.x, t[4 * u + 1] = y.y, t[4 * u + 2] = y.z, t[4 * u + 3] = y.w;
+        }
+        f(e, t);
+      }
+    }
     for (; i + 3 * INV_THREADS < n4; i += 4 * INV_THREADS) {
       int4 x[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) x[u] = v[i + u * INV_THREADS];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int e = 4 * (i + u * INV_THREADS);
-        f(e, x[u].x);
-        f(e + 1, x[u].y);
-        f(e + 2, x[u].z);
-        f(e + 3, x[u].w);
+        const int e0 = 4 * (i + u * INV_THREADS);
+        e[4 * u] = e0, e[4 * u + 1] = e0 + 1, e[4 * u + 2] = e0 + 2, e[4 * u + 3] = e0 + 3;
+        t[4 * u] = x[u].x, t[4 * u + 1] = x[u].y, t[4 * u + 2] = x[u].z, t[4 * u + 3] = x[u].w;
       }
+      f(e, t);
     }
+#pragma unroll
+    for (int q = 4; q < 16; ++q) e[q] = 0, t[q] = -1;
     for (; i < n4; i += INV_THREADS) {
       const int4 x = v[i];
-      f(4 * i, x.x);
-      f(4 * i + 1, x.y);
-      f(4 * i + 2, x.z);
-      f(4 * i + 3, x.w);
+      e[0] = 4 * i, e[1] = 4 * i + 1, e[2] = 4 * i + 2, e[3] = 4 * i + 3;
+      t[0] = x.x, t[1] = x.y, t[2] = x.z, t[3] = x.w;
+      f(e, t);
     }
     return;
   }
-  for (; i < per_head; i += INV_THREADS) f(i, ih[i]);
+#pragma unroll
+  for (int q = 1; q < 16; ++q) e[q] = 0, t[q] = -1;
+  for (; i < per_head; i += INV_THREADS) {
+    e[0] = i, t[0] = ih[i];
+    f(e, t);
+  }
 }
 
 // Grid: NXCD * ceil(nwork / NXCD) workgroups of INV_THREADS, nwork = BH *
-// parts, parts = ceil(N / T); dynamic LDS (T + 2 * INV_WAVES) * 4 bytes.
+// parts, parts = ceil(N / T); dynamic LDS (T + 2 * INV_WAVES + 64) * 4 bytes.
 __global__ __launch_bounds__(INV_THREADS) void inv_index_kernel(const int32_t *__restrict__ idx,
                                                                 int32_t *__restrict__ start,
                                                                 int32_t *__restrict__ slot, int per_head, int N,
                                                                 int T, int parts, int64_t nwork) {
-  extern __shared__ uint32_t inv_lds[];
+  extern __shared__ uint32_t inv_lds[];  // counters, wave sums, a spare word per lane
   uint32_t *cnt = inv_lds, *wsum = inv_lds + T;
   // a head's ranges on consecutive slots of one XCD, which share its sets in L2
   const int64_t w = xcd_slot((int)blockIdx.x, (int)(gridDim.x / NXCD));
@@ -1381,12 +1407,16 @@ __global__ __launch_bounds__(INV_THREADS) void inv_index_kernel(const int32_t *_
   for (uint32_t i = threadIdx.x; i < nt; i += INV_THREADS) cnt[i] = 0;
   __syncthreads();
   uint32_t below = 0;
-  inv_entries(ih, per_head, [&](int, int tok) {
-    const uint32_t r = (uint32_t)tok - (uint32_t)t0;
-    if ((uint32_t)tok < (uint32_t)t0)
-      ++below;
-    else if (r < nt)
-      atomicAdd(&cnt[r], 1u);
+  // (entries of other tokens count into a word of their lane past the
+  // counters: atomics without branches, whose results wait only once)
+  uint32_t *const spare = inv_lds + T + 2 * INV_WAVES + (threadIdx.x & 63);
+  inv_entries(ih, per_head, [&](const int(&)[16], const int(&t)[16]) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const uint32_t r = (uint32_t)t[q] - (uint32_t)t0;
+      below += (uint32_t)t[q] < (uint32_t)t0 ? 1u : 0u;
+      atomicAdd(r < nt ? &cnt[r] : spare, 1u);
+    }
   });
   __syncthreads();
   // exclusive scan of the counts from the base (consecutive runs per thread)
@@ -1421,9 +1451,16 @@ __global__ __launch_bounds__(INV_THREADS) void inv_index_kernel(const int32_t *_
   __syncthreads();  // (the copy above reads the starts before the atomics move them)
   // place: cnt holds each token's next free position (< base + all <= per_head)
   int32_t *sl = slot + bh * per_head;
-  inv_entries(ih, per_head, [&](int e, int tok) {
-    const uint32_t r = (uint32_t)tok - (uint32_t)t0;
-    if (r < nt) sl[atomicAdd(&cnt[r], 1u)] = e;
+  inv_entries(ih, per_head, [&](const int(&e)[16], const int(&t)[16]) {
+    uint32_t r[16], pos[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      r[q] = (uint32_t)t[q] - (uint32_t)t0;
+      pos[q] = atomicAdd(r[q] < nt ? &cnt[r[q]] : spare, 1u);
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q)
+      if (r[q] < nt) sl[pos[q]] = e[q];
   });
 }
 
@@ -1675,7 +1712,7 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
     parts = (c.N + span - 1) / span;
     const int64_t nwork = heads * parts;
     hipLaunchKernelGGL(inv_index_kernel, dim3((unsigned)((nwork + NXCD - 1) / NXCD * NXCD)), dim3(INV_THREADS),
-                       (size_t)(span + 2 * INV_WAVES) * 4, st, b.idx, b.inv_start, b.inv_slot, per_head, c.N, span, parts,
+                       (size_t)(span + 2 * INV_WAVES + 64) * 4, st, b.idx, b.inv_start, b.inv_slot, per_head, c.N, span, parts,
                        nwork);
     if ((err = launched("inv_index_kernel", st)) != hipSuccess) return err;
     if (!fused_finish) {  // (else the landmark-value key pass sums the staged rows)
