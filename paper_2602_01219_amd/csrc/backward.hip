@@ -1541,9 +1541,12 @@ __global__ __launch_bounds__(256) void lse_rows_kernel(const float2 *__restrict_
 
 // The gradients in the io type: dq = the direct part + the pooling backward
 // of the landmark queries' gradient (each token of window W_i receives
-// dq_lm_i / |W_i|), dk, dv from their accumulators. One thread per 4 dims.
-// Along each axis a position lies in at most two adaptive windows, among
-// floor(pos * g / G) - 1 .. + 1.
+// dq_lm_i / |W_i|), dk, dv from their accumulators. One thread per 16 dims
+// (four 4-dim chunks, FIN_CPT threads per row side by side on each chunk),
+// so a token's windows are found once per 16 dims. Along each axis a
+// position lies in at most two adaptive windows, among floor(pos * g / G) -
+// 1 .. + 1.
+template <int D> constexpr int FIN_TPR = D / 16;  // threads per row
 template <typename T, int D, bool POOL, bool KV = true>
 __global__ __launch_bounds__(256) void bwd_finish_kernel(const float *__restrict__ dq_direct,
                                                          const float *__restrict__ dq_lm,
@@ -1551,20 +1554,29 @@ __global__ __launch_bounds__(256) void bwd_finish_kernel(const float *__restrict
                                                          const float *__restrict__ dv_acc, T *__restrict__ dq,
                                                          T *__restrict__ dk, T *__restrict__ dv, int64_t rows, int N,
                                                          int M, int gh, int gw, int lh, int lw) {
-  constexpr int C = D / 4;
+  constexpr int C = FIN_TPR<D>;
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t row = t / C;
   const int c = (int)(t % C);
   if (row >= rows) return;
-  const int64_t bh = row / N;
-  const int tok = (int)(row % N);
-  const int64_t at = row * D + 4 * c;
-  float4 x = *reinterpret_cast<const float4 *>(dq_direct + at);
+  int64_t bh;
+  int tok;
+  if (rows <= (int64_t)UINT32_MAX) {  // (32-bit division where the rows allow it)
+    bh = (int64_t)((uint32_t)row / (uint32_t)N);
+    tok = (int)((uint32_t)row - (uint32_t)bh * (uint32_t)N);
+  } else {
+    bh = row / N;
+    tok = (int)(row % N);
+  }
+  const int64_t at = row * D + 4 * c;  // chunk j at at + 4 C j
+  float4 x[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) x[j] = *reinterpret_cast<const float4 *>(dq_direct + at + 4 * C * j);
   if (POOL) {
     // 32-bit index arithmetic: positions stay below 2^16 (N <= 65536) and
     // window counts at most 1024 (M <= 1024), so every product below is
     // under 2^27
-    const uint32_t pr = (uint32_t)tok / (uint32_t)gw, pc = (uint32_t)tok % (uint32_t)gw;
+    const uint32_t pr = (uint32_t)tok / (uint32_t)gw, pc = (uint32_t)tok - pr * (uint32_t)gw;
     const int ar = (int)(pr * (uint32_t)lh / (uint32_t)gh), ac = (int)(pc * (uint32_t)lw / (uint32_t)gw);
     for (int a = max(0, ar - 1); a <= min(lh - 1, ar + 1); ++a) {
       const int r0 = (int)((uint32_t)a * (uint32_t)gh / (uint32_t)lh);
@@ -1575,25 +1587,39 @@ __global__ __launch_bounds__(256) void bwd_finish_kernel(const float *__restrict
         const int s1 = (int)(((uint32_t)(b + 1) * (uint32_t)gw + (uint32_t)lw - 1u) / (uint32_t)lw);
         if ((int)pc < s0 || (int)pc >= s1) continue;
         const float inv = 1.f / (float)((r1 - r0) * (s1 - s0));
-        const float4 y = *reinterpret_cast<const float4 *>(dq_lm + (bh * M + a * lw + b) * D + 4 * c);
-        x.x += y.x * inv;
-        x.y += y.y * inv;
-        x.z += y.z * inv;
-        x.w += y.w * inv;
+        const float *src = dq_lm + (bh * M + a * lw + b) * D + 4 * c;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float4 y = *reinterpret_cast<const float4 *>(src + 4 * C * j);
+          x[j].x += y.x * inv;
+          x[j].y += y.y * inv;
+          x[j].z += y.z * inv;
+          x[j].w += y.w * inv;
+        }
       }
     }
   }
-  auto put = [&](T *dst, float4 f) {
+  auto put = [&](T *dst, int j, float4 f) {
     T vals[4] = {from_f32<T>(f.x), from_f32<T>(f.y), from_f32<T>(f.z), from_f32<T>(f.w)};
     if (sizeof(T) == 2)
-      *reinterpret_cast<uint2 *>(dst + at) = *reinterpret_cast<const uint2 *>(vals);
+      *reinterpret_cast<uint2 *>(dst + at + 4 * C * j) = *reinterpret_cast<const uint2 *>(vals);
     else
-      *reinterpret_cast<uint4 *>(dst + at) = *reinterpret_cast<const uint4 *>(vals);
+      *reinterpret_cast<uint4 *>(dst + at + 4 * C * j) = *reinterpret_cast<const uint4 *>(vals);
   };
-  put(dq, x);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) put(dq, j, x[j]);
   if (KV) {  // (else the landmark-value key pass wrote dk and dv)
-    put(dk, *reinterpret_cast<const float4 *>(dk_acc + at));
-    put(dv, *reinterpret_cast<const float4 *>(dv_acc + at));
+    float4 yk[4], yv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      yk[j] = *reinterpret_cast<const float4 *>(dk_acc + at + 4 * C * j);
+      yv[j] = *reinterpret_cast<const float4 *>(dv_acc + at + 4 * C * j);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      put(dk, j, yk[j]);
+      put(dv, j, yv[j]);
+    }
   }
 }
 
@@ -1773,7 +1799,7 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
     }
   }
   const int64_t rows = BH(c) * c.N;
-  const int64_t threads = rows * (D / 4);
+  const int64_t threads = rows * FIN_TPR<D>;
   const dim3 fg((unsigned)((threads + 255) / 256));
   if (fused_finish)
     hipLaunchKernelGGL((bwd_finish_kernel<T, D, true, false>), fg, dim3(256), 0, st, b.dq_direct, b.dq_lm_acc,
