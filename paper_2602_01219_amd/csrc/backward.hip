@@ -1521,22 +1521,44 @@ __global__ __launch_bounds__(256) void inv_gather_kernel(const float *__restrict
 }
 
 // Log-sum-exp (log2 units) of every landmark row's scores, from the score
-// pass's per-chunk (max, sum) partials: one thread per row.
-__global__ __launch_bounds__(256) void lse_rows_kernel(const float2 *__restrict__ part_ml, float *__restrict__ lse,
-                                                       int64_t rows, int M, int nch) {
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= rows) return;
-  const int64_t bh = t / M;
-  const int lm = (int)(t % M);
+// pass's per-chunk (max, sum) partials: LSE_S waves per 64 consecutive rows
+// (a lane per row), wave w combining chunks w, w + LSE_S, ..., then the
+// LSE_S partial pairs of each row combined through LDS.
+constexpr int LSE_S = 16;
+__device__ __forceinline__ void lse_combine(float &m, float &l, float2 x) {
+  const float mn = fmaxf(m, x.x);
+  if (mn == -INFINITY) return;  // (nothing but empty partials so far)
+  l = l * __builtin_amdgcn_exp2f(m - mn) + x.y * __builtin_amdgcn_exp2f(x.x - mn);
+  m = mn;
+}
+__global__ __launch_bounds__(64 * LSE_S) void lse_rows_kernel(const float2 *__restrict__ part_ml,
+                                                              float *__restrict__ lse, int64_t rows, int M,
+                                                              int nch) {
+  __shared__ float2 part[LSE_S][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t t = (int64_t)blockIdx.x * 64 + lane;
   float m = -INFINITY, l = 0.f;
-  for (int c = 0; c < nch; ++c) {
-    const float2 x = part_ml[(bh * nch + c) * M + lm];
-    const float mn = fmaxf(m, x.x);
-    if (mn == -INFINITY) continue;
-    l = l * __builtin_amdgcn_exp2f(m - mn) + x.y * __builtin_amdgcn_exp2f(x.x - mn);
-    m = mn;
+  if (t < rows) {
+    const int64_t bh = t / M;
+    const float2 *src = part_ml + bh * nch * M + (t - bh * M);
+    int c = w;
+    for (; c + 3 * LSE_S < nch; c += 4 * LSE_S) {
+      float2 x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) x[u] = src[(int64_t)(c + u * LSE_S) * M];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) lse_combine(m, l, x[u]);
+    }
+    for (; c < nch; c += LSE_S) lse_combine(m, l, src[(int64_t)c * M]);
   }
-  lse[t] = m + __log2f(l);
+  part[w][lane] = make_float2(m, l);
+  __syncthreads();
+  if (w == 0 && t < rows) {
+    m = -INFINITY, l = 0.f;
+#pragma unroll
+    for (int i = 0; i < LSE_S; ++i) lse_combine(m, l, part[i][lane]);
+    lse[t] = m + __log2f(l);
+  }
 }
 
 // The gradients in the io type: dq = the direct part + the pooling backward
@@ -1658,8 +1680,8 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
   hipError_t err;
   if (c.use_shared) {
     const int64_t rows = BH(c) * c.M;
-    hipLaunchKernelGGL(lse_rows_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, st, (const float2 *)b.part_ml,
-                       b.lse_lm, rows, c.M, score_chunks(c));
+    hipLaunchKernelGGL(lse_rows_kernel, dim3((unsigned)((rows + 63) / 64)), dim3(64 * LSE_S), 0, st,
+                       (const float2 *)b.part_ml, b.lse_lm, rows, c.M, score_chunks(c));
     if ((err = launched("lse_rows_kernel", st)) != hipSuccess) return err;
   }
   // dQ of the MiTA attention, and each query's log-sum-exp and D
