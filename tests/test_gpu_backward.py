@@ -131,3 +131,22 @@ def test_backward_rejects_s_above_one_and_overlaps():
     with pytest.raises(mita.MitaError) as ex:
         mita.backward(cfg, q, k, v, o, o, dq=q)
     assert ex.value.status == mita.MITA_ERR_INVALID_ARG
+
+
+# Shapes whose inverse index splits a head's tokens into ranges that do not
+# divide N, with more heads than XCDs, through the fp32 gather pass and the
+# bf16 fused finish (d = 64 and 128).
+BWD_EDGE = [(36, 36, 6, 6, 36, 64, "bf16", 3, 3), (36, 36, 6, 6, 36, 64, "f32", 1, 3),
+            (33, 41, 5, 4, 300, 128, "bf16", 2, 5)]
+
+
+@pytest.mark.parametrize("case", BWD_EDGE, ids=[f"{c[0]}x{c[1]}_m{c[2]*c[3]}_k{c[4]}_d{c[5]}_{c[6]}_b{c[7]}h{c[8]}"
+                                                for c in BWD_EDGE])
+def test_backward_edge_cases(case):
+    gh, gw, lh, lw, kk, d, dtype, B, H = case
+    wl = synth.Workload(name="bwd_edge", B=B, H=H, grid_h=gh, grid_w=gw, d=d, lm_h=lh, lm_w=lw, k=kk, dtype=dtype,
+                        clusters=4, std=0.5, cluster_map="iid", seed=91 + gh * gw, use_shared=1, use_routed=1)
+    inp = synth.generate(wl)
+    cfg = mita.Config.from_workload(wl)
+    log(f"[backward edge] {case}")
+    _check_backward(cfg, inp, [(0, 0), (B - 1, H - 1)])
