@@ -1292,31 +1292,35 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) v
 }
 
 // The landmark values' gradient in bf16 (the MFMA operand of the DMA-tiled
-// landmark-value kernels) and each landmark row's D = dV~ . V~ (fp32), one
-// thread per row.
+// landmark-value kernels) and each landmark row's D = dV~ . V~ (fp32): D / 8
+// consecutive lanes per row, 8 dims each, their partial dots summed by a
+// butterfly over those lanes.
 template <int D>
 __global__ __launch_bounds__(256) void lmv_prep_kernel(const float *__restrict__ dv_lm, const bf16_t *__restrict__ v_lm,
                                                        bf16_t *__restrict__ dv16, float *__restrict__ D_lm,
                                                        int64_t rows) {
+  constexpr int L = D / 8;  // lanes per row (8 or 16: rows never straddle a wave)
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= rows) return;
+  const int64_t row = t / L;
+  const int c = 8 * (int)(t % L);
   float dsum = 0.f;
-#pragma unroll
-  for (int c = 0; c < D; c += 8) {
-    const float4 f0 = *reinterpret_cast<const float4 *>(dv_lm + t * D + c);
-    const float4 f1 = *reinterpret_cast<const float4 *>(dv_lm + t * D + c + 4);
+  if (row < rows) {
+    const float4 f0 = *reinterpret_cast<const float4 *>(dv_lm + row * D + c);
+    const float4 f1 = *reinterpret_cast<const float4 *>(dv_lm + row * D + c + 4);
     const float f[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
     float vv[8];
-    load16_f32(v_lm + t * D + c, vv);
+    load16_f32(v_lm + row * D + c, vv);
     bf16_t tt[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       dsum = __builtin_fmaf(vv[i], f[i], dsum);
       tt[i] = from_f32<bf16_t>(f[i]);
     }
-    *reinterpret_cast<uint4 *>(dv16 + t * D + c) = *reinterpret_cast<const uint4 *>(tt);
+    *reinterpret_cast<uint4 *>(dv16 + row * D + c) = *reinterpret_cast<const uint4 *>(tt);
   }
-  D_lm[t] = dsum;
+#pragma unroll
+  for (int o = L / 2; o > 0; o >>= 1) dsum += __shfl_xor(dsum, o);
+  if (row < rows && c == 0) D_lm[row] = dsum;
 }
 
 // Inverse index of the top-k sets: for each token, the slots e * k + j with
@@ -1788,8 +1792,8 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
       // chunks (atomic adds per chunk), then the keys' gradient by token
       // blocks with all landmark rows streamed (each row added once)
       const int64_t mrows = BH(c) * c.M;
-      hipLaunchKernelGGL((lmv_prep_kernel<D>), dim3((unsigned)((mrows + 255) / 256)), dim3(256), 0, st, b.dv_lm_acc,
-                         (const bf16_t *)b.v_lm, (bf16_t *)b.dv_lm16, b.D_lm, mrows);
+      hipLaunchKernelGGL((lmv_prep_kernel<D>), dim3((unsigned)((mrows * (D / 8) + 255) / 256)), dim3(256), 0, st,
+                         b.dv_lm_acc, (const bf16_t *)b.v_lm, (bf16_t *)b.dv_lm16, b.D_lm, mrows);
       if ((err = launched("lmv_prep_kernel", st)) != hipSuccess) return err;
       a.dv_lm16 = b.dv_lm16;
       a.D_lm = b.D_lm;
