@@ -111,12 +111,15 @@ def test_backward_dense_equivalence_is_attention_backward():
     dO = to_dev(_upstream(wl), wl.dtype)
     o = mita.forward(cfg, q, k, v)
     dq, dk, dv = mita.backward(cfg, q, k, v, o, dO)
-    tq, tk, tv = (x.float().detach().requires_grad_() for x in (q, k, v))
+    # the reference in float64 on the CPU (no device library in the reference)
+    tq, tk, tv = (x.double().cpu().detach().requires_grad_() for x in (q, k, v))
     ref = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv)
-    (ref * dO.float()).sum().backward()
+    (ref * dO.double().cpu()).sum().backward()
     for name, got, r in (("dq", dq, tq.grad), ("dk", dk, tk.grad), ("dv", dv, tv.grad)):
-        err = ((got.float() - r).abs().amax() / r.abs().amax()).item()
-        log(f"  dense equivalence {name}: max-rel {err:.3e} vs SDPA autograd (fp32)")
+        g = got.double().cpu()
+        assert bool(torch.isfinite(g).all()), f"{name}: {int((~torch.isfinite(g)).sum())} non-finite values"
+        err = ((g - r).abs().amax() / r.abs().amax()).item()
+        log(f"  dense equivalence {name}: max-rel {err:.3e} vs SDPA autograd (float64, CPU)")
         assert err <= TOL["bf16"]
 
 
