@@ -1136,9 +1136,14 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) v
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           float pr = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][qb][r], sl2, -lq[qb][r]));
-          if (MK && 16 * qb + 4 * g + r >= nv) pr = 0.f;
+          float zr = pr * (dp[c][qb][r] - dq[qb][r]);
+          // rows past the chunk's last query: their log-sum-exp and D slots
+          // in LDS were not written for this chunk and may hold any bits
+          // (0 * NaN would spread into every key's dK), so both weights are
+          // set, not scaled, to zero
+          if (MK && 16 * qb + 4 * g + r >= nv) pr = zr = 0.f;
           pp[4 * qb + r] = pr;
-          zz[4 * qb + r] = pr * (dp[c][qb][r] - dq[qb][r]);
+          zz[4 * qb + r] = zr;
         }
       pf[c].from_f32(pp);
       zf[c].from_f32(zz);
