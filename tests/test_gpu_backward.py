@@ -16,6 +16,9 @@ from __future__ import annotations
 
 import dataclasses
 import functools
+import os
+import shutil
+import subprocess
 
 import numpy as np
 import pytest
@@ -153,3 +156,67 @@ def test_backward_edge_cases(case):
     cfg = mita.Config.from_workload(wl)
     log(f"[backward edge] {case}")
     _check_backward(cfg, inp, [(0, 0), (B - 1, H - 1)])
+
+
+@functools.lru_cache(maxsize=None)
+def _region_tool(tmpdir):
+    src = os.path.join(os.path.dirname(__file__), "host", "bwd_float_regions.cpp")
+    exe = os.path.join(tmpdir, "bwd_float_regions")
+    r = subprocess.run(["g++", "-std=c++17", "-O1", "-I", os.path.join(os.path.dirname(__file__), "..", "include"),
+                        src, "-o", exe], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    return exe
+
+
+def _float_regions(cfg, tmpdir):
+    """Byte ranges (kind, begin, end) of the floating-point regions of the
+    backward's workspace, from the library's own layout header built for the host."""
+    args = [cfg.B, cfg.H, cfg.grid_h, cfg.grid_w, cfg.d, cfg.lm_h, cfg.lm_w, cfg.k, cfg.use_shared, cfg.use_routed,
+            int(cfg.dtype == "bf16")]
+    r = subprocess.run([_region_tool(tmpdir), *map(str, args)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stdout + r.stderr
+    out = [l.split() for l in r.stdout.splitlines()]
+    total = int(next(l[1] for l in out if l[0] == "total"))
+    assert total == mita.workspace_size(cfg, mita.WS_BACKWARD)
+    return [(l[0], int(l[1]), int(l[2])) for l in out if l[0] != "total"]
+
+
+# Shapes with a partial query tile in every key pass: route-only k = N (most
+# experts hold a few queries), the landmark rows as queries with M = 16 < 32
+# (bf16, both branches), and the fp32 kernels.
+WS_CASES = [("dense_equiv_bf16", 1, 2), ("vits_bf16", 2, 2), ("tiny_f32", None, None)]
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="the layout helper needs g++")
+@pytest.mark.parametrize("name,B,H", WS_CASES, ids=[c[0] for c in WS_CASES])
+def test_backward_does_not_read_stale_workspace_or_lds(name, B, H, tmp_path_factory):
+    """Regression: rows past a chunk's last query in the key passes once took
+    0 * (dP - D) with D from an LDS slot not written for that chunk, which made
+    every key's dk NaN when the slot held NaN bits. With the workspace's float
+    regions filled with NaN beforehand (integer regions zero), the gradients
+    must be finite and equal those from a zeroed workspace (to the rounding of
+    the backward's unordered fp32 sums)."""
+    inp = _inputs(name, B, H)
+    wl = inp.wl
+    cfg = mita.Config.from_workload(wl)
+    q, k, v = (to_dev(x, wl.dtype) for x in (inp.q, inp.k, inp.v))
+    dO = to_dev(_upstream(wl), wl.dtype)
+    o = mita.forward(cfg, q, k, v)
+    ws = torch.zeros(mita.workspace_size(cfg, mita.WS_BACKWARD), dtype=torch.uint8, device="cuda")
+    clean = [g.float().clone() for g in mita.backward(cfg, q, k, v, o, dO, ws=ws)]
+    regions = _float_regions(cfg, str(tmp_path_factory.mktemp("layout")))
+    ws.zero_()
+    for kind, a, b in regions:
+        if b > a:
+            view = ws[a:b].view(torch.float32 if kind == "f32" else q.dtype)
+            view.fill_(float("nan"))
+    outs = [torch.full_like(q, float("nan")) for _ in range(3)]
+    mita.backward(cfg, q, k, v, o, dO, dq=outs[0], dk=outs[1], dv=outs[2], ws=ws)
+    torch.cuda.synchronize()
+    for gname, g, ref in zip(("dq", "dk", "dv"), outs, clean):
+        g = g.float()
+        bad = int((~torch.isfinite(g)).sum())
+        err = ((g - ref).abs().amax() / ref.abs().amax()).item() if bad == 0 else float("nan")
+        log(f"  {name} {gname}: {bad} non-finite, max-rel {err:.3e} against the zeroed workspace")
+        assert bad == 0
+        assert err <= 1e-2
