@@ -35,7 +35,7 @@ respect to q, k and v by the chain rule through Eq. mita, Eq. landmark-value
 and the pooling, the top-k sets and the routing held fixed (they are
 piecewise constant in the inputs and take no gradient).
 
-Readings where the paper is silent or ambiguous (listed in the design doc):
+Readings where the paper is silent or ambiguous:
   * pooling windows: start = floor(i*G/g), end = ceil((i+1)*G/g) per axis
     (the adaptive-average-pool rule Algorithm 1 names); 1-D pooling when
     grid_h == 1.
