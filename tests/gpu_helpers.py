@@ -3,6 +3,9 @@ validation bounds, and the error metric. No method arithmetic lives here
 beyond the comparison itself (the oracle computes every expected value)."""
 from __future__ import annotations
 
+import functools
+import os
+import subprocess
 import sys
 
 import numpy as np
@@ -109,3 +112,36 @@ def check_routing(L_ref: np.ndarray, tau: np.ndarray, expert_gpu: np.ndarray):
     best = np.max(L_ref - tau, axis=1)
     assert (got >= best).all(), f"routing outside the rounding budget at {np.nonzero(got < best)[0][:5]}"
     return int((np.argmax(L_ref, axis=1) == expert_gpu).sum())
+
+
+@functools.lru_cache(maxsize=None)
+def _region_tool(tmpdir: str) -> str:
+    here = os.path.dirname(os.path.abspath(__file__))
+    exe = os.path.join(tmpdir, "ws_float_regions")
+    r = subprocess.run(["g++", "-std=c++17", "-O1", "-I", os.path.join(here, "..", "include"),
+                        os.path.join(here, "host", "ws_float_regions.cpp"), "-o", exe], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    return exe
+
+
+def float_regions(cfg, tmpdir: str, forward: bool):
+    """Byte ranges (kind, begin, end) of the floating-point regions of the
+    forward's or the backward's workspace (kind "f32" or "io"), from the
+    library's own layout header built for the host."""
+    from paper_2602_01219_amd import mita
+    args = [cfg.B, cfg.H, cfg.grid_h, cfg.grid_w, cfg.d, cfg.lm_h, cfg.lm_w, cfg.k, cfg.use_shared, cfg.use_routed,
+            int(cfg.dtype == "bf16"), cfg.s, int(forward)]
+    r = subprocess.run([_region_tool(tmpdir), *map(str, args)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stdout + r.stderr
+    out = [l.split() for l in r.stdout.splitlines()]
+    total = int(next(l[1] for l in out if l[0] == "total"))
+    assert total == mita.workspace_size(cfg, mita.WS_FORWARD if forward else mita.WS_BACKWARD)
+    return [(l[0], int(l[1]), int(l[2])) for l in out if l[0] != "total"]
+
+
+def fill_float_regions(ws, regions, io_dtype):
+    """Zero the workspace, then fill its floating-point regions with NaN."""
+    ws.zero_()
+    for kind, a, b in regions:
+        if b > a:
+            ws[a:b].view(torch.float32 if kind == "f32" else io_dtype).fill_(float("nan"))

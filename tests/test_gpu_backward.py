@@ -16,9 +16,7 @@ from __future__ import annotations
 
 import dataclasses
 import functools
-import os
 import shutil
-import subprocess
 
 import numpy as np
 import pytest
@@ -26,7 +24,8 @@ import torch
 
 from oracle import mita_oracle as O
 from paper_2602_01219_amd import mita, synth
-from tests.gpu_helpers import check_routing, check_selection, from_dev, log, maxrel, to_dev
+from tests.gpu_helpers import (check_routing, check_selection, fill_float_regions, float_regions, from_dev, log,
+                               maxrel, to_dev)
 from tests.test_gpu_parity import _bounds
 
 pytestmark = pytest.mark.gpu
@@ -158,29 +157,6 @@ def test_backward_edge_cases(case):
     _check_backward(cfg, inp, [(0, 0), (B - 1, H - 1)])
 
 
-@functools.lru_cache(maxsize=None)
-def _region_tool(tmpdir):
-    src = os.path.join(os.path.dirname(__file__), "host", "bwd_float_regions.cpp")
-    exe = os.path.join(tmpdir, "bwd_float_regions")
-    r = subprocess.run(["g++", "-std=c++17", "-O1", "-I", os.path.join(os.path.dirname(__file__), "..", "include"),
-                        src, "-o", exe], capture_output=True, text=True)
-    assert r.returncode == 0, r.stderr
-    return exe
-
-
-def _float_regions(cfg, tmpdir):
-    """Byte ranges (kind, begin, end) of the floating-point regions of the
-    backward's workspace, from the library's own layout header built for the host."""
-    args = [cfg.B, cfg.H, cfg.grid_h, cfg.grid_w, cfg.d, cfg.lm_h, cfg.lm_w, cfg.k, cfg.use_shared, cfg.use_routed,
-            int(cfg.dtype == "bf16")]
-    r = subprocess.run([_region_tool(tmpdir), *map(str, args)], capture_output=True, text=True)
-    assert r.returncode == 0, r.stdout + r.stderr
-    out = [l.split() for l in r.stdout.splitlines()]
-    total = int(next(l[1] for l in out if l[0] == "total"))
-    assert total == mita.workspace_size(cfg, mita.WS_BACKWARD)
-    return [(l[0], int(l[1]), int(l[2])) for l in out if l[0] != "total"]
-
-
 # Shapes with a partial query tile in every key pass: route-only k = N (most
 # experts hold a few queries), the landmark rows as queries with M = 16 < 32
 # (bf16, both branches), and the fp32 kernels.
@@ -204,12 +180,8 @@ def test_backward_does_not_read_stale_workspace_or_lds(name, B, H, tmp_path_fact
     o = mita.forward(cfg, q, k, v)
     ws = torch.zeros(mita.workspace_size(cfg, mita.WS_BACKWARD), dtype=torch.uint8, device="cuda")
     clean = [g.float().clone() for g in mita.backward(cfg, q, k, v, o, dO, ws=ws)]
-    regions = _float_regions(cfg, str(tmp_path_factory.mktemp("layout")))
-    ws.zero_()
-    for kind, a, b in regions:
-        if b > a:
-            view = ws[a:b].view(torch.float32 if kind == "f32" else q.dtype)
-            view.fill_(float("nan"))
+    regions = float_regions(cfg, str(tmp_path_factory.mktemp("layout")), forward=False)
+    fill_float_regions(ws, regions, q.dtype)
     outs = [torch.full_like(q, float("nan")) for _ in range(3)]
     mita.backward(cfg, q, k, v, o, dO, dq=outs[0], dk=outs[1], dv=outs[2], ws=ws)
     torch.cuda.synchronize()

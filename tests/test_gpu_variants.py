@@ -19,6 +19,7 @@ from __future__ import annotations
 
 import dataclasses
 import functools
+import shutil
 
 import numpy as np
 import pytest
@@ -26,7 +27,8 @@ import torch
 
 from oracle import mita_oracle as O
 from paper_2602_01219_amd import mita, synth
-from tests.gpu_helpers import U, check_selection, from_dev, log, maxrel, to_dev, tol_for
+from tests.gpu_helpers import (U, check_selection, fill_float_regions, float_regions, from_dev, log, maxrel, to_dev,
+                               tol_for)
 from tests.test_gpu_parity import _bounds
 
 pytestmark = pytest.mark.gpu
@@ -338,3 +340,30 @@ def test_tome_is_deterministic():
     a2, s2 = mita.landmarks_tome(cfg, q)
     torch.cuda.synchronize()
     assert _same(a1, a2) and torch.equal(s1, s2)
+
+
+# The forward on every path writes each float of its workspace before reading
+# it and reads no LDS it has not written: with the workspace's float regions
+# filled with NaN beforehand (integer regions zero), the output is bitwise the
+# output from a zeroed workspace (the forward is deterministic).
+FWD_WS_CASES = [("dense_pred_bf16", 1, 2, 1), ("vits_bf16", 2, 2, 1), ("tiny_f32", None, None, 1),
+                ("long_bf16", 1, 1, 1), ("dense_equiv_bf16", 1, 2, 1), ("vitb_hr_bf16", 1, 2, 2)]
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="the layout helper needs g++")
+@pytest.mark.parametrize("name,B,H,s", FWD_WS_CASES, ids=[f"{c[0]}_s{c[3]}" for c in FWD_WS_CASES])
+def test_forward_does_not_read_stale_workspace(name, B, H, s, tmp_path_factory):
+    inp = synth.generate(synth.WORKLOADS[name], B=B, H=H)
+    wl = inp.wl
+    cfg = dataclasses.replace(mita.Config.from_workload(wl), s=s)
+    q, k, v = _dev(inp)
+    ws = torch.zeros(mita.workspace_size(cfg, mita.WS_FORWARD), dtype=torch.uint8, device="cuda")
+    clean = mita.forward(cfg, q, k, v, ws=ws).clone()
+    fill_float_regions(ws, float_regions(cfg, str(tmp_path_factory.mktemp("layout")), forward=True), q.dtype)
+    o = torch.full_like(q, float("nan"))
+    mita.forward(cfg, q, k, v, o=o, ws=ws)
+    torch.cuda.synchronize()
+    same = bool(torch.equal(o.view(torch.int16) if o.dtype == torch.bfloat16 else o.view(torch.int32),
+                            clean.view(torch.int16) if clean.dtype == torch.bfloat16 else clean.view(torch.int32)))
+    log(f"  {name} s={s}: {int((~torch.isfinite(o.float())).sum())} non-finite, bitwise equal {same}")
+    assert same
