@@ -1573,7 +1573,7 @@ __global__ __launch_bounds__(64 * LSE_S) void lse_rows_kernel(const float2 *__re
 // The gradients in the io type: dq = the direct part + the pooling backward
 // of the landmark queries' gradient (each token of window W_i receives
 // dq_lm_i / |W_i|), dk, dv from their accumulators. One thread per 16 dims
-// (four 4-dim chunks, FIN_CPT threads per row side by side on each chunk),
+// (four 4-dim chunks, FIN_TPR threads per row side by side on each chunk),
 // so a token's windows are found once per 16 dims. Along each axis a
 // position lies in at most two adaptive windows, among floor(pos * g / G) -
 // 1 .. + 1.
