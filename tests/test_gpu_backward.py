@@ -140,9 +140,11 @@ def test_backward_rejects_s_above_one_and_overlaps():
 
 # Shapes whose inverse index splits a head's tokens into ranges that do not
 # divide N, with more heads than XCDs, through the fp32 gather pass and the
-# bf16 fused finish (d = 64 and 128).
+# bf16 fused finish (d = 64 and 128); M k = 255 entries per head takes the
+# inverse index's one-entry loads (M k not a multiple of 4), in both dtypes.
 BWD_EDGE = [(36, 36, 6, 6, 36, 64, "bf16", 3, 3), (36, 36, 6, 6, 36, 64, "f32", 1, 3),
-            (33, 41, 5, 4, 300, 128, "bf16", 2, 5)]
+            (33, 41, 5, 4, 300, 128, "bf16", 2, 5), (15, 20, 3, 5, 17, 64, "bf16", 2, 3),
+            (15, 20, 3, 5, 17, 128, "f32", 1, 2)]
 
 
 @pytest.mark.parametrize("case", BWD_EDGE, ids=[f"{c[0]}x{c[1]}_m{c[2]*c[3]}_k{c[4]}_d{c[5]}_{c[6]}_b{c[7]}h{c[8]}"
