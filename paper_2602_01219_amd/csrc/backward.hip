@@ -1012,7 +1012,7 @@ constexpr int KV16_QC = 512;  // queries per staged chunk
 constexpr int KV_ROUTED = 0, KV_SHARED = 1, KV_LMV = 2;
 
 template <int D, int KM, int NG>
-__global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) void bwd_kv16_kernel(KvArgs a) {
+__device__ __forceinline__ void bwd_kv16_body(KvArgs a) {
   constexpr bool ROUTED = KM == KV_ROUTED;
   constexpr int NW = 4 / NG;
   constexpr int NT = 64 * NW;
@@ -1240,10 +1240,40 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) v
             v4[db].x += yv.x; v4[db].y += yv.y; v4[db].z += yv.z; v4[db].w += yv.w;
           }
         };
+        if constexpr (D == 64) {
+          // two rows' loads in flight before either is added (slot order
+          // kept; the registers come from running two waves per SIMD)
+          auto add2 = [&](int64_t r0, int64_t r1) {
+            float4 yk[2][D / 16], yv[2][D / 16];
 #pragma unroll
-        for (int i = 0; i < FS; ++i)
-          if (i < n) add(src[i]);
-        for (int i = FS; i < n; ++i) add((bh * per_head + a.inv_slot[bh * per_head + s0 + i]) * D);
+            for (int db = 0; db < D / 16; ++db) {
+              yk[0][db] = *reinterpret_cast<const float4 *>(a.stage_k + r0 + 16 * db + 4 * g);
+              yv[0][db] = *reinterpret_cast<const float4 *>(a.stage_v + r0 + 16 * db + 4 * g);
+              yk[1][db] = *reinterpret_cast<const float4 *>(a.stage_k + r1 + 16 * db + 4 * g);
+              yv[1][db] = *reinterpret_cast<const float4 *>(a.stage_v + r1 + 16 * db + 4 * g);
+            }
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+#pragma unroll
+              for (int db = 0; db < D / 16; ++db) {
+                k4[db].x += yk[b][db].x; k4[db].y += yk[b][db].y; k4[db].z += yk[b][db].z; k4[db].w += yk[b][db].w;
+                v4[db].x += yv[b][db].x; v4[db].y += yv[b][db].y; v4[db].z += yv[b][db].z; v4[db].w += yv[b][db].w;
+              }
+          };
+          int i = 0;
+#pragma unroll
+          for (int j = 0; j < FS; j += 2)
+            if (j + 1 < n) add2(src[j], src[j + 1]), i = j + 2;
+          for (; i + 1 < n; i += 2)
+            add2((bh * per_head + a.inv_slot[bh * per_head + s0 + i]) * D,
+                 (bh * per_head + a.inv_slot[bh * per_head + s0 + i + 1]) * D);
+          if (i < n) add(i < FS ? src[i] : (bh * per_head + a.inv_slot[bh * per_head + s0 + i]) * D);
+        } else {
+#pragma unroll
+          for (int i = 0; i < FS; ++i)
+            if (i < n) add(src[i]);
+          for (int i = FS; i < n; ++i) add((bh * per_head + a.inv_slot[bh * per_head + s0 + i]) * D);
+        }
       }
       const int64_t at = (bh * N + kb0 + key) * D + 4 * g;
 #pragma unroll
@@ -1294,6 +1324,19 @@ __global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) v
       }
     }
   }
+}
+
+// Three waves per SIMD; the landmark-value mode at d = 64 runs two, whose
+// registers hold two staged rows in flight in its finish (measured at 16384
+// tokens, 12 heads, 2 batches: that pass 379 -> 353 us, while the routed pass
+// with two waves went 361 -> 391 us).
+template <int D, int KM, int NG>
+__global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(3))) void bwd_kv16_kernel(KvArgs a) {
+  bwd_kv16_body<D, KM, NG>(a);
+}
+template <int NG>
+__global__ __launch_bounds__(256 / NG) __attribute__((amdgpu_waves_per_eu(2))) void bwd_kv16_lmv64_kernel(KvArgs a) {
+  bwd_kv16_body<64, KV_LMV, NG>(a);
 }
 
 // The landmark values' gradient in bf16 (the MFMA operand of the DMA-tiled
@@ -1821,7 +1864,10 @@ static hipError_t bwd_t(const mita_cfg_t &c, const BwdBufs &b, hipStream_t st) {
       kv.dv_out = b.dv;
       kv.ntotal = (c.N + BWD_KB - 1) / BWD_KB;
       const unsigned nxl = (unsigned)((kv.ntotal + NXCD - 1) / NXCD * NXCD);
-      hipLaunchKernelGGL((bwd_kv16_kernel<D, KV_LMV, NG>), dim3(nxl, bh), dim3(256 / NG), 0, st, kv);
+      if constexpr (D == 64)
+        hipLaunchKernelGGL((bwd_kv16_lmv64_kernel<NG>), dim3(nxl, bh), dim3(256 / NG), 0, st, kv);
+      else
+        hipLaunchKernelGGL((bwd_kv16_kernel<D, KV_LMV, NG>), dim3(nxl, bh), dim3(256 / NG), 0, st, kv);
       if ((err = launched("bwd_kv_landmark_kernel", st)) != hipSuccess) return err;
     } else {
       hipLaunchKernelGGL((bwd_kernel<T, D, BWD_LMV, true, false>), dim3((unsigned)(nlb * nch), bh), dim3(256), 0,
